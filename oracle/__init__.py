@@ -1,0 +1,222 @@
+"""CPU oracle for the SLO-aware annealing scheduler -- TEST INFRASTRUCTURE ONLY.
+
+Plain single-threaded C (``oracle/*.c``) behind ctypes. Only ``tests/``,
+``__graft_entry__.smoke()`` and the CPU-baseline leg of ``bench.py`` may use it;
+the GPU library never imports, links or calls it, and it shares no code with the
+GPU library.
+
+What it computes and which passage it follows is documented in ``oracle/oracle.h``.
+Pins against the paper and the mathematics live in ``tests/test_oracle_*.py``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRCS = ("replay.c", "rng.c", "anneal.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
+          "-Wall", "-Wextra", "-Wno-unused-parameter"]
+
+R_CUR_N, R_CUR_T, R_BEST_N, R_BEST_T, R_BEST_ITER, R_ACCEPTS, R_DIGEST, R_ALLMET = range(8)
+TAG_ANNEAL = 0x53414E4E
+TAG_FY = 0x46495348
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc into oracle/liboracle.so."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        cmd = ["gcc", *CFLAGS, "-o", tmp, *[os.path.join(_HERE, s) for s in _SRCS], "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+class _Queue(C.Structure):
+    _fields_ = [("n", C.c_int32), ("in_len", C.c_void_p), ("out_len", C.c_void_p),
+                ("kind", C.c_void_p), ("thr_us", C.c_void_p)]
+
+
+class _Model(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("policy", C.c_int32), ("p0", C.c_int64),
+                ("p1", C.c_int64), ("d0", C.c_int64), ("d1", C.c_int64), ("d2", C.c_int64),
+                ("t_ref_us", C.c_int64), ("swap_threshold", C.c_uint64)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        L = C.CDLL(_LIB_PATH)
+        vp, i32, i64, u32, u64, dbl = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_double
+        L.orc_replay.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.orc_replay.restype = C.c_int
+        L.orc_eval_rows.argtypes = [vp, vp, vp, i64, i64, vp]
+        L.orc_philox.argtypes = [vp, vp, vp]
+        L.orc_det_exp.argtypes = [dbl]
+        L.orc_det_exp.restype = dbl
+        L.orc_accept.argtypes = [i64, i64, dbl, u32]
+        L.orc_accept.restype = C.c_int
+        L.orc_fy_perm.argtypes = [u64, i32, u32, vp]
+        L.orc_start.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.orc_start.restype = C.c_int
+        L.orc_swap.argtypes = [vp, i32, i32]
+        L.orc_insert.argtypes = [vp, i32, i32]
+        L.orc_positions.argtypes = [i32, u32, u32, vp, vp]
+        L.orc_anneal_chain.argtypes = [vp, vp, vp, i64, C.c_int, i32, i32, dbl, dbl, u64, vp, vp,
+                                       vp, vp]
+        L.orc_brute.argtypes = [vp, vp, vp, vp, vp]
+        L.orc_brute.restype = i64
+        L.orc_solo.argtypes = [vp, vp, i32]
+        L.orc_solo.restype = i64
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(C.c_void_p)
+
+
+class _Args:
+    """Keeps the contiguous arrays alive while C structs point at them."""
+
+    def __init__(self, queue, model):
+        self.in_len = np.ascontiguousarray(queue.in_len, dtype=np.uint16)
+        self.out_len = np.ascontiguousarray(queue.out_len, dtype=np.uint16)
+        self.kind = np.ascontiguousarray(queue.kind, dtype=np.uint8)
+        self.thr = np.ascontiguousarray(queue.thr_us, dtype=np.uint32)
+        self.n = int(self.in_len.shape[0])
+        self.q = _Queue(self.n, _p(self.in_len).value, _p(self.out_len).value, _p(self.kind).value,
+                        _p(self.thr).value)
+        self.m = _Model(int(model.max_batch), int(model.policy), int(model.p0), int(model.p1),
+                        int(model.d0), int(model.d1), int(model.d2), int(model.t_ref_us),
+                        int(model.swap_threshold))
+        self.qp = C.byref(self.q)
+        self.mp = C.byref(self.m)
+
+
+def replay(queue, model, perm, detail: bool = False):
+    """(n_met, t_sum) of one order, plus per-request (ttft, e2e) when detail is set."""
+    a = _Args(queue, model)
+    perm = np.ascontiguousarray(perm, dtype=np.uint16)
+    nm, ts = C.c_int64(), C.c_int64()
+    ttft = np.zeros(a.n, np.int64)
+    e2e = np.zeros(a.n, np.int64)
+    lib().orc_replay(a.qp, a.mp, _p(perm), C.byref(nm), C.byref(ts), _p(ttft), _p(e2e))
+    if detail:
+        return nm.value, ts.value, ttft, e2e
+    return nm.value, ts.value
+
+
+def eval_rows(queue, model, perms: np.ndarray, row0: int = 0, rows: int | None = None) -> np.ndarray:
+    a = _Args(queue, model)
+    perms = np.ascontiguousarray(perms, dtype=np.uint16)
+    if rows is None:
+        rows = perms.shape[0] - row0
+    out = np.zeros((rows, 2), np.int64)
+    lib().orc_eval_rows(a.qp, a.mp, _p(perms), row0, rows, _p(out))
+    return out
+
+
+def philox(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, np.uint32)
+    lib().orc_philox(_p(c), _p(k), _p(out))
+    return out
+
+
+def det_exp(x: float) -> float:
+    return lib().orc_det_exp(float(x))
+
+
+def accept(delta: int, t_ref: int, T: float, w3: int) -> bool:
+    return bool(lib().orc_accept(int(delta), int(t_ref), float(T), int(w3)))
+
+
+def fy_perm(seed: int, n: int, idx: int) -> np.ndarray:
+    out = np.zeros(n, np.uint16)
+    lib().orc_fy_perm(int(seed), int(n), int(idx), _p(out))
+    return out
+
+
+def fy_perms(seed: int, n: int, rows: int, row0: int = 0) -> np.ndarray:
+    return np.stack([fy_perm(seed, n, row0 + k) for k in range(rows)]) if rows else np.zeros((0, n), np.uint16)
+
+
+def positions(n: int, w1: int, w2: int) -> tuple[int, int]:
+    i, j = C.c_int32(), C.c_int32()
+    lib().orc_positions(int(n), int(w1), int(w2), C.byref(i), C.byref(j))
+    return i.value, j.value
+
+
+def swap(perm, i, j) -> np.ndarray:
+    p = np.array(perm, dtype=np.uint16)
+    lib().orc_swap(_p(p), int(i), int(j))
+    return p
+
+
+def insert(perm, i, j) -> np.ndarray:
+    p = np.array(perm, dtype=np.uint16)
+    lib().orc_insert(_p(p), int(i), int(j))
+    return p
+
+
+def solo(queue, model, r: int) -> int:
+    a = _Args(queue, model)
+    return lib().orc_solo(a.qp, a.mp, int(r))
+
+
+def start(queue, model):
+    """(start order, t_ref, allmet, start_n, start_t)."""
+    a = _Args(queue, model)
+    st = np.zeros(a.n, np.uint16)
+    t_ref, sn, stt = C.c_int64(), C.c_int64(), C.c_int64()
+    allmet = lib().orc_start(a.qp, a.mp, _p(st), C.byref(t_ref), C.byref(sn), C.byref(stt))
+    return st, t_ref.value, bool(allmet), sn.value, stt.value
+
+
+def anneal_chain(queue, model, chain: int, iters: int, T0: float, alpha: float, seed: int,
+                 start_info=None, trace: bool = False) -> dict:
+    """One annealing chain; returns final/best orders, the per-chain record and (optionally) the trace."""
+    a = _Args(queue, model)
+    if start_info is None:
+        start_info = start(queue, model)
+    st, t_ref, allmet = start_info[0], start_info[1], start_info[2]
+    st = np.ascontiguousarray(st, dtype=np.uint16)
+    cur = np.zeros(a.n, np.uint16)
+    best = np.zeros(a.n, np.uint16)
+    rec = np.zeros(8, np.int64)
+    tr = np.zeros((iters, 4), np.int64) if trace else None
+    lib().orc_anneal_chain(a.qp, a.mp, _p(st), int(t_ref), int(allmet), int(chain), int(iters),
+                           float(T0), float(alpha), int(seed), _p(cur), _p(best), _p(rec),
+                           _p(tr) if trace else None)
+    out = dict(cur=cur, best=best, rec=rec)
+    if trace:
+        out["trace"] = tr
+    return out
+
+
+def brute(queue, model):
+    """(best_n, best_t, first optimal order, number of optimal orders) over all n! orders."""
+    a = _Args(queue, model)
+    if a.n > 10:
+        raise ValueError("brute force is limited to n <= 10")
+    bn, bt = C.c_int64(), C.c_int64()
+    bp = np.zeros(a.n, np.uint16)
+    cnt = lib().orc_brute(a.qp, a.mp, C.byref(bn), C.byref(bt), _p(bp))
+    return bn.value, bt.value, bp, int(cnt)
+
+
+def better(k1, k2) -> bool:
+    """Score order: attainment first, then lower total latency."""
+    return k1[0] > k2[0] or (k1[0] == k2[0] and k1[1] < k2[1])

@@ -1,0 +1,102 @@
+/* CPU oracle for the SLO-aware simulated-annealing scheduler -- TEST INFRASTRUCTURE ONLY.
+ *
+ * Plain, slow, single-threaded C. Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may call it. It shares no code, header, table or
+ * constant with the GPU library; the two meet only through the seeded input
+ * generator and through the results the tests compare.
+ *
+ * Paper: "SLO-Aware Scheduling for Large Language Model Inferences" (Huang et al.).
+ *   - objective and SLO flags: Section "Problem Formulation", Eqs. for G = n/t,
+ *     t = sum of e2e latencies, n = sum x_i, x_i, TTFT, TPOT;
+ *   - latency model: Section "Latency Predictor" (prefill, per-token decode and its
+ *     accumulation over the output tokens, TPOT = decode time / output length);
+ *   - search: Algorithm 1 "Simulated-Annealing Priority Mapping" and Section
+ *     "Priority Mapping Algorithm".
+ *
+ * All latencies are int64 microseconds. The only floating point is the fp64
+ * Metropolis test (orc_accept), compiled without FMA contraction or fast-math.
+ *
+ * Parity pins (what checks this oracle against something other than itself) are
+ * listed per function below; "parity unpinned" marks the annealing trajectory,
+ * which has no published values and is checked only for its properties.
+ */
+#ifndef SLO_ORACLE_H
+#define SLO_ORACLE_H
+#include <stdint.h>
+
+enum { ORC_TTFT = 0, ORC_TPOT = 1, ORC_E2E = 2 };
+enum { ORC_STATIC = 0, ORC_CONTINUOUS = 1 };
+enum { ORC_TAG_ANNEAL = 0x53414e4e, ORC_TAG_FY = 0x46495348 };
+
+typedef struct {
+  int32_t n;
+  const uint16_t *in_len, *out_len;
+  const uint8_t *kind;
+  const uint32_t *thr_us;
+} orc_queue;
+
+typedef struct {
+  int32_t max_batch, policy;
+  int64_t p0, p1, d0, d1, d2;
+  int64_t t_ref_us;
+  uint64_t swap_threshold;
+} orc_model;
+
+/* per-chain record layout (int64 each) */
+enum { ORC_R_CUR_N, ORC_R_CUR_T, ORC_R_BEST_N, ORC_R_BEST_T, ORC_R_BEST_ITER,
+       ORC_R_ACCEPTS, ORC_R_DIGEST, ORC_R_ALLMET, ORC_R_WORDS };
+
+/* Step-by-step timeline of one priority order. Returns 0, or -1 if perm is not a
+ * permutation of 0..n-1. ttft/e2e (nullable) receive per-request values indexed by
+ * request id. Pinned by hand-worked timelines, Smith's rule at batch size 1,
+ * closed-form decode sums, and batching invariants. */
+int orc_replay(const orc_queue *q, const orc_model *m, const uint16_t *perm,
+               int64_t *n_met, int64_t *t_sum, int64_t *ttft, int64_t *e2e);
+
+/* Rows of a k x n permutation matrix; out is k x 2 (n_met, t_sum) or (-1,-1). */
+void orc_eval_rows(const orc_queue *q, const orc_model *m, const uint16_t *perms,
+                   int64_t row0, int64_t rows, int64_t *out);
+
+/* Philox4x32-10 block (Salmon et al., SC'11). Pinned by published known-answer vectors. */
+void orc_philox(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* exp(x) for x <= 0 by Cody-Waite reduction and a Taylor polynomial; 0 below -708.
+ * Pinned by its error against the C library exp. */
+double orc_det_exp(double x);
+
+/* Metropolis acceptance for a maximisation with energy f = n - t/t_ref:
+ * accept iff delta >= 0, or u < exp(delta / (t_ref * T)) with u = w3 * 2^-32. */
+int orc_accept(int64_t delta, int64_t t_ref, double T, uint32_t w3);
+
+/* Fisher-Yates shuffle of 0..n-1, draws from Philox keyed by seed, row idx. */
+void orc_fy_perm(uint64_t seed, int32_t n, uint32_t idx, uint16_t *perm);
+
+/* Start of every chain (Algorithm 1 initialisation): stable sort by solo latency;
+ * the input order replaces it when its key is strictly better. Returns allmet flag. */
+int orc_start(const orc_queue *q, const orc_model *m, uint16_t *start, int64_t *t_ref,
+              int64_t *start_n, int64_t *start_t);
+
+/* The two moves. */
+void orc_swap(uint16_t *p, int32_t i, int32_t j);
+void orc_insert(uint16_t *p, int32_t from, int32_t to);
+
+/* Proposal positions from one Philox block (i uniform, j uniform over the others). */
+void orc_positions(int32_t n, uint32_t w1, uint32_t w2, int32_t *i, int32_t *j);
+
+/* One annealing chain. start/t_ref from orc_start. cur/best receive n entries,
+ * rec ORC_R_WORDS int64. trace (nullable) receives iters x 4 int64:
+ * (accepted, n, t, move) after each proposal. Parity unpinned (trajectory). */
+void orc_anneal_chain(const orc_queue *q, const orc_model *m, const uint16_t *start,
+                      int64_t t_ref, int allmet, int32_t chain, int32_t iters, double T0,
+                      double alpha, uint64_t seed, uint16_t *cur, uint16_t *best, int64_t *rec,
+                      int64_t *trace);
+
+/* Exhaustive search over all n! orders (n <= 10): optimum key and the
+ * lexicographically first optimal order; returns the number of optimal orders. */
+int64_t orc_brute(const orc_queue *q, const orc_model *m, int64_t *best_n, int64_t *best_t,
+                  uint16_t *best_perm);
+
+/* Solo latency of one request (its replay alone). */
+int64_t orc_solo(const orc_queue *q, const orc_model *m, int32_t r);
+
+#endif

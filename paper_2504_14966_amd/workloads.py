@@ -1,0 +1,195 @@
+"""Seeded synthetic request queues and run settings for the five benchmark workloads.
+
+This module only draws inputs. It holds none of the scheduler's arithmetic (no latency
+model evaluation, no objective, no annealing), so both the HIP path and the CPU oracle
+can consume what it produces.
+
+Each queue stands in for the paper's evenly mixed, shuffled chat/code request pool
+(Section "Experimental setup": ShareGPT-style chat with TTFT/TPOT SLOs and code
+completion with an end-to-end SLO, prompt lengths below 2k). The datasets themselves
+are not used; only their shape is imitated with lognormal length distributions.
+
+Request attributes follow the problem formulation (Section "Problem Formulation"):
+input length l_i, predicted output length l_o, one SLO kind and its threshold in
+integer microseconds. Kinds: 0 = TTFT, 1 = TPOT, 2 = end-to-end.
+"""
+from __future__ import annotations
+
+import hashlib
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+KIND_TTFT = 0
+KIND_TPOT = 1
+KIND_E2E = 2
+
+POLICY_STATIC = 0
+POLICY_CONTINUOUS = 1
+
+# Base SLO thresholds in microseconds, indexed by kind (TTFT, TPOT, E2E).
+BASE_THR_SINGLE = (200_000, 50_000, 8_000_000)
+BASE_THR_CHAT = BASE_THR_SINGLE
+BASE_THR_CODE = (300_000, 75_000, 12_000_000)  # 1.5x: ratio of mean outputs 300/200
+
+# Generation streams: one independent PCG64 stream per purpose.
+_S_IN, _S_OUT, _S_KIND, _S_THR, _S_CLASS = 1, 2, 3, 4, 5
+
+
+@dataclass
+class Queue:
+    """Structure-of-arrays request queue (length n)."""
+    in_len: np.ndarray   # uint16
+    out_len: np.ndarray  # uint16, >= 1
+    kind: np.ndarray     # uint8 in {0, 1, 2}
+    thr_us: np.ndarray   # uint32
+
+    @property
+    def n(self) -> int:
+        return int(self.in_len.shape[0])
+
+    def sha256(self) -> str:
+        h = hashlib.sha256()
+        for a in (self.in_len, self.out_len, self.kind, self.thr_us):
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+
+@dataclass
+class Model:
+    """Integer-microsecond latency model and admission policy.
+
+    prefill of an admitted group = sum over its requests of (p0 + p1 * l_in);
+    one decode step = d0 + d1 * b + d2 * (sum of the active requests' context lengths).
+    """
+    max_batch: int
+    policy: int
+    p0: int
+    p1: int
+    d0: int
+    d1: int
+    d2: int
+    t_ref_us: int = 0
+    swap_threshold: int = 1 << 31
+
+
+@dataclass
+class Workload:
+    name: str
+    queue: Queue
+    model: Model
+    chains: int = 0
+    iters: int = 0
+    T0: float = 1.0
+    alpha: float = 0.999
+    seed: int = 0
+    eval_rows: int = 0          # > 0 for the evaluation-only workload
+    perm_seed: int = 0
+    extra: dict = field(default_factory=dict)
+
+
+def lognormal_params(mean: float, sd: float) -> tuple[float, float]:
+    """(mu, sigma) of the lognormal whose mean and standard deviation are given."""
+    s2 = math.log1p((sd / mean) ** 2)
+    return math.log(mean) - s2 / 2.0, math.sqrt(s2)
+
+
+def _rng(seed: int, purpose: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed, spawn_key=(purpose,))))
+
+
+def _lengths(rng, mean, sd, lo, hi, size) -> np.ndarray:
+    mu, sigma = lognormal_params(mean, sd)
+    x = rng.lognormal(mu, sigma, size=size)
+    return np.clip(np.floor(x + 0.5), lo, hi).astype(np.uint16)
+
+
+def single_class_queue(n: int, seed: int, in_mean=300.0, in_sd=250.0, in_hi=2048) -> Queue:
+    """One request class: lognormal input/output lengths, kinds uniform over 3."""
+    in_len = _lengths(_rng(seed, _S_IN), in_mean, in_sd, 16, in_hi, n)
+    out_len = _lengths(_rng(seed, _S_OUT), 250.0, 200.0, 8, 1024, n)
+    kind = _rng(seed, _S_KIND).integers(0, 3, size=n).astype(np.uint8)
+    thr = np.asarray(BASE_THR_SINGLE, dtype=np.uint32)[kind]
+    return Queue(in_len, out_len, kind, thr.astype(np.uint32))
+
+
+def two_class_queue(n: int, seed: int, kind_probs=None, thr_jitter=0.0) -> Queue:
+    """Evenly mixed code-like and chat-like requests, shuffled.
+
+    Both classes keep the single-class coefficient of variation (input 250/300,
+    output 200/250). code: input mean 400, output mean 300; chat: input mean 150,
+    output mean 200. With thr_jitter > 0 each threshold is integer-uniform on
+    [round((1-j)*base), round((1+j)*base)] of its class.
+    """
+    if n % 2:
+        raise ValueError("two-class queue needs an even n")
+    half = n // 2
+    cls = np.concatenate([np.zeros(half, np.uint8), np.ones(half, np.uint8)])  # 0 code, 1 chat
+    cls = _rng(seed, _S_CLASS).permutation(cls)
+    r_in, r_out = _rng(seed, _S_IN), _rng(seed, _S_OUT)
+    code_in = _lengths(r_in, 400.0, 400.0 * 250 / 300, 16, 2048, n)
+    chat_in = _lengths(r_in, 150.0, 150.0 * 250 / 300, 16, 2048, n)
+    code_out = _lengths(r_out, 300.0, 300.0 * 200 / 250, 8, 1024, n)
+    chat_out = _lengths(r_out, 200.0, 200.0 * 200 / 250, 8, 1024, n)
+    in_len = np.where(cls == 0, code_in, chat_in).astype(np.uint16)
+    out_len = np.where(cls == 0, code_out, chat_out).astype(np.uint16)
+    rk = _rng(seed, _S_KIND)
+    if kind_probs is None:
+        kind = rk.integers(0, 3, size=n).astype(np.uint8)
+    else:
+        kind = rk.choice(3, size=n, p=np.asarray(kind_probs, dtype=np.float64)).astype(np.uint8)
+    base = np.where(cls[:, None] == 0, np.asarray(BASE_THR_CODE)[None, :],
+                    np.asarray(BASE_THR_CHAT)[None, :])[np.arange(n), kind].astype(np.int64)
+    if thr_jitter > 0:
+        lo = np.floor((1.0 - thr_jitter) * base + 0.5).astype(np.int64)
+        hi = np.floor((1.0 + thr_jitter) * base + 0.5).astype(np.int64)
+        thr = _rng(seed, _S_THR).integers(lo, hi + 1)
+    else:
+        thr = base
+    return Queue(in_len, out_len, kind, thr.astype(np.uint32))
+
+
+def make_queue(n: int, seed: int = 0, in_hi: int = 2048) -> Queue:
+    """A small single-class queue for tests (any n >= 1)."""
+    return single_class_queue(n, seed, in_hi=in_hi)
+
+
+def random_queue(rng: np.random.Generator, n: int, max_in=2048, max_out=64, thr_hi=None) -> Queue:
+    """Uniformly random small queue for property tests (short outputs keep replays cheap)."""
+    in_len = rng.integers(1, max_in + 1, size=n).astype(np.uint16)
+    out_len = rng.integers(1, max_out + 1, size=n).astype(np.uint16)
+    kind = rng.integers(0, 3, size=n).astype(np.uint8)
+    if thr_hi is None:
+        thr_hi = 20_000 * n * max_out
+    thr = rng.integers(0, thr_hi, size=n).astype(np.uint32)
+    return Queue(in_len, out_len, kind, thr)
+
+
+MODEL_A = dict(p0=2000, p1=40, d0=8000, d1=300, d2=2)   # workloads 1, 2, 3, 5
+MODEL_B = dict(p0=2000, p1=40, d0=8000, d1=250, d2=1)   # burst workload 4
+
+
+def workload(idx: int) -> Workload:
+    """The five benchmark workloads (1-based index)."""
+    if idx == 1:
+        return Workload("tiny-n8-b4-static", single_class_queue(8, 0),
+                        Model(4, POLICY_STATIC, **MODEL_A), chains=1, iters=2000, T0=1.0, alpha=0.999)
+    if idx == 2:
+        return Workload("mix-n64-b16-static", two_class_queue(64, 0),
+                        Model(16, POLICY_STATIC, **MODEL_A), chains=1024, iters=10000, T0=1.0, alpha=0.999)
+    if idx == 3:
+        return Workload("mix-n256-b32-continuous", two_class_queue(256, 0, kind_probs=(0.4, 0.3, 0.3),
+                                                                   thr_jitter=0.25),
+                        Model(32, POLICY_CONTINUOUS, **MODEL_A), chains=2048, iters=20000, T0=1.0, alpha=0.999)
+    if idx == 4:
+        return Workload("burst-n1024-b64-static", single_class_queue(1024, 0, in_mean=300.0, in_sd=600.0,
+                                                                     in_hi=8192),
+                        Model(64, POLICY_STATIC, **MODEL_B), chains=4096, iters=5000, T0=2.0, alpha=0.9995)
+    if idx == 5:
+        return Workload("eval-n128-b16-static", two_class_queue(128, 0),
+                        Model(16, POLICY_STATIC, **MODEL_A), eval_rows=1 << 20, perm_seed=0)
+    raise ValueError(f"no workload {idx}")
+
+
+ALL_WORKLOADS = (1, 2, 3, 4, 5)
