@@ -1,0 +1,140 @@
+/* sloanneal -- MI355X (gfx950) library for the data-parallel hot path of the SLO-aware
+ * LLM request scheduler of Huang et al., "SLO-Aware Scheduling for Large Language Model
+ * Inferences": simulated annealing over request priority orders (Algorithm 1), each
+ * proposal scored by replaying a batched-serving timeline under the integer latency model.
+ *
+ * Conventions for every entry point:
+ *   - array arguments are DEVICE pointers unless stated otherwise; the caller owns them
+ *     (e.g. torch tensors) and the library never frees or retains them;
+ *   - work is enqueued on the caller's stream and runs asynchronously. sched_eval and
+ *     sched_anneal first copy the n-entry request queue to the host and synchronise the
+ *     stream once, to validate it and to choose integer widths; nothing else blocks;
+ *   - every call returns SCHED_OK (0) or a negative SCHED_E* code and then enqueues nothing;
+ *   - the library keeps no global state: all annealing state lives in the caller's
+ *     workspace, so calls on distinct workspaces and streams are independent;
+ *   - latencies are int64 microseconds; results are bit-identical run to run.
+ */
+#ifndef SLOANNEAL_H
+#define SLOANNEAL_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  SCHED_OK = 0,
+  SCHED_EINVAL = -1, /* a size, pointer, parameter or queue entry is out of range */
+  SCHED_ENOSPC = -2, /* workspace smaller than sched_ws_bytes(n, chains) */
+  SCHED_ERANGE = -3, /* the queue and model could overflow the int64 clock or objective */
+  SCHED_EHIP = -4    /* a HIP runtime call failed; sched_strerror gives its message */
+};
+
+/* SLO kinds (Problem Formulation, the SLO-met flag x_i): a request meets its SLO when
+ * TTFT <= thr, or TPOT <= thr, or end-to-end latency <= thr. TPOT is the decode time
+ * divided by the output length and is checked exactly as (e2e - TTFT) <= thr * l_out. */
+enum { SCHED_TTFT = 0, SCHED_TPOT = 1, SCHED_E2E = 2 };
+
+/* Admission policy. STATIC: consecutive groups of max_batch requests in priority order
+ * form batches; a batch starts when the previous one has drained (batch index and
+ * waiting time of the Problem Formulation). CONTINUOUS: a finished request frees its
+ * slot, refilled from the priority order at the next iteration. */
+enum { SCHED_STATIC = 0, SCHED_CONTINUOUS = 1 };
+
+#define SCHED_MAX_N 1024
+#define SCHED_MAX_BATCH 64
+
+/* Request queue, structure of arrays, n entries, DEVICE pointers (paper: newly arrived
+ * jobs with input length, predicted output length, SLO kind and threshold). */
+typedef struct {
+  int32_t n;                /* 1 .. SCHED_MAX_N */
+  const uint16_t *in_len;   /* input (prompt) tokens l_i */
+  const uint16_t *out_len;  /* predicted output tokens l_o, >= 1 */
+  const uint8_t *kind;      /* SCHED_TTFT / SCHED_TPOT / SCHED_E2E */
+  const uint32_t *thr_us;   /* SLO threshold in microseconds (per token for TPOT) */
+} sched_queue_t;
+
+/* Latency model in integer microseconds (Latency Predictor section, integer form) and
+ * annealing constants. Host struct. All coefficients must be >= 0.
+ *   prefill iteration of an admitted group = sum over the group of (p0 + p1 * l_in);
+ *     decodes already running stall during it; the group's TTFT is its end;
+ *   decode iteration = d0 + d1 * b + d2 * ctx, b = running requests, ctx = the sum of
+ *     their context lengths; a request's k-th decode step has context l_in + k;
+ *   a request ends with its l_out-th decode iteration. */
+typedef struct {
+  int32_t max_batch;        /* 1 .. SCHED_MAX_BATCH */
+  int32_t policy;           /* SCHED_STATIC or SCHED_CONTINUOUS */
+  int64_t p0, p1, d0, d1, d2;
+  int64_t t_ref_us;         /* Metropolis latency scale; 0 => total latency of the input order */
+  uint64_t swap_threshold;  /* proposal is a swap iff Philox word 0 < this (0 .. 2^32); 2^31 = 50/50 */
+} sched_model_t;
+
+/* Score K priority orders (objective of the Problem Formulation, kept as the integer
+ * pair n = requests meeting their SLO, t = sum of end-to-end latencies).
+ *   perms  : k x n uint16, row-major; row r is a priority order (position -> request id)
+ *   out    : k x 2 int64 (n_met, t_sum); a row that is not a permutation of 0..n-1 gets
+ *            (-1, -1)
+ *   detail : nullable; k x n x 2 int64 (ttft, e2e) indexed by request id; rows that are
+ *            not permutations are left untouched
+ * Returns SCHED_EINVAL for k < 0, a null pointer, a bad queue or model, SCHED_ERANGE if
+ * the clock could overflow. k == 0 is a no-op. */
+int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
+               int64_t k, int64_t *out, int64_t *detail, hipStream_t stream);
+
+/* Bytes of workspace sched_anneal needs for n requests and `chains` chains (0 on bad sizes). */
+size_t sched_ws_bytes(int32_t n, int32_t chains);
+
+/* Run `chains` independent annealing chains of `iters` proposals each (Algorithm 1 with a
+ * geometric schedule T_k = T0 * alpha^k, one proposal per iteration). All chains start
+ * from the Algorithm 1 start order: requests sorted by solo latency (stable), replaced by
+ * the input order when that scores strictly better. Proposal k of chain c uses the
+ * Philox4x32-10 block with counter (k, c, 0, 0x53414E4E) and key (seed low, seed high):
+ * word 0 picks swap or insert, words 1 and 2 the positions, word 3 the acceptance draw.
+ * A worse candidate is accepted iff w3 * 2^-32 < exp(delta / (t_ref * T_k)) with
+ * delta = (n' - n) * t_ref - (t' - t); others are always accepted. Each chain tracks its
+ * best-so-far order (attainment first, then lower total latency); the best over chains
+ * (lowest chain id on ties) is reduced at the end.
+ *   ws : DEVICE workspace of at least sched_ws_bytes(n, chains) bytes, 256-byte aligned;
+ *        it holds the start order, per-chain records and orders after the call.
+ * Returns SCHED_EINVAL for chains < 1, iters < 0, T0 <= 0, alpha <= 0 or non-finite,
+ * a bad queue or model; SCHED_ENOSPC for a short workspace; SCHED_ERANGE on overflow risk. */
+int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t chains,
+                 int32_t iters, double T0, double alpha, uint64_t seed, void *ws, size_t ws_bytes,
+                 hipStream_t stream);
+
+/* Best order over all chains of the last sched_anneal on ws.
+ *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain). */
+int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream);
+
+/* Per-chain readout of the last sched_anneal on ws (observability and parity checks).
+ *   per_chain  : chains x 8 int64 (DEVICE) = (cur n, cur t, best n, best t, best iteration
+ *                or -1, accepted proposals, trajectory digest, start-order-meets-all flag)
+ *   cur_perms  : nullable, chains x n uint16 final orders
+ *   best_perms : nullable, chains x n uint16 best orders
+ * The digest folds (iteration, n, t) of every accepted proposal, in order, with 64-bit
+ * FNV-1a steps: d = (d ^ word) * 0x100000001B3, starting at 0xCBF29CE484222325. */
+int sched_chains(const void *ws, int64_t *per_chain, uint16_t *cur_perms, uint16_t *best_perms,
+                 hipStream_t stream);
+
+/* Start order and constants of the last sched_anneal on ws.
+ *   start_out : n uint16 (DEVICE); info_out : 4 int64 (DEVICE) = (t_ref, start n, start t,
+ *               1 if the solo-latency order meets every SLO else 0). */
+int sched_start_info(const void *ws, uint16_t *start_out, int64_t *info_out, hipStream_t stream);
+
+/* Fill rows row0 .. row0+k-1 of a Fisher-Yates permutation family: row r shuffles 0..n-1
+ * for positions p = n-1 down to 1 with j = (w * (p + 1)) >> 32, w = word (p mod 4) of the
+ * Philox4x32-10 block with counter (p / 4, r, 1, 0x46495348) and key (seed low, seed high).
+ *   perms : k x n uint16 (DEVICE), row-major. */
+int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t *perms,
+                    hipStream_t stream);
+
+/* Static message for a SCHED_* code; for SCHED_EHIP the last HIP error seen by this thread. */
+const char *sched_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,83 @@
+// Shared device definitions: the model passed to kernels, the packed request record
+// staged in LDS, the workspace layout and 64-lane wavefront helpers.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sa {
+
+constexpr int kWave = 64;
+
+// Integer latency model plus sizes, passed by value to every kernel.
+struct DevModel {
+  int32_t n;       // requests
+  int32_t B;       // max batch
+  int32_t policy;  // 0 static, 1 continuous
+  int32_t pad;
+  uint64_t p0, p1, d0, d1, d2;
+};
+
+// One request packed into 16 bytes for a single ds_read_b128 gather:
+//   x = l_in | l_out << 16, y = threshold (us), z = kind, w = prefill cost p0 + p1*l_in
+//   (low 32 bits; the high bits live in the separate pf_hi when the model is wide).
+__device__ __forceinline__ uint32_t req_lin(uint4 r) { return r.x & 0xFFFFu; }
+__device__ __forceinline__ uint32_t req_lout(uint4 r) { return r.x >> 16; }
+
+// Workspace layout (bytes), identical on host and device.
+struct WsHeader {
+  uint64_t magic;
+  int32_t n, chains, iters, policy;
+  int64_t t_ref, start_n, start_t, allmet;
+  int64_t best_chain, best_n, best_t;
+  int64_t reserved[20];
+};
+static_assert(sizeof(WsHeader) <= 256, "header fits its slot");
+constexpr uint64_t kWsMagic = 0x534c4f414e4e3031ull;  // "SLOANN01"
+
+__host__ __device__ __forceinline__ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ __forceinline__ size_t ws_perm_stride(int n) { return round_up((size_t)n, 128); }  // u16 entries
+__host__ __device__ __forceinline__ size_t ws_off_start() { return 256; }
+__host__ __device__ __forceinline__ size_t ws_off_records(int n) {
+  return ws_off_start() + round_up(2 * (size_t)n, 256);
+}
+__host__ __device__ __forceinline__ size_t ws_off_cur(int n, int chains) {
+  return ws_off_records(n) + round_up((size_t)chains * 64, 256);
+}
+__host__ __device__ __forceinline__ size_t ws_off_best(int n, int chains) {
+  return ws_off_cur(n, chains) + (size_t)chains * ws_perm_stride(n) * 2;
+}
+__host__ __device__ __forceinline__ size_t ws_total(int n, int chains) {
+  return ws_off_best(n, chains) + (size_t)chains * ws_perm_stride(n) * 2;
+}
+
+// ---- wavefront helpers (64 lanes) ----
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63u); }
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = min(v, (uint32_t)__shfl_xor((int)v, o));
+  return v;
+}
+__device__ __forceinline__ int rank_in_mask(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+__device__ __forceinline__ int ballot_count(bool p) { return __popcll(__ballot(p)); }
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+}  // namespace sa

@@ -1,0 +1,93 @@
+// Device random numbers and the Metropolis test for gfx950.
+//
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel Random Numbers: As Easy as 1, 2, 3",
+// SC'11): ten rounds of two 32x32->64 multiplies, a cross of the counter words and a key
+// xor; the key advances by the two Weyl increments between rounds. Callers pass
+// wave-uniform counters and keys, so the compiler keeps the whole block on the scalar unit.
+//
+// fast_exp_neg: e^x for x <= 0 written from the mathematics: x = k ln2 + r with
+// k = floor(x / ln2 + 1/2) and |r| <= ln2 / 2, r formed with ln2 split into a 32-bit head
+// (exact products with k) and a tail; e^r as its Taylor series to degree 13 evaluated by
+// Horner's rule; times 2^k assembled from exponent bits. Each step is one IEEE-754
+// double operation with contraction disabled, so the value is a fixed function of x.
+// Below -708 (and for -inf / NaN) it returns 0.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sa {
+
+constexpr uint32_t kTagAnneal = 0x53414E4Eu;
+constexpr uint32_t kTagShuffle = 0x46495348u;
+
+struct u32x4 {
+  uint32_t x, y, z, w;
+};
+
+__device__ __forceinline__ u32x4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                               uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t lo0 = 0xD2511F53u * c0;
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c0);
+    const uint32_t lo1 = 0xCD9E8D57u * c2;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2);
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return {c0, c1, c2, c3};
+}
+
+#pragma clang fp contract(off)
+__device__ __forceinline__ double fast_exp_neg(double x) {
+  if (!(x >= -708.0)) return 0.0;
+  if (x > 0.0) x = 0.0;
+  const double kd = floor(x * 1.4426950408889634 + 0.5);
+  const double r = (x - kd * 6.93147180369123816490e-01) - kd * 1.90821492927058770002e-10;
+  double p = 1.0 / 6227020800.0;
+  p = p * r + 1.0 / 479001600.0;
+  p = p * r + 1.0 / 39916800.0;
+  p = p * r + 1.0 / 3628800.0;
+  p = p * r + 1.0 / 362880.0;
+  p = p * r + 1.0 / 40320.0;
+  p = p * r + 1.0 / 5040.0;
+  p = p * r + 1.0 / 720.0;
+  p = p * r + 1.0 / 120.0;
+  p = p * r + 1.0 / 24.0;
+  p = p * r + 1.0 / 6.0;
+  p = p * r + 0.5;
+  p = p * r + 1.0;
+  p = p * r + 1.0;
+  const int64_t k = (int64_t)kd;
+  const double scale = __longlong_as_double((long long)((uint64_t)(k + 1023) << 52));
+  return p * scale;
+}
+
+// Metropolis rule for a maximisation with energy n - t / t_ref, scaled by t_ref so that
+// delta is an exact integer: keep any candidate that is not worse; keep a worse one
+// iff u < e^(delta / (t_ref * T)), u = w3 * 2^-32.
+__device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
+  if (delta >= 0) return true;
+  const double x = (double)delta / ((double)t_ref * T);
+  const double u = (double)w3 * (1.0 / 4294967296.0);
+  return u < fast_exp_neg(x);
+}
+
+// Multiply-shift mapping of two 32-bit words to distinct positions i != j in [0, n).
+__device__ __forceinline__ void pick_positions(int n, uint32_t w1, uint32_t w2, int &i, int &j) {
+  i = (int)(((uint64_t)w1 * (uint64_t)n) >> 32);
+  if (n < 2) {
+    j = i;
+    return;
+  }
+  const int jp = (int)(((uint64_t)w2 * (uint64_t)(n - 1)) >> 32);
+  j = jp + (jp >= i ? 1 : 0);
+}
+
+}  // namespace sa

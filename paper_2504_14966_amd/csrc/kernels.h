@@ -1,0 +1,355 @@
+// Kernels of the annealing hot path (gfx950, wave64).
+//
+//   eval_kernel    : one wave per priority order; validates the row, replays it.
+//   start_kernel   : Algorithm 1 initialisation (one workgroup): solo latency of every
+//                    request, stable bitonic sort by (solo, id), scores of the sorted and
+//                    the input orders, t_ref; writes the workspace header and start order.
+//   anneal_kernel  : one wave per chain; per iteration a Philox block, a candidate order
+//                    built on the fly from the current one, its replay, the Metropolis
+//                    test and best-so-far tracking.
+//   reduce_kernel  : lexicographic argmax over chains (n desc, t asc, chain asc).
+//   small copy kernels for the readouts and the Fisher-Yates family.
+#pragma once
+#include "device_common.h"
+#include "device_replay.h"
+#include "device_rng.h"
+
+namespace sa {
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+
+struct QueuePtrs {
+  const uint16_t *in_len, *out_len;
+  const uint8_t *kind;
+  const uint32_t *thr;
+};
+
+// Cooperative, coalesced load of the request records into LDS.
+__device__ __forceinline__ void load_requests(const QueuePtrs &q, int n, uint4 *req) {
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r], 0u);
+  }
+}
+
+__device__ __forceinline__ size_t lds_align(size_t x) { return (x + 15) & ~size_t(15); }
+
+template <bool DETAIL>
+__global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, const uint16_t *__restrict__ perms,
+                                                       int64_t rows, int64_t *__restrict__ out,
+                                                       int64_t *__restrict__ detail) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t per_wave = lds_align((size_t)n * 2) + 64 * 16 + 32 * 4;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
+  uint16_t *perm = reinterpret_cast<uint16_t *>(wbase);
+  uint4 *stage = reinterpret_cast<uint4 *>(wbase + lds_align((size_t)n * 2));
+  uint32_t *bitmap = reinterpret_cast<uint32_t *>(wbase + lds_align((size_t)n * 2) + 64 * 16);
+  load_requests(q, n, req);
+  __syncthreads();
+  const int lane = lane_id();
+  for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < rows;
+       row += (int64_t)gridDim.x * kWavesPerBlock) {
+    const uint16_t *src = perms + row * n;
+    if (lane < 32) bitmap[lane] = 0u;
+    wave_sync_lds();
+    bool bad = false;
+    for (int p = lane; p < n; p += kWave) {
+      const uint32_t v = src[p];
+      perm[p] = (uint16_t)v;
+      if (v >= (uint32_t)n) {
+        bad = true;
+      } else {
+        const uint32_t bit = 1u << (v & 31u);
+        const uint32_t old = atomicOr(&bitmap[v >> 5], bit);
+        if (old & bit) bad = true;
+      }
+    }
+    wave_sync_lds();
+    if (__ballot(bad) != 0ull) {
+      if (lane == 0) {
+        out[2 * row] = -1;
+        out[2 * row + 1] = -1;
+      }
+      continue;
+    }
+    const Score s = replay<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, DETAIL ? detail + row * n * 2 : nullptr);
+    if (lane == 0) {
+      out[2 * row] = s.n;
+      out[2 * row + 1] = (int64_t)s.t;
+    }
+    wave_sync_lds();
+  }
+}
+
+__device__ __forceinline__ bool key_better(int64_t n1, uint64_t t1, int64_t n2, uint64_t t2) {
+  return n1 > n2 || (n1 == n2 && t1 < t2);
+}
+
+// One workgroup of 1024 threads; n <= 1024.
+__global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, int chains, int iters,
+                                                      int64_t t_ref_user, unsigned char *ws) {
+  __shared__ uint4 req[1024];
+  __shared__ uint64_t key_solo[1024];
+  __shared__ uint16_t key_id[1024];
+  __shared__ uint16_t ident[1024];
+  __shared__ uint4 stage[64];
+  const int n = m.n;
+  const int tid = threadIdx.x;
+  load_requests(q, n, req);
+  int np = 1;
+  while (np < n) np <<= 1;
+  if (tid < np) {
+    if (tid < n) {
+      const uint32_t lin = q.in_len[tid], L = q.out_len[tid];
+      // a request replayed alone: prefill, then L decode steps at batch size 1 with
+      // context l_in + k, k = 1..L
+      key_solo[tid] = m.p0 + m.p1 * lin + (uint64_t)L * (m.d0 + m.d1 + m.d2 * lin) + m.d2 * ((uint64_t)L * (L + 1) / 2);
+      key_id[tid] = (uint16_t)tid;
+      ident[tid] = (uint16_t)tid;
+    } else {
+      key_solo[tid] = ~0ull;
+      key_id[tid] = 0xFFFFu;
+    }
+  }
+  __syncthreads();
+  for (int k = 2; k <= np; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (tid < np) {
+        const int o = tid ^ j;
+        if (o > tid) {
+          const uint64_t a = key_solo[tid], b = key_solo[o];
+          const uint16_t ia = key_id[tid], ib = key_id[o];
+          const bool a_gt = a > b || (a == b && ia > ib);
+          const bool up = (tid & k) == 0;
+          if (a_gt == up) {
+            key_solo[tid] = b;
+            key_solo[o] = a;
+            key_id[tid] = ib;
+            key_id[o] = ia;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (tid < 64) {
+    const Score sorted = replay<false>(m, req, key_id, Remap{0, 0, 0}, stage, nullptr);
+    const Score input = replay<false>(m, req, ident, Remap{0, 0, 0}, stage, nullptr);
+    const bool use_input = key_better(input.n, input.t, sorted.n, sorted.t);
+    uint16_t *start = reinterpret_cast<uint16_t *>(ws + ws_off_start());
+    for (int p = tid; p < n; p += 64) start[p] = use_input ? (uint16_t)p : key_id[p];
+    if (tid == 0) {
+      WsHeader *h = reinterpret_cast<WsHeader *>(ws);
+      h->magic = kWsMagic;
+      h->n = n;
+      h->chains = chains;
+      h->iters = iters;
+      h->policy = m.policy;
+      h->t_ref = t_ref_user > 0 ? t_ref_user : (input.t > 1 ? (int64_t)input.t : 1);
+      h->start_n = use_input ? input.n : sorted.n;
+      h->start_t = (int64_t)(use_input ? input.t : sorted.t);
+      h->allmet = sorted.n == n ? 1 : 0;
+      h->best_chain = -1;
+      h->best_n = -1;
+      h->best_t = -1;
+    }
+  }
+}
+
+constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ull;
+constexpr uint64_t kFnvPrime = 0x100000001B3ull;
+
+// Per-wave LDS: current and candidate-scratch orders, replay staging.
+__global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
+                                                         double alpha, uint32_t key0, uint32_t key1,
+                                                         uint64_t swap_thr, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t per_wave = lds_align((size_t)n * 2) * 2 + 64 * 16;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
+  uint16_t *bufA = reinterpret_cast<uint16_t *>(wbase);
+  uint16_t *bufB = reinterpret_cast<uint16_t *>(wbase + lds_align((size_t)n * 2));
+  uint4 *stage = reinterpret_cast<uint4 *>(wbase + 2 * lds_align((size_t)n * 2));
+  load_requests(q, n, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * kWavesPerBlock + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  int64_t cn = h->start_n;
+  uint64_t ct = (uint64_t)h->start_t;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    bufA[p] = v;
+    gbest[p] = v;
+  }
+  wave_sync_lds();
+  uint16_t *cur = bufA, *cand = bufB;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  double T = T0;
+  for (int k = 0; k < iters; ++k) {
+    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
+    int i, j;
+    pick_positions(n, w.y, w.z, i, j);
+    const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
+    const Score s = replay<false>(m, req, cur, rm, stage, nullptr);
+    const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
+    const bool acc = metropolis(delta, t_ref, T, w.w);
+    if (acc) {
+      for (int p = lane; p < n; p += kWave) cand[p] = cur[rm.src(p)];
+      wave_sync_lds();
+      uint16_t *tmp = cur;
+      cur = cand;
+      cand = tmp;
+      cn = s.n;
+      ct = s.t;
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (key_better(cn, ct, bn, bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        for (int p = lane; p < n; p += kWave) gbest[p] = cur[p];
+      }
+    }
+    T = T * alpha;
+  }
+  for (int p = lane; p < n; p += kWave) gcur[p] = cur[p];
+  if (lane == 0) {
+    int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
+    rec[0] = cn;
+    rec[1] = (int64_t)ct;
+    rec[2] = bn;
+    rec[3] = (int64_t)bt;
+    rec[4] = biter;
+    rec[5] = accepts;
+    rec[6] = (int64_t)digest;
+    rec[7] = allmet;
+  }
+}
+
+// One workgroup: argmax over chains of (best n, -best t, -chain).
+__global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
+  __shared__ int64_t sn[1024];
+  __shared__ uint64_t st[1024];
+  __shared__ int32_t sc[1024];
+  WsHeader *h = reinterpret_cast<WsHeader *>(ws);
+  const int n = h->n, chains = h->chains;
+  const int64_t *rec = reinterpret_cast<const int64_t *>(ws + ws_off_records(n));
+  int64_t bn = -1;
+  uint64_t bt = ~0ull;
+  int32_t bc = 0x7FFFFFFF;
+  for (int c = threadIdx.x; c < chains; c += blockDim.x) {
+    const int64_t cn = rec[(size_t)c * 8 + 2];
+    const uint64_t ctt = (uint64_t)rec[(size_t)c * 8 + 3];
+    if (key_better(cn, ctt, bn, bt) || (cn == bn && ctt == bt && c < bc)) {
+      bn = cn;
+      bt = ctt;
+      bc = c;
+    }
+  }
+  sn[threadIdx.x] = bn;
+  st[threadIdx.x] = bt;
+  sc[threadIdx.x] = bc;
+  __syncthreads();
+  for (int o = blockDim.x / 2; o > 0; o >>= 1) {
+    if ((int)threadIdx.x < o) {
+      const int u = threadIdx.x + o;
+      if (key_better(sn[u], st[u], sn[threadIdx.x], st[threadIdx.x]) ||
+          (sn[u] == sn[threadIdx.x] && st[u] == st[threadIdx.x] && sc[u] < sc[threadIdx.x])) {
+        sn[threadIdx.x] = sn[u];
+        st[threadIdx.x] = st[u];
+        sc[threadIdx.x] = sc[u];
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    h->best_chain = sc[0];
+    h->best_n = sn[0];
+    h->best_t = (int64_t)st[0];
+  }
+}
+
+__global__ void __launch_bounds__(256) best_copy_kernel(const unsigned char *ws, uint16_t *perm_out, int64_t *key_out) {
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int n = h->n, chains = h->chains;
+  const int64_t c = h->best_chain;
+  const uint16_t *src = reinterpret_cast<const uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)c * ws_perm_stride(n);
+  for (int p = threadIdx.x; p < n; p += blockDim.x) perm_out[p] = src[p];
+  if (threadIdx.x == 0) {
+    key_out[0] = h->best_n;
+    key_out[1] = h->best_t;
+    key_out[2] = c;
+  }
+}
+
+__global__ void __launch_bounds__(256) chains_copy_kernel(const unsigned char *ws, int64_t *per_chain, uint16_t *cur_out,
+                                                           uint16_t *best_out) {
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int n = h->n, chains = h->chains;
+  const size_t stride = ws_perm_stride(n);
+  const int64_t *rec = reinterpret_cast<const int64_t *>(ws + ws_off_records(n));
+  const uint16_t *cur = reinterpret_cast<const uint16_t *>(ws + ws_off_cur(n, chains));
+  const uint16_t *best = reinterpret_cast<const uint16_t *>(ws + ws_off_best(n, chains));
+  const int64_t total = (int64_t)chains * 8;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < total; u += (int64_t)gridDim.x * blockDim.x)
+    per_chain[u] = rec[u];
+  const int64_t tp = (int64_t)chains * n;
+  for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < tp; u += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t c = u / n, p = u - c * n;
+    if (cur_out) cur_out[u] = cur[c * stride + p];
+    if (best_out) best_out[u] = best[c * stride + p];
+  }
+}
+
+__global__ void __launch_bounds__(256) start_copy_kernel(const unsigned char *ws, uint16_t *start_out, int64_t *info) {
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int n = h->n;
+  const uint16_t *src = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  for (int p = threadIdx.x; p < n; p += blockDim.x) start_out[p] = src[p];
+  if (threadIdx.x == 0) {
+    info[0] = h->t_ref;
+    info[1] = h->start_n;
+    info[2] = h->start_t;
+    info[3] = h->allmet;
+  }
+}
+
+// One thread per row: Durstenfeld's in-place Fisher-Yates, drawing from Philox.
+__global__ void __launch_bounds__(256) shuffle_kernel(uint32_t key0, uint32_t key1, int n, int64_t row0, int64_t rows,
+                                                       uint16_t *perms) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= rows) return;
+  const uint32_t idx = (uint32_t)(row0 + t);
+  uint16_t *p = perms + t * n;
+  for (int u = 0; u < n; ++u) p[u] = (uint16_t)u;
+  u32x4 w{0, 0, 0, 0};
+  for (int k = n - 1; k >= 1; --k) {
+    if (k == n - 1 || (k & 3) == 3) w = philox4x32_10((uint32_t)k >> 2, idx, 1u, kTagShuffle, key0, key1);
+    const uint32_t word = (k & 3) == 0 ? w.x : (k & 3) == 1 ? w.y : (k & 3) == 2 ? w.z : w.w;
+    const uint32_t j = (uint32_t)(((uint64_t)word * (uint64_t)(k + 1)) >> 32);
+    const uint16_t a = p[k];
+    p[k] = p[j];
+    p[j] = a;
+  }
+}
+
+}  // namespace sa

@@ -1,0 +1,217 @@
+// C-ABI of the annealing library (declared in include/sloanneal.h): argument and queue
+// validation, int64 range pre-checks, workspace sizing and kernel launches on the caller's
+// stream.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/sloanneal.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_hip_msg;
+
+int hip_fail(hipError_t e) {
+  g_hip_msg = hipGetErrorString(e);
+  return SCHED_EHIP;
+}
+
+#define HIP_TRY(expr)                       \
+  do {                                      \
+    hipError_t _e = (expr);                 \
+    if (_e != hipSuccess) return hip_fail(_e); \
+  } while (0)
+
+struct HostQueue {
+  std::vector<uint16_t> in_len, out_len;
+  std::vector<uint8_t> kind;
+  std::vector<uint32_t> thr;
+};
+
+int check_model(const sched_model_t *m, int n) {
+  if (!m) return SCHED_EINVAL;
+  if (m->max_batch < 1 || m->max_batch > SCHED_MAX_BATCH) return SCHED_EINVAL;
+  if (m->policy != SCHED_STATIC && m->policy != SCHED_CONTINUOUS) return SCHED_EINVAL;
+  if (m->p0 < 0 || m->p1 < 0 || m->d0 < 0 || m->d1 < 0 || m->d2 < 0 || m->t_ref_us < 0) return SCHED_EINVAL;
+  if (m->swap_threshold > (1ull << 32)) return SCHED_EINVAL;
+  (void)n;
+  return SCHED_OK;
+}
+
+// Reads the queue back (one stream synchronisation) and validates every entry.
+int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h) {
+  if (!q || q->n < 1 || q->n > SCHED_MAX_N) return SCHED_EINVAL;
+  if (!q->in_len || !q->out_len || !q->kind || !q->thr_us) return SCHED_EINVAL;
+  const size_t n = (size_t)q->n;
+  h.in_len.resize(n);
+  h.out_len.resize(n);
+  h.kind.resize(n);
+  h.thr.resize(n);
+  HIP_TRY(hipMemcpyAsync(h.in_len.data(), q->in_len, n * 2, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipMemcpyAsync(h.out_len.data(), q->out_len, n * 2, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipMemcpyAsync(h.kind.data(), q->kind, n, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipMemcpyAsync(h.thr.data(), q->thr_us, n * 4, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  for (size_t r = 0; r < n; ++r) {
+    if (h.out_len[r] < 1 || h.kind[r] > 2) return SCHED_EINVAL;
+  }
+  return SCHED_OK;
+}
+
+// Worst-case clock: every request's prefill plus, per request, its decode iterations at
+// the largest possible step cost. The sum over requests and the Metropolis delta
+// (|dn| <= n times t_ref) must stay below 2^62.
+int range_check(const HostQueue &h, const sched_model_t *m, int n) {
+  const long double lim = std::ldexp(1.0L, 62);
+  long double max_lin = 0, max_lout = 0, sum_lout = 0, pre = 0;
+  for (int r = 0; r < n; ++r) {
+    max_lin = std::max<long double>(max_lin, h.in_len[r]);
+    max_lout = std::max<long double>(max_lout, h.out_len[r]);
+    sum_lout += h.out_len[r];
+    pre += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
+  }
+  const long double b = std::min(n, m->max_batch);
+  const long double step = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * b * (max_lin + max_lout);
+  const long double clock = pre + sum_lout * step;
+  const long double tsum = clock * n;
+  const long double tref = m->t_ref_us > 0 ? (long double)m->t_ref_us : tsum;
+  if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
+  return SCHED_OK;
+}
+
+sa::DevModel dev_model(const sched_model_t *m, int n) {
+  sa::DevModel d;
+  d.n = n;
+  d.B = m->max_batch;
+  d.policy = m->policy;
+  d.pad = 0;
+  d.p0 = (uint64_t)m->p0;
+  d.p1 = (uint64_t)m->p1;
+  d.d0 = (uint64_t)m->d0;
+  d.d1 = (uint64_t)m->d1;
+  d.d2 = (uint64_t)m->d2;
+  return d;
+}
+
+sa::QueuePtrs dev_queue(const sched_queue_t *q) {
+  return sa::QueuePtrs{q->in_len, q->out_len, q->kind, q->thr_us};
+}
+
+size_t eval_lds_bytes(int n) {
+  const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 + 64 * 16 + 32 * 4;
+  return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
+}
+
+size_t anneal_lds_bytes(int n) {
+  const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 * 2 + 64 * 16;
+  return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
+}
+
+}  // namespace
+
+extern "C" {
+
+int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms, int64_t k, int64_t *out,
+               int64_t *detail, hipStream_t stream) {
+  if (k < 0) return SCHED_EINVAL;
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  int rc = check_model(model, queue->n);
+  if (rc) return rc;
+  if (k > 0 && (!perms || !out)) return SCHED_EINVAL;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h))) return rc;
+  if ((rc = range_check(h, model, queue->n))) return rc;
+  if (k == 0) return SCHED_OK;
+  const int n = queue->n;
+  const sa::DevModel dm = dev_model(model, n);
+  const int64_t want = (k + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+  const int grid = (int)std::min<int64_t>(want, 256 * 32);
+  const size_t lds = eval_lds_bytes(n);
+  if (detail) {
+    sa::eval_kernel<true><<<grid, sa::kBlock, lds, stream>>>(dm, dev_queue(queue), perms, k, out, detail);
+  } else {
+    sa::eval_kernel<false><<<grid, sa::kBlock, lds, stream>>>(dm, dev_queue(queue), perms, k, out, nullptr);
+  }
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+size_t sched_ws_bytes(int32_t n, int32_t chains) {
+  if (n < 1 || n > SCHED_MAX_N || chains < 1) return 0;
+  return sa::ws_total(n, chains);
+}
+
+int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t chains, int32_t iters, double T0,
+                 double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
+    return SCHED_EINVAL;
+  int rc = check_model(model, queue->n);
+  if (rc) return rc;
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
+  if (ws_bytes < sched_ws_bytes(queue->n, chains)) return SCHED_ENOSPC;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h))) return rc;
+  if ((rc = range_check(h, model, queue->n))) return rc;
+  const int n = queue->n;
+  const sa::DevModel dm = dev_model(model, n);
+  unsigned char *w = static_cast<unsigned char *>(ws);
+  sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
+  HIP_TRY(hipGetLastError());
+  const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+  sa::anneal_kernel<<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
+      dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold, w);
+  HIP_TRY(hipGetLastError());
+  sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream) {
+  if (!ws || !perm_out || !key_out) return SCHED_EINVAL;
+  sa::best_copy_kernel<<<1, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), perm_out, key_out);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_chains(const void *ws, int64_t *per_chain, uint16_t *cur_perms, uint16_t *best_perms, hipStream_t stream) {
+  if (!ws || !per_chain) return SCHED_EINVAL;
+  sa::chains_copy_kernel<<<256, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), per_chain, cur_perms,
+                                                  best_perms);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_start_info(const void *ws, uint16_t *start_out, int64_t *info_out, hipStream_t stream) {
+  if (!ws || !start_out || !info_out) return SCHED_EINVAL;
+  sa::start_copy_kernel<<<1, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), start_out, info_out);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t *perms, hipStream_t stream) {
+  if (n < 1 || n > SCHED_MAX_N || row0 < 0 || k < 0 || row0 + k > (int64_t)UINT32_MAX + 1) return SCHED_EINVAL;
+  if (k == 0) return SCHED_OK;
+  if (!perms) return SCHED_EINVAL;
+  const int64_t grid = (k + 255) / 256;
+  sa::shuffle_kernel<<<(unsigned)grid, 256, 0, stream>>>((uint32_t)seed, (uint32_t)(seed >> 32), n, row0, k, perms);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+const char *sched_strerror(int code) {
+  switch (code) {
+    case SCHED_OK: return "ok";
+    case SCHED_EINVAL: return "invalid argument, size, model parameter or queue entry";
+    case SCHED_ENOSPC: return "workspace smaller than sched_ws_bytes(n, chains)";
+    case SCHED_ERANGE: return "queue and model could overflow the int64 clock or objective";
+    case SCHED_EHIP: return g_hip_msg.empty() ? "HIP runtime error" : g_hip_msg.c_str();
+    default: return "unknown error code";
+  }
+}
+
+}  // extern "C"

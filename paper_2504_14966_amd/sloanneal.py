@@ -1,0 +1,203 @@
+"""ctypes binding of libsloanneal.so (C-ABI in include/sloanneal.h).
+
+Argument marshalling only: every step of the scheduler runs in the library's HIP
+kernels. torch supplies device memory and the stream. There is no CPU fallback: if
+the library or a GPU is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsloanneal.so")
+
+SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, -4
+EXPORTS = ("sched_eval", "sched_ws_bytes", "sched_anneal", "sched_best", "sched_chains", "sched_start_info",
+           "sched_gen_perms", "sched_strerror")
+
+
+class SchedError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+class _Queue(C.Structure):
+    _fields_ = [("n", C.c_int32), ("in_len", C.c_void_p), ("out_len", C.c_void_p), ("kind", C.c_void_p),
+                ("thr_us", C.c_void_p)]
+
+
+class _Model(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("policy", C.c_int32), ("p0", C.c_int64), ("p1", C.c_int64),
+                ("d0", C.c_int64), ("d1", C.c_int64), ("d2", C.c_int64), ("t_ref_us", C.c_int64),
+                ("swap_threshold", C.c_uint64)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """dlopen the library and declare its signatures (no GPU needed)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libsloanneal.so is not built ({path}); run __graft_entry__.build()")
+    L = C.CDLL(path)
+    vp, i32, i64, u64, dbl, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_double, C.c_size_t
+    L.sched_eval.argtypes = [vp, vp, vp, i64, vp, vp, vp]
+    L.sched_eval.restype = C.c_int
+    L.sched_ws_bytes.argtypes = [i32, i32]
+    L.sched_ws_bytes.restype = sz
+    L.sched_anneal.argtypes = [vp, vp, i32, i32, dbl, dbl, u64, vp, sz, vp]
+    L.sched_anneal.restype = C.c_int
+    L.sched_best.argtypes = [vp, vp, vp, vp]
+    L.sched_best.restype = C.c_int
+    L.sched_chains.argtypes = [vp, vp, vp, vp, vp]
+    L.sched_chains.restype = C.c_int
+    L.sched_start_info.argtypes = [vp, vp, vp, vp]
+    L.sched_start_info.restype = C.c_int
+    L.sched_gen_perms.argtypes = [u64, i32, i64, i64, vp, vp]
+    L.sched_gen_perms.restype = C.c_int
+    L.sched_strerror.argtypes = [C.c_int]
+    L.sched_strerror.restype = C.c_char_p
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != SCHED_OK:
+        raise SchedError(rc, load_library().sched_strerror(rc).decode())
+
+
+def _stream(stream) -> C.c_void_p:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t: torch.Tensor | None):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("sloanneal takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("sloanneal takes contiguous tensors")
+    return C.c_void_p(t.data_ptr())
+
+
+@dataclass
+class DeviceQueue:
+    """A request queue resident in device memory (structure of arrays)."""
+    in_len: torch.Tensor   # int16 bits of uint16
+    out_len: torch.Tensor
+    kind: torch.Tensor     # uint8
+    thr_us: torch.Tensor   # int32 bits of uint32
+
+    @property
+    def n(self) -> int:
+        return int(self.in_len.shape[0])
+
+    @classmethod
+    def from_queue(cls, q, device="cuda") -> "DeviceQueue":
+        def dev(a, np_dt, t_dt):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np_dt).view(t_dt)).to(device)
+        return cls(dev(q.in_len, np.uint16, np.int16), dev(q.out_len, np.uint16, np.int16),
+                   dev(q.kind, np.uint8, np.uint8), dev(q.thr_us, np.uint32, np.int32))
+
+    def c(self) -> _Queue:
+        return _Queue(self.n, self.in_len.data_ptr(), self.out_len.data_ptr(), self.kind.data_ptr(),
+                      self.thr_us.data_ptr())
+
+
+def _model(m) -> _Model:
+    return _Model(int(m.max_batch), int(m.policy), int(m.p0), int(m.p1), int(m.d0), int(m.d1), int(m.d2),
+                  int(m.t_ref_us), int(m.swap_threshold))
+
+
+def perms_to_device(perms: np.ndarray, device="cuda") -> torch.Tensor:
+    """k x n orders as an int16 device tensor holding the uint16 bits."""
+    return torch.from_numpy(np.ascontiguousarray(perms, dtype=np.uint16).view(np.int16)).to(device)
+
+
+def sched_eval(dq: DeviceQueue, model, perms: torch.Tensor, out: torch.Tensor | None = None,
+               detail: bool | torch.Tensor = False, stream=None):
+    """(n_met, t_sum) per row of perms (k x n, int16/uint16 bits); optionally per-request (ttft, e2e)."""
+    L = load_library()
+    k = int(perms.shape[0]) if perms.dim() == 2 else 0
+    if perms.dim() != 2 or int(perms.shape[1]) != dq.n:
+        raise ValueError("perms must be k x n")
+    if out is None:
+        out = torch.empty((k, 2), dtype=torch.int64, device=perms.device)
+    det = None
+    if isinstance(detail, torch.Tensor):
+        det = detail
+    elif detail:
+        det = torch.zeros((k, dq.n, 2), dtype=torch.int64, device=perms.device)
+    q, m = dq.c(), _model(model)
+    _check(L.sched_eval(C.byref(q), C.byref(m), _ptr(perms), k, _ptr(out), _ptr(det), _stream(stream)))
+    return (out, det) if det is not None else out
+
+
+def ws_bytes(n: int, chains: int) -> int:
+    return int(load_library().sched_ws_bytes(int(n), int(chains)))
+
+
+def alloc_ws(n: int, chains: int, device="cuda") -> torch.Tensor:
+    nb = ws_bytes(n, chains)
+    if nb == 0:
+        raise ValueError("bad workspace size request")
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def sched_anneal(dq: DeviceQueue, model, chains: int, iters: int, T0: float, alpha: float, seed: int,
+                 ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    L = load_library()
+    if ws is None:
+        ws = alloc_ws(dq.n, chains)
+    q, m = dq.c(), _model(model)
+    _check(L.sched_anneal(C.byref(q), C.byref(m), int(chains), int(iters), float(T0), float(alpha),
+                          int(seed) & (2**64 - 1), _ptr(ws), int(ws.numel()), _stream(stream)))
+    return ws
+
+
+def sched_best(ws: torch.Tensor, n: int, stream=None):
+    perm = torch.empty(n, dtype=torch.int16, device=ws.device)
+    key = torch.empty(3, dtype=torch.int64, device=ws.device)
+    _check(load_library().sched_best(_ptr(ws), _ptr(perm), _ptr(key), _stream(stream)))
+    return perm, key
+
+
+def sched_chains(ws: torch.Tensor, n: int, chains: int, perms: bool = False, stream=None):
+    rec = torch.empty((chains, 8), dtype=torch.int64, device=ws.device)
+    cur = best = None
+    if perms:
+        cur = torch.empty((chains, n), dtype=torch.int16, device=ws.device)
+        best = torch.empty((chains, n), dtype=torch.int16, device=ws.device)
+    _check(load_library().sched_chains(_ptr(ws), _ptr(rec), _ptr(cur), _ptr(best), _stream(stream)))
+    return (rec, cur, best) if perms else rec
+
+
+def sched_start_info(ws: torch.Tensor, n: int, stream=None):
+    start = torch.empty(n, dtype=torch.int16, device=ws.device)
+    info = torch.empty(4, dtype=torch.int64, device=ws.device)
+    _check(load_library().sched_start_info(_ptr(ws), _ptr(start), _ptr(info), _stream(stream)))
+    return start, info
+
+
+def sched_gen_perms(seed: int, n: int, k: int, row0: int = 0, out: torch.Tensor | None = None, stream=None,
+                    device="cuda") -> torch.Tensor:
+    if out is None:
+        out = torch.empty((k, n), dtype=torch.int16, device=device)
+    _check(load_library().sched_gen_perms(int(seed) & (2**64 - 1), int(n), int(row0), int(k), _ptr(out),
+                                          _stream(stream)))
+    return out
+
+
+def as_u16(t: torch.Tensor) -> np.ndarray:
+    """Host numpy uint16 view of an int16 device tensor."""
+    return t.cpu().numpy().view(np.uint16)

@@ -1,0 +1,41 @@
+"""Helpers for the GPU parity tests: running the oracle over many chains in worker
+processes (spawned, so they never inherit the parent's GPU state)."""
+import multiprocessing as mp
+import os
+
+import numpy as np
+
+
+def _chain_job(args):
+    import oracle
+    q, m, chain, iters, T0, alpha, seed, info = args
+    r = oracle.anneal_chain(q, m, chain, iters, T0, alpha, seed, start_info=info)
+    return chain, r["rec"], r["cur"], r["best"]
+
+
+def _rows_job(args):
+    import oracle
+    q, m, perms = args
+    return oracle.eval_rows(q, m, perms)
+
+
+def workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def oracle_chains(q, m, chains, iters, T0, alpha, seed, info):
+    jobs = [(q, m, int(c), iters, T0, alpha, seed, info) for c in chains]
+    with mp.get_context("spawn").Pool(min(workers(), len(jobs))) as pool:
+        out = pool.map(_chain_job, jobs)
+    return {c: (rec, cur, best) for c, rec, cur, best in out}
+
+
+def oracle_rows(q, m, perms: np.ndarray) -> np.ndarray:
+    parts = np.array_split(perms, max(1, min(workers(), len(perms) // 256 + 1)))
+    with mp.get_context("spawn").Pool(len(parts)) as pool:
+        out = pool.map(_rows_job, [(q, m, p) for p in parts])
+    return np.concatenate(out)
