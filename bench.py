@@ -1,0 +1,201 @@
+#!/usr/bin/env python3
+"""Benchmark of the SLO-aware annealing hot path on one MI355X.
+
+One step = one pass of the whole hot path over the burst workload (1024 requests, max
+batch 64, static admission, 4096 chains x 5000 proposals, T0 2.0, alpha 0.9995):
+sched_anneal (start order, every chain, cross-chain reduction) followed by sched_best.
+Inputs are resident in device memory before timing starts.
+
+Prints ONE JSON line: SA chain-iterations/s (value), plus schedule evaluations/s of the
+evaluation workload (2^20 orders of 128 requests), the rates of the other annealing
+workloads, the roofline of the dominant kernel and the CPU oracle baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+PEAK_LANE_OPS = 256 * 4 * 16 * 2.4e9  # CUs x SIMDs x lanes x clock: int32 VALU lane-ops/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algo_lane_ops_per_iter(W) -> float:
+    """Algorithmic int32 lane-ops of one chain-iteration (one proposal scored).
+
+    The anneal kernel scores every proposal with a full timeline replay of the candidate
+    order. One request evaluated by the static closed form costs 3 lane-ops per batch
+    member it is paired with (minimum of output lengths, multiply-add of the context term,
+    multiply-add into the accumulator) plus 10 for its gather, prefill share, start offset,
+    SLO test and latency sum. Continuous admission costs, per request, one event of about
+    40 lane-ops over the slots it shares. Scalar work (Philox, acceptance) is not counted.
+    """
+    n, B = W.queue.n, W.model.max_batch
+    if W.model.policy == 0:
+        return float(n * (3 * min(B, n) + 10))
+    return float(n * 40)
+
+
+def time_anneal(sl, W, steps, warmup, torch):
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    ws = sl.alloc_ws(W.queue.n, W.chains)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        sl.sched_anneal(dq, W.model, W.chains, W.iters, W.T0, W.alpha, W.seed, ws=ws)
+        sl.sched_best(ws, W.queue.n)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s in range(steps):
+        ev[s][0].record(stream)
+        sl.sched_anneal(dq, W.model, W.chains, W.iters, W.T0, W.alpha, W.seed, ws=ws)
+        ev[s][1].record(stream)
+        perm, key = sl.sched_best(ws, W.queue.n)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    return wall, kern_ms, key.cpu().tolist()
+
+
+def time_eval(sl, W, reps, torch):
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    perms = sl.sched_gen_perms(W.perm_seed, W.queue.n, W.eval_rows)
+    out = torch.empty((W.eval_rows, 2), dtype=torch.int64, device="cuda")
+    sl.sched_eval(dq, W.model, perms, out=out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    a.record(stream)
+    for _ in range(reps):
+        sl.sched_eval(dq, W.model, perms, out=out)
+    b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall / reps, a.elapsed_time(b) / reps
+
+
+def _oracle_job(args):
+    import oracle
+    wl, chains, iters = args
+    from paper_2504_14966_amd.workloads import workload
+    W = workload(wl)
+    info = oracle.start(W.queue, W.model)
+    t = time.perf_counter()
+    for c in chains:
+        oracle.anneal_chain(W.queue, W.model, c, iters, W.T0, W.alpha, W.seed, start_info=info)
+    return time.perf_counter() - t
+
+
+def cpu_baseline(wl: int, chains_per_core: int, iters: int):
+    import multiprocessing as mp
+    import oracle
+    oracle.build(force=False)
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    cores = max(1, min(cores, 16))
+    jobs = [(wl, list(range(k * chains_per_core, (k + 1) * chains_per_core)), iters) for k in range(cores)]
+    t = time.perf_counter()
+    with mp.get_context("spawn").Pool(cores) as pool:
+        per = pool.map(_oracle_job, jobs)
+    wall = time.perf_counter() - t
+    total = cores * chains_per_core * iters
+    return dict(value=total / wall, unit="chain-iters/s", cores=cores, kind="oracle",
+                sample=f"workload {wl}: chains 0..{cores * chains_per_core - 1}, {iters} iterations each, "
+                       f"{cores} worker processes, {wall:.1f} s wall ({total / sum(per):.0f} chain-iters/s per core)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4])
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extras", action="store_true", help="skip the other workloads")
+    ap.add_argument("--cpu-chains-per-core", type=int, default=2)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the chains are independent, so a multi-GPU run would split "
+              "them and reduce one 24-byte key; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2504_14966_amd.sloanneal as sl
+    from paper_2504_14966_amd.workloads import workload
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    sl.load_library()
+
+    W = workload(args.workload)
+    log(f"[bench] workload {W.name}: {W.chains} chains x {W.iters} iters, warmup {args.warmup}, steps {args.steps}")
+    wall, kern_ms, key = time_anneal(sl, W, args.steps, args.warmup, torch)
+    ms_per_step = wall * 1000.0 / args.steps
+    chain_iters = W.chains * W.iters
+    value = chain_iters * args.steps / wall
+    k_ms = float(np.mean(kern_ms))
+    ops = algo_lane_ops_per_iter(W) * chain_iters
+    achieved = ops / (k_ms * 1e-3)
+    log(f"[bench] {value:.4g} chain-iters/s, anneal call {k_ms:.2f} ms, best key {key}")
+
+    extras = {}
+    if not args.no_extras:
+        W5 = workload(5)
+        wall5, k5 = time_eval(sl, W5, 5, torch)
+        extras["eval_workload"] = dict(workload=W5.name, rows=W5.eval_rows, evals_per_s=W5.eval_rows / wall5,
+                                       kernel_ms=k5)
+        log(f"[bench] eval {W5.eval_rows / wall5:.4g} evals/s ({k5:.2f} ms per 2^20 rows)")
+        for wl in (2, 3):
+            if wl == args.workload:
+                continue
+            Wx = workload(wl)
+            wx, kx, keyx = time_anneal(sl, Wx, 1, 1, torch)
+            extras[f"anneal_{Wx.name}"] = dict(chain_iters_per_s=Wx.chains * Wx.iters / wx, ms=kx[0], best=keyx)
+            log(f"[bench] {Wx.name}: {Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({kx[0]:.1f} ms)")
+
+    cpu = None
+    if not args.no_cpu:
+        log("[bench] CPU oracle baseline ...")
+        cpu = cpu_baseline(args.workload, args.cpu_chains_per_core, W.iters)
+        log(f"[bench] oracle {cpu['value']:.4g} chain-iters/s on {cpu['cores']} cores")
+
+    line = {
+        "metric": "SA chain-iterations/s",
+        "value": value,
+        "unit": "chain-iters/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": W.name, "requests": W.queue.n, "max_batch": W.model.max_batch,
+                   "policy": "static" if W.model.policy == 0 else "continuous", "chains": W.chains,
+                   "iters": W.iters, "T0": W.T0, "alpha": W.alpha, "parallelism": "chains"},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "kernel": "anneal_kernel", "kernel_ms": k_ms,
+                     "algo_lane_ops_per_chain_iter": algo_lane_ops_per_iter(W)},
+        "cpu_baseline": cpu,
+        "extras": extras,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
