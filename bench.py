@@ -125,7 +125,9 @@ def main():
     ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the other workloads")
-    ap.add_argument("--cpu-chains-per-core", type=int, default=2)
+    ap.add_argument("--cpu-chains-per-core", type=int, default=8)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run one 256 MiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the chains are independent, so a multi-GPU run would split "
@@ -138,6 +140,14 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     sl.load_library()
+
+    if args.copy_calibration:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     W = workload(args.workload)
     log(f"[bench] workload {W.name}: {W.chains} chains x {W.iters} iters, warmup {args.warmup}, steps {args.steps}")

@@ -46,6 +46,7 @@ enum { SCHED_STATIC = 0, SCHED_CONTINUOUS = 1 };
 
 #define SCHED_MAX_N 1024
 #define SCHED_MAX_BATCH 64
+#define SCHED_THR_MAX 0xFFFFFFFEu /* largest accepted SLO threshold (us) */
 
 /* Request queue, structure of arrays, n entries, DEVICE pointers (paper: newly arrived
  * jobs with input length, predicted output length, SLO kind and threshold). */
@@ -54,7 +55,7 @@ typedef struct {
   const uint16_t *in_len;   /* input (prompt) tokens l_i */
   const uint16_t *out_len;  /* predicted output tokens l_o, >= 1 */
   const uint8_t *kind;      /* SCHED_TTFT / SCHED_TPOT / SCHED_E2E */
-  const uint32_t *thr_us;   /* SLO threshold in microseconds (per token for TPOT) */
+  const uint32_t *thr_us;   /* SLO threshold in microseconds (per token for TPOT), <= SCHED_THR_MAX */
 } sched_queue_t;
 
 /* Latency model in integer microseconds (Latency Predictor section, integer form) and

@@ -1,0 +1,610 @@
+// Annealing chains under static admission with delta re-simulation (gfx950, wave64).
+//
+// Why a delta works. Under static admission the batch of position p is p / B and a
+// batch's duration does not depend on when it starts (waiting-time equation of the
+// Problem Formulation). A swap of positions in batches a < c, or an insert that moves
+// one request from batch a to batch c (or back), changes the membership of batches
+// a..c by exactly one request each: one request leaves (o) and one joins (e). Every
+// other batch keeps its members and only its start time shifts by the change in
+// duration of the changed batches before it. A move inside one batch changes nothing.
+//
+// State per chain (LDS): the order (u16 per position), every request's finish offset F
+// within its batch including the prefill (u32, indexed by request id), and one record
+// per batch: start S, sum of F, prefill P, duration D = max F, SLO-met count at S, and
+// two bounds on S inside which no member's SLO flag changes (see Slack below).
+//
+// For a changed batch with prefill P -> P' = P + pf(e) - pf(o), a staying member m gets
+//   F'_m = F_m + (P' - P) + (w(e, m) - w(o, m)) / 2,
+// and the newcomer F'_e = P' + L_e * d0 + sum over the new members j of w(j, e) / 2, where
+//   w(j, m) = mu * (e_j + d2 * mu),  mu = min(L_j, L_m),  e_j = 2 (d1 + d2 l_j) + d2,
+// is twice the per-token decode cost that member j adds to m's decode iterations
+// (d1 * mu + d2 * (l_j mu + mu (mu + 1) / 2)). Both factors stay below 2^24, so each w is
+// one 24-bit multiply-add and one 24-bit multiply.
+//
+// The candidate objective is n + (met-count changes) and t + (size * start shift summed
+// over later batches) + (change of sum F of the changed batches). A batch whose members
+// are unchanged and whose new start stays inside its two bounds keeps its met count: it
+// costs one lane of a batch-parallel check. Only batches that cross a bound are recounted
+// member by member.
+//
+// Candidate F values are written speculatively (acceptance is the common case); a
+// rejected proposal restores them with the reverse update (o and e exchanged). Candidate
+// batch records go to a second array that is copied on accept.
+//
+// Lane layout: a batch occupies Bp = 2^LG lanes (B <= Bp), G = 64 / Bp batches per row.
+// Widths: F, P, D, w and slacks are u32 (the host checks every finish offset and 2w stay
+// below 2^32 and the multiply-add operands below 2^24); starts, sums, objective are u64.
+#pragma once
+#include "device_common.h"
+#include "device_replay.h"
+#include "device_rng.h"
+
+namespace sa {
+
+struct alignas(16) BatchRec {
+  uint64_t S;    // start time
+  uint64_t SF;   // sum of member finish offsets
+  uint32_t P;    // prefill of the batch
+  uint32_t D;    // duration = max finish offset
+  uint32_t cnt;  // members meeting their SLO when the batch starts at S
+  uint32_t A;    // every member keeps its SLO flag while Bv <= start <= A
+  uint32_t Bv;
+  uint32_t pad[3];
+};
+
+struct StaticParams {
+  uint32_t d0, d2;
+  uint32_t bmagic;  // floor(2^32 / B) + 1: p / B == (p * bmagic) >> 32 for p < 2^16
+  uint32_t pad;
+};
+
+__device__ __forceinline__ uint32_t div_b(uint32_t p, uint32_t bmagic) {
+  return (uint32_t)(((uint64_t)p * bmagic) >> 32);
+}
+
+// Request record in LDS: x = l_in | l_out << 16, y = threshold, z = kind | e << 2, w = prefill.
+struct Req {
+  uint32_t L, thr, kind, e, pf;
+};
+__device__ __forceinline__ Req load_req(const uint4 *req, int r) {
+  const uint4 v = req[r];
+  return Req{v.x >> 16, v.y, v.z & 3u, v.z >> 2, v.w};
+}
+
+// twice the decode cost member j (output L_j, e_j) adds to a member with output Lm
+__device__ __forceinline__ uint32_t w2(uint32_t Lj, uint32_t ej, uint32_t Lm, uint32_t d2) {
+  const uint32_t mu = min(Lj, Lm);
+  return __umul24(mu, __umul24(d2, mu) + ej);
+}
+
+// SLO flag of a member as a function of its batch start S: TPOT does not depend on S;
+// TTFT (offset P) and end-to-end (offset F) are met iff S <= thr - offset =: slack.
+struct Slack {
+  bool always, never;
+  uint32_t s;
+};
+__device__ __forceinline__ Slack slack_of(uint32_t kind, uint32_t thr, uint32_t L, uint32_t P, uint32_t F) {
+  if (kind == 1) {
+    const bool ok = (uint64_t)(F - P) <= (uint64_t)thr * L;
+    return Slack{ok, !ok, 0u};
+  }
+  const uint32_t off = kind == 0 ? P : F;
+  if (off > thr) return Slack{false, true, 0u};
+  return Slack{false, false, thr - off};
+}
+__device__ __forceinline__ bool slack_met(const Slack &x, uint64_t S) { return x.always || (!x.never && S <= x.s); }
+
+// Cross-lane primitives on gfx950 DPP: quad_perm [1,0,3,2] and [2,3,0,1] pair lanes at
+// distance 1 and 2, row_half_mirror pairs the two quads of each half-row and row_mirror
+// the two half-rows, so four DPP steps all-reduce a 16-lane row; whole-wave results come
+// from v_readlane of the four row leaders into scalar registers.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
+
+__device__ __forceinline__ uint32_t readlane(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+
+struct OpAdd {
+  __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return a + b; }
+};
+struct OpMax {
+  __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return max(a, b); }
+};
+struct OpMin {
+  __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return min(a, b); }
+};
+
+template <int LG>
+struct Seg {
+  static constexpr int Bp = 1 << LG;
+  // all-reduce over each segment of Bp lanes; every lane receives its segment's result.
+  // Lanes outside any batch must hold the identity of Op.
+  template <class Op>
+  __device__ static __forceinline__ uint32_t all(uint32_t v, int lane) {
+    if constexpr (LG >= 1) v = Op::f(v, dpp<kQuadXor1>(v));
+    if constexpr (LG >= 2) v = Op::f(v, dpp<kQuadXor2>(v));
+    if constexpr (LG >= 3) v = Op::f(v, dpp<kRowHalfMirror>(v));
+    if constexpr (LG >= 4) v = Op::f(v, dpp<kRowMirror>(v));
+    if constexpr (LG == 5) {
+      const uint32_t s01 = Op::f(readlane(v, 0), readlane(v, 16));
+      const uint32_t s23 = Op::f(readlane(v, 32), readlane(v, 48));
+      v = lane < 32 ? s01 : s23;
+    }
+    if constexpr (LG == 6) {
+      v = Op::f(Op::f(readlane(v, 0), readlane(v, 16)), Op::f(readlane(v, 32), readlane(v, 48)));
+    }
+    return v;
+  }
+  // exact sum of 32-bit values as two 16-bit-half sums (each below 2^22)
+  __device__ static __forceinline__ uint64_t sum_wide(uint32_t v, int lane) {
+    const uint32_t lo = all<OpAdd>(v & 0xFFFFu, lane), hi = all<OpAdd>(v >> 16, lane);
+    return (uint64_t)lo + ((uint64_t)hi << 16);
+  }
+  // segment-uniform v: exclusive prefix over the segments of the row, and the row total
+  __device__ static __forceinline__ void scan(int64_t v, int lane, int64_t &excl, int64_t &total) {
+    if constexpr (LG == 6) {
+      excl = 0;
+      total = v;
+    } else if constexpr (LG >= 4) {
+      int64_t s[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t lo = readlane((uint32_t)(uint64_t)v, u * 16), hi = readlane((uint32_t)((uint64_t)v >> 32), u * 16);
+        s[u] = (int64_t)(((uint64_t)hi << 32) | lo);
+      }
+      if constexpr (LG == 5) {
+        total = s[0] + s[2];
+        excl = lane < 32 ? 0 : s[0];
+      } else {
+        total = s[0] + s[1] + s[2] + s[3];
+        const int g = lane >> 4;
+        excl = g == 0 ? 0 : (g == 1 ? s[0] : (g == 2 ? s[0] + s[1] : s[0] + s[1] + s[2]));
+      }
+    } else {
+      int64_t x = (lane & (Bp - 1)) == 0 ? v : 0;
+#pragma unroll
+      for (int o = Bp; o < kWave; o <<= 1) {
+        const int64_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+      }
+      excl = __shfl(x, lane & ~(Bp - 1)) - v;
+      total = __shfl(x, kWave - Bp);
+    }
+  }
+  __device__ static __forceinline__ int count(bool p, int seg) {
+    uint64_t m = __ballot(p);
+    if (Bp < kWave) m = (m >> (seg << LG)) & ((1ull << (Bp & 63)) - 1ull);
+    return __popcll(m);
+  }
+  // sum over lanes of a value that only segment leaders (lanes 0, Bp, 2Bp, ...) hold
+  __device__ static __forceinline__ int64_t leader_sum(int64_t v) {
+    if constexpr (LG >= 4) {
+      int64_t s = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (LG == 6 && u > 0) break;
+        if (LG == 5 && (u & 1)) continue;
+        const uint32_t lo = readlane((uint32_t)(uint64_t)v, u * 16), hi = readlane((uint32_t)((uint64_t)v >> 32), u * 16);
+        s += (int64_t)(((uint64_t)hi << 32) | lo);
+      }
+      return s;
+    } else {
+      return (int64_t)wave_sum_u64((uint64_t)v);
+    }
+  }
+};
+
+// A proposal: move type (1 swap, 2 insert), positions, changed batch range [a, c].
+struct Move {
+  int type, i, j, a, c;
+  __device__ __forceinline__ bool changes(int k) const { return k >= a && k <= c && (type == 2 || k == a || k == c); }
+};
+
+template <int LG>
+struct StaticChain {
+  const uint4 *req;
+  uint16_t *perm;
+  uint32_t *F;
+  BatchRec *cur;
+  BatchRec *cand;
+  StaticParams sp;
+  int N, B, M, R;  // requests, batch size, batches, rows
+  int lane, seg, mm;
+  static constexpr int Bp = 1 << LG;
+  static constexpr int G = kWave >> LG;
+
+  __device__ __forceinline__ int batch_size(int k) const { return min(B, N - k * B); }
+  // requests in batches [k0, k1)
+  __device__ __forceinline__ int64_t requests_in(int k0, int k1) const {
+    return k1 <= k0 ? 0 : (int64_t)min(N, k1 * B) - (int64_t)k0 * B;
+  }
+
+  // Member-level pass over one row. Batches below `a` are left alone; changed batches get
+  // candidate F (written speculatively); every other live batch is recounted at its start
+  // moved by base_shift plus the duration changes of the changed batches before it in the
+  // row. Writes candidate records and adds the met-count change of the row's batches to
+  // dn_l, and (with add_dt) their latency change to dt_l (segment leaders). Returns the
+  // row's total duration change.
+  __device__ int64_t row_pass(int row, const Move &mv, int64_t base_shift, bool add_dt, int64_t &dn_l,
+                              int64_t &dt_l) {
+    const int k = row * G + seg;
+    const int q = k * B + mm;
+    const bool valid = mm < B && q < N;
+    const bool seg_live = k < M && k >= mv.a;                // uniform per segment
+    const bool seg_changed = seg_live && mv.changes(k);
+    const int k0 = row * G, k1 = min(row * G + G - 1, M - 1);
+    const bool row_changed = mv.type == 2 ? (mv.a <= k1 && mv.c >= k0)
+                                          : ((mv.a >= k0 && mv.a <= k1) || (mv.c >= k0 && mv.c <= k1));
+    BatchRec br{0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
+    if (seg_live) br = cur[k];
+    int r = 0;
+    if (valid) r = perm[q];
+    Req rq{0, 0, 0, 0, 0};
+    uint32_t Fn = 0, Pn = br.P, Dn = br.D;
+    uint64_t SFn = br.SF;
+    if (row_changed) {
+      int o = 0, e = 0;
+      if (seg_changed) out_in(k, mv, o, e);
+      const Req ro = load_req(req, o), re = load_req(req, e);
+      if (seg_changed) Pn = br.P + re.pf - ro.pf;
+      const bool is_out = seg_changed && valid && r == o;
+      const int rn = is_out ? e : r;
+      if (valid) rq = load_req(req, rn);
+      // newcomer: prefill, its own decode steps and what every new member adds to them
+      const uint32_t te = (seg_changed && valid) ? w2(rq.L, rq.e, re.L, sp.d2) : 0u;
+      const uint32_t Fe = Pn + re.L * sp.d0 + (Seg<LG>::template all<OpAdd>(te, lane) >> 1);
+      if (valid) {
+        if (!seg_changed) {
+          Fn = F[r];
+        } else if (is_out) {
+          Fn = Fe;
+        } else {
+          const int32_t dw = (int32_t)(w2(re.L, re.e, rq.L, sp.d2) - w2(ro.L, ro.e, rq.L, sp.d2));
+          Fn = F[r] + (Pn - br.P) + (uint32_t)(dw >> 1);
+        }
+        if (seg_changed) F[rn] = Fn;
+      }
+      const uint32_t Dm = Seg<LG>::template all<OpMax>(Fn, lane);
+      const uint64_t SFm = Seg<LG>::sum_wide(Fn, lane);
+      if (seg_changed) {
+        Dn = Dm;
+        SFn = SFm;
+      }
+    } else if (valid) {
+      rq = load_req(req, r);
+      Fn = F[r];
+    }
+    const int64_t dlt = seg_changed ? (int64_t)Dn - (int64_t)br.D : 0;
+    int64_t excl, total;
+    Seg<LG>::scan(dlt, lane, excl, total);
+    const int64_t shift = base_shift + excl;
+    const uint64_t Sn = br.S + (uint64_t)shift;
+    const bool in_range = valid && seg_live;
+    const Slack x = slack_of(rq.kind, rq.thr, rq.L, Pn, Fn);
+    const bool met = in_range && slack_met(x, Sn);
+    const int cnt = Seg<LG>::count(met, seg);
+    const uint32_t A = Seg<LG>::template all<OpMin>((in_range && met && !x.always) ? x.s : 0xFFFFFFFFu, lane);
+    const uint32_t Bv = Seg<LG>::template all<OpMax>((in_range && !met && !x.never) ? x.s + 1u : 0u, lane);
+    if (mm == 0 && seg_live) {
+      dn_l += (int64_t)cnt - (int64_t)br.cnt;
+      if (add_dt) dt_l += (int64_t)batch_size(k) * shift + (int64_t)(SFn - br.SF);
+      cand[k] = BatchRec{Sn, SFn, Pn, Dn, (uint32_t)cnt, A, Bv, {0, 0, 0}};
+    }
+    return total;
+  }
+
+  // Full evaluation of the current order: F of every request and every batch record.
+  __device__ Score init() {
+    uint64_t carry = 0, tl = 0;
+    int64_t nmet = 0;
+    for (int row = 0; row < R; ++row) {
+      const int k = row * G + seg;
+      const int q = k * B + mm;
+      const bool valid = mm < B && q < N;
+      Req rq{0, 0, 0, 0, 0};
+      int r = 0;
+      if (valid) {
+        r = perm[q];
+        rq = load_req(req, r);
+      }
+      // pairwise closed form over the members of this lane's batch
+      uint32_t P = 0, acc = 0;
+      for (int jj = 0; jj < B; ++jj) {
+        const int qj = k * B + jj;
+        if (k < M && qj < N) {
+          const Req o = load_req(req, perm[qj]);
+          P += o.pf;
+          acc += w2(o.L, o.e, rq.L, sp.d2);
+        }
+      }
+      const uint32_t Fv = valid ? P + rq.L * sp.d0 + (acc >> 1) : 0u;
+      if (valid) F[r] = Fv;
+      const uint32_t D = Seg<LG>::template all<OpMax>(Fv, lane);
+      const uint64_t SF = Seg<LG>::sum_wide(Fv, lane);
+      int64_t excl, total;
+      Seg<LG>::scan(k < M ? (int64_t)D : 0, lane, excl, total);
+      const uint64_t S = carry + (uint64_t)excl;
+      const Slack x = slack_of(rq.kind, rq.thr, rq.L, P, Fv);
+      const bool met = valid && slack_met(x, S);
+      const int cnt = Seg<LG>::count(met, seg);
+      const uint32_t A = Seg<LG>::template all<OpMin>((valid && met && !x.always) ? x.s : 0xFFFFFFFFu, lane);
+      const uint32_t Bv = Seg<LG>::template all<OpMax>((valid && !met && !x.never) ? x.s + 1u : 0u, lane);
+      if (mm == 0 && k < M) {
+        cur[k] = BatchRec{S, SF, P, D, (uint32_t)cnt, A, Bv, {0, 0, 0}};
+        tl += (uint64_t)batch_size(k) * S + SF;
+        nmet += cnt;
+      }
+      carry += (uint64_t)total;
+    }
+    wave_sync_lds();
+    return Score{(int64_t)wave_sum_u64((uint64_t)nmet), wave_sum_u64(tl)};
+  }
+
+  // Leaving (o) and joining (e) request of changed batch k.
+  __device__ __forceinline__ void out_in(int k, const Move &mv, int &o, int &e) const {
+    int opos, epos;
+    if (mv.type == 1) {  // swap
+      const int lo = min(mv.i, mv.j), hi = max(mv.i, mv.j);
+      opos = (k == mv.a) ? lo : hi;
+      epos = (k == mv.a) ? hi : lo;
+    } else if (mv.i < mv.j) {  // insert moving right: each batch passes its first member left
+      opos = (k == mv.a) ? mv.i : k * B;
+      epos = (k == mv.c) ? mv.i : (k + 1) * B;
+    } else {  // insert moving left: each batch passes its last member right
+      opos = (k == mv.c) ? mv.i : (k + 1) * B - 1;
+      epos = (k == mv.a) ? mv.i : k * B - 1;
+    }
+    o = perm[opos];
+    e = perm[epos];
+  }
+
+  // Batch-parallel pass over batches [k0, k1), all with unchanged members and starts
+  // moved by `shift`: candidate records, their latency change, and a bitmask of the rows
+  // holding a batch whose new start leaves its bounds (those need a member recount).
+  __device__ uint64_t shift_range(int k0, int k1, int64_t shift, int64_t &dt_l) {
+    uint64_t rows = 0;
+    for (int kk0 = k0; kk0 < k1; kk0 += kWave) {
+      const int kk = kk0 + lane;
+      bool flip = false;
+      if (kk < k1) {
+        BatchRec b = cur[kk];
+        b.S += (uint64_t)shift;
+        flip = b.S > (uint64_t)b.A || b.S < (uint64_t)b.Bv;
+        cand[kk] = b;
+      }
+      uint64_t f = __ballot(flip);
+      while (f) {
+        const int l = __builtin_ctzll(f);
+        f &= f - 1;
+        rows |= 1ull << ((kk0 + l) / G);
+      }
+    }
+    if (lane == 0) dt_l += shift * requests_in(k0, k1);
+    return rows;
+  }
+
+  // Candidate objective change of a move with a < c. Writes candidate F (speculative) and
+  // candidate records for batches a..klast.
+  __device__ void propose(const Move &mv, int64_t &dn, int64_t &dt, int &klast) {
+    int64_t dn_l = 0, dt_l = 0;
+    const int row_a = mv.a >> (6 - LG), row_c = mv.c >> (6 - LG);
+    // rows holding changed batches: for a swap the rows of a and c, for an insert a..c
+    int64_t carry = row_pass(row_a, mv, 0, true, dn_l, dt_l);
+    const int64_t shift_mid = carry;  // start change of the batches between a and c (swap)
+    uint64_t flagged = 0;
+    if (mv.type == 2) {
+      for (int row = row_a + 1; row <= row_c; ++row) carry += row_pass(row, mv, carry, true, dn_l, dt_l);
+    } else if (row_c > row_a) {
+      // the batches strictly between the two rows: their records are copied on accept, so
+      // they are written even when the shift is 0 (no batch then leaves its bounds)
+      if (row_c > row_a + 1) flagged |= shift_range((row_a + 1) * G, row_c * G, shift_mid, dt_l);
+      carry += row_pass(row_c, mv, carry, true, dn_l, dt_l);
+    }
+    const int kb = (row_c + 1) * G;  // first batch after the rows of a..c
+    if (carry != 0 && kb < M) {
+      flagged |= shift_range(kb, M, carry, dt_l);
+      klast = M - 1;
+    } else {
+      klast = min(kb - 1, M - 1);
+    }
+    // member-level recount of the rows holding a batch that left its bounds; their
+    // latency change was already added by shift_range (sums of F are unchanged there)
+    while (flagged) {
+      const int row = __builtin_ctzll(flagged);
+      flagged &= flagged - 1;
+      row_pass(row, mv, row * G >= kb ? carry : shift_mid, false, dn_l, dt_l);
+    }
+    dn = Seg<LG>::leader_sum(dn_l);
+    dt = Seg<LG>::leader_sum(dt_l);
+  }
+
+  // Restore F of the changed batches after a rejected proposal (reverse update).
+  __device__ void undo(const Move &mv) {
+    const int row_a = mv.a >> (6 - LG), row_c = mv.c >> (6 - LG);
+    for (int row = row_a; row <= row_c; ++row) {
+      if (mv.type == 1 && row != row_a && row != row_c) continue;
+      const int k = row * G + seg;
+      const int q = k * B + mm;
+      const bool valid = mm < B && q < N;
+      const bool seg_changed = k < M && mv.changes(k);
+      int o = 0, e = 0;
+      uint32_t Pold = 0;
+      if (seg_changed) {
+        out_in(k, mv, o, e);
+        Pold = cur[k].P;
+      }
+      const Req ro = load_req(req, o), re = load_req(req, e);
+      const uint32_t Pn = Pold + re.pf - ro.pf;
+      int r = 0;
+      Req rq{0, 0, 0, 0, 0};
+      if (valid) {
+        r = perm[q];
+        rq = load_req(req, r);
+      }
+      const uint32_t to = (seg_changed && valid) ? w2(rq.L, rq.e, ro.L, sp.d2) : 0u;
+      const uint32_t Fo = Pold + ro.L * sp.d0 + (Seg<LG>::template all<OpAdd>(to, lane) >> 1);
+      if (seg_changed && valid) {
+        if (r == o) {
+          F[o] = Fo;
+        } else {
+          const int32_t dw = (int32_t)(w2(ro.L, ro.e, rq.L, sp.d2) - w2(re.L, re.e, rq.L, sp.d2));
+          F[r] = F[r] + (Pold - Pn) + (uint32_t)(dw >> 1);
+        }
+      }
+    }
+  }
+
+  // Apply an accepted move to the order held in LDS.
+  __device__ void apply_move(int type, int i, int j) {
+    if (type == 1) {
+      if (lane == 0) {
+        const uint16_t x = perm[i];
+        perm[i] = perm[j];
+        perm[j] = x;
+      }
+    } else {
+      const uint16_t x = perm[i];
+      wave_sync_lds();
+      if (i < j) {
+        for (int p0 = i; p0 < j; p0 += kWave) {
+          const int p = p0 + lane;
+          uint16_t v = 0;
+          if (p < j) v = perm[p + 1];
+          wave_sync_lds();
+          if (p < j) perm[p] = v;
+          wave_sync_lds();
+        }
+      } else {
+        for (int p0 = i; p0 > j; p0 -= kWave) {
+          const int p = p0 - lane;
+          uint16_t v = 0;
+          if (p > j) v = perm[p - 1];
+          wave_sync_lds();
+          if (p > j) perm[p] = v;
+          wave_sync_lds();
+        }
+      }
+      if (lane == 0) perm[j] = x;
+    }
+    wave_sync_lds();
+  }
+};
+
+// One wave per chain; blockDim / 64 chains per workgroup.
+template <int LG>
+__global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
+                                                              int iters, double T0, double alpha, uint32_t key0,
+                                                              uint32_t key1, uint64_t swap_thr, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n, B = m.B;
+  const int M = (n + B - 1) / B;
+  constexpr int G = kWave >> LG;
+  const int R = (M + G - 1) / G;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
+  const size_t f_b = ((size_t)n * 4 + 15) & ~size_t(15);
+  const size_t rec_b = (size_t)M * sizeof(BatchRec);
+  const size_t per_wave = perm_b + f_b + 2 * rec_b;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (size_t)n * 16 + (size_t)wave * per_wave;
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r] | (e << 2), pf);
+  }
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  StaticChain<LG> st{req,
+                     reinterpret_cast<uint16_t *>(wb),
+                     reinterpret_cast<uint32_t *>(wb + perm_b),
+                     reinterpret_cast<BatchRec *>(wb + perm_b + f_b),
+                     reinterpret_cast<BatchRec *>(wb + perm_b + f_b + rec_b),
+                     sp, n, B, M, R, lane, lane >> LG, lane & ((1 << LG) - 1)};
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    st.perm[p] = v;
+    gbest[p] = v;
+  }
+  wave_sync_lds();
+  const Score s0 = st.init();
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  double T = T0;
+  for (int k = 0; k < iters; ++k) {
+    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
+    int i, j;
+    pick_positions(n, w.y, w.z, i, j);
+    Move mv;
+    mv.type = (uint64_t)w.x < swap_thr ? 1 : 2;
+    mv.i = i;
+    mv.j = j;
+    mv.a = (int)div_b((uint32_t)min(i, j), sp.bmagic);
+    mv.c = (int)div_b((uint32_t)max(i, j), sp.bmagic);
+    bool acc;
+    if (mv.a == mv.c) {
+      // same batch: every batch keeps its members, the objective is unchanged
+      acc = true;
+      st.apply_move(mv.type, i, j);
+    } else {
+      int64_t dn, dt;
+      int klast;
+      st.propose(mv, dn, dt, klast);
+      const int64_t delta = dn * t_ref - dt;
+      acc = metropolis(delta, t_ref, T, w.w);
+      if (acc) {
+        st.apply_move(mv.type, i, j);
+        for (int kk = mv.a + lane; kk <= klast; kk += kWave) st.cur[kk] = st.cand[kk];
+        wave_sync_lds();
+        cn += dn;
+        ct += (uint64_t)dt;
+      } else {
+        st.undo(mv);
+        wave_sync_lds();
+      }
+    }
+    if (acc) {
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (cn > bn || (cn == bn && ct < bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        for (int p = lane; p < n; p += kWave) gbest[p] = st.perm[p];
+      }
+    }
+    T = T * alpha;
+  }
+  for (int p = lane; p < n; p += kWave) gcur[p] = st.perm[p];
+  if (lane == 0) {
+    int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
+    rec[0] = cn;
+    rec[1] = (int64_t)ct;
+    rec[2] = bn;
+    rec[3] = (int64_t)bt;
+    rec[4] = biter;
+    rec[5] = accepts;
+    rec[6] = (int64_t)digest;
+    rec[7] = allmet;
+  }
+}
+
+}  // namespace sa

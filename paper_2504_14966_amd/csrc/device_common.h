@@ -23,6 +23,16 @@ struct DevModel {
 __device__ __forceinline__ uint32_t req_lin(uint4 r) { return r.x & 0xFFFFu; }
 __device__ __forceinline__ uint32_t req_lout(uint4 r) { return r.x >> 16; }
 
+struct QueuePtrs {
+  const uint16_t *in_len, *out_len;
+  const uint8_t *kind;
+  const uint32_t *thr;
+};
+
+// 64-bit FNV-1a steps folding the accepted trajectory of a chain.
+constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ull;
+constexpr uint64_t kFnvPrime = 0x100000001B3ull;
+
 // Workspace layout (bytes), identical on host and device.
 struct WsHeader {
   uint64_t magic;

@@ -19,12 +19,6 @@ namespace sa {
 constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 
-struct QueuePtrs {
-  const uint16_t *in_len, *out_len;
-  const uint8_t *kind;
-  const uint32_t *thr;
-};
-
 // Cooperative, coalesced load of the request records into LDS.
 __device__ __forceinline__ void load_requests(const QueuePtrs &q, int n, uint4 *req) {
   for (int r = threadIdx.x; r < n; r += blockDim.x) {
@@ -159,9 +153,6 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
     }
   }
 }
-
-constexpr uint64_t kFnvOffset = 0xCBF29CE484222325ull;
-constexpr uint64_t kFnvPrime = 0x100000001B3ull;
 
 // Per-wave LDS: current and candidate-scratch orders, replay staging.
 __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,

@@ -10,6 +10,7 @@
 
 #include "../../include/sloanneal.h"
 #include "kernels.h"
+#include "anneal_static.h"
 
 namespace {
 
@@ -57,7 +58,7 @@ int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h) {
   HIP_TRY(hipMemcpyAsync(h.thr.data(), q->thr_us, n * 4, hipMemcpyDeviceToHost, stream));
   HIP_TRY(hipStreamSynchronize(stream));
   for (size_t r = 0; r < n; ++r) {
-    if (h.out_len[r] < 1 || h.kind[r] > 2) return SCHED_EINVAL;
+    if (h.out_len[r] < 1 || h.kind[r] > 2 || h.thr[r] > SCHED_THR_MAX) return SCHED_EINVAL;
   }
   return SCHED_OK;
 }
@@ -104,6 +105,55 @@ sa::QueuePtrs dev_queue(const sched_queue_t *q) {
 size_t eval_lds_bytes(int n) {
   const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 + 64 * 16 + 32 * 4;
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
+}
+
+// The delta kernel keeps finish offsets, prefills, slacks and doubled pair costs in 32
+// bits and forms each doubled pair cost mu * (e + d2 * mu), e = 2 (d1 + d2 l_in) + d2, with
+// 24-bit multiplies. Every finish offset is at most B * max prefill + L_max * d0 + B *
+// (d1 * L_max + d2 * (l_max * L_max + L_max (L_max + 1) / 2)).
+bool static_narrow(const HostQueue &h, const sched_model_t *m, int n) {
+  long double lmax = 0, Lmax = 0;
+  for (int r = 0; r < n; ++r) {
+    lmax = std::max<long double>(lmax, h.in_len[r]);
+    Lmax = std::max<long double>(Lmax, h.out_len[r]);
+  }
+  const long double b = std::min(n, m->max_batch);
+  const long double pf = (long double)m->p0 + (long double)m->p1 * lmax;
+  const long double fmax = b * pf + Lmax * m->d0 +
+                           b * ((long double)m->d1 * Lmax + (long double)m->d2 * (lmax * Lmax + Lmax * (Lmax + 1) / 2));
+  const long double emax = 2.0L * ((long double)m->d1 + (long double)m->d2 * lmax) + m->d2;
+  const long double inner = emax + (long double)m->d2 * Lmax;
+  const long double two24 = 16777216.0L, two32 = 4294967296.0L;
+  return fmax < two32 - 1 && inner < two24 && (long double)m->d2 < two24 && b * Lmax * inner < two32 &&
+         (long double)m->d0 < two32;
+}
+
+size_t static_wave_lds(int n, int B) {
+  const size_t M = (size_t)(n + B - 1) / B;
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)n * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(sa::BatchRec);
+}
+
+int device_attr(hipDeviceAttribute_t attr, int fallback) {
+  int dev = 0, v = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, attr, dev) != hipSuccess) return fallback;
+  return v;
+}
+int max_lds_per_block() { return device_attr(hipDeviceAttributeMaxSharedMemoryPerBlock, 65536); }
+int cu_count() { return device_attr(hipDeviceAttributeMultiprocessorCount, 256); }
+
+template <int LG>
+hipError_t launch_static(int waves, size_t lds, const sa::DevModel &dm, const sa::StaticParams &sp,
+                         const sa::QueuePtrs &q, int chains, int iters, double T0, double alpha, uint64_t seed,
+                         uint64_t swap_thr, unsigned char *w, hipStream_t stream) {
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_static_kernel<LG>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int grid = (chains + waves - 1) / waves;
+  sa::anneal_static_kernel<LG><<<grid, waves * 64, lds, stream>>>(dm, sp, q, chains, iters, T0, alpha, (uint32_t)seed,
+                                                                  (uint32_t)(seed >> 32), swap_thr, w);
+  return hipGetLastError();
 }
 
 size_t anneal_lds_bytes(int n) {
@@ -162,10 +212,44 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
   HIP_TRY(hipGetLastError());
-  const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
-  sa::anneal_kernel<<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
-      dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold, w);
-  HIP_TRY(hipGetLastError());
+  bool done = false;
+  if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+    // chains per workgroup: enough to spread the chains over every CU, at most 16 and
+    // at most what the LDS holds
+    const size_t soa = (size_t)n * 16, per = static_wave_lds(n, model->max_batch);
+    const int lim = max_lds_per_block();
+    const int cus = std::max(1, cu_count());
+    int waves = 1;
+    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+    if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= chains)) {
+      int lg = 0;
+      while ((1 << lg) < model->max_batch) ++lg;
+      sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
+                          (uint32_t)((1ull << 32) / (uint64_t)model->max_batch + 1), 0u};
+      const size_t lds = soa + per * waves;
+      const sa::QueuePtrs qp = dev_queue(queue);
+      const uint64_t st = model->swap_threshold;
+      hipError_t e = hipSuccess;
+      switch (lg) {
+        case 0: e = launch_static<0>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        case 1: e = launch_static<1>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        case 2: e = launch_static<2>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        case 3: e = launch_static<3>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        case 4: e = launch_static<4>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        case 5: e = launch_static<5>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        default: e = launch_static<6>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+      }
+      if (e != hipSuccess) return hip_fail(e);
+      done = true;
+    }
+  }
+  if (!done) {
+    const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+    sa::anneal_kernel<<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
+        dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold, w);
+    HIP_TRY(hipGetLastError());
+  }
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;

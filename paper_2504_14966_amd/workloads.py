@@ -162,7 +162,7 @@ def random_queue(rng: np.random.Generator, n: int, max_in=2048, max_out=64, thr_
     kind = rng.integers(0, 3, size=n).astype(np.uint8)
     if thr_hi is None:
         thr_hi = 20_000 * n * max_out
-    thr = rng.integers(0, thr_hi, size=n).astype(np.uint32)
+    thr = (rng.integers(0, thr_hi, size=n) % 0xFFFFFFFF).astype(np.uint32)  # at most 2^32 - 2
     return Queue(in_len, out_len, kind, thr)
 
 
