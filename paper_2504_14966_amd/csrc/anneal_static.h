@@ -456,40 +456,7 @@ struct StaticChain {
     }
   }
 
-  // Apply an accepted move to the order held in LDS.
-  __device__ void apply_move(int type, int i, int j) {
-    if (type == 1) {
-      if (lane == 0) {
-        const uint16_t x = perm[i];
-        perm[i] = perm[j];
-        perm[j] = x;
-      }
-    } else {
-      const uint16_t x = perm[i];
-      wave_sync_lds();
-      if (i < j) {
-        for (int p0 = i; p0 < j; p0 += kWave) {
-          const int p = p0 + lane;
-          uint16_t v = 0;
-          if (p < j) v = perm[p + 1];
-          wave_sync_lds();
-          if (p < j) perm[p] = v;
-          wave_sync_lds();
-        }
-      } else {
-        for (int p0 = i; p0 > j; p0 -= kWave) {
-          const int p = p0 - lane;
-          uint16_t v = 0;
-          if (p > j) v = perm[p - 1];
-          wave_sync_lds();
-          if (p > j) perm[p] = v;
-          wave_sync_lds();
-        }
-      }
-      if (lane == 0) perm[j] = x;
-    }
-    wave_sync_lds();
-  }
+  __device__ __forceinline__ void apply_move(int type, int i, int j) { apply_move_lds(perm, type, i, j, lane); }
 };
 
 // One wave per chain; blockDim / 64 chains per workgroup.

@@ -13,13 +13,13 @@ struct DevModel {
   int32_t n;       // requests
   int32_t B;       // max batch
   int32_t policy;  // 0 static, 1 continuous
-  int32_t pad;
+  int32_t flags;   // bit 0: continuous-admission event arithmetic fits 32 bits
   uint64_t p0, p1, d0, d1, d2;
 };
 
 // One request packed into 16 bytes for a single ds_read_b128 gather:
-//   x = l_in | l_out << 16, y = threshold (us), z = kind, w = prefill cost p0 + p1*l_in
-//   (low 32 bits; the high bits live in the separate pf_hi when the model is wide).
+//   x = l_in | l_out << 16, y = threshold (us), z = kind (low 2 bits), w = prefill cost
+//   p0 + p1 * l_in when it fits 32 bits (DevModel flags bit 0).
 __device__ __forceinline__ uint32_t req_lin(uint4 r) { return r.x & 0xFFFFu; }
 __device__ __forceinline__ uint32_t req_lout(uint4 r) { return r.x >> 16; }
 
@@ -42,6 +42,7 @@ struct WsHeader {
   int64_t reserved[20];
 };
 static_assert(sizeof(WsHeader) <= 256, "header fits its slot");
+constexpr int kFlagNarrowPrefill = 1;
 constexpr uint64_t kWsMagic = 0x534c4f414e4e3031ull;  // "SLOANN01"
 
 __host__ __device__ __forceinline__ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

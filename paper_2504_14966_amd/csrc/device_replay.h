@@ -45,6 +45,43 @@ struct Score {
   uint64_t t;
 };
 
+// Apply a move (1 swap, 2 insert: remove at i, re-insert at j) to an order in LDS, in place,
+// by one wave. Inserts shift the positions between i and j in chunks of 64, each chunk
+// read completely before it is written.
+__device__ __forceinline__ void apply_move_lds(uint16_t *perm, int type, int i, int j, int lane) {
+  if (type == 1) {
+    if (lane == 0) {
+      const uint16_t x = perm[i];
+      perm[i] = perm[j];
+      perm[j] = x;
+    }
+  } else if (type == 2) {
+    const uint16_t x = perm[i];
+    wave_sync_lds();
+    if (i < j) {
+      for (int p0 = i; p0 < j; p0 += kWave) {
+        const int p = p0 + lane;
+        uint16_t v = 0;
+        if (p < j) v = perm[p + 1];
+        wave_sync_lds();
+        if (p < j) perm[p] = v;
+        wave_sync_lds();
+      }
+    } else {
+      for (int p0 = i; p0 > j; p0 -= kWave) {
+        const int p = p0 - lane;
+        uint16_t v = 0;
+        if (p > j) v = perm[p - 1];
+        wave_sync_lds();
+        if (p > j) perm[p] = v;
+        wave_sync_lds();
+      }
+    }
+    if (lane == 0) perm[j] = x;
+  }
+  wave_sync_lds();
+}
+
 __device__ __forceinline__ bool slo_met(uint32_t kind, uint32_t thr, uint32_t L, uint64_t ttft, uint64_t e2e) {
   if (kind == 0) return ttft <= (uint64_t)thr;
   if (kind == 2) return e2e <= (uint64_t)thr;

@@ -13,6 +13,7 @@
 #include "device_common.h"
 #include "device_replay.h"
 #include "device_rng.h"
+#include "device_cont.h"
 
 namespace sa {
 
@@ -20,11 +21,21 @@ constexpr int kWavesPerBlock = 4;
 constexpr int kBlock = kWave * kWavesPerBlock;
 
 // Cooperative, coalesced load of the request records into LDS.
-__device__ __forceinline__ void load_requests(const QueuePtrs &q, int n, uint4 *req) {
-  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+__device__ __forceinline__ void load_requests(const QueuePtrs &q, const DevModel &m, uint4 *req) {
+  for (int r = threadIdx.x; r < m.n; r += blockDim.x) {
     const uint32_t lin = q.in_len[r], lout = q.out_len[r];
-    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r], 0u);
+    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r], (uint32_t)(m.p0 + m.p1 * lin));
   }
+}
+
+// Replay of one order: static closed form, or the continuous event loop (32-bit prefill
+// sums when they fit, the 64-bit variant otherwise).
+template <bool DETAIL>
+__device__ __forceinline__ Score replay_any(const DevModel &m, const uint4 *req, const uint16_t *perm, Remap rm,
+                                            uint4 *stage, int64_t *detail) {
+  if (m.policy == 0) return replay_static<DETAIL>(m, req, perm, rm, stage, detail);
+  if (m.flags & kFlagNarrowPrefill) return replay_cont_fast<DETAIL>(m, req, perm, rm, detail);
+  return replay_continuous<DETAIL>(m, req, perm, rm, detail);
 }
 
 __device__ __forceinline__ size_t lds_align(size_t x) { return (x + 15) & ~size_t(15); }
@@ -42,7 +53,7 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
   uint16_t *perm = reinterpret_cast<uint16_t *>(wbase);
   uint4 *stage = reinterpret_cast<uint4 *>(wbase + lds_align((size_t)n * 2));
   uint32_t *bitmap = reinterpret_cast<uint32_t *>(wbase + lds_align((size_t)n * 2) + 64 * 16);
-  load_requests(q, n, req);
+  load_requests(q, m, req);
   __syncthreads();
   const int lane = lane_id();
   for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < rows;
@@ -70,7 +81,7 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
       }
       continue;
     }
-    const Score s = replay<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, DETAIL ? detail + row * n * 2 : nullptr);
+    const Score s = replay_any<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, DETAIL ? detail + row * n * 2 : nullptr);
     if (lane == 0) {
       out[2 * row] = s.n;
       out[2 * row + 1] = (int64_t)s.t;
@@ -93,7 +104,7 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
   __shared__ uint4 stage[64];
   const int n = m.n;
   const int tid = threadIdx.x;
-  load_requests(q, n, req);
+  load_requests(q, m, req);
   int np = 1;
   while (np < n) np <<= 1;
   if (tid < np) {
@@ -167,7 +178,7 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
   uint16_t *bufA = reinterpret_cast<uint16_t *>(wbase);
   uint16_t *bufB = reinterpret_cast<uint16_t *>(wbase + lds_align((size_t)n * 2));
   uint4 *stage = reinterpret_cast<uint4 *>(wbase + 2 * lds_align((size_t)n * 2));
-  load_requests(q, n, req);
+  load_requests(q, m, req);
   __syncthreads();
   const int chain = uniform((int)blockIdx.x * kWavesPerBlock + wave);
   if (chain >= chains) return;
@@ -198,7 +209,7 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
     int i, j;
     pick_positions(n, w.y, w.z, i, j);
     const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
-    const Score s = replay<false>(m, req, cur, rm, stage, nullptr);
+    const Score s = replay_any<false>(m, req, cur, rm, stage, nullptr);
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
     const bool acc = metropolis(delta, t_ref, T, w.w);
     if (acc) {
@@ -223,6 +234,82 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
     T = T * alpha;
   }
   for (int p = lane; p < n; p += kWave) gcur[p] = cur[p];
+  if (lane == 0) {
+    int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
+    rec[0] = cn;
+    rec[1] = (int64_t)ct;
+    rec[2] = bn;
+    rec[3] = (int64_t)bt;
+    rec[4] = biter;
+    rec[5] = accepts;
+    rec[6] = (int64_t)digest;
+    rec[7] = allmet;
+  }
+}
+
+// Continuous admission: one wave per chain, blockDim / 64 chains per workgroup. Every
+// proposal is replayed from the start by the event loop (the candidate order is read
+// through a remap of the current one); an accepted move is applied in place.
+__global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
+                                                            double alpha, uint32_t key0, uint32_t key1,
+                                                            uint64_t swap_thr, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  uint16_t *perm = reinterpret_cast<uint16_t *>(lds + lds_align((size_t)n * 16) + (size_t)wave * lds_align((size_t)n * 2));
+  load_requests(q, m, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  int64_t cn = h->start_n;
+  uint64_t ct = (uint64_t)h->start_t;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    perm[p] = v;
+    gbest[p] = v;
+  }
+  wave_sync_lds();
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  double T = T0;
+  for (int k = 0; k < iters; ++k) {
+    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
+    int i, j;
+    pick_positions(n, w.y, w.z, i, j);
+    const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
+    const Score s = replay_cont_fast<false>(m, req, perm, rm, nullptr);
+    const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
+    const bool acc = metropolis(delta, t_ref, T, w.w);
+    if (acc) {
+      apply_move_lds(perm, i == j ? 0 : rm.kind, i, j, lane);
+      cn = s.n;
+      ct = s.t;
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (key_better(cn, ct, bn, bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        for (int p = lane; p < n; p += kWave) gbest[p] = perm[p];
+      }
+    }
+    T = T * alpha;
+  }
+  for (int p = lane; p < n; p += kWave) gcur[p] = perm[p];
   if (lane == 0) {
     int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
     rec[0] = cn;

@@ -84,12 +84,27 @@ int range_check(const HostQueue &h, const sched_model_t *m, int n) {
   return SCHED_OK;
 }
 
-sa::DevModel dev_model(const sched_model_t *m, int n) {
+// The continuous event loop's 32-bit arithmetic: group prefill sums, the context sum C of
+// the running requests, d0 + d1 b + d2 C and d2 b all stay below 2^32.
+bool prefill_narrow(const HostQueue &h, const sched_model_t *m, int n) {
+  long double lmax = 0, Lmax = 0;
+  for (int r = 0; r < n; ++r) {
+    lmax = std::max<long double>(lmax, h.in_len[r]);
+    Lmax = std::max<long double>(Lmax, h.out_len[r]);
+  }
+  const long double b = std::min(n, m->max_batch), two32 = 4294967296.0L;
+  const long double pf = (long double)m->p0 + (long double)m->p1 * lmax;
+  const long double cmax = b * (lmax + Lmax);
+  const long double x = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * cmax;
+  return pf * b < two32 && cmax < two32 && x < two32 && (long double)m->d2 * b < two32;
+}
+
+sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill) {
   sa::DevModel d;
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
-  d.pad = 0;
+  d.flags = narrow_prefill ? sa::kFlagNarrowPrefill : 0;
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
@@ -177,7 +192,7 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n);
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n));
   const int64_t want = (k + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
   const int grid = (int)std::min<int64_t>(want, 256 * 32);
   const size_t lds = eval_lds_bytes(n);
@@ -208,7 +223,7 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if ((rc = fetch_queue(queue, stream, h))) return rc;
   if ((rc = range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n);
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n));
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
   HIP_TRY(hipGetLastError());
@@ -243,6 +258,23 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
       if (e != hipSuccess) return hip_fail(e);
       done = true;
     }
+  }
+  if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
+    const size_t soa = (size_t)n * 16, per = ((size_t)n * 2 + 15) & ~size_t(15);
+    const int cus = std::max(1, cu_count());
+    int waves = 1;
+    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    const size_t lds = soa + per * waves;
+    if (lds > 65536) {
+      HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_cont_kernel),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    }
+    const int grid = (chains + waves - 1) / waves;
+    sa::anneal_cont_kernel<<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+                                                              (uint32_t)seed, (uint32_t)(seed >> 32),
+                                                              model->swap_threshold, w);
+    HIP_TRY(hipGetLastError());
+    done = true;
   }
   if (!done) {
     const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
