@@ -30,20 +30,66 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algo_lane_ops_per_iter(W) -> float:
-    """Algorithmic int32 lane-ops of one chain-iteration (one proposal scored).
+# Algorithmic int32 lane-ops of the delta algorithm (static admission):
+#   per member of a batch whose membership changes: two doubled pair costs of 3 ops each
+#   (minimum, two 24-bit multiply-adds), the newcomer's pair cost (3), the offset update
+#   (3), the slack and SLO test (4), and one combining op in each of the six per-batch
+#   reductions (newcomer sum, duration max, two sums of offsets, two slack bounds) = 22;
+#   per batch whose start only shifts: one bounds check of 4 ops.
+OPS_CHANGED_MEMBER = 22
+OPS_SHIFTED_BATCH = 4
+# Continuous admission (event loop): per event the slot minimum, finish test, SLO test
+# and context update over the B slots (about 5 ops per slot) and, per admitted request,
+# its gather and state setup (about 6); about n events per proposal.
+OPS_CONT_PER_SLOT_EVENT = 5
 
-    The anneal kernel scores every proposal with a full timeline replay of the candidate
-    order. One request evaluated by the static closed form costs 3 lane-ops per batch
-    member it is paired with (minimum of output lengths, multiply-add of the context term,
-    multiply-add into the accumulator) plus 10 for its gather, prefill share, start offset,
-    SLO test and latency sum. Continuous admission costs, per request, one event of about
-    40 lane-ops over the slots it shares. Scalar work (Philox, acceptance) is not counted.
-    """
+
+def expected_work(W) -> dict:
+    """Expected work units of one proposal, averaged exactly over the proposal law
+    (i uniform, j uniform over the other positions, swap or insert by the swap threshold)."""
     n, B = W.queue.n, W.model.max_batch
-    if W.model.policy == 0:
-        return float(n * (3 * min(B, n) + 10))
-    return float(n * 40)
+    if W.model.policy != 0:
+        return dict(ops=float(n * (OPS_CONT_PER_SLOT_EVENT * min(B, n) + 6)))
+    M = -(-n // B)
+    sizes = np.array([min(B, n - k * B) for k in range(M)], dtype=np.float64)
+    csum = np.concatenate([[0.0], np.cumsum(sizes)])
+    i, j = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    off = i != j
+    a = (np.minimum(i, j) // B)[off]
+    c = (np.maximum(i, j) // B)[off]
+    same = a == c
+    # swap: batches a and c change, batches strictly between and after shift
+    sw_members = np.where(same, 0.0, sizes[a] + sizes[c])
+    sw_shift = np.where(same, 0.0, (c - a - 1) + (M - 1 - c))
+    # insert: batches a..c change, batches after c shift
+    in_members = np.where(same, 0.0, csum[c + 1] - csum[a])
+    in_shift = np.where(same, 0.0, M - 1 - c)
+    p_swap = min(W.model.swap_threshold, 1 << 32) / float(1 << 32)
+    members = p_swap * sw_members.mean() + (1 - p_swap) * in_members.mean()
+    shifted = p_swap * sw_shift.mean() + (1 - p_swap) * in_shift.mean()
+    return dict(changed_members=members, shifted_batches=shifted,
+                ops=OPS_CHANGED_MEMBER * members + OPS_SHIFTED_BATCH * shifted)
+
+
+# HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# passes (KiB, scaled by the factor a 256 MiB device copy gives each counter: 2.0 for
+# FETCH_SIZE, 1.0 for WRITE_SIZE), keyed by the SHA-256 of the kernel sources they were
+# taken on; any other source gives null.
+TRAFFIC_BY_SOURCE = {}
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2504_14966_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    return TRAFFIC_BY_SOURCE.get(kernel_source_hash())
 
 
 def time_anneal(sl, W, steps, warmup, torch):
@@ -156,7 +202,8 @@ def main():
     chain_iters = W.chains * W.iters
     value = chain_iters * args.steps / wall
     k_ms = float(np.mean(kern_ms))
-    ops = algo_lane_ops_per_iter(W) * chain_iters
+    work = expected_work(W)
+    ops = work["ops"] * chain_iters
     achieved = ops / (k_ms * 1e-3)
     log(f"[bench] {value:.4g} chain-iters/s, anneal call {k_ms:.2f} ms, best key {key}")
 
@@ -198,9 +245,9 @@ def main():
                    "policy": "static" if W.model.policy == 0 else "continuous", "chains": W.chains,
                    "iters": W.iters, "T0": W.T0, "alpha": W.alpha, "parallelism": "chains"},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
-                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
-                     "kernel": "anneal_kernel", "kernel_ms": k_ms,
-                     "algo_lane_ops_per_chain_iter": algo_lane_ops_per_iter(W)},
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": measured_traffic(),
+                     "kernel": "anneal_static_kernel<6>", "kernel_ms": k_ms,
+                     "algo_lane_ops_per_chain_iter": work["ops"], "work_per_chain_iter": work},
         "cpu_baseline": cpu,
         "extras": extras,
     }
