@@ -112,3 +112,217 @@ __device__ Score replay_cont_fast(const DevModel &m, const uint4 *__restrict__ r
 }
 
 }  // namespace sa
+
+namespace sa {
+
+// ---------------------------------------------------------------------------------------
+// Continuous admission in O(n) wave operations: list scheduling, then scans.
+//
+// In decode-step units continuous batching is list scheduling on B identical slots: the
+// first min(B, n) requests start at step 0, and every time a running request finishes (the
+// smallest finish step among the running ones) the next request in priority order takes
+// its slot at that step and finishes l_out steps later. So the k-th finish event (in step
+// order) is the k-th pop of a sorted list of the running requests' finish steps, and event
+// k admits position min(B, n) + k - 1 while requests wait. The list lives in lanes,
+// ascending: a pop is a one-lane DPP wave shift and an insert is a ballot plus a select.
+// Keys pack (finish step << 10 | position), so ties are broken by position; which of two
+// requests finishing at the same step is popped first changes no result.
+//
+// The clock then follows from prefix sums over the events. Between events k-1 and k
+// (s_k = f_k - f_{k-1} decode steps) the running count is b_k = min(n0, n - k + 1), and the
+// context sum C_k at the segment start obeys C_{k+1} = C_k + b_k s_k - (l + l_out of the
+// finishing request) + (l of the admitted request). The segment costs
+//   seg_k = s_k (d0 + d1 b_k + d2 C_k) + d2 b_k s_k (s_k + 1) / 2,
+// and event k's admission adds its prefill pre_k. All finishes at one step happen before
+// that step's single admission group, so with SEG and PRE the inclusive prefix sums and
+// [rs_k, re_k] the run of events sharing step f_k:
+//   e2e(finishing request of k) = PR0 + SEG_k + PRE_{rs_k - 1},
+//   TTFT(request admitted at k) = PR0 + SEG_k + PRE_{re_k},
+// where PR0 is the prefill of the initial group. Scans are DPP row shifts plus row
+// broadcasts (6 steps for 64 lanes).
+// ---------------------------------------------------------------------------------------
+
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143, kDppWaveShl1 = 0x130, kDppWaveShr1 = 0x138;
+
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint32_t dpp_old(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWMASK, 0xF, false);
+}
+
+// inclusive scans over the 64 lanes
+__device__ __forceinline__ uint32_t scan_add32(uint32_t v) {
+  v += dpp_old<kDppRowShr1, 0xF>(0u, v);
+  v += dpp_old<kDppRowShr2, 0xF>(0u, v);
+  v += dpp_old<kDppRowShr4, 0xF>(0u, v);
+  v += dpp_old<kDppRowShr8, 0xF>(0u, v);
+  v += dpp_old<kDppRowBcast15, 0xA>(0u, v);
+  v += dpp_old<kDppRowBcast31, 0xC>(0u, v);
+  return v;
+}
+__device__ __forceinline__ uint32_t scan_max32(uint32_t v) {
+  v = max(v, dpp_old<kDppRowShr1, 0xF>(0u, v));
+  v = max(v, dpp_old<kDppRowShr2, 0xF>(0u, v));
+  v = max(v, dpp_old<kDppRowShr4, 0xF>(0u, v));
+  v = max(v, dpp_old<kDppRowShr8, 0xF>(0u, v));
+  v = max(v, dpp_old<kDppRowBcast15, 0xA>(0u, v));
+  v = max(v, dpp_old<kDppRowBcast31, 0xC>(0u, v));
+  return v;
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint64_t add_dpp64(uint64_t v) {
+  const uint32_t lo = dpp_old<CTRL, ROWMASK>(0u, (uint32_t)v), hi = dpp_old<CTRL, ROWMASK>(0u, (uint32_t)(v >> 32));
+  return v + (((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ uint64_t scan_add64(uint64_t v) {
+  v = add_dpp64<kDppRowShr1, 0xF>(v);
+  v = add_dpp64<kDppRowShr2, 0xF>(v);
+  v = add_dpp64<kDppRowShr4, 0xF>(v);
+  v = add_dpp64<kDppRowShr8, 0xF>(v);
+  v = add_dpp64<kDppRowBcast15, 0xA>(v);
+  v = add_dpp64<kDppRowBcast31, 0xC>(v);
+  return v;
+}
+__device__ __forceinline__ uint64_t rl64(uint64_t v, int l) {
+  return ((uint64_t)rl((uint32_t)(v >> 32), l) << 32) | rl((uint32_t)v, l);
+}
+
+// Per-wave LDS scratch of the list-scheduling replay (bytes, 8-aligned).
+__host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) {
+  return ((size_t)4 * n + 4 * 3 * (size_t)(n + 1) + 7) / 8 * 8 + (size_t)16 * (n + 1);
+}
+
+template <bool DETAIL>
+__device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm, Remap rm,
+                                unsigned char *scratch, int64_t *detail) {
+  const int lane = lane_id();
+  const int N = m.n, B = m.B;
+  const int n0 = min(B, N), nadm = N - n0;
+  const uint32_t d0 = (uint32_t)m.d0, d1 = (uint32_t)m.d1, d2 = (uint32_t)m.d2;
+  uint32_t *ev = reinterpret_cast<uint32_t *>(scratch);  // packed key of event k at [k - 1]
+  uint32_t *preA = ev + N;                                // PRE_k at [k], PRE_0 = 0
+  uint32_t *rsA = preA + (N + 1);                         // run start of event k at [k]
+  uint32_t *runpre = rsA + (N + 1);                       // PRE at the end of the run starting at k
+  uint64_t *segA = reinterpret_cast<uint64_t *>(scratch + ((size_t)4 * N + 4 * 3 * (size_t)(N + 1) + 7) / 8 * 8);
+  uint64_t *tta = segA + (N + 1);                         // TTFT of the request admitted at event k
+  constexpr uint32_t kInf = 0xFFFFFFFFu;
+
+  // initial group: positions 0 .. n0-1 start at step 0
+  uint32_t key = kInf, lin0 = 0, pf0 = 0;
+  if (lane < n0) {
+    const uint4 rq = req[perm[rm.src(lane)]];
+    key = ((rq.x >> 16) << 10) | (uint32_t)lane;
+    lin0 = rq.x & 0xFFFFu;
+    pf0 = rq.w;
+  }
+  const uint64_t PR0 = wsum32(pf0);
+  const uint32_t C1 = wsum32(lin0);
+  int rank = 0;
+  for (int u = 0; u < n0; ++u) rank += rl(key, u) < key ? 1 : 0;
+  if (lane < n0) runpre[rank] = key;
+  wave_sync_lds();
+  uint32_t list = lane < n0 ? runpre[lane] : kInf;
+  wave_sync_lds();
+
+  // list scheduling: pop the earliest finish, admit the next position at that step
+  uint32_t evbuf = 0, Lbuf = 0;
+  for (int a = 0; a < nadm; ++a) {
+    const uint32_t top = __builtin_amdgcn_readfirstlane(list);
+    evbuf = lane == (a & 63) ? top : evbuf;
+    if ((a & 63) == 63) ev[a - 63 + lane] = evbuf;
+    const int p = n0 + a;
+    if (a == 0 || (p & 63) == 0) {
+      const int qq = (p & ~63) + lane;
+      Lbuf = qq < N ? (req[perm[rm.src(qq)]].x >> 16) : 0u;
+    }
+    const uint32_t nk = (((top >> 10) + rl(Lbuf, p & 63)) << 10) | (uint32_t)p;
+    const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
+    const int ins = __popcll(__ballot(sh < nk));
+    list = lane < ins ? sh : (lane == ins ? nk : list);
+  }
+  if ((nadm & 63) != 0 && lane < (nadm & 63)) ev[(nadm & ~63) + lane] = evbuf;
+  if (lane < n0) ev[nadm + lane] = list;
+  if (lane == 0) preA[0] = 0u;
+  wave_sync_lds();
+
+  // pass A: segment costs, prefills, run starts and their prefix sums
+  uint32_t fcarry = 0, Ccarry = C1, precarry = 0, rscarry = 0;
+  uint64_t segcarry = 0;
+  for (int c0 = 0; c0 < N; c0 += kWave) {
+    const int k = c0 + lane + 1;
+    const bool v = k <= N;
+    const uint32_t kk = v ? ev[k - 1] : 0u;
+    const uint32_t f = kk >> 10;
+    const int q = (int)(kk & 1023u);
+    const uint32_t fprev = dpp_old<kDppWaveShr1, 0xF>(fcarry, f);
+    const uint32_t s = v ? f - fprev : 0u;
+    const uint32_t b = (uint32_t)min(n0, N - k + 1);
+    uint32_t outq = 0, la = 0, pfa = 0;
+    if (v) {
+      const uint4 rq = req[perm[rm.src(q)]];
+      outq = (rq.x & 0xFFFFu) + (rq.x >> 16);
+    }
+    const bool adm = v && k <= nadm;
+    if (adm) {
+      const uint4 ra = req[perm[rm.src(n0 + k - 1)]];
+      la = ra.x & 0xFFFFu;
+      pfa = ra.w;
+    }
+    const uint32_t dC = v ? b * s - outq + la : 0u;  // two's complement: a signed change
+    const uint32_t dCi = scan_add32(dC);
+    const uint32_t Ck = Ccarry + dCi - dC;
+    const uint64_t seg = v ? (uint64_t)s * (d0 + d1 * b + d2 * Ck) + (uint64_t)(d2 * b) * ((s * (s + 1u)) >> 1) : 0ull;
+    const uint64_t SEG = segcarry + scan_add64(seg);
+    const uint32_t PRE = precarry + scan_add32(adm ? pfa : 0u);
+    const uint32_t rs = max(rscarry, scan_max32((v && (k == 1 || s != 0)) ? (uint32_t)k : 0u));
+    const uint32_t fnext = k < N ? (ev[k] >> 10) : kInf;
+    if (v) {
+      preA[k] = PRE;
+      rsA[k] = rs;
+      segA[k] = SEG;
+      if (k == N || fnext != f) runpre[rs] = PRE;
+    }
+    fcarry = rl(f, kWave - 1);
+    Ccarry += rl(dCi, kWave - 1);
+    segcarry = rl64(SEG, kWave - 1);
+    precarry = rl(PRE, kWave - 1);
+    rscarry = rl(rs, kWave - 1);
+  }
+  wave_sync_lds();
+
+  // pass B: end-to-end latency of each finishing request, TTFT of each admitted one, SLOs
+  uint64_t tsum = 0;
+  int64_t nmet = 0;
+  for (int c0 = 0; c0 < N; c0 += kWave) {
+    const int k = c0 + lane + 1;
+    const bool v = k <= N;
+    uint32_t q = 0, rsk = 1;
+    uint64_t SEG = 0;
+    if (v) {
+      q = ev[k - 1] & 1023u;
+      rsk = rsA[k];
+      SEG = segA[k];
+    }
+    const uint64_t e2e = PR0 + SEG + (rsk > 1 ? preA[rsk - 1] : 0u);
+    if (v && k <= nadm) tta[k] = PR0 + SEG + runpre[rsk];
+    wave_sync_lds();
+    bool met = false;
+    if (v) {
+      const int r = perm[rm.src((int)q)];
+      const uint4 rq = req[r];
+      const uint64_t ttft = (int)q < n0 ? PR0 : tta[q - n0 + 1];
+      const uint32_t kind = rq.z & 3u, thr = rq.y, L = rq.x >> 16;
+      met = kind == 0 ? ttft <= (uint64_t)thr : (kind == 2 ? e2e <= (uint64_t)thr : e2e - ttft <= (uint64_t)thr * L);
+      tsum += e2e;
+      if (DETAIL) {
+        detail[2 * r] = (int64_t)ttft;
+        detail[2 * r + 1] = (int64_t)e2e;
+      }
+    }
+    nmet += __popcll(__ballot(met));
+  }
+  wave_sync_lds();
+  return Score{nmet, wave_sum_u64(tsum)};
+}
+
+}  // namespace sa

@@ -47,12 +47,14 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
-  const size_t per_wave = lds_align((size_t)n * 2) + 64 * 16 + 32 * 4;
+  const bool ls = m.policy == 1 && (m.flags & kFlagListSched);
+  const size_t per_wave = lds_align((size_t)n * 2) + 64 * 16 + 32 * 4 + (ls ? lds_align(cont_ls_scratch_bytes(n)) : 0);
   const int wave = uniform((int)(threadIdx.x >> 6));
   unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
   uint16_t *perm = reinterpret_cast<uint16_t *>(wbase);
   uint4 *stage = reinterpret_cast<uint4 *>(wbase + lds_align((size_t)n * 2));
   uint32_t *bitmap = reinterpret_cast<uint32_t *>(wbase + lds_align((size_t)n * 2) + 64 * 16);
+  unsigned char *scratch = wbase + lds_align((size_t)n * 2) + 64 * 16 + 32 * 4;
   load_requests(q, m, req);
   __syncthreads();
   const int lane = lane_id();
@@ -81,7 +83,9 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
       }
       continue;
     }
-    const Score s = replay_any<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, DETAIL ? detail + row * n * 2 : nullptr);
+    int64_t *drow = DETAIL ? detail + row * n * 2 : nullptr;
+    const Score s = ls ? replay_cont_ls<DETAIL>(m, req, perm, Remap{0, 0, 0}, scratch, drow)
+                       : replay_any<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, drow);
     if (lane == 0) {
       out[2 * row] = s.n;
       out[2 * row + 1] = (int64_t)s.t;
@@ -248,8 +252,10 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
 }
 
 // Continuous admission: one wave per chain, blockDim / 64 chains per workgroup. Every
-// proposal is replayed from the start by the event loop (the candidate order is read
-// through a remap of the current one); an accepted move is applied in place.
+// proposal is replayed from the start, by list scheduling and scans (LS) or by the event
+// loop; the candidate order is read through a remap of the current one and an accepted
+// move is applied in place.
+template <bool LS>
 __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
                                                             double alpha, uint32_t key0, uint32_t key1,
                                                             uint64_t swap_thr, unsigned char *ws) {
@@ -258,7 +264,9 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const int wave = uniform((int)(threadIdx.x >> 6));
-  uint16_t *perm = reinterpret_cast<uint16_t *>(lds + lds_align((size_t)n * 16) + (size_t)wave * lds_align((size_t)n * 2));
+  const size_t per_wave = lds_align((size_t)n * 2) + (LS ? lds_align(cont_ls_scratch_bytes(n)) : 0);
+  uint16_t *perm = reinterpret_cast<uint16_t *>(lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave);
+  unsigned char *scratch = reinterpret_cast<unsigned char *>(perm) + lds_align((size_t)n * 2);
   load_requests(q, m, req);
   __syncthreads();
   const int chain = uniform((int)blockIdx.x * waves + wave);
@@ -289,7 +297,8 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     int i, j;
     pick_positions(n, w.y, w.z, i, j);
     const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
-    const Score s = replay_cont_fast<false>(m, req, perm, rm, nullptr);
+    const Score s = LS ? replay_cont_ls<false>(m, req, perm, rm, scratch, nullptr)
+                       : replay_cont_fast<false>(m, req, perm, rm, nullptr);
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
     const bool acc = metropolis(delta, t_ref, T, w.w);
     if (acc) {

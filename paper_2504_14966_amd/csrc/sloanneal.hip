@@ -99,12 +99,24 @@ bool prefill_narrow(const HostQueue &h, const sched_model_t *m, int n) {
   return pf * b < two32 && cmax < two32 && x < two32 && (long double)m->d2 * b < two32;
 }
 
-sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill) {
+// List scheduling packs (finish step << 10 | position) into 32 bits and keeps prefix
+// sums of prefill costs in 32 bits: the total of all output lengths stays below 2^22 and
+// the total prefill below 2^32.
+bool list_sched_ok(const HostQueue &h, const sched_model_t *m, int n) {
+  long double lsum = 0, pfsum = 0;
+  for (int r = 0; r < n; ++r) {
+    lsum += h.out_len[r];
+    pfsum += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
+  }
+  return n <= 1024 && lsum < 4194304.0L && pfsum < 4294967296.0L;
+}
+
+sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false) {
   sa::DevModel d;
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
-  d.flags = narrow_prefill ? sa::kFlagNarrowPrefill : 0;
+  d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0);
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
@@ -117,8 +129,9 @@ sa::QueuePtrs dev_queue(const sched_queue_t *q) {
   return sa::QueuePtrs{q->in_len, q->out_len, q->kind, q->thr_us};
 }
 
-size_t eval_lds_bytes(int n) {
-  const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 + 64 * 16 + 32 * 4;
+size_t eval_lds_bytes(int n, bool ls) {
+  const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 + 64 * 16 + 32 * 4 +
+                          (ls ? (sa::cont_ls_scratch_bytes(n) + 15) / 16 * 16 : 0);
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
 }
 
@@ -192,10 +205,15 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n));
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n));
   const int64_t want = (k + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
   const int grid = (int)std::min<int64_t>(want, 256 * 32);
-  const size_t lds = eval_lds_bytes(n);
+  const size_t lds = eval_lds_bytes(n, dm.policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagListSched));
+  if (lds > 65536) {
+    HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(detail ? (const void *)&sa::eval_kernel<true>
+                                                                      : (const void *)&sa::eval_kernel<false>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+  }
   if (detail) {
     sa::eval_kernel<true><<<grid, sa::kBlock, lds, stream>>>(dm, dev_queue(queue), perms, k, out, detail);
   } else {
@@ -223,7 +241,7 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if ((rc = fetch_queue(queue, stream, h))) return rc;
   if ((rc = range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n));
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n));
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
   HIP_TRY(hipGetLastError());
@@ -260,21 +278,31 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
     }
   }
   if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
-    const size_t soa = (size_t)n * 16, per = ((size_t)n * 2 + 15) & ~size_t(15);
+    const bool ls = (dm.flags & sa::kFlagListSched) != 0;
+    const size_t soa = (size_t)n * 16;
+    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0);
     const int cus = std::max(1, cu_count());
+    const int lim = max_lds_per_block();
     int waves = 1;
     while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
     const size_t lds = soa + per * waves;
-    if (lds > 65536) {
-      HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_cont_kernel),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+    if (lds <= (size_t)lim) {
+      const void *fn = ls ? (const void *)&sa::anneal_cont_kernel<true> : (const void *)&sa::anneal_cont_kernel<false>;
+      if (lds > 65536) HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      const int grid = (chains + waves - 1) / waves;
+      if (ls) {
+        sa::anneal_cont_kernel<true><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+                                                                        (uint32_t)seed, (uint32_t)(seed >> 32),
+                                                                        model->swap_threshold, w);
+      } else {
+        sa::anneal_cont_kernel<false><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+                                                                         (uint32_t)seed, (uint32_t)(seed >> 32),
+                                                                         model->swap_threshold, w);
+      }
+      HIP_TRY(hipGetLastError());
+      done = true;
     }
-    const int grid = (chains + waves - 1) / waves;
-    sa::anneal_cont_kernel<<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
-                                                              (uint32_t)seed, (uint32_t)(seed >> 32),
-                                                              model->swap_threshold, w);
-    HIP_TRY(hipGetLastError());
-    done = true;
   }
   if (!done) {
     const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
