@@ -224,23 +224,27 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   uint32_t list = lane < n0 ? runpre[lane] : kInf;
   wave_sync_lds();
 
-  // list scheduling: pop the earliest finish, admit the next position at that step
-  uint32_t evbuf = 0, Lbuf = 0;
-  for (int a = 0; a < nadm; ++a) {
-    const uint32_t top = __builtin_amdgcn_readfirstlane(list);
-    evbuf = lane == (a & 63) ? top : evbuf;
-    if ((a & 63) == 63) ev[a - 63 + lane] = evbuf;
-    const int p = n0 + a;
-    if (a == 0 || (p & 63) == 0) {
-      const int qq = (p & ~63) + lane;
-      Lbuf = qq < N ? (req[perm[rm.src(qq)]].x >> 16) : 0u;
+  // list scheduling: pop the earliest finish, admit the next position at that step. The
+  // list shifted down one lane (sh) merged with the new key nk is, lane by lane,
+  // sh < nk ? sh : (list < nk ? nk : list), since the popped minimum is below nk.
+  for (int c0 = 0; c0 < nadm; c0 += kWave) {
+    const int cnt = min(kWave, nadm - c0);
+    uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
+    if (lane < cnt) {
+      const int p = n0 + c0 + lane;
+      LP = ((req[perm[rm.src(p)]].x >> 16) << 10) | (uint32_t)p;
     }
-    const uint32_t nk = (((top >> 10) + rl(Lbuf, p & 63)) << 10) | (uint32_t)p;
-    const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
-    const int ins = __popcll(__ballot(sh < nk));
-    list = lane < ins ? sh : (lane == ins ? nk : list);
+    uint32_t evbuf = 0;
+    uint32_t top = __builtin_amdgcn_readfirstlane(list);
+    for (int t = 0; t < cnt; ++t) {
+      const uint32_t nk = (top & ~1023u) + rl(LP, t);
+      evbuf = lane == t ? top : evbuf;
+      const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
+      list = sh < nk ? sh : (list < nk ? nk : list);
+      top = __builtin_amdgcn_readfirstlane(list);
+    }
+    if (lane < cnt) ev[c0 + lane] = evbuf;
   }
-  if ((nadm & 63) != 0 && lane < (nadm & 63)) ev[(nadm & ~63) + lane] = evbuf;
   if (lane < n0) ev[nadm + lane] = list;
   if (lane == 0) preA[0] = 0u;
   wave_sync_lds();
