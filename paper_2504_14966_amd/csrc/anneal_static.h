@@ -84,13 +84,11 @@ struct Slack {
   uint32_t s;
 };
 __device__ __forceinline__ Slack slack_of(uint32_t kind, uint32_t thr, uint32_t L, uint32_t P, uint32_t F) {
-  if (kind == 1) {
-    const bool ok = (uint64_t)(F - P) <= (uint64_t)thr * L;
-    return Slack{ok, !ok, 0u};
-  }
+  const bool tpot = kind == 1;
+  const bool tpot_ok = (uint64_t)(F - P) <= (uint64_t)thr * L;
   const uint32_t off = kind == 0 ? P : F;
-  if (off > thr) return Slack{false, true, 0u};
-  return Slack{false, false, thr - off};
+  const bool late = off > thr;
+  return Slack{tpot && tpot_ok, tpot ? !tpot_ok : late, thr - off};
 }
 __device__ __forceinline__ bool slack_met(const Slack &x, uint64_t S) { return x.always || (!x.never && S <= x.s); }
 
@@ -102,17 +100,21 @@ template <int CTRL>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
 }
+// quad_perm and the two mirrors read a valid lane for every lane, so no fill value is used
 constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
 
 __device__ __forceinline__ uint32_t readlane(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
 
 struct OpAdd {
+  static constexpr uint32_t identity = 0u;
   __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return a + b; }
 };
 struct OpMax {
+  static constexpr uint32_t identity = 0u;
   __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return max(a, b); }
 };
 struct OpMin {
+  static constexpr uint32_t identity = 0xFFFFFFFFu;
   __device__ static __forceinline__ uint32_t f(uint32_t a, uint32_t b) { return min(a, b); }
 };
 
@@ -127,13 +129,17 @@ struct Seg {
     if constexpr (LG >= 2) v = Op::f(v, dpp<kQuadXor2>(v));
     if constexpr (LG >= 3) v = Op::f(v, dpp<kRowHalfMirror>(v));
     if constexpr (LG >= 4) v = Op::f(v, dpp<kRowMirror>(v));
+    if constexpr (LG >= 5) {
+      // rows 1 and 3 combine the last lane of rows 0 and 2: each 32-lane half is reduced
+      // in its last row
+      v = Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x142, 0xA, 0xF, false));
+    }
     if constexpr (LG == 5) {
-      const uint32_t s01 = Op::f(readlane(v, 0), readlane(v, 16));
-      const uint32_t s23 = Op::f(readlane(v, 32), readlane(v, 48));
-      v = lane < 32 ? s01 : s23;
+      v = lane < 32 ? readlane(v, 31) : readlane(v, 63);
     }
     if constexpr (LG == 6) {
-      v = Op::f(Op::f(readlane(v, 0), readlane(v, 16)), Op::f(readlane(v, 32), readlane(v, 48)));
+      v = Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x143, 0xC, 0xF, false));
+      v = readlane(v, 63);
     }
     return v;
   }
@@ -237,44 +243,36 @@ struct StaticChain {
     const int k0 = row * G, k1 = min(row * G + G - 1, M - 1);
     const bool row_changed = mv.type == 2 ? (mv.a <= k1 && mv.c >= k0)
                                           : ((mv.a >= k0 && mv.a <= k1) || (mv.c >= k0 && mv.c <= k1));
-    BatchRec br{0, 0, 0, 0, 0, 0, 0, {0, 0, 0}};
-    if (seg_live) br = cur[k];
-    int r = 0;
-    if (valid) r = perm[q];
-    Req rq{0, 0, 0, 0, 0};
-    uint32_t Fn = 0, Pn = br.P, Dn = br.D;
+    const BatchRec br = cur[min(k, M - 1)];
+    const int r = valid ? (int)perm[min(q, N - 1)] : N;  // lanes outside a batch use the spare slot N
+    Req rq = load_req(req, r);
+    uint32_t Fn = F[r];  // the spare slot N reads as 0 for lanes outside a batch
+    uint32_t Pn = br.P, Dn = br.D;
     uint64_t SFn = br.SF;
     if (row_changed) {
       int o = 0, e = 0;
-      if (seg_changed) out_in(k, mv, o, e);
+      out_in(seg_changed ? k : mv.a, mv, o, e);
       const Req ro = load_req(req, o), re = load_req(req, e);
-      if (seg_changed) Pn = br.P + re.pf - ro.pf;
-      const bool is_out = seg_changed && valid && r == o;
+      const uint32_t Pc = br.P + re.pf - ro.pf;
+      const bool is_out = seg_changed && r == o;
       const int rn = is_out ? e : r;
-      if (valid) rq = load_req(req, rn);
+      if (is_out) rq = re;
       // newcomer: prefill, its own decode steps and what every new member adds to them
       const uint32_t te = (seg_changed && valid) ? w2(rq.L, rq.e, re.L, sp.d2) : 0u;
-      const uint32_t Fe = Pn + re.L * sp.d0 + (Seg<LG>::template all<OpAdd>(te, lane) >> 1);
-      if (valid) {
-        if (!seg_changed) {
-          Fn = F[r];
-        } else if (is_out) {
-          Fn = Fe;
-        } else {
-          const int32_t dw = (int32_t)(w2(re.L, re.e, rq.L, sp.d2) - w2(ro.L, ro.e, rq.L, sp.d2));
-          Fn = F[r] + (Pn - br.P) + (uint32_t)(dw >> 1);
-        }
-        if (seg_changed) F[rn] = Fn;
+      const uint32_t Fe = Pc + __umul24(re.L, sp.d0) + (Seg<LG>::template all<OpAdd>(te, lane) >> 1);
+      const int32_t dw = (int32_t)(w2(re.L, re.e, rq.L, sp.d2) - w2(ro.L, ro.e, rq.L, sp.d2));
+      const uint32_t Fc = is_out ? Fe : Fn + (Pc - br.P) + (uint32_t)(dw >> 1);
+      if (seg_changed) {
+        Fn = valid ? Fc : 0u;
+        Pn = Pc;
       }
+      if (seg_changed && valid) F[rn] = Fc;
       const uint32_t Dm = Seg<LG>::template all<OpMax>(Fn, lane);
       const uint64_t SFm = Seg<LG>::sum_wide(Fn, lane);
       if (seg_changed) {
         Dn = Dm;
         SFn = SFm;
       }
-    } else if (valid) {
-      rq = load_req(req, r);
-      Fn = F[r];
     }
     const int64_t dlt = seg_changed ? (int64_t)Dn - (int64_t)br.D : 0;
     int64_t excl, total;
@@ -299,6 +297,7 @@ struct StaticChain {
   __device__ Score init() {
     uint64_t carry = 0, tl = 0;
     int64_t nmet = 0;
+    if (lane == 0) F[N] = 0u;  // spare slot read by lanes outside a batch
     for (int row = 0; row < R; ++row) {
       const int k = row * G + seg;
       const int q = k * B + mm;
@@ -319,7 +318,7 @@ struct StaticChain {
           acc += w2(o.L, o.e, rq.L, sp.d2);
         }
       }
-      const uint32_t Fv = valid ? P + rq.L * sp.d0 + (acc >> 1) : 0u;
+      const uint32_t Fv = valid ? P + __umul24(rq.L, sp.d0) + (acc >> 1) : 0u;
       if (valid) F[r] = Fv;
       const uint32_t D = Seg<LG>::template all<OpMax>(Fv, lane);
       const uint64_t SF = Seg<LG>::sum_wide(Fv, lane);
@@ -444,7 +443,7 @@ struct StaticChain {
         rq = load_req(req, r);
       }
       const uint32_t to = (seg_changed && valid) ? w2(rq.L, rq.e, ro.L, sp.d2) : 0u;
-      const uint32_t Fo = Pold + ro.L * sp.d0 + (Seg<LG>::template all<OpAdd>(to, lane) >> 1);
+      const uint32_t Fo = Pold + __umul24(ro.L, sp.d0) + (Seg<LG>::template all<OpAdd>(to, lane) >> 1);
       if (seg_changed && valid) {
         if (r == o) {
           F[o] = Fo;
@@ -472,12 +471,16 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
-  const size_t f_b = ((size_t)n * 4 + 15) & ~size_t(15);
+  const size_t f_b = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
   const size_t rec_b = (size_t)M * sizeof(BatchRec);
   const size_t per_wave = perm_b + f_b + 2 * rec_b;
   const int wave = uniform((int)(threadIdx.x >> 6));
-  unsigned char *wb = lds + (size_t)n * 16 + (size_t)wave * per_wave;
-  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
+  for (int r = threadIdx.x; r <= n; r += blockDim.x) {
+    if (r == n) {
+      req[r] = make_uint4(0u, 0u, 0u, 0u);  // spare record for lanes outside a batch
+      continue;
+    }
     const uint32_t lin = q.in_len[r], lout = q.out_len[r];
     const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
     const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);

@@ -153,12 +153,12 @@ bool static_narrow(const HostQueue &h, const sched_model_t *m, int n) {
   const long double inner = emax + (long double)m->d2 * Lmax;
   const long double two24 = 16777216.0L, two32 = 4294967296.0L;
   return fmax < two32 - 1 && inner < two24 && (long double)m->d2 < two24 && b * Lmax * inner < two32 &&
-         (long double)m->d0 < two32;
+         (long double)m->d0 < two24;
 }
 
 size_t static_wave_lds(int n, int B) {
   const size_t M = (size_t)(n + B - 1) / B;
-  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)n * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(sa::BatchRec);
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(sa::BatchRec);
 }
 
 int device_attr(hipDeviceAttribute_t attr, int fallback) {
@@ -249,7 +249,7 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     // chains per workgroup: enough to spread the chains over every CU, at most 16 and
     // at most what the LDS holds
-    const size_t soa = (size_t)n * 16, per = static_wave_lds(n, model->max_batch);
+    const size_t soa = (size_t)(n + 1) * 16, per = static_wave_lds(n, model->max_batch);
     const int lim = max_lds_per_block();
     const int cus = std::max(1, cu_count());
     int waves = 1;
