@@ -54,11 +54,10 @@ struct alignas(16) BatchRec {
 
 struct StaticParams {
   uint32_t d0, d2;
-  uint32_t bmagic;  // floor(2^32 / B) + 1: p / B == (p * bmagic) >> 32 for p < 2^16
-  uint32_t pad;
+  uint64_t bmagic;  // floor(2^32 / B) + 1 (2^32 + 1 for B = 1): p / B == (p * bmagic) >> 32 for p < 2^16
 };
 
-__device__ __forceinline__ uint32_t div_b(uint32_t p, uint32_t bmagic) {
+__device__ __forceinline__ uint32_t div_b(uint32_t p, uint64_t bmagic) {
   return (uint32_t)(((uint64_t)p * bmagic) >> 32);
 }
 
@@ -79,13 +78,15 @@ __device__ __forceinline__ uint32_t w2(uint32_t Lj, uint32_t ej, uint32_t Lm, ui
 
 // SLO flag of a member as a function of its batch start S: TPOT does not depend on S;
 // TTFT (offset P) and end-to-end (offset F) are met iff S <= thr - offset =: slack.
+// For TPOT requests the record's threshold field holds min(thr * l_out, 2^32 - 1): the
+// decode time F - P is below 2^32 - 1, so the test (F - P) <= thr * l_out is one compare.
 struct Slack {
   bool always, never;
   uint32_t s;
 };
 __device__ __forceinline__ Slack slack_of(uint32_t kind, uint32_t thr, uint32_t L, uint32_t P, uint32_t F) {
   const bool tpot = kind == 1;
-  const bool tpot_ok = (uint64_t)(F - P) <= (uint64_t)thr * L;
+  const bool tpot_ok = F - P <= thr;
   const uint32_t off = kind == 0 ? P : F;
   const bool late = off > thr;
   return Slack{tpot && tpot_ok, tpot ? !tpot_ok : late, thr - off};
@@ -484,7 +485,10 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
     const uint32_t lin = q.in_len[r], lout = q.out_len[r];
     const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
     const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
-    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r] | (e << 2), pf);
+    const uint32_t kind = q.kind[r];
+    const uint64_t thr_l = (uint64_t)q.thr[r] * lout;
+    const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
+    req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
   }
   __syncthreads();
   const int chain = uniform((int)blockIdx.x * waves + wave);

@@ -259,7 +259,7 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
       int lg = 0;
       while ((1 << lg) < model->max_batch) ++lg;
       sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
-                          (uint32_t)((1ull << 32) / (uint64_t)model->max_batch + 1), 0u};
+                          (1ull << 32) / (uint64_t)model->max_batch + 1};
       const size_t lds = soa + per * waves;
       const sa::QueuePtrs qp = dev_queue(queue);
       const uint64_t st = model->swap_threshold;

@@ -1,0 +1,85 @@
+"""GPU parity of every kernel path the host dispatch can choose, against the oracle.
+
+The library picks a kernel from the queue and model: the static delta kernel (32-bit
+finish offsets, LDS for the batch records), the continuous list-scheduling replay (total
+output below 2^22 tokens), the continuous event loop (32-bit event arithmetic), or the
+general full-replay kernels (64-bit everything). Each case below is built so that its
+sizes and coefficients fall on one path; all must agree with the oracle bit for bit.
+"""
+import os
+import sys
+import zlib
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(__file__))
+from gpu_helpers import oracle_chains  # noqa: E402
+
+from paper_2504_14966_amd.workloads import Model, Queue  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2504_14966_amd.sloanneal as m
+    m.load_library()
+    return m
+
+
+def _queue(rng, n, in_lo, in_hi, out_lo, out_hi, thr_hi):
+    return Queue(rng.integers(in_lo, in_hi + 1, n).astype(np.uint16), rng.integers(out_lo, out_hi + 1, n).astype(np.uint16),
+                 rng.integers(0, 3, n).astype(np.uint8), rng.integers(0, thr_hi, n).astype(np.uint32))
+
+
+CASES = {
+    # static, B = 1 over 1024 requests: delta kernel with one lane per batch
+    "static_b1_n1024": (lambda r: _queue(r, 1024, 16, 2048, 1, 6, 4_000_000_000), Model(1, 0, 2000, 40, 8000, 300, 2), 8, 150),
+    # static, d2 so large that pair costs exceed 24 bits: general full-replay kernel
+    "static_wide": (lambda r: _queue(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 0, 2000, 40, 8000, 300, 1 << 22), 16, 300),
+    # continuous, total output above 2^22 tokens: event loop instead of list scheduling
+    "cont_event_loop": (lambda r: _queue(r, 128, 16, 2048, 40000, 65535, 4_000_000_000), Model(64, 1, 2000, 40, 8000, 300, 2), 4, 40),
+    # continuous, context cost above 32 bits: general 64-bit event loop
+    "cont_wide": (lambda r: _queue(r, 24, 16, 2048, 4, 40, 4_000_000_000), Model(6, 1, 2000, 40, 8000, 300, 1 << 25), 16, 300),
+    # continuous, list scheduling with ties (equal output lengths) and B > n
+    "cont_ls_ties": (lambda r: _queue(r, 40, 16, 64, 5, 7, 3_000_000), Model(16, 1, 2000, 40, 8000, 300, 2), 16, 400),
+    "cont_ls_b_gt_n": (lambda r: _queue(r, 20, 16, 2048, 8, 200, 3_000_000), Model(32, 1, 2000, 40, 8000, 300, 2), 8, 300),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_eval_path(sl, orc, name):
+    mk, m, _, _ = CASES[name]
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    q = mk(rng)
+    rows = 6
+    perms = np.stack([rng.permutation(q.n) for _ in range(rows)]).astype(np.uint16)
+    dq = sl.DeviceQueue.from_queue(q)
+    out, det = sl.sched_eval(dq, m, sl.perms_to_device(perms), detail=True)
+    out, det = out.cpu().numpy(), det.cpu().numpy()
+    for r in range(rows):
+        nn, tt, ttft, e2e = orc.replay(q, m, perms[r], detail=True)
+        assert out[r].tolist() == [nn, tt], (name, r)
+        assert np.array_equal(det[r, :, 0], ttft) and np.array_equal(det[r, :, 1], e2e), (name, r)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_anneal_path(sl, orc, name):
+    import torch
+    mk, m, chains, iters = CASES[name]
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    q = mk(rng)
+    dq = sl.DeviceQueue.from_queue(q)
+    ws = sl.sched_anneal(dq, m, chains, iters, 0.7, 0.99, 11)
+    rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    torch.cuda.synchronize()
+    rec, cur, best = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best)
+    info = orc.start(q, m)
+    want = oracle_chains(q, m, list(range(chains)), iters, 0.7, 0.99, 11, info)
+    for c in range(chains):
+        wrec, wcur, wbest = want[c]
+        assert rec[c].tolist() == wrec.tolist(), (name, c)
+        assert cur[c].tolist() == wcur.tolist() and best[c].tolist() == wbest.tolist(), (name, c)
