@@ -582,3 +582,113 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
 }
 
 }  // namespace sa
+
+namespace sa {
+
+// Evaluation of whole orders under static admission, one wave per order, with the same
+// 32-bit arithmetic as the annealing kernel: per batch the prefill sum, each member's
+// finish offset by the pairwise closed form (one 8-byte LDS read and three 24-bit ops
+// per pair), the batch duration, the start scan across batches and the SLO test.
+template <int LG, bool DETAIL>
+__global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticParams sp, QueuePtrs q,
+                                                           const uint16_t *__restrict__ perms, int64_t rows,
+                                                           int64_t *__restrict__ out, int64_t *__restrict__ detail) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  constexpr int Bp = 1 << LG, G = kWave >> LG;
+  const int n = m.n, B = m.B;
+  const int M = (n + B - 1) / B, R = (M + G - 1) / G;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
+  const size_t per_wave = perm_b + 64 * 8 + 32 * 4;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  const int waves = blockDim.x >> 6;
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
+  uint16_t *perm = reinterpret_cast<uint16_t *>(wb);
+  uint2 *stage = reinterpret_cast<uint2 *>(wb + perm_b);
+  uint32_t *bitmap = reinterpret_cast<uint32_t *>(wb + perm_b + 64 * 8);
+  for (int r = threadIdx.x; r <= n; r += blockDim.x) {
+    if (r == n) {
+      req[r] = make_uint4(0u, 0u, 0u, 0u);
+      continue;
+    }
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    const uint32_t kind = q.kind[r];
+    const uint64_t thr_l = (uint64_t)q.thr[r] * lout;
+    const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
+    req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
+  }
+  __syncthreads();
+  const int lane = lane_id();
+  const int seg = lane >> LG, mm = lane & (Bp - 1);
+  const uint32_t d2m = sp.d2 & 0xFFFFFFu;
+  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+    const uint16_t *src = perms + row * n;
+    if (lane < 32) bitmap[lane] = 0u;
+    wave_sync_lds();
+    bool bad = false;
+    for (int p = lane; p < n; p += kWave) {
+      const uint32_t v = src[p];
+      perm[p] = (uint16_t)v;
+      if (v >= (uint32_t)n) {
+        bad = true;
+      } else {
+        const uint32_t bit = 1u << (v & 31u);
+        if (atomicOr(&bitmap[v >> 5], bit) & bit) bad = true;
+      }
+    }
+    wave_sync_lds();
+    if (__ballot(bad) != 0ull) {
+      if (lane == 0) {
+        out[2 * row] = -1;
+        out[2 * row + 1] = -1;
+      }
+      continue;
+    }
+    uint64_t carry = 0, tl = 0;
+    int nmet = 0;
+    for (int rr = 0; rr < R; ++rr) {
+      const int k = rr * G + seg;
+      const int qpos = k * B + mm;
+      const bool valid = mm < B && qpos < n;
+      const int r = valid ? (int)perm[min(qpos, n - 1)] : n;
+      const Req x = load_req(req, r);
+      stage[lane] = make_uint2(x.L, x.e);
+      wave_sync_lds();
+      const uint32_t P = Seg<LG>::template all<OpAdd>(x.pf, lane);
+      uint32_t acc = 0;
+      const int base = seg << LG;
+      for (int jj = 0; jj < B; ++jj) {
+        const uint2 sj = stage[base + jj];
+        const uint32_t mu = min(sj.x, x.L);
+        acc += mu * ((d2m * mu + sj.y) & 0xFFFFFFu);
+      }
+      wave_sync_lds();
+      const uint32_t F = valid ? P + __umul24(x.L, sp.d0) + (acc >> 1) : 0u;
+      const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);
+      int64_t excl, total;
+      Seg<LG>::scan(k < M ? (int64_t)D : 0, lane, excl, total);
+      const uint64_t S = carry + (uint64_t)excl;
+      const Slack sl = slack_of(x.kind, x.thr, x.L, P, F);
+      const bool met = valid && slack_met(sl, S);
+      nmet += __popcll(__ballot(met));
+      if (valid) {
+        tl += S + F;
+        if (DETAIL) {
+          detail[row * n * 2 + 2 * r] = (int64_t)(S + P);
+          detail[row * n * 2 + 2 * r + 1] = (int64_t)(S + F);
+        }
+      }
+      carry += (uint64_t)total;
+    }
+    const uint64_t t = wave_sum_u64(tl);
+    if (lane == 0) {
+      out[2 * row] = nmet;
+      out[2 * row + 1] = (int64_t)t;
+    }
+    wave_sync_lds();
+  }
+}
+
+}  // namespace sa

@@ -208,6 +208,36 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n));
   const int64_t want = (k + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
   const int grid = (int)std::min<int64_t>(want, 256 * 32);
+  if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+    int lg = 0;
+    while ((1 << lg) < model->max_batch) ++lg;
+    const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
+    const size_t lds = (size_t)(n + 1) * 16 + ((((size_t)n * 2 + 15) & ~size_t(15)) + 64 * 8 + 32 * 4) * 4;
+    const int64_t want4 = (k + 3) / 4;
+    const int g4 = (int)std::min<int64_t>(want4, 256 * 32);
+    hipError_t e = hipSuccess;
+#define SA_EVAL_CASE(L)                                                                                            \
+  case L:                                                                                                        \
+    if (detail)                                                                                                  \
+      sa::eval_static_kernel<L, true><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, detail);  \
+    else                                                                                                         \
+      sa::eval_static_kernel<L, false><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, nullptr); \
+    break;
+    switch (lg) {
+      SA_EVAL_CASE(0)
+      SA_EVAL_CASE(1)
+      SA_EVAL_CASE(2)
+      SA_EVAL_CASE(3)
+      SA_EVAL_CASE(4)
+      SA_EVAL_CASE(5)
+      default:
+        SA_EVAL_CASE(6)
+    }
+#undef SA_EVAL_CASE
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e);
+    return SCHED_OK;
+  }
   const size_t lds = eval_lds_bytes(n, dm.policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagListSched));
   if (lds > 65536) {
     HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(detail ? (const void *)&sa::eval_kernel<true>
