@@ -38,10 +38,10 @@ def log(*a):
 #   per batch whose start only shifts: one bounds check of 4 ops.
 OPS_CHANGED_MEMBER = 22
 OPS_SHIFTED_BATCH = 4
-# Continuous admission (event loop): per event the slot minimum, finish test, SLO test
-# and context update over the B slots (about 5 ops per slot) and, per admitted request,
-# its gather and state setup (about 6); about n events per proposal.
-OPS_CONT_PER_SLOT_EVENT = 5
+# Continuous admission (list scheduling): per admission 4 ops on each of the B list slots
+# (shift, two compares, select); per event about 22 ops over the two scan passes.
+OPS_CONT_PER_SLOT_ADMISSION = 4
+OPS_CONT_PER_EVENT = 22
 
 
 def expected_work(W) -> dict:
@@ -49,7 +49,8 @@ def expected_work(W) -> dict:
     (i uniform, j uniform over the other positions, swap or insert by the swap threshold)."""
     n, B = W.queue.n, W.model.max_batch
     if W.model.policy != 0:
-        return dict(ops=float(n * (OPS_CONT_PER_SLOT_EVENT * min(B, n) + 6)))
+        b = min(B, n)
+        return dict(ops=float((n - b) * OPS_CONT_PER_SLOT_ADMISSION * b + n * OPS_CONT_PER_EVENT))
     M = -(-n // B)
     sizes = np.array([min(B, n - k * B) for k in range(M)], dtype=np.float64)
     csum = np.concatenate([[0.0], np.cumsum(sizes)])
@@ -73,16 +74,20 @@ def expected_work(W) -> dict:
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
 # passes (KiB, scaled by the factor a 256 MiB device copy gives each counter: 2.0 for
-# FETCH_SIZE, 1.0 for WRITE_SIZE), keyed by the SHA-256 of the kernel sources they were
-# taken on; any other source gives null.
-TRAFFIC_BY_SOURCE = {}
+# FETCH_SIZE, 1.0 for WRITE_SIZE), keyed by the SHA-256 of the sources that kernel is
+# compiled and launched from; any other source gives null.
+STATIC_KERNEL_SOURCES = ("anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h", "sloanneal.hip")
+TRAFFIC_BY_SOURCE = {
+    # FETCH_SIZE 189.06 KiB x 2.0 + WRITE_SIZE 16,665.4 KiB x 1.0, burst workload, one launch
+    "482311857c729ddd67a6505e147f7f52efdcd5c106ad68e2de95812e0b0e2707": 17452495,
+}
 
 
 def kernel_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2504_14966_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in STATIC_KERNEL_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
