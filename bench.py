@@ -76,7 +76,8 @@ def expected_work(W) -> dict:
 # passes (KiB, scaled by the factor a 256 MiB device copy gives each counter: 2.0 for
 # FETCH_SIZE, 1.0 for WRITE_SIZE), keyed by the SHA-256 of the sources that kernel is
 # compiled and launched from; any other source gives null.
-STATIC_KERNEL_SOURCES = ("anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h", "sloanneal.hip")
+STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
+                         "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
     # FETCH_SIZE 189.06 KiB x 2.0 + WRITE_SIZE 16,665.4 KiB x 1.0, burst workload, one launch
     "482311857c729ddd67a6505e147f7f52efdcd5c106ad68e2de95812e0b0e2707": 17452495,
@@ -251,7 +252,7 @@ def main():
                    "iters": W.iters, "T0": W.T0, "alpha": W.alpha, "parallelism": "chains"},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": measured_traffic(),
-                     "kernel": "anneal_static_kernel<6>", "kernel_ms": k_ms,
+                     "kernel": "anneal_wave_kernel", "kernel_ms": k_ms,
                      "algo_lane_ops_per_chain_iter": work["ops"], "work_per_chain_iter": work},
         "cpu_baseline": cpu,
         "extras": extras,

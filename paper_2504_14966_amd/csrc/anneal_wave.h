@@ -1,0 +1,413 @@
+// Annealing chains under static admission when one batch fills one wave (33 <= B <= 64).
+//
+// Same delta re-simulation as the row kernel (a move changes the membership of batches
+// a..c by one leaving request o and one joining request e each; later batches only shift),
+// laid out for a batch per wave:
+//   - the batch records (start, prefill, duration, met count, slack bounds) live in vector
+//     registers, lane k holding batch k (at most 32 batches), so reading a record is a
+//     v_readlane and shifting a range of batches is one lane-parallel update;
+//   - at the start of a proposal one lane-parallel pass computes, for every changed batch,
+//     o and e, their request fields, the prefill change, the newcomer's finish offset up to
+//     its pair-cost sum, and the leaving member's old finish offset, and leaves them in a
+//     48-byte LDS entry per batch; each changed batch then reads its entry as a broadcast;
+//   - the newcomer's pair-cost sum is reduced over the current members and corrected by
+//     w(e, e) - w(o, e), so no lane swaps its request before the reduction;
+//   - the change of the sum of finish offsets, needed for the latency delta, is
+//     (size - 1) * dP + sum over staying members of half their pair-cost change + Fe - Fo
+//     (|sum| < 2^31 because B * max w < 2^32 is a host condition of this path).
+// A rejected proposal restores staying members by the reverse update and every leaving
+// member from the old value kept by the prologue.
+#pragma once
+#include "anneal_static.h"
+
+namespace sa {
+
+// 24-bit vector multiply(-add): operands below 2^24, results below 2^32
+__device__ __forceinline__ uint32_t vmad24(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t d;
+  asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+  return d;
+}
+__device__ __forceinline__ uint32_t vmul24(uint32_t a, uint32_t b) {
+  uint32_t d;
+  asm("v_mul_u32_u24 %0, %1, %2" : "=v"(d) : "v"(a), "v"(b));
+  return d;
+}
+__device__ __forceinline__ uint32_t rfl(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+
+// batch records, lane k = batch k
+struct LaneRecs {
+  uint32_t Slo, Shi, P, D, cnt, A, Bv;
+};
+
+struct WaveChain {
+  const uint4 *req;
+  uint16_t *perm;  // the order, n entries
+  uint32_t *F;     // n + 1 entries, F[n] = 0
+  uint4 *tab;      // 3 entries per batch, written by the prologue for changed batches
+  uint32_t d0, d2;
+  int N, B, M, lane;
+  LaneRecs cur, cand;
+  uint32_t fo, ovec;  // lane k: old F and id of the leaving member of changed batch k
+
+  __device__ __forceinline__ int batch_size(int k) const { return min(B, N - k * B); }
+  __device__ __forceinline__ int64_t requests_in(int k0, int k1) const {
+    return k1 <= k0 ? 0 : (int64_t)min(N, k1 * B) - (int64_t)k0 * B;
+  }
+  __device__ __forceinline__ uint64_t start_of(const LaneRecs &R, int k) const {
+    return ((uint64_t)readlane(R.Shi, k) << 32) | readlane(R.Slo, k);
+  }
+  __device__ __forceinline__ void put(LaneRecs &R, int k, uint64_t S, uint32_t P, uint32_t D, uint32_t cnt,
+                                      uint32_t A, uint32_t Bv) const {
+    const bool me = lane == k;
+    R.Slo = me ? (uint32_t)S : R.Slo;
+    R.Shi = me ? (uint32_t)(S >> 32) : R.Shi;
+    R.P = me ? P : R.P;
+    R.D = me ? D : R.D;
+    R.cnt = me ? cnt : R.cnt;
+    R.A = me ? A : R.A;
+    R.Bv = me ? Bv : R.Bv;
+  }
+
+  // SLO flags of the members at start S (TTFT and end-to-end members are met iff
+  // S <= thr - offset; TPOT members do not depend on S), the met count and the bounds
+  // [Bv, A] of starts that keep every flag.
+  struct Slo {
+    uint32_t cnt, A, Bv;
+  };
+  __device__ __forceinline__ Slo slo(bool valid, uint32_t kind, uint32_t thr, uint32_t P, uint32_t Fv, uint64_t S) const {
+    // thresholds are at most 2^32 - 2, so a start of 2^32 or more compares like 2^32 - 1
+    const uint32_t S32 = (S >> 32) ? 0xFFFFFFFFu : (uint32_t)S;
+    const bool tpot = kind == 1u;
+    const bool tpot_ok = Fv - P <= thr;
+    const uint32_t off = kind == 0u ? P : Fv;
+    const uint32_t sl = thr - off;
+    const bool always = tpot && tpot_ok;
+    const bool never = tpot ? !tpot_ok : off > thr;
+    const bool met = valid && (always || (!never && S32 <= sl));
+    Slo x;
+    x.cnt = (uint32_t)__popcll(__ballot(met));
+    x.A = Seg<6>::template all<OpMin>((met && !always) ? sl : 0xFFFFFFFFu, lane);
+    x.Bv = Seg<6>::template all<OpMax>((valid && !met && !never) ? sl + 1u : 0u, lane);
+    return x;
+  }
+
+  // Full evaluation of the current order (pairwise closed form per batch).
+  __device__ Score init() {
+    if (lane == 0) F[N] = 0u;
+    wave_sync_lds();
+    uint64_t carry = 0, tl = 0;
+    int64_t nmet = 0;
+    cur = LaneRecs{0, 0, 0, 0, 0, 0, 0};
+    for (int k = 0; k < M; ++k) {
+      const int q0 = k * B;
+      const int bs = batch_size(k);
+      const bool valid = lane < bs;
+      const int r = valid ? (int)perm[q0 + lane] : N;
+      const Req rq = load_req(req, r);
+      uint32_t P = 0, acc = 0;
+      for (int jj = 0; jj < bs; ++jj) {
+        const Req o = load_req(req, perm[q0 + jj]);
+        P += o.pf;
+        acc += w2(o.L, o.e, rq.L, d2);
+      }
+      const uint32_t Fv = valid ? P + __umul24(rq.L, d0) + (acc >> 1) : 0u;
+      if (valid) F[r] = Fv;
+      const uint32_t D = Seg<6>::template all<OpMax>(Fv, lane);
+      const uint64_t SF = Seg<6>::sum_wide(Fv, lane);
+      const Slo x = slo(valid, rq.kind, rq.thr, P, Fv, carry);
+      put(cur, k, carry, P, D, x.cnt, x.A, x.Bv);
+      tl += (uint64_t)bs * carry + SF;
+      nmet += x.cnt;
+      carry += D;
+    }
+    wave_sync_lds();
+    return Score{nmet, tl};
+  }
+
+  // Lane-parallel setup of the changed batches of a move (lane k = batch k).
+  __device__ void prologue(const Move &mv) {
+    const int k = lane;
+    const bool chg = k < M && mv.changes(k);
+    int opos, epos;
+    if (mv.type == 1) {
+      const int lo = min(mv.i, mv.j), hi = max(mv.i, mv.j);
+      opos = k == mv.a ? lo : hi;
+      epos = k == mv.a ? hi : lo;
+    } else if (mv.i < mv.j) {  // insert moving right: each batch passes its first member left
+      opos = k == mv.a ? mv.i : k * B;
+      epos = k == mv.c ? mv.i : (k + 1) * B;
+    } else {  // insert moving left: each batch passes its last member right
+      opos = k == mv.c ? mv.i : (k + 1) * B - 1;
+      epos = k == mv.a ? mv.i : k * B - 1;
+    }
+    if (!chg) {
+      opos = 0;
+      epos = 0;
+    }
+    const uint32_t o = perm[opos], e = perm[epos];
+    const uint4 ro = req[o], re = req[e];
+    fo = F[o];
+    ovec = o;
+    const uint32_t Lo = ro.x >> 16, eo = ro.z >> 2, Le = re.x >> 16, ee = re.z >> 2;
+    const uint32_t dP = re.w - ro.w;
+    const uint32_t Pc = cur.P + dP;
+    const uint32_t corr = w2(Le, ee, Le, d2) - w2(Lo, eo, Le, d2);  // w(e, e) - w(o, e)
+    const uint32_t FeBase = Pc + __umul24(Le, d0);
+    if (chg) {
+      tab[3 * k] = make_uint4(o, e, Lo, eo);
+      tab[3 * k + 1] = make_uint4(Le, ee, dP, corr);
+      tab[3 * k + 2] = make_uint4(FeBase, re.z & 3u, re.y, Pc);
+    }
+    wave_sync_lds();
+  }
+
+  // Candidate of changed batch k starting `shift` later: finish offsets (written to F),
+  // record, met-count and latency changes. Returns the duration change.
+  __device__ int64_t changed_row(int k, int64_t shift, int64_t &dn, int64_t &dt) {
+    const int q0 = k * B;
+    const int bs = batch_size(k);
+    const bool valid = lane < bs;
+    const uint4 t0 = tab[3 * k], t1 = tab[3 * k + 1], t2 = tab[3 * k + 2];
+    const uint32_t o = t0.x, e = t0.y, Lo = t0.z, eo = t0.w;
+    const uint32_t Le = t1.x, ee = t1.y, dP = t1.z, corr = t1.w;
+    const uint32_t FeBase = t2.x, kinde = t2.y, thre = t2.z, Pc = t2.w;
+    // lanes past the batch read the zero spare record and F[n] = 0
+    uint32_t r = N;
+    if (valid) r = perm[q0 + lane];
+    const uint4 rq = req[r];
+    const uint32_t Fm = F[r];
+    const uint32_t Lm = rq.x >> 16, em = rq.z >> 2;
+    const uint32_t mue = min(Lm, Le), muo = min(Lm, Lo);
+    const uint32_t te = vmul24(mue, vmad24(d2, mue, em));   // w(m, e)
+    const uint32_t wem = vmul24(mue, vmad24(d2, mue, ee));  // w(e, m)
+    const uint32_t wom = vmul24(muo, vmad24(d2, muo, eo));  // w(o, m)
+    const int32_t dwh = (int32_t)(wem - wom) >> 1;
+    const uint32_t tsum = Seg<6>::template all<OpAdd>(te, lane);
+    const uint32_t Fe = FeBase + ((tsum + corr) >> 1);
+    const bool is_out = r == o;
+    const uint32_t Fc = is_out ? Fe : Fm + dP + (uint32_t)dwh;
+    if (valid) F[is_out ? e : r] = Fc;
+    const uint32_t Fn = valid ? Fc : 0u;
+    const int32_t dsum = (int32_t)Seg<6>::template all<OpAdd>((valid && !is_out) ? (uint32_t)dwh : 0u, lane);
+    const uint32_t Dn = Seg<6>::template all<OpMax>(Fn, lane);
+    const uint64_t S = start_of(cur, k) + (uint64_t)shift;
+    const Slo x = slo(valid, is_out ? kinde : (rq.z & 3u), is_out ? thre : rq.y, Pc, Fn, S);
+    const uint32_t D0 = readlane(cur.D, k), cnt0 = readlane(cur.cnt, k), Fo = readlane(fo, k);
+    put(cand, k, S, Pc, Dn, x.cnt, x.A, x.Bv);
+    dn += (int64_t)x.cnt - (int64_t)cnt0;
+    const int64_t dSF = (int64_t)(bs - 1) * (int64_t)(int32_t)rfl(dP) + (int64_t)dsum + ((int64_t)rfl(Fe) - (int64_t)Fo);
+    dt += (int64_t)bs * shift + dSF;
+    return (int64_t)Dn - (int64_t)D0;
+  }
+
+  // Member recount of unchanged batch k whose start moved by `shift` out of its bounds.
+  __device__ void recount_row(int k, int64_t shift, int64_t &dn) {
+    const int q0 = k * B;
+    const bool valid = lane < batch_size(k);
+    uint32_t r = N;
+    if (valid) r = perm[q0 + lane];
+    const uint4 rq = req[r];
+    const uint32_t Fm = F[r];
+    const uint64_t S = start_of(cur, k) + (uint64_t)shift;
+    const Slo x = slo(valid, rq.z & 3u, rq.y, readlane(cur.P, k), Fm, S);
+    const bool me = lane == k;
+    cand.cnt = me ? x.cnt : cand.cnt;
+    cand.A = me ? x.A : cand.A;
+    cand.Bv = me ? x.Bv : cand.Bv;
+    dn += (int64_t)x.cnt - (int64_t)readlane(cur.cnt, k);
+  }
+
+  // Batches [k0, k1) keep their members and start `shift` later: new starts, latency
+  // change, and the mask of those whose start leaves its bounds.
+  __device__ uint64_t shift_range(int k0, int k1, int64_t shift, int64_t &dt) {
+    const bool in = lane >= k0 && lane < k1;
+    const uint64_t S = (((uint64_t)cur.Shi << 32) | cur.Slo) + (uint64_t)shift;
+    cand.Slo = in ? (uint32_t)S : cand.Slo;
+    cand.Shi = in ? (uint32_t)(S >> 32) : cand.Shi;
+    const bool flip = in && (S > (uint64_t)cur.A || S < (uint64_t)cur.Bv);
+    dt += shift * requests_in(k0, k1);
+    return __ballot(flip);
+  }
+
+  __device__ void propose(const Move &mv, int64_t &dn, int64_t &dt, int &klast) {
+    cand = cur;
+    prologue(mv);
+    dn = 0;
+    dt = 0;
+    int64_t carry = changed_row(mv.a, 0, dn, dt);
+    const int64_t shift_mid = carry;  // start change of the batches between a and c (swap)
+    uint64_t flagged = 0;
+    if (mv.type == 2) {
+      for (int k = mv.a + 1; k <= mv.c; ++k) carry += changed_row(k, carry, dn, dt);
+    } else {
+      // the batches strictly between a and c: candidate starts are written even for a
+      // zero shift, since the records are copied on accept
+      if (mv.c > mv.a + 1) flagged |= shift_range(mv.a + 1, mv.c, shift_mid, dt);
+      carry += changed_row(mv.c, shift_mid, dn, dt);
+    }
+    const int kb = mv.c + 1;
+    if (carry != 0 && kb < M) {
+      flagged |= shift_range(kb, M, carry, dt);
+      klast = M - 1;
+    } else {
+      klast = mv.c;
+    }
+    while (flagged) {
+      const int k = __builtin_ctzll(flagged);
+      flagged &= flagged - 1;
+      recount_row(k, k >= kb ? carry : shift_mid, dn);
+    }
+  }
+
+  // Restore F after a rejected proposal.
+  __device__ void undo(const Move &mv) {
+    for (int k = mv.a; k <= mv.c; ++k) {
+      if (mv.type == 1 && k != mv.a && k != mv.c) continue;
+      const int q0 = k * B;
+      const bool valid = lane < batch_size(k);
+      const uint4 t0 = tab[3 * k], t1 = tab[3 * k + 1];
+      const uint32_t o = t0.x, Lo = t0.z, eo = t0.w, Le = t1.x, ee = t1.y, dP = t1.z;
+      uint32_t r = N;
+      if (valid) r = perm[q0 + lane];
+      const uint32_t Lm = req[r].x >> 16;
+      const uint32_t Fm = F[r];
+      const uint32_t mue = min(Lm, Le), muo = min(Lm, Lo);
+      const uint32_t wem = vmul24(mue, vmad24(d2, mue, ee));
+      const uint32_t wom = vmul24(muo, vmad24(d2, muo, eo));
+      const int32_t dwh = (int32_t)(wem - wom) >> 1;
+      if (valid && r != o) F[r] = Fm - dP - (uint32_t)dwh;
+    }
+    // every leaving member's slot held a newcomer's candidate value
+    if (lane < M && mv.changes(lane)) F[ovec] = fo;
+    wave_sync_lds();
+  }
+
+  __device__ __forceinline__ void apply_move(int type, int i, int j) { apply_move_lds(perm, type, i, j, lane); }
+};
+
+
+// One wave per chain; blockDim / 64 chains per workgroup.
+__global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
+                                                            int iters, double T0, double alpha, uint32_t key0,
+                                                            uint32_t key1, uint64_t swap_thr, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n, B = m.B;
+  const int M = (n + B - 1) / B;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
+  const size_t f_b = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
+  const size_t per_wave = perm_b + f_b + (size_t)M * 48;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
+  for (int r = threadIdx.x; r <= n; r += blockDim.x) {
+    if (r == n) {
+      req[r] = make_uint4(0u, 0u, 0u, 0u);  // spare record for lanes outside a batch
+      continue;
+    }
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    const uint32_t kind = q.kind[r];
+    const uint64_t thr_l = (uint64_t)q.thr[r] * lout;
+    const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
+    req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
+  }
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  WaveChain st;
+  st.req = req;
+  st.perm = reinterpret_cast<uint16_t *>(wb);
+  st.F = reinterpret_cast<uint32_t *>(wb + perm_b);
+  st.tab = reinterpret_cast<uint4 *>(wb + perm_b + f_b);
+  st.d0 = sp.d0;
+  st.d2 = sp.d2;
+  st.N = n;
+  st.B = B;
+  st.M = M;
+  st.lane = lane;
+  st.fo = 0u;
+  st.ovec = 0u;
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    st.perm[p] = v;
+    gbest[p] = v;
+  }
+  wave_sync_lds();
+  const Score s0 = st.init();
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  double T = T0;
+  for (int k = 0; k < iters; ++k) {
+    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
+    int i, j;
+    pick_positions(n, w.y, w.z, i, j);
+    Move mv;
+    mv.type = (uint64_t)w.x < swap_thr ? 1 : 2;
+    mv.i = i;
+    mv.j = j;
+    mv.a = (int)div_b((uint32_t)min(i, j), sp.bmagic);
+    mv.c = (int)div_b((uint32_t)max(i, j), sp.bmagic);
+    bool acc;
+    if (mv.a == mv.c) {
+      // same batch: every batch keeps its members, the objective is unchanged
+      acc = true;
+      st.apply_move(mv.type, i, j);
+    } else {
+      int64_t dn, dt;
+      int klast;
+      st.propose(mv, dn, dt, klast);
+      const int64_t delta = dn * t_ref - dt;
+      acc = metropolis(delta, t_ref, T, w.w);
+      if (acc) {
+        st.apply_move(mv.type, i, j);
+        st.cur = st.cand;
+        cn += dn;
+        ct += (uint64_t)dt;
+      } else {
+        st.undo(mv);
+      }
+    }
+    if (acc) {
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (cn > bn || (cn == bn && ct < bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        for (int p = lane; p < n; p += kWave) gbest[p] = st.perm[p];
+      }
+    }
+    T = T * alpha;
+  }
+  for (int p = lane; p < n; p += kWave) gcur[p] = st.perm[p];
+  if (lane == 0) {
+    int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
+    rec[0] = cn;
+    rec[1] = (int64_t)ct;
+    rec[2] = bn;
+    rec[3] = (int64_t)bt;
+    rec[4] = biter;
+    rec[5] = accepts;
+    rec[6] = (int64_t)digest;
+    rec[7] = allmet;
+  }
+}
+
+}  // namespace sa

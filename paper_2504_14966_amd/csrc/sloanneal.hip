@@ -11,6 +11,7 @@
 #include "../../include/sloanneal.h"
 #include "kernels.h"
 #include "anneal_static.h"
+#include "anneal_wave.h"
 
 namespace {
 
@@ -161,6 +162,13 @@ size_t static_wave_lds(int n, int B) {
   return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(sa::BatchRec);
 }
 
+// LDS per chain of the one-batch-per-wave kernel: order, finish offsets, 48 bytes of
+// proposal table per batch
+size_t wave_chain_lds(int n, int B) {
+  const size_t M = (size_t)(n + B - 1) / B;
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + M * 48;
+}
+
 int device_attr(hipDeviceAttribute_t attr, int fallback) {
   int dev = 0, v = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, attr, dev) != hipSuccess) return fallback;
@@ -279,15 +287,18 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     // chains per workgroup: enough to spread the chains over every CU, at most 16 and
     // at most what the LDS holds
-    const size_t soa = (size_t)(n + 1) * 16, per = static_wave_lds(n, model->max_batch);
+    int lg = 0;
+    while ((1 << lg) < model->max_batch) ++lg;
+    // a batch of more than 32 requests fills a wave: the lane-per-batch kernel
+    const bool wave_kernel = lg == 6;
+    const size_t soa = (size_t)(n + 1) * 16;
+    const size_t per = wave_kernel ? wave_chain_lds(n, model->max_batch) : static_wave_lds(n, model->max_batch);
     const int lim = max_lds_per_block();
     const int cus = std::max(1, cu_count());
     int waves = 1;
     while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
     while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
     if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= chains)) {
-      int lg = 0;
-      while ((1 << lg) < model->max_batch) ++lg;
       sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
                           (1ull << 32) / (uint64_t)model->max_batch + 1};
       const size_t lds = soa + per * waves;
@@ -301,7 +312,18 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
         case 3: e = launch_static<3>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
         case 4: e = launch_static<4>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
         case 5: e = launch_static<5>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        default: e = launch_static<6>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
+        default: {
+          if (lds > 65536) {
+            e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_wave_kernel),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) break;
+          }
+          const int grid = (chains + waves - 1) / waves;
+          sa::anneal_wave_kernel<<<grid, waves * 64, lds, stream>>>(dm, sp, qp, chains, iters, T0, alpha, (uint32_t)seed,
+                                                                    (uint32_t)(seed >> 32), st, w);
+          e = hipGetLastError();
+          break;
+        }
       }
       if (e != hipSuccess) return hip_fail(e);
       done = true;

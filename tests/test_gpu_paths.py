@@ -1,9 +1,10 @@
 """GPU parity of every kernel path the host dispatch can choose, against the oracle.
 
-The library picks a kernel from the queue and model: the static delta kernel (32-bit
-finish offsets, LDS for the batch records), the continuous list-scheduling replay (total
-output below 2^22 tokens), the continuous event loop (32-bit event arithmetic), or the
-general full-replay kernels (64-bit everything). Each case below is built so that its
+The library picks a kernel from the queue and model: the static delta kernels (32-bit
+finish offsets; batch records in LDS for B <= 32, in lane-per-batch registers for B > 32),
+the continuous list-scheduling replay (total output below 2^22 tokens), the continuous
+event loop (32-bit event arithmetic), or the general full-replay kernels (64-bit
+everything). Each case below is built so that its
 sizes and coefficients fall on one path; all must agree with the oracle bit for bit.
 """
 import os
@@ -38,6 +39,10 @@ def _queue(rng, n, in_lo, in_hi, out_lo, out_hi, thr_hi):
 CASES = {
     # static, B = 1 over 1024 requests: delta kernel with one lane per batch
     "static_b1_n1024": (lambda r: _queue(r, 1024, 16, 2048, 1, 6, 4_000_000_000), Model(1, 0, 2000, 40, 8000, 300, 2), 8, 150),
+    # static, one batch per wave (B > 32) with a ragged last batch: lane-per-batch kernel
+    "static_wave_ragged": (lambda r: _queue(r, 150, 16, 2048, 1, 300, 4_000_000_000), Model(40, 0, 2000, 40, 8000, 300, 2), 8, 400),
+    # static, B > 32 and B > n: a single batch, every move keeps the objective
+    "static_wave_one_batch": (lambda r: _queue(r, 50, 16, 2048, 1, 300, 4_000_000_000), Model(64, 0, 2000, 40, 8000, 300, 2), 4, 100),
     # static, d2 so large that pair costs exceed 24 bits: general full-replay kernel
     "static_wide": (lambda r: _queue(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 0, 2000, 40, 8000, 300, 1 << 22), 16, 300),
     # continuous, total output above 2^22 tokens: event loop instead of list scheduling
