@@ -35,6 +35,44 @@ __device__ __forceinline__ uint32_t vmul24(uint32_t a, uint32_t b) {
 }
 __device__ __forceinline__ uint32_t rfl(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
 
+// Whole-wave all-reduces of two or three values at once, step by step, so that the DPP
+// steps of one fill the wait states the other needs between dependent steps. The result
+// is read from lane 63 into a scalar register.
+template <class Op>
+__device__ __forceinline__ uint32_t dpp_step(uint32_t v, int step) {
+  switch (step) {
+    case 0: return Op::f(v, dpp<kQuadXor1>(v));
+    case 1: return Op::f(v, dpp<kQuadXor2>(v));
+    case 2: return Op::f(v, dpp<kRowHalfMirror>(v));
+    case 3: return Op::f(v, dpp<kRowMirror>(v));
+    // rows 1 and 3 take the last lane of rows 0 and 2, then rows 2 and 3 the last lane of row 1
+    case 4: return Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x142, 0xA, 0xF, false));
+    default: return Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x143, 0xC, 0xF, false));
+  }
+}
+template <class O1, class O2>
+__device__ __forceinline__ void wave_all2(uint32_t &a, uint32_t &b) {
+#pragma unroll
+  for (int s = 0; s < 6; ++s) {
+    a = dpp_step<O1>(a, s);
+    b = dpp_step<O2>(b, s);
+  }
+  a = readlane(a, 63);
+  b = readlane(b, 63);
+}
+template <class O1, class O2, class O3>
+__device__ __forceinline__ void wave_all3(uint32_t &a, uint32_t &b, uint32_t &c) {
+#pragma unroll
+  for (int s = 0; s < 6; ++s) {
+    a = dpp_step<O1>(a, s);
+    b = dpp_step<O2>(b, s);
+    c = dpp_step<O3>(c, s);
+  }
+  a = readlane(a, 63);
+  b = readlane(b, 63);
+  c = readlane(c, 63);
+}
+
 // batch records, lane k = batch k
 struct LaneRecs {
   uint32_t Slo, Shi, P, D, cnt, A, Bv;
@@ -43,7 +81,7 @@ struct LaneRecs {
 struct WaveChain {
   const uint4 *req;
   uint16_t *perm;  // the order, n entries
-  uint32_t *F;     // n + 1 entries, F[n] = 0
+  uint32_t *F;     // n + 2 entries: F[n] = 0 is read by lanes past a batch, F[n + 1] takes their writes
   uint4 *tab;      // 3 entries per batch, written by the prologue for changed batches
   uint32_t d0, d2;
   int N, B, M, lane;
@@ -59,23 +97,23 @@ struct WaveChain {
   }
   __device__ __forceinline__ void put(LaneRecs &R, int k, uint64_t S, uint32_t P, uint32_t D, uint32_t cnt,
                                       uint32_t A, uint32_t Bv) const {
-    const bool me = lane == k;
-    R.Slo = me ? (uint32_t)S : R.Slo;
-    R.Shi = me ? (uint32_t)(S >> 32) : R.Shi;
-    R.P = me ? P : R.P;
-    R.D = me ? D : R.D;
-    R.cnt = me ? cnt : R.cnt;
-    R.A = me ? A : R.A;
-    R.Bv = me ? Bv : R.Bv;
+    // written as other ? old : new so that a scalar new value is the select's first operand
+    const bool other = lane != k;
+    R.Slo = other ? R.Slo : (uint32_t)S;
+    R.Shi = other ? R.Shi : (uint32_t)(S >> 32);
+    R.P = other ? R.P : P;
+    R.D = other ? R.D : D;
+    R.cnt = other ? R.cnt : cnt;
+    R.A = other ? R.A : A;
+    R.Bv = other ? R.Bv : Bv;
   }
 
   // SLO flags of the members at start S (TTFT and end-to-end members are met iff
   // S <= thr - offset; TPOT members do not depend on S), the met count and the bounds
   // [Bv, A] of starts that keep every flag.
-  struct Slo {
-    uint32_t cnt, A, Bv;
-  };
-  __device__ __forceinline__ Slo slo(bool valid, uint32_t kind, uint32_t thr, uint32_t P, uint32_t Fv, uint64_t S) const {
+  // Per lane: the contribution to A (min) and Bv (max); returns the met count.
+  __device__ __forceinline__ uint32_t slo(bool valid, uint32_t kind, uint32_t thr, uint32_t P, uint32_t Fv, uint64_t S,
+                                          uint32_t &a_in, uint32_t &b_in) const {
     // thresholds are at most 2^32 - 2, so a start of 2^32 or more compares like 2^32 - 1
     const uint32_t S32 = (S >> 32) ? 0xFFFFFFFFu : (uint32_t)S;
     const bool tpot = kind == 1u;
@@ -85,16 +123,17 @@ struct WaveChain {
     const bool always = tpot && tpot_ok;
     const bool never = tpot ? !tpot_ok : off > thr;
     const bool met = valid && (always || (!never && S32 <= sl));
-    Slo x;
-    x.cnt = (uint32_t)__popcll(__ballot(met));
-    x.A = Seg<6>::template all<OpMin>((met && !always) ? sl : 0xFFFFFFFFu, lane);
-    x.Bv = Seg<6>::template all<OpMax>((valid && !met && !never) ? sl + 1u : 0u, lane);
-    return x;
+    a_in = (met && !always) ? sl : 0xFFFFFFFFu;
+    b_in = (valid && !met && !never) ? sl + 1u : 0u;
+    return (uint32_t)__popcll(__ballot(met));
   }
 
   // Full evaluation of the current order (pairwise closed form per batch).
   __device__ Score init() {
-    if (lane == 0) F[N] = 0u;
+    if (lane == 0) {
+      F[N] = 0u;
+      F[N + 1] = 0u;
+    }
     wave_sync_lds();
     uint64_t carry = 0, tl = 0;
     int64_t nmet = 0;
@@ -113,12 +152,13 @@ struct WaveChain {
       }
       const uint32_t Fv = valid ? P + __umul24(rq.L, d0) + (acc >> 1) : 0u;
       if (valid) F[r] = Fv;
-      const uint32_t D = Seg<6>::template all<OpMax>(Fv, lane);
       const uint64_t SF = Seg<6>::sum_wide(Fv, lane);
-      const Slo x = slo(valid, rq.kind, rq.thr, P, Fv, carry);
-      put(cur, k, carry, P, D, x.cnt, x.A, x.Bv);
+      uint32_t D = Fv, A, Bv;
+      const uint32_t cnt = slo(valid, rq.kind, rq.thr, P, Fv, carry, A, Bv);
+      wave_all3<OpMax, OpMin, OpMax>(D, A, Bv);
+      put(cur, k, carry, P, D, cnt, A, Bv);
       tl += (uint64_t)bs * carry + SF;
-      nmet += x.cnt;
+      nmet += cnt;
       carry += D;
     }
     wave_sync_lds();
@@ -165,7 +205,6 @@ struct WaveChain {
   // Candidate of changed batch k starting `shift` later: finish offsets (written to F),
   // record, met-count and latency changes. Returns the duration change.
   __device__ int64_t changed_row(int k, int64_t shift, int64_t &dn, int64_t &dt) {
-    const int q0 = k * B;
     const int bs = batch_size(k);
     const bool valid = lane < bs;
     const uint4 t0 = tab[3 * k], t1 = tab[3 * k + 1], t2 = tab[3 * k + 2];
@@ -174,7 +213,7 @@ struct WaveChain {
     const uint32_t FeBase = t2.x, kinde = t2.y, thre = t2.z, Pc = t2.w;
     // lanes past the batch read the zero spare record and F[n] = 0
     uint32_t r = N;
-    if (valid) r = perm[q0 + lane];
+    if (valid) r = perm[k * B + lane];
     const uint4 rq = req[r];
     const uint32_t Fm = F[r];
     const uint32_t Lm = rq.x >> 16, em = rq.z >> 2;
@@ -183,20 +222,21 @@ struct WaveChain {
     const uint32_t wem = vmul24(mue, vmad24(d2, mue, ee));  // w(e, m)
     const uint32_t wom = vmul24(muo, vmad24(d2, muo, eo));  // w(o, m)
     const int32_t dwh = (int32_t)(wem - wom) >> 1;
-    const uint32_t tsum = Seg<6>::template all<OpAdd>(te, lane);
-    const uint32_t Fe = FeBase + ((tsum + corr) >> 1);
     const bool is_out = r == o;
+    uint32_t tsum = te, dsum = (valid && !is_out) ? (uint32_t)dwh : 0u;
+    wave_all2<OpAdd, OpAdd>(tsum, dsum);
+    const uint32_t Fe = FeBase + ((tsum + corr) >> 1);
     const uint32_t Fc = is_out ? Fe : Fm + dP + (uint32_t)dwh;
-    if (valid) F[is_out ? e : r] = Fc;
+    F[valid ? (is_out ? e : r) : N + 1] = Fc;
     const uint32_t Fn = valid ? Fc : 0u;
-    const int32_t dsum = (int32_t)Seg<6>::template all<OpAdd>((valid && !is_out) ? (uint32_t)dwh : 0u, lane);
-    const uint32_t Dn = Seg<6>::template all<OpMax>(Fn, lane);
     const uint64_t S = start_of(cur, k) + (uint64_t)shift;
-    const Slo x = slo(valid, is_out ? kinde : (rq.z & 3u), is_out ? thre : rq.y, Pc, Fn, S);
+    uint32_t Dn = Fn, A, Bv;
+    const uint32_t cnt = slo(valid, is_out ? kinde : (rq.z & 3u), is_out ? thre : rq.y, Pc, Fn, S, A, Bv);
+    wave_all3<OpMax, OpMin, OpMax>(Dn, A, Bv);
     const uint32_t D0 = readlane(cur.D, k), cnt0 = readlane(cur.cnt, k), Fo = readlane(fo, k);
-    put(cand, k, S, Pc, Dn, x.cnt, x.A, x.Bv);
-    dn += (int64_t)x.cnt - (int64_t)cnt0;
-    const int64_t dSF = (int64_t)(bs - 1) * (int64_t)(int32_t)rfl(dP) + (int64_t)dsum + ((int64_t)rfl(Fe) - (int64_t)Fo);
+    put(cand, k, S, Pc, Dn, cnt, A, Bv);
+    dn += (int64_t)cnt - (int64_t)cnt0;
+    const int64_t dSF = (int64_t)(bs - 1) * (int64_t)(int32_t)rfl(dP) + (int64_t)(int32_t)dsum + ((int64_t)rfl(Fe) - (int64_t)Fo);
     dt += (int64_t)bs * shift + dSF;
     return (int64_t)Dn - (int64_t)D0;
   }
@@ -210,12 +250,14 @@ struct WaveChain {
     const uint4 rq = req[r];
     const uint32_t Fm = F[r];
     const uint64_t S = start_of(cur, k) + (uint64_t)shift;
-    const Slo x = slo(valid, rq.z & 3u, rq.y, readlane(cur.P, k), Fm, S);
-    const bool me = lane == k;
-    cand.cnt = me ? x.cnt : cand.cnt;
-    cand.A = me ? x.A : cand.A;
-    cand.Bv = me ? x.Bv : cand.Bv;
-    dn += (int64_t)x.cnt - (int64_t)readlane(cur.cnt, k);
+    uint32_t A, Bv;
+    const uint32_t cnt = slo(valid, rq.z & 3u, rq.y, readlane(cur.P, k), Fm, S, A, Bv);
+    wave_all2<OpMin, OpMax>(A, Bv);
+    const bool other = lane != k;
+    cand.cnt = other ? cand.cnt : cnt;
+    cand.A = other ? cand.A : A;
+    cand.Bv = other ? cand.Bv : Bv;
+    dn += (int64_t)cnt - (int64_t)readlane(cur.cnt, k);
   }
 
   // Batches [k0, k1) keep their members and start `shift` later: new starts, latency
@@ -297,7 +339,7 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
-  const size_t f_b = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
+  const size_t f_b = ((size_t)(n + 2) * 4 + 15) & ~size_t(15);
   const size_t per_wave = perm_b + f_b + (size_t)M * 48;
   const int wave = uniform((int)(threadIdx.x >> 6));
   unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;

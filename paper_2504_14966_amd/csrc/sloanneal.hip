@@ -166,7 +166,7 @@ size_t static_wave_lds(int n, int B) {
 // proposal table per batch
 size_t wave_chain_lds(int n, int B) {
   const size_t M = (size_t)(n + B - 1) / B;
-  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + M * 48;
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 2) * 4 + 15) & ~size_t(15)) + M * 48;
 }
 
 int device_attr(hipDeviceAttribute_t attr, int fallback) {
