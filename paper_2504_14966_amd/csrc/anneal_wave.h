@@ -394,16 +394,27 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
   double T = T0;
+  // lane l holds the proposal of iteration k0 + l, drawn 64 at a time: i | j << 10 |
+  // (type - 1) << 20 | a << 21 | c << 26 (n <= 1024, at most 32 batches), and word 3
+  uint32_t mvpack = 0, w3v = 0;
   for (int k = 0; k < iters; ++k) {
-    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
-    int i, j;
-    pick_positions(n, w.y, w.z, i, j);
+    const int l = k & (kWave - 1);
+    if (l == 0) {
+      const u32x4 w = philox4x32_10((uint32_t)(k + lane), (uint32_t)chain, 0u, kTagAnneal, key0, key1);
+      int pi, pj;
+      pick_positions(n, w.y, w.z, pi, pj);
+      const uint32_t a = div_b((uint32_t)min(pi, pj), sp.bmagic), c = div_b((uint32_t)max(pi, pj), sp.bmagic);
+      mvpack = (uint32_t)pi | ((uint32_t)pj << 10) | (((uint64_t)w.x < swap_thr ? 0u : 1u) << 20) | (a << 21) | (c << 26);
+      w3v = w.w;
+    }
+    const uint32_t pk = readlane(mvpack, l), w3 = readlane(w3v, l);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     Move mv;
-    mv.type = (uint64_t)w.x < swap_thr ? 1 : 2;
+    mv.type = (int)((pk >> 20) & 1u) + 1;
     mv.i = i;
     mv.j = j;
-    mv.a = (int)div_b((uint32_t)min(i, j), sp.bmagic);
-    mv.c = (int)div_b((uint32_t)max(i, j), sp.bmagic);
+    mv.a = (int)((pk >> 21) & 31u);
+    mv.c = (int)(pk >> 26);
     bool acc;
     if (mv.a == mv.c) {
       // same batch: every batch keeps its members, the objective is unchanged
@@ -414,7 +425,7 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
       int klast;
       st.propose(mv, dn, dt, klast);
       const int64_t delta = dn * t_ref - dt;
-      acc = metropolis(delta, t_ref, T, w.w);
+      acc = metropolis(delta, t_ref, T, w3);
       if (acc) {
         st.apply_move(mv.type, i, j);
         st.cur = st.cand;

@@ -56,25 +56,31 @@ __device__ __forceinline__ void apply_move_lds(uint16_t *perm, int type, int i, 
       perm[j] = x;
     }
   } else if (type == 2) {
+    // shift the positions between i and j by one towards i, 4 x 64 positions per round:
+    // the reads of a round cover positions the round's writes do not reach, so one wait
+    // per round suffices (LDS accesses of a wave execute in order)
     const uint16_t x = perm[i];
-    wave_sync_lds();
     if (i < j) {
-      for (int p0 = i; p0 < j; p0 += kWave) {
-        const int p = p0 + lane;
-        uint16_t v = 0;
-        if (p < j) v = perm[p + 1];
-        wave_sync_lds();
-        if (p < j) perm[p] = v;
-        wave_sync_lds();
+      for (int c0 = i; c0 < j; c0 += 4 * kWave) {
+        uint16_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = perm[min(c0 + u * kWave + lane + 1, j)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = c0 + u * kWave + lane;
+          if (p < j) perm[p] = v[u];
+        }
       }
     } else {
-      for (int p0 = i; p0 > j; p0 -= kWave) {
-        const int p = p0 - lane;
-        uint16_t v = 0;
-        if (p > j) v = perm[p - 1];
-        wave_sync_lds();
-        if (p > j) perm[p] = v;
-        wave_sync_lds();
+      for (int c0 = i; c0 > j; c0 -= 4 * kWave) {
+        uint16_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = perm[max(c0 - u * kWave - lane - 1, j)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int p = c0 - u * kWave - lane;
+          if (p > j) perm[p] = v[u];
+        }
       }
     }
     if (lane == 0) perm[j] = x;
