@@ -521,12 +521,13 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
   double T = T0;
+  ProposalStream ps;
   for (int k = 0; k < iters; ++k) {
-    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
-    int i, j;
-    pick_positions(n, w.y, w.z, i, j);
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     Move mv;
-    mv.type = (uint64_t)w.x < swap_thr ? 1 : 2;
+    mv.type = (int)((pk >> 20) & 1u) + 1;
     mv.i = i;
     mv.j = j;
     mv.a = (int)div_b((uint32_t)min(i, j), sp.bmagic);
@@ -541,7 +542,7 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
       int klast;
       st.propose(mv, dn, dt, klast);
       const int64_t delta = dn * t_ref - dt;
-      acc = metropolis(delta, t_ref, T, w.w);
+      acc = metropolis(delta, t_ref, T, w3);
       if (acc) {
         st.apply_move(mv.type, i, j);
         for (int kk = mv.a + lane; kk <= klast; kk += kWave) st.cur[kk] = st.cand[kk];

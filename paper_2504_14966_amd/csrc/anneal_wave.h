@@ -394,20 +394,10 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
   double T = T0;
-  // lane l holds the proposal of iteration k0 + l, drawn 64 at a time: i | j << 10 |
-  // (type - 1) << 20 | a << 21 | c << 26 (n <= 1024, at most 32 batches), and word 3
-  uint32_t mvpack = 0, w3v = 0;
+  ProposalStream ps;  // at most 32 batches: the batch indices travel with the move
   for (int k = 0; k < iters; ++k) {
-    const int l = k & (kWave - 1);
-    if (l == 0) {
-      const u32x4 w = philox4x32_10((uint32_t)(k + lane), (uint32_t)chain, 0u, kTagAnneal, key0, key1);
-      int pi, pj;
-      pick_positions(n, w.y, w.z, pi, pj);
-      const uint32_t a = div_b((uint32_t)min(pi, pj), sp.bmagic), c = div_b((uint32_t)max(pi, pj), sp.bmagic);
-      mvpack = (uint32_t)pi | ((uint32_t)pj << 10) | (((uint64_t)w.x < swap_thr ? 0u : 1u) << 20) | (a << 21) | (c << 26);
-      w3v = w.w;
-    }
-    const uint32_t pk = readlane(mvpack, l), w3 = readlane(w3v, l);
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, sp.bmagic);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     Move mv;
     mv.type = (int)((pk >> 20) & 1u) + 1;

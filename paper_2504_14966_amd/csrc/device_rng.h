@@ -90,4 +90,33 @@ __device__ __forceinline__ void pick_positions(int n, uint32_t w1, uint32_t w2, 
   j = jp + (jp >= i ? 1 : 0);
 }
 
+// Proposals drawn 64 iterations at a time: lane l computes the Philox block of iteration
+// k0 + l (counter (k0 + l, chain, 0, kTagAnneal)) and keeps the move packed as
+// i | j << 10 | (type - 1) << 20, and, when a batch-index magic is given (at most 32
+// batches), a << 21 | c << 26 with a and c the batches of min(i, j) and max(i, j); each
+// iteration reads its move and acceptance word with v_readlane. Needs n <= 1024.
+struct ProposalStream {
+  uint32_t pk = 0, w3 = 0;
+  __device__ __forceinline__ void refill(int k0, int lane, int n, uint32_t chain, uint32_t key0, uint32_t key1,
+                                         uint64_t swap_thr, uint64_t bmagic) {
+    const u32x4 w = philox4x32_10((uint32_t)(k0 + lane), chain, 0u, kTagAnneal, key0, key1);
+    int i, j;
+    pick_positions(n, w.y, w.z, i, j);
+    pk = (uint32_t)i | ((uint32_t)j << 10) | (((uint64_t)w.x < swap_thr ? 0u : 1u) << 20);
+    if (bmagic) {
+      const uint32_t a = (uint32_t)(((uint64_t)(uint32_t)min(i, j) * bmagic) >> 32);
+      const uint32_t c = (uint32_t)(((uint64_t)(uint32_t)max(i, j) * bmagic) >> 32);
+      pk |= (a << 21) | (c << 26);
+    }
+    w3 = w.w;
+  }
+  // the move of iteration k (refilled when k % 64 == 0)
+  __device__ __forceinline__ uint32_t packed(int k) const {
+    return (uint32_t)__builtin_amdgcn_readlane((int)pk, k & 63);
+  }
+  __device__ __forceinline__ uint32_t word3(int k) const {
+    return (uint32_t)__builtin_amdgcn_readlane((int)w3, k & 63);
+  }
+};
+
 }  // namespace sa

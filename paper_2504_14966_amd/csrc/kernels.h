@@ -208,14 +208,15 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
   double T = T0;
+  ProposalStream ps;
   for (int k = 0; k < iters; ++k) {
-    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
-    int i, j;
-    pick_positions(n, w.y, w.z, i, j);
-    const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+    const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
     const Score s = replay_any<false>(m, req, cur, rm, stage, nullptr);
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
-    const bool acc = metropolis(delta, t_ref, T, w.w);
+    const bool acc = metropolis(delta, t_ref, T, w3);
     if (acc) {
       for (int p = lane; p < n; p += kWave) cand[p] = cur[rm.src(p)];
       wave_sync_lds();
@@ -292,15 +293,16 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
   double T = T0;
+  ProposalStream ps;
   for (int k = 0; k < iters; ++k) {
-    const u32x4 w = philox4x32_10((uint32_t)k, (uint32_t)chain, 0u, kTagAnneal, key0, key1);
-    int i, j;
-    pick_positions(n, w.y, w.z, i, j);
-    const Remap rm{(uint64_t)w.x < swap_thr ? 1 : 2, i, j};
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+    const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
     const Score s = LS ? replay_cont_ls<false>(m, req, perm, rm, scratch, nullptr)
                        : replay_cont_fast<false>(m, req, perm, rm, nullptr);
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
-    const bool acc = metropolis(delta, t_ref, T, w.w);
+    const bool acc = metropolis(delta, t_ref, T, w3);
     if (acc) {
       apply_move_lds(perm, i == j ? 0 : rm.kind, i, j, lane);
       cn = s.n;
