@@ -72,9 +72,29 @@ __device__ __forceinline__ double fast_exp_neg(double x) {
 // Metropolis rule for a maximisation with energy n - t / t_ref, scaled by t_ref so that
 // delta is an exact integer: keep any candidate that is not worse; keep a worse one
 // iff u < e^(delta / (t_ref * T)), u = w3 * 2^-32.
+//
+// Most worse candidates are decided by a single-precision screen: with xl an estimate of
+// x log2(e) (x = delta / (t_ref T)) and lu one of log2(u), g = xl - lu estimates
+// log2(e^x / u). The estimates carry a relative error below 2^-20 (xl: four roundings and
+// a 1-ulp reciprocal) and an absolute error below 2^-16 (lu: the 1-ulp hardware log2 of a
+// value below 32 in magnitude, and the rounding of w3), and fast_exp_neg is within a few
+// double ulps of e^x, so |g| > |xl| 2^-16 + 2^-10 fixes the sign of log2(E / u) with
+// E = fast_exp_neg(x), i.e. the exact decision u < E. Candidates inside that band, w3 = 0,
+// and denominators outside [1e-30, 1e30] take the double-precision rule itself. The
+// screen needs xl > lu + 2^-10 >= -32 to accept, far above the -708 cutoff of
+// fast_exp_neg, so its acceptances never fall where E = 0.
 __device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
   if (delta >= 0) return true;
-  const double x = (double)delta / ((double)t_ref * T);
+  const double den = (double)t_ref * T;
+  if (w3 != 0u && den > 1e-30 && den < 1e30) {
+    const float xl = (float)delta * __builtin_amdgcn_rcpf((float)den) * 1.44269504f;
+    const float lu = __builtin_amdgcn_logf((float)w3) - 32.0f;
+    const float g = xl - lu;
+    const float tau = fabsf(xl) * 1.52587890625e-5f + 9.765625e-4f;
+    if (g > tau) return true;
+    if (g < -tau) return false;
+  }
+  const double x = (double)delta / den;
   const double u = (double)w3 * (1.0 / 4294967296.0);
   return u < fast_exp_neg(x);
 }
