@@ -187,6 +187,13 @@ __device__ __forceinline__ uint64_t rl64(uint64_t v, int l) {
   return ((uint64_t)rl((uint32_t)(v >> 32), l) << 32) | rl((uint32_t)v, l);
 }
 
+// median of three unsigned values (c wave-uniform)
+__device__ __forceinline__ uint32_t med3_u32(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t d;
+  asm("v_med3_u32 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "s"(c));
+  return d;
+}
+
 // Per-wave LDS scratch of the list-scheduling replay (bytes, 8-aligned).
 __host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) {
   return ((size_t)4 * n + 4 * 3 * (size_t)(n + 1) + 7) / 8 * 8 + (size_t)16 * (n + 1);
@@ -224,9 +231,38 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   uint32_t list = lane < n0 ? runpre[lane] : kInf;
   wave_sync_lds();
 
-  // list scheduling: pop the earliest finish, admit the next position at that step. The
-  // list shifted down one lane (sh) merged with the new key nk is, lane by lane,
-  // sh < nk ? sh : (list < nk ? nk : list), since the popped minimum is below nk.
+  // list scheduling: pop the earliest finish, admit the next position at that step.
+  if (n0 <= 32) {
+    // Sliding window: before step t of a chunk lanes [0, t) hold the keys popped so far
+    // and lanes [t, t + n0) the running keys, sorted, with kInf above. Popping list[t] and
+    // inserting nk leaves lane i = median(list[i - 1], list[i], nk) for every lane: below
+    // t the medians return the pops unchanged (they are sorted and below nk), at t the pop
+    // itself, above t the merge of the remaining keys with nk. After S = 64 - n0 steps
+    // the pops are stored and the window moves back to lane 0.
+    for (int done = 0; done < nadm;) {
+      const int S = min(kWave - n0, nadm - done);
+      uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
+      if (lane < S) {
+        const int p = n0 + done + lane;
+        LP = ((req[perm[rm.src(p)]].x >> 16) << 10) | (uint32_t)p;
+      }
+      uint32_t top = __builtin_amdgcn_readfirstlane(list);
+      for (int t = 0; t < S; ++t) {
+        const uint32_t nk = (top & ~1023u) + rl(LP, t);
+        const uint32_t below = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)list, kDppWaveShr1, 0xF, 0xF, true);
+        list = med3_u32(below, list, nk);
+        top = rl(list, t + 1);
+      }
+      if (lane < S) ev[done + lane] = list;
+      const uint32_t moved = (uint32_t)__builtin_amdgcn_ds_bpermute((lane + S) << 2, (int)list);
+      list = lane < n0 ? moved : kInf;
+      done += S;
+    }
+  } else {
+  // With the list sorted, lane i of the list after the pop and the insert of nk is the
+  // median of list[i], list[i + 1] and nk, i.e. max(list[i], min(list[i + 1], nk)). The
+  // popped keys enter lane 0 of a second register that moves up one lane per step, so
+  // after a chunk of cnt steps lane cnt - 1 - t holds the pop of step t.
   for (int c0 = 0; c0 < nadm; c0 += kWave) {
     const int cnt = min(kWave, nadm - c0);
     uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
@@ -234,16 +270,17 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
       const int p = n0 + c0 + lane;
       LP = ((req[perm[rm.src(p)]].x >> 16) << 10) | (uint32_t)p;
     }
-    uint32_t evbuf = 0;
+    uint32_t evq = 0;
     uint32_t top = __builtin_amdgcn_readfirstlane(list);
     for (int t = 0; t < cnt; ++t) {
       const uint32_t nk = (top & ~1023u) + rl(LP, t);
-      evbuf = lane == t ? top : evbuf;
+      evq = dpp_old<kDppWaveShr1, 0xF>(list, evq);  // lane 0 takes list[0], the key popped now
       const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
-      list = sh < nk ? sh : (list < nk ? nk : list);
+      list = max(list, min(sh, nk));
       top = __builtin_amdgcn_readfirstlane(list);
     }
-    if (lane < cnt) ev[c0 + lane] = evbuf;
+    if (lane < cnt) ev[c0 + cnt - 1 - lane] = evq;
+  }
   }
   if (lane < n0) ev[nadm + lane] = list;
   if (lane == 0) preA[0] = 0u;

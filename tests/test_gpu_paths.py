@@ -52,6 +52,10 @@ CASES = {
     # continuous, list scheduling with ties (equal output lengths) and B > n
     "cont_ls_ties": (lambda r: _queue(r, 40, 16, 64, 5, 7, 3_000_000), Model(16, 1, 2000, 40, 8000, 300, 2), 16, 400),
     "cont_ls_b_gt_n": (lambda r: _queue(r, 20, 16, 2048, 8, 200, 3_000_000), Model(32, 1, 2000, 40, 8000, 300, 2), 8, 300),
+    # continuous, list scheduling with more than 32 running requests (one-lane pop register
+    # instead of the sliding window), including a full 64-lane list
+    "cont_ls_b48": (lambda r: _queue(r, 100, 16, 2048, 4, 200, 3_000_000), Model(48, 1, 2000, 40, 8000, 300, 2), 8, 300),
+    "cont_ls_b64": (lambda r: _queue(r, 150, 16, 2048, 4, 200, 3_000_000), Model(64, 1, 2000, 40, 8000, 300, 2), 8, 200),
 }
 
 
