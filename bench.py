@@ -79,8 +79,8 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 189.06 KiB x 2.0 + WRITE_SIZE 16,665.4 KiB x 1.0, burst workload, one launch
-    "482311857c729ddd67a6505e147f7f52efdcd5c106ad68e2de95812e0b0e2707": 17452495,
+    # FETCH_SIZE 179.9 KiB x 2.0 + WRITE_SIZE 16,685.4 KiB x 1.0, burst workload, one launch
+    "ab90f59315f60758414de071a86233f75961a12d4ab72e342d85afc7adca5ae2": 17454289,
 }
 
 
