@@ -84,6 +84,13 @@ TRAFFIC_BY_SOURCE = {
 }
 
 
+# VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
+# the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
+VALU_BUSY_BY_SOURCE = {
+    "ab90f59315f60758414de071a86233f75961a12d4ab72e342d85afc7adca5ae2": 0.693,
+}
+
+
 def kernel_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
@@ -96,6 +103,10 @@ def kernel_source_hash() -> str:
 
 def measured_traffic():
     return TRAFFIC_BY_SOURCE.get(kernel_source_hash())
+
+
+def measured_valu_busy():
+    return VALU_BUSY_BY_SOURCE.get(kernel_source_hash())
 
 
 def time_anneal(sl, W, steps, warmup, torch):
@@ -169,6 +180,57 @@ def cpu_baseline(wl: int, chains_per_core: int, iters: int):
                        f"{cores} worker processes, {wall:.1f} s wall ({total / sum(per):.0f} chain-iters/s per core)")
 
 
+# Oracle samples per workload (chains x iterations, or evaluation rows), as planned for the
+# CPU baseline: whole chains of every annealing workload and the first 65,536 rows of the
+# evaluation workload, plus the exhaustive search of the 8-request queue.
+CPU_SAMPLES = {1: dict(chains=1), 2: dict(chains=64), 3: dict(chains=16), 4: dict(chains=16), 5: dict(rows=65536)}
+
+
+def _oracle_sample_job(args):
+    import oracle
+    from paper_2504_14966_amd.workloads import workload
+    wl, lo, hi = args
+    W = workload(wl)
+    if W.eval_rows:
+        perms = oracle.fy_perms(W.perm_seed, W.queue.n, hi - lo, row0=lo)
+        t = time.perf_counter()
+        oracle.eval_rows(W.queue, W.model, perms)
+        return time.perf_counter() - t
+    info = oracle.start(W.queue, W.model)
+    t = time.perf_counter()
+    for c in range(lo, hi):
+        oracle.anneal_chain(W.queue, W.model, c, W.iters, W.T0, W.alpha, W.seed, start_info=info)
+    return time.perf_counter() - t
+
+
+def cpu_all(cores: int) -> dict:
+    """Oracle rates on every workload's sample: single-core and all-core (work / wall)."""
+    import multiprocessing as mp
+    import oracle
+    from paper_2504_14966_amd.workloads import workload
+    oracle.build(force=False)
+    out = {}
+    with mp.get_context("spawn").Pool(cores) as pool:
+        for wl, smp in CPU_SAMPLES.items():
+            W = workload(wl)
+            units = smp.get("rows") or smp["chains"]
+            per = max(1, -(-units // cores))
+            jobs = [(wl, lo, min(units, lo + per)) for lo in range(0, units, per)]
+            t = time.perf_counter()
+            per_t = pool.map(_oracle_sample_job, jobs)
+            wall = time.perf_counter() - t
+            work = units if W.eval_rows else units * W.iters
+            unit = "evals/s" if W.eval_rows else "chain-iters/s"
+            out[W.name] = dict(unit=unit, work=work, one_core=work / sum(per_t), all_cores=work / wall,
+                               processes=len(jobs), wall_s=wall)
+            log(f"[bench] oracle {W.name}: {work / sum(per_t):.4g} {unit} per core, {work / wall:.4g} on {len(jobs)} processes")
+        W1 = workload(1)
+        t = time.perf_counter()
+        oracle.brute(W1.queue, W1.model)
+        out["brute_force_n8"] = dict(unit="s", orders=40320, seconds=time.perf_counter() - t)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -178,6 +240,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the other workloads")
     ap.add_argument("--cpu-chains-per-core", type=int, default=8)
+    ap.add_argument("--cpu-all", action="store_true",
+                    help="also time the oracle on every workload's sample (adds about a minute)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one 256 MiB device-to-device copy (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -220,7 +284,7 @@ def main():
         extras["eval_workload"] = dict(workload=W5.name, rows=W5.eval_rows, evals_per_s=W5.eval_rows / wall5,
                                        kernel_ms=k5)
         log(f"[bench] eval {W5.eval_rows / wall5:.4g} evals/s ({k5:.2f} ms per 2^20 rows)")
-        for wl in (2, 3):
+        for wl in (1, 2, 3):
             if wl == args.workload:
                 continue
             Wx = workload(wl)
@@ -229,6 +293,12 @@ def main():
             log(f"[bench] {Wx.name}: {Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({kx[0]:.1f} ms)")
 
     cpu = None
+    if args.cpu_all:
+        try:
+            ncores = max(1, min(len(os.sched_getaffinity(0)), 16))
+        except AttributeError:
+            ncores = max(1, min(os.cpu_count() or 1, 16))
+        extras["oracle_all_workloads"] = cpu_all(ncores)
     if not args.no_cpu:
         log("[bench] CPU oracle baseline ...")
         cpu = cpu_baseline(args.workload, args.cpu_chains_per_core, W.iters)
@@ -252,6 +322,7 @@ def main():
                    "iters": W.iters, "T0": W.T0, "alpha": W.alpha, "parallelism": "chains"},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": measured_traffic(),
+                     "rocprof_valu_busy": measured_valu_busy(),
                      "kernel": "anneal_wave_kernel", "kernel_ms": k_ms,
                      "algo_lane_ops_per_chain_iter": work["ops"], "work_per_chain_iter": work},
         "cpu_baseline": cpu,
