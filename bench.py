@@ -30,12 +30,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-# Algorithmic int32 lane-ops of the delta algorithm (static admission):
-#   per member of a batch whose membership changes: two doubled pair costs of 3 ops each
-#   (minimum, two 24-bit multiply-adds), the newcomer's pair cost (3), the offset update
-#   (3), the slack and SLO test (4), and one combining op in each of the six per-batch
-#   reductions (newcomer sum, duration max, two sums of offsets, two slack bounds) = 22;
-#   per batch whose start only shifts: one bounds check of 4 ops.
+# Algorithmic work per proposal, the method's per-unit figure: a proposal re-evaluates the
+# requests from the first changed batch onward; a request whose batch changed membership
+# costs about 90 int32 lane-ops (its finish offset: rank among the batch by output length
+# and the segment sums, then e2e, the SLO test and its reduction share), any other
+# re-evaluated request about 10 (e2e = start + offset, the SLO test, a reduction share). A
+# move inside one batch changes nothing and costs nothing.
+OPS_CHANGED_REQUEST = 90
+OPS_REEVALUATED_REQUEST = 10
+# The delta algorithm's own leaner count, reported beside it: per member of a changed batch
+# two doubled pair costs (3 ops each), the newcomer's pair cost (3), the offset update (3),
+# the slack and SLO test (4) and one op in each of six per-batch reductions = 22; per batch
+# whose start only shifts one bounds check of 4 ops.
 OPS_CHANGED_MEMBER = 22
 OPS_SHIFTED_BATCH = 4
 # Continuous admission (list scheduling): per admission 4 ops on each of the B list slots
@@ -45,8 +51,8 @@ OPS_CONT_PER_EVENT = 22
 
 
 def expected_work(W) -> dict:
-    """Expected work units of one proposal, averaged exactly over the proposal law
-    (i uniform, j uniform over the other positions, swap or insert by the swap threshold)."""
+    """Expected work of one proposal, averaged exactly over the proposal law (i uniform, j
+    uniform over the other positions, swap or insert by the swap threshold)."""
     n, B = W.queue.n, W.model.max_batch
     if W.model.policy != 0:
         b = min(B, n)
@@ -65,11 +71,15 @@ def expected_work(W) -> dict:
     # insert: batches a..c change, batches after c shift
     in_members = np.where(same, 0.0, csum[c + 1] - csum[a])
     in_shift = np.where(same, 0.0, M - 1 - c)
+    # requests from the start of the first changed batch onward
+    reeval = np.where(same, 0.0, n - csum[a])
     p_swap = min(W.model.swap_threshold, 1 << 32) / float(1 << 32)
     members = p_swap * sw_members.mean() + (1 - p_swap) * in_members.mean()
     shifted = p_swap * sw_shift.mean() + (1 - p_swap) * in_shift.mean()
-    return dict(changed_members=members, shifted_batches=shifted,
-                ops=OPS_CHANGED_MEMBER * members + OPS_SHIFTED_BATCH * shifted)
+    reevaluated = reeval.mean()
+    return dict(changed_members=members, reevaluated_requests=reevaluated, shifted_batches=shifted,
+                ops=OPS_CHANGED_REQUEST * members + OPS_REEVALUATED_REQUEST * (reevaluated - members),
+                delta_algorithm_ops=OPS_CHANGED_MEMBER * members + OPS_SHIFTED_BATCH * shifted)
 
 
 # HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
@@ -323,6 +333,8 @@ def main():
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": measured_traffic(),
                      "rocprof_valu_busy": measured_valu_busy(),
+                     "delta_algorithm_frac": (work.get("delta_algorithm_ops", 0.0) * chain_iters / (k_ms * 1e-3))
+                                             / PEAK_LANE_OPS,
                      "kernel": "anneal_wave_kernel", "kernel_ms": k_ms,
                      "algo_lane_ops_per_chain_iter": work["ops"], "work_per_chain_iter": work},
         "cpu_baseline": cpu,
