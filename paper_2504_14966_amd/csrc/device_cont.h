@@ -18,6 +18,8 @@
 // are selects rather than branches. Every event retires at least one request, so at most
 // n events occur.
 #pragma once
+#include <type_traits>
+
 #include "device_common.h"
 #include "device_replay.h"
 
@@ -194,14 +196,24 @@ __device__ __forceinline__ uint32_t med3_u32(uint32_t a, uint32_t b, uint32_t c)
   return d;
 }
 
-// Per-wave LDS scratch of the list-scheduling replay (bytes, 8-aligned).
-__host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) {
-  return ((size_t)4 * n + 4 * 3 * (size_t)(n + 1) + 7) / 8 * 8 + (size_t)16 * (n + 1);
-}
+// Per-wave LDS scratch of the list-scheduling replay (bytes, 16-aligned): event keys,
+// prefill prefix sums, run starts, run-end prefills (4 B per event), segment-cost prefix
+// sums and TTFTs (8 B per event), and the candidate order's request records by position.
+__host__ __device__ __forceinline__ size_t cont_ls_off_seg(int n) { return ((size_t)4 * n + 12 * (size_t)(n + 1) + 7) / 8 * 8; }
+__host__ __device__ __forceinline__ size_t cont_ls_off_pos(int n) { return (cont_ls_off_seg(n) + 16 * (size_t)(n + 1) + 15) / 16 * 16; }
+__host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) { return cont_ls_off_pos(n) + 16 * (size_t)n; }
 
-template <bool DETAIL>
+__device__ __forceinline__ uint32_t scan_add(uint32_t v) { return scan_add32(v); }
+__device__ __forceinline__ uint64_t scan_add(uint64_t v) { return scan_add64(v); }
+__device__ __forceinline__ uint32_t rl_any(uint32_t v, int l) { return rl(v, l); }
+__device__ __forceinline__ uint64_t rl_any(uint64_t v, int l) { return rl64(v, l); }
+
+// NARROW: every time on the timeline fits 32 bits (the host bounds the total by
+// sum(prefill) + (d0 + d1) sum(l_out) + d2 sum(l_out l_in + l_out (l_out + 1) / 2)).
+template <bool DETAIL, bool NARROW>
 __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm, Remap rm,
                                 unsigned char *scratch, int64_t *detail) {
+  using TT = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
   const int lane = lane_id();
   const int N = m.n, B = m.B;
   const int n0 = min(B, N), nadm = N - n0;
@@ -210,19 +222,24 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   uint32_t *preA = ev + N;                                // PRE_k at [k], PRE_0 = 0
   uint32_t *rsA = preA + (N + 1);                         // run start of event k at [k]
   uint32_t *runpre = rsA + (N + 1);                       // PRE at the end of the run starting at k
-  uint64_t *segA = reinterpret_cast<uint64_t *>(scratch + ((size_t)4 * N + 4 * 3 * (size_t)(N + 1) + 7) / 8 * 8);
-  uint64_t *tta = segA + (N + 1);                         // TTFT of the request admitted at event k
+  TT *segA = reinterpret_cast<TT *>(scratch + cont_ls_off_seg(N));
+  TT *tta = segA + (N + 1);                               // TTFT of the request admitted at event k
+  uint4 *posr = reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(N));  // record of the request at position p
   constexpr uint32_t kInf = 0xFFFFFFFFu;
+
+  // the candidate order's records, once, so later lookups by position are one LDS read
+  for (int p = lane; p < N; p += kWave) posr[p] = req[perm[rm.src(p)]];
+  wave_sync_lds();
 
   // initial group: positions 0 .. n0-1 start at step 0
   uint32_t key = kInf, lin0 = 0, pf0 = 0;
   if (lane < n0) {
-    const uint4 rq = req[perm[rm.src(lane)]];
+    const uint4 rq = posr[lane];
     key = ((rq.x >> 16) << 10) | (uint32_t)lane;
     lin0 = rq.x & 0xFFFFu;
     pf0 = rq.w;
   }
-  const uint64_t PR0 = wsum32(pf0);
+  const TT PR0 = (TT)wsum32(pf0);
   const uint32_t C1 = wsum32(lin0);
   int rank = 0;
   for (int u = 0; u < n0; ++u) rank += rl(key, u) < key ? 1 : 0;
@@ -244,7 +261,7 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
       uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
       if (lane < S) {
         const int p = n0 + done + lane;
-        LP = ((req[perm[rm.src(p)]].x >> 16) << 10) | (uint32_t)p;
+        LP = ((posr[p].x >> 16) << 10) | (uint32_t)p;
       }
       uint32_t top = __builtin_amdgcn_readfirstlane(list);
       for (int t = 0; t < S; ++t) {
@@ -259,28 +276,28 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
       done += S;
     }
   } else {
-  // With the list sorted, lane i of the list after the pop and the insert of nk is the
-  // median of list[i], list[i + 1] and nk, i.e. max(list[i], min(list[i + 1], nk)). The
-  // popped keys enter lane 0 of a second register that moves up one lane per step, so
-  // after a chunk of cnt steps lane cnt - 1 - t holds the pop of step t.
-  for (int c0 = 0; c0 < nadm; c0 += kWave) {
-    const int cnt = min(kWave, nadm - c0);
-    uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
-    if (lane < cnt) {
-      const int p = n0 + c0 + lane;
-      LP = ((req[perm[rm.src(p)]].x >> 16) << 10) | (uint32_t)p;
+    // With the list sorted, lane i of the list after the pop and the insert of nk is the
+    // median of list[i], list[i + 1] and nk, i.e. max(list[i], min(list[i + 1], nk)). The
+    // popped keys enter lane 0 of a second register that moves up one lane per step, so
+    // after a chunk of cnt steps lane cnt - 1 - t holds the pop of step t.
+    for (int c0 = 0; c0 < nadm; c0 += kWave) {
+      const int cnt = min(kWave, nadm - c0);
+      uint32_t LP = 0;
+      if (lane < cnt) {
+        const int p = n0 + c0 + lane;
+        LP = ((posr[p].x >> 16) << 10) | (uint32_t)p;
+      }
+      uint32_t evq = 0;
+      uint32_t top = __builtin_amdgcn_readfirstlane(list);
+      for (int t = 0; t < cnt; ++t) {
+        const uint32_t nk = (top & ~1023u) + rl(LP, t);
+        evq = dpp_old<kDppWaveShr1, 0xF>(list, evq);  // lane 0 takes list[0], the key popped now
+        const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
+        list = max(list, min(sh, nk));
+        top = __builtin_amdgcn_readfirstlane(list);
+      }
+      if (lane < cnt) ev[c0 + cnt - 1 - lane] = evq;
     }
-    uint32_t evq = 0;
-    uint32_t top = __builtin_amdgcn_readfirstlane(list);
-    for (int t = 0; t < cnt; ++t) {
-      const uint32_t nk = (top & ~1023u) + rl(LP, t);
-      evq = dpp_old<kDppWaveShr1, 0xF>(list, evq);  // lane 0 takes list[0], the key popped now
-      const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
-      list = max(list, min(sh, nk));
-      top = __builtin_amdgcn_readfirstlane(list);
-    }
-    if (lane < cnt) ev[c0 + cnt - 1 - lane] = evq;
-  }
   }
   if (lane < n0) ev[nadm + lane] = list;
   if (lane == 0) preA[0] = 0u;
@@ -288,7 +305,7 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
 
   // pass A: segment costs, prefills, run starts and their prefix sums
   uint32_t fcarry = 0, Ccarry = C1, precarry = 0, rscarry = 0;
-  uint64_t segcarry = 0;
+  TT segcarry = 0;
   for (int c0 = 0; c0 < N; c0 += kWave) {
     const int k = c0 + lane + 1;
     const bool v = k <= N;
@@ -298,23 +315,18 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     const uint32_t fprev = dpp_old<kDppWaveShr1, 0xF>(fcarry, f);
     const uint32_t s = v ? f - fprev : 0u;
     const uint32_t b = (uint32_t)min(n0, N - k + 1);
-    uint32_t outq = 0, la = 0, pfa = 0;
-    if (v) {
-      const uint4 rq = req[perm[rm.src(q)]];
-      outq = (rq.x & 0xFFFFu) + (rq.x >> 16);
-    }
     const bool adm = v && k <= nadm;
-    if (adm) {
-      const uint4 ra = req[perm[rm.src(n0 + k - 1)]];
-      la = ra.x & 0xFFFFu;
-      pfa = ra.w;
-    }
+    const uint4 rq = posr[v ? q : 0];
+    const uint4 ra = posr[adm ? n0 + k - 1 : 0];
+    const uint32_t outq = v ? (rq.x & 0xFFFFu) + (rq.x >> 16) : 0u;
+    const uint32_t la = adm ? (ra.x & 0xFFFFu) : 0u, pfa = adm ? ra.w : 0u;
     const uint32_t dC = v ? b * s - outq + la : 0u;  // two's complement: a signed change
     const uint32_t dCi = scan_add32(dC);
     const uint32_t Ck = Ccarry + dCi - dC;
-    const uint64_t seg = v ? (uint64_t)s * (d0 + d1 * b + d2 * Ck) + (uint64_t)(d2 * b) * ((s * (s + 1u)) >> 1) : 0ull;
-    const uint64_t SEG = segcarry + scan_add64(seg);
-    const uint32_t PRE = precarry + scan_add32(adm ? pfa : 0u);
+    TT seg = 0;
+    if (v) seg = (TT)s * (TT)(d0 + d1 * b + d2 * Ck) + (TT)(d2 * b) * (TT)((s * (s + 1u)) >> 1);
+    const TT SEG = segcarry + scan_add(seg);
+    const uint32_t PRE = precarry + scan_add32(pfa);
     const uint32_t rs = max(rscarry, scan_max32((v && (k == 1 || s != 0)) ? (uint32_t)k : 0u));
     const uint32_t fnext = k < N ? (ev[k] >> 10) : kInf;
     if (v) {
@@ -325,7 +337,7 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     }
     fcarry = rl(f, kWave - 1);
     Ccarry += rl(dCi, kWave - 1);
-    segcarry = rl64(SEG, kWave - 1);
+    segcarry = rl_any(SEG, kWave - 1);
     precarry = rl(PRE, kWave - 1);
     rscarry = rl(rs, kWave - 1);
   }
@@ -338,24 +350,24 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     const int k = c0 + lane + 1;
     const bool v = k <= N;
     uint32_t q = 0, rsk = 1;
-    uint64_t SEG = 0;
+    TT SEG = 0;
     if (v) {
       q = ev[k - 1] & 1023u;
       rsk = rsA[k];
       SEG = segA[k];
     }
-    const uint64_t e2e = PR0 + SEG + (rsk > 1 ? preA[rsk - 1] : 0u);
-    if (v && k <= nadm) tta[k] = PR0 + SEG + runpre[rsk];
+    const TT e2e = PR0 + SEG + (TT)(rsk > 1 ? preA[rsk - 1] : 0u);
+    if (v && k <= nadm) tta[k] = PR0 + SEG + (TT)runpre[rsk];
     wave_sync_lds();
     bool met = false;
     if (v) {
-      const int r = perm[rm.src((int)q)];
-      const uint4 rq = req[r];
-      const uint64_t ttft = (int)q < n0 ? PR0 : tta[q - n0 + 1];
+      const uint4 rq = posr[q];
+      const TT ttft = (int)q < n0 ? PR0 : tta[q - n0 + 1];
       const uint32_t kind = rq.z & 3u, thr = rq.y, L = rq.x >> 16;
-      met = kind == 0 ? ttft <= (uint64_t)thr : (kind == 2 ? e2e <= (uint64_t)thr : e2e - ttft <= (uint64_t)thr * L);
-      tsum += e2e;
+      met = kind == 0 ? ttft <= (TT)thr : (kind == 2 ? e2e <= (TT)thr : (uint64_t)(e2e - ttft) <= (uint64_t)thr * L);
+      tsum += (uint64_t)e2e;
       if (DETAIL) {
+        const int r = perm[rm.src((int)q)];
         detail[2 * r] = (int64_t)ttft;
         detail[2 * r + 1] = (int64_t)e2e;
       }

@@ -58,8 +58,8 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
   load_requests(q, m, req);
   __syncthreads();
   const int lane = lane_id();
-  for (int64_t row = (int64_t)blockIdx.x * kWavesPerBlock + wave; row < rows;
-       row += (int64_t)gridDim.x * kWavesPerBlock) {
+  const int waves = blockDim.x >> 6;
+  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
     const uint16_t *src = perms + row * n;
     if (lane < 32) bitmap[lane] = 0u;
     wave_sync_lds();
@@ -84,7 +84,8 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
       continue;
     }
     int64_t *drow = DETAIL ? detail + row * n * 2 : nullptr;
-    const Score s = ls ? replay_cont_ls<DETAIL>(m, req, perm, Remap{0, 0, 0}, scratch, drow)
+    const Score s = ls ? ((m.flags & kFlagNarrowTime) ? replay_cont_ls<DETAIL, true>(m, req, perm, Remap{0, 0, 0}, scratch, drow)
+                                                      : replay_cont_ls<DETAIL, false>(m, req, perm, Remap{0, 0, 0}, scratch, drow))
                        : replay_any<DETAIL>(m, req, perm, Remap{0, 0, 0}, stage, drow);
     if (lane == 0) {
       out[2 * row] = s.n;
@@ -299,7 +300,8 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
-    const Score s = LS ? replay_cont_ls<false>(m, req, perm, rm, scratch, nullptr)
+    const Score s = LS ? ((m.flags & kFlagNarrowTime) ? replay_cont_ls<false, true>(m, req, perm, rm, scratch, nullptr)
+                                                      : replay_cont_ls<false, false>(m, req, perm, rm, scratch, nullptr))
                        : replay_cont_fast<false>(m, req, perm, rm, nullptr);
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
     const bool acc = metropolis(delta, t_ref, T, w3);

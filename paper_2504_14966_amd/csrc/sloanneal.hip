@@ -112,12 +112,29 @@ bool list_sched_ok(const HostQueue &h, const sched_model_t *m, int n) {
   return n <= 1024 && lsum < 4194304.0L && pfsum < 4294967296.0L;
 }
 
-sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false) {
+// Continuous admission: every time on the timeline is at most the sum of the prefills plus
+// the decode steps' costs, sum over steps of d0 + d1 b + d2 C. There are at most sum(l_out)
+// steps, the b terms add up to sum(l_out) and the C terms to sum(l_out l_in + l_out (l_out
+// + 1) / 2), whatever the order.
+bool timeline_narrow(const HostQueue &h, const sched_model_t *m, int n) {
+  long double pf = 0, L = 0, ctx = 0;
+  for (int r = 0; r < n; ++r) {
+    const long double lo = h.out_len[r], li = h.in_len[r];
+    pf += (long double)m->p0 + (long double)m->p1 * li;
+    L += lo;
+    ctx += lo * li + lo * (lo + 1) / 2;
+  }
+  return pf + ((long double)m->d0 + (long double)m->d1) * L + (long double)m->d2 * ctx < 4294967296.0L;
+}
+
+sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false,
+                       bool narrow_time = false) {
   sa::DevModel d;
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
-  d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0);
+  d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0) |
+            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0);
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
@@ -130,10 +147,10 @@ sa::QueuePtrs dev_queue(const sched_queue_t *q) {
   return sa::QueuePtrs{q->in_len, q->out_len, q->kind, q->thr_us};
 }
 
-size_t eval_lds_bytes(int n, bool ls) {
+size_t eval_lds_bytes(int n, bool ls, int waves) {
   const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 + 64 * 16 + 32 * 4 +
                           (ls ? (sa::cont_ls_scratch_bytes(n) + 15) / 16 * 16 : 0);
-  return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
+  return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * waves;
 }
 
 // The delta kernel keeps finish offsets, prefills, slacks and doubled pair costs in 32
@@ -213,9 +230,8 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n));
-  const int64_t want = (k + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
-  const int grid = (int)std::min<int64_t>(want, 256 * 32);
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
+                                    timeline_narrow(h, model, n));
   if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     int lg = 0;
     while ((1 << lg) < model->max_batch) ++lg;
@@ -246,16 +262,21 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
     if (e != hipSuccess) return hip_fail(e);
     return SCHED_OK;
   }
-  const size_t lds = eval_lds_bytes(n, dm.policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagListSched));
+  // one order per wave, up to four waves per workgroup as the LDS allows
+  const bool ls = dm.policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagListSched);
+  int waves = sa::kWavesPerBlock;
+  while (waves > 1 && eval_lds_bytes(n, ls, waves) > (size_t)max_lds_per_block()) waves >>= 1;
+  const size_t lds = eval_lds_bytes(n, ls, waves);
+  const int grid = (int)std::min<int64_t>((k + waves - 1) / waves, 256 * 32);
   if (lds > 65536) {
     HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(detail ? (const void *)&sa::eval_kernel<true>
                                                                       : (const void *)&sa::eval_kernel<false>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
   }
   if (detail) {
-    sa::eval_kernel<true><<<grid, sa::kBlock, lds, stream>>>(dm, dev_queue(queue), perms, k, out, detail);
+    sa::eval_kernel<true><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), perms, k, out, detail);
   } else {
-    sa::eval_kernel<false><<<grid, sa::kBlock, lds, stream>>>(dm, dev_queue(queue), perms, k, out, nullptr);
+    sa::eval_kernel<false><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), perms, k, out, nullptr);
   }
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
@@ -279,7 +300,8 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if ((rc = fetch_queue(queue, stream, h))) return rc;
   if ((rc = range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n));
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
+                                    timeline_narrow(h, model, n));
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
   HIP_TRY(hipGetLastError());

@@ -56,6 +56,8 @@ CASES = {
     # instead of the sliding window), including a full 64-lane list
     "cont_ls_b48": (lambda r: _queue(r, 100, 16, 2048, 4, 200, 3_000_000), Model(48, 1, 2000, 40, 8000, 300, 2), 8, 300),
     "cont_ls_b64": (lambda r: _queue(r, 150, 16, 2048, 4, 200, 3_000_000), Model(64, 1, 2000, 40, 8000, 300, 2), 8, 200),
+    # continuous, list scheduling with a timeline longer than 2^32 us (64-bit segment sums)
+    "cont_ls_wide_time": (lambda r: _queue(r, 40, 16, 2048, 20000, 60000, 4_000_000_000), Model(8, 1, 2000, 40, 8000, 300, 2), 4, 60),
 }
 
 
