@@ -93,7 +93,8 @@ def test_workload_4_full(sl, orc):
 
 @pytest.mark.parametrize("n,B,policy,thr", [(1, 1, 0, 1 << 31), (2, 3, 1, 1 << 31), (9, 3, 0, 0), (9, 3, 1, 1 << 32),
                                             (17, 5, 0, 1 << 31), (40, 40, 0, 1 << 31), (70, 6, 1, 3 << 30),
-                                            (130, 64, 0, 1 << 30), (200, 13, 1, 1 << 31)])
+                                            (130, 64, 0, 1 << 30), (200, 13, 1, 1 << 31), (300, 33, 0, 1 << 31),
+                                            (1000, 50, 0, 3 << 30)])
 def test_random_small_chains(sl, orc, n, B, policy, thr):
     rng = np.random.default_rng(n * 31 + B)
     q = random_queue(rng, n, max_in=3000, max_out=120, thr_hi=50_000 * n)
