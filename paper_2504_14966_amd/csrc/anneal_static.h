@@ -144,6 +144,47 @@ struct Seg {
     }
     return v;
   }
+  // the same reductions taken two or three at a time, step by step, so that the DPP steps
+  // of one fill the wait states of the other
+  static constexpr int kSteps = LG;  // quad, quad, half-row, row, then one or two row broadcasts
+  template <class Op>
+  __device__ static __forceinline__ uint32_t step(uint32_t v, int s) {
+    switch (s) {
+      case 0: return Op::f(v, dpp<kQuadXor1>(v));
+      case 1: return Op::f(v, dpp<kQuadXor2>(v));
+      case 2: return Op::f(v, dpp<kRowHalfMirror>(v));
+      case 3: return Op::f(v, dpp<kRowMirror>(v));
+      case 4: return Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x142, 0xA, 0xF, false));
+      default: return Op::f(v, (uint32_t)__builtin_amdgcn_update_dpp((int)Op::identity, (int)v, 0x143, 0xC, 0xF, false));
+    }
+  }
+  __device__ static __forceinline__ uint32_t finish(uint32_t v, int lane) {
+    if constexpr (LG == 5) return lane < 32 ? readlane(v, 31) : readlane(v, 63);
+    if constexpr (LG == 6) return readlane(v, 63);
+    return v;
+  }
+  template <class O1, class O2>
+  __device__ static __forceinline__ void all2(uint32_t &a, uint32_t &b, int lane) {
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      a = step<O1>(a, s);
+      b = step<O2>(b, s);
+    }
+    a = finish(a, lane);
+    b = finish(b, lane);
+  }
+  template <class O1, class O2, class O3>
+  __device__ static __forceinline__ void all3(uint32_t &a, uint32_t &b, uint32_t &c, int lane) {
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      a = step<O1>(a, s);
+      b = step<O2>(b, s);
+      c = step<O3>(c, s);
+    }
+    a = finish(a, lane);
+    b = finish(b, lane);
+    c = finish(c, lane);
+  }
   // exact sum of 32-bit values as two 16-bit-half sums (each below 2^22)
   __device__ static __forceinline__ uint64_t sum_wide(uint32_t v, int lane) {
     const uint32_t lo = all<OpAdd>(v & 0xFFFFu, lane), hi = all<OpAdd>(v >> 16, lane);
@@ -268,8 +309,9 @@ struct StaticChain {
         Pn = Pc;
       }
       if (seg_changed && valid) F[rn] = Fc;
-      const uint32_t Dm = Seg<LG>::template all<OpMax>(Fn, lane);
-      const uint64_t SFm = Seg<LG>::sum_wide(Fn, lane);
+      uint32_t Dm = Fn, SFlo = Fn & 0xFFFFu, SFhi = Fn >> 16;
+      Seg<LG>::template all3<OpMax, OpAdd, OpAdd>(Dm, SFlo, SFhi, lane);
+      const uint64_t SFm = (uint64_t)SFlo + ((uint64_t)SFhi << 16);
       if (seg_changed) {
         Dn = Dm;
         SFn = SFm;
@@ -284,8 +326,9 @@ struct StaticChain {
     const Slack x = slack_of(rq.kind, rq.thr, rq.L, Pn, Fn);
     const bool met = in_range && slack_met(x, Sn);
     const int cnt = Seg<LG>::count(met, seg);
-    const uint32_t A = Seg<LG>::template all<OpMin>((in_range && met && !x.always) ? x.s : 0xFFFFFFFFu, lane);
-    const uint32_t Bv = Seg<LG>::template all<OpMax>((in_range && !met && !x.never) ? x.s + 1u : 0u, lane);
+    uint32_t A = (in_range && met && !x.always) ? x.s : 0xFFFFFFFFu;
+    uint32_t Bv = (in_range && !met && !x.never) ? x.s + 1u : 0u;
+    Seg<LG>::template all2<OpMin, OpMax>(A, Bv, lane);
     if (mm == 0 && seg_live) {
       dn_l += (int64_t)cnt - (int64_t)br.cnt;
       if (add_dt) dt_l += (int64_t)batch_size(k) * shift + (int64_t)(SFn - br.SF);
