@@ -203,6 +203,37 @@ __host__ __device__ __forceinline__ size_t cont_ls_off_seg(int n) { return ((siz
 __host__ __device__ __forceinline__ size_t cont_ls_off_pos(int n) { return (cont_ls_off_seg(n) + 16 * (size_t)(n + 1) + 15) / 16 * 16; }
 __host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) { return cont_ls_off_pos(n) + 16 * (size_t)n; }
 
+// Kept by the annealing kernel between proposals when min(B, n) <= 32 (sliding window):
+// the current order's admission pops, the running keys at the start of every window chunk
+// and its initial group, plus the same for the candidate. A candidate that changes only
+// positions >= lo keeps the current order's first admissions, so its replay restarts at
+// the window chunk holding admission lo - n0 from that chunk's running keys.
+struct LsCache {
+  uint32_t *ev_cur, *ev_cand;      // n pops each
+  uint32_t *snap_cur, *snap_cand;  // running keys at the start of chunk c, at [32 c + lane]
+  uint32_t list0_cur, list0_cand;  // initial group's sorted keys (lanes < n0), kInf above
+  uint32_t pr0_cur, pr0_cand;      // its prefill sum
+  uint32_t c1_cur, c1_cand;        // its context sum
+  int lo;                          // first position the candidate changes
+  __device__ __forceinline__ void accept() {
+    uint32_t *t = ev_cur;
+    ev_cur = ev_cand;
+    ev_cand = t;
+    t = snap_cur;
+    snap_cur = snap_cand;
+    snap_cand = t;
+    list0_cur = list0_cand;
+    pr0_cur = pr0_cand;
+    c1_cur = c1_cand;
+  }
+};
+// LDS for one LsCache: two pop arrays and two snapshot arrays
+__host__ __device__ __forceinline__ size_t cont_inc_bytes(int n, int B) {
+  const int n0 = n < B ? n : B, nadm = n - n0;
+  const size_t chunks = nadm > 0 ? (size_t)((nadm + (64 - n0) - 1) / (64 - n0)) : 0;
+  return 2 * (((size_t)4 * n + 15) / 16 * 16) + 2 * chunks * 32 * 4;
+}
+
 __device__ __forceinline__ uint32_t scan_add(uint32_t v) { return scan_add32(v); }
 __device__ __forceinline__ uint64_t scan_add(uint64_t v) { return scan_add64(v); }
 __device__ __forceinline__ uint32_t rl_any(uint32_t v, int l) { return rl(v, l); }
@@ -210,16 +241,16 @@ __device__ __forceinline__ uint64_t rl_any(uint64_t v, int l) { return rl64(v, l
 
 // NARROW: every time on the timeline fits 32 bits (the host bounds the total by
 // sum(prefill) + (d0 + d1) sum(l_out) + d2 sum(l_out l_in + l_out (l_out + 1) / 2)).
-template <bool DETAIL, bool NARROW>
+template <bool DETAIL, bool NARROW, bool INC = false>
 __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm, Remap rm,
-                                unsigned char *scratch, int64_t *detail) {
+                                unsigned char *scratch, int64_t *detail, LsCache *cache = nullptr) {
   using TT = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
   const int lane = lane_id();
   const int N = m.n, B = m.B;
   const int n0 = min(B, N), nadm = N - n0;
   const uint32_t d0 = (uint32_t)m.d0, d1 = (uint32_t)m.d1, d2 = (uint32_t)m.d2;
-  uint32_t *ev = reinterpret_cast<uint32_t *>(scratch);  // packed key of event k at [k - 1]
-  uint32_t *preA = ev + N;                                // PRE_k at [k], PRE_0 = 0
+  uint32_t *ev = INC ? cache->ev_cand : reinterpret_cast<uint32_t *>(scratch);  // key of event k at [k - 1]
+  uint32_t *preA = reinterpret_cast<uint32_t *>(scratch) + N;  // PRE_k at [k], PRE_0 = 0
   uint32_t *rsA = preA + (N + 1);                         // run start of event k at [k]
   uint32_t *runpre = rsA + (N + 1);                       // PRE at the end of the run starting at k
   TT *segA = reinterpret_cast<TT *>(scratch + cont_ls_off_seg(N));
@@ -231,22 +262,36 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   for (int p = lane; p < N; p += kWave) posr[p] = req[perm[rm.src(p)]];
   wave_sync_lds();
 
-  // initial group: positions 0 .. n0-1 start at step 0
-  uint32_t key = kInf, lin0 = 0, pf0 = 0;
-  if (lane < n0) {
-    const uint4 rq = posr[lane];
-    key = ((rq.x >> 16) << 10) | (uint32_t)lane;
-    lin0 = rq.x & 0xFFFFu;
-    pf0 = rq.w;
+  // initial group: positions 0 .. n0-1 start at step 0 (kept from the current order when
+  // the candidate changes no position below n0)
+  uint32_t list, pr0u, C1;
+  if (INC && cache->lo >= n0) {
+    list = cache->list0_cur;
+    pr0u = cache->pr0_cur;
+    C1 = cache->c1_cur;
+  } else {
+    uint32_t key = kInf, lin0 = 0, pf0 = 0;
+    if (lane < n0) {
+      const uint4 rq = posr[lane];
+      key = ((rq.x >> 16) << 10) | (uint32_t)lane;
+      lin0 = rq.x & 0xFFFFu;
+      pf0 = rq.w;
+    }
+    pr0u = wsum32(pf0);
+    C1 = wsum32(lin0);
+    int rank = 0;
+    for (int u = 0; u < n0; ++u) rank += rl(key, u) < key ? 1 : 0;
+    if (lane < n0) runpre[rank] = key;
+    wave_sync_lds();
+    list = lane < n0 ? runpre[lane] : kInf;
+    wave_sync_lds();
   }
-  const TT PR0 = (TT)wsum32(pf0);
-  const uint32_t C1 = wsum32(lin0);
-  int rank = 0;
-  for (int u = 0; u < n0; ++u) rank += rl(key, u) < key ? 1 : 0;
-  if (lane < n0) runpre[rank] = key;
-  wave_sync_lds();
-  uint32_t list = lane < n0 ? runpre[lane] : kInf;
-  wave_sync_lds();
+  if (INC) {
+    cache->list0_cand = list;
+    cache->pr0_cand = pr0u;
+    cache->c1_cand = C1;
+  }
+  const TT PR0 = (TT)pr0u;
 
   // list scheduling: pop the earliest finish, admit the next position at that step.
   if (n0 <= 32) {
@@ -256,8 +301,20 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     // t the medians return the pops unchanged (they are sorted and below nk), at t the pop
     // itself, above t the merge of the remaining keys with nk. After S = 64 - n0 steps
     // the pops are stored and the window moves back to lane 0.
-    for (int done = 0; done < nadm;) {
-      const int S = min(kWave - n0, nadm - done);
+    const int Sfull = kWave - n0;
+    int done = 0;
+    if (INC) {
+      // the candidate's admissions before the chunk holding its first change are the
+      // current order's: copy their pops and chunk-start keys, restart from that chunk
+      const int cr = cache->lo >= n0 ? (cache->lo - n0) / Sfull : 0;
+      done = min(cr * Sfull, nadm);
+      for (int x = lane; x < done; x += kWave) cache->ev_cand[x] = cache->ev_cur[x];
+      for (int x = lane; x < cr * 32; x += kWave) cache->snap_cand[x] = cache->snap_cur[x];
+      if (done > 0) list = lane < n0 ? cache->snap_cur[cr * 32 + lane] : kInf;
+    }
+    while (done < nadm) {
+      const int S = min(Sfull, nadm - done);
+      if (INC && lane < n0) cache->snap_cand[(done / Sfull) * 32 + lane] = list;
       uint32_t LP = 0;  // (l_out << 10) | position of the positions admitted in this chunk
       if (lane < S) {
         const int p = n0 + done + lane;

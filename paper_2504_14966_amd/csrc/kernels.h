@@ -266,7 +266,11 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const int wave = uniform((int)(threadIdx.x >> 6));
-  const size_t per_wave = lds_align((size_t)n * 2) + (LS ? lds_align(cont_ls_scratch_bytes(n)) : 0);
+  // with at most 32 running requests the list-scheduling replay restarts at the first
+  // changed admission, keeping the current order's pops and chunk-start keys
+  const bool inc = LS && min(m.B, n) <= 32;
+  const size_t ls_b = LS ? lds_align(cont_ls_scratch_bytes(n)) : 0;
+  const size_t per_wave = lds_align((size_t)n * 2) + ls_b + (inc ? cont_inc_bytes(n, m.B) : 0);
   uint16_t *perm = reinterpret_cast<uint16_t *>(lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave);
   unsigned char *scratch = reinterpret_cast<unsigned char *>(perm) + lds_align((size_t)n * 2);
   load_requests(q, m, req);
@@ -289,6 +293,23 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     gbest[p] = v;
   }
   wave_sync_lds();
+  const bool narrow_t = (m.flags & kFlagNarrowTime) != 0;
+  LsCache cache{};
+  if (inc) {
+    unsigned char *ib = scratch + ls_b;
+    const size_t evb = ((size_t)4 * n + 15) / 16 * 16, snapb = (cont_inc_bytes(n, m.B) - 2 * evb) / 2;
+    cache.ev_cur = reinterpret_cast<uint32_t *>(ib);
+    cache.ev_cand = reinterpret_cast<uint32_t *>(ib + evb);
+    cache.snap_cur = reinterpret_cast<uint32_t *>(ib + 2 * evb);
+    cache.snap_cand = reinterpret_cast<uint32_t *>(ib + 2 * evb + snapb);
+    // the start order's state
+    cache.lo = 0;
+    if (narrow_t)
+      replay_cont_ls<false, true, true>(m, req, perm, Remap{0, 0, 0}, scratch, nullptr, &cache);
+    else
+      replay_cont_ls<false, false, true>(m, req, perm, Remap{0, 0, 0}, scratch, nullptr, &cache);
+    cache.accept();
+  }
   int64_t bn = cn;
   uint64_t bt = ct;
   int64_t biter = -1, accepts = 0;
@@ -300,13 +321,21 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
-    const Score s = LS ? ((m.flags & kFlagNarrowTime) ? replay_cont_ls<false, true>(m, req, perm, rm, scratch, nullptr)
-                                                      : replay_cont_ls<false, false>(m, req, perm, rm, scratch, nullptr))
-                       : replay_cont_fast<false>(m, req, perm, rm, nullptr);
+    Score s;
+    if (inc) {
+      cache.lo = min(i, j);
+      s = narrow_t ? replay_cont_ls<false, true, true>(m, req, perm, rm, scratch, nullptr, &cache)
+                   : replay_cont_ls<false, false, true>(m, req, perm, rm, scratch, nullptr, &cache);
+    } else {
+      s = LS ? (narrow_t ? replay_cont_ls<false, true>(m, req, perm, rm, scratch, nullptr)
+                         : replay_cont_ls<false, false>(m, req, perm, rm, scratch, nullptr))
+             : replay_cont_fast<false>(m, req, perm, rm, nullptr);
+    }
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
     const bool acc = metropolis(delta, t_ref, T, w3);
     if (acc) {
       apply_move_lds(perm, i == j ? 0 : rm.kind, i, j, lane);
+      if (inc) cache.accept();
       cn = s.n;
       ct = s.t;
       ++accepts;

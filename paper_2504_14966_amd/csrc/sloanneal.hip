@@ -354,7 +354,9 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
     const bool ls = (dm.flags & sa::kFlagListSched) != 0;
     const size_t soa = (size_t)n * 16;
-    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0);
+    const bool inc = ls && std::min(model->max_batch, n) <= 32;
+    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0) +
+                       (inc ? sa::cont_inc_bytes(n, model->max_batch) : 0);
     const int cus = std::max(1, cu_count());
     const int lim = max_lds_per_block();
     int waves = 1;
