@@ -209,6 +209,8 @@ __host__ __device__ __forceinline__ size_t cont_ls_scratch_bytes(int n) { return
 // positions >= lo keeps the current order's first admissions, so its replay restarts at
 // the window chunk holding admission lo - n0 from that chunk's running keys.
 struct LsCache {
+  // with a cache the records by position (in the scratch) are the candidate order's: the
+  // kernel applies each move to them and takes it back on reject
   uint32_t *ev_cur, *ev_cand;      // n pops each
   uint32_t *snap_cur, *snap_cand;  // running keys at the start of chunk c, at [32 c + lane]
   uint32_t list0_cur, list0_cand;  // initial group's sorted keys (lanes < n0), kInf above
@@ -258,9 +260,12 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   uint4 *posr = reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(N));  // record of the request at position p
   constexpr uint32_t kInf = 0xFFFFFFFFu;
 
-  // the candidate order's records, once, so later lookups by position are one LDS read
-  for (int p = lane; p < N; p += kWave) posr[p] = req[perm[rm.src(p)]];
-  wave_sync_lds();
+  // the candidate order's records, so later lookups by position are one LDS read (kept by
+  // the annealing kernel, which applies each move to them, when a cache is given)
+  if (!INC) {
+    for (int p = lane; p < N; p += kWave) posr[p] = req[perm[rm.src(p)]];
+    wave_sync_lds();
+  }
 
   // initial group: positions 0 .. n0-1 start at step 0 (kept from the current order when
   // the candidate changes no position below n0)

@@ -48,10 +48,11 @@ struct Score {
 // Apply a move (1 swap, 2 insert: remove at i, re-insert at j) to an order in LDS, in place,
 // by one wave. Inserts shift the positions between i and j in chunks of 64, each chunk
 // read completely before it is written.
-__device__ __forceinline__ void apply_move_lds(uint16_t *perm, int type, int i, int j, int lane) {
+template <typename T>
+__device__ __forceinline__ void apply_move_lds(T *perm, int type, int i, int j, int lane) {
   if (type == 1) {
     if (lane == 0) {
-      const uint16_t x = perm[i];
+      const T x = perm[i];
       perm[i] = perm[j];
       perm[j] = x;
     }
@@ -59,10 +60,10 @@ __device__ __forceinline__ void apply_move_lds(uint16_t *perm, int type, int i, 
     // shift the positions between i and j by one towards i, 4 x 64 positions per round:
     // the reads of a round cover positions the round's writes do not reach, so one wait
     // per round suffices (LDS accesses of a wave execute in order)
-    const uint16_t x = perm[i];
+    const T x = perm[i];
     if (i < j) {
       for (int c0 = i; c0 < j; c0 += 4 * kWave) {
-        uint16_t v[4];
+        T v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = perm[min(c0 + u * kWave + lane + 1, j)];
 #pragma unroll
@@ -73,7 +74,7 @@ __device__ __forceinline__ void apply_move_lds(uint16_t *perm, int type, int i, 
       }
     } else {
       for (int c0 = i; c0 > j; c0 -= 4 * kWave) {
-        uint16_t v[4];
+        T v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = perm[max(c0 - u * kWave - lane - 1, j)];
 #pragma unroll

@@ -302,7 +302,10 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     cache.ev_cand = reinterpret_cast<uint32_t *>(ib + evb);
     cache.snap_cur = reinterpret_cast<uint32_t *>(ib + 2 * evb);
     cache.snap_cand = reinterpret_cast<uint32_t *>(ib + 2 * evb + snapb);
-    // the start order's state
+    // the start order's records by position and its state
+    uint4 *posr = reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(n));
+    for (int p = lane; p < n; p += kWave) posr[p] = req[perm[p]];
+    wave_sync_lds();
     cache.lo = 0;
     if (narrow_t)
       replay_cont_ls<false, true, true>(m, req, perm, Remap{0, 0, 0}, scratch, nullptr, &cache);
@@ -323,6 +326,7 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
     Score s;
     if (inc) {
+      apply_move_lds(reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(n)), i == j ? 0 : rm.kind, i, j, lane);
       cache.lo = min(i, j);
       s = narrow_t ? replay_cont_ls<false, true, true>(m, req, perm, rm, scratch, nullptr, &cache)
                    : replay_cont_ls<false, false, true>(m, req, perm, rm, scratch, nullptr, &cache);
@@ -333,6 +337,7 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
     }
     const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
     const bool acc = metropolis(delta, t_ref, T, w3);
+    if (inc && !acc) apply_move_lds(reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(n)), i == j ? 0 : rm.kind, j, i, lane);
     if (acc) {
       apply_move_lds(perm, i == j ? 0 : rm.kind, i, j, lane);
       if (inc) cache.accept();
