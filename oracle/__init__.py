@@ -17,7 +17,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = ("replay.c", "rng.c", "anneal.c")
+_SRCS = ("replay.c", "rng.c", "anneal.c", "sized.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", "-Wno-unused-parameter"]
@@ -78,6 +78,22 @@ def lib():
         L.orc_brute.restype = i64
         L.orc_solo.argtypes = [vp, vp, i32]
         L.orc_solo.restype = i64
+        L.orc_check_starts.argtypes = [vp, i32, i32]
+        L.orc_check_starts.restype = C.c_int
+        L.orc_max_starts.argtypes = [i32, i32, vp]
+        L.orc_replay_batches.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_replay_batches.restype = C.c_int
+        L.orc_eval_rows_batches.argtypes = [vp, vp, vp, vp, i64, i64, vp]
+        L.orc_squeeze.argtypes = [vp, vp, i32, i32, i32]
+        L.orc_squeeze.restype = C.c_int
+        L.orc_delay.argtypes = [vp, vp, i32, i32, i32]
+        L.orc_delay.restype = C.c_int
+        L.orc_op3.argtypes = [u32]
+        L.orc_op3.restype = C.c_int
+        L.orc_anneal_chain_batches.argtypes = [vp, vp, vp, i64, C.c_int, i32, i32, dbl, dbl, u64,
+                                               vp, vp, vp, vp, vp, vp]
+        L.orc_brute_batches.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.orc_brute_batches.restype = i64
         _lib = L
     return _lib
 
@@ -220,3 +236,96 @@ def brute(queue, model):
 def better(k1, k2) -> bool:
     """Score order: attainment first, then lower total latency."""
     return k1[0] > k2[0] or (k1[0] == k2[0] and k1[1] < k2[1])
+
+
+# ---- joint search over order and batch sizes (sized.c) ----
+
+def check_starts(starts, n: int, B: int) -> bool:
+    st = np.ascontiguousarray(starts, dtype=np.uint8)
+    return bool(lib().orc_check_starts(_p(st), int(n), int(B)))
+
+
+def max_starts(n: int, B: int) -> np.ndarray:
+    st = np.zeros(n, np.uint8)
+    lib().orc_max_starts(int(n), int(B), _p(st))
+    return st
+
+
+def replay_batches(queue, model, perm, starts, detail: bool = False):
+    """(n_met, t_sum) of one order with explicit batches; (-1, -1) for an invalid row."""
+    a = _Args(queue, model)
+    perm = np.ascontiguousarray(perm, dtype=np.uint16)
+    st = np.ascontiguousarray(starts, dtype=np.uint8)
+    nm, ts = C.c_int64(), C.c_int64()
+    ttft = np.zeros(a.n, np.int64)
+    e2e = np.zeros(a.n, np.int64)
+    lib().orc_replay_batches(a.qp, a.mp, _p(perm), _p(st), C.byref(nm), C.byref(ts), _p(ttft), _p(e2e))
+    if detail:
+        return nm.value, ts.value, ttft, e2e
+    return nm.value, ts.value
+
+
+def eval_rows_batches(queue, model, perms: np.ndarray, starts: np.ndarray) -> np.ndarray:
+    a = _Args(queue, model)
+    perms = np.ascontiguousarray(perms, dtype=np.uint16)
+    st = np.ascontiguousarray(starts, dtype=np.uint8)
+    assert perms.shape == st.shape
+    out = np.zeros((perms.shape[0], 2), np.int64)
+    lib().orc_eval_rows_batches(a.qp, a.mp, _p(perms), _p(st), 0, perms.shape[0], _p(out))
+    return out
+
+
+def squeeze(perm, starts, B: int, i: int):
+    """(made, order, starts) after squeezeLastIter at position i."""
+    p = np.array(perm, dtype=np.uint16)
+    st = np.array(starts, dtype=np.uint8)
+    made = lib().orc_squeeze(_p(p), _p(st), int(p.shape[0]), int(B), int(i))
+    return bool(made), p, st
+
+
+def delay(perm, starts, B: int, i: int):
+    """(made, order, starts) after delayNextIter at position i."""
+    p = np.array(perm, dtype=np.uint16)
+    st = np.array(starts, dtype=np.uint8)
+    made = lib().orc_delay(_p(p), _p(st), int(p.shape[0]), int(B), int(i))
+    return bool(made), p, st
+
+
+def op3(w0: int) -> int:
+    return int(lib().orc_op3(int(w0)))
+
+
+def anneal_chain_batches(queue, model, chain: int, iters: int, T0: float, alpha: float, seed: int,
+                         start_info=None, trace: bool = False) -> dict:
+    """One chain of the joint order / batch-size search."""
+    a = _Args(queue, model)
+    if start_info is None:
+        start_info = start(queue, model)
+    st, t_ref, allmet = start_info[0], start_info[1], start_info[2]
+    st = np.ascontiguousarray(st, dtype=np.uint16)
+    cur = np.zeros(a.n, np.uint16)
+    best = np.zeros(a.n, np.uint16)
+    cst = np.zeros(a.n, np.uint8)
+    bst = np.zeros(a.n, np.uint8)
+    rec = np.zeros(8, np.int64)
+    tr = np.zeros((iters, 4), np.int64) if trace else None
+    lib().orc_anneal_chain_batches(a.qp, a.mp, _p(st), int(t_ref), int(allmet), int(chain), int(iters),
+                                   float(T0), float(alpha), int(seed), _p(cur), _p(cst), _p(best), _p(bst),
+                                   _p(rec), _p(tr) if trace else None)
+    out = dict(cur=cur, cur_starts=cst, best=best, best_starts=bst, rec=rec)
+    if trace:
+        out["trace"] = tr
+    return out
+
+
+def brute_batches(queue, model):
+    """(best_n, best_t, first optimal order, its starts, number of optimal pairs) over every
+    order and every batch layout."""
+    a = _Args(queue, model)
+    if a.n > 8:
+        raise ValueError("the joint brute force is limited to n <= 8")
+    bn, bt = C.c_int64(), C.c_int64()
+    bp = np.zeros(a.n, np.uint16)
+    bs = np.zeros(a.n, np.uint8)
+    cnt = lib().orc_brute_batches(a.qp, a.mp, C.byref(bn), C.byref(bt), _p(bp), _p(bs))
+    return bn.value, bt.value, bp, bs, int(cnt)

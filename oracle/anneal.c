@@ -8,8 +8,8 @@
  *   - one proposal per iteration, cooled geometrically: T_k = T0 * alpha^k, formed by
  *     one fp64 multiply per iteration;
  *   - proposals: swap two positions (randSwapping) or remove one request and re-insert
- *     it elsewhere; the two batch-boundary moves of the paper are not part of this
- *     path because batches are formed by the admission policy;
+ *     it elsewhere; batches are formed by the admission policy. The joint search over
+ *     order and batch sizes with the paper's squeeze / delay moves is in sized.c;
  *   - acceptance: see orc_accept (rng.c); equal scores are accepted;
  *   - score order: (n1, t1) beats (n2, t2) iff n1 > n2, or n1 == n2 and t1 < t2
  *     (attainment first, then mean latency);

@@ -25,7 +25,10 @@
 #include <stdint.h>
 
 enum { ORC_TTFT = 0, ORC_TPOT = 1, ORC_E2E = 2 };
-enum { ORC_STATIC = 0, ORC_CONTINUOUS = 1 };
+/* ORC_STATIC_SEARCH: static admission whose batch sizes are searched together with the
+ * order (batch-size sequence of the Problem Formulation, squeeze / delay moves of
+ * Algorithm 1). Replayed with maximum-size batches it is ORC_STATIC. */
+enum { ORC_STATIC = 0, ORC_CONTINUOUS = 1, ORC_STATIC_SEARCH = 2 };
 enum { ORC_TAG_ANNEAL = 0x53414e4e, ORC_TAG_FY = 0x46495348 };
 
 typedef struct {
@@ -98,5 +101,55 @@ int64_t orc_brute(const orc_queue *q, const orc_model *m, int64_t *best_n, int64
 
 /* Solo latency of one request (its replay alone). */
 int64_t orc_solo(const orc_queue *q, const orc_model *m, int32_t r);
+
+/* ---- joint search over order and batch sizes (sized.c) ----
+ * starts: one flag per position, 1 where a batch begins; starts[0] = 1 and every batch
+ * holds at most max_batch requests. */
+
+/* 1 iff starts is a valid batch layout of n positions with batches of at most B. */
+int orc_check_starts(const uint8_t *starts, int32_t n, int32_t B);
+
+/* Maximum-size layout: a batch starts at every multiple of B. */
+void orc_max_starts(int32_t n, int32_t B, uint8_t *starts);
+
+/* Step-by-step static timeline with the given batches (batch index from the cumulated
+ * batch sizes, waiting time = earlier batch durations). Returns -1 and (-1, -1) when perm
+ * is not a permutation or starts is not a valid layout. Pinned by hand-worked timelines
+ * with unequal batch sizes, by orc_replay for maximum-size layouts, by the batch-size-1
+ * closed form, and by within-batch order invariance. */
+int orc_replay_batches(const orc_queue *q, const orc_model *m, const uint16_t *perm,
+                       const uint8_t *starts, int64_t *n_met, int64_t *t_sum, int64_t *ttft,
+                       int64_t *e2e);
+
+/* Rows of k x n orders and k x n layouts; out is k x 2 (n_met, t_sum) or (-1, -1). */
+void orc_eval_rows_batches(const orc_queue *q, const orc_model *m, const uint16_t *perms,
+                           const uint8_t *starts, int64_t row0, int64_t rows, int64_t *out);
+
+/* squeezeLastIter / delayNextIter at position i, in place. Return 1 if the move is
+ * allowed and made, 0 (arrays untouched) otherwise. Pinned by worked examples and by
+ * layout validity over random sequences of moves. */
+int orc_squeeze(uint16_t *perm, uint8_t *starts, int32_t n, int32_t B, int32_t i);
+int orc_delay(uint16_t *perm, uint8_t *starts, int32_t n, int32_t B, int32_t i);
+
+/* Move choice of the joint search: floor(w0 * 3 / 2^32): 0 squeeze, 1 delay, 2 swap. */
+int orc_op3(uint32_t w0);
+
+/* One chain of the joint search: the start order of orc_start with maximum-size batches;
+ * each iteration draws the Philox block of orc_anneal_chain, picks the move by orc_op3
+ * (position i from w1 for squeeze and delay; i, j from w1, w2 for swap) and applies the
+ * acceptance test of orc_accept. A move that is not allowed changes nothing and is not
+ * counted as accepted. trace (nullable): iters x 4 int64 (accepted, n, t, move | 4 if not
+ * allowed). Parity unpinned (trajectory). */
+void orc_anneal_chain_batches(const orc_queue *q, const orc_model *m, const uint16_t *start,
+                              int64_t t_ref, int allmet, int32_t chain, int32_t iters, double T0,
+                              double alpha, uint64_t seed, uint16_t *cur, uint8_t *cur_starts,
+                              uint16_t *best, uint8_t *best_starts, int64_t *rec, int64_t *trace);
+
+/* Exhaustive search over every order and every layout (n <= 8): the optimum key, the
+ * first optimal (order, layout) with orders in lexicographic order and, per order,
+ * layouts by increasing bit mask of the starts at positions 1 .. n-1; returns the number
+ * of optimal (order, layout) pairs. */
+int64_t orc_brute_batches(const orc_queue *q, const orc_model *m, int64_t *best_n, int64_t *best_t,
+                          uint16_t *best_perm, uint8_t *best_starts);
 
 #endif

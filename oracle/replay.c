@@ -45,7 +45,8 @@ int orc_replay(const orc_queue *q, const orc_model *m, const uint16_t *perm,
   int64_t t = 0;
   int32_t next = 0, b = 0;
   while (next < n || b > 0) {
-    int admit = next < n && (m->policy == ORC_STATIC ? b == 0 : b < B);
+    /* both static policies admit a new batch only when the previous one has drained */
+    int admit = next < n && (m->policy == ORC_CONTINUOUS ? b < B : b == 0);
     if (admit) {
       int32_t g = B - b;
       if (g > n - next) g = n - next;
