@@ -41,8 +41,12 @@ enum { SCHED_TTFT = 0, SCHED_TPOT = 1, SCHED_E2E = 2 };
 /* Admission policy. STATIC: consecutive groups of max_batch requests in priority order
  * form batches; a batch starts when the previous one has drained (batch index and
  * waiting time of the Problem Formulation). CONTINUOUS: a finished request frees its
- * slot, refilled from the priority order at the next iteration. */
-enum { SCHED_STATIC = 0, SCHED_CONTINUOUS = 1 };
+ * slot, refilled from the priority order at the next iteration. STATIC_SEARCH: static
+ * batches whose sizes (each 1 .. max_batch) are searched together with the order, the
+ * argmax over positions and batch indices of the Problem Formulation, explored by the
+ * squeeze and delay moves of Algorithm 1. Evaluated without a layout, and at the start
+ * of every chain, its batches have the maximum size, which makes it STATIC. */
+enum { SCHED_STATIC = 0, SCHED_CONTINUOUS = 1, SCHED_STATIC_SEARCH = 2 };
 
 #define SCHED_MAX_N 1024
 #define SCHED_MAX_BATCH 64
@@ -67,10 +71,11 @@ typedef struct {
  *   a request ends with its l_out-th decode iteration. */
 typedef struct {
   int32_t max_batch;        /* 1 .. SCHED_MAX_BATCH */
-  int32_t policy;           /* SCHED_STATIC or SCHED_CONTINUOUS */
+  int32_t policy;           /* SCHED_STATIC, SCHED_CONTINUOUS or SCHED_STATIC_SEARCH */
   int64_t p0, p1, d0, d1, d2;
   int64_t t_ref_us;         /* Metropolis latency scale; 0 => total latency of the input order */
-  uint64_t swap_threshold;  /* proposal is a swap iff Philox word 0 < this (0 .. 2^32); 2^31 = 50/50 */
+  uint64_t swap_threshold;  /* proposal is a swap iff Philox word 0 < this (0 .. 2^32); 2^31 = 50/50;
+                               unused by SCHED_STATIC_SEARCH, whose three moves are equally likely */
 } sched_model_t;
 
 /* Score K priority orders (objective of the Problem Formulation, kept as the integer
@@ -84,6 +89,21 @@ typedef struct {
  * the clock could overflow. k == 0 is a no-op. */
 int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
                int64_t k, int64_t *out, int64_t *detail, hipStream_t stream);
+
+/* Score K (order, batch layout) pairs under static admission with the given batches
+ * (batch-size sequence b_0 .. b_{M-1} of the Problem Formulation: the batch index of a
+ * position comes from the cumulated sizes, a batch waits for the previous one to drain).
+ *   perms  : k x n uint16, row-major priority orders, as for sched_eval
+ *   starts : k x n uint8, row-major; starts[r][p] = 1 where a batch begins at position p,
+ *            else 0. A valid layout has starts[r][0] = 1 and every batch at most
+ *            max_batch positions long
+ *   out    : k x 2 int64 (n_met, t_sum); (-1, -1) if the order is not a permutation or the
+ *            layout is not valid
+ *   detail : nullable; k x n x 2 int64 (ttft, e2e) by request id; invalid rows untouched
+ * model->policy must be SCHED_STATIC or SCHED_STATIC_SEARCH (SCHED_EINVAL otherwise);
+ * other errors as for sched_eval. */
+int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
+                       const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail, hipStream_t stream);
 
 /* Bytes of workspace sched_anneal needs for n requests and `chains` chains (0 on bad sizes). */
 size_t sched_ws_bytes(int32_t n, int32_t chains);
@@ -100,6 +120,16 @@ size_t sched_ws_bytes(int32_t n, int32_t chains);
  * (lowest chain id on ties) is reduced at the end.
  *   ws : DEVICE workspace of at least sched_ws_bytes(n, chains) bytes, 256-byte aligned;
  *        it holds the start order, per-chain records and orders after the call.
+ * With model->policy == SCHED_STATIC_SEARCH the state is the order and its batch layout
+ * (Algorithm 1's joint search): every chain starts from the start order with maximum-size
+ * batches, and proposal k picks move floor(w0 * 3 / 2^32): 0 squeezeLastIter (the request
+ * at position i = floor(w1 * n / 2^32) joins the batch before its own as its last member,
+ * allowed when its batch is not the first and the one before holds fewer than max_batch),
+ * 1 delayNextIter (it joins the batch after its own as its first member, allowed when that
+ * batch holds fewer than max_batch; from the last batch it opens a new one, allowed when
+ * it does not run alone), 2 a swap of positions i and j (as above). A move that is not
+ * allowed changes nothing and counts as neither accepted nor rejected (no digest step).
+ * Layouts are read back with sched_starts.
  * Returns SCHED_EINVAL for chains < 1, iters < 0, T0 <= 0, alpha <= 0 or non-finite,
  * a bad queue or model; SCHED_ENOSPC for a short workspace; SCHED_ERANGE on overflow risk. */
 int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t chains,
@@ -124,6 +154,16 @@ int sched_chains(const void *ws, int64_t *per_chain, uint16_t *cur_perms, uint16
  *   start_out : n uint16 (DEVICE); info_out : 4 int64 (DEVICE) = (t_ref, start n, start t,
  *               1 if the solo-latency order meets every SLO else 0). */
 int sched_start_info(const void *ws, uint16_t *start_out, int64_t *info_out, hipStream_t stream);
+
+/* Batch layouts of the last sched_anneal on ws with SCHED_STATIC_SEARCH (start flags,
+ * one uint8 per position as for sched_eval_batches). After a run with another policy every
+ * layout reads as the maximum-size one (a start at every multiple of max_batch). All
+ * outputs DEVICE and nullable, at least one given (SCHED_EINVAL otherwise):
+ *   cur_starts    : chains x n, each chain's final layout
+ *   best_starts   : chains x n, each chain's best-so-far layout
+ *   winner_starts : n, the layout of the best order over chains (the one sched_best returns) */
+int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint8_t *winner_starts,
+                 hipStream_t stream);
 
 /* Fill rows row0 .. row0+k-1 of a Fisher-Yates permutation family: row r shuffles 0..n-1
  * for positions p = n-1 down to 1 with j = (w * (p + 1)) >> 32, w = word (p mod 4) of the

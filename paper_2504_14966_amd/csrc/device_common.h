@@ -12,7 +12,7 @@ constexpr int kWave = 64;
 struct DevModel {
   int32_t n;       // requests
   int32_t B;       // max batch
-  int32_t policy;  // 0 static, 1 continuous
+  int32_t policy;  // 0 static, 1 continuous, 2 static with searched batch sizes
   int32_t flags;   // bit 0: continuous-admission event arithmetic fits 32 bits
   uint64_t p0, p1, d0, d1, d2;
 };
@@ -39,7 +39,8 @@ struct WsHeader {
   int32_t n, chains, iters, policy;
   int64_t t_ref, start_n, start_t, allmet;
   int64_t best_chain, best_n, best_t;
-  int64_t reserved[20];
+  int64_t max_batch;
+  int64_t reserved[19];
 };
 static_assert(sizeof(WsHeader) <= 256, "header fits its slot");
 constexpr int kFlagNarrowPrefill = 1;  // continuous event arithmetic fits 32 bits
@@ -59,8 +60,16 @@ __host__ __device__ __forceinline__ size_t ws_off_cur(int n, int chains) {
 __host__ __device__ __forceinline__ size_t ws_off_best(int n, int chains) {
   return ws_off_cur(n, chains) + (size_t)chains * ws_perm_stride(n) * 2;
 }
-__host__ __device__ __forceinline__ size_t ws_total(int n, int chains) {
+// batch layouts of the joint order / batch-size search: one start flag per position
+__host__ __device__ __forceinline__ size_t ws_flag_stride(int n) { return round_up((size_t)n, 256); }  // bytes
+__host__ __device__ __forceinline__ size_t ws_off_cur_starts(int n, int chains) {
   return ws_off_best(n, chains) + (size_t)chains * ws_perm_stride(n) * 2;
+}
+__host__ __device__ __forceinline__ size_t ws_off_best_starts(int n, int chains) {
+  return ws_off_cur_starts(n, chains) + (size_t)chains * ws_flag_stride(n);
+}
+__host__ __device__ __forceinline__ size_t ws_total(int n, int chains) {
+  return ws_off_best_starts(n, chains) + (size_t)chains * ws_flag_stride(n);
 }
 
 // ---- wavefront helpers (64 lanes) ----

@@ -229,7 +229,7 @@ __device__ Score replay_continuous(const DevModel &m, const uint4 *__restrict__ 
 template <bool DETAIL>
 __device__ __forceinline__ Score replay(const DevModel &m, const uint4 *req, const uint16_t *perm, Remap rm,
                                         uint4 *stage, int64_t *detail) {
-  if (m.policy == 0) return replay_static<DETAIL>(m, req, perm, rm, stage, detail);
+  if (m.policy != 1) return replay_static<DETAIL>(m, req, perm, rm, stage, detail);  // both static policies
   return replay_continuous<DETAIL>(m, req, perm, rm, detail);
 }
 

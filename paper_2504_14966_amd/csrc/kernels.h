@@ -33,7 +33,7 @@ __device__ __forceinline__ void load_requests(const QueuePtrs &q, const DevModel
 template <bool DETAIL>
 __device__ __forceinline__ Score replay_any(const DevModel &m, const uint4 *req, const uint16_t *perm, Remap rm,
                                             uint4 *stage, int64_t *detail) {
-  if (m.policy == 0) return replay_static<DETAIL>(m, req, perm, rm, stage, detail);
+  if (m.policy != 1) return replay_static<DETAIL>(m, req, perm, rm, stage, detail);  // both static policies
   if (m.flags & kFlagNarrowPrefill) return replay_cont_fast<DETAIL>(m, req, perm, rm, detail);
   return replay_continuous<DETAIL>(m, req, perm, rm, detail);
 }
@@ -159,6 +159,7 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
       h->chains = chains;
       h->iters = iters;
       h->policy = m.policy;
+      h->max_batch = m.B;
       h->t_ref = t_ref_user > 0 ? t_ref_user : (input.t > 1 ? (int64_t)input.t : 1);
       h->start_n = use_input ? input.n : sorted.n;
       h->start_t = (int64_t)(use_input ? input.t : sorted.t);

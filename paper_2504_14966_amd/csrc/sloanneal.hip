@@ -12,6 +12,7 @@
 #include "kernels.h"
 #include "anneal_static.h"
 #include "anneal_wave.h"
+#include "anneal_sized.h"
 
 namespace {
 
@@ -37,7 +38,7 @@ struct HostQueue {
 int check_model(const sched_model_t *m, int n) {
   if (!m) return SCHED_EINVAL;
   if (m->max_batch < 1 || m->max_batch > SCHED_MAX_BATCH) return SCHED_EINVAL;
-  if (m->policy != SCHED_STATIC && m->policy != SCHED_CONTINUOUS) return SCHED_EINVAL;
+  if (m->policy != SCHED_STATIC && m->policy != SCHED_CONTINUOUS && m->policy != SCHED_STATIC_SEARCH) return SCHED_EINVAL;
   if (m->p0 < 0 || m->p1 < 0 || m->d0 < 0 || m->d1 < 0 || m->d2 < 0 || m->t_ref_us < 0) return SCHED_EINVAL;
   if (m->swap_threshold > (1ull << 32)) return SCHED_EINVAL;
   (void)n;
@@ -209,6 +210,22 @@ hipError_t launch_static(int waves, size_t lds, const sa::DevModel &dm, const sa
   return hipGetLastError();
 }
 
+// Joint order / batch-size search: the full-replay kernel, one chain per wave, four per
+// workgroup.
+int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
+                 int chains, int iters, double T0, double alpha, uint64_t seed, unsigned char *w, hipStream_t stream) {
+  (void)h;
+  (void)model;
+  const int n = dm.n;
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb + 64 * 16);
+  const int grid = (chains + 3) / 4;
+  sa::anneal_sized_generic_kernel<<<grid, 256, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+                                                              (uint32_t)seed, (uint32_t)(seed >> 32), w);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
 size_t anneal_lds_bytes(int n) {
   const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 * 2 + 64 * 16;
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
@@ -232,7 +249,7 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   const int n = queue->n;
   const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
                                     timeline_narrow(h, model, n));
-  if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+  if (model->policy != SCHED_CONTINUOUS && static_narrow(h, model, n)) {
     int lg = 0;
     while ((1 << lg) < model->max_batch) ++lg;
     const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
@@ -306,7 +323,11 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
   HIP_TRY(hipGetLastError());
   bool done = false;
-  if (model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+  if (model->policy == SCHED_STATIC_SEARCH) {
+    if ((rc = launch_sized(h, model, dm, queue, chains, iters, T0, alpha, seed, w, stream))) return rc;
+    done = true;
+  }
+  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     // chains per workgroup: enough to spread the chains over every CU, at most 16 and
     // at most what the LDS holds
     int lg = 0;
@@ -419,6 +440,40 @@ int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t 
   if (!perms) return SCHED_EINVAL;
   const int64_t grid = (k + 255) / 256;
   sa::shuffle_kernel<<<(unsigned)grid, 256, 0, stream>>>((uint32_t)seed, (uint32_t)(seed >> 32), n, row0, k, perms);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
+                       const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail, hipStream_t stream) {
+  if (k < 0) return SCHED_EINVAL;
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  int rc = check_model(model, queue->n);
+  if (rc) return rc;
+  if (model->policy == SCHED_CONTINUOUS) return SCHED_EINVAL;
+  if (k > 0 && (!perms || !starts || !out)) return SCHED_EINVAL;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h))) return rc;
+  if ((rc = range_check(h, model, queue->n))) return rc;
+  if (k == 0) return SCHED_OK;
+  const int n = queue->n;
+  const sa::DevModel dm = dev_model(model, n, false);
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 64 * 16 + 32 * 4);
+  const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
+  if (detail)
+    sa::eval_sized_kernel<true><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), perms, starts, k, out, detail);
+  else
+    sa::eval_sized_kernel<false><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), perms, starts, k, out, nullptr);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint8_t *winner_starts,
+                 hipStream_t stream) {
+  if (!ws || (!cur_starts && !best_starts && !winner_starts)) return SCHED_EINVAL;
+  sa::starts_copy_kernel<<<256, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), cur_starts, best_starts,
+                                                  winner_starts);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }

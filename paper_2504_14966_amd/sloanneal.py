@@ -17,8 +17,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsloanneal.so")
 
 SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, -4
-EXPORTS = ("sched_eval", "sched_ws_bytes", "sched_anneal", "sched_best", "sched_chains", "sched_start_info",
-           "sched_gen_perms", "sched_strerror")
+EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_best", "sched_chains",
+           "sched_start_info", "sched_starts", "sched_gen_perms", "sched_strerror")
+POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 
 
 class SchedError(RuntimeError):
@@ -52,6 +53,10 @@ def load_library(path: str = LIB_PATH):
     vp, i32, i64, u64, dbl, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_uint64, C.c_double, C.c_size_t
     L.sched_eval.argtypes = [vp, vp, vp, i64, vp, vp, vp]
     L.sched_eval.restype = C.c_int
+    L.sched_eval_batches.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp]
+    L.sched_eval_batches.restype = C.c_int
+    L.sched_starts.argtypes = [vp, vp, vp, vp, vp]
+    L.sched_starts.restype = C.c_int
     L.sched_ws_bytes.argtypes = [i32, i32]
     L.sched_ws_bytes.restype = sz
     L.sched_anneal.argtypes = [vp, vp, i32, i32, dbl, dbl, u64, vp, sz, vp]
@@ -143,6 +148,33 @@ def sched_eval(dq: DeviceQueue, model, perms: torch.Tensor, out: torch.Tensor | 
     return (out, det) if det is not None else out
 
 
+def starts_to_device(starts: np.ndarray, device="cuda") -> torch.Tensor:
+    """k x n batch-start flags as a uint8 device tensor."""
+    return torch.from_numpy(np.ascontiguousarray(starts, dtype=np.uint8)).to(device)
+
+
+def sched_eval_batches(dq: DeviceQueue, model, perms: torch.Tensor, starts: torch.Tensor,
+                       out: torch.Tensor | None = None, detail: bool | torch.Tensor = False, stream=None):
+    """(n_met, t_sum) per (order, layout) row: perms k x n (uint16 bits), starts k x n uint8."""
+    L = load_library()
+    if perms.dim() != 2 or int(perms.shape[1]) != dq.n or tuple(starts.shape) != tuple(perms.shape):
+        raise ValueError("perms and starts must both be k x n")
+    if starts.dtype != torch.uint8:
+        raise ValueError("starts must be uint8")
+    k = int(perms.shape[0])
+    if out is None:
+        out = torch.empty((k, 2), dtype=torch.int64, device=perms.device)
+    det = None
+    if isinstance(detail, torch.Tensor):
+        det = detail
+    elif detail:
+        det = torch.zeros((k, dq.n, 2), dtype=torch.int64, device=perms.device)
+    q, m = dq.c(), _model(model)
+    _check(L.sched_eval_batches(C.byref(q), C.byref(m), _ptr(perms), _ptr(starts), k, _ptr(out), _ptr(det),
+                                _stream(stream)))
+    return (out, det) if det is not None else out
+
+
 def ws_bytes(n: int, chains: int) -> int:
     return int(load_library().sched_ws_bytes(int(n), int(chains)))
 
@@ -187,6 +219,15 @@ def sched_start_info(ws: torch.Tensor, n: int, stream=None):
     info = torch.empty(4, dtype=torch.int64, device=ws.device)
     _check(load_library().sched_start_info(_ptr(ws), _ptr(start), _ptr(info), _stream(stream)))
     return start, info
+
+
+def sched_starts(ws: torch.Tensor, n: int, chains: int, stream=None):
+    """Batch layouts after a batch-size search: (cur chains x n, best chains x n, winner n), uint8."""
+    cur = torch.empty((chains, n), dtype=torch.uint8, device=ws.device)
+    best = torch.empty((chains, n), dtype=torch.uint8, device=ws.device)
+    win = torch.empty(n, dtype=torch.uint8, device=ws.device)
+    _check(load_library().sched_starts(_ptr(ws), _ptr(cur), _ptr(best), _ptr(win), _stream(stream)))
+    return cur, best, win
 
 
 def sched_gen_perms(seed: int, n: int, k: int, row0: int = 0, out: torch.Tensor | None = None, stream=None,

@@ -27,6 +27,7 @@ KIND_E2E = 2
 
 POLICY_STATIC = 0
 POLICY_CONTINUOUS = 1
+POLICY_STATIC_SEARCH = 2  # static batches whose sizes are searched with the order
 
 # Base SLO thresholds in microseconds, indexed by kind (TTFT, TPOT, E2E).
 BASE_THR_SINGLE = (200_000, 50_000, 8_000_000)
@@ -166,6 +167,17 @@ def random_queue(rng: np.random.Generator, n: int, max_in=2048, max_out=64, thr_
     return Queue(in_len, out_len, kind, thr)
 
 
+def random_layouts(rng: np.random.Generator, k: int, n: int, B: int) -> np.ndarray:
+    """k x n batch-start flags (uint8): batch sizes drawn uniformly from 1..B, last one cut at n."""
+    out = np.zeros((k, n), np.uint8)
+    for r in range(k):
+        p = 0
+        while p < n:
+            out[r, p] = 1
+            p += int(rng.integers(1, B + 1))
+    return out
+
+
 MODEL_A = dict(p0=2000, p1=40, d0=8000, d1=300, d2=2)   # workloads 1, 2, 3, 5
 MODEL_B = dict(p0=2000, p1=40, d0=8000, d1=250, d2=1)   # burst workload 4
 
@@ -193,3 +205,16 @@ def workload(idx: int) -> Workload:
 
 
 ALL_WORKLOADS = (1, 2, 3, 4, 5)
+
+
+def search_workload(idx: int) -> Workload:
+    """The static annealing workloads (1, 2 or 4) with the batch sizes searched as well:
+    same queue, model coefficients, chains, iterations and cooling."""
+    W = workload(idx)
+    if W.model.policy != POLICY_STATIC or not W.chains:
+        raise ValueError(f"workload {idx} is not a static annealing workload")
+    m = W.model
+    return Workload(W.name.replace("-static", "-search"), W.queue,
+                    Model(m.max_batch, POLICY_STATIC_SEARCH, m.p0, m.p1, m.d0, m.d1, m.d2, m.t_ref_us,
+                          m.swap_threshold),
+                    chains=W.chains, iters=W.iters, T0=W.T0, alpha=W.alpha, seed=W.seed)

@@ -39,3 +39,32 @@ def oracle_rows(q, m, perms: np.ndarray) -> np.ndarray:
     with mp.get_context("spawn").Pool(len(parts)) as pool:
         out = pool.map(_rows_job, [(q, m, p) for p in parts])
     return np.concatenate(out)
+
+
+def _chain_batches_job(args):
+    import oracle
+    q, m, chain, iters, T0, alpha, seed, info = args
+    r = oracle.anneal_chain_batches(q, m, chain, iters, T0, alpha, seed, start_info=info)
+    return chain, r["rec"], r["cur"], r["best"], r["cur_starts"], r["best_starts"]
+
+
+def oracle_chains_batches(q, m, chains, iters, T0, alpha, seed, info):
+    """Chains of the joint order / batch-size search, in worker processes."""
+    jobs = [(q, m, int(c), iters, T0, alpha, seed, info) for c in chains]
+    with mp.get_context("spawn").Pool(min(workers(), len(jobs))) as pool:
+        out = pool.map(_chain_batches_job, jobs)
+    return {c: dict(rec=rec, cur=cur, best=best, cur_starts=cs, best_starts=bs) for c, rec, cur, best, cs, bs in out}
+
+
+def _rows_batches_job(args):
+    import oracle
+    q, m, perms, starts = args
+    return oracle.eval_rows_batches(q, m, perms, starts)
+
+
+def oracle_rows_batches(q, m, perms: np.ndarray, starts: np.ndarray) -> np.ndarray:
+    k = max(1, min(workers(), len(perms) // 256 + 1))
+    parts = list(zip(np.array_split(perms, k), np.array_split(starts, k)))
+    with mp.get_context("spawn").Pool(len(parts)) as pool:
+        out = pool.map(_rows_batches_job, [(q, m, p, s) for p, s in parts])
+    return np.concatenate(out)

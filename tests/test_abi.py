@@ -55,7 +55,7 @@ def test_host_side_rejections_without_gpu(lib):
     assert lib.sched_eval(C.byref(q), C.byref(m), None, 0, None, None, None) == sl.SCHED_EINVAL
     q = sl._Queue(8, 8, 8, 8, 8)
     for bad in (sl._Model(0, 0, 1, 1, 1, 1, 1, 0, 0), sl._Model(65, 0, 1, 1, 1, 1, 1, 0, 0),
-                sl._Model(4, 2, 1, 1, 1, 1, 1, 0, 0), sl._Model(4, 0, -1, 1, 1, 1, 1, 0, 0),
+                sl._Model(4, 3, 1, 1, 1, 1, 1, 0, 0), sl._Model(4, 0, -1, 1, 1, 1, 1, 0, 0),
                 sl._Model(4, 0, 1, 1, 1, 1, 1, 0, (1 << 32) + 1)):
         assert lib.sched_eval(C.byref(q), C.byref(bad), 8, 1, 8, None, None) == sl.SCHED_EINVAL
     assert lib.sched_eval(C.byref(q), C.byref(m), None, 1, None, None, None) == sl.SCHED_EINVAL
@@ -70,6 +70,12 @@ def test_host_side_rejections_without_gpu(lib):
     assert lib.sched_best(None, 8, 8, None) == sl.SCHED_EINVAL
     assert lib.sched_chains(None, 8, None, None, None) == sl.SCHED_EINVAL
     assert lib.sched_start_info(None, 8, 8, None) == sl.SCHED_EINVAL
+    assert lib.sched_starts(None, 8, 8, 8, None) == sl.SCHED_EINVAL
+    assert lib.sched_starts(256, None, None, None, None) == sl.SCHED_EINVAL
+    assert lib.sched_eval_batches(C.byref(q), C.byref(m), 8, None, 1, 8, None, None) == sl.SCHED_EINVAL
+    assert lib.sched_eval_batches(C.byref(q), C.byref(m), 8, 8, -1, 8, None, None) == sl.SCHED_EINVAL
+    mc = sl._Model(4, 1, 2000, 40, 8000, 300, 2, 0, 1 << 31)
+    assert lib.sched_eval_batches(C.byref(q), C.byref(mc), 8, 8, 1, 8, None, None) == sl.SCHED_EINVAL
     assert lib.sched_gen_perms(0, 0, 0, 1, 8, None) == sl.SCHED_EINVAL
     assert lib.sched_gen_perms(0, 8, -1, 1, 8, None) == sl.SCHED_EINVAL
     assert lib.sched_gen_perms(0, 8, 0, 0, None, None) == sl.SCHED_OK

@@ -1,0 +1,175 @@
+"""GPU parity of the joint search over order and batch sizes against the CPU oracle, bit
+for bit: sched_eval_batches on random and adversarial (order, layout) rows, and
+sched_anneal with SCHED_STATIC_SEARCH per chain (final and best orders and layouts, keys,
+best iteration, accept count, trajectory digest) plus the cross-chain winner."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(__file__))
+from gpu_helpers import oracle_chains_batches, oracle_rows_batches  # noqa: E402
+
+from paper_2504_14966_amd.workloads import (Model, Queue, random_layouts, random_queue,  # noqa: E402
+                                            search_workload, workload)
+
+pytestmark = pytest.mark.gpu
+SEARCH = 2
+
+
+@pytest.fixture(scope="module")
+def sl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2504_14966_amd.sloanneal as m
+    m.load_library()
+    return m
+
+
+def _eval(sl, q, m, perms, starts, detail=False):
+    import torch
+    dq = sl.DeviceQueue.from_queue(q)
+    res = sl.sched_eval_batches(dq, m, sl.perms_to_device(perms), sl.starts_to_device(starts), detail=detail)
+    torch.cuda.synchronize()
+    if detail:
+        return res[0].cpu().numpy(), res[1].cpu().numpy()
+    return res.cpu().numpy()
+
+
+@pytest.mark.parametrize("wl,k", [(1, 512), (2, 2048), (5, 2048), (4, 256)])
+def test_eval_batches_random_layouts(sl, orc, wl, k):
+    W = workload(wl)
+    q, B = W.queue, W.model.max_batch
+    m = Model(B, SEARCH, W.model.p0, W.model.p1, W.model.d0, W.model.d1, W.model.d2)
+    rng = np.random.default_rng(100 + wl)
+    perms = np.stack([rng.permutation(q.n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, q.n, B)
+    got = _eval(sl, q, m, perms, starts)
+    want = oracle_rows_batches(q, m, perms, starts)
+    assert np.array_equal(got, want)
+    # the maximum-size layout through sched_eval_batches is sched_eval
+    mx = np.stack([orc.max_starts(q.n, B)] * 64)
+    import torch
+    dq = sl.DeviceQueue.from_queue(q)
+    plain = sl.sched_eval(dq, W.model, sl.perms_to_device(perms[:64])).cpu().numpy()
+    assert np.array_equal(_eval(sl, q, m, perms[:64], mx), plain)
+    torch.cuda.synchronize()
+
+
+def test_eval_batches_detail_and_invalid_rows(sl, orc):
+    W = workload(2)
+    q, B = W.queue, W.model.max_batch
+    m = Model(B, SEARCH, W.model.p0, W.model.p1, W.model.d0, W.model.d1, W.model.d2)
+    rng = np.random.default_rng(7)
+    k = 40
+    perms = np.stack([rng.permutation(q.n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, q.n, B)
+    starts[1, 0] = 0                      # no batch at position 0
+    starts[2, :] = 0
+    starts[2, 0] = 1                      # one batch of 64 > 16
+    starts[3, 5] = 2                      # a flag that is not 0 or 1
+    starts[4, :] = 0
+    starts[4, ::16] = 1
+    starts[4, 0] = 1                      # exactly 16 per batch: valid
+    starts[5, :] = 0
+    starts[5, ::17] = 1                   # 17 > 16: invalid
+    perms[6, 3] = perms[6, 4]             # not a permutation
+    perms[7, 0] = q.n                     # id out of range
+    starts[8, :] = 1                      # all batches of one: valid
+    out, det = _eval(sl, q, m, perms, starts, detail=True)
+    for r in range(k):
+        n_, t_, ttft, e2e = orc.replay_batches(q, m, perms[r], starts[r], detail=True)
+        assert out[r].tolist() == [n_, t_], r
+        if n_ >= 0:
+            assert det[r, :, 0].tolist() == ttft.tolist() and det[r, :, 1].tolist() == e2e.tolist(), r
+        else:
+            assert not det[r].any(), r
+    assert [out[r, 0] for r in (1, 2, 3, 5, 6, 7)] == [-1] * 6 and out[4, 0] >= 0 and out[8, 0] >= 0
+
+
+@pytest.mark.parametrize("n,B,seed", [(1, 4, 0), (2, 1, 1), (3, 2, 2), (37, 5, 3), (64, 64, 4), (130, 33, 5),
+                                      (1024, 64, 6), (1000, 7, 7)])
+def test_eval_batches_edge_shapes(sl, orc, n, B, seed):
+    rng = np.random.default_rng(seed)
+    q = random_queue(rng, n, max_in=3000, max_out=200)
+    m = Model(B, SEARCH, 2000, 40, 8000, 300, 2)
+    k = 24
+    perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, n, B)
+    starts[0] = 1
+    starts[1] = orc.max_starts(n, B)
+    assert np.array_equal(_eval(sl, q, m, perms, starts), orc.eval_rows_batches(q, m, perms, starts))
+
+
+def _anneal(sl, q, m, chains, iters, T0, alpha, seed):
+    import torch
+    dq = sl.DeviceQueue.from_queue(q)
+    ws = sl.sched_anneal(dq, m, chains, iters, T0, alpha, seed)
+    rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    cs, bs, ws_win = sl.sched_starts(ws, q.n, chains)
+    bp, key = sl.sched_best(ws, q.n)
+    torch.cuda.synchronize()
+    return dict(rec=rec.cpu().numpy(), cur=sl.as_u16(cur), best=sl.as_u16(best), cur_starts=cs.cpu().numpy(),
+                best_starts=bs.cpu().numpy(), win_starts=ws_win.cpu().numpy(), best_perm=sl.as_u16(bp),
+                key=key.cpu().numpy())
+
+
+def _check_chains(orc, res, q, m, sample, iters, T0, alpha, seed):
+    info = orc.start(q, m)
+    want = oracle_chains_batches(q, m, sample, iters, T0, alpha, seed, info)
+    for c in sample:
+        w = want[c]
+        assert res["rec"][c].tolist() == w["rec"].tolist(), f"chain {c}"
+        for f in ("cur", "best", "cur_starts", "best_starts"):
+            assert res[f][c].tolist() == w[f].tolist(), f"chain {c} {f}"
+    r = res["rec"]
+    k = max(range(len(r)), key=lambda c: (r[c, 2], -r[c, 3], -c))
+    assert res["key"].tolist() == [r[k, 2], r[k, 3], k]
+    assert res["best_perm"].tolist() == res["best"][k].tolist()
+    assert res["win_starts"].tolist() == res["best_starts"][k].tolist()
+    for c in list(sample)[:4]:
+        assert orc.replay_batches(q, m, res["cur"][c], res["cur_starts"][c]) == (r[c, 0], r[c, 1])
+        assert orc.replay_batches(q, m, res["best"][c], res["best_starts"][c]) == (r[c, 2], r[c, 3])
+
+
+def test_anneal_search_worked_queue(sl, orc):
+    """The 3-request queue whose joint optimum needs a batch of one (hand-worked: (3, 132036))."""
+    q = Queue(np.array([100, 50, 200], np.uint16), np.array([2, 3, 1], np.uint16), np.array([0, 2, 1], np.uint8),
+              np.array([8000, 70000, 9200], np.uint32))
+    m = Model(2, SEARCH, 2000, 40, 8000, 300, 2)
+    res = _anneal(sl, q, m, 64, 300, 1.0, 0.99, 0)
+    _check_chains(orc, res, q, m, range(64), 300, 1.0, 0.99, 0)
+    assert res["key"][:2].tolist() == [3, 132036]
+
+
+@pytest.mark.parametrize("n,B,chains,iters,seed", [(1, 3, 5, 40, 0), (2, 1, 8, 100, 1), (9, 4, 70, 700, 2),
+                                                   (40, 7, 33, 900, 3), (100, 33, 20, 600, 4),
+                                                   (64, 64, 10, 500, 5)])
+def test_anneal_search_random_queues(sl, orc, n, B, chains, iters, seed):
+    rng = np.random.default_rng(seed)
+    q = random_queue(rng, n, max_in=1500, max_out=40, thr_hi=400_000 * max(1, n // B))
+    m = Model(B, SEARCH, 2000, 40, 8000, 300, 2)
+    res = _anneal(sl, q, m, chains, iters, 1.0, 0.995, 11 + seed)
+    _check_chains(orc, res, q, m, range(chains), iters, 1.0, 0.995, 11 + seed)
+
+
+@pytest.mark.parametrize("wl,chains,iters,sample", [(1, 64, 2000, range(8)), (2, 1024, 2000, (0, 511, 1023)),
+                                                     (4, 256, 300, (0, 255))])
+def test_anneal_search_workloads(sl, orc, wl, chains, iters, sample):
+    W = search_workload(wl)
+    res = _anneal(sl, W.queue, W.model, chains, iters, W.T0, W.alpha, W.seed)
+    _check_chains(orc, res, W.queue, W.model, sample, iters, W.T0, W.alpha, W.seed)
+
+
+def test_starts_after_fixed_policy_runs(sl):
+    W = workload(1)
+    import torch
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    ws = sl.sched_anneal(dq, W.model, 4, 50, W.T0, W.alpha, 0)
+    cs, bs, win = sl.sched_starts(ws, W.queue.n, 4)
+    torch.cuda.synchronize()
+    want = [int(p % W.model.max_batch == 0) for p in range(W.queue.n)]
+    assert all(row.tolist() == want for row in cs.cpu().numpy())
+    assert all(row.tolist() == want for row in bs.cpu().numpy())
+    assert win.cpu().numpy().tolist() == want
