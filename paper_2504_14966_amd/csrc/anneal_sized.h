@@ -371,6 +371,369 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
   if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
 }
 
+// ---- delta kernel: timelines that fit 32 bits ----
+//
+// Per chain (one wave), in LDS:
+//   perm, flags   the current order and layout;
+//   F[r]          request r's finish offset within its batch, prefill included (u32);
+//   S[p]          start time of the batch holding position p (u32); S[n] = end of the
+//                 timeline;
+//   lim[p]        the member at p meets its SLO iff S[p] < lim[p] (u32): thr - P + 1 for
+//                 TTFT (P = batch prefill), thr - F + 1 for end-to-end, all or nothing for
+//                 TPOT (F - P against thr * l_out, which does not depend on the start);
+//                 0 when it can never be met.
+// A move changes the members of at most two batches (A before C). Each is scored in one
+// pass with its new members in lanes: a member that stays gets
+//   F' = F + [pf(g) + w(g, m) / 2] - [pf(o) + w(o, m) / 2]
+// for the request g that joins and o that leaves (either may be absent), and the newcomer
+//   F'(g) = P' + L_g d0 + sum over the new members j of w(j, g) / 2,
+// with w(j, m) = mu (e_j + d2 mu), mu = min(L_j, L_m), e_j = 2 (d1 + d2 l_j) + d2, twice
+// what j adds to m's decode iterations. Three DPP reductions give P', the newcomer's sum
+// and the new duration. Every request of the two batches is counted once, in its new
+// batch, against its old start, offset and limit (read at its old position), so the
+// changes of n and t over them are lane sums. Later batches keep their members and only
+// shift: by D'(A) - D(A) between A and C (swap), by the change of the end of the two
+// batches after C; their met counts are recounted position by position (S + shift <
+// lim). Nothing is written until the proposal is accepted.
+//
+// Widths (host check): every finish offset, batch prefill, doubled pair-cost sum over a
+// batch and 24-bit multiply operand as in the fixed-size delta kernel, and every time on
+// the timeline of any layout below 2^32 - 1.
+
+struct SizedState {
+  const uint4 *req;
+  uint16_t *perm;
+  uint8_t *flags;
+  uint32_t *F, *S, *lim;
+  int n, B, lane;
+  uint32_t d0, d2;
+};
+
+// limit of a member: met iff batch start < limit
+__device__ __forceinline__ uint32_t member_limit(uint32_t kind, uint32_t thr, uint32_t P, uint32_t F) {
+  if (kind == 1) return F - P <= thr ? 0xFFFFFFFFu : 0u;
+  const uint32_t off = kind == 0 ? P : F;
+  return thr >= off ? thr - off + 1u : 0u;
+}
+
+// New values of one changed batch's members (lanes 0 .. xe - xs - 1).
+struct BatchNew {
+  uint32_t Fn, limn;
+  int r;
+  uint32_t D;
+};
+
+__device__ __forceinline__ BatchNew batch_pass(const SizedState &c, int xs, int xe, const Remap &rm, int g, int o,
+                                               uint32_t SX, int64_t &dt, int &dn) {
+  const int lane = c.lane;
+  const int p = xs + lane;
+  const bool act = p < xe;
+  const Req rg = load_req(c.req, g >= 0 ? g : c.n), ro = load_req(c.req, o >= 0 ? o : c.n);
+  uint32_t pf = 0, tsum = 0, Fst = 0, kind = 0, thr = 0, Fold = 0, Sold = 0, limold = 0;
+  int r = 0;
+  if (act) {
+    const int q = rm.src(p);
+    r = c.perm[q];
+    const Req rq = load_req(c.req, r);
+    kind = rq.kind;
+    thr = rq.thr;
+    pf = rq.pf;
+    Fold = c.F[r];
+    Sold = c.S[q];
+    limold = c.lim[q];
+    if (g >= 0) tsum = w2(rq.L, rq.e, rg.L, c.d2);
+    if (r != g) {
+      uint32_t f = Fold;
+      if (g >= 0) f += rg.pf + (w2(rg.L, rg.e, rq.L, c.d2) >> 1);
+      if (o >= 0) f -= ro.pf + (w2(ro.L, ro.e, rq.L, c.d2) >> 1);
+      Fst = f;
+    }
+  }
+  uint32_t P = pf, T = tsum, Mx = Fst;
+  Seg<6>::template all3<OpAdd, OpAdd, OpMax>(P, T, Mx, lane);
+  const uint32_t Fg = g >= 0 ? P + __umul24(rg.L, c.d0) + (T >> 1) : 0u;
+  const uint32_t Fn = (act && r == g) ? Fg : Fst;
+  const uint32_t limn = member_limit(kind, thr, P, Fn);
+  const bool met_new = act && SX < limn, met_old = act && Sold < limold;
+  dn += __popcll(__ballot(met_new)) - __popcll(__ballot(met_old));
+  if (act) dt += (int64_t)(SX + Fn) - (int64_t)(Sold + Fold);
+  return BatchNew{Fn, limn, r, max(Mx, Fg)};
+}
+
+// met-count change of positions [a, b) when their batch starts move by delta (mod 2^32)
+__device__ __forceinline__ int recount_shift(const SizedState &c, int a, int b, uint32_t delta) {
+  int dn = 0;
+  for (int c0 = a; c0 < b; c0 += kWave) {
+    const int p = c0 + c.lane;
+    bool was = false, now = false;
+    if (p < b) {
+      const uint32_t sv = c.S[p], lv = c.lim[p];
+      was = sv < lv;
+      now = sv + delta < lv;
+    }
+    dn += __popcll(__ballot(now)) - __popcll(__ballot(was));
+  }
+  return dn;
+}
+
+__device__ __forceinline__ void apply_shift(const SizedState &c, int a, int b_incl, uint32_t delta) {
+  for (int c0 = a; c0 <= b_incl; c0 += kWave) {
+    const int p = c0 + c.lane;
+    if (p <= b_incl) c.S[p] += delta;
+  }
+}
+
+__device__ __forceinline__ void write_batch(const SizedState &c, int xs, int xe, const BatchNew &bn, uint32_t SX) {
+  const int p = xs + c.lane;
+  if (p < xe) {
+    c.F[bn.r] = bn.Fn;
+    c.S[p] = SX;
+    c.lim[p] = bn.limn;
+  }
+}
+
+// F, S, lim of an order with maximum-size batches; returns its (n, t).
+__device__ Score sized_init(const SizedState &c) {
+  const int lane = c.lane;
+  uint32_t Sc = 0;
+  int64_t nmet = 0;
+  uint64_t tl = 0;
+  for (int s = 0; s < c.n; s += c.B) {
+    const int b = min(c.B, c.n - s);
+    const bool act = lane < b;
+    const int r = act ? (int)c.perm[s + lane] : c.n;
+    const Req rq = load_req(c.req, r);
+    uint32_t acc = 0;
+    for (int j = 0; j < b; ++j) {
+      const uint32_t Lj = readlane(rq.L, j), ej = readlane(rq.e, j);
+      acc += w2(Lj, ej, rq.L, c.d2);
+    }
+    uint32_t P = act ? rq.pf : 0u;
+    P = Seg<6>::template all<OpAdd>(P, lane);
+    const uint32_t F = act ? P + __umul24(rq.L, c.d0) + (acc >> 1) : 0u;
+    const uint32_t D = Seg<6>::template all<OpMax>(F, lane);
+    const uint32_t limv = member_limit(rq.kind, rq.thr, P, F);
+    if (act) {
+      c.F[r] = F;
+      c.S[s + lane] = Sc;
+      c.lim[s + lane] = limv;
+      tl += (uint64_t)(Sc + F);
+    }
+    nmet += __popcll(__ballot(act && Sc < limv));
+    Sc += D;
+  }
+  if (lane == 0) c.S[c.n] = Sc;
+  wave_sync_lds();
+  return Score{nmet, wave_sum_u64(tl)};
+}
+
+// One wave per chain, blockDim / 64 chains per workgroup.
+__global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
+                                                             int iters, double T0, double alpha, uint32_t key0,
+                                                             uint32_t key1, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n, B = m.B;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15), sb = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
+  const size_t per_wave = pb + fb + 2 * ub + sb;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
+  for (int r = threadIdx.x; r <= n; r += blockDim.x) {
+    if (r == n) {
+      req[r] = make_uint4(0u, 0u, 0u, 0u);  // spare record: a zero request for absent movers
+      continue;
+    }
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    const uint32_t kind = q.kind[r];
+    const uint64_t thr_l = (uint64_t)q.thr[r] * lout;
+    const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
+    req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
+  }
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  SizedState c{req,
+               reinterpret_cast<uint16_t *>(wb),
+               wb + pb,
+               reinterpret_cast<uint32_t *>(wb + pb + fb),
+               reinterpret_cast<uint32_t *>(wb + pb + fb + ub),
+               reinterpret_cast<uint32_t *>(wb + pb + fb + ub + sb),
+               n, B, lane, sp.d0, sp.d2};
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref, allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n), fstride = ws_flag_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  uint8_t *gbest_f = ws + ws_off_best_starts(n, chains) + (size_t)chain * fstride;
+  uint8_t *gcur_f = ws + ws_off_cur_starts(n, chains) + (size_t)chain * fstride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    const uint8_t fl = (uint8_t)(p % B == 0);
+    c.perm[p] = v;
+    c.flags[p] = fl;
+    gbest[p] = v;
+    gbest_f[p] = fl;
+  }
+  wave_sync_lds();
+  const Score s0 = sized_init(c);
+  int64_t cn = s0.n, bn = s0.n, biter = -1, accepts = 0;
+  uint64_t ct = s0.t, bt = s0.t, digest = kFnvOffset;
+  double T = T0;
+  SizedDraws ds;
+  for (int k = 0; k < iters; ++k) {
+    if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, (uint32_t)chain, key0, key1);
+    const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
+    const int op = (int)(pk >> 20), i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+    // plan: new ranges of the changed batches A = [as, ae) and C = [cs, ce), who joins and
+    // leaves each, the shifted ranges and the flag writes
+    bool made = false, inside = false;
+    int as = 0, ae = 0, cs = 0, ce = 0, gA = -1, oA = -1, gC = -1, oC = -1, mid0 = 0, mid1 = 0, uend = n;
+    int set0 = -1, clr0 = -1;
+    Remap rm{0, 0, 0};
+    uint32_t SA = 0, SCold = 0, DAold = 0;
+    if (op == 2) {
+      if (n >= 2) {
+        made = true;
+        const int lo = min(i, j), hi = max(i, j);
+        const int sa = batch_begin(c.flags, lo, lane), ea = batch_end(c.flags, n, lo, lane);
+        rm = Remap{1, lo, hi};
+        if (hi < ea) {
+          inside = true;
+        } else {
+          const int sc = batch_begin(c.flags, hi, lane), ec = batch_end(c.flags, n, hi, lane);
+          const int plo = uniform(c.perm[lo]), phi = uniform(c.perm[hi]);
+          as = sa, ae = ea, cs = sc, ce = ec;
+          gA = phi, oA = plo, gC = plo, oC = phi;
+          mid0 = ea, mid1 = sc, uend = ec;
+          SA = c.S[sa];
+          SCold = c.S[sc];
+          DAold = c.S[ea] - SA;
+        }
+      }
+    } else {
+      const int s = batch_begin(c.flags, i, lane), e = batch_end(c.flags, n, i, lane);
+      const int x = uniform(c.perm[i]);
+      if (op == 0) {
+        if (s > 0) {
+          const int sp2 = batch_begin(c.flags, s - 1, lane);
+          if (s - sp2 < B) {
+            made = true;
+            rm = Remap{2, i, s};
+            as = sp2, ae = s + 1, gA = x;
+            cs = s + 1, ce = e, oC = x;
+            uend = e;
+            clr0 = s;
+            set0 = s + 1 < e ? s + 1 : -1;
+            SA = c.S[sp2];
+          }
+        }
+      } else if (e == n) {
+        if (e - s >= 2) {
+          made = true;
+          rm = Remap{2, i, n - 1};
+          as = s, ae = n - 1, oA = x;
+          cs = n - 1, ce = n, gC = x;
+          uend = n;
+          set0 = n - 1;
+          SA = c.S[s];
+        }
+      } else {
+        const int en = batch_end(c.flags, n, e, lane);
+        if (en - e < B) {
+          made = true;
+          rm = Remap{2, i, e - 1};
+          as = s, ae = e - 1, oA = x;
+          cs = e - 1, ce = en, gC = x;
+          uend = en;
+          set0 = e - 1;
+          clr0 = e;
+          SA = c.S[s];
+        }
+      }
+    }
+    if (!made) {
+      T = T * alpha;
+      continue;
+    }
+    int64_t dtl = 0;
+    int dn = 0;
+    int64_t dT = 0;
+    BatchNew nA{0, 0, 0, 0}, nC{0, 0, 0, 0};
+    uint32_t SC = 0, shift_mid = 0, shift_end = 0;
+    if (!inside) {
+      if (as < ae) nA = batch_pass(c, as, ae, rm, gA, oA, SA, dtl, dn);
+      const uint32_t DA = as < ae ? nA.D : 0u;
+      SC = op == 2 ? SCold + DA - DAold : SA + DA;
+      if (cs < ce) nC = batch_pass(c, cs, ce, rm, gC, oC, SC, dtl, dn);
+      const uint32_t DC = cs < ce ? nC.D : 0u;
+      const uint32_t old_end = c.S[uend];
+      shift_end = SC + DC - old_end;
+      const int64_t d_end = (int64_t)(SC + DC) - (int64_t)old_end;
+      dn += recount_shift(c, uend, n, shift_end);
+      dT = d_end * (int64_t)(n - uend);
+      if (op == 2 && mid0 < mid1) {
+        shift_mid = DA - DAold;
+        dn += recount_shift(c, mid0, mid1, shift_mid);
+        dT += ((int64_t)DA - (int64_t)DAold) * (int64_t)(mid1 - mid0);
+      }
+      dT += wave_sum_i64(dtl);
+    }
+    const int64_t nn = cn + dn;
+    const uint64_t nt = ct + (uint64_t)dT;
+    const int64_t delta = (int64_t)dn * t_ref - dT;
+    if (metropolis(delta, t_ref, T, w3)) {
+      if (inside) {
+        if (lane == 0) {
+          const uint32_t a = c.lim[rm.i];
+          c.lim[rm.i] = c.lim[rm.j];
+          c.lim[rm.j] = a;
+        }
+        apply_move_lds(c.perm, 1, rm.i, rm.j, lane);
+      } else {
+        // shifts first: they read S of positions the batch writes below do not touch
+        if (op == 2 && mid0 < mid1) apply_shift(c, mid0, mid1 - 1, shift_mid);
+        apply_shift(c, uend, n, shift_end);
+        wave_sync_lds();
+        apply_move_lds(c.perm, rm.kind, rm.i, rm.j, lane);
+        if (lane == 0) {
+          if (clr0 >= 0) c.flags[clr0] = 0;
+          if (set0 >= 0) c.flags[set0] = 1;
+        }
+        if (as < ae) write_batch(c, as, ae, nA, SA);
+        if (cs < ce) write_batch(c, cs, ce, nC, SC);
+        wave_sync_lds();
+      }
+      cn = nn;
+      ct = nt;
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (key_better(cn, ct, bn, bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        for (int p = lane; p < n; p += kWave) {
+          gbest[p] = c.perm[p];
+          gbest_f[p] = c.flags[p];
+        }
+      }
+    }
+    T = T * alpha;
+  }
+  for (int p = lane; p < n; p += kWave) {
+    gcur[p] = c.perm[p];
+    gcur_f[p] = c.flags[p];
+  }
+  if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
+}
+
 // Readouts of the layouts: per chain current and best flags, and the best chain's.
 __global__ void __launch_bounds__(256) starts_copy_kernel(const unsigned char *ws, uint8_t *cur_out, uint8_t *best_out,
                                                            uint8_t *winner_out) {

@@ -210,13 +210,54 @@ hipError_t launch_static(int waves, size_t lds, const sa::DevModel &dm, const sa
   return hipGetLastError();
 }
 
-// Joint order / batch-size search: the full-replay kernel, one chain per wave, four per
-// workgroup.
+// The batch-size search's delta kernel keeps finish offsets, prefills and pair costs as the
+// fixed-size delta kernel does (static_narrow) and every time on the timeline in 32 bits:
+// whatever the layout, the timeline ends within the sum of all prefills plus, per decode
+// iteration, d0 + d1 b + d2 C; there are at most sum(l_out) iterations, the b terms add up
+// to sum(l_out) and the C terms to sum(l_out l_in + l_out (l_out + 1) / 2).
+bool sized_narrow(const HostQueue &h, const sched_model_t *m, int n) {
+  long double pf = 0, L = 0, ctx = 0;
+  for (int r = 0; r < n; ++r) {
+    const long double lo = h.out_len[r], li = h.in_len[r];
+    pf += (long double)m->p0 + (long double)m->p1 * li;
+    L += lo;
+    ctx += lo * li + lo * (lo + 1) / 2;
+  }
+  const long double end = pf + ((long double)m->d0 + (long double)m->d1) * L + (long double)m->d2 * ctx;
+  return static_narrow(h, m, n) && end < 4294967295.0L - 1.0L;
+}
+
+size_t sized_chain_lds(int n) {
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15), sb = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
+  return pb + fb + 2 * ub + sb;
+}
+
+// Joint order / batch-size search: the delta kernel when the widths allow (as many chains
+// per workgroup as spread the chains over every CU, at most 16 and at most what the LDS
+// holds), else the full-replay kernel, four chains per workgroup.
 int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
                  int chains, int iters, double T0, double alpha, uint64_t seed, unsigned char *w, hipStream_t stream) {
-  (void)h;
-  (void)model;
   const int n = dm.n;
+  if (sized_narrow(h, model, n)) {
+    const size_t soa = (size_t)(n + 1) * 16, per = sized_chain_lds(n);
+    const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
+    int waves = 1;
+    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+    if (soa + per * waves <= (size_t)lim) {
+      const size_t lds = soa + per * waves;
+      if (lds > 65536)
+        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
+      const int grid = (chains + waves - 1) / waves;
+      sa::anneal_sized_kernel<<<grid, waves * 64, lds, stream>>>(dm, sp, dev_queue(queue), chains, iters, T0, alpha,
+                                                                 (uint32_t)seed, (uint32_t)(seed >> 32), w);
+      HIP_TRY(hipGetLastError());
+      return SCHED_OK;
+    }
+  }
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb + 64 * 16);
   const int grid = (chains + 3) / 4;

@@ -173,3 +173,35 @@ def test_starts_after_fixed_policy_runs(sl):
     assert all(row.tolist() == want for row in cs.cpu().numpy())
     assert all(row.tolist() == want for row in bs.cpu().numpy())
     assert win.cpu().numpy().tolist() == want
+
+
+def _pq(rng, n, in_lo, in_hi, out_lo, out_hi, thr_hi):
+    return Queue(rng.integers(in_lo, in_hi + 1, n).astype(np.uint16), rng.integers(out_lo, out_hi + 1, n).astype(np.uint16),
+                 rng.integers(0, 3, n).astype(np.uint8), rng.integers(0, thr_hi, n).astype(np.uint32))
+
+
+# Each case falls on one kernel path of the batch-size search: the delta kernel (32-bit
+# offsets and timeline) or the full-replay kernel (64-bit everything).
+SEARCH_PATHS = {
+    # delta kernel: batch size 1 (squeeze and delay never allowed)
+    "delta_b1": (lambda r: _pq(r, 300, 16, 2048, 1, 6, 4_000_000_000), Model(1, SEARCH, 2000, 40, 8000, 300, 2), 6, 300),
+    # delta kernel: one batch of everything at the start; delays open new last batches
+    "delta_one_batch": (lambda r: _pq(r, 50, 16, 2048, 1, 300, 3_000_000), Model(64, SEARCH, 2000, 40, 8000, 300, 2), 8, 600),
+    # delta kernel: equal output lengths (ties in every batch)
+    "delta_ties": (lambda r: _pq(r, 90, 16, 64, 7, 7, 2_000_000), Model(12, SEARCH, 2000, 40, 8000, 300, 2), 8, 800),
+    # full replay: pair costs beyond 24 bits
+    "replay_wide": (lambda r: _pq(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, SEARCH, 2000, 40, 8000, 300, 1 << 22), 8, 300),
+    # full replay: 32-bit offsets but a timeline longer than 2^32 us
+    "replay_long_timeline": (lambda r: _pq(r, 200, 16, 2048, 5000, 20000, 4_000_000_000),
+                             Model(2, SEARCH, 2000, 40, 8000, 300, 2), 4, 100),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SEARCH_PATHS))
+def test_anneal_search_paths(sl, orc, name):
+    import zlib
+    mk, m, chains, iters = SEARCH_PATHS[name]
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    q = mk(rng)
+    res = _anneal(sl, q, m, chains, iters, 0.7, 0.99, 5)
+    _check_chains(orc, res, q, m, range(chains), iters, 0.7, 0.99, 5)
