@@ -262,7 +262,7 @@ def main():
 
     import torch
     import paper_2504_14966_amd.sloanneal as sl
-    from paper_2504_14966_amd.workloads import workload
+    from paper_2504_14966_amd.workloads import search_workload, workload
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     sl.load_library()
@@ -301,6 +301,14 @@ def main():
             wx, kx, keyx = time_anneal(sl, Wx, 1, 1, torch)
             extras[f"anneal_{Wx.name}"] = dict(chain_iters_per_s=Wx.chains * Wx.iters / wx, ms=kx[0], best=keyx)
             log(f"[bench] {Wx.name}: {Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({kx[0]:.1f} ms)")
+        # the joint order / batch-size search (squeeze, delay and swap moves) on the same queues
+        for wl in (2, 4):
+            Wx = search_workload(wl)
+            wx, kx, keyx = time_anneal(sl, Wx, 2, 1, torch)
+            extras[f"anneal_{Wx.name}"] = dict(chain_iters_per_s=2 * Wx.chains * Wx.iters / wx, ms=float(np.mean(kx)),
+                                               best=keyx)
+            log(f"[bench] {Wx.name}: {2 * Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({np.mean(kx):.1f} ms), "
+                f"best {keyx}")
 
     cpu = None
     if args.cpu_all:
