@@ -94,6 +94,19 @@ def lib():
                                                vp, vp, vp, vp, vp, vp]
         L.orc_brute_batches.argtypes = [vp, vp, vp, vp, vp, vp]
         L.orc_brute_batches.restype = i64
+        L.orc_better.argtypes = [vp, i64, i64, i64, i64]
+        L.orc_better.restype = C.c_int
+        L.orc_accept_ratio.argtypes = [i64, i64, i64, i64, dbl, u32]
+        L.orc_accept_ratio.restype = C.c_int
+        L.orc_levels.argtypes = [dbl, dbl, dbl]
+        L.orc_levels.restype = i32
+        L.orc_start_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+        L.orc_start_ex.restype = C.c_int
+        L.orc_anneal_chain_ex.argtypes = [vp, vp, vp, vp, i64, C.c_int, i32, i32, dbl, dbl, u64, vp, vp, vp, vp]
+        L.orc_anneal_chain_batches_ex.argtypes = [vp, vp, vp, vp, i64, C.c_int, i32, i32, dbl, dbl, u64,
+                                                  vp, vp, vp, vp, vp, vp]
+        L.orc_brute_ex.argtypes = [vp, vp, vp, vp, vp, vp]
+        L.orc_brute_ex.restype = i64
         _lib = L
     return _lib
 
@@ -192,44 +205,73 @@ def solo(queue, model, r: int) -> int:
     return lib().orc_solo(a.qp, a.mp, int(r))
 
 
-def start(queue, model):
+OBJ_LEX, OBJ_RATIO = 0, 1
+
+
+class Search(C.Structure):
+    """Search settings: objective (OBJ_LEX attainment then latency, OBJ_RATIO G = n / t),
+    proposals per temperature level, early exit when the solo-latency order meets every SLO."""
+    _fields_ = [("objective", C.c_int32), ("level_len", C.c_int32), ("early_exit", C.c_int32),
+                ("reserved", C.c_int32)]
+
+    def __init__(self, objective=OBJ_LEX, level_len=1, early_exit=0):
+        super().__init__(int(objective), int(level_len), int(early_exit), 0)
+
+
+def _search(search):
+    return C.byref(search if search is not None else Search())
+
+
+def start(queue, model, search: Search | None = None):
     """(start order, t_ref, allmet, start_n, start_t)."""
     a = _Args(queue, model)
     st = np.zeros(a.n, np.uint16)
     t_ref, sn, stt = C.c_int64(), C.c_int64(), C.c_int64()
-    allmet = lib().orc_start(a.qp, a.mp, _p(st), C.byref(t_ref), C.byref(sn), C.byref(stt))
+    allmet = lib().orc_start_ex(a.qp, a.mp, _search(search), _p(st), C.byref(t_ref), C.byref(sn), C.byref(stt))
     return st, t_ref.value, bool(allmet), sn.value, stt.value
 
 
+def better_key(k1, k2, search: Search | None = None) -> bool:
+    return bool(lib().orc_better(_search(search), int(k1[0]), int(k1[1]), int(k2[0]), int(k2[1])))
+
+
+def accept_ratio(num: int, t_ref: int, t: int, t2: int, T: float, w3: int) -> bool:
+    return bool(lib().orc_accept_ratio(int(num), int(t_ref), int(t), int(t2), float(T), int(w3)))
+
+
+def levels(T0: float, T_thres: float, tau: float) -> int:
+    return int(lib().orc_levels(float(T0), float(T_thres), float(tau)))
+
+
 def anneal_chain(queue, model, chain: int, iters: int, T0: float, alpha: float, seed: int,
-                 start_info=None, trace: bool = False) -> dict:
+                 start_info=None, trace: bool = False, search: Search | None = None) -> dict:
     """One annealing chain; returns final/best orders, the per-chain record and (optionally) the trace."""
     a = _Args(queue, model)
     if start_info is None:
-        start_info = start(queue, model)
+        start_info = start(queue, model, search)
     st, t_ref, allmet = start_info[0], start_info[1], start_info[2]
     st = np.ascontiguousarray(st, dtype=np.uint16)
     cur = np.zeros(a.n, np.uint16)
     best = np.zeros(a.n, np.uint16)
     rec = np.zeros(8, np.int64)
     tr = np.zeros((iters, 4), np.int64) if trace else None
-    lib().orc_anneal_chain(a.qp, a.mp, _p(st), int(t_ref), int(allmet), int(chain), int(iters),
-                           float(T0), float(alpha), int(seed), _p(cur), _p(best), _p(rec),
-                           _p(tr) if trace else None)
+    lib().orc_anneal_chain_ex(a.qp, a.mp, _search(search), _p(st), int(t_ref), int(allmet), int(chain),
+                              int(iters), float(T0), float(alpha), int(seed), _p(cur), _p(best), _p(rec),
+                              _p(tr) if trace else None)
     out = dict(cur=cur, best=best, rec=rec)
     if trace:
         out["trace"] = tr
     return out
 
 
-def brute(queue, model):
+def brute(queue, model, search: Search | None = None):
     """(best_n, best_t, first optimal order, number of optimal orders) over all n! orders."""
     a = _Args(queue, model)
     if a.n > 10:
         raise ValueError("brute force is limited to n <= 10")
     bn, bt = C.c_int64(), C.c_int64()
     bp = np.zeros(a.n, np.uint16)
-    cnt = lib().orc_brute(a.qp, a.mp, C.byref(bn), C.byref(bt), _p(bp))
+    cnt = lib().orc_brute_ex(a.qp, a.mp, _search(search), C.byref(bn), C.byref(bt), _p(bp))
     return bn.value, bt.value, bp, int(cnt)
 
 
@@ -296,11 +338,11 @@ def op3(w0: int) -> int:
 
 
 def anneal_chain_batches(queue, model, chain: int, iters: int, T0: float, alpha: float, seed: int,
-                         start_info=None, trace: bool = False) -> dict:
+                         start_info=None, trace: bool = False, search: Search | None = None) -> dict:
     """One chain of the joint order / batch-size search."""
     a = _Args(queue, model)
     if start_info is None:
-        start_info = start(queue, model)
+        start_info = start(queue, model, search)
     st, t_ref, allmet = start_info[0], start_info[1], start_info[2]
     st = np.ascontiguousarray(st, dtype=np.uint16)
     cur = np.zeros(a.n, np.uint16)
@@ -309,9 +351,9 @@ def anneal_chain_batches(queue, model, chain: int, iters: int, T0: float, alpha:
     bst = np.zeros(a.n, np.uint8)
     rec = np.zeros(8, np.int64)
     tr = np.zeros((iters, 4), np.int64) if trace else None
-    lib().orc_anneal_chain_batches(a.qp, a.mp, _p(st), int(t_ref), int(allmet), int(chain), int(iters),
-                                   float(T0), float(alpha), int(seed), _p(cur), _p(cst), _p(best), _p(bst),
-                                   _p(rec), _p(tr) if trace else None)
+    lib().orc_anneal_chain_batches_ex(a.qp, a.mp, _search(search), _p(st), int(t_ref), int(allmet), int(chain),
+                                      int(iters), float(T0), float(alpha), int(seed), _p(cur), _p(cst), _p(best),
+                                      _p(bst), _p(rec), _p(tr) if trace else None)
     out = dict(cur=cur, cur_starts=cst, best=best, best_starts=bst, rec=rec)
     if trace:
         out["trace"] = tr

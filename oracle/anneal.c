@@ -6,13 +6,16 @@
  *     index); the input order replaces it if its key is strictly better. The early
  *     exit when the sorted order meets every SLO is reported as a flag only;
  *   - one proposal per iteration, cooled geometrically: T_k = T0 * alpha^k, formed by
- *     one fp64 multiply per iteration;
+ *     one fp64 multiply per iteration; with search settings, one multiply per level of
+ *     level_len proposals (T_k = T0 * alpha^floor(k / level_len)), the paper's per-level
+ *     cooling;
  *   - proposals: swap two positions (randSwapping) or remove one request and re-insert
  *     it elsewhere; batches are formed by the admission policy. The joint search over
  *     order and batch sizes with the paper's squeeze / delay moves is in sized.c;
  *   - acceptance: see orc_accept (rng.c); equal scores are accepted;
  *   - score order: (n1, t1) beats (n2, t2) iff n1 > n2, or n1 == n2 and t1 < t2
- *     (attainment first, then mean latency);
+ *     (attainment first, then mean latency); with the ratio objective iff n1 t2 > n2 t1
+ *     (G = n / t of the Problem Formulation), accepted by orc_accept_ratio;
  *   - every chain also keeps its best-so-far order (strict improvements only).
  * Random draws: one Philox4x32-10 block per (seed, chain, iteration), counter
  * (iteration, chain, 0, ORC_TAG_ANNEAL), key (seed low, seed high). Word 0 picks the
@@ -39,12 +42,20 @@ void orc_insert(uint16_t *p, int32_t from, int32_t to) {
   p[to] = x;
 }
 
-static int better(int64_t n1, int64_t t1, int64_t n2, int64_t t2) {
+static const orc_search DEFAULT_SEARCH = { ORC_OBJ_LEX, 1, 0, 0 };
+
+int orc_better(const orc_search *s, int64_t n1, int64_t t1, int64_t n2, int64_t t2) {
+  if (s->objective == ORC_OBJ_RATIO) return n1 * t2 > n2 * t1;
   return n1 > n2 || (n1 == n2 && t1 < t2);
 }
 
 int orc_start(const orc_queue *q, const orc_model *m, uint16_t *start, int64_t *t_ref,
               int64_t *start_n, int64_t *start_t) {
+  return orc_start_ex(q, m, &DEFAULT_SEARCH, start, t_ref, start_n, start_t);
+}
+
+int orc_start_ex(const orc_queue *q, const orc_model *m, const orc_search *s, uint16_t *start,
+                 int64_t *t_ref, int64_t *start_n, int64_t *start_t) {
   const int32_t n = q->n;
   int64_t *solo = (int64_t *)malloc(sizeof(int64_t) * (size_t)n);
   for (int32_t r = 0; r < n; r++) solo[r] = orc_solo(q, m, r);
@@ -63,7 +74,8 @@ int orc_start(const orc_queue *q, const orc_model *m, uint16_t *start, int64_t *
   uint16_t *ident = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)n);
   for (int32_t p = 0; p < n; p++) ident[p] = (uint16_t)p;
   orc_replay(q, m, ident, &in_n, &in_t, 0, 0);
-  if (better(in_n, in_t, sn, st)) {
+  /* the early exit keeps the sorted order; otherwise the better of the two starts */
+  if (!(s->early_exit && allmet) && orc_better(s, in_n, in_t, sn, st)) {
     memcpy(start, ident, sizeof(uint16_t) * (size_t)n);
     sn = in_n;
     st = in_t;
@@ -83,7 +95,17 @@ void orc_anneal_chain(const orc_queue *q, const orc_model *m, const uint16_t *st
                       int64_t t_ref, int allmet, int32_t chain, int32_t iters, double T0,
                       double alpha, uint64_t seed, uint16_t *cur, uint16_t *best, int64_t *rec,
                       int64_t *trace) {
+  orc_anneal_chain_ex(q, m, &DEFAULT_SEARCH, start, t_ref, allmet, chain, iters, T0, alpha, seed,
+                      cur, best, rec, trace);
+}
+
+void orc_anneal_chain_ex(const orc_queue *q, const orc_model *m, const orc_search *s,
+                         const uint16_t *start, int64_t t_ref, int allmet, int32_t chain,
+                         int32_t iters, double T0, double alpha, uint64_t seed, uint16_t *cur,
+                         uint16_t *best, int64_t *rec, int64_t *trace) {
   const int32_t n = q->n;
+  if (s->early_exit && allmet) iters = 0;
+  int32_t level_left = s->level_len;
   uint16_t *cand = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)n);
   memcpy(cur, start, sizeof(uint16_t) * (size_t)n);
   memcpy(best, start, sizeof(uint16_t) * (size_t)n);
@@ -105,14 +127,19 @@ void orc_anneal_chain(const orc_queue *q, const orc_model *m, const uint16_t *st
     else orc_insert(cand, i, j);
     int64_t nn, nt;
     orc_replay(q, m, cand, &nn, &nt, 0, 0);
-    int64_t delta = (nn - cn) * t_ref - (nt - ct);
-    int acc = orc_accept(delta, t_ref, T, w[3]);
+    int acc;
+    if (s->objective == ORC_OBJ_RATIO) {
+      acc = orc_accept_ratio(nn * ct - cn * nt, t_ref, ct, nt, T, w[3]);
+    } else {
+      int64_t delta = (nn - cn) * t_ref - (nt - ct);
+      acc = orc_accept(delta, t_ref, T, w[3]);
+    }
     if (acc) {
       memcpy(cur, cand, sizeof(uint16_t) * (size_t)n);
       cn = nn;
       ct = nt;
       accepts++;
-      if (better(cn, ct, bn, bt)) {
+      if (orc_better(s, cn, ct, bn, bt)) {
         memcpy(best, cur, sizeof(uint16_t) * (size_t)n);
         bn = cn;
         bt = ct;
@@ -128,7 +155,10 @@ void orc_anneal_chain(const orc_queue *q, const orc_model *m, const uint16_t *st
       trace[4 * (int64_t)k + 2] = ct;
       trace[4 * (int64_t)k + 3] = move;
     }
-    T = T * alpha;
+    if (--level_left == 0) {
+      level_left = s->level_len;
+      T = T * alpha;
+    }
   }
   rec[ORC_R_CUR_N] = cn;
   rec[ORC_R_CUR_T] = ct;
@@ -155,6 +185,11 @@ static int next_perm(uint16_t *p, int32_t n) {
 
 int64_t orc_brute(const orc_queue *q, const orc_model *m, int64_t *best_n, int64_t *best_t,
                   uint16_t *best_perm) {
+  return orc_brute_ex(q, m, &DEFAULT_SEARCH, best_n, best_t, best_perm);
+}
+
+int64_t orc_brute_ex(const orc_queue *q, const orc_model *m, const orc_search *s, int64_t *best_n,
+                     int64_t *best_t, uint16_t *best_perm) {
   const int32_t n = q->n;
   uint16_t p[16];
   for (int32_t u = 0; u < n; u++) p[u] = (uint16_t)u;
@@ -162,13 +197,13 @@ int64_t orc_brute(const orc_queue *q, const orc_model *m, int64_t *best_n, int64
   do {
     int64_t nn, nt;
     orc_replay(q, m, p, &nn, &nt, 0, 0);
-    if (bn < 0 || better(nn, nt, bn, bt)) {
+    if (bn < 0 || orc_better(s, nn, nt, bn, bt)) {
       bn = nn;
       bt = nt;
       count = 1;
       memcpy(best_perm, p, sizeof(uint16_t) * (size_t)n);
-    } else if (nn == bn && nt == bt) {
-      count++;
+    } else if (!orc_better(s, bn, bt, nn, nt)) {
+      count++;  /* as good as the best: equal key, or equal ratio */
     }
   } while (next_perm(p, n));
   *best_n = bn;

@@ -99,6 +99,42 @@ void orc_anneal_chain(const orc_queue *q, const orc_model *m, const uint16_t *st
 int64_t orc_brute(const orc_queue *q, const orc_model *m, int64_t *best_n, int64_t *best_t,
                   uint16_t *best_perm);
 
+/* ---- the paper's own schedule and objective (search settings) ----
+ * objective ORC_OBJ_LEX: attainment first, then lower total latency (energy n - t/t_ref).
+ * objective ORC_OBJ_RATIO: the paper's G = n / t (Problem Formulation), energy G * t_ref;
+ *   a candidate is better iff n1 t2 > n2 t1.
+ * level_len: proposals per temperature level; T is multiplied by alpha after each level
+ *   (Algorithm 1 cools once per level of iter proposals), so T_k = T0 alpha^floor(k/L).
+ * early_exit: Algorithm 1's first test -- when the solo-latency order meets every SLO it is
+ *   the result; the chain makes no proposal. */
+enum { ORC_OBJ_LEX = 0, ORC_OBJ_RATIO = 1 };
+typedef struct {
+  int32_t objective, level_len, early_exit, reserved;
+} orc_search;
+
+/* 1 iff key (n1, t1) is strictly better than (n2, t2) under the objective. */
+int orc_better(const orc_search *s, int64_t n1, int64_t t1, int64_t n2, int64_t t2);
+
+/* Metropolis for the ratio objective: num = n' t - n t' (exact int64); accept iff num >= 0
+ * or u < exp(x), x = ((double)num * t_ref) / (((double)t * t') * T), u = w3 * 2^-32. */
+int orc_accept_ratio(int64_t num, int64_t t_ref, int64_t t, int64_t t2, double T, uint32_t w3);
+
+/* Temperature levels of Algorithm 1: T = T0, then T *= tau after each level, until T <
+ * T_thres (the first level always runs). Pinned: T0 500, T_thres 20, tau 0.95 -> 63. */
+int32_t orc_levels(double T0, double T_thres, double tau);
+
+/* orc_start / orc_anneal_chain / orc_anneal_chain_batches / orc_brute under search
+ * settings (the plain functions use {ORC_OBJ_LEX, 1, 0}). With early_exit and a
+ * solo-latency order that meets every SLO, the start is that order. */
+int orc_start_ex(const orc_queue *q, const orc_model *m, const orc_search *s, uint16_t *start,
+                 int64_t *t_ref, int64_t *start_n, int64_t *start_t);
+void orc_anneal_chain_ex(const orc_queue *q, const orc_model *m, const orc_search *s,
+                         const uint16_t *start, int64_t t_ref, int allmet, int32_t chain,
+                         int32_t iters, double T0, double alpha, uint64_t seed, uint16_t *cur,
+                         uint16_t *best, int64_t *rec, int64_t *trace);
+int64_t orc_brute_ex(const orc_queue *q, const orc_model *m, const orc_search *s, int64_t *best_n,
+                     int64_t *best_t, uint16_t *best_perm);
+
 /* Solo latency of one request (its replay alone). */
 int64_t orc_solo(const orc_queue *q, const orc_model *m, int32_t r);
 
@@ -151,5 +187,11 @@ void orc_anneal_chain_batches(const orc_queue *q, const orc_model *m, const uint
  * of optimal (order, layout) pairs. */
 int64_t orc_brute_batches(const orc_queue *q, const orc_model *m, int64_t *best_n, int64_t *best_t,
                           uint16_t *best_perm, uint8_t *best_starts);
+
+void orc_anneal_chain_batches_ex(const orc_queue *q, const orc_model *m, const orc_search *s,
+                                 const uint16_t *start, int64_t t_ref, int allmet, int32_t chain,
+                                 int32_t iters, double T0, double alpha, uint64_t seed,
+                                 uint16_t *cur, uint8_t *cur_starts, uint16_t *best,
+                                 uint8_t *best_starts, int64_t *rec, int64_t *trace);
 
 #endif

@@ -84,6 +84,25 @@ int orc_accept(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
   return u < orc_det_exp(x);
 }
 
+int orc_accept_ratio(int64_t num, int64_t t_ref, int64_t t, int64_t t2, double T, uint32_t w3) {
+  if (num >= 0) return 1;
+  double a = (double)num * (double)t_ref;
+  double den = ((double)t * (double)t2) * T;
+  double x = a / den;
+  double u = (double)w3 * (1.0 / 4294967296.0);
+  return u < orc_det_exp(x);
+}
+
+int32_t orc_levels(double T0, double T_thres, double tau) {
+  int32_t levels = 0;
+  double T = T0;
+  do {
+    levels++;
+    T = T * tau;
+  } while (T >= T_thres && levels < (1 << 30));
+  return levels;
+}
+
 void orc_fy_perm(uint64_t seed, int32_t n, uint32_t idx, uint16_t *perm) {
   uint32_t key[2] = { (uint32_t)seed, (uint32_t)(seed >> 32) };
   for (int32_t p = 0; p < n; p++) perm[p] = (uint16_t)p;

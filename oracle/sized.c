@@ -170,7 +170,19 @@ void orc_anneal_chain_batches(const orc_queue *q, const orc_model *m, const uint
                               int64_t t_ref, int allmet, int32_t chain, int32_t iters, double T0,
                               double alpha, uint64_t seed, uint16_t *cur, uint8_t *cur_starts,
                               uint16_t *best, uint8_t *best_starts, int64_t *rec, int64_t *trace) {
+  const orc_search lex = { ORC_OBJ_LEX, 1, 0, 0 };
+  orc_anneal_chain_batches_ex(q, m, &lex, start, t_ref, allmet, chain, iters, T0, alpha, seed, cur,
+                              cur_starts, best, best_starts, rec, trace);
+}
+
+void orc_anneal_chain_batches_ex(const orc_queue *q, const orc_model *m, const orc_search *s,
+                                 const uint16_t *start, int64_t t_ref, int allmet, int32_t chain,
+                                 int32_t iters, double T0, double alpha, uint64_t seed,
+                                 uint16_t *cur, uint8_t *cur_starts, uint16_t *best,
+                                 uint8_t *best_starts, int64_t *rec, int64_t *trace) {
   const int32_t n = q->n, B = m->max_batch;
+  if (s->early_exit && allmet) iters = 0;
+  int32_t level_left = s->level_len;
   uint16_t *cand = (uint16_t *)malloc(sizeof(uint16_t) * (size_t)n);
   uint8_t *cst = (uint8_t *)malloc((size_t)n);
   memcpy(cur, start, sizeof(uint16_t) * (size_t)n);
@@ -203,15 +215,19 @@ void orc_anneal_chain_batches(const orc_queue *q, const orc_model *m, const uint
     if (made) {
       int64_t nn, nt;
       orc_replay_batches(q, m, cand, cst, &nn, &nt, 0, 0);
-      int64_t delta = (nn - cn) * t_ref - (nt - ct);
-      acc = orc_accept(delta, t_ref, T, w[3]);
+      if (s->objective == ORC_OBJ_RATIO) {
+        acc = orc_accept_ratio(nn * ct - cn * nt, t_ref, ct, nt, T, w[3]);
+      } else {
+        int64_t delta = (nn - cn) * t_ref - (nt - ct);
+        acc = orc_accept(delta, t_ref, T, w[3]);
+      }
       if (acc) {
         memcpy(cur, cand, sizeof(uint16_t) * (size_t)n);
         memcpy(cur_starts, cst, (size_t)n);
         cn = nn;
         ct = nt;
         accepts++;
-        if (better_key(cn, ct, bn, bt)) {
+        if (orc_better(s, cn, ct, bn, bt)) {
           memcpy(best, cur, sizeof(uint16_t) * (size_t)n);
           memcpy(best_starts, cur_starts, (size_t)n);
           bn = cn;
@@ -229,7 +245,10 @@ void orc_anneal_chain_batches(const orc_queue *q, const orc_model *m, const uint
       trace[4 * (int64_t)k + 2] = ct;
       trace[4 * (int64_t)k + 3] = op | (made ? 0 : 4);
     }
-    T = T * alpha;
+    if (--level_left == 0) {
+      level_left = s->level_len;
+      T = T * alpha;
+    }
   }
   rec[ORC_R_CUR_N] = cn;
   rec[ORC_R_CUR_T] = ct;
