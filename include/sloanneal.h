@@ -136,6 +136,39 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
                  int32_t iters, double T0, double alpha, uint64_t seed, void *ws, size_t ws_bytes,
                  hipStream_t stream);
 
+/* Search settings of Algorithm 1 beyond the workloads' defaults.
+ *   objective  : SCHED_OBJ_LEX (default): attainment first, then lower total latency, with
+ *                Metropolis energy n - t / t_ref. SCHED_OBJ_RATIO: the paper's objective
+ *                G = n / t (Problem Formulation), energy G * t_ref; a worse candidate is kept
+ *                iff w3 * 2^-32 < exp(x), x = (num * t_ref) / ((t * t') * T_k) in double
+ *                arithmetic in that order, num = n' t - n t'; keys compare by n1 t2 vs n2 t1
+ *                (best-so-far, the cross-chain winner and the start rule alike). Needs
+ *                p0 + d0 + d1 >= 1 (a positive total latency).
+ *   level_len  : proposals per temperature level, >= 1: T_k = T0 * alpha^floor(k / level_len)
+ *                (Algorithm 1 lowers T once per level of `iter` proposals; 1 = per proposal).
+ *   early_exit : 1 = Algorithm 1's first test: when the requests sorted by solo latency meet
+ *                every SLO, that order is the start and the result and no proposal runs.
+ *   reserved   : 0. */
+enum { SCHED_OBJ_LEX = 0, SCHED_OBJ_RATIO = 1 };
+typedef struct {
+  int32_t objective, level_len, early_exit, reserved;
+} sched_search_t;
+
+/* sched_anneal with search settings (search == NULL: {SCHED_OBJ_LEX, 1, 0, 0}, which is
+ * sched_anneal). The paper's schedule (T0 500, T_thres 20, tau 0.95, iter 100) is
+ * T0 = 500, alpha = 0.95, level_len = 100, iters = 100 * sched_levels(500, 20, 0.95).
+ * Errors as sched_anneal, and SCHED_EINVAL for bad settings; SCHED_ERANGE when the ratio's
+ * int64 cross products could overflow. */
+int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
+                    int32_t chains, int32_t iters, double T0, double alpha, uint64_t seed, void *ws,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* Number of temperature levels of Algorithm 1: T starts at T0 and is multiplied by tau after
+ * each level until it falls below T_thres (the first level always runs); computed on the
+ * host by repeated double multiplication. SCHED_EINVAL for T0 or T_thres not positive and
+ * finite, or tau outside (0, 1). */
+int32_t sched_levels(double T0, double T_thres, double tau);
+
 /* Best order over all chains of the last sched_anneal on ws.
  *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain). */
 int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream);

@@ -279,9 +279,11 @@ __device__ __forceinline__ void write_record(unsigned char *ws, int n, int chain
 
 // Full replay per proposal (any widths): one wave per chain; per wave LDS holds the
 // current and candidate orders and flags and the replay staging.
+template <int OBJ>
 __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, QueuePtrs q, int chains, int iters,
                                                                     double T0, double alpha, uint32_t key0,
-                                                                    uint32_t key1, unsigned char *ws) {
+                                                                    uint32_t key1, SearchParams srch,
+                                                                    unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n, B = m.B;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
@@ -323,9 +325,10 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
   wave_sync_lds();
   int64_t bn = cn, biter = -1, accepts = 0;
   uint64_t bt = ct, digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   SizedDraws ds;
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, (uint32_t)chain, key0, key1);
     const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
     const SizedMove mv = plan_move(fcur, n, B, (int)(pk >> 20), (int)(pk & 1023u), (int)((pk >> 10) & 1023u), lane);
@@ -337,8 +340,7 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
       wave_sync_lds();
       apply_sized_move(cand, fcand, mv, lane);
       const Score s = replay_batches<false>(m, req, cand, fcand, stage, nullptr);
-      const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
-      if (metropolis(delta, t_ref, T, w3)) {
+      if (obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3)) {
         uint16_t *tp = cur;
         cur = cand;
         cand = tp;
@@ -351,7 +353,7 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
         digest = (digest ^ (uint64_t)k) * kFnvPrime;
         digest = (digest ^ (uint64_t)cn) * kFnvPrime;
         digest = (digest ^ ct) * kFnvPrime;
-        if (key_better(cn, ct, bn, bt)) {
+        if (obj_better<OBJ>(cn, ct, bn, bt)) {
           bn = cn;
           bt = ct;
           biter = k;
@@ -362,7 +364,7 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
         }
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) {
     gcur[p] = cur[p];
@@ -528,9 +530,10 @@ __device__ Score sized_init(const SizedState &c) {
 }
 
 // One wave per chain, blockDim / 64 chains per workgroup.
+template <int OBJ>
 __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
                                                              int iters, double T0, double alpha, uint32_t key0,
-                                                             uint32_t key1, unsigned char *ws) {
+                                                             uint32_t key1, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n, B = m.B;
   const int waves = blockDim.x >> 6;
@@ -584,9 +587,10 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
   const Score s0 = sized_init(c);
   int64_t cn = s0.n, bn = s0.n, biter = -1, accepts = 0;
   uint64_t ct = s0.t, bt = s0.t, digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   SizedDraws ds;
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, (uint32_t)chain, key0, key1);
     const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
     const int op = (int)(pk >> 20), i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
@@ -658,7 +662,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
       }
     }
     if (!made) {
-      T = T * alpha;
+      cool.step();
       continue;
     }
     int64_t dtl = 0;
@@ -686,8 +690,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     }
     const int64_t nn = cn + dn;
     const uint64_t nt = ct + (uint64_t)dT;
-    const int64_t delta = (int64_t)dn * t_ref - dT;
-    if (metropolis(delta, t_ref, T, w3)) {
+    if (obj_accept<OBJ>(cn, ct, dn, dT, t_ref, cool.T, w3)) {
       if (inside) {
         if (lane == 0) {
           const uint32_t a = c.lim[rm.i];
@@ -715,7 +718,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
       digest = (digest ^ (uint64_t)k) * kFnvPrime;
       digest = (digest ^ (uint64_t)cn) * kFnvPrime;
       digest = (digest ^ ct) * kFnvPrime;
-      if (key_better(cn, ct, bn, bt)) {
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
         bn = cn;
         bt = ct;
         biter = k;
@@ -725,7 +728,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
         }
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) {
     gcur[p] = c.perm[p];

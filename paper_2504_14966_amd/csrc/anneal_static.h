@@ -503,10 +503,11 @@ struct StaticChain {
 };
 
 // One wave per chain; blockDim / 64 chains per workgroup.
-template <int LG>
+template <int LG, int OBJ>
 __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
                                                               int iters, double T0, double alpha, uint32_t key0,
-                                                              uint32_t key1, uint64_t swap_thr, unsigned char *ws) {
+                                                              uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                              unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n, B = m.B;
   const int M = (n + B - 1) / B;
@@ -563,9 +564,10 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
   uint64_t bt = ct;
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   ProposalStream ps;
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
@@ -584,8 +586,7 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
       int64_t dn, dt;
       int klast;
       st.propose(mv, dn, dt, klast);
-      const int64_t delta = dn * t_ref - dt;
-      acc = metropolis(delta, t_ref, T, w3);
+      acc = obj_accept<OBJ>(cn, ct, dn, dt, t_ref, cool.T, w3);
       if (acc) {
         st.apply_move(mv.type, i, j);
         for (int kk = mv.a + lane; kk <= klast; kk += kWave) st.cur[kk] = st.cand[kk];
@@ -602,14 +603,14 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
       digest = (digest ^ (uint64_t)k) * kFnvPrime;
       digest = (digest ^ (uint64_t)cn) * kFnvPrime;
       digest = (digest ^ ct) * kFnvPrime;
-      if (cn > bn || (cn == bn && ct < bt)) {
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
         bn = cn;
         bt = ct;
         biter = k;
         for (int p = lane; p < n; p += kWave) gbest[p] = st.perm[p];
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) gcur[p] = st.perm[p];
   if (lane == 0) {

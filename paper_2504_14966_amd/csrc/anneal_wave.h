@@ -329,10 +329,13 @@ struct WaveChain {
 };
 
 
-// One wave per chain; blockDim / 64 chains per workgroup.
+// One wave per chain; blockDim / 64 chains per workgroup. OBJ: objective (0 attainment,
+// then total latency; 1 ratio n / t).
+template <int OBJ>
 __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
                                                             int iters, double T0, double alpha, uint32_t key0,
-                                                            uint32_t key1, uint64_t swap_thr, unsigned char *ws) {
+                                                            uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                            unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n, B = m.B;
   const int M = (n + B - 1) / B;
@@ -393,9 +396,10 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
   uint64_t bt = ct;
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   ProposalStream ps;  // at most 32 batches: the batch indices travel with the move
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, sp.bmagic);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
@@ -414,8 +418,7 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
       int64_t dn, dt;
       int klast;
       st.propose(mv, dn, dt, klast);
-      const int64_t delta = dn * t_ref - dt;
-      acc = metropolis(delta, t_ref, T, w3);
+      acc = obj_accept<OBJ>(cn, ct, dn, dt, t_ref, cool.T, w3);
       if (acc) {
         st.apply_move(mv.type, i, j);
         st.cur = st.cand;
@@ -430,14 +433,14 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
       digest = (digest ^ (uint64_t)k) * kFnvPrime;
       digest = (digest ^ (uint64_t)cn) * kFnvPrime;
       digest = (digest ^ ct) * kFnvPrime;
-      if (cn > bn || (cn == bn && ct < bt)) {
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
         bn = cn;
         bt = ct;
         biter = k;
         for (int p = lane; p < n; p += kWave) gbest[p] = st.perm[p];
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) gcur[p] = st.perm[p];
   if (lane == 0) {

@@ -40,9 +40,17 @@ struct WsHeader {
   int64_t t_ref, start_n, start_t, allmet;
   int64_t best_chain, best_n, best_t;
   int64_t max_batch;
-  int64_t reserved[19];
+  int64_t objective, level_len, early_exit;
+  int64_t reserved[16];
 };
 static_assert(sizeof(WsHeader) <= 256, "header fits its slot");
+// Search settings of Algorithm 1: objective 0 = attainment, then total latency; 1 = the
+// ratio G = n / t. level_len proposals per temperature level. early_exit: no proposals when
+// the solo-latency order meets every SLO.
+struct SearchParams {
+  int32_t objective, level_len, early_exit, pad;
+};
+
 constexpr int kFlagNarrowPrefill = 1;  // continuous event arithmetic fits 32 bits
 constexpr int kFlagListSched = 2;      // continuous list scheduling: keys and prefill sums fit
 constexpr int kFlagNarrowTime = 4;     // list scheduling: every time on the timeline fits 32 bits

@@ -99,6 +99,67 @@ __device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double 
   return u < fast_exp_neg(x);
 }
 
+// Metropolis rule for the ratio objective G = n / t, with energy G * t_ref: a candidate
+// (n', t') from (n, t) changes the energy by num * t_ref / (t t'), num = n' t - n t' (exact
+// int64: the host bounds n * t below 2^63). Keep it iff num >= 0, or u < e^x with
+// x = (num * t_ref) / ((t * t') * T) formed by three double operations in that order. The
+// single-precision screen is the one above with the same error budget: (float) of the
+// numerator and of the denominator, a 1-ulp reciprocal and two products.
+__device__ __forceinline__ bool metropolis_ratio(int64_t num, int64_t t_ref, uint64_t t, uint64_t t2, double T,
+                                                 uint32_t w3) {
+  if (num >= 0) return true;
+  const double a = (double)num * (double)t_ref;
+  const double den = ((double)t * (double)t2) * T;
+  if (w3 != 0u && den > 1e-30 && den < 1e30 && a > -1e30) {
+    const float xl = (float)a * __builtin_amdgcn_rcpf((float)den) * 1.44269504f;
+    const float lu = __builtin_amdgcn_logf((float)w3) - 32.0f;
+    const float g = xl - lu;
+    const float tau = fabsf(xl) * 1.52587890625e-5f + 9.765625e-4f;
+    if (g > tau) return true;
+    if (g < -tau) return false;
+  }
+  const double x = a / den;
+  const double u = (double)w3 * (1.0 / 4294967296.0);
+  return u < fast_exp_neg(x);
+}
+
+// Objective OBJ (0: attainment, then total latency; 1: ratio n / t): strict improvement.
+template <int OBJ>
+__device__ __forceinline__ bool obj_better(int64_t n1, uint64_t t1, int64_t n2, uint64_t t2) {
+  if constexpr (OBJ == 0) {
+    return n1 > n2 || (n1 == n2 && t1 < t2);
+  } else {
+    return n1 * (int64_t)t2 > n2 * (int64_t)t1;
+  }
+}
+
+// Acceptance of a candidate that changes the key (cn, ct) by (dn, dt).
+template <int OBJ>
+__device__ __forceinline__ bool obj_accept(int64_t cn, uint64_t ct, int64_t dn, int64_t dt, int64_t t_ref, double T,
+                                           uint32_t w3) {
+  if constexpr (OBJ == 0) {
+    const int64_t delta = dn * t_ref - dt;
+    return metropolis(delta, t_ref, T, w3);
+  } else {
+    const int64_t nn = cn + dn;
+    const uint64_t nt = ct + (uint64_t)dt;
+    return metropolis_ratio(nn * (int64_t)ct - cn * (int64_t)nt, t_ref, ct, nt, T, w3);
+  }
+}
+
+// Temperature: T0, multiplied by alpha after every `len` proposals (Algorithm 1 cools once
+// per level; len = 1 is one multiply per proposal).
+struct Cooling {
+  double T, alpha;
+  int left, len;
+  __device__ __forceinline__ void step() {
+    if (--left == 0) {
+      left = len;
+      T = T * alpha;
+    }
+  }
+};
+
 // Multiply-shift mapping of two 32-bit words to distinct positions i != j in [0, n).
 __device__ __forceinline__ void pick_positions(int n, uint32_t w1, uint32_t w2, int &i, int &j) {
   i = (int)(((uint64_t)w1 * (uint64_t)n) >> 32);

@@ -101,7 +101,7 @@ __device__ __forceinline__ bool key_better(int64_t n1, uint64_t t1, int64_t n2, 
 
 // One workgroup of 1024 threads; n <= 1024.
 __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, int chains, int iters,
-                                                      int64_t t_ref_user, unsigned char *ws) {
+                                                      int64_t t_ref_user, SearchParams srch, unsigned char *ws) {
   __shared__ uint4 req[1024];
   __shared__ uint64_t key_solo[1024];
   __shared__ uint16_t key_id[1024];
@@ -149,7 +149,11 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
   if (tid < 64) {
     const Score sorted = replay<false>(m, req, key_id, Remap{0, 0, 0}, stage, nullptr);
     const Score input = replay<false>(m, req, ident, Remap{0, 0, 0}, stage, nullptr);
-    const bool use_input = key_better(input.n, input.t, sorted.n, sorted.t);
+    // the better of the two starts; with the early exit, a sorted order that meets every
+    // SLO is the result itself
+    const bool input_better = srch.objective ? obj_better<1>(input.n, input.t, sorted.n, sorted.t)
+                                             : obj_better<0>(input.n, input.t, sorted.n, sorted.t);
+    const bool use_input = !(srch.early_exit && sorted.n == n) && input_better;
     uint16_t *start = reinterpret_cast<uint16_t *>(ws + ws_off_start());
     for (int p = tid; p < n; p += 64) start[p] = use_input ? (uint16_t)p : key_id[p];
     if (tid == 0) {
@@ -160,6 +164,9 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
       h->iters = iters;
       h->policy = m.policy;
       h->max_batch = m.B;
+      h->objective = srch.objective;
+      h->level_len = srch.level_len;
+      h->early_exit = srch.early_exit;
       h->t_ref = t_ref_user > 0 ? t_ref_user : (input.t > 1 ? (int64_t)input.t : 1);
       h->start_n = use_input ? input.n : sorted.n;
       h->start_t = (int64_t)(use_input ? input.t : sorted.t);
@@ -172,9 +179,10 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
 }
 
 // Per-wave LDS: current and candidate-scratch orders, replay staging.
+template <int OBJ>
 __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
                                                          double alpha, uint32_t key0, uint32_t key1,
-                                                         uint64_t swap_thr, unsigned char *ws) {
+                                                         uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
@@ -209,16 +217,16 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
   uint64_t bt = ct;
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   ProposalStream ps;
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
     const Score s = replay_any<false>(m, req, cur, rm, stage, nullptr);
-    const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
-    const bool acc = metropolis(delta, t_ref, T, w3);
+    const bool acc = obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3);
     if (acc) {
       for (int p = lane; p < n; p += kWave) cand[p] = cur[rm.src(p)];
       wave_sync_lds();
@@ -231,14 +239,14 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
       digest = (digest ^ (uint64_t)k) * kFnvPrime;
       digest = (digest ^ (uint64_t)cn) * kFnvPrime;
       digest = (digest ^ ct) * kFnvPrime;
-      if (key_better(cn, ct, bn, bt)) {
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
         bn = cn;
         bt = ct;
         biter = k;
         for (int p = lane; p < n; p += kWave) gbest[p] = cur[p];
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) gcur[p] = cur[p];
   if (lane == 0) {
@@ -258,10 +266,10 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
 // proposal is replayed from the start, by list scheduling and scans (LS) or by the event
 // loop; the candidate order is read through a remap of the current one and an accepted
 // move is applied in place.
-template <bool LS>
+template <bool LS, int OBJ>
 __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
                                                             double alpha, uint32_t key0, uint32_t key1,
-                                                            uint64_t swap_thr, unsigned char *ws) {
+                                                            uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
   const int n = m.n;
   const int waves = blockDim.x >> 6;
@@ -318,9 +326,10 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
   uint64_t bt = ct;
   int64_t biter = -1, accepts = 0;
   uint64_t digest = kFnvOffset;
-  double T = T0;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
   ProposalStream ps;
-  for (int k = 0; k < iters; ++k) {
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
     if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
@@ -336,8 +345,7 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
                          : replay_cont_ls<false, false>(m, req, perm, rm, scratch, nullptr))
              : replay_cont_fast<false>(m, req, perm, rm, nullptr);
     }
-    const int64_t delta = (s.n - cn) * t_ref - (int64_t)(s.t - ct);
-    const bool acc = metropolis(delta, t_ref, T, w3);
+    const bool acc = obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3);
     if (inc && !acc) apply_move_lds(reinterpret_cast<uint4 *>(scratch + cont_ls_off_pos(n)), i == j ? 0 : rm.kind, j, i, lane);
     if (acc) {
       apply_move_lds(perm, i == j ? 0 : rm.kind, i, j, lane);
@@ -348,14 +356,14 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
       digest = (digest ^ (uint64_t)k) * kFnvPrime;
       digest = (digest ^ (uint64_t)cn) * kFnvPrime;
       digest = (digest ^ ct) * kFnvPrime;
-      if (key_better(cn, ct, bn, bt)) {
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
         bn = cn;
         bt = ct;
         biter = k;
         for (int p = lane; p < n; p += kWave) gbest[p] = perm[p];
       }
     }
-    T = T * alpha;
+    cool.step();
   }
   for (int p = lane; p < n; p += kWave) gcur[p] = perm[p];
   if (lane == 0) {
@@ -379,13 +387,23 @@ __global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
   WsHeader *h = reinterpret_cast<WsHeader *>(ws);
   const int n = h->n, chains = h->chains;
   const int64_t *rec = reinterpret_cast<const int64_t *>(ws + ws_off_records(n));
+  const bool ratio = h->objective != 0;
+  // a chain wins over another iff its best key is strictly better, or neither is better
+  // and its id is lower
+  auto wins = [ratio](int64_t n1, uint64_t t1, int32_t c1, int64_t n2, uint64_t t2, int32_t c2) {
+    if (c2 == 0x7FFFFFFF) return c1 != 0x7FFFFFFF;
+    if (c1 == 0x7FFFFFFF) return false;
+    const bool b12 = ratio ? obj_better<1>(n1, t1, n2, t2) : obj_better<0>(n1, t1, n2, t2);
+    const bool b21 = ratio ? obj_better<1>(n2, t2, n1, t1) : obj_better<0>(n2, t2, n1, t1);
+    return b12 || (!b21 && c1 < c2);
+  };
   int64_t bn = -1;
   uint64_t bt = ~0ull;
   int32_t bc = 0x7FFFFFFF;
   for (int c = threadIdx.x; c < chains; c += blockDim.x) {
     const int64_t cn = rec[(size_t)c * 8 + 2];
     const uint64_t ctt = (uint64_t)rec[(size_t)c * 8 + 3];
-    if (key_better(cn, ctt, bn, bt) || (cn == bn && ctt == bt && c < bc)) {
+    if (wins(cn, ctt, c, bn, bt, bc)) {
       bn = cn;
       bt = ctt;
       bc = c;
@@ -398,8 +416,7 @@ __global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
   for (int o = blockDim.x / 2; o > 0; o >>= 1) {
     if ((int)threadIdx.x < o) {
       const int u = threadIdx.x + o;
-      if (key_better(sn[u], st[u], sn[threadIdx.x], st[threadIdx.x]) ||
-          (sn[u] == sn[threadIdx.x] && st[u] == st[threadIdx.x] && sc[u] < sc[threadIdx.x])) {
+      if (wins(sn[u], st[u], sc[u], sn[threadIdx.x], st[threadIdx.x], sc[threadIdx.x])) {
         sn[threadIdx.x] = sn[u];
         st[threadIdx.x] = st[u];
         sc[threadIdx.x] = sc[u];

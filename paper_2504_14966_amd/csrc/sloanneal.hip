@@ -86,6 +86,22 @@ int range_check(const HostQueue &h, const sched_model_t *m, int n) {
   return SCHED_OK;
 }
 
+// The ratio objective compares n1 t2 with n2 t1 and forms n' t - n t' in int64: the
+// worst-case total latency times (n + 1) stays below 2^62.
+int ratio_range_check(const HostQueue &h, const sched_model_t *m, int n) {
+  long double max_lin = 0, max_lout = 0, sum_lout = 0, pre = 0;
+  for (int r = 0; r < n; ++r) {
+    max_lin = std::max<long double>(max_lin, h.in_len[r]);
+    max_lout = std::max<long double>(max_lout, h.out_len[r]);
+    sum_lout += h.out_len[r];
+    pre += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
+  }
+  const long double b = std::min(n, m->max_batch);
+  const long double step = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * b * (max_lin + max_lout);
+  const long double tsum = (pre + sum_lout * step) * n;
+  return tsum * (n + 1) < std::ldexp(1.0L, 62) ? SCHED_OK : SCHED_ERANGE;
+}
+
 // The continuous event loop's 32-bit arithmetic: group prefill sums, the context sum C of
 // the running requests, d0 + d1 b + d2 C and d2 b all stay below 2^32.
 bool prefill_narrow(const HostQueue &h, const sched_model_t *m, int n) {
@@ -195,18 +211,19 @@ int device_attr(hipDeviceAttribute_t attr, int fallback) {
 int max_lds_per_block() { return device_attr(hipDeviceAttributeMaxSharedMemoryPerBlock, 65536); }
 int cu_count() { return device_attr(hipDeviceAttributeMultiprocessorCount, 256); }
 
-template <int LG>
+template <int LG, int OBJ>
 hipError_t launch_static(int waves, size_t lds, const sa::DevModel &dm, const sa::StaticParams &sp,
                          const sa::QueuePtrs &q, int chains, int iters, double T0, double alpha, uint64_t seed,
-                         uint64_t swap_thr, unsigned char *w, hipStream_t stream) {
+                         uint64_t swap_thr, const sa::SearchParams &srch, unsigned char *w, hipStream_t stream) {
   if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_static_kernel<LG>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_static_kernel<LG, OBJ>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
   const int grid = (chains + waves - 1) / waves;
-  sa::anneal_static_kernel<LG><<<grid, waves * 64, lds, stream>>>(dm, sp, q, chains, iters, T0, alpha, (uint32_t)seed,
-                                                                  (uint32_t)(seed >> 32), swap_thr, w);
+  sa::anneal_static_kernel<LG, OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, q, chains, iters, T0, alpha,
+                                                                       (uint32_t)seed, (uint32_t)(seed >> 32), swap_thr,
+                                                                       srch, w);
   return hipGetLastError();
 }
 
@@ -236,8 +253,10 @@ size_t sized_chain_lds(int n) {
 // Joint order / batch-size search: the delta kernel when the widths allow (as many chains
 // per workgroup as spread the chains over every CU, at most 16 and at most what the LDS
 // holds), else the full-replay kernel, four chains per workgroup.
+template <int OBJ>
 int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
-                 int chains, int iters, double T0, double alpha, uint64_t seed, unsigned char *w, hipStream_t stream) {
+                 int chains, int iters, double T0, double alpha, uint64_t seed, const sa::SearchParams &srch,
+                 unsigned char *w, hipStream_t stream) {
   const int n = dm.n;
   if (sized_narrow(h, model, n)) {
     const size_t soa = (size_t)(n + 1) * 16, per = sized_chain_lds(n);
@@ -248,12 +267,13 @@ int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevMo
     if (soa + per * waves <= (size_t)lim) {
       const size_t lds = soa + per * waves;
       if (lds > 65536)
-        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel),
+        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel<OBJ>),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
       const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
       const int grid = (chains + waves - 1) / waves;
-      sa::anneal_sized_kernel<<<grid, waves * 64, lds, stream>>>(dm, sp, dev_queue(queue), chains, iters, T0, alpha,
-                                                                 (uint32_t)seed, (uint32_t)(seed >> 32), w);
+      sa::anneal_sized_kernel<OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, dev_queue(queue), chains, iters, T0,
+                                                                      alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
+                                                                      srch, w);
       HIP_TRY(hipGetLastError());
       return SCHED_OK;
     }
@@ -261,8 +281,8 @@ int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevMo
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb + 64 * 16);
   const int grid = (chains + 3) / 4;
-  sa::anneal_sized_generic_kernel<<<grid, 256, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
-                                                              (uint32_t)seed, (uint32_t)(seed >> 32), w);
+  sa::anneal_sized_generic_kernel<OBJ><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+                                                                   (uint32_t)seed, (uint32_t)(seed >> 32), srch, w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }
@@ -270,6 +290,105 @@ int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevMo
 size_t anneal_lds_bytes(int n) {
   const size_t per_wave = ((size_t)n * 2 + 15) / 16 * 16 * 2 + 64 * 16;
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
+}
+
+// Every chain of one sched_anneal: the kernel for the policy and the widths the queue and
+// model allow (see the checks above), objective OBJ.
+template <int OBJ>
+int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
+                  int chains, int iters, double T0, double alpha, uint64_t seed, const sa::SearchParams &srch,
+                  unsigned char *w, hipStream_t stream) {
+  const int n = dm.n;
+  int rc = SCHED_OK;
+  bool done = false;
+  if (model->policy == SCHED_STATIC_SEARCH) {
+    if ((rc = launch_sized<OBJ>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream))) return rc;
+    done = true;
+  }
+  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+    // chains per workgroup: enough to spread the chains over every CU, at most 16 and
+    // at most what the LDS holds
+    int lg = 0;
+    while ((1 << lg) < model->max_batch) ++lg;
+    // a batch of more than 32 requests fills a wave: the lane-per-batch kernel
+    const bool wave_kernel = lg == 6;
+    const size_t soa = (size_t)(n + 1) * 16;
+    const size_t per = wave_kernel ? wave_chain_lds(n, model->max_batch) : static_wave_lds(n, model->max_batch);
+    const int lim = max_lds_per_block();
+    const int cus = std::max(1, cu_count());
+    int waves = 1;
+    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+    if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= chains)) {
+      sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
+                          (1ull << 32) / (uint64_t)model->max_batch + 1};
+      const size_t lds = soa + per * waves;
+      const sa::QueuePtrs qp = dev_queue(queue);
+      const uint64_t st = model->swap_threshold;
+      hipError_t e = hipSuccess;
+      switch (lg) {
+        case 0: e = launch_static<0, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        case 1: e = launch_static<1, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        case 2: e = launch_static<2, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        case 3: e = launch_static<3, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        case 4: e = launch_static<4, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        case 5: e = launch_static<5, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
+        default: {
+          if (lds > 65536) {
+            e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_wave_kernel<OBJ>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+            if (e != hipSuccess) break;
+          }
+          const int grid = (chains + waves - 1) / waves;
+          sa::anneal_wave_kernel<OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, qp, chains, iters, T0, alpha,
+                                                                         (uint32_t)seed, (uint32_t)(seed >> 32), st,
+                                                                         srch, w);
+          e = hipGetLastError();
+          break;
+        }
+      }
+      if (e != hipSuccess) return hip_fail(e);
+      done = true;
+    }
+  }
+  if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
+    const bool ls = (dm.flags & sa::kFlagListSched) != 0;
+    const size_t soa = (size_t)n * 16;
+    const bool inc = ls && std::min(model->max_batch, n) <= 32;
+    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0) +
+                       (inc ? sa::cont_inc_bytes(n, model->max_batch) : 0);
+    const int cus = std::max(1, cu_count());
+    const int lim = max_lds_per_block();
+    int waves = 1;
+    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+    const size_t lds = soa + per * waves;
+    if (lds <= (size_t)lim) {
+      const void *fn =
+          ls ? (const void *)&sa::anneal_cont_kernel<true, OBJ> : (const void *)&sa::anneal_cont_kernel<false, OBJ>;
+      if (lds > 65536) HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
+      const int grid = (chains + waves - 1) / waves;
+      if (ls) {
+        sa::anneal_cont_kernel<true, OBJ><<<grid, waves * 64, lds, stream>>>(
+            dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
+            srch, w);
+      } else {
+        sa::anneal_cont_kernel<false, OBJ><<<grid, waves * 64, lds, stream>>>(
+            dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
+            srch, w);
+      }
+      HIP_TRY(hipGetLastError());
+      done = true;
+    }
+  }
+  if (!done) {
+    const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+    sa::anneal_kernel<OBJ><<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
+        dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
+        srch, w);
+    HIP_TRY(hipGetLastError());
+  }
+  return SCHED_OK;
 }
 
 }  // namespace
@@ -347,107 +466,41 @@ size_t sched_ws_bytes(int32_t n, int32_t chains) {
 
 int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t chains, int32_t iters, double T0,
                  double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
+  return sched_anneal_ex(queue, model, nullptr, chains, iters, T0, alpha, seed, ws, ws_bytes, stream);
+}
+
+int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
+                    int32_t chains, int32_t iters, double T0, double alpha, uint64_t seed, void *ws, size_t ws_bytes,
+                    hipStream_t stream) {
   if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
   if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
     return SCHED_EINVAL;
+  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
+  if (search) {
+    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
+        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
+      return SCHED_EINVAL;
+    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
+  }
   int rc = check_model(model, queue->n);
   if (rc) return rc;
+  // the ratio needs a positive total latency: every request takes at least p0 + d0 + d1
+  if (srch.objective == SCHED_OBJ_RATIO && model->p0 + model->d0 + model->d1 < 1) return SCHED_EINVAL;
   if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
   if (ws_bytes < sched_ws_bytes(queue->n, chains)) return SCHED_ENOSPC;
   HostQueue h;
   if ((rc = fetch_queue(queue, stream, h))) return rc;
   if ((rc = range_check(h, model, queue->n))) return rc;
+  if (srch.objective == SCHED_OBJ_RATIO && (rc = ratio_range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
   const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
                                     timeline_narrow(h, model, n));
   unsigned char *w = static_cast<unsigned char *>(ws);
-  sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, w);
+  sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
-  bool done = false;
-  if (model->policy == SCHED_STATIC_SEARCH) {
-    if ((rc = launch_sized(h, model, dm, queue, chains, iters, T0, alpha, seed, w, stream))) return rc;
-    done = true;
-  }
-  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
-    // chains per workgroup: enough to spread the chains over every CU, at most 16 and
-    // at most what the LDS holds
-    int lg = 0;
-    while ((1 << lg) < model->max_batch) ++lg;
-    // a batch of more than 32 requests fills a wave: the lane-per-batch kernel
-    const bool wave_kernel = lg == 6;
-    const size_t soa = (size_t)(n + 1) * 16;
-    const size_t per = wave_kernel ? wave_chain_lds(n, model->max_batch) : static_wave_lds(n, model->max_batch);
-    const int lim = max_lds_per_block();
-    const int cus = std::max(1, cu_count());
-    int waves = 1;
-    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
-    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-    if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= chains)) {
-      sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
-                          (1ull << 32) / (uint64_t)model->max_batch + 1};
-      const size_t lds = soa + per * waves;
-      const sa::QueuePtrs qp = dev_queue(queue);
-      const uint64_t st = model->swap_threshold;
-      hipError_t e = hipSuccess;
-      switch (lg) {
-        case 0: e = launch_static<0>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        case 1: e = launch_static<1>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        case 2: e = launch_static<2>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        case 3: e = launch_static<3>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        case 4: e = launch_static<4>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        case 5: e = launch_static<5>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, w, stream); break;
-        default: {
-          if (lds > 65536) {
-            e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_wave_kernel),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) break;
-          }
-          const int grid = (chains + waves - 1) / waves;
-          sa::anneal_wave_kernel<<<grid, waves * 64, lds, stream>>>(dm, sp, qp, chains, iters, T0, alpha, (uint32_t)seed,
-                                                                    (uint32_t)(seed >> 32), st, w);
-          e = hipGetLastError();
-          break;
-        }
-      }
-      if (e != hipSuccess) return hip_fail(e);
-      done = true;
-    }
-  }
-  if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
-    const bool ls = (dm.flags & sa::kFlagListSched) != 0;
-    const size_t soa = (size_t)n * 16;
-    const bool inc = ls && std::min(model->max_batch, n) <= 32;
-    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0) +
-                       (inc ? sa::cont_inc_bytes(n, model->max_batch) : 0);
-    const int cus = std::max(1, cu_count());
-    const int lim = max_lds_per_block();
-    int waves = 1;
-    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
-    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-    const size_t lds = soa + per * waves;
-    if (lds <= (size_t)lim) {
-      const void *fn = ls ? (const void *)&sa::anneal_cont_kernel<true> : (const void *)&sa::anneal_cont_kernel<false>;
-      if (lds > 65536) HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      const int grid = (chains + waves - 1) / waves;
-      if (ls) {
-        sa::anneal_cont_kernel<true><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
-                                                                        (uint32_t)seed, (uint32_t)(seed >> 32),
-                                                                        model->swap_threshold, w);
-      } else {
-        sa::anneal_cont_kernel<false><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
-                                                                         (uint32_t)seed, (uint32_t)(seed >> 32),
-                                                                         model->swap_threshold, w);
-      }
-      HIP_TRY(hipGetLastError());
-      done = true;
-    }
-  }
-  if (!done) {
-    const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
-    sa::anneal_kernel<<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
-        dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold, w);
-    HIP_TRY(hipGetLastError());
-  }
+  rc = srch.objective ? launch_chains<1>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream)
+                      : launch_chains<0>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream);
+  if (rc) return rc;
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
@@ -517,6 +570,19 @@ int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint
                                                   winner_starts);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
+}
+
+int32_t sched_levels(double T0, double T_thres, double tau) {
+  if (!(T0 > 0.0) || !std::isfinite(T0) || !(T_thres > 0.0) || !std::isfinite(T_thres) || !(tau > 0.0) ||
+      !(tau < 1.0))
+    return SCHED_EINVAL;
+  int32_t levels = 0;
+  double T = T0;
+  do {
+    ++levels;
+    T = T * tau;
+  } while (T >= T_thres && levels < (1 << 30));
+  return levels;
 }
 
 const char *sched_strerror(int code) {

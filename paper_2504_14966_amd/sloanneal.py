@@ -17,9 +17,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsloanneal.so")
 
 SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, -4
-EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_best", "sched_chains",
-           "sched_start_info", "sched_starts", "sched_gen_perms", "sched_strerror")
+EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
+           "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_strerror")
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
+OBJ_LEX, OBJ_RATIO = 0, 1
 
 
 class SchedError(RuntimeError):
@@ -31,6 +32,16 @@ class SchedError(RuntimeError):
 class _Queue(C.Structure):
     _fields_ = [("n", C.c_int32), ("in_len", C.c_void_p), ("out_len", C.c_void_p), ("kind", C.c_void_p),
                 ("thr_us", C.c_void_p)]
+
+
+class Search(C.Structure):
+    """Search settings (sched_search_t): objective OBJ_LEX or OBJ_RATIO, proposals per
+    temperature level, early exit when the solo-latency order meets every SLO."""
+    _fields_ = [("objective", C.c_int32), ("level_len", C.c_int32), ("early_exit", C.c_int32),
+                ("reserved", C.c_int32)]
+
+    def __init__(self, objective=OBJ_LEX, level_len=1, early_exit=0):
+        super().__init__(int(objective), int(level_len), int(early_exit), 0)
 
 
 class _Model(C.Structure):
@@ -61,6 +72,10 @@ def load_library(path: str = LIB_PATH):
     L.sched_ws_bytes.restype = sz
     L.sched_anneal.argtypes = [vp, vp, i32, i32, dbl, dbl, u64, vp, sz, vp]
     L.sched_anneal.restype = C.c_int
+    L.sched_anneal_ex.argtypes = [vp, vp, vp, i32, i32, dbl, dbl, u64, vp, sz, vp]
+    L.sched_anneal_ex.restype = C.c_int
+    L.sched_levels.argtypes = [dbl, dbl, dbl]
+    L.sched_levels.restype = i32
     L.sched_best.argtypes = [vp, vp, vp, vp]
     L.sched_best.restype = C.c_int
     L.sched_chains.argtypes = [vp, vp, vp, vp, vp]
@@ -187,14 +202,27 @@ def alloc_ws(n: int, chains: int, device="cuda") -> torch.Tensor:
 
 
 def sched_anneal(dq: DeviceQueue, model, chains: int, iters: int, T0: float, alpha: float, seed: int,
-                 ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+                 ws: torch.Tensor | None = None, stream=None, search: Search | None = None) -> torch.Tensor:
+    """Run the chains; with `search`, sched_anneal_ex (objective, per-level cooling, early exit)."""
     L = load_library()
     if ws is None:
         ws = alloc_ws(dq.n, chains)
     q, m = dq.c(), _model(model)
-    _check(L.sched_anneal(C.byref(q), C.byref(m), int(chains), int(iters), float(T0), float(alpha),
-                          int(seed) & (2**64 - 1), _ptr(ws), int(ws.numel()), _stream(stream)))
+    if search is None:
+        _check(L.sched_anneal(C.byref(q), C.byref(m), int(chains), int(iters), float(T0), float(alpha),
+                              int(seed) & (2**64 - 1), _ptr(ws), int(ws.numel()), _stream(stream)))
+    else:
+        _check(L.sched_anneal_ex(C.byref(q), C.byref(m), C.byref(search), int(chains), int(iters), float(T0),
+                                 float(alpha), int(seed) & (2**64 - 1), _ptr(ws), int(ws.numel()), _stream(stream)))
     return ws
+
+
+def sched_levels(T0: float, T_thres: float, tau: float) -> int:
+    """Temperature levels of Algorithm 1 (T0 cooled by tau until below T_thres)."""
+    v = int(load_library().sched_levels(float(T0), float(T_thres), float(tau)))
+    if v < 0:
+        raise SchedError(v, load_library().sched_strerror(v).decode())
+    return v
 
 
 def sched_best(ws: torch.Tensor, n: int, stream=None):

@@ -6,10 +6,15 @@ import os
 import numpy as np
 
 
+def _search(search):
+    import oracle
+    return None if search is None else oracle.Search(*search)
+
+
 def _chain_job(args):
     import oracle
-    q, m, chain, iters, T0, alpha, seed, info = args
-    r = oracle.anneal_chain(q, m, chain, iters, T0, alpha, seed, start_info=info)
+    q, m, chain, iters, T0, alpha, seed, info, search = args
+    r = oracle.anneal_chain(q, m, chain, iters, T0, alpha, seed, start_info=info, search=_search(search))
     return chain, r["rec"], r["cur"], r["best"]
 
 
@@ -27,8 +32,9 @@ def workers() -> int:
     return max(1, min(n, 16))
 
 
-def oracle_chains(q, m, chains, iters, T0, alpha, seed, info):
-    jobs = [(q, m, int(c), iters, T0, alpha, seed, info) for c in chains]
+def oracle_chains(q, m, chains, iters, T0, alpha, seed, info, search=None):
+    """search: None or (objective, level_len, early_exit)."""
+    jobs = [(q, m, int(c), iters, T0, alpha, seed, info, search) for c in chains]
     with mp.get_context("spawn").Pool(min(workers(), len(jobs))) as pool:
         out = pool.map(_chain_job, jobs)
     return {c: (rec, cur, best) for c, rec, cur, best in out}
@@ -43,14 +49,14 @@ def oracle_rows(q, m, perms: np.ndarray) -> np.ndarray:
 
 def _chain_batches_job(args):
     import oracle
-    q, m, chain, iters, T0, alpha, seed, info = args
-    r = oracle.anneal_chain_batches(q, m, chain, iters, T0, alpha, seed, start_info=info)
+    q, m, chain, iters, T0, alpha, seed, info, search = args
+    r = oracle.anneal_chain_batches(q, m, chain, iters, T0, alpha, seed, start_info=info, search=_search(search))
     return chain, r["rec"], r["cur"], r["best"], r["cur_starts"], r["best_starts"]
 
 
-def oracle_chains_batches(q, m, chains, iters, T0, alpha, seed, info):
+def oracle_chains_batches(q, m, chains, iters, T0, alpha, seed, info, search=None):
     """Chains of the joint order / batch-size search, in worker processes."""
-    jobs = [(q, m, int(c), iters, T0, alpha, seed, info) for c in chains]
+    jobs = [(q, m, int(c), iters, T0, alpha, seed, info, search) for c in chains]
     with mp.get_context("spawn").Pool(min(workers(), len(jobs))) as pool:
         out = pool.map(_chain_batches_job, jobs)
     return {c: dict(rec=rec, cur=cur, best=best, cur_starts=cs, best_starts=bs) for c, rec, cur, best, cs, bs in out}

@@ -1,0 +1,169 @@
+"""GPU parity of the search settings -- the paper's ratio objective G = n / t, per-level
+cooling and early exit (sched_anneal_ex) -- against the oracle, bit for bit, on every kernel
+path: per chain the final and best orders (and layouts for the batch-size search), keys,
+best iteration, accept count and trajectory digest, and the cross-chain winner."""
+import os
+import sys
+import zlib
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(__file__))
+from gpu_helpers import oracle_chains, oracle_chains_batches  # noqa: E402
+
+from paper_2504_14966_amd.workloads import Model, Queue, random_queue, search_workload, workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+RATIO, LEX = 1, 0
+
+
+@pytest.fixture(scope="module")
+def sl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2504_14966_amd.sloanneal as m
+    m.load_library()
+    return m
+
+
+def _run(sl, q, m, chains, iters, T0, alpha, seed, search):
+    import torch
+    dq = sl.DeviceQueue.from_queue(q)
+    ws = sl.sched_anneal(dq, m, chains, iters, T0, alpha, seed, search=sl.Search(*search))
+    rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    st, info = sl.sched_start_info(ws, q.n)
+    bp, key = sl.sched_best(ws, q.n)
+    out = dict(rec=rec, cur=cur, best=best, start=st, info=info, bp=bp, key=key)
+    if m.policy == 2:
+        out["cur_starts"], out["best_starts"], out["win_starts"] = sl.sched_starts(ws, q.n, chains)
+    torch.cuda.synchronize()
+    res = {}
+    for k, v in out.items():
+        res[k] = sl.as_u16(v) if k in ("cur", "best", "start", "bp") else v.cpu().numpy()
+    return res
+
+
+def _winner(rec, objective):
+    best = 0
+    for c in range(1, len(rec)):
+        n1, t1, n2, t2 = int(rec[c, 2]), int(rec[c, 3]), int(rec[best, 2]), int(rec[best, 3])
+        better = n1 * t2 > n2 * t1 if objective == RATIO else (n1 > n2 or (n1 == n2 and t1 < t2))
+        if better:
+            best = c
+    return best
+
+
+def _check(orc, res, q, m, sample, iters, T0, alpha, seed, search):
+    s = orc.Search(*search)
+    info = orc.start(q, m, s)
+    assert res["start"].tolist() == info[0].tolist()
+    assert res["info"].tolist() == [info[1], info[3], info[4], int(info[2])]
+    if m.policy == 2:
+        want = oracle_chains_batches(q, m, sample, iters, T0, alpha, seed, info, search)
+        for c in sample:
+            w = want[c]
+            assert res["rec"][c].tolist() == w["rec"].tolist(), f"chain {c}"
+            assert res["cur"][c].tolist() == w["cur"].tolist() and res["best"][c].tolist() == w["best"].tolist(), c
+            assert res["cur_starts"][c].tolist() == w["cur_starts"].tolist(), c
+            assert res["best_starts"][c].tolist() == w["best_starts"].tolist(), c
+    else:
+        want = oracle_chains(q, m, sample, iters, T0, alpha, seed, info, search)
+        for c in sample:
+            rec, cur, best = want[c]
+            assert res["rec"][c].tolist() == rec.tolist(), f"chain {c}"
+            assert res["cur"][c].tolist() == cur.tolist() and res["best"][c].tolist() == best.tolist(), f"chain {c}"
+    k = _winner(res["rec"], search[0])
+    assert res["key"].tolist() == [res["rec"][k, 2], res["rec"][k, 3], k]
+    assert res["bp"].tolist() == res["best"][k].tolist()
+
+
+# (workload, chains, iters, sample): every annealing kernel of the five workloads and the
+# batch-size search, with the ratio objective and several proposals per temperature level
+@pytest.mark.parametrize("wl,chains,iters,sample", [(1, 64, 2000, range(8)), (2, 512, 1500, (0, 255, 511)),
+                                                     (3, 64, 300, (0, 63)), (4, 256, 300, (0, 255))])
+@pytest.mark.parametrize("search", [(RATIO, 7, 0), (LEX, 13, 0)])
+def test_workloads(sl, orc, wl, chains, iters, sample, search):
+    W = workload(wl)
+    res = _run(sl, W.queue, W.model, chains, iters, W.T0, W.alpha, W.seed, search)
+    _check(orc, res, W.queue, W.model, sample, iters, W.T0, W.alpha, W.seed, search)
+
+
+@pytest.mark.parametrize("wl,chains,iters,sample", [(2, 256, 1500, (0, 255)), (4, 128, 300, (0, 127))])
+def test_search_workloads_ratio(sl, orc, wl, chains, iters, sample):
+    W = search_workload(wl)
+    res = _run(sl, W.queue, W.model, chains, iters, W.T0, W.alpha, W.seed, (RATIO, 5, 0))
+    _check(orc, res, W.queue, W.model, sample, iters, W.T0, W.alpha, W.seed, (RATIO, 5, 0))
+
+
+def _pq(rng, n, in_lo, in_hi, out_lo, out_hi, thr_hi):
+    return Queue(rng.integers(in_lo, in_hi + 1, n).astype(np.uint16), rng.integers(out_lo, out_hi + 1, n).astype(np.uint16),
+                 rng.integers(0, 3, n).astype(np.uint8), rng.integers(0, thr_hi, n).astype(np.uint32))
+
+
+# the kernels the host picks for wide integers, batch size 1 and the event loop
+PATHS = {
+    "static_b1": (lambda r: _pq(r, 300, 16, 2048, 1, 6, 4_000_000_000), Model(1, 0, 2000, 40, 8000, 300, 2), 6, 200),
+    "static_wide": (lambda r: _pq(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 0, 2000, 40, 8000, 300, 1 << 22), 8, 300),
+    "cont_event_loop": (lambda r: _pq(r, 128, 16, 2048, 40000, 65535, 4_000_000_000), Model(64, 1, 2000, 40, 8000, 300, 2),
+                        4, 40),
+    "cont_wide": (lambda r: _pq(r, 24, 16, 2048, 4, 40, 4_000_000_000), Model(6, 1, 2000, 40, 8000, 300, 1 << 25), 8, 300),
+    "cont_ls_b48": (lambda r: _pq(r, 100, 16, 2048, 4, 200, 3_000_000), Model(48, 1, 2000, 40, 8000, 300, 2), 8, 300),
+    "search_wide": (lambda r: _pq(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 2, 2000, 40, 8000, 300, 1 << 22), 8, 300),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PATHS))
+def test_paths_ratio(sl, orc, name):
+    mk, m, chains, iters = PATHS[name]
+    q = mk(np.random.default_rng(zlib.crc32(name.encode())))
+    res = _run(sl, q, m, chains, iters, 0.7, 0.99, 9, (RATIO, 3, 0))
+    _check(orc, res, q, m, range(chains), iters, 0.7, 0.99, 9, (RATIO, 3, 0))
+
+
+@pytest.mark.parametrize("policy", [0, 2])
+def test_paper_schedule(sl, orc, policy):
+    """T0 500, T_thres 20, tau 0.95, iter 100 (63 levels, 6300 proposals), objective G, early
+    exit, on the 8-request queue (max batch 4)."""
+    W = workload(1)
+    levels = sl.sched_levels(500.0, 20.0, 0.95)
+    assert levels == orc.levels(500.0, 20.0, 0.95) == 63
+    m = Model(4, policy, W.model.p0, W.model.p1, W.model.d0, W.model.d1, W.model.d2)
+    search = (RATIO, 100, 1)
+    res = _run(sl, W.queue, m, 32, 100 * levels, 500.0, 0.95, 0, search)
+    _check(orc, res, W.queue, m, range(32), 100 * levels, 500.0, 0.95, 0, search)
+
+
+def test_early_exit(sl, orc):
+    rng = np.random.default_rng(5)
+    q = random_queue(rng, 40, max_in=800, max_out=20)
+    q.kind[:] = 2
+    q.thr_us[:] = 10**9
+    for policy, B in ((0, 4), (0, 40), (1, 8), (2, 4)):
+        m = Model(B, policy, 2000, 40, 8000, 300, 2)
+        res = _run(sl, q, m, 16, 300, 1.0, 0.99, 0, (LEX, 1, 1))
+        _check(orc, res, q, m, range(16), 300, 1.0, 0.99, 0, (LEX, 1, 1))
+        assert (res["rec"][:, 5] == 0).all() and (res["rec"][:, 4] == -1).all() and res["info"][3] == 1
+        assert all(res["cur"][c].tolist() == res["start"].tolist() for c in range(16))
+
+
+def test_levels_and_rejections(sl):
+    import ctypes as C
+    assert sl.sched_levels(10.0, 20.0, 0.9) == 1
+    L = sl.load_library()
+    for args in ((0.0, 20.0, 0.95), (500.0, 0.0, 0.95), (500.0, 20.0, 1.0), (500.0, 20.0, 0.0),
+                 (float("inf"), 20.0, 0.9)):
+        assert L.sched_levels(*args) == sl.SCHED_EINVAL
+    W = workload(1)
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    ws = sl.alloc_ws(W.queue.n, 4)
+    q, m = dq.c(), sl._model(W.model)
+    for bad in (sl.Search(2, 1, 0), sl.Search(0, 0, 0), sl.Search(0, 1, 2)):
+        rc = L.sched_anneal_ex(C.byref(q), C.byref(m), C.byref(bad), 4, 10, 1.0, 0.9, 0, C.c_void_p(ws.data_ptr()),
+                               ws.numel(), None)
+        assert rc == sl.SCHED_EINVAL
+    zero = Model(4, 0, 0, 40, 0, 0, 2)   # a zero-latency request is possible: no ratio
+    mz = sl._model(zero)
+    rc = L.sched_anneal_ex(C.byref(q), C.byref(mz), C.byref(sl.Search(1, 1, 0)), 4, 10, 1.0, 0.9, 0,
+                           C.c_void_p(ws.data_ptr()), ws.numel(), None)
+    assert rc == sl.SCHED_EINVAL
