@@ -301,6 +301,27 @@ def main():
             wx, kx, keyx = time_anneal(sl, Wx, 1, 1, torch)
             extras[f"anneal_{Wx.name}"] = dict(chain_iters_per_s=Wx.chains * Wx.iters / wx, ms=kx[0], best=keyx)
             log(f"[bench] {Wx.name}: {Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({kx[0]:.1f} ms)")
+        # the paper's own schedule and objective on the 64-request queue: T0 500, T_thres 20,
+        # tau 0.95, 100 proposals per level (63 levels), G = n / t, early exit
+        Wp = workload(2)
+        lv = sl.sched_levels(500.0, 20.0, 0.95)
+        dq = sl.DeviceQueue.from_queue(Wp.queue)
+        ws = sl.alloc_ws(Wp.queue.n, Wp.chains)
+        srch = sl.Search(sl.OBJ_RATIO, 100, 1)
+        sl.sched_anneal(dq, Wp.model, Wp.chains, 100 * lv, 500.0, 0.95, 0, ws=ws, search=srch)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        sl.sched_anneal(dq, Wp.model, Wp.chains, 100 * lv, 500.0, 0.95, 0, ws=ws, search=srch)
+        b.record()
+        _, keyp = sl.sched_best(ws, Wp.queue.n)
+        torch.cuda.synchronize()
+        msp = a.elapsed_time(b)
+        extras["anneal_paper_schedule_mix-n64-b16"] = dict(chains=Wp.chains, iters=100 * lv, ms=msp,
+                                                          chain_iters_per_s=Wp.chains * 100 * lv / (msp * 1e-3),
+                                                          best=keyp.cpu().tolist())
+        log(f"[bench] paper schedule (G, 63 levels x 100) on mix-n64: {Wp.chains * 100 * lv / (msp * 1e-3):.4g} "
+            f"chain-iters/s ({msp:.1f} ms), best {keyp.cpu().tolist()}")
         # the joint order / batch-size search (squeeze, delay and swap moves) on the same queues
         for wl in (2, 4):
             Wx = search_workload(wl)
