@@ -17,7 +17,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = ("replay.c", "rng.c", "anneal.c", "sized.c")
+_SRCS = ("replay.c", "rng.c", "anneal.c", "sized.c", "multi.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", "-Wno-unused-parameter"]
@@ -107,6 +107,7 @@ def lib():
                                                   vp, vp, vp, vp, vp, vp]
         L.orc_brute_ex.argtypes = [vp, vp, vp, vp, vp, vp]
         L.orc_brute_ex.restype = i64
+        L.orc_assign.argtypes = [vp, i32, vp, vp]
         _lib = L
     return _lib
 
@@ -371,3 +372,38 @@ def brute_batches(queue, model):
     bs = np.zeros(a.n, np.uint8)
     cnt = lib().orc_brute_batches(a.qp, a.mp, C.byref(bn), C.byref(bt), _p(bp), _p(bs))
     return bn.value, bt.value, bp, bs, int(cnt)
+
+
+# ---- multiple instances (multi.c) ----
+
+def assign(queue, instances: int, capacity) -> np.ndarray:
+    """Instance of every request (Scheduling Solution, instance assignment)."""
+    a = _Args(queue, _NoModel())
+    cap = np.ascontiguousarray(capacity, dtype=np.int64)
+    assert cap.shape == (instances,) and 1 <= instances <= 64
+    out = np.zeros(a.n, np.int32)
+    lib().orc_assign(a.qp, int(instances), _p(cap), _p(out))
+    return out
+
+
+class _NoModel:
+    """Model fields for calls that use none of them."""
+    max_batch, policy, p0, p1, d0, d1, d2, t_ref_us, swap_threshold = 1, 0, 0, 0, 0, 0, 0, 0, 0
+
+
+def sub_queue(queue, inst_of, k):
+    """The requests of instance k in arrival order, and their ids."""
+    from types import SimpleNamespace
+    ids = np.flatnonzero(np.asarray(inst_of) == k)
+    return SimpleNamespace(in_len=queue.in_len[ids], out_len=queue.out_len[ids], kind=queue.kind[ids],
+                           thr_us=queue.thr_us[ids], n=len(ids)), ids
+
+
+def anneal_instance(queue, model, inst_of, k, chains_per_instance: int, chain: int, iters: int, T0: float,
+                    alpha: float, seed: int, search=None) -> dict:
+    """Chain `chain` of instance k: the single-queue chain on the instance's requests, drawing
+    from Philox chain index k * chains_per_instance + chain."""
+    sq, ids = sub_queue(queue, inst_of, k)
+    res = anneal_chain(sq, model, k * chains_per_instance + chain, iters, T0, alpha, seed, search=search)
+    res["ids"] = ids
+    return res

@@ -194,4 +194,10 @@ void orc_anneal_chain_batches_ex(const orc_queue *q, const orc_model *m, const o
                                  uint16_t *cur, uint8_t *cur_starts, uint16_t *best,
                                  uint8_t *best_starts, int64_t *rec, int64_t *trace);
 
+/* ---- multiple instances (multi.c) ----
+ * Instance assignment of the Scheduling Solution (1 <= instances <= 64): inst_out[r] for
+ * every request in arrival order. capacity: tokens per instance. Pinned by hand-worked
+ * assignments, round-robin for equal capacities, and per-iteration capacity bounds. */
+void orc_assign(const orc_queue *q, int32_t instances, const int64_t *capacity, int32_t *inst_out);
+
 #endif
