@@ -51,6 +51,7 @@ enum { SCHED_STATIC = 0, SCHED_CONTINUOUS = 1, SCHED_STATIC_SEARCH = 2 };
 #define SCHED_MAX_N 1024
 #define SCHED_MAX_BATCH 64
 #define SCHED_THR_MAX 0xFFFFFFFEu /* largest accepted SLO threshold (us) */
+#define SCHED_MAX_INSTANCES 64
 
 /* Request queue, structure of arrays, n entries, DEVICE pointers (paper: newly arrived
  * jobs with input length, predicted output length, SLO kind and threshold). */
@@ -168,6 +169,54 @@ int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, cons
  * host by repeated double multiplication. SCHED_EINVAL for T0 or T_thres not positive and
  * finite, or tau outside (0, 1). */
 int32_t sched_levels(double T0, double T_thres, double tau);
+
+/* ---- several serving instances (Scheduling Solution section, Algorithm 2) ----
+ * Callers: a scheduler in front of several LLM instances that first assigns the newly
+ * arrived requests to instances and then orders each instance's requests. */
+
+/* Instance assignment (InstAssign): requests in arrival order, each to the instance with
+ * the largest remaining memory in tokens; a request holds in_len + out_len tokens. When
+ * even that instance cannot hold the request, every instance's remaining memory is reset
+ * to its capacity (a fresh iteration) and the request goes to the instance with the largest
+ * capacity, even if it does not fit there. Ties go to the lowest index.
+ *   capacity : DEVICE, instances x int64 tokens per instance (token_num(m) = m * mu / sigma,
+ *              computed by the caller), each 1 .. 2^48
+ *   inst_out : DEVICE, n x int32, the instance of every request
+ * SCHED_EINVAL for instances outside 1 .. SCHED_MAX_INSTANCES, null pointers, a bad queue
+ * or a capacity out of range. */
+int sched_assign(const sched_queue_t *queue, int32_t instances, const int64_t *capacity, int32_t *inst_out,
+                 hipStream_t stream);
+
+/* Bytes of workspace sched_anneal_multi needs (0 on bad sizes). */
+size_t sched_ws_bytes_multi(int32_t n, int32_t instances, int32_t chains);
+
+/* Priority mapping within every instance independently, all instances side by side: the
+ * requests with inst_of[r] == k, in arrival order, form instance k's queue, and instance k
+ * runs `chains` chains on it exactly as sched_anneal_ex would on that queue, except that
+ * its chain c draws from Philox chain index k * chains + c. One launch per step covers every
+ * instance (chains by full replay of each proposal). model->policy must be SCHED_STATIC or
+ * SCHED_CONTINUOUS; search as for sched_anneal_ex (NULL for the defaults).
+ *   inst_of : DEVICE, n x int32 in 0 .. instances - 1 (e.g. from sched_assign)
+ *   ws      : DEVICE, at least sched_ws_bytes_multi(n, instances, chains) bytes, 256-aligned
+ * Instance k's chains are read with sched_best / sched_chains / sched_start_info on
+ * sched_multi_instance_ws(ws, ...k); their orders index the instance's own queue. An
+ * instance with no request runs nothing. Errors as sched_anneal_ex. */
+int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
+                       const int32_t *inst_of, int32_t instances, int32_t chains, int32_t iters, double T0,
+                       double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Instance k's single-queue workspace inside a sched_anneal_multi workspace (pointer
+ * arithmetic only; NULL on bad arguments). */
+void *sched_multi_instance_ws(void *ws, int32_t n, int32_t instances, int32_t chains, int32_t instance);
+
+/* Every instance's best order, as global request ids, instance after instance.
+ *   orders : DEVICE, n x uint16: instance 0's requests in its best priority order, then
+ *            instance 1's, ...
+ *   keys   : DEVICE nullable, instances x 3 int64 (n_met, t_sum, chain); (-1, -1, -1) for an
+ *            instance without requests
+ *   counts : DEVICE nullable, instances x int32 requests per instance */
+int sched_multi_best(const void *ws, int32_t instances, uint16_t *orders, int64_t *keys, int32_t *counts,
+                     hipStream_t stream);
 
 /* Best order over all chains of the last sched_anneal on ws.
  *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain). */

@@ -99,9 +99,9 @@ __device__ __forceinline__ bool key_better(int64_t n1, uint64_t t1, int64_t n2, 
   return n1 > n2 || (n1 == n2 && t1 < t2);
 }
 
-// One workgroup of 1024 threads; n <= 1024.
-__global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, int chains, int iters,
-                                                      int64_t t_ref_user, SearchParams srch, unsigned char *ws) {
+// Algorithm 1 initialisation by one workgroup of 1024 threads; n <= 1024.
+__device__ void start_body(const DevModel &m, const QueuePtrs &q, int chains, int iters, int64_t t_ref_user,
+                           const SearchParams &srch, unsigned char *ws) {
   __shared__ uint4 req[1024];
   __shared__ uint64_t key_solo[1024];
   __shared__ uint16_t key_id[1024];
@@ -178,24 +178,22 @@ __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, in
   }
 }
 
-// Per-wave LDS: current and candidate-scratch orders, replay staging.
+__global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, int chains, int iters,
+                                                      int64_t t_ref_user, SearchParams srch, unsigned char *ws) {
+  start_body(m, q, chains, iters, t_ref_user, srch, ws);
+}
+
+// One chain by one wave, full replay per proposal: the chain's record slot is `chain`, its
+// random stream is Philox chain index `rng_chain`. wbase: the wave's LDS (current and
+// candidate-scratch orders, replay staging); req: the request records in LDS.
 template <int OBJ>
-__global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
-                                                         double alpha, uint32_t key0, uint32_t key1,
-                                                         uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
-  extern __shared__ __align__(16) unsigned char lds[];
+__device__ void anneal_chain_body(const DevModel &m, const uint4 *req, unsigned char *wbase, int chains, int chain,
+                                  uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0, uint32_t key1,
+                                  uint64_t swap_thr, const SearchParams &srch, unsigned char *ws) {
   const int n = m.n;
-  uint4 *req = reinterpret_cast<uint4 *>(lds);
-  const size_t per_wave = lds_align((size_t)n * 2) * 2 + 64 * 16;
-  const int wave = uniform((int)(threadIdx.x >> 6));
-  unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
   uint16_t *bufA = reinterpret_cast<uint16_t *>(wbase);
   uint16_t *bufB = reinterpret_cast<uint16_t *>(wbase + lds_align((size_t)n * 2));
   uint4 *stage = reinterpret_cast<uint4 *>(wbase + 2 * lds_align((size_t)n * 2));
-  load_requests(q, m, req);
-  __syncthreads();
-  const int chain = uniform((int)blockIdx.x * kWavesPerBlock + wave);
-  if (chain >= chains) return;
   const int lane = lane_id();
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
   const int64_t t_ref = h->t_ref;
@@ -221,7 +219,7 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
   ProposalStream ps;
   const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
   for (int k = 0; k < iters_run; ++k) {
-    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     const Remap rm{(int)((pk >> 20) & 1u) + 1, i, j};
@@ -260,6 +258,25 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
     rec[6] = (int64_t)digest;
     rec[7] = allmet;
   }
+}
+
+// Per-wave LDS: current and candidate-scratch orders, replay staging.
+template <int OBJ>
+__global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
+                                                         double alpha, uint32_t key0, uint32_t key1,
+                                                         uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t per_wave = lds_align((size_t)n * 2) * 2 + 64 * 16;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
+  load_requests(q, m, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * kWavesPerBlock + wave);
+  if (chain >= chains) return;
+  anneal_chain_body<OBJ>(m, req, wbase, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                         ws);
 }
 
 // Continuous admission: one wave per chain, blockDim / 64 chains per workgroup. Every
@@ -379,8 +396,9 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
   }
 }
 
-// One workgroup: argmax over chains of (best n, -best t, -chain).
-__global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
+// One workgroup of 1024 threads: argmax over chains of the best key (lowest chain id
+// among equals).
+__device__ void reduce_body(unsigned char *ws) {
   __shared__ int64_t sn[1024];
   __shared__ uint64_t st[1024];
   __shared__ int32_t sc[1024];
@@ -430,6 +448,8 @@ __global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
     h->best_t = (int64_t)st[0];
   }
 }
+
+__global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) { reduce_body(ws); }
 
 __global__ void __launch_bounds__(256) best_copy_kernel(const unsigned char *ws, uint16_t *perm_out, int64_t *key_out) {
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);

@@ -3,6 +3,7 @@
 // stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -13,6 +14,7 @@
 #include "anneal_static.h"
 #include "anneal_wave.h"
 #include "anneal_sized.h"
+#include "multi.h"
 
 namespace {
 
@@ -568,6 +570,104 @@ int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint
   if (!ws || (!cur_starts && !best_starts && !winner_starts)) return SCHED_EINVAL;
   sa::starts_copy_kernel<<<256, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), cur_starts, best_starts,
                                                   winner_starts);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_assign(const sched_queue_t *queue, int32_t instances, const int64_t *capacity, int32_t *inst_out,
+                 hipStream_t stream) {
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !capacity || !inst_out) return SCHED_EINVAL;
+  HostQueue h;
+  int rc = fetch_queue(queue, stream, h);
+  if (rc) return rc;
+  std::vector<int64_t> cap((size_t)instances);
+  HIP_TRY(hipMemcpyAsync(cap.data(), capacity, (size_t)instances * 8, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  for (int64_t c : cap)
+    if (c < 1 || c > (int64_t(1) << 48)) return SCHED_EINVAL;
+  sa::assign_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+size_t sched_ws_bytes_multi(int32_t n, int32_t instances, int32_t chains) {
+  if (n < 1 || n > SCHED_MAX_N || instances < 1 || instances > SCHED_MAX_INSTANCES || chains < 1) return 0;
+  return sa::mws_total(n, instances, chains);
+}
+
+int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
+                       const int32_t *inst_of, int32_t instances, int32_t chains, int32_t iters, double T0,
+                       double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !inst_of) return SCHED_EINVAL;
+  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
+    return SCHED_EINVAL;
+  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
+  if (search) {
+    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
+        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
+      return SCHED_EINVAL;
+    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
+  }
+  int rc = check_model(model, queue->n);
+  if (rc) return rc;
+  if (model->policy == SCHED_STATIC_SEARCH) return SCHED_EINVAL;
+  if (srch.objective == SCHED_OBJ_RATIO && model->p0 + model->d0 + model->d1 < 1) return SCHED_EINVAL;
+  const int n = queue->n;
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
+  if (ws_bytes < sched_ws_bytes_multi(n, instances, chains)) return SCHED_ENOSPC;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h))) return rc;
+  std::vector<int32_t> inst((size_t)n);
+  HIP_TRY(hipMemcpyAsync(inst.data(), inst_of, (size_t)n * 4, hipMemcpyDeviceToHost, stream));
+  HIP_TRY(hipStreamSynchronize(stream));
+  std::vector<int> cnt((size_t)instances, 0);
+  for (int32_t v : inst) {
+    if (v < 0 || v >= instances) return SCHED_EINVAL;
+    ++cnt[(size_t)v];
+  }
+  // every instance's queue is part of the whole one, so the whole queue's bounds hold for it
+  if ((rc = range_check(h, model, n))) return rc;
+  if (srch.objective == SCHED_OBJ_RATIO && (rc = ratio_range_check(h, model, n))) return rc;
+  const int nk_max = *std::max_element(cnt.begin(), cnt.end());
+  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
+                                    timeline_narrow(h, model, n));
+  unsigned char *w = static_cast<unsigned char *>(ws);
+  sa::multi_header_kernel<<<1, 1, 0, stream>>>(w, n, instances, chains, (int64_t)sa::mws_slot_bytes(n, chains));
+  HIP_TRY(hipGetLastError());
+  sa::gather_kernel<<<instances, 1024, 0, stream>>>(dev_queue(queue), n, inst_of, chains, instances, w);
+  HIP_TRY(hipGetLastError());
+  sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(dm, n, instances, chains, iters, model->t_ref_us, srch, w);
+  HIP_TRY(hipGetLastError());
+  if (nk_max > 0) {
+    const int groups = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+    const size_t lds = anneal_lds_bytes(nk_max);
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    if (srch.objective)
+      sa::multi_anneal_kernel<1><<<instances * groups, sa::kBlock, lds, stream>>>(
+          dm, n, instances, chains, groups, iters, T0, alpha, k0, k1, model->swap_threshold, srch, w);
+    else
+      sa::multi_anneal_kernel<0><<<instances * groups, sa::kBlock, lds, stream>>>(
+          dm, n, instances, chains, groups, iters, T0, alpha, k0, k1, model->swap_threshold, srch, w);
+    HIP_TRY(hipGetLastError());
+  }
+  sa::multi_reduce_kernel<<<instances, 1024, 0, stream>>>(n, instances, chains, w);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+void *sched_multi_instance_ws(void *ws, int32_t n, int32_t instances, int32_t chains, int32_t instance) {
+  if (!ws || n < 1 || n > SCHED_MAX_N || instances < 1 || instances > SCHED_MAX_INSTANCES || chains < 1 ||
+      instance < 0 || instance >= instances)
+    return nullptr;
+  return static_cast<unsigned char *>(ws) + sa::mws_off_slot(n, instances, chains, instance);
+}
+
+int sched_multi_best(const void *ws, int32_t instances, uint16_t *orders, int64_t *keys, int32_t *counts,
+                     hipStream_t stream) {
+  if (!ws || !orders || instances < 1 || instances > SCHED_MAX_INSTANCES) return SCHED_EINVAL;
+  sa::multi_best_kernel<<<instances, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), orders, keys, counts);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }

@@ -18,7 +18,9 @@ LIB_PATH = os.path.join(HERE, "libsloanneal.so")
 
 SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, -4
 EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
-           "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_strerror")
+           "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_assign",
+           "sched_ws_bytes_multi", "sched_anneal_multi", "sched_multi_instance_ws", "sched_multi_best",
+           "sched_strerror")
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 OBJ_LEX, OBJ_RATIO = 0, 1
 
@@ -76,6 +78,16 @@ def load_library(path: str = LIB_PATH):
     L.sched_anneal_ex.restype = C.c_int
     L.sched_levels.argtypes = [dbl, dbl, dbl]
     L.sched_levels.restype = i32
+    L.sched_assign.argtypes = [vp, i32, vp, vp, vp]
+    L.sched_assign.restype = C.c_int
+    L.sched_ws_bytes_multi.argtypes = [i32, i32, i32]
+    L.sched_ws_bytes_multi.restype = sz
+    L.sched_anneal_multi.argtypes = [vp, vp, vp, vp, i32, i32, i32, dbl, dbl, u64, vp, sz, vp]
+    L.sched_anneal_multi.restype = C.c_int
+    L.sched_multi_instance_ws.argtypes = [vp, i32, i32, i32, i32]
+    L.sched_multi_instance_ws.restype = vp
+    L.sched_multi_best.argtypes = [vp, i32, vp, vp, vp, vp]
+    L.sched_multi_best.restype = C.c_int
     L.sched_best.argtypes = [vp, vp, vp, vp]
     L.sched_best.restype = C.c_int
     L.sched_chains.argtypes = [vp, vp, vp, vp, vp]
@@ -270,3 +282,57 @@ def sched_gen_perms(seed: int, n: int, k: int, row0: int = 0, out: torch.Tensor 
 def as_u16(t: torch.Tensor) -> np.ndarray:
     """Host numpy uint16 view of an int16 device tensor."""
     return t.cpu().numpy().view(np.uint16)
+
+
+# ---- several serving instances ----
+
+def sched_assign(dq: DeviceQueue, capacity: torch.Tensor, stream=None) -> torch.Tensor:
+    """Instance of every request (capacity: int64 device tensor, tokens per instance)."""
+    out = torch.empty(dq.n, dtype=torch.int32, device=capacity.device)
+    q = dq.c()
+    _check(load_library().sched_assign(C.byref(q), int(capacity.numel()), _ptr(capacity), _ptr(out), _stream(stream)))
+    return out
+
+
+class MultiWorkspace:
+    """A sched_anneal_multi workspace and the single-queue views of its instances."""
+
+    def __init__(self, n: int, instances: int, chains: int, device="cuda"):
+        nb = int(load_library().sched_ws_bytes_multi(int(n), int(instances), int(chains)))
+        if nb == 0:
+            raise ValueError("bad multi-instance workspace size request")
+        self.n, self.instances, self.chains = int(n), int(instances), int(chains)
+        self.buf = torch.empty(nb, dtype=torch.uint8, device=device)
+
+    def instance(self, k: int) -> torch.Tensor:
+        """Instance k's workspace, as a view usable with sched_best / sched_chains / sched_start_info."""
+        p = load_library().sched_multi_instance_ws(_ptr(self.buf), self.n, self.instances, self.chains, int(k))
+        if not p:
+            raise ValueError("bad instance")
+        off = int(p) - self.buf.data_ptr()
+        return self.buf[off:]
+
+
+def sched_anneal_multi(dq: DeviceQueue, model, inst_of: torch.Tensor, instances: int, chains: int, iters: int,
+                       T0: float, alpha: float, seed: int, search: Search | None = None,
+                       mws: MultiWorkspace | None = None, stream=None) -> MultiWorkspace:
+    L = load_library()
+    if mws is None:
+        mws = MultiWorkspace(dq.n, instances, chains, device=inst_of.device)
+    q, m = dq.c(), _model(model)
+    _check(L.sched_anneal_multi(C.byref(q), C.byref(m), C.byref(search) if search is not None else None,
+                                _ptr(inst_of), int(instances), int(chains), int(iters), float(T0), float(alpha),
+                                int(seed) & (2**64 - 1), _ptr(mws.buf), int(mws.buf.numel()), _stream(stream)))
+    return mws
+
+
+def sched_multi_best(mws: MultiWorkspace, stream=None):
+    """(orders n uint16 bits: each instance's best order as global ids, instance after
+    instance; keys instances x 3; counts instances)."""
+    dev = mws.buf.device
+    orders = torch.empty(mws.n, dtype=torch.int16, device=dev)
+    keys = torch.empty((mws.instances, 3), dtype=torch.int64, device=dev)
+    counts = torch.empty(mws.instances, dtype=torch.int32, device=dev)
+    _check(load_library().sched_multi_best(_ptr(mws.buf), mws.instances, _ptr(orders), _ptr(keys), _ptr(counts),
+                                           _stream(stream)))
+    return orders, keys, counts

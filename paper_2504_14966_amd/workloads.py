@@ -218,3 +218,13 @@ def search_workload(idx: int) -> Workload:
                     Model(m.max_batch, POLICY_STATIC_SEARCH, m.p0, m.p1, m.d0, m.d1, m.d2, m.t_ref_us,
                           m.swap_threshold),
                     chains=W.chains, iters=W.iters, T0=W.T0, alpha=W.alpha, seed=W.seed)
+
+
+def multi_workload() -> Workload:
+    """Several serving instances: the two-class 1024-request queue (max batch 16, static)
+    spread over 8 instances of 40,000 tokens each by the instance assignment, 512 chains per
+    instance (4096 in all) x 2000 proposals, T0 1.0, alpha 0.999."""
+    W = Workload("multi-8x-n1024-b16-static", two_class_queue(1024, 0), Model(16, POLICY_STATIC, **MODEL_A),
+                 chains=512, iters=2000, T0=1.0, alpha=0.999)
+    W.extra = dict(instances=8, capacity=[40_000] * 8)
+    return W
