@@ -262,7 +262,7 @@ def main():
 
     import torch
     import paper_2504_14966_amd.sloanneal as sl
-    from paper_2504_14966_amd.workloads import search_workload, workload
+    from paper_2504_14966_amd.workloads import multi_workload, search_workload, workload
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     sl.load_library()
@@ -322,6 +322,47 @@ def main():
                                                           best=keyp.cpu().tolist())
         log(f"[bench] paper schedule (G, 63 levels x 100) on mix-n64: {Wp.chains * 100 * lv / (msp * 1e-3):.4g} "
             f"chain-iters/s ({msp:.1f} ms), best {keyp.cpu().tolist()}")
+        # several serving instances: the 1024-request queue assigned to 8 instances, every
+        # instance's chains in one launch, against the instances annealed one after another
+        Wm = multi_workload()
+        Im = Wm.extra["instances"]
+        dqm = sl.DeviceQueue.from_queue(Wm.queue)
+        capm = torch.tensor(Wm.extra["capacity"], dtype=torch.int64, device="cuda")
+        inst = sl.sched_assign(dqm, capm)
+        mws = sl.sched_anneal_multi(dqm, Wm.model, inst, Im, Wm.chains, Wm.iters, Wm.T0, Wm.alpha, Wm.seed)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        inst = sl.sched_assign(dqm, capm)
+        sl.sched_anneal_multi(dqm, Wm.model, inst, Im, Wm.chains, Wm.iters, Wm.T0, Wm.alpha, Wm.seed, mws=mws)
+        sl.sched_multi_best(mws)
+        b.record()
+        torch.cuda.synchronize()
+        ms_one = a.elapsed_time(b)
+        inst_h = inst.cpu().numpy()
+        subs = []
+        for k in range(Im):
+            ids = np.flatnonzero(inst_h == k)
+            from paper_2504_14966_amd.workloads import Queue
+            subs.append(sl.DeviceQueue.from_queue(Queue(Wm.queue.in_len[ids], Wm.queue.out_len[ids], Wm.queue.kind[ids],
+                                                        Wm.queue.thr_us[ids])))
+        wss = [sl.alloc_ws(sq.n, Wm.chains) for sq in subs]
+        for sq, w in zip(subs, wss):
+            sl.sched_anneal(sq, Wm.model, Wm.chains, Wm.iters, Wm.T0, Wm.alpha, Wm.seed, ws=w)
+        torch.cuda.synchronize()
+        a.record()
+        for sq, w in zip(subs, wss):
+            sl.sched_anneal(sq, Wm.model, Wm.chains, Wm.iters, Wm.T0, Wm.alpha, Wm.seed, ws=w)
+        b.record()
+        torch.cuda.synchronize()
+        ms_seq = a.elapsed_time(b)
+        ci = Im * Wm.chains * Wm.iters
+        extras[f"anneal_{Wm.name}"] = dict(instances=Im, chains_per_instance=Wm.chains, iters=Wm.iters,
+                                           requests_per_instance=np.bincount(inst_h, minlength=Im).tolist(),
+                                           one_launch_ms=ms_one, chain_iters_per_s=ci / (ms_one * 1e-3),
+                                           one_after_another_ms=ms_seq)
+        log(f"[bench] {Wm.name}: {ci / (ms_one * 1e-3):.4g} chain-iters/s in one launch ({ms_one:.1f} ms, "
+            f"assignment included); instances one after another {ms_seq:.1f} ms")
         # the joint order / batch-size search (squeeze, delay and swap moves) on the same queues
         for wl in (2, 4):
             Wx = search_workload(wl)
