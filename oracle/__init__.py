@@ -17,7 +17,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = ("replay.c", "rng.c", "anneal.c", "sized.c", "multi.c")
+_SRCS = ("replay.c", "rng.c", "anneal.c", "sized.c", "multi.c", "fit.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 CFLAGS = ["-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
           "-Wall", "-Wextra", "-Wno-unused-parameter"]
@@ -108,6 +108,16 @@ def lib():
         L.orc_brute_ex.argtypes = [vp, vp, vp, vp, vp, vp]
         L.orc_brute_ex.restype = i64
         L.orc_assign.argtypes = [vp, i32, vp, vp]
+        L.orc_fit_prefill.argtypes = [vp, i64, i64]
+        L.orc_fit_prefill.restype = i64
+        L.orc_fit_decode.argtypes = [vp, i64, i64, i64]
+        L.orc_fit_decode.restype = i64
+        L.orc_replay_fit.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_replay_fit.restype = C.c_int
+        L.orc_start_fit.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_start_fit.restype = C.c_int
+        L.orc_anneal_chain_fit.argtypes = [vp, vp, vp, vp, vp, i64, C.c_int, i32, i32, dbl, dbl, u64, vp, vp, vp,
+                                           vp, vp]
         _lib = L
     return _lib
 
@@ -407,3 +417,81 @@ def anneal_instance(queue, model, inst_of, k, chains_per_instance: int, chain: i
     res = anneal_chain(sq, model, k * chains_per_instance + chain, iters, T0, alpha, seed, search=search)
     res["ids"] = ids
     return res
+
+
+# ---- the fitted latency predictor taken literally (fit.c) ----
+
+KIND_TTFT_TPOT = 3
+# Table 2 of the paper (milliseconds), exactly in integer units of 10 ns
+TABLE2_10NS = dict(ap=10_000, bp=570_000, cp=1_000, dp=4_367_000, ad=20, bd=27_500, cd=88, dd=1_585_000)
+
+
+class FitModel(C.Structure):
+    _fields_ = [("max_batch", C.c_int32), ("policy", C.c_int32), ("ap", C.c_int64), ("bp", C.c_int64),
+                ("cp", C.c_int64), ("dp", C.c_int64), ("ad", C.c_int64), ("bd", C.c_int64), ("cd", C.c_int64),
+                ("dd", C.c_int64), ("t_ref", C.c_int64), ("swap_threshold", C.c_uint64)]
+
+    def __init__(self, max_batch, policy=0, ap=0, bp=0, cp=0, dp=0, ad=0, bd=0, cd=0, dd=0, t_ref=0,
+                 swap_threshold=1 << 31):
+        super().__init__(int(max_batch), int(policy), int(ap), int(bp), int(cp), int(dp), int(ad), int(bd), int(cd),
+                         int(dd), int(t_ref), int(swap_threshold))
+
+
+def _thr2(q, thr2):
+    if thr2 is None:
+        return None
+    a = np.ascontiguousarray(thr2, dtype=np.uint32)
+    assert a.shape == (q.n,)
+    return a
+
+
+def fit_prefill(fm: FitModel, b: int, l: int) -> int:
+    return int(lib().orc_fit_prefill(C.byref(fm), int(b), int(l)))
+
+
+def fit_decode(fm: FitModel, b: int, l: int, L: int) -> int:
+    return int(lib().orc_fit_decode(C.byref(fm), int(b), int(l), int(L)))
+
+
+def replay_fit(queue, fm: FitModel, perm, starts=None, thr2=None, detail: bool = False):
+    a = _Args(queue, _NoModel())
+    perm = np.ascontiguousarray(perm, dtype=np.uint16)
+    st = None if starts is None else np.ascontiguousarray(starts, dtype=np.uint8)
+    t2 = _thr2(a, thr2)
+    nm, ts = C.c_int64(), C.c_int64()
+    ttft = np.zeros(a.n, np.int64)
+    e2e = np.zeros(a.n, np.int64)
+    lib().orc_replay_fit(a.qp, C.byref(fm), _p(perm), _p(st) if st is not None else None,
+                         _p(t2) if t2 is not None else None, C.byref(nm), C.byref(ts), _p(ttft), _p(e2e))
+    if detail:
+        return nm.value, ts.value, ttft, e2e
+    return nm.value, ts.value
+
+
+def start_fit(queue, fm: FitModel, search=None, thr2=None):
+    a = _Args(queue, _NoModel())
+    t2 = _thr2(a, thr2)
+    st = np.zeros(a.n, np.uint16)
+    t_ref, sn, stt = C.c_int64(), C.c_int64(), C.c_int64()
+    allmet = lib().orc_start_fit(a.qp, C.byref(fm), _search(search), _p(t2) if t2 is not None else None, _p(st),
+                                 C.byref(t_ref), C.byref(sn), C.byref(stt))
+    return st, t_ref.value, bool(allmet), sn.value, stt.value
+
+
+def anneal_chain_fit(queue, fm: FitModel, chain: int, iters: int, T0: float, alpha: float, seed: int,
+                     search=None, thr2=None, start_info=None) -> dict:
+    a = _Args(queue, _NoModel())
+    t2 = _thr2(a, thr2)
+    if start_info is None:
+        start_info = start_fit(queue, fm, search, thr2)
+    st, t_ref, allmet = start_info[0], start_info[1], start_info[2]
+    st = np.ascontiguousarray(st, dtype=np.uint16)
+    cur = np.zeros(a.n, np.uint16)
+    best = np.zeros(a.n, np.uint16)
+    cst = np.zeros(a.n, np.uint8)
+    bst = np.zeros(a.n, np.uint8)
+    rec = np.zeros(8, np.int64)
+    lib().orc_anneal_chain_fit(a.qp, C.byref(fm), _search(search), _p(t2) if t2 is not None else None, _p(st),
+                               int(t_ref), int(allmet), int(chain), int(iters), float(T0), float(alpha), int(seed),
+                               _p(cur), _p(cst), _p(best), _p(bst), _p(rec))
+    return dict(cur=cur, cur_starts=cst, best=best, best_starts=bst, rec=rec)

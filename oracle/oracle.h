@@ -200,4 +200,38 @@ void orc_anneal_chain_batches_ex(const orc_queue *q, const orc_model *m, const o
  * assignments, round-robin for equal capacities, and per-iteration capacity bounds. */
 void orc_assign(const orc_queue *q, int32_t instances, const int64_t *capacity, int32_t *inst_out);
 
+/* ---- the fitted latency predictor taken literally (fit.c) ----
+ * Per request in a static batch of b: t_p(b, l) = ap b l + bp b + cp l + dp; decode
+ * sum_{k=1..L} tau_d(b, l + k), tau_d(b, l) = ad b l + bd b + cd l + dd; a batch lasts as
+ * long as its slowest member. Kind ORC_TTFT_TPOT: TTFT <= thr and TPOT <= thr2 (the
+ * paper's chat SLO), thr2 from a second array. All times in the caller's unit. */
+enum { ORC_TTFT_TPOT = 3 };
+typedef struct {
+  int32_t max_batch, policy;  /* policy: ORC_STATIC (maximum-size batches) or ORC_STATIC_SEARCH */
+  int64_t ap, bp, cp, dp, ad, bd, cd, dd;
+  int64_t t_ref;              /* Metropolis scale; 0: total latency of the input order */
+  uint64_t swap_threshold;    /* fixed-size batches: swap iff w0 < this, else insert */
+} orc_fit_model;
+
+int64_t orc_fit_prefill(const orc_fit_model *f, int64_t b, int64_t l);
+int64_t orc_fit_decode(const orc_fit_model *f, int64_t b, int64_t l, int64_t L);
+
+/* Timeline of one order (starts: nullable, maximum-size batches). (-1, -1) for an order
+ * that is not a permutation, an invalid layout, a kind above 3, or kind 3 without thr2.
+ * Pinned by hand-worked timelines with the paper's Table 2 coefficients, the closed form
+ * of the decode sum, batch size 1 (Smith's rule) and the dual kind's two special cases. */
+int orc_replay_fit(const orc_queue *q, const orc_fit_model *f, const uint16_t *perm, const uint8_t *starts,
+                   const uint32_t *thr2, int64_t *n_met, int64_t *t_sum, int64_t *ttft, int64_t *e2e);
+
+/* Start order (requests sorted by their latency alone, b = 1; the input order when it is
+ * strictly better, unless the early exit applies) and one chain: fixed-size batches with
+ * swap / insert moves, or searched batch sizes with squeeze / delay / swap, as the other
+ * chains. Parity unpinned (trajectory). */
+int orc_start_fit(const orc_queue *q, const orc_fit_model *f, const orc_search *s, const uint32_t *thr2,
+                  uint16_t *start, int64_t *t_ref, int64_t *start_n, int64_t *start_t);
+void orc_anneal_chain_fit(const orc_queue *q, const orc_fit_model *f, const orc_search *s, const uint32_t *thr2,
+                          const uint16_t *start, int64_t t_ref, int allmet, int32_t chain, int32_t iters, double T0,
+                          double alpha, uint64_t seed, uint16_t *cur, uint8_t *cur_starts, uint16_t *best,
+                          uint8_t *best_starts, int64_t *rec);
+
 #endif
