@@ -170,6 +170,48 @@ int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, cons
  * finite, or tau outside (0, 1). */
 int32_t sched_levels(double T0, double T_thres, double tau);
 
+/* ---- the Latency Predictor's fitted model taken literally ----
+ * Each member of a static batch of b requests has its own prediction (equations for t_p,
+ * tau_d and t_d, with their batch-size interaction terms): prefill
+ *   t_p(b, l) = ap * b * l + bp * b + cp * l + dp,
+ * decode summed over its l_out tokens of tau_d(b, l + k) = ad * b * (l + k) + bd * b +
+ * cd * (l + k) + dd; TTFT = wait + t_p, e2e = wait + t_p + t_d, TPOT = t_d / l_out. A batch
+ * lasts as long as its slowest member and waits for every earlier batch. Coefficients are
+ * integers >= 0 in one time unit of the caller's choice, thresholds in the same unit (the
+ * paper's Table 2, in ms, is exact in units of 10 ns: ap 10000, bp 570000, cp 1000,
+ * dp 4367000, ad 20, bd 27500, cd 88, dd 1585000). Host struct. */
+typedef struct {
+  int32_t max_batch;        /* 1 .. SCHED_MAX_BATCH */
+  int32_t policy;           /* SCHED_STATIC (maximum-size batches) or SCHED_STATIC_SEARCH */
+  int64_t ap, bp, cp, dp;   /* prefill */
+  int64_t ad, bd, cd, dd;   /* per-token decode */
+  int64_t t_ref;            /* Metropolis latency scale; 0 => total latency of the input order */
+  uint64_t swap_threshold;  /* SCHED_STATIC: swap iff Philox word 0 < this, else insert */
+} sched_fit_model_t;
+
+/* The paper's chat SLO (the definition of x_i for h_i = 0): TTFT <= thr_us AND
+ * TPOT <= tpot_thr, the second threshold from the tpot_thr array of the fitted-model calls. */
+enum { SCHED_TTFT_TPOT = 3 };
+
+/* sched_eval / sched_eval_batches under the fitted model.
+ *   tpot_thr : nullable DEVICE n x uint32, the TPOT thresholds of SCHED_TTFT_TPOT requests
+ *              (SCHED_EINVAL for a queue with that kind when it is null)
+ *   starts   : nullable DEVICE k x n uint8 batch layouts (as for sched_eval_batches); null =
+ *              maximum-size batches
+ * Other arguments, outputs and errors as for sched_eval_batches; SCHED_ERANGE when the
+ * latencies could overflow int64. */
+int sched_eval_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
+                   const uint16_t *perms, const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail,
+                   hipStream_t stream);
+
+/* sched_anneal_ex under the fitted model: the start order sorts requests by their latency
+ * alone (b = 1); fixed-size batches take swap / insert proposals and SCHED_STATIC_SEARCH the
+ * squeeze / delay / swap moves (layouts read back with sched_starts); every proposal is
+ * replayed in full. Readouts as for sched_anneal. The ratio objective needs dp + dd >= 1. */
+int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
+                     const sched_search_t *search, int32_t chains, int32_t iters, double T0, double alpha,
+                     uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* ---- several serving instances (Scheduling Solution section, Algorithm 2) ----
  * Callers: a scheduler in front of several LLM instances that first assigns the newly
  * arrived requests to instances and then orders each instance's requests. */

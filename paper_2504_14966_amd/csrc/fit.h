@@ -1,0 +1,329 @@
+// The Latency Predictor's fitted model taken literally (gfx950, wave64).
+//
+// Each member of a static batch of b requests has its own prediction: prefill
+//   t_p(b, l) = ap b l + bp b + cp l + dp,
+// and decode summed over its L output tokens of tau_d(b, l + k) = ad b (l + k) + bd b +
+// cd (l + k) + dd, which is in closed form
+//   t_d = L (bd b + dd) + (ad b + cd) (L l + L (L + 1) / 2).
+// TTFT = wait + t_p, e2e = wait + t_p + t_d, TPOT = t_d / L; a batch lasts as long as its
+// slowest member and waits for every earlier batch. Coefficients are integers in the
+// caller's time unit (the paper's Table 2, in milliseconds, is exact in units of 10 ns).
+//
+// SLO kinds: the three single ones and kind 3, the paper's chat SLO (TTFT <= thr and TPOT
+// <= thr2, thr2 from a second per-request array).
+//
+// Batches are either of the maximum size or given by start flags (the batch-size search),
+// and every proposal is replayed in full, one batch at a time with the members in lanes:
+// per member one closed form, per batch a wave maximum. All arithmetic is 64-bit.
+#pragma once
+#include "anneal_sized.h"
+
+namespace sa {
+
+struct DevFit {
+  int32_t n, B, policy, pad;
+  uint64_t ap, bp, cp, dp, ad, bd, cd, dd;
+};
+
+// Request record: x = l_in | l_out << 16, y = threshold, z = kind, w = second threshold.
+__device__ __forceinline__ void load_fit_requests(const QueuePtrs &q, const uint32_t *thr2, int n, uint4 *req) {
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
+    req[r] = make_uint4(lin | (lout << 16), q.thr[r], (uint32_t)q.kind[r], thr2 ? thr2[r] : 0u);
+  }
+}
+
+__device__ __forceinline__ uint64_t fit_prefill(const DevFit &f, uint64_t b, uint64_t l) {
+  return f.ap * b * l + f.bp * b + f.cp * l + f.dp;
+}
+__device__ __forceinline__ uint64_t fit_decode(const DevFit &f, uint64_t b, uint64_t l, uint64_t L) {
+  return L * (f.bd * b + f.dd) + (f.ad * b + f.cd) * (L * l + L * (L + 1) / 2);
+}
+
+__device__ __forceinline__ bool fit_met(uint32_t kind, uint64_t thr, uint64_t thr2, uint64_t L, uint64_t ttft,
+                                        uint64_t td, uint64_t e2e) {
+  if (kind == 0) return ttft <= thr;
+  if (kind == 2) return e2e <= thr;
+  if (kind == 1) return td <= thr * L;
+  return ttft <= thr && td <= thr2 * L;
+}
+
+// flags: start flags of the layout, or null for batches of the maximum size.
+template <bool DETAIL>
+__device__ Score replay_fit(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm, const uint8_t *flags,
+                            int64_t *detail) {
+  const int lane = lane_id();
+  const int n = f.n;
+  uint64_t S = 0, tl = 0;
+  int64_t nmet = 0;
+  for (int s = 0; s < n;) {
+    const int e = flags ? batch_end(flags, n, s, lane) : min(n, s + f.B);
+    const int b = e - s;
+    const bool valid = lane < b;
+    uint64_t exec = 0;
+    bool met = false;
+    if (valid) {
+      const int r = perm[s + lane];
+      const uint4 rq = req[r];
+      const uint64_t l = rq.x & 0xFFFFu, L = rq.x >> 16;
+      const uint64_t tp = fit_prefill(f, (uint64_t)b, l), td = fit_decode(f, (uint64_t)b, l, L);
+      exec = tp + td;
+      const uint64_t ttft = S + tp, e2e = S + exec;
+      met = fit_met(rq.z, rq.y, rq.w, L, ttft, td, e2e);
+      tl += e2e;
+      if (DETAIL) {
+        detail[2 * r] = (int64_t)ttft;
+        detail[2 * r + 1] = (int64_t)e2e;
+      }
+    }
+    nmet += ballot_count(met);
+    S += wave_max_u64(exec);
+    s = e;
+  }
+  return Score{nmet, wave_sum_u64(tl)};
+}
+
+// K rows: one wave per row; rows validated first ((-1, -1) otherwise). starts nullable.
+template <bool DETAIL>
+__global__ void __launch_bounds__(256) eval_fit_kernel(DevFit f, QueuePtrs q, const uint32_t *__restrict__ thr2,
+                                                        const uint16_t *__restrict__ perms,
+                                                        const uint8_t *__restrict__ starts, int64_t rows,
+                                                        int64_t *__restrict__ out, int64_t *__restrict__ detail) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = f.n;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t per_wave = pb + fb + 32 * 4;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (((size_t)n * 16 + 15) & ~size_t(15)) + (size_t)wave * per_wave;
+  uint16_t *perm = reinterpret_cast<uint16_t *>(wb);
+  uint8_t *flags = wb + pb;
+  uint32_t *bitmap = reinterpret_cast<uint32_t *>(wb + pb + fb);
+  load_fit_requests(q, thr2, n, req);
+  __syncthreads();
+  const int lane = lane_id();
+  const int waves = blockDim.x >> 6;
+  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+    const uint16_t *src = perms + row * n;
+    if (lane < 32) bitmap[lane] = 0u;
+    wave_sync_lds();
+    bool bad = false;
+    for (int p = lane; p < n; p += kWave) {
+      const uint32_t v = src[p];
+      perm[p] = (uint16_t)v;
+      if (starts) flags[p] = starts[row * n + p];
+      if (v >= (uint32_t)n) {
+        bad = true;
+      } else {
+        const uint32_t bit = 1u << (v & 31u);
+        const uint32_t old = atomicOr(&bitmap[v >> 5], bit);
+        if (old & bit) bad = true;
+      }
+    }
+    wave_sync_lds();
+    const bool ok = __ballot(bad) == 0ull && (!starts || layout_ok(flags, n, f.B, lane));
+    if (!ok) {
+      if (lane == 0) {
+        out[2 * row] = -1;
+        out[2 * row + 1] = -1;
+      }
+      continue;
+    }
+    const Score s =
+        replay_fit<DETAIL>(f, req, perm, starts ? flags : nullptr, DETAIL ? detail + row * n * 2 : nullptr);
+    if (lane == 0) {
+      out[2 * row] = s.n;
+      out[2 * row + 1] = (int64_t)s.t;
+    }
+    wave_sync_lds();
+  }
+}
+
+// Algorithm 1 initialisation under the fitted model, one workgroup of 1024 threads: every
+// request's latency alone (b = 1), a stable bitonic sort by (latency, id), the scores of the
+// sorted and the input orders with maximum-size batches, t_ref.
+__global__ void __launch_bounds__(1024) start_fit_kernel(DevFit f, QueuePtrs q, const uint32_t *thr2, int chains,
+                                                          int iters, int64_t t_ref_user, SearchParams srch,
+                                                          unsigned char *ws) {
+  __shared__ uint4 req[1024];
+  __shared__ uint64_t key_solo[1024];
+  __shared__ uint16_t key_id[1024];
+  __shared__ uint16_t ident[1024];
+  const int n = f.n;
+  const int tid = threadIdx.x;
+  load_fit_requests(q, thr2, n, req);
+  int np = 1;
+  while (np < n) np <<= 1;
+  if (tid < np) {
+    if (tid < n) {
+      const uint64_t l = q.in_len[tid], L = q.out_len[tid];
+      key_solo[tid] = fit_prefill(f, 1, l) + fit_decode(f, 1, l, L);
+      key_id[tid] = (uint16_t)tid;
+      ident[tid] = (uint16_t)tid;
+    } else {
+      key_solo[tid] = ~0ull;
+      key_id[tid] = 0xFFFFu;
+    }
+  }
+  __syncthreads();
+  for (int k = 2; k <= np; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      if (tid < np) {
+        const int o = tid ^ j;
+        if (o > tid) {
+          const uint64_t a = key_solo[tid], b = key_solo[o];
+          const uint16_t ia = key_id[tid], ib = key_id[o];
+          const bool a_gt = a > b || (a == b && ia > ib);
+          const bool up = (tid & k) == 0;
+          if (a_gt == up) {
+            key_solo[tid] = b;
+            key_solo[o] = a;
+            key_id[tid] = ib;
+            key_id[o] = ia;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (tid < 64) {
+    const Score sorted = replay_fit<false>(f, req, key_id, nullptr, nullptr);
+    const Score input = replay_fit<false>(f, req, ident, nullptr, nullptr);
+    const bool input_better = srch.objective ? obj_better<1>(input.n, input.t, sorted.n, sorted.t)
+                                             : obj_better<0>(input.n, input.t, sorted.n, sorted.t);
+    const bool use_input = !(srch.early_exit && sorted.n == n) && input_better;
+    uint16_t *start = reinterpret_cast<uint16_t *>(ws + ws_off_start());
+    for (int p = tid; p < n; p += 64) start[p] = use_input ? (uint16_t)p : key_id[p];
+    if (tid == 0) {
+      WsHeader *h = reinterpret_cast<WsHeader *>(ws);
+      h->magic = kWsMagic;
+      h->n = n;
+      h->chains = chains;
+      h->iters = iters;
+      h->policy = f.policy;
+      h->max_batch = f.B;
+      h->objective = srch.objective;
+      h->level_len = srch.level_len;
+      h->early_exit = srch.early_exit;
+      h->t_ref = t_ref_user > 0 ? t_ref_user : (input.t > 1 ? (int64_t)input.t : 1);
+      h->start_n = use_input ? input.n : sorted.n;
+      h->start_t = (int64_t)(use_input ? input.t : sorted.t);
+      h->allmet = sorted.n == n ? 1 : 0;
+      h->best_chain = -1;
+      h->best_n = -1;
+      h->best_t = -1;
+    }
+  }
+}
+
+// One wave per chain, four per workgroup; full replay per proposal. Fixed-size batches take
+// swap / insert proposals (swap iff w0 < swap_thr); the batch-size search takes squeeze /
+// delay / swap. Per-wave LDS: current and candidate orders and flags.
+template <int OBJ>
+__global__ void __launch_bounds__(256) anneal_fit_kernel(DevFit f, QueuePtrs q, const uint32_t *thr2, int chains,
+                                                          int iters, double T0, double alpha, uint32_t key0,
+                                                          uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                          unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = f.n, B = f.B;
+  const bool search = f.policy == 2;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t per_wave = 2 * pb + 2 * fb;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  const int waves = blockDim.x >> 6;
+  unsigned char *wb = lds + (((size_t)n * 16 + 15) & ~size_t(15)) + (size_t)wave * per_wave;
+  uint16_t *cur = reinterpret_cast<uint16_t *>(wb);
+  uint16_t *cand = reinterpret_cast<uint16_t *>(wb + pb);
+  uint8_t *fcur = wb + 2 * pb, *fcand = wb + 2 * pb + fb;
+  load_fit_requests(q, thr2, n, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  const int lane = lane_id();
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref, allmet = h->allmet;
+  int64_t cn = h->start_n;
+  uint64_t ct = (uint64_t)h->start_t;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n), fstride = ws_flag_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  uint8_t *gbest_f = ws + ws_off_best_starts(n, chains) + (size_t)chain * fstride;
+  uint8_t *gcur_f = ws + ws_off_cur_starts(n, chains) + (size_t)chain * fstride;
+  for (int p = lane; p < n; p += kWave) {
+    const uint16_t v = start[p];
+    const uint8_t fl = (uint8_t)(p % B == 0);
+    cur[p] = v;
+    fcur[p] = fl;
+    gbest[p] = v;
+    gbest_f[p] = fl;
+  }
+  wave_sync_lds();
+  int64_t bn = cn, biter = -1, accepts = 0;
+  uint64_t bt = ct, digest = kFnvOffset;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
+  SizedDraws ds;
+  ProposalStream ps;
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
+    uint32_t w3;
+    SizedMove mv;
+    if (search) {
+      if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, (uint32_t)chain, key0, key1);
+      const uint32_t pk = ds.packed(k);
+      w3 = ds.word3(k);
+      mv = plan_move(fcur, n, B, (int)(pk >> 20), (int)(pk & 1023u), (int)((pk >> 10) & 1023u), lane);
+    } else {
+      if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+      const uint32_t pk = ps.packed(k);
+      w3 = ps.word3(k);
+      const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+      // a fixed-size move: swap (op 2) or insert (from i to j, flags untouched)
+      mv = SizedMove{true, ((pk >> 20) & 1u) ? 3 : 2, i, j, j, -1, -1};
+    }
+    if (mv.made) {
+      for (int p = lane; p < n; p += kWave) {
+        cand[p] = cur[p];
+        fcand[p] = fcur[p];
+      }
+      wave_sync_lds();
+      if (mv.op == 3)
+        apply_move_lds(cand, 2, mv.i, mv.j, lane);
+      else
+        apply_sized_move(cand, fcand, mv, lane);
+      const Score s = replay_fit<false>(f, req, cand, fcand, nullptr);
+      if (obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3)) {
+        uint16_t *tp = cur;
+        cur = cand;
+        cand = tp;
+        uint8_t *tf = fcur;
+        fcur = fcand;
+        fcand = tf;
+        cn = s.n;
+        ct = s.t;
+        ++accepts;
+        digest = (digest ^ (uint64_t)k) * kFnvPrime;
+        digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+        digest = (digest ^ ct) * kFnvPrime;
+        if (obj_better<OBJ>(cn, ct, bn, bt)) {
+          bn = cn;
+          bt = ct;
+          biter = k;
+          for (int p = lane; p < n; p += kWave) {
+            gbest[p] = cur[p];
+            gbest_f[p] = fcur[p];
+          }
+        }
+      }
+    }
+    cool.step();
+  }
+  for (int p = lane; p < n; p += kWave) {
+    gcur[p] = cur[p];
+    gcur_f[p] = fcur[p];
+  }
+  if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
+}
+
+}  // namespace sa

@@ -15,6 +15,7 @@
 #include "anneal_wave.h"
 #include "anneal_sized.h"
 #include "multi.h"
+#include "fit.h"
 
 namespace {
 
@@ -47,8 +48,9 @@ int check_model(const sched_model_t *m, int n) {
   return SCHED_OK;
 }
 
-// Reads the queue back (one stream synchronisation) and validates every entry.
-int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h) {
+// Reads the queue back (one stream synchronisation) and validates every entry (kinds up to
+// max_kind).
+int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h, int max_kind = 2) {
   if (!q || q->n < 1 || q->n > SCHED_MAX_N) return SCHED_EINVAL;
   if (!q->in_len || !q->out_len || !q->kind || !q->thr_us) return SCHED_EINVAL;
   const size_t n = (size_t)q->n;
@@ -62,7 +64,7 @@ int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h) {
   HIP_TRY(hipMemcpyAsync(h.thr.data(), q->thr_us, n * 4, hipMemcpyDeviceToHost, stream));
   HIP_TRY(hipStreamSynchronize(stream));
   for (size_t r = 0; r < n; ++r) {
-    if (h.out_len[r] < 1 || h.kind[r] > 2 || h.thr[r] > SCHED_THR_MAX) return SCHED_EINVAL;
+    if (h.out_len[r] < 1 || h.kind[r] > max_kind || h.thr[r] > SCHED_THR_MAX) return SCHED_EINVAL;
   }
   return SCHED_OK;
 }
@@ -86,6 +88,40 @@ int range_check(const HostQueue &h, const sched_model_t *m, int n) {
   const long double tref = m->t_ref_us > 0 ? (long double)m->t_ref_us : tsum;
   if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
   return SCHED_OK;
+}
+
+// The fitted model: every coefficient >= 0, batches of 1 .. 64. A member's time is largest
+// at the largest batch, and a batch lasts at most the sum of its members' times, so the
+// timeline ends before the sum over requests of their time in a batch of min(n, B); the sum
+// of latencies, the Metropolis delta and (for the ratio) the cross products stay below 2^62.
+int check_fit(const sched_fit_model_t *f) {
+  if (!f || f->max_batch < 1 || f->max_batch > SCHED_MAX_BATCH) return SCHED_EINVAL;
+  if (f->policy != SCHED_STATIC && f->policy != SCHED_STATIC_SEARCH) return SCHED_EINVAL;
+  if (f->ap < 0 || f->bp < 0 || f->cp < 0 || f->dp < 0 || f->ad < 0 || f->bd < 0 || f->cd < 0 || f->dd < 0 ||
+      f->t_ref < 0 || f->swap_threshold > (1ull << 32))
+    return SCHED_EINVAL;
+  return SCHED_OK;
+}
+
+int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool ratio) {
+  const long double b = std::min(n, f->max_batch);
+  long double end = 0;
+  for (int r = 0; r < n; ++r) {
+    const long double l = h.in_len[r], L = h.out_len[r];
+    end += (long double)f->ap * b * l + (long double)f->bp * b + (long double)f->cp * l + (long double)f->dp +
+           L * ((long double)f->bd * b + (long double)f->dd) +
+           ((long double)f->ad * b + (long double)f->cd) * (L * l + L * (L + 1) / 2);
+  }
+  const long double tsum = end * n, lim = std::ldexp(1.0L, 62);
+  const long double tref = f->t_ref > 0 ? (long double)f->t_ref : tsum;
+  if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
+  if (ratio && !(tsum * (n + 1) < lim)) return SCHED_ERANGE;
+  return SCHED_OK;
+}
+
+sa::DevFit dev_fit(const sched_fit_model_t *f, int n) {
+  return sa::DevFit{n, f->max_batch, f->policy, 0, (uint64_t)f->ap, (uint64_t)f->bp, (uint64_t)f->cp,
+                    (uint64_t)f->dp, (uint64_t)f->ad, (uint64_t)f->bd, (uint64_t)f->cd, (uint64_t)f->dd};
 }
 
 // The ratio objective compares n1 t2 with n2 t1 and forms n' t - n t' in int64: the
@@ -668,6 +704,74 @@ int sched_multi_best(const void *ws, int32_t instances, uint16_t *orders, int64_
                      hipStream_t stream) {
   if (!ws || !orders || instances < 1 || instances > SCHED_MAX_INSTANCES) return SCHED_EINVAL;
   sa::multi_best_kernel<<<instances, 256, 0, stream>>>(static_cast<const unsigned char *>(ws), orders, keys, counts);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_eval_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
+                   const uint16_t *perms, const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail,
+                   hipStream_t stream) {
+  if (k < 0) return SCHED_EINVAL;
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  int rc = check_fit(fit);
+  if (rc) return rc;
+  if (k > 0 && (!perms || !out)) return SCHED_EINVAL;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
+  if ((rc = fit_range_check(h, fit, queue->n, false))) return rc;
+  if (k == 0) return SCHED_OK;
+  const int n = queue->n;
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 32 * 4);
+  const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
+  const sa::DevFit df = dev_fit(fit, n);
+  if (detail)
+    sa::eval_fit_kernel<true><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, perms, starts, k, out, detail);
+  else
+    sa::eval_fit_kernel<false><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, perms, starts, k, out,
+                                                           nullptr);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
+int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
+                     const sched_search_t *search, int32_t chains, int32_t iters, double T0, double alpha,
+                     uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
+  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
+    return SCHED_EINVAL;
+  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
+  if (search) {
+    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
+        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
+      return SCHED_EINVAL;
+    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
+  }
+  int rc = check_fit(fit);
+  if (rc) return rc;
+  if (srch.objective == SCHED_OBJ_RATIO && fit->dp + fit->dd < 1) return SCHED_EINVAL;  // positive latencies
+  if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
+  if (ws_bytes < sched_ws_bytes(queue->n, chains)) return SCHED_ENOSPC;
+  HostQueue h;
+  if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
+  if ((rc = fit_range_check(h, fit, queue->n, srch.objective == SCHED_OBJ_RATIO))) return rc;
+  const int n = queue->n;
+  const sa::DevFit df = dev_fit(fit, n);
+  unsigned char *w = static_cast<unsigned char *>(ws);
+  sa::start_fit_kernel<<<1, 1024, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, fit->t_ref, srch, w);
+  HIP_TRY(hipGetLastError());
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb);
+  const int grid = (chains + 3) / 4;
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  if (srch.objective)
+    sa::anneal_fit_kernel<1><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0, k1,
+                                                         fit->swap_threshold, srch, w);
+  else
+    sa::anneal_fit_kernel<0><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0, k1,
+                                                         fit->swap_threshold, srch, w);
+  HIP_TRY(hipGetLastError());
+  sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }

@@ -20,7 +20,8 @@ SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, 
 EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
            "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_assign",
            "sched_ws_bytes_multi", "sched_anneal_multi", "sched_multi_instance_ws", "sched_multi_best",
-           "sched_strerror")
+           "sched_eval_fit", "sched_anneal_fit", "sched_strerror")
+KIND_TTFT_TPOT = 3
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 OBJ_LEX, OBJ_RATIO = 0, 1
 
@@ -88,6 +89,10 @@ def load_library(path: str = LIB_PATH):
     L.sched_multi_instance_ws.restype = vp
     L.sched_multi_best.argtypes = [vp, i32, vp, vp, vp, vp]
     L.sched_multi_best.restype = C.c_int
+    L.sched_eval_fit.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    L.sched_eval_fit.restype = C.c_int
+    L.sched_anneal_fit.argtypes = [vp, vp, vp, vp, i32, i32, dbl, dbl, u64, vp, sz, vp]
+    L.sched_anneal_fit.restype = C.c_int
     L.sched_best.argtypes = [vp, vp, vp, vp]
     L.sched_best.restype = C.c_int
     L.sched_chains.argtypes = [vp, vp, vp, vp, vp]
@@ -336,3 +341,54 @@ def sched_multi_best(mws: MultiWorkspace, stream=None):
     _check(load_library().sched_multi_best(_ptr(mws.buf), mws.instances, _ptr(orders), _ptr(keys), _ptr(counts),
                                            _stream(stream)))
     return orders, keys, counts
+
+
+# ---- the fitted latency model ----
+
+class FitModel(C.Structure):
+    """sched_fit_model_t: per-request prefill ap*b*l + bp*b + cp*l + dp and per-token decode
+    ad*b*l + bd*b + cd*l + dd in one integer time unit (Table 2 in units of 10 ns: TABLE2_10NS)."""
+    _fields_ = [("max_batch", C.c_int32), ("policy", C.c_int32), ("ap", C.c_int64), ("bp", C.c_int64),
+                ("cp", C.c_int64), ("dp", C.c_int64), ("ad", C.c_int64), ("bd", C.c_int64), ("cd", C.c_int64),
+                ("dd", C.c_int64), ("t_ref", C.c_int64), ("swap_threshold", C.c_uint64)]
+
+    def __init__(self, max_batch, policy=0, ap=0, bp=0, cp=0, dp=0, ad=0, bd=0, cd=0, dd=0, t_ref=0,
+                 swap_threshold=1 << 31):
+        super().__init__(int(max_batch), int(policy), int(ap), int(bp), int(cp), int(dp), int(ad), int(bd), int(cd),
+                         int(dd), int(t_ref), int(swap_threshold))
+
+
+TABLE2_10NS = dict(ap=10_000, bp=570_000, cp=1_000, dp=4_367_000, ad=20, bd=27_500, cd=88, dd=1_585_000)
+
+
+def thr_to_device(thr: np.ndarray, device="cuda") -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(thr, dtype=np.uint32).view(np.int32)).to(device)
+
+
+def sched_eval_fit(dq: DeviceQueue, fit: FitModel, perms: torch.Tensor, starts: torch.Tensor | None = None,
+                   tpot_thr: torch.Tensor | None = None, detail: bool = False, stream=None):
+    L = load_library()
+    k = int(perms.shape[0])
+    if perms.dim() != 2 or int(perms.shape[1]) != dq.n:
+        raise ValueError("perms must be k x n")
+    if starts is not None and (tuple(starts.shape) != tuple(perms.shape) or starts.dtype != torch.uint8):
+        raise ValueError("starts must be k x n uint8")
+    out = torch.empty((k, 2), dtype=torch.int64, device=perms.device)
+    det = torch.zeros((k, dq.n, 2), dtype=torch.int64, device=perms.device) if detail else None
+    q = dq.c()
+    _check(L.sched_eval_fit(C.byref(q), C.byref(fit), _ptr(tpot_thr), _ptr(perms), _ptr(starts), k, _ptr(out),
+                            _ptr(det), _stream(stream)))
+    return (out, det) if detail else out
+
+
+def sched_anneal_fit(dq: DeviceQueue, fit: FitModel, chains: int, iters: int, T0: float, alpha: float, seed: int,
+                     tpot_thr: torch.Tensor | None = None, search: Search | None = None,
+                     ws: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    L = load_library()
+    if ws is None:
+        ws = alloc_ws(dq.n, chains)
+    q = dq.c()
+    _check(L.sched_anneal_fit(C.byref(q), C.byref(fit), _ptr(tpot_thr), C.byref(search) if search is not None else None,
+                              int(chains), int(iters), float(T0), float(alpha), int(seed) & (2**64 - 1), _ptr(ws),
+                              int(ws.numel()), _stream(stream)))
+    return ws

@@ -228,3 +228,21 @@ def multi_workload() -> Workload:
                  chains=512, iters=2000, T0=1.0, alpha=0.999)
     W.extra = dict(instances=8, capacity=[40_000] * 8)
     return W
+
+
+# Table 2 of the paper (milliseconds) in integer units of 10 ns
+TABLE2_10NS = dict(ap=10_000, bp=570_000, cp=1_000, dp=4_367_000, ad=20, bd=27_500, cd=88, dd=1_585_000)
+
+
+def chat_code_queue_10ns(n: int, seed: int):
+    """The two-class queue for the fitted model: code requests keep an end-to-end SLO, chat
+    requests take the paper's chat SLO (TTFT and TPOT together); thresholds in units of
+    10 ns. Code: e2e 30 s; chat: TTFT 10 s and TPOT 50 ms (the paper's SLO settings).
+    Returns the queue and the per-request TPOT thresholds (0 for code requests)."""
+    q = two_class_queue(n, seed)
+    # the class labels two_class_queue drew (same stream): 0 code, 1 chat
+    cls = _rng(seed, _S_CLASS).permutation(np.concatenate([np.zeros(n // 2, np.uint8), np.ones(n // 2, np.uint8)]))
+    kind = np.where(cls == 0, 2, 3).astype(np.uint8)
+    thr = np.where(cls == 0, 3_000_000_000, 1_000_000_000).astype(np.uint32)
+    thr2 = np.where(cls == 0, 0, 5_000_000).astype(np.uint32)
+    return Queue(q.in_len, q.out_len, kind, thr), thr2
