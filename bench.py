@@ -363,6 +363,27 @@ def main():
                                            one_after_another_ms=ms_seq)
         log(f"[bench] {Wm.name}: {ci / (ms_one * 1e-3):.4g} chain-iters/s in one launch ({ms_one:.1f} ms, "
             f"assignment included); instances one after another {ms_seq:.1f} ms")
+        # the fitted model taken literally (Table 2 in units of 10 ns) on 256 chat / code
+        # requests with the paper's SLOs (code: e2e 30 s; chat: TTFT 10 s and TPOT 50 ms),
+        # batch sizes searched (max 16), 2048 chains x 2000 proposals
+        from paper_2504_14966_amd.workloads import TABLE2_10NS, chat_code_queue_10ns
+        qf, thr2 = chat_code_queue_10ns(256, 0)
+        fit = sl.FitModel(16, sl.POLICY_STATIC_SEARCH, **TABLE2_10NS)
+        dqf, t2 = sl.DeviceQueue.from_queue(qf), sl.thr_to_device(thr2)
+        wsf = sl.alloc_ws(qf.n, 2048)
+        sl.sched_anneal_fit(dqf, fit, 2048, 2000, 1.0, 0.999, 0, tpot_thr=t2, ws=wsf)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        sl.sched_anneal_fit(dqf, fit, 2048, 2000, 1.0, 0.999, 0, tpot_thr=t2, ws=wsf)
+        b.record()
+        _, keyf = sl.sched_best(wsf, qf.n)
+        torch.cuda.synchronize()
+        msf = a.elapsed_time(b)
+        extras["anneal_fit-table2-chatcode-n256-b16-search"] = dict(ms=msf, chain_iters_per_s=2048 * 2000 / (msf * 1e-3),
+                                                                    best=keyf.cpu().tolist(), time_unit="10 ns")
+        log(f"[bench] fitted model, chat/code n256 batch sizes searched: {2048 * 2000 / (msf * 1e-3):.4g} "
+            f"chain-iters/s ({msf:.1f} ms), best {keyf.cpu().tolist()}")
         # the joint order / batch-size search (squeeze, delay and swap moves) on the same queues
         for wl in (2, 4):
             Wx = search_workload(wl)
