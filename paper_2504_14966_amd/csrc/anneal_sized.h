@@ -462,10 +462,30 @@ __device__ __forceinline__ BatchNew batch_pass(const SizedState &c, int xs, int 
   return BatchNew{Fn, limn, r, max(Mx, Fg)};
 }
 
-// met-count change of positions [a, b) when their batch starts move by delta (mod 2^32)
+// met-count change of positions [a, b) when their batch starts move by delta (mod 2^32).
+// Long ranges take four chunks of 64 positions per round with every load issued before the
+// compares; short ones a chunk at a time.
 __device__ __forceinline__ int recount_shift(const SizedState &c, int a, int b, uint32_t delta) {
   int dn = 0;
-  for (int c0 = a; c0 < b; c0 += kWave) {
+  int c0 = a;
+  if (b - a > 2 * kWave) {
+    for (; c0 + 4 * kWave <= b; c0 += 4 * kWave) {
+      uint32_t sv[4], lv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        sv[u] = c.S[c0 + u * kWave + c.lane];
+        lv[u] = c.lim[c0 + u * kWave + c.lane];
+      }
+      uint32_t cnt_now = 0, cnt_was = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        cnt_was += (uint32_t)__popcll(__ballot(sv[u] < lv[u]));
+        cnt_now += (uint32_t)__popcll(__ballot(sv[u] + delta < lv[u]));
+      }
+      dn += (int)cnt_now - (int)cnt_was;
+    }
+  }
+  for (; c0 < b; c0 += kWave) {
     const int p = c0 + c.lane;
     bool was = false, now = false;
     if (p < b) {
@@ -478,8 +498,19 @@ __device__ __forceinline__ int recount_shift(const SizedState &c, int a, int b, 
   return dn;
 }
 
+// S[p] += delta for p in [a, b_incl]; long ranges four chunks per round, loads before stores
 __device__ __forceinline__ void apply_shift(const SizedState &c, int a, int b_incl, uint32_t delta) {
-  for (int c0 = a; c0 <= b_incl; c0 += kWave) {
+  int c0 = a;
+  if (b_incl - a >= 2 * kWave) {
+    for (; c0 + 4 * kWave <= b_incl + 1; c0 += 4 * kWave) {
+      uint32_t sv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sv[u] = c.S[c0 + u * kWave + c.lane];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) c.S[c0 + u * kWave + c.lane] = sv[u] + delta;
+    }
+  }
+  for (; c0 <= b_incl; c0 += kWave) {
     const int p = c0 + c.lane;
     if (p <= b_incl) c.S[p] += delta;
   }
