@@ -502,25 +502,10 @@ struct StaticChain {
   __device__ __forceinline__ void apply_move(int type, int i, int j) { apply_move_lds(perm, type, i, j, lane); }
 };
 
-// One wave per chain; blockDim / 64 chains per workgroup.
-template <int LG, int OBJ>
-__global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
-                                                              int iters, double T0, double alpha, uint32_t key0,
-                                                              uint32_t key1, uint64_t swap_thr, SearchParams srch,
-                                                              unsigned char *ws) {
-  extern __shared__ __align__(16) unsigned char lds[];
-  const int n = m.n, B = m.B;
-  const int M = (n + B - 1) / B;
-  constexpr int G = kWave >> LG;
-  const int R = (M + G - 1) / G;
-  const int waves = blockDim.x >> 6;
-  uint4 *req = reinterpret_cast<uint4 *>(lds);
-  const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
-  const size_t f_b = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
-  const size_t rec_b = (size_t)M * sizeof(BatchRec);
-  const size_t per_wave = perm_b + f_b + 2 * rec_b;
-  const int wave = uniform((int)(threadIdx.x >> 6));
-  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
+// The request records of the static delta kernels, staged by the whole workgroup: n records
+// and a zero spare record at index n.
+__device__ __forceinline__ void load_static_records(const QueuePtrs &q, const DevModel &m, uint4 *req) {
+  const int n = m.n;
   for (int r = threadIdx.x; r <= n; r += blockDim.x) {
     if (r == n) {
       req[r] = make_uint4(0u, 0u, 0u, 0u);  // spare record for lanes outside a batch
@@ -534,9 +519,28 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
     const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
     req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
   }
-  __syncthreads();
-  const int chain = uniform((int)blockIdx.x * waves + wave);
-  if (chain >= chains) return;
+}
+
+// LDS of one chain of the row kernel: order, finish offsets, current and candidate batch records.
+__host__ __device__ __forceinline__ size_t static_chain_bytes(int n, int B) {
+  const size_t M = (size_t)(n + B - 1) / B;
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(BatchRec);
+}
+
+// One chain of the row kernel by one wave: record slot `chain`, Philox chain index
+// `rng_chain`, the request records in `req`, the chain's LDS at `wb`.
+template <int LG, int OBJ>
+__device__ void anneal_static_body(const DevModel &m, const StaticParams &sp, const uint4 *req, unsigned char *wb,
+                                   int chains, int chain, uint32_t rng_chain, int iters, double T0, double alpha,
+                                   uint32_t key0, uint32_t key1, uint64_t swap_thr, const SearchParams &srch,
+                                   unsigned char *ws) {
+  const int n = m.n, B = m.B;
+  const int M = (n + B - 1) / B;
+  constexpr int G = kWave >> LG;
+  const int R = (M + G - 1) / G;
+  const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
+  const size_t f_b = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
+  const size_t rec_b = (size_t)M * sizeof(BatchRec);
   const int lane = lane_id();
   StaticChain<LG> st{req,
                      reinterpret_cast<uint16_t *>(wb),
@@ -568,7 +572,7 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
   ProposalStream ps;
   const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
   for (int k = 0; k < iters_run; ++k) {
-    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, 0);
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     Move mv;
@@ -624,6 +628,26 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
     rec[6] = (int64_t)digest;
     rec[7] = allmet;
   }
+}
+
+// One wave per chain; blockDim / 64 chains per workgroup.
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
+                                                              int iters, double T0, double alpha, uint32_t key0,
+                                                              uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                              unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * static_chain_bytes(n, m.B);
+  load_static_records(q, m, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  anneal_static_body<LG, OBJ>(m, sp, req, wb, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr,
+                              srch, ws);
 }
 
 }  // namespace sa

@@ -329,39 +329,25 @@ struct WaveChain {
 };
 
 
-// One wave per chain; blockDim / 64 chains per workgroup. OBJ: objective (0 attainment,
-// then total latency; 1 ratio n / t).
+// LDS of one chain of the one-batch-per-wave kernel: order, finish offsets (two spare
+// slots), 48 bytes of proposal table per batch.
+__host__ __device__ __forceinline__ size_t wave_chain_bytes(int n, int B) {
+  const size_t M = (size_t)(n + B - 1) / B;
+  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 2) * 4 + 15) & ~size_t(15)) + M * 48;
+}
+
+// One chain by one wave: record slot `chain`, Philox chain index `rng_chain`, the request
+// records in `req`, the chain's LDS at `wb`. OBJ: objective (0 attainment, then total
+// latency; 1 ratio n / t).
 template <int OBJ>
-__global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
-                                                            int iters, double T0, double alpha, uint32_t key0,
-                                                            uint32_t key1, uint64_t swap_thr, SearchParams srch,
-                                                            unsigned char *ws) {
-  extern __shared__ __align__(16) unsigned char lds[];
+__device__ void anneal_wave_body(const DevModel &m, const StaticParams &sp, const uint4 *req, unsigned char *wb,
+                                 int chains, int chain, uint32_t rng_chain, int iters, double T0, double alpha,
+                                 uint32_t key0, uint32_t key1, uint64_t swap_thr, const SearchParams &srch,
+                                 unsigned char *ws) {
   const int n = m.n, B = m.B;
   const int M = (n + B - 1) / B;
-  const int waves = blockDim.x >> 6;
-  uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t perm_b = ((size_t)n * 2 + 15) & ~size_t(15);
   const size_t f_b = ((size_t)(n + 2) * 4 + 15) & ~size_t(15);
-  const size_t per_wave = perm_b + f_b + (size_t)M * 48;
-  const int wave = uniform((int)(threadIdx.x >> 6));
-  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
-  for (int r = threadIdx.x; r <= n; r += blockDim.x) {
-    if (r == n) {
-      req[r] = make_uint4(0u, 0u, 0u, 0u);  // spare record for lanes outside a batch
-      continue;
-    }
-    const uint32_t lin = q.in_len[r], lout = q.out_len[r];
-    const uint32_t pf = (uint32_t)(m.p0 + m.p1 * lin);
-    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
-    const uint32_t kind = q.kind[r];
-    const uint64_t thr_l = (uint64_t)q.thr[r] * lout;
-    const uint32_t thr = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : q.thr[r];
-    req[r] = make_uint4(lin | (lout << 16), thr, kind | (e << 2), pf);
-  }
-  __syncthreads();
-  const int chain = uniform((int)blockIdx.x * waves + wave);
-  if (chain >= chains) return;
   const int lane = lane_id();
   WaveChain st;
   st.req = req;
@@ -400,7 +386,7 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
   ProposalStream ps;  // at most 32 batches: the batch indices travel with the move
   const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
   for (int k = 0; k < iters_run; ++k) {
-    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, (uint32_t)chain, key0, key1, swap_thr, sp.bmagic);
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, sp.bmagic);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     Move mv;
@@ -454,6 +440,26 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
     rec[6] = (int64_t)digest;
     rec[7] = allmet;
   }
+}
+
+// One wave per chain; blockDim / 64 chains per workgroup.
+template <int OBJ>
+__global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
+                                                            int iters, double T0, double alpha, uint32_t key0,
+                                                            uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                            unsigned char *ws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int n = m.n;
+  const int waves = blockDim.x >> 6;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * wave_chain_bytes(n, m.B);
+  load_static_records(q, m, req);
+  __syncthreads();
+  const int chain = uniform((int)blockIdx.x * waves + wave);
+  if (chain >= chains) return;
+  anneal_wave_body<OBJ>(m, sp, req, wb, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                        ws);
 }
 
 }  // namespace sa

@@ -21,6 +21,8 @@
 // out for the instance's request count (so the single-queue readouts work on it), followed
 // by the instance's queue (structure of arrays) and the global ids of its requests.
 #pragma once
+#include "anneal_static.h"
+#include "anneal_wave.h"
 #include "kernels.h"
 
 namespace sa {
@@ -191,6 +193,41 @@ __global__ void __launch_bounds__(kBlock) multi_anneal_kernel(DevModel m, int n,
   if (chain >= chains) return;
   anneal_chain_body<OBJ>(mk, req, wbase, chains, chain, (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1,
                          swap_thr, srch, slot);
+}
+
+// Static admission with the delta kernels: instances x groups of `waves` chains, one wave per
+// chain; LG = log2 of the batch lanes' group width (0..5: the row kernel) or 6 (one batch per
+// wave). LDS is sized by the host for the largest instance; each workgroup lays it out for
+// its own instance's request count.
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(1024) multi_static_kernel(DevModel m, StaticParams sp, int n, int instances,
+                                                             int chains, int groups, int iters, double T0,
+                                                             double alpha, uint32_t key0, uint32_t key1,
+                                                             uint64_t swap_thr, SearchParams srch, unsigned char *mws) {
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
+  const int nk = slot_n(mws, k);
+  if (nk == 0) return;
+  unsigned char *slot = mws + mws_off_slot(n, instances, chains, k);
+  const SlotQueue sq = slot_queue(slot, n, chains);
+  DevModel mk = m;
+  mk.n = nk;
+  uint4 *req = reinterpret_cast<uint4 *>(lds);
+  const int waves = blockDim.x >> 6;
+  const int wave = uniform((int)(threadIdx.x >> 6));
+  const size_t per = LG == 6 ? wave_chain_bytes(nk, m.B) : static_chain_bytes(nk, m.B);
+  unsigned char *wb = lds + (size_t)(nk + 1) * 16 + (size_t)wave * per;
+  load_static_records(QueuePtrs{sq.in_len, sq.out_len, sq.kind, sq.thr}, mk, req);
+  __syncthreads();
+  const int chain = uniform(g * waves + wave);
+  if (chain >= chains) return;
+  const uint32_t rng_chain = (uint32_t)(k * chains + chain);
+  if constexpr (LG == 6)
+    anneal_wave_body<OBJ>(mk, sp, req, wb, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                          slot);
+  else
+    anneal_static_body<LG, OBJ>(mk, sp, req, wb, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr,
+                                srch, slot);
 }
 
 // One workgroup per instance: its winner over chains.

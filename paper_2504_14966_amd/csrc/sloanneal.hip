@@ -229,17 +229,8 @@ bool static_narrow(const HostQueue &h, const sched_model_t *m, int n) {
          (long double)m->d0 < two24;
 }
 
-size_t static_wave_lds(int n, int B) {
-  const size_t M = (size_t)(n + B - 1) / B;
-  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 1) * 4 + 15) & ~size_t(15)) + 2 * M * sizeof(sa::BatchRec);
-}
-
-// LDS per chain of the one-batch-per-wave kernel: order, finish offsets, 48 bytes of
-// proposal table per batch
-size_t wave_chain_lds(int n, int B) {
-  const size_t M = (size_t)(n + B - 1) / B;
-  return (((size_t)n * 2 + 15) & ~size_t(15)) + (((size_t)(n + 2) * 4 + 15) & ~size_t(15)) + M * 48;
-}
+size_t static_wave_lds(int n, int B) { return sa::static_chain_bytes(n, B); }
+size_t wave_chain_lds(int n, int B) { return sa::wave_chain_bytes(n, B); }
 
 int device_attr(hipDeviceAttribute_t attr, int fallback) {
   int dev = 0, v = 0;
@@ -426,6 +417,64 @@ int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevM
         srch, w);
     HIP_TRY(hipGetLastError());
   }
+  return SCHED_OK;
+}
+
+template <int LG, int OBJ>
+hipError_t launch_multi_static_lg(int grid, int waves, size_t lds, const sa::DevModel &dm, const sa::StaticParams &sp,
+                                  int n, int instances, int chains, int groups, int iters, double T0, double alpha,
+                                  uint64_t seed, uint64_t swap_thr, const sa::SearchParams &srch, unsigned char *w,
+                                  hipStream_t stream) {
+  if (lds > 65536) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::multi_static_kernel<LG, OBJ>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  sa::multi_static_kernel<LG, OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, n, instances, chains, groups, iters, T0,
+                                                                      alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
+                                                                      swap_thr, srch, w);
+  return hipGetLastError();
+}
+
+// Every instance's chains on the static delta kernels, with as many chains per workgroup as
+// the single-queue launch would take for all of them (LDS for the largest instance); sets
+// `done` when the LDS allows it.
+template <int OBJ>
+int launch_multi_static(const sched_model_t *model, const sa::DevModel &dm, int n, int nk_max, int instances,
+                        int chains, int total, int iters, double T0, double alpha, uint64_t seed,
+                        const sa::SearchParams &srch, unsigned char *w, hipStream_t stream, bool &done) {
+  int lg = 0;
+  while ((1 << lg) < model->max_batch) ++lg;
+  const size_t soa = (size_t)(nk_max + 1) * 16;
+  const size_t per = lg == 6 ? wave_chain_lds(nk_max, model->max_batch) : static_wave_lds(nk_max, model->max_batch);
+  const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
+  int waves = 1;
+  while (waves < 16 && waves < chains && (int64_t)waves * cus < total) waves <<= 1;
+  while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+  if (soa + per * waves > (size_t)lim || (waves < 4 && (int64_t)waves * cus < total)) return SCHED_OK;
+  const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
+  const size_t lds = soa + per * waves;
+  const int groups = (chains + waves - 1) / waves, grid = instances * groups;
+  const uint64_t st = model->swap_threshold;
+  hipError_t e = hipSuccess;
+  switch (lg) {
+#define SA_MULTI_LG(L)                                                                                            \
+  case L:                                                                                                          \
+    e = launch_multi_static_lg<L, OBJ>(grid, waves, lds, dm, sp, n, instances, chains, groups, iters, T0, alpha, \
+                                       seed, st, srch, w, stream);                                               \
+    break;
+    SA_MULTI_LG(0)
+    SA_MULTI_LG(1)
+    SA_MULTI_LG(2)
+    SA_MULTI_LG(3)
+    SA_MULTI_LG(4)
+    SA_MULTI_LG(5)
+    SA_MULTI_LG(6)
+#undef SA_MULTI_LG
+    default: return SCHED_EINVAL;
+  }
+  if (e != hipSuccess) return hip_fail(e);
+  done = true;
   return SCHED_OK;
 }
 
@@ -676,7 +725,19 @@ int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, c
   HIP_TRY(hipGetLastError());
   sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(dm, n, instances, chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
-  if (nk_max > 0) {
+  bool done = nk_max == 0;
+  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
+    // every instance's queue is part of the whole one, so the delta kernel's widths hold
+    const int total = instances * chains;
+    if (srch.objective)
+      rc = launch_multi_static<1>(model, dm, n, nk_max, instances, chains, total, iters, T0, alpha, seed, srch, w,
+                                  stream, done);
+    else
+      rc = launch_multi_static<0>(model, dm, n, nk_max, instances, chains, total, iters, T0, alpha, seed, srch, w,
+                                  stream, done);
+    if (rc) return rc;
+  }
+  if (!done) {
     const int groups = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
     const size_t lds = anneal_lds_bytes(nk_max);
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);

@@ -112,6 +112,36 @@ def test_anneal_multi_empty_and_single_instances(sl, orc):
     _check_instances(sl, orc, q, m, np.zeros(q.n, np.int32), 1, 8, 300, 1.0, 0.99, 1, None, range(8))
 
 
+def test_anneal_multi_one_request_instance(sl, orc):
+    rng = np.random.default_rng(6)
+    q = random_queue(rng, 40, max_in=1500, max_out=40, thr_hi=600_000)
+    m = Model(8, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    inst = np.zeros(q.n, np.int32)
+    inst[5] = 1                    # instance 1 serves a single request
+    inst[20:] = 2
+    _check_instances(sl, orc, q, m, inst, 3, 16, 300, 1.0, 0.99, 2, None, range(16))
+
+
+@pytest.mark.parametrize("B,search", [(48, None), (48, (1, 4, 1)), (33, (0, 7, 0)), (64, None)])
+def test_anneal_multi_batch_per_wave(sl, orc, B, search):
+    # batches of more than 32 requests: the one-batch-per-wave delta kernel per instance
+    rng = np.random.default_rng(20 + B)
+    q = random_queue(rng, 300, max_in=1500, max_out=40, thr_hi=900_000)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    inst = orc.assign(q, 3, [9000, 6000, 4000])
+    _check_instances(sl, orc, q, m, inst, 3, 20, 300, 0.8, 0.99, 5, search, range(0, 20, 3))
+
+
+def test_anneal_multi_static_wide(sl, orc):
+    # 2 (d1 + d2 l_in) + d2 beyond 24 bits: static admission on the full-replay kernel
+    rng = np.random.default_rng(31)
+    q = random_queue(rng, 120, max_in=1500, max_out=40, thr_hi=2_000_000_000)
+    assert int(q.in_len.max()) * 2 * 8000 > 1 << 24
+    m = Model(8, 0, p0=2000, p1=40, d0=8000, d1=300, d2=8000)
+    inst = orc.assign(q, 4, [20000, 15000, 9000, 6000])
+    _check_instances(sl, orc, q, m, inst, 4, 12, 300, 1.0, 0.99, 7, None, range(0, 12, 4))
+
+
 def test_multi_workload_sampled(sl, orc):
     W = multi_workload()
     I, cap = W.extra["instances"], W.extra["capacity"]
