@@ -50,6 +50,40 @@ OPS_CONT_PER_SLOT_ADMISSION = 4
 OPS_CONT_PER_EVENT = 22
 
 
+def run_studies(chains: int = 1024) -> dict:
+    """The paper's parameter studies in model space (T0 / iter, output-length prediction,
+    latency-predictor coefficients) at their scenarios, `chains` runs of the scheduler per
+    point. Per point: label, G improvement over the arrival order (mean over chains, the
+    scheduler's winner), wall ms of the point, proposals per chain."""
+    from paper_2504_14966_amd import studies
+    from paper_2504_14966_amd.workloads import STUDY_SCENARIOS
+
+    def rows(pts):
+        out = []
+        for p in pts:
+            imp = p.improvement()
+            out.append([p.label, round(imp["mean"], 4), round(imp["winner"], 4), round(p.ms, 2), p.iters])
+        return out
+
+    t0 = time.perf_counter()
+    res, npts = {}, 0
+    for n, B in STUDY_SCENARIOS:
+        for name, fn in (("T0_iter", studies.t0_iter_study), ("length", studies.length_study)):
+            r = rows(fn(n, B, chains=chains))
+            res[f"{name}_n{n}_b{B}"] = r
+            npts += len(r)
+            best = max(r, key=lambda x: x[1])
+            log(f"[bench] study {name} n{n} b{B}: {len(r)} points, best mean improvement {best[1]:+.1%} ({best[0]}), "
+                f"{np.mean([x[3] for x in r]):.1f} ms per point")
+    r = rows(studies.coefficient_study(chains=chains))
+    res["coefficients_n10_b4"] = r
+    npts += len(r)
+    log(f"[bench] study coefficients n10 b4: {len(r)} points, worst mean improvement "
+        f"{min(x[1] for x in r):+.1%}, {np.mean([x[3] for x in r]):.1f} ms per point")
+    wall = time.perf_counter() - t0
+    return dict(chains_per_point=chains, points=npts, wall_s=wall, ms_per_point=wall * 1e3 / npts, results=res)
+
+
 def expected_work(W) -> dict:
     """Expected work of one proposal, averaged exactly over the proposal law (i uniform, j
     uniform over the other positions, swap or insert by the swap threshold)."""
@@ -249,6 +283,7 @@ def main():
     ap.add_argument("--workload", type=int, default=4, choices=[1, 2, 3, 4])
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-extras", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-studies", action="store_true", help="skip the parameter studies")
     ap.add_argument("--cpu-chains-per-core", type=int, default=8)
     ap.add_argument("--cpu-all", action="store_true",
                     help="also time the oracle on every workload's sample (adds about a minute)")
@@ -392,6 +427,8 @@ def main():
                                                best=keyx)
             log(f"[bench] {Wx.name}: {2 * Wx.chains * Wx.iters / wx:.4g} chain-iters/s ({np.mean(kx):.1f} ms), "
                 f"best {keyx}")
+        if not args.no_studies:
+            extras["studies"] = run_studies()
 
     cpu = None
     if args.cpu_all:

@@ -246,3 +246,53 @@ def chat_code_queue_10ns(n: int, seed: int):
     thr = np.where(cls == 0, 3_000_000_000, 1_000_000_000).astype(np.uint32)
     thr2 = np.where(cls == 0, 0, 5_000_000).astype(np.uint32)
     return Queue(q.in_len, q.out_len, kind, thr), thr2
+
+
+# ---- inputs of the parameter studies (Experiments) ----
+
+_S_PRED, _S_SAMPLE = 6, 7
+
+# Output-length distributions of the two classes as two_class_queue draws them: (mean, SD)
+OUT_DIST_CODE = (300.0, 300.0 * 200 / 250)
+OUT_DIST_CHAT = (200.0, 200.0 * 200 / 250)
+
+# The scenarios of the T0 / iter study and of the output-length study: (requests, max batch)
+STUDY_SCENARIOS = ((10, 1), (20, 2), (40, 4))
+
+
+def chat_code_classes(n: int, seed: int) -> np.ndarray:
+    """Class of every request of two_class_queue(n, seed) (same stream): 0 code, 1 chat."""
+    return _rng(seed, _S_CLASS).permutation(np.concatenate([np.zeros(n // 2, np.uint8), np.ones(n // 2, np.uint8)]))
+
+
+def perturbed_out_len(out_len: np.ndarray, variation: float, seed: int) -> np.ndarray:
+    """Predicted output lengths within a relative variation of the actual ones (the Impact of
+    Output Length Prediction study: actual lengths varied by 2.5, 5 or 10 %): l (1 + v u)
+    with u uniform on [-1, 1], rounded to the nearest integer, kept in [1, 65535]."""
+    u = _rng(seed, _S_PRED).uniform(-1.0, 1.0, size=out_len.shape[0])
+    x = out_len.astype(np.float64) * (1.0 + variation * u)
+    return np.clip(np.floor(x + 0.5), 1, 65535).astype(np.uint16)
+
+
+def sampled_out_len(cls: np.ndarray, seed: int) -> np.ndarray:
+    """The profiling-based predictor of the paper's setup: for every request a random integer
+    from the normal distribution with its class's output-length mean and SD, rounded to the
+    nearest integer and kept in [1, 1024] (the range two_class_queue draws from)."""
+    r = _rng(seed, _S_SAMPLE)
+    mean = np.where(cls == 0, OUT_DIST_CODE[0], OUT_DIST_CHAT[0])
+    sd = np.where(cls == 0, OUT_DIST_CODE[1], OUT_DIST_CHAT[1])
+    x = r.normal(mean, sd)
+    return np.clip(np.floor(x + 0.5), 1, 1024).astype(np.uint16)
+
+
+def perturbed_fit(coef: dict, letter: str, variation: float) -> dict:
+    """Latency-predictor coefficients with one parameter of Table 2 varied (the Impact of
+    Latency Prediction study): the prefill and decode coefficients named by `letter`
+    ('a' alpha: b l, 'b' beta: b, 'c' gamma: l, 'd' delta: constant) scaled by
+    (1 + variation) and rounded to the nearest integer; every other coefficient unchanged."""
+    if letter not in "abcd" or len(letter) != 1:
+        raise ValueError("letter is one of a, b, c, d")
+    out = dict(coef)
+    for k in (letter + "p", letter + "d"):
+        out[k] = int(math.floor(coef[k] * (1.0 + variation) + 0.5))
+    return out
