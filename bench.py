@@ -123,15 +123,15 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 180.9 KiB x 2.0 + WRITE_SIZE 16,679.9 KiB x 1.0, burst workload, one launch
-    "1ce0be33a3c524a95eb5c295c30f3950353721c32e4b1070a4bfb3bc408d6f92": 17450705,
+    # FETCH_SIZE 177.25 KiB x 2.0 + WRITE_SIZE 16,681.8 KiB x 1.0, burst workload, one launch
+    "a82139e2f59d358d1db1bdf627e94316bcfc79bff15281ab22d045a9d5701db6": 17445138,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "1ce0be33a3c524a95eb5c295c30f3950353721c32e4b1070a4bfb3bc408d6f92": 0.692,
+    "a82139e2f59d358d1db1bdf627e94316bcfc79bff15281ab22d045a9d5701db6": 0.688,
 }
 
 
