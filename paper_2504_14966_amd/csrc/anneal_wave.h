@@ -108,6 +108,13 @@ struct WaveChain {
     R.Bv = other ? R.Bv : Bv;
   }
 
+  // v_writelane of a wave-uniform value into lane k (lane select in m0, so that the value's
+  // scalar register is the instruction's one scalar operand); k comes from the scalar unit.
+  static __device__ __forceinline__ uint32_t wlane(uint32_t v, int k, uint32_t old) {
+    asm volatile("v_writelane_b32 %0, %1, m0" : "=v"(old) : "s"(v), "{m0}"(k), "0"(old));
+    return old;
+  }
+
   // SLO flags of the members at start S (TTFT and end-to-end members are met iff
   // S <= thr - offset; TPOT members do not depend on S), the met count and the bounds
   // [Bv, A] of starts that keep every flag.
@@ -234,7 +241,14 @@ struct WaveChain {
     const uint32_t cnt = slo(valid, is_out ? kinde : (rq.z & 3u), is_out ? thre : rq.y, Pc, Fn, S, A, Bv);
     wave_all3<OpMax, OpMin, OpMax>(Dn, A, Bv);
     const uint32_t D0 = readlane(cur.D, k), cnt0 = readlane(cur.cnt, k), Fo = readlane(fo, k);
-    put(cand, k, S, Pc, Dn, cnt, A, Bv);
+    // the scalar fields by v_writelane, the prefill (a vector register) by a select
+    cand.Slo = wlane((uint32_t)S, k, cand.Slo);
+    cand.Shi = wlane((uint32_t)(S >> 32), k, cand.Shi);
+    cand.P = lane != k ? cand.P : Pc;
+    cand.D = wlane(Dn, k, cand.D);
+    cand.cnt = wlane(cnt, k, cand.cnt);
+    cand.A = wlane(A, k, cand.A);
+    cand.Bv = wlane(Bv, k, cand.Bv);
     dn += (int64_t)cnt - (int64_t)cnt0;
     const int64_t dSF = (int64_t)(bs - 1) * (int64_t)(int32_t)rfl(dP) + (int64_t)(int32_t)dsum + ((int64_t)rfl(Fe) - (int64_t)Fo);
     dt += (int64_t)bs * shift + dSF;
@@ -253,10 +267,9 @@ struct WaveChain {
     uint32_t A, Bv;
     const uint32_t cnt = slo(valid, rq.z & 3u, rq.y, readlane(cur.P, k), Fm, S, A, Bv);
     wave_all2<OpMin, OpMax>(A, Bv);
-    const bool other = lane != k;
-    cand.cnt = other ? cand.cnt : cnt;
-    cand.A = other ? cand.A : A;
-    cand.Bv = other ? cand.Bv : Bv;
+    cand.cnt = wlane(cnt, k, cand.cnt);
+    cand.A = wlane(A, k, cand.A);
+    cand.Bv = wlane(Bv, k, cand.Bv);
     dn += (int64_t)cnt - (int64_t)readlane(cur.cnt, k);
   }
 
