@@ -66,7 +66,59 @@ __host__ __device__ __forceinline__ SlotQueue slot_queue(unsigned char *slot, in
                    reinterpret_cast<uint32_t *>(base + 3 * a + b)};
 }
 
-// One wave: instance of every request.
+// Capacities below this many tokens take the sorted-key assignment below.
+constexpr int64_t kAssignNarrowCap = int64_t(1) << 25;
+
+// One wave: instance of every request, every capacity below kAssignNarrowCap. Instance k's
+// remaining tokens rem travel in a 32-bit key ((rem + 2^17) << 6) | (63 - k): rem stays
+// above -2^17 (an instance is overdrawn only by the first request after a reset, by less
+// than one request of at most 2 * 65535 tokens) and below 2^25, so the key is positive and
+// below 2^32, larger keys mean more room, and equal room orders the lower index first.
+// The keys sit in lanes sorted in descending order (lanes past the instances hold 0), so
+// the roomiest instance is lane 0; placing a request pops it and inserts the reduced key,
+// and lane i of the new list is the median of list[i], list[i + 1] and that key (one DPP
+// shift and one v_med3_u32). A reset restores the initial sorted list. Request sizes are
+// loaded 64 at a time and the instances written 64 at a time.
+__global__ void __launch_bounds__(64) assign_sorted_kernel(QueuePtrs q, int n, int instances,
+                                                            const int64_t *__restrict__ capacity,
+                                                            int32_t *__restrict__ inst_out) {
+  __shared__ uint32_t srt[64];
+  const int lane = lane_id();
+  const bool live = lane < instances;
+  const uint32_t key0 = live ? ((uint32_t)(capacity[lane] + (int64_t(1) << 17)) << 6) | (uint32_t)(63 - lane) : 0u;
+  // rank among the instances' keys (distinct by their index bits); other lanes keep theirs
+  int rank = lane;
+  if (live) {
+    rank = 0;
+    for (int u = 0; u < instances; ++u) rank += (uint32_t)__builtin_amdgcn_readlane((int)key0, u) > key0 ? 1 : 0;
+  }
+  srt[rank] = key0;
+  __syncthreads();
+  const uint32_t init = srt[lane];
+  const uint32_t init_top = (uint32_t)__builtin_amdgcn_readfirstlane((int)init);
+  uint32_t list = init;
+  for (int c0 = 0; c0 < n; c0 += kWave) {
+    const int cnt = min(kWave, n - c0);
+    const uint32_t needv = lane < cnt ? (uint32_t)q.in_len[c0 + lane] + (uint32_t)q.out_len[c0 + lane] : 0u;
+    uint32_t outv = 0;
+    for (int t = 0; t < cnt; ++t) {
+      const uint32_t need = (uint32_t)__builtin_amdgcn_readlane((int)needv, t);
+      uint32_t top = (uint32_t)__builtin_amdgcn_readfirstlane((int)list);
+      if ((int32_t)(top >> 6) - (1 << 17) < (int32_t)need) {  // even the roomiest cannot hold it
+        list = init;
+        top = init_top;
+      }
+      const uint32_t nk = top - (need << 6);
+      const uint32_t above = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)list, 0x130, 0xF, 0xF, true);  // list[i + 1]
+      list = med3_u32(above, list, nk);
+      const uint32_t k = 63u - (top & 63u);
+      outv = lane == t ? k : outv;
+    }
+    if (lane < cnt) inst_out[c0 + lane] = (int32_t)outv;
+  }
+}
+
+// One wave: instance of every request, 64-bit remaining tokens (any capacity).
 __global__ void __launch_bounds__(64) assign_kernel(QueuePtrs q, int n, int instances,
                                                      const int64_t *__restrict__ capacity, int32_t *__restrict__ inst_out) {
   const int lane = lane_id();

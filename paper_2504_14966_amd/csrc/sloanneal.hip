@@ -669,9 +669,15 @@ int sched_assign(const sched_queue_t *queue, int32_t instances, const int64_t *c
   std::vector<int64_t> cap((size_t)instances);
   HIP_TRY(hipMemcpyAsync(cap.data(), capacity, (size_t)instances * 8, hipMemcpyDeviceToHost, stream));
   HIP_TRY(hipStreamSynchronize(stream));
-  for (int64_t c : cap)
+  bool narrow = true;
+  for (int64_t c : cap) {
     if (c < 1 || c > (int64_t(1) << 48)) return SCHED_EINVAL;
-  sa::assign_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
+    narrow = narrow && c < sa::kAssignNarrowCap;
+  }
+  if (narrow)
+    sa::assign_sorted_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
+  else
+    sa::assign_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }

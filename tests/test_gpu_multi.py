@@ -53,6 +53,26 @@ def test_assign_random(sl, orc, seed):
     assert np.array_equal(_assign(sl, q, cap), orc.assign(q, I, cap))
 
 
+@pytest.mark.parametrize("seed", range(3))
+def test_assign_wide_capacities(sl, orc, seed):
+    # capacities from 2^25 tokens up take the 64-bit assignment; mixed with small ones too
+    rng = np.random.default_rng(40 + seed)
+    I = [3, 17, 64][seed]
+    q = random_queue(rng, int(rng.integers(200, 1025)), max_in=60000, max_out=60000)
+    cap = rng.integers(1 << 25, 1 << 26, size=I).astype(np.int64)
+    cap[::2] = rng.integers(1000, 200000, size=len(cap[::2]))
+    assert np.array_equal(_assign(sl, q, cap), orc.assign(q, I, cap))
+
+
+def test_assign_narrow_edges(sl, orc):
+    # capacities just below 2^25, requests of up to 2 * 65535 tokens, overdrawn instances
+    rng = np.random.default_rng(7)
+    q = random_queue(rng, 1024, max_in=65535, max_out=65535)
+    for cap in ([(1 << 25) - 1] * 5, [1, 2, 3], [131070, 131069, 1], [1 << 20] * 64):
+        cap = np.array(cap, np.int64)
+        assert np.array_equal(_assign(sl, q, cap), orc.assign(q, len(cap), cap)), cap[:4]
+
+
 def _check_instances(sl, orc, q, m, inst, I, C, iters, T0, alpha, seed, search, sample):
     import torch
     dq = sl.DeviceQueue.from_queue(q)
