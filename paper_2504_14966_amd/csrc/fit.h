@@ -23,6 +23,8 @@ namespace sa {
 struct DevFit {
   int32_t n, B, policy, pad;
   uint64_t ap, bp, cp, dp, ad, bd, cd, dd;
+  uint32_t win, pad2;  // win = 1: every member's time is below 2^57 (the windowed replay's keys fit)
+  uint64_t bmagic;     // floor(2^32 / B) + 1: lane / B = (lane * bmagic) >> 32 for lanes below 64
 };
 
 // Request record: x = l_in | l_out << 16, y = threshold, z = kind, w = second threshold.
@@ -48,10 +50,11 @@ __device__ __forceinline__ bool fit_met(uint32_t kind, uint64_t thr, uint64_t th
   return ttft <= thr && td <= thr2 * L;
 }
 
-// flags: start flags of the layout, or null for batches of the maximum size.
+// flags: start flags of the layout, or null for batches of the maximum size. One batch at
+// a time (any member time).
 template <bool DETAIL>
-__device__ Score replay_fit(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm, const uint8_t *flags,
-                            int64_t *detail) {
+__device__ Score replay_fit_batches(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm,
+                                    const uint8_t *flags, int64_t *detail) {
   const int lane = lane_id();
   const int n = f.n;
   uint64_t S = 0, tl = 0;
@@ -81,6 +84,99 @@ __device__ Score replay_fit(const DevFit &f, const uint4 *__restrict__ req, cons
     s = e;
   }
   return Score{nmet, wave_sum_u64(tl)};
+}
+
+// 64-bit inclusive max-scan over the 64 lanes.
+__device__ __forceinline__ uint64_t scan_max64_step(uint64_t v, uint32_t lo, uint32_t hi) {
+  const uint64_t o = ((uint64_t)hi << 32) | lo;
+  return o > v ? o : v;
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint64_t max_dpp64(uint64_t v) {
+  return scan_max64_step(v, dpp_old<CTRL, ROWMASK>(0u, (uint32_t)v), dpp_old<CTRL, ROWMASK>(0u, (uint32_t)(v >> 32)));
+}
+__device__ __forceinline__ uint64_t scan_max64(uint64_t v) {
+  v = max_dpp64<kDppRowShr1, 0xF>(v);
+  v = max_dpp64<kDppRowShr2, 0xF>(v);
+  v = max_dpp64<kDppRowShr4, 0xF>(v);
+  v = max_dpp64<kDppRowShr8, 0xF>(v);
+  v = max_dpp64<kDppRowBcast15, 0xA>(v);
+  v = max_dpp64<kDppRowBcast31, 0xC>(v);
+  return v;
+}
+
+// The same timeline over windows of whole batches: a window starts at a batch start and
+// takes every batch that ends within the next 64 positions, one position per lane. A lane's
+// batch and size come from the mask of batch-last lanes; its time from the closed forms.
+// The batch durations are one max-scan of the key (batch start lane << 58 | time): batch
+// starts never decrease across lanes, so the running maximum of the key at a lane is the
+// running maximum of the time within the lane's own batch, and at the batch's last lane its
+// duration (needs every time below 2^58). The batches' start times are one add-scan of the
+// durations at the batch-last lanes.
+template <bool DETAIL>
+__device__ Score replay_fit_windows(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm,
+                                    const uint8_t *flags, int64_t *detail) {
+  const int lane = lane_id();
+  const int n = f.n, B = f.B;
+  constexpr uint64_t kTimeMask = (uint64_t(1) << 58) - 1;
+  uint64_t S0 = 0, tl = 0;
+  int64_t nmet = 0;
+  for (int s = 0; s < n;) {
+    const int p = s + lane;
+    // lane begins a batch (lane 0 always does) or is the end of the queue
+    bool st = p == n;
+    if (p < n) {
+      if (flags) st = lane == 0 || flags[p] != 0;
+      else st = (uint64_t)lane == (((uint64_t)lane * f.bmagic) >> 32) * (uint64_t)B;
+    }
+    // position s + 64 begins a batch or is the end of the queue
+    bool st64 = s + kWave == n;
+    if (s + kWave < n) st64 = flags ? flags[s + kWave] != 0 : (kWave % B) == 0;
+    uint64_t lastm = (__ballot(st) >> 1) | (st64 ? uint64_t(1) << 63 : 0ull);  // batch-last lanes
+    // a valid layout always closes a batch within 64 positions; a malformed one is cut
+    // there so that the window advances
+    if (lastm == 0ull) lastm = uint64_t(1) << 63;
+    const int w = 64 - __clzll(lastm);  // lanes [0, w) hold whole batches
+    const bool in = lane < w;
+    const uint64_t below = lastm & ((uint64_t(1) << lane) - 1);
+    const int b0 = below ? 64 - __clzll(below) : 0;              // first lane of the lane's batch
+    const int b1 = lane + __builtin_ctzll(in ? (lastm >> lane) : 1ull);  // its last lane
+    uint64_t tp = 0, E = 0;
+    uint4 rq = make_uint4(0u, 0u, 0u, 0u);
+    int r = 0;
+    if (in) {
+      r = perm[p];
+      rq = req[r];
+      const uint64_t b = (uint64_t)(b1 - b0 + 1), l = rq.x & 0xFFFFu, L = rq.x >> 16;
+      tp = fit_prefill(f, b, l);
+      E = tp + fit_decode(f, b, l, L);
+    }
+    const uint64_t D = scan_max64(in ? ((uint64_t)b0 << 58) | E : 0ull) & kTimeMask;
+    const uint64_t contrib = (in && lane == b1) ? D : 0ull;
+    const uint64_t incl = scan_add64(contrib);
+    const uint64_t S = S0 + (incl - contrib);
+    bool met = false;
+    if (in) {
+      const uint64_t L = rq.x >> 16, ttft = S + tp, e2e = S + E;
+      met = fit_met(rq.z, rq.y, rq.w, L, ttft, E - tp, e2e);
+      tl += e2e;
+      if (DETAIL) {
+        detail[2 * r] = (int64_t)ttft;
+        detail[2 * r + 1] = (int64_t)e2e;
+      }
+    }
+    nmet += ballot_count(met);
+    S0 += rl64(incl, kWave - 1);
+    s += w;
+  }
+  return Score{nmet, wave_sum_u64(tl)};
+}
+
+template <bool DETAIL>
+__device__ __forceinline__ Score replay_fit(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm,
+                                            const uint8_t *flags, int64_t *detail) {
+  if (f.win) return replay_fit_windows<DETAIL>(f, req, perm, flags, detail);
+  return replay_fit_batches<DETAIL>(f, req, perm, flags, detail);
 }
 
 // K rows: one wave per row; rows validated first ((-1, -1) otherwise). starts nullable.

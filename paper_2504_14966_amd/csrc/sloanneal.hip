@@ -103,7 +103,10 @@ int check_fit(const sched_fit_model_t *f) {
   return SCHED_OK;
 }
 
-int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool ratio) {
+// Sum over requests of their time in a batch of min(n, B): a member's time grows with its
+// batch size, and a batch lasts at most the sum of its members' times, so this bounds the
+// timeline and every member's time.
+long double fit_timeline_bound(const HostQueue &h, const sched_fit_model_t *f, int n) {
   const long double b = std::min(n, f->max_batch);
   long double end = 0;
   for (int r = 0; r < n; ++r) {
@@ -112,6 +115,11 @@ int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool 
            L * ((long double)f->bd * b + (long double)f->dd) +
            ((long double)f->ad * b + (long double)f->cd) * (L * l + L * (L + 1) / 2);
   }
+  return end;
+}
+
+int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool ratio) {
+  const long double end = fit_timeline_bound(h, f, n);
   const long double tsum = end * n, lim = std::ldexp(1.0L, 62);
   const long double tref = f->t_ref > 0 ? (long double)f->t_ref : tsum;
   if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
@@ -119,9 +127,11 @@ int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool 
   return SCHED_OK;
 }
 
-sa::DevFit dev_fit(const sched_fit_model_t *f, int n) {
+// win: the windowed replay's keys hold every member's time (below 2^57 with margin)
+sa::DevFit dev_fit(const sched_fit_model_t *f, int n, bool win) {
   return sa::DevFit{n, f->max_batch, f->policy, 0, (uint64_t)f->ap, (uint64_t)f->bp, (uint64_t)f->cp,
-                    (uint64_t)f->dp, (uint64_t)f->ad, (uint64_t)f->bd, (uint64_t)f->cd, (uint64_t)f->dd};
+                    (uint64_t)f->dp, (uint64_t)f->ad, (uint64_t)f->bd, (uint64_t)f->cd, (uint64_t)f->dd,
+                    win ? 1u : 0u, 0u, (1ull << 32) / (uint64_t)f->max_batch + 1};
 }
 
 // The ratio objective compares n1 t2 with n2 t1 and forms n' t - n t' in int64: the
@@ -791,7 +801,7 @@ int sched_eval_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, con
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
-  const sa::DevFit df = dev_fit(fit, n);
+  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57));
   if (detail)
     sa::eval_fit_kernel<true><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, perms, starts, k, out, detail);
   else
@@ -823,7 +833,7 @@ int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, c
   if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
   if ((rc = fit_range_check(h, fit, queue->n, srch.objective == SCHED_OBJ_RATIO))) return rc;
   const int n = queue->n;
-  const sa::DevFit df = dev_fit(fit, n);
+  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57));
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_fit_kernel<<<1, 1024, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, fit->t_ref, srch, w);
   HIP_TRY(hipGetLastError());

@@ -127,3 +127,28 @@ def test_anneal_fit_shapes(sl, orc, n, B, policy):
         w = orc.anneal_chain_fit(q, fo, c, iters, 0.5, 0.99, 7, start_info=info)
         assert res["rec"][c].tolist() == w["rec"].tolist(), c
         assert res["best"][c].tolist() == w["best"].tolist(), c
+
+
+@pytest.mark.parametrize("policy", [0, 2])
+def test_fit_huge_times_batch_replay(sl, orc, policy):
+    # member times of 2^56 and more: the windowed replay's keys would not hold them, so the
+    # batch-at-a-time replay runs (its bound 2^57 <= timeline, timeline * (n + 2) < 2^62)
+    import torch
+    rng = np.random.default_rng(90 + policy)
+    n, B = 3, 2
+    q = random_queue(rng, n, max_in=1000, max_out=100, thr_hi=2**32 - 2)
+    coef = dict(ap=3, bp=5, cp=7, dp=1 << 56, ad=1, bd=2, cd=3, dd=11)
+    fd, fo = sl.FitModel(B, policy, **coef), orc.FitModel(B, policy, **coef)
+    perms = np.stack([rng.permutation(n) for _ in range(12)]).astype(np.uint16)
+    starts = random_layouts(rng, 12, n, B)
+    dq = sl.DeviceQueue.from_queue(q)
+    out = sl.sched_eval_fit(dq, fd, sl.perms_to_device(perms), sl.starts_to_device(starts))
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    for r in range(12):
+        assert out[r].tolist() == list(orc.replay_fit(q, fo, perms[r], starts[r])), r
+    res = _anneal(sl, q, fd, 4, 50, 0.5, 0.99, 3, None, None)
+    info = orc.start_fit(q, fo)
+    for c in range(4):
+        w = orc.anneal_chain_fit(q, fo, c, 50, 0.5, 0.99, 3, start_info=info)
+        assert res["rec"][c].tolist() == w["rec"].tolist(), c
