@@ -123,15 +123,15 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 177.25 KiB x 2.0 + WRITE_SIZE 16,681.8 KiB x 1.0, burst workload, one launch
-    "a82139e2f59d358d1db1bdf627e94316bcfc79bff15281ab22d045a9d5701db6": 17445138,
+    # FETCH_SIZE 181.9 KiB x 2.0 + WRITE_SIZE 16,683.6 KiB x 1.0, burst workload, one launch
+    "7f50b15a163625a609cbd8c209f43acf9df88fd35fe270abe3f4c00c94de9fc9": 17456592,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "a82139e2f59d358d1db1bdf627e94316bcfc79bff15281ab22d045a9d5701db6": 0.688,
+    "7f50b15a163625a609cbd8c209f43acf9df88fd35fe270abe3f4c00c94de9fc9": 0.679,
 }
 
 
