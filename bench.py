@@ -123,15 +123,15 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 181.9 KiB x 2.0 + WRITE_SIZE 16,683.6 KiB x 1.0, burst workload, one launch
-    "7f50b15a163625a609cbd8c209f43acf9df88fd35fe270abe3f4c00c94de9fc9": 17456592,
+    # FETCH_SIZE 179.6 KiB x 2.0 + WRITE_SIZE 16,684.4 KiB x 1.0, burst workload, one launch
+    "afd2309b5e8953be0dc1424bf2998d84d111943efd137c6aec77b409596abbf1": 17452625,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "7f50b15a163625a609cbd8c209f43acf9df88fd35fe270abe3f4c00c94de9fc9": 0.679,
+    "afd2309b5e8953be0dc1424bf2998d84d111943efd137c6aec77b409596abbf1": 0.677,
 }
 
 
@@ -297,7 +297,7 @@ def main():
 
     import torch
     import paper_2504_14966_amd.sloanneal as sl
-    from paper_2504_14966_amd.workloads import multi_workload, search_workload, workload
+    from paper_2504_14966_amd.workloads import POLICY_STATIC_SEARCH, Model, multi_workload, search_workload, workload
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     sl.load_library()
@@ -329,6 +329,29 @@ def main():
         extras["eval_workload"] = dict(workload=W5.name, rows=W5.eval_rows, evals_per_s=W5.eval_rows / wall5,
                                        kernel_ms=k5)
         log(f"[bench] eval {W5.eval_rows / wall5:.4g} evals/s ({k5:.2f} ms per 2^20 rows)")
+        # the same 2^20 orders with explicit batch layouts (sched_eval_batches): 1024 random
+        # layouts of batch sizes uniform in 1..16, repeated over the rows
+        from paper_2504_14966_amd.workloads import random_layouts
+        m5 = W5.model
+        ms5 = Model(m5.max_batch, POLICY_STATIC_SEARCH, m5.p0, m5.p1, m5.d0, m5.d1, m5.d2)
+        lay = random_layouts(np.random.default_rng(5), 1024, W5.queue.n, m5.max_batch)
+        st5 = torch.from_numpy(np.tile(lay, (W5.eval_rows // 1024, 1))).to("cuda")
+        dq5 = sl.DeviceQueue.from_queue(W5.queue)
+        pm5 = sl.sched_gen_perms(W5.perm_seed, W5.queue.n, W5.eval_rows)
+        o5 = torch.empty((W5.eval_rows, 2), dtype=torch.int64, device="cuda")
+        sl.sched_eval_batches(dq5, ms5, pm5, st5, out=o5)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(5):
+            sl.sched_eval_batches(dq5, ms5, pm5, st5, out=o5)
+        b.record()
+        torch.cuda.synchronize()
+        msl = a.elapsed_time(b) / 5
+        extras["eval_layouts"] = dict(workload="eval-n128-b16-layouts", rows=W5.eval_rows, ms=msl,
+                                      evals_per_s=W5.eval_rows / (msl * 1e-3))
+        log(f"[bench] eval with batch layouts {W5.eval_rows / (msl * 1e-3):.4g} evals/s ({msl:.2f} ms per 2^20 rows)")
+        del st5, pm5, o5
         for wl in (1, 2, 3):
             if wl == args.workload:
                 continue

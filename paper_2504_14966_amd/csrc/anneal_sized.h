@@ -81,8 +81,8 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
 // The batch lasts max F; the next batch starts when it ends (waiting time = sum of the
 // earlier batch durations).
 template <bool DETAIL>
-__device__ Score replay_batches(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
-                                const uint8_t *flags, uint4 *stage, int64_t *detail) {
+__device__ Score replay_batches_one(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
+                                    const uint8_t *flags, uint4 *stage, int64_t *detail) {
   const int lane = lane_id();
   const int n = m.n;
   uint64_t S = 0, tl = 0;
@@ -129,6 +129,92 @@ __device__ Score replay_batches(const DevModel &m, const uint4 *__restrict__ req
     s = e;
   }
   return Score{nmet, wave_sum_u64(tl)};
+}
+
+// The same timeline over windows of whole batches, one position per lane: a window starts
+// at a batch start and takes every batch that ends within the next 64 positions. Each lane
+// sums its pair terms over its own batch's members from the staged records (as many steps
+// as the window's largest batch), which also gives the batch prefill. Batch durations are
+// one max-scan of (first lane of the batch << 58 | finish offset) -- first lanes never
+// decrease across lanes, so the running maximum at a lane is the running maximum within its
+// own batch -- and the start times one add-scan of the durations at the batch-last lanes.
+// Needs every time below 2^58 (kFlagWindows).
+template <bool DETAIL>
+__device__ Score replay_batches_windows(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
+                                        const uint8_t *flags, uint4 *stage, int64_t *detail) {
+  const int lane = lane_id();
+  const int n = m.n;
+  constexpr uint64_t kTimeMask = (uint64_t(1) << 58) - 1;
+  uint64_t S0 = 0, tl = 0;
+  int64_t nmet = 0;
+  for (int s = 0; s < n;) {
+    const int p = s + lane;
+    const bool st = p == n || (p < n && (lane == 0 || flags[p] != 0));  // begins a batch, or the end
+    bool st64 = s + kWave == n;                                         // position s + 64 likewise
+    if (s + kWave < n) st64 = flags[s + kWave] != 0;
+    uint64_t lastm = (__ballot(st) >> 1) | (st64 ? uint64_t(1) << 63 : 0ull);  // batch-last lanes
+    // a valid layout always closes a batch within 64 positions; a malformed one is cut
+    // there so that the window advances
+    if (lastm == 0ull) lastm = uint64_t(1) << 63;
+    const int w = 64 - __clzll(lastm);
+    const bool in = lane < w;
+    const uint64_t below = lastm & ((uint64_t(1) << lane) - 1);
+    const int b0 = below ? 64 - __clzll(below) : 0;
+    const int b1 = lane + __builtin_ctzll(in ? (lastm >> lane) : 1ull);
+    uint32_t lin = 0, L = 0, thr = 0, kind = 0;
+    int r = 0;
+    if (in) {
+      r = perm[p];
+      const uint4 rq = req[r];
+      lin = req_lin(rq);
+      L = req_lout(rq);
+      thr = rq.y;
+      kind = rq.z & 3u;
+    }
+    const uint64_t pf = in ? m.p0 + m.p1 * (uint64_t)lin : 0;
+    stage[lane] = make_uint4(L, lin, (uint32_t)pf, (uint32_t)(pf >> 32));
+    wave_sync_lds();
+    const int bl = in ? b1 - b0 + 1 : 0;
+    int jmax = bl;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) jmax = max(jmax, __shfl_xor(jmax, o));
+    uint64_t P = 0, acc = 0;
+    for (int j = 0; j < jmax; ++j) {
+      if (j < bl) {
+        const uint4 sj = stage[b0 + j];
+        P += (uint64_t)sj.z | ((uint64_t)sj.w << 32);
+        const uint64_t mu = min(sj.x, L);
+        acc += m.d1 * mu + m.d2 * ((uint64_t)sj.y * mu + (mu * (mu + 1) >> 1));
+      }
+    }
+    wave_sync_lds();
+    const uint64_t F = P + (uint64_t)L * m.d0 + acc;
+    const uint64_t D = scan_max64(in ? ((uint64_t)b0 << 58) | F : 0ull) & kTimeMask;
+    const uint64_t contrib = (in && lane == b1) ? D : 0ull;
+    const uint64_t incl = scan_add64(contrib);
+    const uint64_t S = S0 + (incl - contrib);
+    bool met = false;
+    if (in) {
+      const uint64_t e2e = S + F, ttft = S + P;
+      tl += e2e;
+      met = slo_met(kind, thr, L, ttft, e2e);
+      if (DETAIL) {
+        detail[2 * r] = (int64_t)ttft;
+        detail[2 * r + 1] = (int64_t)e2e;
+      }
+    }
+    nmet += ballot_count(met);
+    S0 += rl64(incl, kWave - 1);
+    s += w;
+  }
+  return Score{nmet, wave_sum_u64(tl)};
+}
+
+template <bool DETAIL>
+__device__ __forceinline__ Score replay_batches(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
+                                                const uint8_t *flags, uint4 *stage, int64_t *detail) {
+  if (m.flags & kFlagWindows) return replay_batches_windows<DETAIL>(m, req, perm, flags, stage, detail);
+  return replay_batches_one<DETAIL>(m, req, perm, flags, stage, detail);
 }
 
 // K rows of (order, layout): one wave per row, rows validated first ((-1, -1) otherwise).

@@ -185,6 +185,25 @@ __device__ __forceinline__ uint64_t scan_add64(uint64_t v) {
   v = add_dpp64<kDppRowBcast31, 0xC>(v);
   return v;
 }
+// 64-bit inclusive max-scan over the 64 lanes.
+__device__ __forceinline__ uint64_t scan_max64_step(uint64_t v, uint32_t lo, uint32_t hi) {
+  const uint64_t o = ((uint64_t)hi << 32) | lo;
+  return o > v ? o : v;
+}
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint64_t max_dpp64(uint64_t v) {
+  return scan_max64_step(v, dpp_old<CTRL, ROWMASK>(0u, (uint32_t)v), dpp_old<CTRL, ROWMASK>(0u, (uint32_t)(v >> 32)));
+}
+__device__ __forceinline__ uint64_t scan_max64(uint64_t v) {
+  v = max_dpp64<kDppRowShr1, 0xF>(v);
+  v = max_dpp64<kDppRowShr2, 0xF>(v);
+  v = max_dpp64<kDppRowShr4, 0xF>(v);
+  v = max_dpp64<kDppRowShr8, 0xF>(v);
+  v = max_dpp64<kDppRowBcast15, 0xA>(v);
+  v = max_dpp64<kDppRowBcast31, 0xC>(v);
+  return v;
+}
+
 __device__ __forceinline__ uint64_t rl64(uint64_t v, int l) {
   return ((uint64_t)rl((uint32_t)(v >> 32), l) << 32) | rl((uint32_t)v, l);
 }

@@ -86,25 +86,6 @@ __device__ Score replay_fit_batches(const DevFit &f, const uint4 *__restrict__ r
   return Score{nmet, wave_sum_u64(tl)};
 }
 
-// 64-bit inclusive max-scan over the 64 lanes.
-__device__ __forceinline__ uint64_t scan_max64_step(uint64_t v, uint32_t lo, uint32_t hi) {
-  const uint64_t o = ((uint64_t)hi << 32) | lo;
-  return o > v ? o : v;
-}
-template <int CTRL, int ROWMASK>
-__device__ __forceinline__ uint64_t max_dpp64(uint64_t v) {
-  return scan_max64_step(v, dpp_old<CTRL, ROWMASK>(0u, (uint32_t)v), dpp_old<CTRL, ROWMASK>(0u, (uint32_t)(v >> 32)));
-}
-__device__ __forceinline__ uint64_t scan_max64(uint64_t v) {
-  v = max_dpp64<kDppRowShr1, 0xF>(v);
-  v = max_dpp64<kDppRowShr2, 0xF>(v);
-  v = max_dpp64<kDppRowShr4, 0xF>(v);
-  v = max_dpp64<kDppRowShr8, 0xF>(v);
-  v = max_dpp64<kDppRowBcast15, 0xA>(v);
-  v = max_dpp64<kDppRowBcast31, 0xC>(v);
-  return v;
-}
-
 // The same timeline over windows of whole batches: a window starts at a batch start and
 // takes every batch that ends within the next 64 positions, one position per lane. A lane's
 // batch and size come from the mask of batch-last lanes; its time from the closed forms.

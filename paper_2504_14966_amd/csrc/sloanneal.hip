@@ -72,8 +72,9 @@ int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h, int ma
 // Worst-case clock: every request's prefill plus, per request, its decode iterations at
 // the largest possible step cost. The sum over requests and the Metropolis delta
 // (|dn| <= n times t_ref) must stay below 2^62.
-int range_check(const HostQueue &h, const sched_model_t *m, int n) {
-  const long double lim = std::ldexp(1.0L, 62);
+// Bound on the timeline of any order and any batch layout: every prefill, plus per decode
+// step (at most the sum of output lengths) the cost of a full batch of the longest contexts.
+long double timeline_bound(const HostQueue &h, const sched_model_t *m, int n) {
   long double max_lin = 0, max_lout = 0, sum_lout = 0, pre = 0;
   for (int r = 0; r < n; ++r) {
     max_lin = std::max<long double>(max_lin, h.in_len[r]);
@@ -83,7 +84,12 @@ int range_check(const HostQueue &h, const sched_model_t *m, int n) {
   }
   const long double b = std::min(n, m->max_batch);
   const long double step = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * b * (max_lin + max_lout);
-  const long double clock = pre + sum_lout * step;
+  return pre + sum_lout * step;
+}
+
+int range_check(const HostQueue &h, const sched_model_t *m, int n) {
+  const long double lim = std::ldexp(1.0L, 62);
+  const long double clock = timeline_bound(h, m, n);
   const long double tsum = clock * n;
   const long double tref = m->t_ref_us > 0 ? (long double)m->t_ref_us : tsum;
   if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
@@ -193,13 +199,13 @@ bool timeline_narrow(const HostQueue &h, const sched_model_t *m, int n) {
 }
 
 sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false,
-                       bool narrow_time = false) {
+                       bool narrow_time = false, bool windows = false) {
   sa::DevModel d;
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
   d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0) |
-            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0);
+            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0) | (windows ? sa::kFlagWindows : 0);
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
@@ -591,7 +597,7 @@ int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, cons
   if (srch.objective == SCHED_OBJ_RATIO && (rc = ratio_range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
   const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
-                                    timeline_narrow(h, model, n));
+                                    timeline_narrow(h, model, n), timeline_bound(h, model, n) < std::ldexp(1.0L, 57));
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
@@ -648,7 +654,7 @@ int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, c
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, false);
+  const sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57));
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 64 * 16 + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);

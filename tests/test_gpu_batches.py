@@ -205,3 +205,19 @@ def test_anneal_search_paths(sl, orc, name):
     q = mk(rng)
     res = _anneal(sl, q, m, chains, iters, 0.7, 0.99, 5)
     _check_chains(orc, res, q, m, range(chains), iters, 0.7, 0.99, 5)
+
+
+def test_batches_huge_times_one_batch_replay(sl, orc):
+    # times from 2^57 on: the windowed replay's keys would not hold them, so sched_eval_batches
+    # and the full-replay search chains take one batch per step (the timeline bound
+    # 2^57 <= clock, and clock * n * (n + 2) < 2^62 keeps the range check)
+    rng = np.random.default_rng(77)
+    n, B = 3, 2
+    q = random_queue(rng, n, max_in=1000, max_out=20, thr_hi=2**32 - 2)
+    m = Model(B, SEARCH, 1 << 56, 3, 5, 7, 1)
+    k = 24
+    perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, n, B)
+    assert np.array_equal(_eval(sl, q, m, perms, starts), oracle_rows_batches(q, m, perms, starts))
+    res = _anneal(sl, q, m, 4, 60, 0.7, 0.99, 9)
+    _check_chains(orc, res, q, m, range(4), 60, 0.7, 0.99, 9)
