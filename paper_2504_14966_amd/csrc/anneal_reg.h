@@ -1,0 +1,217 @@
+// Annealing chains under static admission for small queues, state in registers (gfx950).
+//
+// For at most 64 requests and a batch size of 1, 2, 4, 8 or 16, lane p holds the request at
+// position p of the order: its output length and id, its pair-cost parameter e = 2 (d1 + d2
+// l_in) + d2 and kind, its prefill and its SLO threshold (for TPOT, threshold times output
+// length, saturated at 2^32 - 1). Batch k is lanes [kB, kB + B), inside one DPP row. A
+// proposal builds the candidate order in registers (a swap is two v_readlane and two
+// v_writelane per field; an insert is one DPP wave shift, a range select and one
+// v_writelane) and replays it in full with no LDS traffic:
+//   - each member's finish offset F = P + L d0 + (sum over the batch's members j of
+//     mu (e_j + d2 mu)) / 2, mu = min(L_j, L), the batch's members reached by rotating the
+//     row (row_ror, or the two rotations that stay inside an 8-lane half, or quad
+//     permutations); the rotations read the same source registers, so they are independent;
+//   - the batch prefill P and duration D by segment all-reduces, the batch starts by one
+//     exclusive 64-bit add-scan of D placed at each batch's last lane;
+//   - TTFT = S + P, e2e = S + F and the SLO tests per lane; the met count by ballot, the
+//     latency sum by one 64-bit wave reduction.
+// The 32-bit products and sums are exact under the fixed-size delta kernel's width checks.
+#pragma once
+#include "anneal_static.h"
+#include "device_cont.h"
+
+namespace sa {
+
+// The small-queue kernel's applicability: n <= 64 and B a power of two up to 16.
+__host__ __device__ __forceinline__ bool reg_kernel_fits(int n, int B) {
+  return n >= 1 && n <= 64 && B >= 1 && B <= 16 && (B & (B - 1)) == 0;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dppv(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
+}
+
+// v_writelane of a wave-uniform value into lane k (lane select in m0)
+__device__ __forceinline__ uint32_t wlane_m0(uint32_t v, int k, uint32_t old) {
+  asm volatile("v_writelane_b32 %0, %1, m0" : "=v"(old) : "s"(v), "{m0}"(k), "0"(old));
+  return old;
+}
+
+// sum over the other members j of the lane's batch of mu (e_j + d2 mu), mu = min(L_j, L)
+template <int LG>
+__device__ __forceinline__ uint32_t pair_sum_others(uint32_t L, uint32_t e, uint32_t d2, int lane) {
+  uint32_t acc = 0;
+  auto term = [&](uint32_t Lj, uint32_t ej) {
+    const uint32_t mu = min(Lj, L);
+    acc += __umul24(mu, __umul24(d2, mu) + ej);
+  };
+  if constexpr (LG == 1) {
+    term(dppv<0xB1>(L), dppv<0xB1>(e));  // quad_perm [1,0,3,2]
+  } else if constexpr (LG == 2) {
+    term(dppv<0x39>(L), dppv<0x39>(e));  // quad_perm [1,2,3,0]
+    term(dppv<0x4E>(L), dppv<0x4E>(e));  // quad_perm [2,3,0,1]
+    term(dppv<0x93>(L), dppv<0x93>(e));  // quad_perm [3,0,1,2]
+  } else if constexpr (LG == 3) {
+    // rotate by r inside the lane's 8-lane half: row_ror:r where that stays in the half,
+    // else row_ror:(r + 8)
+    const int m8 = lane & 7;
+#pragma unroll
+    for (int r = 1; r < 8; ++r) {
+      uint32_t La, ea, Lb, eb;
+      switch (r) {
+        case 1: La = dppv<0x121>(L); ea = dppv<0x121>(e); Lb = dppv<0x129>(L); eb = dppv<0x129>(e); break;
+        case 2: La = dppv<0x122>(L); ea = dppv<0x122>(e); Lb = dppv<0x12A>(L); eb = dppv<0x12A>(e); break;
+        case 3: La = dppv<0x123>(L); ea = dppv<0x123>(e); Lb = dppv<0x12B>(L); eb = dppv<0x12B>(e); break;
+        case 4: La = dppv<0x124>(L); ea = dppv<0x124>(e); Lb = dppv<0x12C>(L); eb = dppv<0x12C>(e); break;
+        case 5: La = dppv<0x125>(L); ea = dppv<0x125>(e); Lb = dppv<0x12D>(L); eb = dppv<0x12D>(e); break;
+        case 6: La = dppv<0x126>(L); ea = dppv<0x126>(e); Lb = dppv<0x12E>(L); eb = dppv<0x12E>(e); break;
+        default: La = dppv<0x127>(L); ea = dppv<0x127>(e); Lb = dppv<0x12F>(L); eb = dppv<0x12F>(e); break;
+      }
+      const bool same = m8 >= r;  // lane - r stays inside the half
+      term(same ? La : Lb, same ? ea : eb);
+    }
+  } else if constexpr (LG == 4) {
+#define SA_ROR(R) term(dppv<0x120 + (R)>(L), dppv<0x120 + (R)>(e));
+    SA_ROR(1) SA_ROR(2) SA_ROR(3) SA_ROR(4) SA_ROR(5) SA_ROR(6) SA_ROR(7) SA_ROR(8)
+    SA_ROR(9) SA_ROR(10) SA_ROR(11) SA_ROR(12) SA_ROR(13) SA_ROR(14) SA_ROR(15)
+#undef SA_ROR
+  }
+  return acc;
+}
+
+// 64-bit all-reduce (sum) over the wave, result in every lane
+__device__ __forceinline__ uint64_t wave_sum64_dpp(uint64_t v) {
+  const uint64_t incl = scan_add64(v);
+  return rl64(incl, kWave - 1);
+}
+
+struct RegState {
+  uint32_t A;  // output length | request id << 16
+  uint32_t E;  // e | kind << 30
+  uint32_t PF, T;
+};
+
+// Full replay of the order held in registers: (met count, total latency).
+template <int LG>
+__device__ __forceinline__ Score reg_replay(const RegState &s, int n, uint32_t d0, uint32_t d2, int lane) {
+  constexpr int B = 1 << LG;
+  const bool valid = lane < n;
+  const uint32_t L = s.A & 0xFFFFu, e = s.E & 0x3FFFFFFFu, kind = s.E >> 30;
+  const uint32_t acc = __umul24(L, __umul24(d2, L) + e) + pair_sum_others<LG>(L, e, d2, lane);
+  const uint32_t P = Seg<LG>::template all<OpAdd>(s.PF, lane);
+  const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
+  const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);
+  const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)D : 0ull;
+  const uint64_t S = scan_add64(contrib) - contrib;
+  const uint64_t ttft = S + P, e2e = S + F;
+  const bool met = valid && (kind == 0 ? ttft <= (uint64_t)s.T : (kind == 2 ? e2e <= (uint64_t)s.T : F - P <= s.T));
+  const int64_t nmet = __popcll(__ballot(met));
+  return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+}
+
+// One chain by one wave: record slot `chain`, Philox chain index `rng_chain`.
+template <int LG, int OBJ>
+__device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chains, int chain, uint32_t rng_chain,
+                                int iters, double T0, double alpha, uint32_t key0, uint32_t key1, uint64_t swap_thr,
+                                const SearchParams &srch, unsigned char *ws) {
+  const int n = m.n;
+  const int lane = lane_id();
+  const uint32_t d0 = (uint32_t)m.d0, d2 = (uint32_t)m.d2;
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  RegState cur{0u, 0u, 0u, 0u};
+  if (lane < n) {
+    const uint32_t r = start[lane];
+    const uint32_t lin = q.in_len[r], L = q.out_len[r], kind = q.kind[r], thr = q.thr[r];
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    const uint64_t thr_l = (uint64_t)thr * L;
+    cur.A = L | (r << 16);
+    cur.E = e | (kind << 30);
+    cur.PF = (uint32_t)(m.p0 + m.p1 * lin);
+    cur.T = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : thr;
+    gbest[lane] = (uint16_t)r;
+  }
+  const Score s0 = reg_replay<LG>(cur, n, d0, d2, lane);
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
+  ProposalStream ps;
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+    RegState cand;
+    if (((pk >> 20) & 1u) == 0u) {
+      // swap positions i and j
+      auto sw = [&](uint32_t x) {
+        const uint32_t xi = readlane(x, i), xj = readlane(x, j);
+        return wlane_m0(xi, j, wlane_m0(xj, i, x));
+      };
+      cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
+    } else {
+      // insert: the request at i moves to j, the ones between shift by one toward i
+      const bool right = i < j;
+      const bool in_rng = right ? (lane >= i && lane < j) : (lane > j && lane <= i);
+      auto ins = [&](uint32_t x) {
+        const uint32_t xi = readlane(x, i);
+        const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);  // x[lane + 1] / x[lane - 1]
+        return wlane_m0(xi, j, in_rng ? sh : x);
+      };
+      cand = RegState{ins(cur.A), ins(cur.E), ins(cur.PF), ins(cur.T)};
+    }
+    const Score s = reg_replay<LG>(cand, n, d0, d2, lane);
+    const bool acc = obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3);
+    if (acc) {
+      cur = cand;
+      cn = s.n;
+      ct = s.t;
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+        if (lane < n) gbest[lane] = (uint16_t)(cur.A >> 16);
+      }
+    }
+    cool.step();
+  }
+  if (lane < n) gcur[lane] = (uint16_t)(cur.A >> 16);
+  if (lane == 0) {
+    int64_t *rec = reinterpret_cast<int64_t *>(ws + ws_off_records(n)) + (size_t)chain * 8;
+    rec[0] = cn;
+    rec[1] = (int64_t)ct;
+    rec[2] = bn;
+    rec[3] = (int64_t)bt;
+    rec[4] = biter;
+    rec[5] = accepts;
+    rec[6] = (int64_t)digest;
+    rec[7] = allmet;
+  }
+}
+
+// One wave per chain; blockDim / 64 chains per workgroup; no LDS.
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
+                                                          double alpha, uint32_t key0, uint32_t key1,
+                                                          uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  anneal_reg_body<LG, OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+}
+
+}  // namespace sa

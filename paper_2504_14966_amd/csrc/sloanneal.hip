@@ -15,6 +15,7 @@
 #include "anneal_wave.h"
 #include "anneal_sized.h"
 #include "multi.h"
+#include "anneal_reg.h"
 #include "fit.h"
 
 namespace {
@@ -348,6 +349,26 @@ int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevM
   bool done = false;
   if (model->policy == SCHED_STATIC_SEARCH) {
     if ((rc = launch_sized<OBJ>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream))) return rc;
+    done = true;
+  }
+  if (!done && model->policy == SCHED_STATIC && sa::reg_kernel_fits(n, model->max_batch) &&
+      static_narrow(h, model, n)) {
+    // small queue: the order and every request field in registers, no LDS; four chains per
+    // workgroup, or fewer so that the chains spread over every CU
+    const int cus = std::max(1, cu_count());
+    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
+    const int grid = (chains + waves - 1) / waves;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    const sa::QueuePtrs qp = dev_queue(queue);
+    const uint64_t st = model->swap_threshold;
+    switch (model->max_batch) {
+      case 1: sa::anneal_reg_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 2: sa::anneal_reg_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 4: sa::anneal_reg_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 8: sa::anneal_reg_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      default: sa::anneal_reg_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+    }
+    HIP_TRY(hipGetLastError());
     done = true;
   }
   if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {

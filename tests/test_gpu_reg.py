@@ -1,0 +1,67 @@
+"""GPU parity of the small-queue annealing kernel (order and request fields in registers:
+at most 64 requests, batch sizes 1, 2, 4, 8 or 16) against the oracle, bit for bit, per
+chain: start order, records, final and best orders, and the cross-chain winner; for every
+batch size, ragged queues, swap-only / insert-only / mixed moves and both objectives."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(__file__))
+from gpu_helpers import oracle_chains  # noqa: E402
+
+from paper_2504_14966_amd.workloads import Model, random_queue  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2504_14966_amd.sloanneal as m
+    m.load_library()
+    return m
+
+
+def _run_check(sl, orc, q, m, chains, iters, T0, alpha, seed, search=None):
+    import torch
+    dq = sl.DeviceQueue.from_queue(q)
+    ws = sl.sched_anneal(dq, m, chains, iters, T0, alpha, seed, search=sl.Search(*search) if search else None)
+    rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    st, info = sl.sched_start_info(ws, q.n)
+    bp, key = sl.sched_best(ws, q.n)
+    torch.cuda.synchronize()
+    rec, cur, best = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best)
+    s_orc = orc.Search(*search) if search else None
+    oi = orc.start(q, m, s_orc)
+    assert sl.as_u16(st).tolist() == oi[0].tolist()
+    assert info.cpu().numpy().tolist() == [oi[1], oi[3], oi[4], int(oi[2])]
+    want = oracle_chains(q, m, range(chains), iters, T0, alpha, seed, oi, search)
+    for c in range(chains):
+        wrec, wcur, wbest = want[c]
+        assert rec[c].tolist() == wrec.tolist(), c
+        assert cur[c].tolist() == wcur.tolist() and best[c].tolist() == wbest.tolist(), c
+    if not (search and search[0]):
+        k = max(range(chains), key=lambda c: (rec[c, 2], -rec[c, 3], -c))
+        assert key.cpu().numpy().tolist() == [rec[k, 2], rec[k, 3], k]
+        assert sl.as_u16(bp).tolist() == best[k].tolist()
+
+
+@pytest.mark.parametrize("n,B", [(2, 1), (13, 1), (3, 2), (31, 2), (5, 4), (64, 4), (9, 8), (57, 8), (16, 16),
+                                 (17, 16), (50, 16), (64, 16)])
+@pytest.mark.parametrize("thr", [0, 1 << 32, 1 << 31])
+def test_reg_kernel_shapes_and_moves(sl, orc, n, B, thr):
+    rng = np.random.default_rng(n * 131 + B * 7 + (thr >> 30))
+    q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=60_000 * n)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2, swap_threshold=thr)
+    _run_check(sl, orc, q, m, 6, 400, 0.8, 0.995, 11)
+
+
+@pytest.mark.parametrize("B,search", [(8, (1, 20, 0)), (16, (1, 7, 1)), (4, (0, 5, 0)), (2, (1, 3, 1))])
+def test_reg_kernel_objectives(sl, orc, B, search):
+    rng = np.random.default_rng(200 + B)
+    q = random_queue(rng, 48, max_in=3000, max_out=150, thr_hi=3_000_000)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    _run_check(sl, orc, q, m, 8, 500, 3.0, 0.97, 5, search)
