@@ -17,8 +17,8 @@
 //     latency sum by one 64-bit wave reduction.
 // The 32-bit products and sums are exact under the fixed-size delta kernel's width checks.
 #pragma once
-#include "anneal_static.h"
-#include "device_cont.h"
+#include "anneal_sized.h"
+#include "anneal_wave.h"
 
 namespace sa {
 
@@ -212,6 +212,229 @@ __global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
   anneal_reg_body<LG, OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+}
+
+// ---- the joint order / batch-size search on small queues, state in registers ----
+//
+// Same register layout of the order; the layout is a 64-bit scalar mask of start flags
+// (bit p set iff a batch begins at position p). The squeeze / delay / swap rules are the
+// ones of plan_move taken on the mask (batch begin = highest flag at or below a position,
+// batch end = next flag above it, or n). The whole queue is one window of at most 64
+// positions: each lane gathers its batch's members with ds_bpermute, eight offsets in flight
+// at a time (pair terms), the batch prefill is the difference of one add-scan at the batch's
+// ends, the batch durations are one 64-bit max-scan of (first position of the batch << 32 |
+// finish offset), the starts one 32-bit add-scan. Every time fits 32 bits (the host's check
+// for the search's delta kernel).
+
+__host__ __device__ __forceinline__ bool reg_sized_fits(int n) { return n >= 1 && n <= 64; }
+
+__device__ __forceinline__ int mask_begin(uint64_t fm, int p) {  // highest start at or below p
+  const uint64_t le = p >= 63 ? fm : fm & ((uint64_t(2) << p) - 1);
+  return 63 - __clzll(le);
+}
+__device__ __forceinline__ int mask_end(uint64_t fm, int n, int p) {  // first start above p, or n
+  const uint64_t gt = p >= 63 ? 0ull : fm & ~((uint64_t(2) << p) - 1);
+  return gt ? min(n, __builtin_ctzll(gt)) : n;
+}
+
+struct RegMove {
+  bool made;
+  int op, i, j, to, set0, clr0;
+};
+
+// plan_move on the mask (all wave-uniform)
+__device__ __forceinline__ RegMove reg_plan(uint64_t fm, int n, int B, int op, int i, int j) {
+  RegMove mv{false, op, i, j, i, -1, -1};
+  if (op == 2) {
+    mv.made = n >= 2;
+    return mv;
+  }
+  const int s = mask_begin(fm, i), e = mask_end(fm, n, i);
+  if (op == 0) {
+    if (s == 0) return mv;
+    const int sp = mask_begin(fm, s - 1);
+    if (s - sp >= B) return mv;
+    mv.made = true;
+    mv.to = s;
+    mv.clr0 = s;
+    mv.set0 = s + 1 < e ? s + 1 : -1;
+    return mv;
+  }
+  if (e == n) {
+    if (e - s < 2) return mv;
+    mv.made = true;
+    mv.to = e - 1;
+    mv.set0 = e - 1;
+    return mv;
+  }
+  const int en = mask_end(fm, n, e);
+  if (en - e >= B) return mv;
+  mv.made = true;
+  mv.to = e - 1;
+  mv.set0 = e - 1;
+  mv.clr0 = e;
+  return mv;
+}
+
+__device__ __forceinline__ uint32_t bperm(uint32_t v, int src) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)v);
+}
+
+// Full replay of the order in registers with the layout fm: (met count, total latency).
+__device__ __forceinline__ Score reg_replay_sized(const RegState &s, uint64_t fm, int n, uint32_t d0, uint32_t d2,
+                                                  int lane) {
+  const bool valid = lane < n;
+  const uint32_t L = s.A & 0xFFFFu, e = s.E & 0x3FFFFFFFu, kind = s.E >> 30;
+  const int b0 = valid ? mask_begin(fm, lane) : lane;
+  const int b1 = valid ? mask_end(fm, n, lane) - 1 : lane;
+  const int bl = b1 - b0 + 1;
+  // the largest batch (lane 63 holds the wave maximum after the six steps)
+  uint32_t mb = (uint32_t)bl;
+#pragma unroll
+  for (int st = 0; st < 6; ++st) mb = dpp_step<OpMax>(mb, st);
+  const int maxb = (int)readlane(mb, 63);
+  // batch prefill from one add-scan: the inclusive sum at the batch's last lane minus the
+  // exclusive sum at its first lane (both gathers unconditional: ds_bpermute reads only
+  // lanes that execute it)
+  const uint32_t pinc = scan_add32(s.PF), pexc = pinc - s.PF;
+  const uint32_t P = bperm(pinc, b1) - bperm(pexc, b0);
+  // pair terms: the batch's members gathered eight offsets at a time, so that eight pairs
+  // of ds_bpermute are in flight before their results are used
+  uint32_t acc = 0;
+  for (int d = 0; d < maxb; d += 8) {
+    uint32_t Lj[8], ej[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int src = min(b0 + d + u, kWave - 1);
+      Lj[u] = bperm(L, src);
+      ej[u] = bperm(e, src);
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t mu = min(Lj[u], L);
+      const uint32_t w = __umul24(mu, __umul24(d2, mu) + ej[u]);
+      acc += d + u < bl ? w : 0u;
+    }
+  }
+  const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
+  const uint64_t D64 = scan_max64(valid ? ((uint64_t)b0 << 32) | F : 0ull);
+  const uint32_t contrib = (valid && lane == b1) ? (uint32_t)D64 : 0u;
+  const uint32_t S = scan_add32(contrib) - contrib;
+  const uint32_t ttft = S + P, e2e = S + F;
+  const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : F - P <= s.T));
+  const int64_t nmet = __popcll(__ballot(met));
+  // the latency sum: 16-bit halves of the 32-bit latencies, each sum below 2^22
+  uint32_t lo = valid ? (e2e & 0xFFFFu) : 0u, hi = valid ? (e2e >> 16) : 0u;
+  wave_all2<OpAdd, OpAdd>(lo, hi);
+  return Score{nmet, (uint64_t)lo + ((uint64_t)hi << 16)};
+}
+
+template <int OBJ>
+__device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int chains, int chain,
+                                      uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0,
+                                      uint32_t key1, const SearchParams &srch, unsigned char *ws) {
+  const int n = m.n, B = m.B;
+  const int lane = lane_id();
+  const uint32_t d0 = (uint32_t)m.d0, d2 = (uint32_t)m.d2;
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n), fstride = ws_flag_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  uint8_t *gbest_f = ws + ws_off_best_starts(n, chains) + (size_t)chain * fstride;
+  uint8_t *gcur_f = ws + ws_off_cur_starts(n, chains) + (size_t)chain * fstride;
+  RegState cur{0u, 0u, 0u, 0u};
+  const bool first = lane < n && lane % B == 0;
+  uint64_t fm = __ballot(first);  // the maximum-size layout
+  if (lane < n) {
+    const uint32_t r = start[lane];
+    const uint32_t lin = q.in_len[r], L = q.out_len[r], kind = q.kind[r], thr = q.thr[r];
+    const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+    const uint64_t thr_l = (uint64_t)thr * L;
+    cur.A = L | (r << 16);
+    cur.E = e | (kind << 30);
+    cur.PF = (uint32_t)(m.p0 + m.p1 * lin);
+    cur.T = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : thr;
+    gbest[lane] = (uint16_t)r;
+    gbest_f[lane] = first ? 1 : 0;
+  }
+  const Score s0 = reg_replay_sized(cur, fm, n, d0, d2, lane);
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
+  SizedDraws ds;
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
+    if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, rng_chain, key0, key1);
+    const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
+    const RegMove mv = reg_plan(fm, n, B, (int)(pk >> 20), (int)(pk & 1023u), (int)((pk >> 10) & 1023u));
+    if (mv.made) {
+      RegState cand;
+      uint64_t fc = fm;
+      if (mv.op == 2) {
+        const int i = mv.i, j = mv.j;
+        auto sw = [&](uint32_t x) {
+          const uint32_t xi = readlane(x, i), xj = readlane(x, j);
+          return wlane_m0(xi, j, wlane_m0(xj, i, x));
+        };
+        cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
+      } else {
+        const int i = mv.i, to = mv.to;
+        const bool right = i < to;
+        const bool in_rng = right ? (lane >= i && lane < to) : (lane > to && lane <= i);
+        auto ins = [&](uint32_t x) {
+          const uint32_t xi = readlane(x, i);
+          const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);
+          return wlane_m0(xi, to, in_rng ? sh : x);
+        };
+        cand = RegState{ins(cur.A), ins(cur.E), ins(cur.PF), ins(cur.T)};
+        if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
+        if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
+      }
+      const Score sc = reg_replay_sized(cand, fc, n, d0, d2, lane);
+      if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
+        cur = cand;
+        fm = fc;
+        cn = sc.n;
+        ct = sc.t;
+        ++accepts;
+        digest = (digest ^ (uint64_t)k) * kFnvPrime;
+        digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+        digest = (digest ^ ct) * kFnvPrime;
+        if (obj_better<OBJ>(cn, ct, bn, bt)) {
+          bn = cn;
+          bt = ct;
+          biter = k;
+          if (lane < n) {
+            gbest[lane] = (uint16_t)(cur.A >> 16);
+            gbest_f[lane] = (uint8_t)((fm >> lane) & 1u);
+          }
+        }
+      }
+    }
+    cool.step();
+  }
+  if (lane < n) {
+    gcur[lane] = (uint16_t)(cur.A >> 16);
+    gcur_f[lane] = (uint8_t)((fm >> lane) & 1u);
+  }
+  if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
+}
+
+template <int OBJ>
+__global__ void __launch_bounds__(256) anneal_reg_sized_kernel(DevModel m, QueuePtrs q, int chains, int iters,
+                                                                double T0, double alpha, uint32_t key0, uint32_t key1,
+                                                                SearchParams srch, unsigned char *ws) {
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  anneal_reg_sized_body<OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, srch, ws);
 }
 
 }  // namespace sa

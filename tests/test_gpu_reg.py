@@ -1,7 +1,9 @@
-"""GPU parity of the small-queue annealing kernel (order and request fields in registers:
-at most 64 requests, batch sizes 1, 2, 4, 8 or 16) against the oracle, bit for bit, per
-chain: start order, records, final and best orders, and the cross-chain winner; for every
-batch size, ragged queues, swap-only / insert-only / mixed moves and both objectives."""
+"""GPU parity of the small-queue annealing kernels (order and request fields in registers,
+at most 64 requests) against the oracle, bit for bit, per chain. Fixed-size batches of 1, 2,
+4, 8 or 16: start order, records, final and best orders, and the cross-chain winner, for
+every batch size, ragged queues, swap-only / insert-only / mixed moves and both objectives.
+The joint order / batch-size search (layout as a register bit mask): records, orders and
+layouts for batch sizes from 1 to 64 and both objectives."""
 import os
 import sys
 
@@ -65,3 +67,40 @@ def test_reg_kernel_objectives(sl, orc, B, search):
     q = random_queue(rng, 48, max_in=3000, max_out=150, thr_hi=3_000_000)
     m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
     _run_check(sl, orc, q, m, 8, 500, 3.0, 0.97, 5, search)
+
+
+def _search_check(sl, orc, q, m, chains, iters, T0, alpha, seed, search=None):
+    import torch
+    sys.path.insert(0, os.path.dirname(__file__))
+    from gpu_helpers import oracle_chains_batches
+    dq = sl.DeviceQueue.from_queue(q)
+    ws = sl.sched_anneal(dq, m, chains, iters, T0, alpha, seed, search=sl.Search(*search) if search else None)
+    rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    cs, bs, win = sl.sched_starts(ws, q.n, chains)
+    torch.cuda.synchronize()
+    rec, cur, best, cs, bs = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best), cs.cpu().numpy(), bs.cpu().numpy()
+    s_orc = orc.Search(*search) if search else None
+    info = orc.start(q, m, s_orc)
+    want = oracle_chains_batches(q, m, range(chains), iters, T0, alpha, seed, info, search)
+    for c in range(chains):
+        w = want[c]
+        assert rec[c].tolist() == w["rec"].tolist(), c
+        assert cur[c].tolist() == w["cur"].tolist() and best[c].tolist() == w["best"].tolist(), c
+        assert cs[c].tolist() == w["cur_starts"].tolist() and bs[c].tolist() == w["best_starts"].tolist(), c
+
+
+@pytest.mark.parametrize("n,B", [(5, 2), (17, 5), (33, 16), (63, 9), (64, 32), (50, 64), (64, 1)])
+def test_reg_search_shapes(sl, orc, n, B):
+    # the joint order / batch-size search on small queues (layout as a register bit mask)
+    rng = np.random.default_rng(500 + n * 3 + B)
+    q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=60_000 * n)
+    m = Model(B, 2, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    _search_check(sl, orc, q, m, 6, 500, 0.8, 0.995, 13)
+
+
+@pytest.mark.parametrize("n,B,search", [(24, 6, (1, 10, 1)), (48, 16, (1, 25, 0)), (40, 3, (0, 4, 1))])
+def test_reg_search_objectives(sl, orc, n, B, search):
+    rng = np.random.default_rng(600 + n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=3_000_000)
+    m = Model(B, 2, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    _search_check(sl, orc, q, m, 6, 600, 3.0, 0.97, 21, search)
