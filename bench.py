@@ -123,15 +123,15 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 175.25 KiB x 2.0 + WRITE_SIZE 16683.1 KiB x 1.0, burst workload, one launch
-    "cb3976faba66e6cc9dd9f3d8778f65a9f2ec836f45f5b8da996bf58577a59f1c": 17442388,
+    # FETCH_SIZE 177.7 KiB x 2.0 + WRITE_SIZE 16,683 KiB x 1.0, burst workload, one launch
+    "40d53b42850d5dbf0359155378a06c44d3edada4b427b65bab234a2fa54ce73c": 17447251,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "cb3976faba66e6cc9dd9f3d8778f65a9f2ec836f45f5b8da996bf58577a59f1c": 0.675,
+    "40d53b42850d5dbf0359155378a06c44d3edada4b427b65bab234a2fa54ce73c": 0.677,
 }
 
 
