@@ -19,6 +19,7 @@
 #pragma once
 #include "anneal_sized.h"
 #include "anneal_wave.h"
+#include "fit.h"
 
 namespace sa {
 
@@ -435,6 +436,160 @@ __global__ void __launch_bounds__(256) anneal_reg_sized_kernel(DevModel m, Queue
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
   anneal_reg_sized_body<OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, srch, ws);
+}
+
+// ---- the fitted latency model on small queues, state in registers ----
+//
+// A member's prefill and decode times depend only on its own lengths and its batch's size,
+// so the replay needs no gathers: each lane takes its batch size from the flag mask and
+// its two closed forms in 64 bits; the batch durations are one 64-bit max-scan of (first
+// position of the batch << 58 | time), the starts one 64-bit add-scan (every time below
+// 2^57, the host's check). Fixed-size batches take swap / insert proposals with the layout
+// fixed; the batch-size search takes squeeze / delay / swap as above.
+
+struct RegFit {
+  uint32_t A;   // output length | request id << 16
+  uint32_t LK;  // input length | kind << 16
+  uint32_t T, T2;
+};
+
+__device__ __forceinline__ Score reg_replay_fit(const DevFit &f, const RegFit &s, uint64_t fm, int lane) {
+  const int n = f.n;
+  const bool valid = lane < n;
+  const uint64_t L = s.A & 0xFFFFu, l = s.LK & 0xFFFFu;
+  const uint32_t kind = s.LK >> 16;
+  const int b0 = valid ? mask_begin(fm, lane) : lane;
+  const int b1 = valid ? mask_end(fm, n, lane) - 1 : lane;
+  const uint64_t b = (uint64_t)(b1 - b0 + 1);
+  const uint64_t tp = fit_prefill(f, b, l), td = fit_decode(f, b, l, L), E = tp + td;
+  constexpr uint64_t kTimeMask = (uint64_t(1) << 58) - 1;
+  const uint64_t D = scan_max64(valid ? ((uint64_t)b0 << 58) | E : 0ull) & kTimeMask;
+  const uint64_t contrib = (valid && lane == b1) ? D : 0ull;
+  const uint64_t S = scan_add64(contrib) - contrib;
+  const uint64_t ttft = S + tp, e2e = S + E;
+  const bool met = valid && fit_met(kind, s.T, s.T2, L, ttft, td, e2e);
+  const int64_t nmet = __popcll(__ballot(met));
+  return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+}
+
+template <int OBJ>
+__device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const uint32_t *thr2, int chains, int chain,
+                                    uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0,
+                                    uint32_t key1, uint64_t swap_thr, const SearchParams &srch, unsigned char *ws) {
+  const int n = f.n, B = f.B;
+  const bool search = f.policy == 2;
+  const int lane = lane_id();
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = h->t_ref;
+  const int64_t allmet = h->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n), fstride = ws_flag_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  uint8_t *gbest_f = ws + ws_off_best_starts(n, chains) + (size_t)chain * fstride;
+  uint8_t *gcur_f = ws + ws_off_cur_starts(n, chains) + (size_t)chain * fstride;
+  RegFit cur{0u, 0u, 0u, 0u};
+  const bool first = lane < n && lane % B == 0;
+  uint64_t fm = __ballot(first);  // the maximum-size layout
+  if (lane < n) {
+    const uint32_t r = start[lane];
+    cur.A = (uint32_t)q.out_len[r] | (r << 16);
+    cur.LK = (uint32_t)q.in_len[r] | ((uint32_t)q.kind[r] << 16);
+    cur.T = q.thr[r];
+    cur.T2 = thr2 ? thr2[r] : 0u;
+    gbest[lane] = (uint16_t)r;
+    gbest_f[lane] = first ? 1 : 0;
+  }
+  const Score s0 = reg_replay_fit(f, cur, fm, lane);
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
+  SizedDraws ds;
+  ProposalStream ps;
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
+    uint32_t w3;
+    RegMove mv;
+    if (search) {
+      if ((k & (kWave - 1)) == 0) ds.refill(k, lane, n, rng_chain, key0, key1);
+      const uint32_t pk = ds.packed(k);
+      w3 = ds.word3(k);
+      mv = reg_plan(fm, n, B, (int)(pk >> 20), (int)(pk & 1023u), (int)((pk >> 10) & 1023u));
+    } else {
+      if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
+      const uint32_t pk = ps.packed(k);
+      w3 = ps.word3(k);
+      const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+      // a fixed-size move: swap (op 2) or insert from i to j (op 3), layout unchanged
+      mv = RegMove{true, ((pk >> 20) & 1u) ? 3 : 2, i, j, j, -1, -1};
+    }
+    if (mv.made) {
+      RegFit cand;
+      uint64_t fc = fm;
+      if (mv.op == 2) {
+        const int i = mv.i, j = mv.j;
+        auto sw = [&](uint32_t x) {
+          const uint32_t xi = readlane(x, i), xj = readlane(x, j);
+          return wlane_m0(xi, j, wlane_m0(xj, i, x));
+        };
+        cand = RegFit{sw(cur.A), sw(cur.LK), sw(cur.T), sw(cur.T2)};
+      } else {
+        const int i = mv.i, to = mv.to;
+        const bool right = i < to;
+        const bool in_rng = right ? (lane >= i && lane < to) : (lane > to && lane <= i);
+        auto ins = [&](uint32_t x) {
+          const uint32_t xi = readlane(x, i);
+          const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);
+          return wlane_m0(xi, to, in_rng ? sh : x);
+        };
+        cand = RegFit{ins(cur.A), ins(cur.LK), ins(cur.T), ins(cur.T2)};
+        if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
+        if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
+      }
+      const Score sc = reg_replay_fit(f, cand, fc, lane);
+      if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
+        cur = cand;
+        fm = fc;
+        cn = sc.n;
+        ct = sc.t;
+        ++accepts;
+        digest = (digest ^ (uint64_t)k) * kFnvPrime;
+        digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+        digest = (digest ^ ct) * kFnvPrime;
+        if (obj_better<OBJ>(cn, ct, bn, bt)) {
+          bn = cn;
+          bt = ct;
+          biter = k;
+          if (lane < n) {
+            gbest[lane] = (uint16_t)(cur.A >> 16);
+            gbest_f[lane] = (uint8_t)((fm >> lane) & 1u);
+          }
+        }
+      }
+    }
+    cool.step();
+  }
+  if (lane < n) {
+    gcur[lane] = (uint16_t)(cur.A >> 16);
+    gcur_f[lane] = (uint8_t)((fm >> lane) & 1u);
+  }
+  if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
+}
+
+template <int OBJ>
+__global__ void __launch_bounds__(256) anneal_reg_fit_kernel(DevFit f, QueuePtrs q, const uint32_t *thr2, int chains,
+                                                              int iters, double T0, double alpha, uint32_t key0,
+                                                              uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                              unsigned char *ws) {
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  anneal_reg_fit_body<OBJ>(f, q, thr2, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                           ws);
 }
 
 }  // namespace sa

@@ -874,17 +874,31 @@ int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, c
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_fit_kernel<<<1, 1024, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, fit->t_ref, srch, w);
   HIP_TRY(hipGetLastError());
-  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
-  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb);
-  const int grid = (chains + 3) / 4;
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  if (srch.objective)
-    sa::anneal_fit_kernel<1><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0, k1,
-                                                         fit->swap_threshold, srch, w);
-  else
-    sa::anneal_fit_kernel<0><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0, k1,
-                                                         fit->swap_threshold, srch, w);
-  HIP_TRY(hipGetLastError());
+  if (n <= 64 && df.win) {
+    // small queue: order, request fields and layout in registers, no LDS
+    const int cus = std::max(1, cu_count());
+    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
+    const int rgrid = (chains + waves - 1) / waves;
+    if (srch.objective)
+      sa::anneal_reg_fit_kernel<1><<<rgrid, waves * 64, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0,
+                                                                     alpha, k0, k1, fit->swap_threshold, srch, w);
+    else
+      sa::anneal_reg_fit_kernel<0><<<rgrid, waves * 64, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0,
+                                                                     alpha, k0, k1, fit->swap_threshold, srch, w);
+    HIP_TRY(hipGetLastError());
+  } else {
+    const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+    const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb);
+    const int grid = (chains + 3) / 4;
+    if (srch.objective)
+      sa::anneal_fit_kernel<1><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0,
+                                                           k1, fit->swap_threshold, srch, w);
+    else
+      sa::anneal_fit_kernel<0><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0,
+                                                           k1, fit->swap_threshold, srch, w);
+    HIP_TRY(hipGetLastError());
+  }
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;

@@ -98,6 +98,20 @@ def _anneal(sl, q, fd, chains, iters, T0, alpha, seed, thr2, search):
                 bs=bs.cpu().numpy(), start=sl.as_u16(st), info=info.cpu().numpy(), key=key.cpu().numpy())
 
 
+def _check_winner(res, ratio):
+    # the cross-chain winner: best key by the objective, lowest chain on ties
+    from fractions import Fraction
+    r = res["rec"]
+    if ratio:
+        k = 0
+        for c in range(1, len(r)):
+            if Fraction(int(r[c, 2]), int(r[c, 3])) > Fraction(int(r[k, 2]), int(r[k, 3])):
+                k = c
+    else:
+        k = max(range(len(r)), key=lambda c: (r[c, 2], -r[c, 3], -c))
+    assert res["key"].tolist() == [r[k, 2], r[k, 3], k]
+
+
 @pytest.mark.parametrize("policy,search", [(0, None), (2, None), (0, (1, 10, 0)), (2, (1, 10, 1))])
 def test_anneal_fit_chat_code(sl, orc, policy, search):
     q, thr2 = chat_code_queue_10ns(64, 0)
@@ -113,6 +127,7 @@ def test_anneal_fit_chat_code(sl, orc, policy, search):
         assert res["rec"][c].tolist() == w["rec"].tolist(), c
         assert res["cur"][c].tolist() == w["cur"].tolist() and res["best"][c].tolist() == w["best"].tolist(), c
         assert res["cs"][c].tolist() == w["cur_starts"].tolist() and res["bs"][c].tolist() == w["best_starts"].tolist(), c
+    _check_winner(res, bool(search and search[0]))
 
 
 @pytest.mark.parametrize("n,B,policy", [(1, 3, 0), (2, 1, 2), (40, 64, 2), (300, 8, 0)])
@@ -127,6 +142,7 @@ def test_anneal_fit_shapes(sl, orc, n, B, policy):
         w = orc.anneal_chain_fit(q, fo, c, iters, 0.5, 0.99, 7, start_info=info)
         assert res["rec"][c].tolist() == w["rec"].tolist(), c
         assert res["best"][c].tolist() == w["best"].tolist(), c
+    _check_winner(res, False)
 
 
 @pytest.mark.parametrize("policy", [0, 2])

@@ -104,3 +104,36 @@ def test_reg_search_objectives(sl, orc, n, B, search):
     q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=3_000_000)
     m = Model(B, 2, p0=2000, p1=40, d0=8000, d1=300, d2=2)
     _search_check(sl, orc, q, m, 6, 600, 3.0, 0.97, 21, search)
+
+
+@pytest.mark.parametrize("n,B,policy,search", [(17, 3, 0, None), (33, 7, 2, None), (64, 64, 0, None),
+                                               (64, 16, 2, (1, 10, 1)), (30, 5, 0, (1, 6, 0)), (1, 4, 2, None)])
+def test_reg_fit(sl, orc, n, B, policy, search):
+    # the fitted model (Table 2) with the chat SLO on small queues: order, fields and layout
+    # in registers
+    import torch
+    from paper_2504_14966_amd.workloads import TABLE2_10NS
+    rng = np.random.default_rng(700 + n + B + policy)
+    q = random_queue(rng, n, max_in=2000, max_out=300, thr_hi=2_000_000_000)
+    q.kind[::3] = 3
+    thr2 = rng.integers(1_500_000, 1_800_000, n).astype(np.uint32)
+    fd, fo = sl.FitModel(B, policy, **TABLE2_10NS), orc.FitModel(B, policy, **TABLE2_10NS)
+    dq = sl.DeviceQueue.from_queue(q)
+    chains, iters = 6, 500
+    ws = sl.sched_anneal_fit(dq, fd, chains, iters, 1.5, 0.98, 4, tpot_thr=sl.thr_to_device(thr2),
+                             search=sl.Search(*search) if search else None)
+    rec, cur, best = sl.sched_chains(ws, n, chains, perms=True)
+    cs, bs, _ = sl.sched_starts(ws, n, chains)
+    _, key = sl.sched_best(ws, n)
+    torch.cuda.synchronize()
+    rec, cur, best, cs, bs = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best), cs.cpu().numpy(), bs.cpu().numpy()
+    s_orc = orc.Search(*search) if search else None
+    info = orc.start_fit(q, fo, s_orc, thr2)
+    for c in range(chains):
+        w = orc.anneal_chain_fit(q, fo, c, iters, 1.5, 0.98, 4, search=s_orc, thr2=thr2, start_info=info)
+        assert rec[c].tolist() == w["rec"].tolist(), c
+        assert cur[c].tolist() == w["cur"].tolist() and best[c].tolist() == w["best"].tolist(), c
+        assert cs[c].tolist() == w["cur_starts"].tolist() and bs[c].tolist() == w["best_starts"].tolist(), c
+    if not (search and search[0]):
+        k = max(range(chains), key=lambda c: (rec[c, 2], -rec[c, 3], -c))
+        assert key.cpu().numpy().tolist() == [rec[k, 2], rec[k, 3], k]
