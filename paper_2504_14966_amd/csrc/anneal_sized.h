@@ -172,19 +172,39 @@ __device__ Score replay_batches_windows(const DevModel &m, const uint4 *__restri
       kind = rq.z & 3u;
     }
     const uint64_t pf = in ? m.p0 + m.p1 * (uint64_t)lin : 0;
-    stage[lane] = make_uint4(L, lin, (uint32_t)pf, (uint32_t)(pf >> 32));
+    const bool narrow = (m.flags & kFlagStaticNarrow) != 0;
+    // narrow widths stage the pair-cost parameter e = 2 (d1 + d2 l_in) + d2 instead of l_in
+    const uint32_t ev = narrow ? (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2) : lin;
+    stage[lane] = make_uint4(L, ev, (uint32_t)pf, (uint32_t)(pf >> 32));
     wave_sync_lds();
     const int bl = in ? b1 - b0 + 1 : 0;
     int jmax = bl;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) jmax = max(jmax, __shfl_xor(jmax, o));
     uint64_t P = 0, acc = 0;
-    for (int j = 0; j < jmax; ++j) {
-      if (j < bl) {
-        const uint4 sj = stage[b0 + j];
-        P += (uint64_t)sj.z | ((uint64_t)sj.w << 32);
-        const uint64_t mu = min(sj.x, L);
-        acc += m.d1 * mu + m.d2 * ((uint64_t)sj.y * mu + (mu * (mu + 1) >> 1));
+    if (narrow) {
+      // doubled pair costs mu (e_j + d2 mu) in 24-bit products (each below 2^32, and their
+      // sum over a batch too: the host's width check), halved once
+      const uint32_t d2 = (uint32_t)m.d2;
+      uint32_t acc2 = 0, P32 = 0;
+      for (int j = 0; j < jmax; ++j) {
+        if (j < bl) {
+          const uint4 sj = stage[b0 + j];
+          P32 += sj.z;
+          const uint32_t mu = min(sj.x, L);
+          acc2 = mad24_v(mu, mad24_v(d2, mu, sj.y), acc2);
+        }
+      }
+      P = P32;
+      acc = acc2 >> 1;
+    } else {
+      for (int j = 0; j < jmax; ++j) {
+        if (j < bl) {
+          const uint4 sj = stage[b0 + j];
+          P += (uint64_t)sj.z | ((uint64_t)sj.w << 32);
+          const uint64_t mu = min(sj.x, L);
+          acc += m.d1 * mu + m.d2 * ((uint64_t)sj.y * mu + (mu * (mu + 1) >> 1));
+        }
       }
     }
     wave_sync_lds();

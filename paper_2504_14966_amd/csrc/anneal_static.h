@@ -70,6 +70,14 @@ __device__ __forceinline__ Req load_req(const uint4 *req, int r) {
   return Req{v.x >> 16, v.y, v.z & 3u, v.z >> 2, v.w};
 }
 
+// v_mad_u32_u24: a * b + c for a, b below 2^24 (the compiler would otherwise fuse the
+// multiply-add into a 64-bit v_mad_u64_u32)
+__device__ __forceinline__ uint32_t mad24_v(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t d;
+  asm("v_mad_u32_u24 %0, %1, %2, %3" : "=v"(d) : "v"(a), "v"(b), "v"(c));
+  return d;
+}
+
 // twice the decode cost member j (output L_j, e_j) adds to a member with output Lm
 __device__ __forceinline__ uint32_t w2(uint32_t Lj, uint32_t ej, uint32_t Lm, uint32_t d2) {
   const uint32_t mu = min(Lj, Lm);
@@ -728,11 +736,22 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
       const uint32_t P = Seg<LG>::template all<OpAdd>(x.pf, lane);
       uint32_t acc = 0;
       const int base = seg << LG;
-      for (int jj = 0; jj < B; ++jj) {
-        const uint2 sj = stage[base + jj];
+      // 24-bit products: d2 mu + e_j < 2^24 and mu (d2 mu + e_j) < 2^32 (host width check);
+      // four members per step so that their reads go out together
+      auto pair = [&](const uint2 sj) {
         const uint32_t mu = min(sj.x, x.L);
-        acc += mu * ((d2m * mu + sj.y) & 0xFFFFFFu);
+        acc = mad24_v(mu, mad24_v(d2m, mu, sj.y), acc);
+      };
+      int jj = 0;
+      for (; jj + 4 <= B; jj += 4) {
+        const uint2 s0 = stage[base + jj], s1 = stage[base + jj + 1], s2 = stage[base + jj + 2],
+                    s3 = stage[base + jj + 3];
+        pair(s0);
+        pair(s1);
+        pair(s2);
+        pair(s3);
       }
+      for (; jj < B; ++jj) pair(stage[base + jj]);
       wave_sync_lds();
       const uint32_t F = valid ? P + __umul24(x.L, sp.d0) + (acc >> 1) : 0u;
       const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);

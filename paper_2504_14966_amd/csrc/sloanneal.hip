@@ -200,13 +200,14 @@ bool timeline_narrow(const HostQueue &h, const sched_model_t *m, int n) {
 }
 
 sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false,
-                       bool narrow_time = false, bool windows = false) {
+                       bool narrow_time = false, bool windows = false, bool static_narrow_w = false) {
   sa::DevModel d;
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
   d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0) |
-            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0) | (windows ? sa::kFlagWindows : 0);
+            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0) | (windows ? sa::kFlagWindows : 0) |
+            (static_narrow_w ? sa::kFlagStaticNarrow : 0);
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
@@ -685,7 +686,8 @@ int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, c
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57));
+  const sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57),
+                                    static_narrow(h, model, n));
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 64 * 16 + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);

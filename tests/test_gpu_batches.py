@@ -221,3 +221,16 @@ def test_batches_huge_times_one_batch_replay(sl, orc):
     assert np.array_equal(_eval(sl, q, m, perms, starts), oracle_rows_batches(q, m, perms, starts))
     res = _anneal(sl, q, m, 4, 60, 0.7, 0.99, 9)
     _check_chains(orc, res, q, m, range(4), 60, 0.7, 0.99, 9)
+
+
+@pytest.mark.parametrize("n,B", [(40, 6), (300, 16)])
+def test_eval_batches_wide_model(sl, orc, n, B):
+    # pair costs beyond 24 bits (d2 large): the windowed replay in 64-bit arithmetic
+    rng = np.random.default_rng(n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=200, thr_hi=4_000_000_000)
+    assert int(q.in_len.max()) * 2 * 9000 > 1 << 24
+    m = Model(B, SEARCH, 2000, 40, 8000, 300, 9000)
+    k = 48
+    perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, n, B)
+    assert np.array_equal(_eval(sl, q, m, perms, starts), oracle_rows_batches(q, m, perms, starts))
