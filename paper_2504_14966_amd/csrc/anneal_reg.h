@@ -45,7 +45,7 @@ __device__ __forceinline__ uint32_t pair_sum_others(uint32_t L, uint32_t e, uint
   uint32_t acc = 0;
   auto term = [&](uint32_t Lj, uint32_t ej) {
     const uint32_t mu = min(Lj, L);
-    acc += __umul24(mu, __umul24(d2, mu) + ej);
+    acc = mad24_v(mu, mad24_v(d2, mu, ej), acc);
   };
   if constexpr (LG == 1) {
     term(dppv<0xB1>(L), dppv<0xB1>(e));  // quad_perm [1,0,3,2]
@@ -99,7 +99,7 @@ __device__ __forceinline__ Score reg_replay(const RegState &s, int n, uint32_t d
   constexpr int B = 1 << LG;
   const bool valid = lane < n;
   const uint32_t L = s.A & 0xFFFFu, e = s.E & 0x3FFFFFFFu, kind = s.E >> 30;
-  const uint32_t acc = __umul24(L, __umul24(d2, L) + e) + pair_sum_others<LG>(L, e, d2, lane);
+  const uint32_t acc = mad24_v(L, mad24_v(d2, L, e), pair_sum_others<LG>(L, e, d2, lane));
   const uint32_t P = Seg<LG>::template all<OpAdd>(s.PF, lane);
   const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
   const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);
@@ -313,7 +313,7 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, uint64_t fm
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint32_t mu = min(Lj[u], L);
-      const uint32_t w = __umul24(mu, __umul24(d2, mu) + ej[u]);
+      const uint32_t w = mad24_v(mu, mad24_v(d2, mu, ej[u]), 0u);
       acc += d + u < bl ? w : 0u;
     }
   }

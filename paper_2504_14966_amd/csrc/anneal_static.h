@@ -81,7 +81,7 @@ __device__ __forceinline__ uint32_t mad24_v(uint32_t a, uint32_t b, uint32_t c) 
 // twice the decode cost member j (output L_j, e_j) adds to a member with output Lm
 __device__ __forceinline__ uint32_t w2(uint32_t Lj, uint32_t ej, uint32_t Lm, uint32_t d2) {
   const uint32_t mu = min(Lj, Lm);
-  return __umul24(mu, __umul24(d2, mu) + ej);
+  return mad24_v(mu, mad24_v(d2, mu, ej), 0u);
 }
 
 // SLO flag of a member as a function of its batch start S: TPOT does not depend on S;
