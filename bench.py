@@ -297,7 +297,8 @@ def main():
 
     import torch
     import paper_2504_14966_amd.sloanneal as sl
-    from paper_2504_14966_amd.workloads import POLICY_STATIC_SEARCH, Model, multi_workload, search_workload, workload
+    from paper_2504_14966_amd.workloads import (POLICY_STATIC, POLICY_STATIC_SEARCH, Model, multi_workload,
+                                                search_workload, workload)
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     sl.load_library()
@@ -421,6 +422,44 @@ def main():
                                            one_after_another_ms=ms_seq)
         log(f"[bench] {Wm.name}: {ci / (ms_one * 1e-3):.4g} chain-iters/s in one launch ({ms_one:.1f} ms, "
             f"assignment included); instances one after another {ms_seq:.1f} ms")
+        # the paper's multi-instance setting in model space: the same 10 requests replicated on
+        # each of I instances (max batch 4), the paper's schedule (G, T0 500 cooled by 0.95 to
+        # 20, 100 proposals per level, early exit), 1024 chains per instance; all instances in
+        # one launch against one sched_anneal per instance
+        from paper_2504_14966_amd.workloads import Queue, two_class_queue
+        q10 = two_class_queue(10, 0)
+        m10 = Model(4, POLICY_STATIC, 2000, 40, 8000, 300, 2)
+        lv10 = sl.sched_levels(500.0, 20.0, 0.95)
+        s10 = sl.Search(sl.OBJ_RATIO, 100, 1)
+        rep = {}
+        for I in (1, 2, 4, 8):
+            qI = Queue(np.tile(q10.in_len, I), np.tile(q10.out_len, I), np.tile(q10.kind, I), np.tile(q10.thr_us, I))
+            dqI = sl.DeviceQueue.from_queue(qI)
+            instI = torch.tensor(np.repeat(np.arange(I, dtype=np.int32), 10), device="cuda")
+            mwsI = sl.sched_anneal_multi(dqI, m10, instI, I, 1024, 100 * lv10, 500.0, 0.95, 0, search=s10)
+            torch.cuda.synchronize()
+            a.record()
+            sl.sched_anneal_multi(dqI, m10, instI, I, 1024, 100 * lv10, 500.0, 0.95, 0, search=s10, mws=mwsI)
+            sl.sched_multi_best(mwsI)
+            b.record()
+            torch.cuda.synchronize()
+            ms1 = a.elapsed_time(b)
+            d10 = sl.DeviceQueue.from_queue(q10)
+            w10 = sl.alloc_ws(10, 1024)
+            sl.sched_anneal(d10, m10, 1024, 100 * lv10, 500.0, 0.95, 0, ws=w10, search=s10)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(I):
+                sl.sched_anneal(d10, m10, 1024, 100 * lv10, 500.0, 0.95, 0, ws=w10, search=s10)
+                sl.sched_best(w10, 10)
+            b.record()
+            torch.cuda.synchronize()
+            rep[I] = dict(one_launch_ms=ms1, one_after_another_ms=a.elapsed_time(b))
+        extras["multi_replicated_n10_b4_paper_schedule"] = dict(chains_per_instance=1024, iters=100 * lv10,
+                                                                 by_instances=rep)
+        log("[bench] 10 requests replicated on 1/2/4/8 instances, paper schedule: one launch " +
+            "/".join(f"{rep[I]['one_launch_ms']:.2f}" for I in rep) + " ms; one after another " +
+            "/".join(f"{rep[I]['one_after_another_ms']:.2f}" for I in rep) + " ms")
         # the fitted model taken literally (Table 2 in units of 10 ns) on 256 chat / code
         # requests with the paper's SLOs (code: e2e 30 s; chat: TTFT 10 s and TPOT 50 ms),
         # batch sizes searched (max 16), 2048 chains x 2000 proposals

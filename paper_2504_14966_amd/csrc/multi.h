@@ -21,6 +21,7 @@
 // out for the instance's request count (so the single-queue readouts work on it), followed
 // by the instance's queue (structure of arrays) and the global ids of its requests.
 #pragma once
+#include "anneal_reg.h"
 #include "anneal_static.h"
 #include "anneal_wave.h"
 #include "kernels.h"
@@ -280,6 +281,27 @@ __global__ void __launch_bounds__(1024) multi_static_kernel(DevModel m, StaticPa
   else
     anneal_static_body<LG, OBJ>(mk, sp, req, wb, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr,
                                 srch, slot);
+}
+
+// Static admission on instances of at most 64 requests and batches of 1, 2, 4, 8 or 16: the
+// register kernel's chain body per instance (block k / groups), no LDS.
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(256) multi_reg_kernel(DevModel m, int n, int instances, int chains, int groups,
+                                                         int iters, double T0, double alpha, uint32_t key0,
+                                                         uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                         unsigned char *mws) {
+  const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
+  const int nk = slot_n(mws, k);
+  if (nk == 0) return;
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform(g * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  unsigned char *slot = mws + mws_off_slot(n, instances, chains, k);
+  const SlotQueue sq = slot_queue(slot, n, chains);
+  DevModel mk = m;
+  mk.n = nk;
+  anneal_reg_body<LG, OBJ>(mk, QueuePtrs{sq.in_len, sq.out_len, sq.kind, sq.thr}, chains, chain,
+                           (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1, swap_thr, srch, slot);
 }
 
 // One workgroup per instance: its winner over chains.

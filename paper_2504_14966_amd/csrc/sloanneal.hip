@@ -781,6 +781,32 @@ int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, c
   sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(dm, n, instances, chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
   bool done = nk_max == 0;
+  if (!done && model->policy == SCHED_STATIC && sa::reg_kernel_fits(nk_max, model->max_batch) &&
+      static_narrow(h, model, n)) {
+    // every instance small: the register kernel per instance, no LDS
+    const int total = instances * chains, cus = std::max(1, cu_count());
+    const int waves = total >= 4 * cus && chains >= 4 ? 4 : (total >= 2 * cus && chains >= 2 ? 2 : 1);
+    const int groups = (chains + waves - 1) / waves, grid = instances * groups;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    const uint64_t st = model->swap_threshold;
+#define SA_MULTI_REG(LG)                                                                                         \
+  if (srch.objective)                                                                                          \
+    sa::multi_reg_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dm, n, instances, chains, groups, iters, T0,     \
+                                                                 alpha, k0, k1, st, srch, w);                  \
+  else                                                                                                         \
+    sa::multi_reg_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dm, n, instances, chains, groups, iters, T0,     \
+                                                                 alpha, k0, k1, st, srch, w);
+    switch (model->max_batch) {
+      case 1: SA_MULTI_REG(0) break;
+      case 2: SA_MULTI_REG(1) break;
+      case 4: SA_MULTI_REG(2) break;
+      case 8: SA_MULTI_REG(3) break;
+      default: SA_MULTI_REG(4) break;
+    }
+#undef SA_MULTI_REG
+    HIP_TRY(hipGetLastError());
+    done = true;
+  }
   if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     // every instance's queue is part of the whole one, so the delta kernel's widths hold
     const int total = instances * chains;

@@ -162,6 +162,17 @@ def test_anneal_multi_static_wide(sl, orc):
     _check_instances(sl, orc, q, m, inst, 4, 12, 300, 1.0, 0.99, 7, None, range(0, 12, 4))
 
 
+@pytest.mark.parametrize("B,search", [(1, None), (4, (1, 6, 0)), (16, None), (8, (1, 9, 1))])
+def test_anneal_multi_small_instances(sl, orc, B, search):
+    # every instance at most 64 requests: the register kernel per instance
+    rng = np.random.default_rng(70 + B)
+    q = random_queue(rng, 130, max_in=1500, max_out=40, thr_hi=900_000)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    inst = orc.assign(q, 4, [3000, 3000, 3000, 3000])
+    assert max(np.bincount(inst, minlength=4)) <= 64
+    _check_instances(sl, orc, q, m, inst, 4, 10, 300, 0.8, 0.99, 6, search, range(0, 10, 3))
+
+
 def test_multi_workload_sampled(sl, orc):
     W = multi_workload()
     I, cap = W.extra["instances"], W.extra["capacity"]
