@@ -171,7 +171,9 @@ __device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chain
       };
       cand = RegState{ins(cur.A), ins(cur.E), ins(cur.PF), ins(cur.T)};
     }
-    const Score s = reg_replay<LG>(cand, n, d0, d2, lane);
+    // a move inside one batch keeps every batch's members: the score is unchanged (and the
+    // move is kept under either objective), so the replay is skipped
+    const Score s = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay<LG>(cand, n, d0, d2, lane);
     const bool acc = obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3);
     if (acc) {
       cur = cand;
@@ -398,7 +400,9 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
         if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
         if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
       }
-      const Score sc = reg_replay_sized(cand, fc, n, d0, d2, lane);
+      // a swap inside one batch changes no batch's members: the score is unchanged
+      const bool same = mv.op == 2 && mask_begin(fm, mv.i) == mask_begin(fm, mv.j);
+      const Score sc = same ? Score{cn, ct} : reg_replay_sized(cand, fc, n, d0, d2, lane);
       if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
         cur = cand;
         fm = fc;
@@ -550,7 +554,10 @@ __device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const u
         if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
         if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
       }
-      const Score sc = reg_replay_fit(f, cand, fc, lane);
+      // a swap, or a fixed-layout insert, inside one batch keeps every member's batch size and
+      // every batch's duration: the score is unchanged
+      const bool same = mv.op >= 2 && mask_begin(fm, mv.i) == mask_begin(fm, mv.j);
+      const Score sc = same ? Score{cn, ct} : reg_replay_fit(f, cand, fc, lane);
       if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
         cur = cand;
         fm = fc;
