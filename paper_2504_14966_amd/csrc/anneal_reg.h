@@ -93,8 +93,10 @@ struct RegState {
   uint32_t PF, T;
 };
 
-// Full replay of the order held in registers: (met count, total latency).
-template <int LG>
+// Full replay of the order held in registers: (met count, total latency). T32: every time on
+// the timeline of any order fits 32 bits (the host's check), so the batch starts and the
+// latency sum run in 32-bit lanes.
+template <int LG, bool T32>
 __device__ __forceinline__ Score reg_replay(const RegState &s, int n, uint32_t d0, uint32_t d2, int lane) {
   constexpr int B = 1 << LG;
   const bool valid = lane < n;
@@ -103,16 +105,36 @@ __device__ __forceinline__ Score reg_replay(const RegState &s, int n, uint32_t d
   const uint32_t P = Seg<LG>::template all<OpAdd>(s.PF, lane);
   const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
   const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);
-  const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)D : 0ull;
-  const uint64_t S = scan_add64(contrib) - contrib;
-  const uint64_t ttft = S + P, e2e = S + F;
-  const bool met = valid && (kind == 0 ? ttft <= (uint64_t)s.T : (kind == 2 ? e2e <= (uint64_t)s.T : F - P <= s.T));
-  const int64_t nmet = __popcll(__ballot(met));
-  return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+  if constexpr (T32) {
+    // inclusive sum of the batch durations up to the lane's batch: D is the same on every
+    // lane of a batch, so the in-row shifts start at the batch size
+    uint32_t v = D;
+    if constexpr (LG <= 0) v += dpp_old<kDppRowShr1, 0xF>(0u, v);
+    if constexpr (LG <= 1) v += dpp_old<kDppRowShr2, 0xF>(0u, v);
+    if constexpr (LG <= 2) v += dpp_old<kDppRowShr4, 0xF>(0u, v);
+    if constexpr (LG <= 3) v += dpp_old<kDppRowShr8, 0xF>(0u, v);
+    v += dpp_old<kDppRowBcast15, 0xA>(0u, v);
+    v += dpp_old<kDppRowBcast31, 0xC>(0u, v);
+    const uint32_t S = v - D;
+    const uint32_t ttft = S + P, e2e = S + F;
+    const uint32_t x = kind == 0 ? ttft : (kind == 2 ? e2e : F - P);
+    const int64_t nmet = __popcll(__ballot(valid && x <= s.T));
+    // the latency sum: 16-bit halves of the 32-bit latencies, each sum below 2^22
+    uint32_t lo = valid ? (e2e & 0xFFFFu) : 0u, hi = valid ? (e2e >> 16) : 0u;
+    wave_all2<OpAdd, OpAdd>(lo, hi);
+    return Score{nmet, (uint64_t)lo + ((uint64_t)hi << 16)};
+  } else {
+    const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)D : 0ull;
+    const uint64_t S = scan_add64(contrib) - contrib;
+    const uint64_t ttft = S + P, e2e = S + F;
+    const bool met = valid && (kind == 0 ? ttft <= (uint64_t)s.T : (kind == 2 ? e2e <= (uint64_t)s.T : F - P <= s.T));
+    const int64_t nmet = __popcll(__ballot(met));
+    return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+  }
 }
 
 // One chain by one wave: record slot `chain`, Philox chain index `rng_chain`.
-template <int LG, int OBJ>
+template <int LG, int OBJ, bool T32>
 __device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chains, int chain, uint32_t rng_chain,
                                 int iters, double T0, double alpha, uint32_t key0, uint32_t key1, uint64_t swap_thr,
                                 const SearchParams &srch, unsigned char *ws) {
@@ -138,7 +160,7 @@ __device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chain
     cur.T = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : thr;
     gbest[lane] = (uint16_t)r;
   }
-  const Score s0 = reg_replay<LG>(cur, n, d0, d2, lane);
+  const Score s0 = reg_replay<LG, T32>(cur, n, d0, d2, lane);
   int64_t cn = s0.n;
   uint64_t ct = s0.t;
   int64_t bn = cn;
@@ -161,19 +183,23 @@ __device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chain
       };
       cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
     } else {
-      // insert: the request at i moves to j, the ones between shift by one toward i
+      // insert: the request at i moves to j, the ones between shift by one toward i (lanes
+      // [i, j) take x[lane + 1], or lanes (j, i] take x[lane - 1])
       const bool right = i < j;
-      const bool in_rng = right ? (lane >= i && lane < j) : (lane > j && lane <= i);
-      auto ins = [&](uint32_t x) {
-        const uint32_t xi = readlane(x, i);
-        const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);  // x[lane + 1] / x[lane - 1]
-        return wlane_m0(xi, j, in_rng ? sh : x);
-      };
-      cand = RegState{ins(cur.A), ins(cur.E), ins(cur.PF), ins(cur.T)};
+      const int lo = right ? i : j + 1;
+      const uint32_t span = (uint32_t)(right ? j - i : i - j);
+      const bool in_rng = (uint32_t)(lane - lo) < span;
+      auto ins = [&](uint32_t x, uint32_t sh) { return wlane_m0(readlane(x, i), j, in_rng ? sh : x); };
+      if (right)
+        cand = RegState{ins(cur.A, dppv<0x130>(cur.A)), ins(cur.E, dppv<0x130>(cur.E)),
+                        ins(cur.PF, dppv<0x130>(cur.PF)), ins(cur.T, dppv<0x130>(cur.T))};
+      else
+        cand = RegState{ins(cur.A, dppv<0x138>(cur.A)), ins(cur.E, dppv<0x138>(cur.E)),
+                        ins(cur.PF, dppv<0x138>(cur.PF)), ins(cur.T, dppv<0x138>(cur.T))};
     }
     // a move inside one batch keeps every batch's members: the score is unchanged (and the
     // move is kept under either objective), so the replay is skipped
-    const Score s = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay<LG>(cand, n, d0, d2, lane);
+    const Score s = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay<LG, T32>(cand, n, d0, d2, lane);
     const bool acc = obj_accept<OBJ>(cn, ct, s.n - cn, (int64_t)(s.t - ct), t_ref, cool.T, w3);
     if (acc) {
       cur = cand;
@@ -214,7 +240,12 @@ __global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
-  anneal_reg_body<LG, OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+  if (m.flags & kFlagTime32)
+    anneal_reg_body<LG, OBJ, true>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                                   ws);
+  else
+    anneal_reg_body<LG, OBJ, false>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
+                                    ws);
 }
 
 // ---- the joint order / batch-size search on small queues, state in registers ----

@@ -56,6 +56,7 @@ constexpr int kFlagListSched = 2;      // continuous list scheduling: keys and p
 constexpr int kFlagNarrowTime = 4;     // list scheduling: every time on the timeline fits 32 bits
 constexpr int kFlagWindows = 8;        // explicit batches: every time below 2^57 (windowed replay)
 constexpr int kFlagStaticNarrow = 16;  // static batches of any layout: 24-bit pair costs, 32-bit offsets
+constexpr int kFlagTime32 = 32;        // static batches of any layout: every time on the timeline fits 32 bits
 constexpr uint64_t kWsMagic = 0x534c4f414e4e3031ull;  // "SLOANN01"
 
 __host__ __device__ __forceinline__ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

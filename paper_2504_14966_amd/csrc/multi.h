@@ -300,8 +300,13 @@ __global__ void __launch_bounds__(256) multi_reg_kernel(DevModel m, int n, int i
   const SlotQueue sq = slot_queue(slot, n, chains);
   DevModel mk = m;
   mk.n = nk;
-  anneal_reg_body<LG, OBJ>(mk, QueuePtrs{sq.in_len, sq.out_len, sq.kind, sq.thr}, chains, chain,
-                           (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1, swap_thr, srch, slot);
+  const QueuePtrs qk{sq.in_len, sq.out_len, sq.kind, sq.thr};
+  if (m.flags & kFlagTime32)
+    anneal_reg_body<LG, OBJ, true>(mk, qk, chains, chain, (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1,
+                                   swap_thr, srch, slot);
+  else
+    anneal_reg_body<LG, OBJ, false>(mk, qk, chains, chain, (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1,
+                                    swap_thr, srch, slot);
 }
 
 // One workgroup per instance: its winner over chains.

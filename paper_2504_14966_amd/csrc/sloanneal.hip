@@ -372,12 +372,14 @@ int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevM
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     const sa::QueuePtrs qp = dev_queue(queue);
     const uint64_t st = model->swap_threshold;
+    sa::DevModel dr = dm;  // every time in 32 bits: the 32-bit start scan and latency sum
+    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
     switch (model->max_batch) {
-      case 1: sa::anneal_reg_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 2: sa::anneal_reg_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 4: sa::anneal_reg_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 8: sa::anneal_reg_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      default: sa::anneal_reg_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dm, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 1: sa::anneal_reg_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 2: sa::anneal_reg_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 4: sa::anneal_reg_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 8: sa::anneal_reg_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      default: sa::anneal_reg_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
     }
     HIP_TRY(hipGetLastError());
     done = true;
@@ -789,12 +791,15 @@ int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, c
     const int groups = (chains + waves - 1) / waves, grid = instances * groups;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     const uint64_t st = model->swap_threshold;
+    // every instance's timeline is within the whole queue's bound
+    sa::DevModel dr = dm;
+    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
 #define SA_MULTI_REG(LG)                                                                                         \
   if (srch.objective)                                                                                          \
-    sa::multi_reg_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dm, n, instances, chains, groups, iters, T0,     \
+    sa::multi_reg_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,     \
                                                                  alpha, k0, k1, st, srch, w);                  \
   else                                                                                                         \
-    sa::multi_reg_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dm, n, instances, chains, groups, iters, T0,     \
+    sa::multi_reg_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,     \
                                                                  alpha, k0, k1, st, srch, w);
     switch (model->max_batch) {
       case 1: SA_MULTI_REG(0) break;

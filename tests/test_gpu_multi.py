@@ -173,6 +173,15 @@ def test_anneal_multi_small_instances(sl, orc, B, search):
     _check_instances(sl, orc, q, m, inst, 4, 10, 300, 0.8, 0.99, 6, search, range(0, 10, 3))
 
 
+def test_anneal_multi_small_instances_wide_timeline(sl, orc):
+    # register kernel per instance with the timeline above 2^32 (64-bit starts and sums)
+    rng = np.random.default_rng(77)
+    q = random_queue(rng, 100, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    m = Model(16, 0, p0=5_000_000, p1=100, d0=16_000_000, d1=1000, d2=3)
+    inst = (np.arange(q.n) % 3).astype(np.int32)
+    _check_instances(sl, orc, q, m, inst, 3, 8, 200, 2.0, 0.99, 4, None, range(0, 8, 3))
+
+
 def test_multi_workload_sampled(sl, orc):
     W = multi_workload()
     I, cap = W.extra["instances"], W.extra["capacity"]

@@ -61,6 +61,32 @@ def test_reg_kernel_shapes_and_moves(sl, orc, n, B, thr):
     _run_check(sl, orc, q, m, 6, 400, 0.8, 0.995, 11)
 
 
+def _static_narrow(q, m):
+    # the fixed-size widths: every finish offset and doubled pair cost in 32 bits, 24-bit factors
+    lmax, Lmax, b = int(q.in_len.max()), int(q.out_len.max()), min(q.n, m.max_batch)
+    pf = m.p0 + m.p1 * lmax
+    fmax = b * pf + Lmax * m.d0 + b * (m.d1 * Lmax + m.d2 * (lmax * Lmax + Lmax * (Lmax + 1) // 2))
+    inner = 2 * (m.d1 + m.d2 * lmax) + m.d2 + m.d2 * Lmax
+    return fmax < 2**32 - 1 and inner < 2**24 and m.d2 < 2**24 and b * Lmax * inner < 2**32 and m.d0 < 2**24
+
+
+def _timeline_end(q, m):
+    # the end of the timeline of any order and layout
+    li, lo = q.in_len.astype(object), q.out_len.astype(object)
+    return sum(m.p0 + m.p1 * li) + (m.d0 + m.d1) * sum(lo) + m.d2 * sum(lo * li + lo * (lo + 1) // 2)
+
+
+@pytest.mark.parametrize("B,search", [(1, None), (16, None), (4, (1, 6, 1)), (8, (0, 4, 0))])
+def test_reg_kernel_wide_timeline(sl, orc, B, search):
+    # per-batch offsets within 32 bits but the whole timeline above 2^32: the batch starts
+    # and the latency sum in 64 bits
+    rng = np.random.default_rng(900 + B)
+    q = random_queue(rng, 64, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    m = Model(B, 0, p0=5_000_000, p1=100, d0=16_000_000, d1=1000, d2=3)
+    assert _static_narrow(q, m) and _timeline_end(q, m) > 2**32
+    _run_check(sl, orc, q, m, 6, 300, 2.0, 0.99, 21, search)
+
+
 @pytest.mark.parametrize("B,search", [(8, (1, 20, 0)), (16, (1, 7, 1)), (4, (0, 5, 0)), (2, (1, 3, 1))])
 def test_reg_kernel_objectives(sl, orc, B, search):
     rng = np.random.default_rng(200 + B)
