@@ -310,23 +310,26 @@ __device__ __forceinline__ RegMove reg_plan(uint64_t fm, int n, int B, int op, i
   return mv;
 }
 
+// v in the lanes of mask, 0 elsewhere, as one v_cndmask (a select the compiler cannot turn
+// into a branch around the instruction that produced v)
+__device__ __forceinline__ uint32_t keep_lanes(uint32_t v, uint64_t mask) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(v), "s"(mask));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t bperm(uint32_t v, int src) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)v);
 }
 
-// Full replay of the order in registers with the layout fm: (met count, total latency).
-__device__ __forceinline__ Score reg_replay_sized(const RegState &s, uint64_t fm, int n, uint32_t d0, uint32_t d2,
-                                                  int lane) {
+// Full replay of the order in registers with the batches given per lane by their first and
+// last positions b0 <= lane <= b1 (lanes at or above n: b0 = b1 = lane), every batch at most
+// maxb long: (met count, total latency).
+__device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int b1, int maxb, int n, uint32_t d0,
+                                                  uint32_t d2, int lane) {
   const bool valid = lane < n;
   const uint32_t L = s.A & 0xFFFFu, e = s.E & 0x3FFFFFFFu, kind = s.E >> 30;
-  const int b0 = valid ? mask_begin(fm, lane) : lane;
-  const int b1 = valid ? mask_end(fm, n, lane) - 1 : lane;
   const int bl = b1 - b0 + 1;
-  // the largest batch (lane 63 holds the wave maximum after the six steps)
-  uint32_t mb = (uint32_t)bl;
-#pragma unroll
-  for (int st = 0; st < 6; ++st) mb = dpp_step<OpMax>(mb, st);
-  const int maxb = (int)readlane(mb, 63);
   // batch prefill from one add-scan: the inclusive sum at the batch's last lane minus the
   // exclusive sum at its first lane (both gathers unconditional: ds_bpermute reads only
   // lanes that execute it)
@@ -351,8 +354,19 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, uint64_t fm
     }
   }
   const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
-  const uint64_t D64 = scan_max64(valid ? ((uint64_t)b0 << 32) | F : 0ull);
-  const uint32_t contrib = (valid && lane == b1) ? (uint32_t)D64 : 0u;
+  // the batch duration at its last lane, by a max-scan confined to batches. Every DPP step
+  // runs on the whole wave (a lane left out would read as 0 to its neighbour): in the row
+  // shifts the sending lane zeroes its value unless its batch reaches the receiver; in the
+  // row broadcasts (one sender, many receivers) the receiver keeps the value only when its
+  // batch starts at or below the sending lane (15 or 47, then 31).
+  uint32_t D = F;
+  D = max(D, dpp_old<kDppRowShr1, 0xF>(0u, b1 >= lane + 1 ? D : 0u));
+  D = max(D, dpp_old<kDppRowShr2, 0xF>(0u, b1 >= lane + 2 ? D : 0u));
+  D = max(D, dpp_old<kDppRowShr4, 0xF>(0u, b1 >= lane + 4 ? D : 0u));
+  D = max(D, dpp_old<kDppRowShr8, 0xF>(0u, b1 >= lane + 8 ? D : 0u));
+  D = max(D, keep_lanes(dpp_old<kDppRowBcast15, 0xA>(0u, D), __ballot(b0 <= (lane | 15) - 16)));
+  D = max(D, keep_lanes(dpp_old<kDppRowBcast31, 0xC>(0u, D), __ballot(b0 <= 31)));
+  const uint32_t contrib = (valid && lane == b1) ? D : 0u;
   const uint32_t S = scan_add32(contrib) - contrib;
   const uint32_t ttft = S + P, e2e = S + F;
   const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : F - P <= s.T));
@@ -394,7 +408,15 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
     gbest[lane] = (uint16_t)r;
     gbest_f[lane] = first ? 1 : 0;
   }
-  const Score s0 = reg_replay_sized(cur, fm, n, d0, d2, lane);
+  // each lane's batch bounds under the current layout (kept: swaps leave them unchanged)
+  const int maxb = min(B, n);
+  auto bounds = [&](uint64_t f, int &b0, int &b1) {
+    b0 = lane < n ? mask_begin(f, lane) : lane;
+    b1 = lane < n ? mask_end(f, n, lane) - 1 : lane;
+  };
+  int cb0, cb1;
+  bounds(fm, cb0, cb1);
+  const Score s0 = reg_replay_sized(cur, cb0, cb1, maxb, n, d0, d2, lane);
   int64_t cn = s0.n;
   uint64_t ct = s0.t;
   int64_t bn = cn;
@@ -411,6 +433,7 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
     if (mv.made) {
       RegState cand;
       uint64_t fc = fm;
+      int nb0 = cb0, nb1 = cb1;
       if (mv.op == 2) {
         const int i = mv.i, j = mv.j;
         auto sw = [&](uint32_t x) {
@@ -419,24 +442,31 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
         };
         cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
       } else {
+        // lanes [i, to) take x[lane + 1], or lanes (to, i] take x[lane - 1]
         const int i = mv.i, to = mv.to;
         const bool right = i < to;
-        const bool in_rng = right ? (lane >= i && lane < to) : (lane > to && lane <= i);
-        auto ins = [&](uint32_t x) {
-          const uint32_t xi = readlane(x, i);
-          const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);
-          return wlane_m0(xi, to, in_rng ? sh : x);
-        };
-        cand = RegState{ins(cur.A), ins(cur.E), ins(cur.PF), ins(cur.T)};
+        const int lo = right ? i : to + 1;
+        const uint32_t span = (uint32_t)(right ? to - i : i - to);
+        const bool in_rng = (uint32_t)(lane - lo) < span;
+        auto ins = [&](uint32_t x, uint32_t sh) { return wlane_m0(readlane(x, i), to, in_rng ? sh : x); };
+        if (right)
+          cand = RegState{ins(cur.A, dppv<0x130>(cur.A)), ins(cur.E, dppv<0x130>(cur.E)),
+                          ins(cur.PF, dppv<0x130>(cur.PF)), ins(cur.T, dppv<0x130>(cur.T))};
+        else
+          cand = RegState{ins(cur.A, dppv<0x138>(cur.A)), ins(cur.E, dppv<0x138>(cur.E)),
+                          ins(cur.PF, dppv<0x138>(cur.PF)), ins(cur.T, dppv<0x138>(cur.T))};
         if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
         if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
+        bounds(fc, nb0, nb1);
       }
       // a swap inside one batch changes no batch's members: the score is unchanged
       const bool same = mv.op == 2 && mask_begin(fm, mv.i) == mask_begin(fm, mv.j);
-      const Score sc = same ? Score{cn, ct} : reg_replay_sized(cand, fc, n, d0, d2, lane);
+      const Score sc = same ? Score{cn, ct} : reg_replay_sized(cand, nb0, nb1, maxb, n, d0, d2, lane);
       if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
         cur = cand;
         fm = fc;
+        cb0 = nb0;
+        cb1 = nb1;
         cn = sc.n;
         ct = sc.t;
         ++accepts;
