@@ -322,44 +322,54 @@ __device__ __forceinline__ uint32_t bperm(uint32_t v, int src) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)v);
 }
 
+// Pair terms of W consecutive members of the lane's batch from offset d: all 2W ds_bpermute
+// are in flight before their results are used.
+template <int W>
+__device__ __forceinline__ uint32_t pair_round(uint32_t L, uint32_t e, uint32_t d2, int b0, int bl, int d,
+                                               uint32_t acc) {
+  uint32_t Lj[W], ej[W];
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
+    const int src = min(b0 + d + u, kWave - 1);
+    Lj[u] = bperm(L, src);
+    ej[u] = bperm(e, src);
+  }
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
+    const uint32_t mu = min(Lj[u], L);
+    const uint32_t w = mad24_v(mu, mad24_v(d2, mu, ej[u]), 0u);
+    acc += d + u < bl ? w : 0u;
+  }
+  return acc;
+}
+
 // Full replay of the order in registers with the batches given per lane by their first and
 // last positions b0 <= lane <= b1 (lanes at or above n: b0 = b1 = lane), every batch at most
-// maxb long: (met count, total latency).
+// maxb long: (met count, total latency). A member's TTFT is the sum of the prefills of every
+// position up to its batch's end plus the decode durations of the earlier batches; its e2e
+// adds its own decode time G after the batch prefill.
 __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int b1, int maxb, int n, uint32_t d0,
                                                   uint32_t d2, int lane) {
   const bool valid = lane < n;
   const uint32_t L = s.A & 0xFFFFu, e = s.E & 0x3FFFFFFFu, kind = s.E >> 30;
   const int bl = b1 - b0 + 1;
-  // batch prefill from one add-scan: the inclusive sum at the batch's last lane minus the
-  // exclusive sum at its first lane (both gathers unconditional: ds_bpermute reads only
-  // lanes that execute it)
-  const uint32_t pinc = scan_add32(s.PF), pexc = pinc - s.PF;
-  const uint32_t P = bperm(pinc, b1) - bperm(pexc, b0);
-  // pair terms: the batch's members gathered eight offsets at a time, so that eight pairs
-  // of ds_bpermute are in flight before their results are used
+  // prefills up to the batch's end: one add-scan read at the batch's last lane (the gather
+  // is unconditional: ds_bpermute reads only lanes that execute it)
+  const uint32_t pend = bperm(scan_add32(s.PF), b1);
+  // pair terms: one round of gathers for batches of up to 8 (16 per round above)
   uint32_t acc = 0;
-  for (int d = 0; d < maxb; d += 8) {
-    uint32_t Lj[8], ej[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int src = min(b0 + d + u, kWave - 1);
-      Lj[u] = bperm(L, src);
-      ej[u] = bperm(e, src);
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const uint32_t mu = min(Lj[u], L);
-      const uint32_t w = mad24_v(mu, mad24_v(d2, mu, ej[u]), 0u);
-      acc += d + u < bl ? w : 0u;
-    }
+  if (maxb <= 8) {
+    acc = pair_round<8>(L, e, d2, b0, bl, 0, 0u);
+  } else {
+    for (int d = 0; d < maxb; d += 16) acc = pair_round<16>(L, e, d2, b0, bl, d, acc);
   }
-  const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
-  // the batch duration at its last lane, by a max-scan confined to batches. Every DPP step
-  // runs on the whole wave (a lane left out would read as 0 to its neighbour): in the row
-  // shifts the sending lane zeroes its value unless its batch reaches the receiver; in the
-  // row broadcasts (one sender, many receivers) the receiver keeps the value only when its
-  // batch starts at or below the sending lane (15 or 47, then 31).
-  uint32_t D = F;
+  const uint32_t G = valid ? __umul24(L, d0) + (acc >> 1) : 0u;
+  // the batch's decode duration at its last lane, by a max-scan confined to batches. Every
+  // DPP step runs on the whole wave (a lane left out would read as 0 to its neighbour): in
+  // the row shifts the sending lane zeroes its value unless its batch reaches the receiver;
+  // in the row broadcasts (one sender, many receivers) the receiver keeps the value only
+  // when its batch starts at or below the sending lane (15 or 47, then 31).
+  uint32_t D = G;
   D = max(D, dpp_old<kDppRowShr1, 0xF>(0u, b1 >= lane + 1 ? D : 0u));
   D = max(D, dpp_old<kDppRowShr2, 0xF>(0u, b1 >= lane + 2 ? D : 0u));
   D = max(D, dpp_old<kDppRowShr4, 0xF>(0u, b1 >= lane + 4 ? D : 0u));
@@ -367,9 +377,8 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int
   D = max(D, keep_lanes(dpp_old<kDppRowBcast15, 0xA>(0u, D), __ballot(b0 <= (lane | 15) - 16)));
   D = max(D, keep_lanes(dpp_old<kDppRowBcast31, 0xC>(0u, D), __ballot(b0 <= 31)));
   const uint32_t contrib = (valid && lane == b1) ? D : 0u;
-  const uint32_t S = scan_add32(contrib) - contrib;
-  const uint32_t ttft = S + P, e2e = S + F;
-  const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : F - P <= s.T));
+  const uint32_t ttft = pend + scan_add32(contrib) - contrib, e2e = ttft + G;
+  const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : G <= s.T));
   const int64_t nmet = __popcll(__ballot(met));
   // the latency sum: 16-bit halves of the 32-bit latencies, each sum below 2^22
   uint32_t lo = valid ? (e2e & 0xFFFFu) : 0u, hi = valid ? (e2e >> 16) : 0u;
