@@ -318,6 +318,35 @@ __device__ __forceinline__ uint32_t keep_lanes(uint32_t v, uint64_t mask) {
   return r;
 }
 
+__device__ __forceinline__ uint32_t add_sat(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
+
+// Inclusive scan over the 64 lanes with additions that saturate at 2^32 - 1: every value is
+// nonnegative, so each lane gets min(its true prefix sum, 2^32 - 1) whatever the order.
+__device__ __forceinline__ uint32_t scan_add_sat32(uint32_t v) {
+  v = add_sat(v, dpp_old<kDppRowShr1, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr2, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr4, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr8, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowBcast15, 0xA>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowBcast31, 0xC>(0u, v));
+  return v;
+}
+
+// Maximum of v over the lane's batch [b0, b1], exact at the batch's last lane b1: a max-scan
+// confined to batches. Every DPP step runs on the whole wave (a lane left out would read as 0
+// to its neighbour): in the row shifts the sending lane zeroes its value unless its batch
+// reaches the receiver; in the row broadcasts (one sender, many receivers) the receiver keeps
+// the value only when its batch starts at or below the sending lane (15 or 47, then 31).
+__device__ __forceinline__ uint32_t seg_max32(uint32_t v, int b0, int b1, int lane) {
+  v = max(v, dpp_old<kDppRowShr1, 0xF>(0u, b1 >= lane + 1 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr2, 0xF>(0u, b1 >= lane + 2 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr4, 0xF>(0u, b1 >= lane + 4 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr8, 0xF>(0u, b1 >= lane + 8 ? v : 0u));
+  v = max(v, keep_lanes(dpp_old<kDppRowBcast15, 0xA>(0u, v), __ballot(b0 <= (lane | 15) - 16)));
+  v = max(v, keep_lanes(dpp_old<kDppRowBcast31, 0xC>(0u, v), __ballot(b0 <= 31)));
+  return v;
+}
+
 __device__ __forceinline__ uint32_t bperm(uint32_t v, int src) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute(src << 2, (int)v);
 }
@@ -364,18 +393,8 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int
     for (int d = 0; d < maxb; d += 16) acc = pair_round<16>(L, e, d2, b0, bl, d, acc);
   }
   const uint32_t G = valid ? __umul24(L, d0) + (acc >> 1) : 0u;
-  // the batch's decode duration at its last lane, by a max-scan confined to batches. Every
-  // DPP step runs on the whole wave (a lane left out would read as 0 to its neighbour): in
-  // the row shifts the sending lane zeroes its value unless its batch reaches the receiver;
-  // in the row broadcasts (one sender, many receivers) the receiver keeps the value only
-  // when its batch starts at or below the sending lane (15 or 47, then 31).
-  uint32_t D = G;
-  D = max(D, dpp_old<kDppRowShr1, 0xF>(0u, b1 >= lane + 1 ? D : 0u));
-  D = max(D, dpp_old<kDppRowShr2, 0xF>(0u, b1 >= lane + 2 ? D : 0u));
-  D = max(D, dpp_old<kDppRowShr4, 0xF>(0u, b1 >= lane + 4 ? D : 0u));
-  D = max(D, dpp_old<kDppRowShr8, 0xF>(0u, b1 >= lane + 8 ? D : 0u));
-  D = max(D, keep_lanes(dpp_old<kDppRowBcast15, 0xA>(0u, D), __ballot(b0 <= (lane | 15) - 16)));
-  D = max(D, keep_lanes(dpp_old<kDppRowBcast31, 0xC>(0u, D), __ballot(b0 <= 31)));
+  // the batch's decode duration at its last lane
+  const uint32_t D = seg_max32(G, b0, b1, lane);
   const uint32_t contrib = (valid && lane == b1) ? D : 0u;
   const uint32_t ttft = pend + scan_add32(contrib) - contrib, e2e = ttft + G;
   const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : G <= s.T));
@@ -527,26 +546,59 @@ struct RegFit {
   uint32_t T, T2;
 };
 
+// M32: every member's time fits 32 bits (the host's check). The closed forms then run in
+// 32-bit arithmetic (exact: products wrap only inside ring expressions whose value fits), the
+// batch starts in a saturating 32-bit scan (a start that saturates can meet no threshold,
+// every threshold being below 2^32 - 1; T and T2 hold the thresholds of the decode-time
+// tests already multiplied by l_out, saturated), and the total latency exactly as the sum of
+// the member times plus each batch's duration times the number of requests after it.
+template <bool M32>
 __device__ __forceinline__ Score reg_replay_fit(const DevFit &f, const RegFit &s, uint64_t fm, int lane) {
   const int n = f.n;
   const bool valid = lane < n;
-  const uint64_t L = s.A & 0xFFFFu, l = s.LK & 0xFFFFu;
   const uint32_t kind = s.LK >> 16;
   const int b0 = valid ? mask_begin(fm, lane) : lane;
   const int b1 = valid ? mask_end(fm, n, lane) - 1 : lane;
-  const uint64_t b = (uint64_t)(b1 - b0 + 1);
-  const uint64_t tp = fit_prefill(f, b, l), td = fit_decode(f, b, l, L), E = tp + td;
-  constexpr uint64_t kTimeMask = (uint64_t(1) << 58) - 1;
-  const uint64_t D = scan_max64(valid ? ((uint64_t)b0 << 58) | E : 0ull) & kTimeMask;
-  const uint64_t contrib = (valid && lane == b1) ? D : 0ull;
-  const uint64_t S = scan_add64(contrib) - contrib;
-  const uint64_t ttft = S + tp, e2e = S + E;
-  const bool met = valid && fit_met(kind, s.T, s.T2, L, ttft, td, e2e);
-  const int64_t nmet = __popcll(__ballot(met));
-  return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+  if constexpr (M32) {
+    const uint32_t L = s.A & 0xFFFFu, l = s.LK & 0xFFFFu, b = (uint32_t)(b1 - b0 + 1);
+    const uint32_t tp = (uint32_t)f.ap * b * l + (uint32_t)f.bp * b + (uint32_t)f.cp * l + (uint32_t)f.dp;
+    const uint32_t td = L * ((uint32_t)f.bd * b + (uint32_t)f.dd) +
+                        ((uint32_t)f.ad * b + (uint32_t)f.cd) * (L * l + ((L * (L + 1u)) >> 1));
+    const uint32_t E = valid ? tp + td : 0u;
+    const uint32_t D = seg_max32(E, b0, b1, lane);
+    const bool last = valid && lane == b1;
+    const uint32_t contrib = last ? D : 0u;
+    // exclusive start: the inclusive scan of the contributions moved up one lane
+    const uint32_t S = scan_add_sat32((uint32_t)__builtin_amdgcn_update_dpp(0, (int)contrib, kDppWaveShr1, 0xF, 0xF,
+                                                                            false));
+    const uint32_t ttft = add_sat(S, tp), e2e = add_sat(S, E);
+    const bool met = valid && (kind == 0   ? ttft <= s.T
+                               : kind == 1 ? td <= s.T
+                               : kind == 2 ? e2e <= s.T
+                                           : (ttft <= s.T && td <= s.T2));
+    const int64_t nmet = __popcll(__ballot(met));
+    // sum of e2e = sum of E + sum over batches of D * (requests after the batch), in 16-bit
+    // halves (each lane below 2^22, each sum below 2^28)
+    const uint32_t after = last ? (uint32_t)(n - 1 - b1) : 0u;
+    uint32_t lo = (E & 0xFFFFu) + (contrib & 0xFFFFu) * after, hi = (E >> 16) + (contrib >> 16) * after;
+    wave_all2<OpAdd, OpAdd>(lo, hi);
+    return Score{nmet, (uint64_t)lo + ((uint64_t)hi << 16)};
+  } else {
+    const uint64_t L = s.A & 0xFFFFu, l = s.LK & 0xFFFFu;
+    const uint64_t b = (uint64_t)(b1 - b0 + 1);
+    const uint64_t tp = fit_prefill(f, b, l), td = fit_decode(f, b, l, L), E = tp + td;
+    constexpr uint64_t kTimeMask = (uint64_t(1) << 58) - 1;
+    const uint64_t D = scan_max64(valid ? ((uint64_t)b0 << 58) | E : 0ull) & kTimeMask;
+    const uint64_t contrib = (valid && lane == b1) ? D : 0ull;
+    const uint64_t S = scan_add64(contrib) - contrib;
+    const uint64_t ttft = S + tp, e2e = S + E;
+    const bool met = valid && fit_met(kind, s.T, s.T2, L, ttft, td, e2e);
+    const int64_t nmet = __popcll(__ballot(met));
+    return Score{nmet, wave_sum64_dpp(valid ? e2e : 0ull)};
+  }
 }
 
-template <int OBJ>
+template <int OBJ, bool M32>
 __device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const uint32_t *thr2, int chains, int chain,
                                     uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0,
                                     uint32_t key1, uint64_t swap_thr, const SearchParams &srch, unsigned char *ws) {
@@ -571,10 +623,16 @@ __device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const u
     cur.LK = (uint32_t)q.in_len[r] | ((uint32_t)q.kind[r] << 16);
     cur.T = q.thr[r];
     cur.T2 = thr2 ? thr2[r] : 0u;
+    if (M32) {
+      // thresholds of the decode-time tests, multiplied by l_out and saturated
+      const uint64_t L = q.out_len[r];
+      if (q.kind[r] == 1) cur.T = (uint32_t)min((uint64_t)cur.T * L, (uint64_t)0xFFFFFFFFu);
+      cur.T2 = (uint32_t)min((uint64_t)cur.T2 * L, (uint64_t)0xFFFFFFFFu);
+    }
     gbest[lane] = (uint16_t)r;
     gbest_f[lane] = first ? 1 : 0;
   }
-  const Score s0 = reg_replay_fit(f, cur, fm, lane);
+  const Score s0 = reg_replay_fit<M32>(f, cur, fm, lane);
   int64_t cn = s0.n;
   uint64_t ct = s0.t;
   int64_t bn = cn;
@@ -627,7 +685,7 @@ __device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const u
       // a swap, or a fixed-layout insert, inside one batch keeps every member's batch size and
       // every batch's duration: the score is unchanged
       const bool same = mv.op >= 2 && mask_begin(fm, mv.i) == mask_begin(fm, mv.j);
-      const Score sc = same ? Score{cn, ct} : reg_replay_fit(f, cand, fc, lane);
+      const Score sc = same ? Score{cn, ct} : reg_replay_fit<M32>(f, cand, fc, lane);
       if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
         cur = cand;
         fm = fc;
@@ -665,8 +723,12 @@ __global__ void __launch_bounds__(256) anneal_reg_fit_kernel(DevFit f, QueuePtrs
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
-  anneal_reg_fit_body<OBJ>(f, q, thr2, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch,
-                           ws);
+  if (f.m32)
+    anneal_reg_fit_body<OBJ, true>(f, q, thr2, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr,
+                                   srch, ws);
+  else
+    anneal_reg_fit_body<OBJ, false>(f, q, thr2, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr,
+                                    srch, ws);
 }
 
 }  // namespace sa

@@ -23,7 +23,8 @@ namespace sa {
 struct DevFit {
   int32_t n, B, policy, pad;
   uint64_t ap, bp, cp, dp, ad, bd, cd, dd;
-  uint32_t win, pad2;  // win = 1: every member's time is below 2^57 (the windowed replay's keys fit)
+  uint32_t win;  // 1: every member's time is below 2^57 (the windowed replay's keys fit)
+  uint32_t m32;  // 1: every member's time, in any batch, is below 2^32 - 1
   uint64_t bmagic;     // floor(2^32 / B) + 1: lane / B = (lane * bmagic) >> 32 for lanes below 64
 };
 

@@ -134,11 +134,25 @@ int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool 
   return SCHED_OK;
 }
 
-// win: the windowed replay's keys hold every member's time (below 2^57 with margin)
-sa::DevFit dev_fit(const sched_fit_model_t *f, int n, bool win) {
+// The largest time of one request in any batch (times grow with the batch size).
+long double fit_member_bound(const HostQueue &h, const sched_fit_model_t *f, int n) {
+  const long double b = std::min(n, f->max_batch);
+  long double mx = 0;
+  for (int r = 0; r < n; ++r) {
+    const long double l = h.in_len[r], L = h.out_len[r];
+    mx = std::max(mx, (long double)f->ap * b * l + (long double)f->bp * b + (long double)f->cp * l +
+                          (long double)f->dp + L * ((long double)f->bd * b + (long double)f->dd) +
+                          ((long double)f->ad * b + (long double)f->cd) * (L * l + L * (L + 1) / 2));
+  }
+  return mx;
+}
+
+// win: the windowed replay's keys hold every member's time (below 2^57 with margin);
+// m32: every member's time fits 32 bits
+sa::DevFit dev_fit(const sched_fit_model_t *f, int n, bool win, bool m32 = false) {
   return sa::DevFit{n, f->max_batch, f->policy, 0, (uint64_t)f->ap, (uint64_t)f->bp, (uint64_t)f->cp,
                     (uint64_t)f->dp, (uint64_t)f->ad, (uint64_t)f->bd, (uint64_t)f->cd, (uint64_t)f->dd,
-                    win ? 1u : 0u, 0u, (1ull << 32) / (uint64_t)f->max_batch + 1};
+                    win ? 1u : 0u, m32 ? 1u : 0u, (1ull << 32) / (uint64_t)f->max_batch + 1};
 }
 
 // The ratio objective compares n1 t2 with n2 t1 and forms n' t - n t' in int64: the
@@ -903,7 +917,8 @@ int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, c
   if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
   if ((rc = fit_range_check(h, fit, queue->n, srch.objective == SCHED_OBJ_RATIO))) return rc;
   const int n = queue->n;
-  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57));
+  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57),
+                                fit_member_bound(h, fit, n) < 4294967295.0L);
   unsigned char *w = static_cast<unsigned char *>(ws);
   sa::start_fit_kernel<<<1, 1024, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, fit->t_ref, srch, w);
   HIP_TRY(hipGetLastError());

@@ -136,14 +136,30 @@ def test_reg_search_objectives(sl, orc, n, B, search):
                                                (64, 16, 2, (1, 10, 1)), (30, 5, 0, (1, 6, 0)), (1, 4, 2, None)])
 def test_reg_fit(sl, orc, n, B, policy, search):
     # the fitted model (Table 2) with the chat SLO on small queues: order, fields and layout
-    # in registers
+    # in registers; every member's time below 2^32 (the 32-bit replay)
+    _reg_fit_check(sl, orc, n, B, policy, search, 1)
+
+
+@pytest.mark.parametrize("n,B,policy,search", [(20, 4, 0, None), (64, 16, 2, (1, 8, 0)), (37, 64, 2, None)])
+def test_reg_fit_wide_members(sl, orc, n, B, policy, search):
+    # coefficients 64 times Table 2's: member times above 2^32, the 64-bit replay
+    _reg_fit_check(sl, orc, n, B, policy, search, 64)
+
+
+def _reg_fit_check(sl, orc, n, B, policy, search, scale):
     import torch
     from paper_2504_14966_amd.workloads import TABLE2_10NS
     rng = np.random.default_rng(700 + n + B + policy)
     q = random_queue(rng, n, max_in=2000, max_out=300, thr_hi=2_000_000_000)
     q.kind[::3] = 3
-    thr2 = rng.integers(1_500_000, 1_800_000, n).astype(np.uint32)
-    fd, fo = sl.FitModel(B, policy, **TABLE2_10NS), orc.FitModel(B, policy, **TABLE2_10NS)
+    thr2 = rng.integers(1_500_000, 1_800_000, n).astype(np.uint32) * (1 if scale == 1 else 40)
+    coef = {k: v * scale for k, v in TABLE2_10NS.items()}
+    fd, fo = sl.FitModel(B, policy, **coef), orc.FitModel(B, policy, **coef)
+    big = max(int(coef["ap"]) * min(n, B) * int(a) + int(coef["bp"]) * min(n, B) + int(coef["cp"]) * int(a)
+              + int(coef["dp"]) + int(L) * (int(coef["bd"]) * min(n, B) + int(coef["dd"]))
+              + (int(coef["ad"]) * min(n, B) + int(coef["cd"])) * (int(L) * int(a) + int(L) * (int(L) + 1) // 2)
+              for a, L in zip(q.in_len, q.out_len))
+    assert (big < 2**32 - 1) == (scale == 1)
     dq = sl.DeviceQueue.from_queue(q)
     chains, iters = 6, 500
     ws = sl.sched_anneal_fit(dq, fd, chains, iters, 1.5, 0.98, 4, tpot_thr=sl.thr_to_device(thr2),
