@@ -376,7 +376,13 @@ __device__ __forceinline__ uint32_t pair_round(uint32_t L, uint32_t e, uint32_t 
 // last positions b0 <= lane <= b1 (lanes at or above n: b0 = b1 = lane), every batch at most
 // maxb long: (met count, total latency). A member's TTFT is the sum of the prefills of every
 // position up to its batch's end plus the decode durations of the earlier batches; its e2e
-// adds its own decode time G after the batch prefill.
+// adds its own decode time G after the batch prefill. Prefills, G and batch durations fit
+// 32 bits (the host's width checks); the timeline need not: its prefix sums saturate at
+// 2^32 - 1, which no threshold reaches, and the total latency is formed exactly as the sum of
+// G, of each prefill times the requests from its batch's start onward and of each batch's
+// decode duration times the requests after it.
+// SAT = false: the whole timeline fits 32 bits (the host's check) and plain 32-bit scans do.
+template <bool SAT>
 __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int b1, int maxb, int n, uint32_t d0,
                                                   uint32_t d2, int lane) {
   const bool valid = lane < n;
@@ -384,7 +390,7 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int
   const int bl = b1 - b0 + 1;
   // prefills up to the batch's end: one add-scan read at the batch's last lane (the gather
   // is unconditional: ds_bpermute reads only lanes that execute it)
-  const uint32_t pend = bperm(scan_add32(s.PF), b1);
+  const uint32_t pend = bperm(SAT ? scan_add_sat32(s.PF) : scan_add32(s.PF), b1);
   // pair terms: one round of gathers for batches of up to 8 (16 per round above)
   uint32_t acc = 0;
   if (maxb <= 8) {
@@ -395,17 +401,33 @@ __device__ __forceinline__ Score reg_replay_sized(const RegState &s, int b0, int
   const uint32_t G = valid ? __umul24(L, d0) + (acc >> 1) : 0u;
   // the batch's decode duration at its last lane
   const uint32_t D = seg_max32(G, b0, b1, lane);
-  const uint32_t contrib = (valid && lane == b1) ? D : 0u;
-  const uint32_t ttft = pend + scan_add32(contrib) - contrib, e2e = ttft + G;
+  const bool last = valid && lane == b1;
+  const uint32_t contrib = last ? D : 0u;
+  uint32_t ttft, e2e, lo, hi;
+  if constexpr (SAT) {
+    // decode durations of the earlier batches: the inclusive scan moved up one lane
+    const uint32_t SD =
+        scan_add_sat32((uint32_t)__builtin_amdgcn_update_dpp(0, (int)contrib, kDppWaveShr1, 0xF, 0xF, false));
+    ttft = add_sat(pend, SD);
+    e2e = add_sat(ttft, G);
+    // the latency sum in 16-bit halves (each lane below 2^23, each sum below 2^29)
+    const uint32_t from = valid ? (uint32_t)(n - b0) : 0u, after = last ? (uint32_t)(n - 1 - b1) : 0u;
+    lo = (G & 0xFFFFu) + (s.PF & 0xFFFFu) * from + (contrib & 0xFFFFu) * after;
+    hi = (G >> 16) + (s.PF >> 16) * from + (contrib >> 16) * after;
+  } else {
+    ttft = pend + scan_add32(contrib) - contrib;
+    e2e = ttft + G;
+    // the latency sum: 16-bit halves of the 32-bit latencies, each sum below 2^22
+    lo = valid ? (e2e & 0xFFFFu) : 0u;
+    hi = valid ? (e2e >> 16) : 0u;
+  }
   const bool met = valid && (kind == 0 ? ttft <= s.T : (kind == 2 ? e2e <= s.T : G <= s.T));
   const int64_t nmet = __popcll(__ballot(met));
-  // the latency sum: 16-bit halves of the 32-bit latencies, each sum below 2^22
-  uint32_t lo = valid ? (e2e & 0xFFFFu) : 0u, hi = valid ? (e2e >> 16) : 0u;
   wave_all2<OpAdd, OpAdd>(lo, hi);
   return Score{nmet, (uint64_t)lo + ((uint64_t)hi << 16)};
 }
 
-template <int OBJ>
+template <int OBJ, bool SAT>
 __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int chains, int chain,
                                       uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0,
                                       uint32_t key1, const SearchParams &srch, unsigned char *ws) {
@@ -444,7 +466,7 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
   };
   int cb0, cb1;
   bounds(fm, cb0, cb1);
-  const Score s0 = reg_replay_sized(cur, cb0, cb1, maxb, n, d0, d2, lane);
+  const Score s0 = reg_replay_sized<SAT>(cur, cb0, cb1, maxb, n, d0, d2, lane);
   int64_t cn = s0.n;
   uint64_t ct = s0.t;
   int64_t bn = cn;
@@ -489,7 +511,7 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
       }
       // a swap inside one batch changes no batch's members: the score is unchanged
       const bool same = mv.op == 2 && mask_begin(fm, mv.i) == mask_begin(fm, mv.j);
-      const Score sc = same ? Score{cn, ct} : reg_replay_sized(cand, nb0, nb1, maxb, n, d0, d2, lane);
+      const Score sc = same ? Score{cn, ct} : reg_replay_sized<SAT>(cand, nb0, nb1, maxb, n, d0, d2, lane);
       if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
         cur = cand;
         fm = fc;
@@ -528,7 +550,10 @@ __global__ void __launch_bounds__(256) anneal_reg_sized_kernel(DevModel m, Queue
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
-  anneal_reg_sized_body<OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, srch, ws);
+  if (m.flags & kFlagTime32)
+    anneal_reg_sized_body<OBJ, false>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, srch, ws);
+  else
+    anneal_reg_sized_body<OBJ, true>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, srch, ws);
 }
 
 // ---- the fitted latency model on small queues, state in registers ----

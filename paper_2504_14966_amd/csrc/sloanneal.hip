@@ -319,12 +319,14 @@ int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevMo
                  int chains, int iters, double T0, double alpha, uint64_t seed, const sa::SearchParams &srch,
                  unsigned char *w, hipStream_t stream) {
   const int n = dm.n;
-  if (sa::reg_sized_fits(n) && sized_narrow(h, model, n)) {
+  if (sa::reg_sized_fits(n) && static_narrow(h, model, n)) {
     // small queue: the order, every request field and the layout in registers, no LDS
     const int cus = std::max(1, cu_count());
     const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
     const int grid = (chains + waves - 1) / waves;
-    sa::anneal_reg_sized_kernel<OBJ><<<grid, waves * 64, 0, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
+    sa::DevModel dr = dm;  // the whole timeline in 32 bits: plain prefix sums
+    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
+    sa::anneal_reg_sized_kernel<OBJ><<<grid, waves * 64, 0, stream>>>(dr, dev_queue(queue), chains, iters, T0, alpha,
                                                                       (uint32_t)seed, (uint32_t)(seed >> 32), srch, w);
     HIP_TRY(hipGetLastError());
     return SCHED_OK;

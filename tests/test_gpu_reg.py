@@ -124,6 +124,17 @@ def test_reg_search_shapes(sl, orc, n, B):
     _search_check(sl, orc, q, m, 6, 500, 0.8, 0.995, 13)
 
 
+@pytest.mark.parametrize("n,B,search", [(64, 16, None), (50, 5, (1, 6, 1)), (64, 64, (0, 4, 0)), (33, 1, None)])
+def test_reg_search_wide_timeline(sl, orc, n, B, search):
+    # per-batch offsets within 32 bits, the whole timeline above 2^32: saturating prefix
+    # sums and the exact latency sum
+    rng = np.random.default_rng(950 + n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    m = Model(B, 2, p0=5_000_000, p1=100, d0=16_000_000 // max(1, B // 16), d1=1000, d2=3)
+    assert _static_narrow(q, m) and _timeline_end(q, m) > 2**32
+    _search_check(sl, orc, q, m, 6, 400, 2.0, 0.99, 23, search)
+
+
 @pytest.mark.parametrize("n,B,search", [(24, 6, (1, 10, 1)), (48, 16, (1, 25, 0)), (40, 3, (0, 4, 1))])
 def test_reg_search_objectives(sl, orc, n, B, search):
     rng = np.random.default_rng(600 + n + B)
