@@ -36,6 +36,7 @@
 // below 2^32 and the multiply-add operands below 2^24); starts, sums, objective are u64.
 #pragma once
 #include "device_common.h"
+#include "device_cont.h"
 #include "device_replay.h"
 #include "device_rng.h"
 
@@ -666,7 +667,10 @@ namespace sa {
 // 32-bit arithmetic as the annealing kernel: per batch the prefill sum, each member's
 // finish offset by the pairwise closed form (one 8-byte LDS read and three 24-bit ops
 // per pair), the batch duration, the start scan across batches and the SLO test.
-template <int LG, bool DETAIL>
+// T32: every time on the timeline fits 32 bits (the host's check; not with DETAIL): the batch
+// starts come from a 32-bit scan of the batch durations that begins at the batch size (the
+// duration is the same on every lane of a batch) and the latency sum from 16-bit halves.
+template <int LG, bool DETAIL, bool T32 = false>
 __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticParams sp, QueuePtrs q,
                                                            const uint16_t *__restrict__ perms, int64_t rows,
                                                            int64_t *__restrict__ out, int64_t *__restrict__ detail) {
@@ -724,6 +728,7 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
       continue;
     }
     uint64_t carry = 0, tl = 0;
+    uint32_t carry32 = 0, tlo = 0, thi = 0;
     int nmet = 0;
     for (int rr = 0; rr < R; ++rr) {
       const int k = rr * G + seg;
@@ -755,22 +760,48 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
       wave_sync_lds();
       const uint32_t F = valid ? P + __umul24(x.L, sp.d0) + (acc >> 1) : 0u;
       const uint32_t D = Seg<LG>::template all<OpMax>(F, lane);
-      int64_t excl, total;
-      Seg<LG>::scan(k < M ? (int64_t)D : 0, lane, excl, total);
-      const uint64_t S = carry + (uint64_t)excl;
       const Slack sl = slack_of(x.kind, x.thr, x.L, P, F);
-      const bool met = valid && slack_met(sl, S);
-      nmet += __popcll(__ballot(met));
-      if (valid) {
-        tl += S + F;
-        if (DETAIL) {
-          detail[row * n * 2 + 2 * r] = (int64_t)(S + P);
-          detail[row * n * 2 + 2 * r + 1] = (int64_t)(S + F);
+      if constexpr (T32) {
+        // inclusive sum of the durations of the round's batches up to the lane's (lanes past
+        // the last batch hold D = 0)
+        uint32_t v = D;
+        if constexpr (LG <= 0) v += dpp_old<kDppRowShr1, 0xF>(0u, v);
+        if constexpr (LG <= 1) v += dpp_old<kDppRowShr2, 0xF>(0u, v);
+        if constexpr (LG <= 2) v += dpp_old<kDppRowShr4, 0xF>(0u, v);
+        if constexpr (LG <= 3) v += dpp_old<kDppRowShr8, 0xF>(0u, v);
+        if constexpr (LG <= 4) v += dpp_old<kDppRowBcast15, 0xA>(0u, v);
+        if constexpr (LG <= 5) v += dpp_old<kDppRowBcast31, 0xC>(0u, v);
+        const uint32_t S = carry32 + v - D;
+        const bool met = valid && slack_met(sl, S);
+        nmet += __popcll(__ballot(met));
+        const uint32_t e2e = S + F;
+        tlo += valid ? (e2e & 0xFFFFu) : 0u;
+        thi += valid ? (e2e >> 16) : 0u;
+        carry32 += readlane(v, kWave - 1);
+      } else {
+        int64_t excl, total;
+        Seg<LG>::scan(k < M ? (int64_t)D : 0, lane, excl, total);
+        const uint64_t S = carry + (uint64_t)excl;
+        const bool met = valid && slack_met(sl, S);
+        nmet += __popcll(__ballot(met));
+        if (valid) {
+          tl += S + F;
+          if (DETAIL) {
+            detail[row * n * 2 + 2 * r] = (int64_t)(S + P);
+            detail[row * n * 2 + 2 * r + 1] = (int64_t)(S + F);
+          }
         }
+        carry += (uint64_t)total;
       }
-      carry += (uint64_t)total;
     }
-    const uint64_t t = wave_sum_u64(tl);
+    uint64_t t;
+    if constexpr (T32) {
+      // each lane's halves below 2^20 (at most 16 rounds), their wave sums below 2^26
+      Seg<6>::template all2<OpAdd, OpAdd>(tlo, thi, lane);
+      t = (uint64_t)tlo + ((uint64_t)thi << 16);
+    } else {
+      t = wave_sum_u64(tl);
+    }
     if (lane == 0) {
       out[2 * row] = nmet;
       out[2 * row + 1] = (int64_t)t;

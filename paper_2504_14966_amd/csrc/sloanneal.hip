@@ -569,11 +569,15 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
     const size_t lds = (size_t)(n + 1) * 16 + ((((size_t)n * 2 + 15) & ~size_t(15)) + 64 * 8 + 32 * 4) * 4;
     const int64_t want4 = (k + 3) / 4;
     const int g4 = (int)std::min<int64_t>(want4, 256 * 32);
+    const bool t32 = sized_narrow(h, model, n);  // the whole timeline in 32 bits
     hipError_t e = hipSuccess;
 #define SA_EVAL_CASE(L)                                                                                            \
   case L:                                                                                                        \
     if (detail)                                                                                                  \
       sa::eval_static_kernel<L, true><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, detail);  \
+    else if (t32)                                                                                                \
+      sa::eval_static_kernel<L, false, true><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out,     \
+                                                                       nullptr);                                 \
     else                                                                                                         \
       sa::eval_static_kernel<L, false><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, nullptr); \
     break;

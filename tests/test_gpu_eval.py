@@ -87,6 +87,35 @@ def test_random_queues_with_detail(sl, orc, n, B, policy):
         assert np.array_equal(det[r, :, 0], ttft) and np.array_equal(det[r, :, 1], e2e), (r, n, B, policy)
 
 
+def _timeline_end(q, m):
+    # the end of the timeline of any order under static batches
+    li, lo = q.in_len.astype(object), q.out_len.astype(object)
+    return sum(m.p0 + m.p1 * li) + (m.d0 + m.d1) * sum(lo) + m.d2 * sum(lo * li + lo * (lo + 1) // 2)
+
+
+@pytest.mark.parametrize("n,B,wide", [(1, 1, False), (7, 3, False), (33, 8, False), (64, 64, False),
+                                      (100, 33, False), (257, 64, False), (300, 1, False), (1024, 64, False),
+                                      (1024, 48, False), (64, 16, True), (130, 17, True), (64, 1, True),
+                                      (200, 5, True)])
+def test_static_rows_without_detail(sl, orc, n, B, wide):
+    # totals only: a timeline within 32 bits takes the 32-bit start scan and latency sum,
+    # a wider one the 64-bit path
+    rng = np.random.default_rng(77 * n + B)
+    if wide:
+        q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+        m = Model(B, 0, p0=5_000_000, p1=100, d0=16_000_000 // max(1, B // 16), d1=1000, d2=3)
+    else:
+        q = random_queue(rng, n, max_in=2048, max_out=200)
+        m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    assert (_timeline_end(q, m) >= 2**32 - 2) == wide
+    rows = 8 if n >= 512 else 24
+    perms = np.stack([rng.permutation(n) for _ in range(rows)]).astype(np.uint16)
+    out = _eval(sl, q, m, perms)
+    for r in range(rows):
+        nn, tt = orc.replay(q, m, perms[r])[:2]
+        assert out[r].tolist() == [nn, tt], (r, n, B)
+
+
 def test_non_permutation_rows(sl, orc):
     W = workload(2)
     n = W.queue.n
