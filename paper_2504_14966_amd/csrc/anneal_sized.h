@@ -230,9 +230,87 @@ __device__ Score replay_batches_windows(const DevModel &m, const uint4 *__restri
   return Score{nmet, wave_sum_u64(tl)};
 }
 
+// The same windows when the pair costs take the narrow widths and the whole timeline fits 32
+// bits (kFlagStaticNarrow and kFlagTime32): 32-bit offsets, durations by the 32-bit max-scan
+// confined to batches, starts by a 32-bit add-scan, the latency sum in 16-bit halves (each
+// lane's below 2^26 over at most 1024 windows).
+template <bool DETAIL>
+__device__ Score replay_batches_windows32(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
+                                          const uint8_t *flags, uint4 *stage, int64_t *detail) {
+  const int lane = lane_id();
+  const int n = m.n;
+  const uint32_t d0 = (uint32_t)m.d0, d2 = (uint32_t)m.d2;
+  uint32_t S0 = 0, tlo = 0, thi = 0;
+  int64_t nmet = 0;
+  for (int s = 0; s < n;) {
+    const int p = s + lane;
+    const bool st = p == n || (p < n && (lane == 0 || flags[p] != 0));  // begins a batch, or the end
+    bool st64 = s + kWave == n;                                         // position s + 64 likewise
+    if (s + kWave < n) st64 = flags[s + kWave] != 0;
+    uint64_t lastm = (__ballot(st) >> 1) | (st64 ? uint64_t(1) << 63 : 0ull);  // batch-last lanes
+    if (lastm == 0ull) lastm = uint64_t(1) << 63;
+    const int w = 64 - __clzll(lastm);
+    const bool in = lane < w;
+    const uint64_t below = lastm & ((uint64_t(1) << lane) - 1);
+    const int b0 = below ? 64 - __clzll(below) : 0;
+    const int b1 = lane + __builtin_ctzll(in ? (lastm >> lane) : 1ull);
+    uint32_t lin = 0, L = 0, thr = 0, kind = 0;
+    int r = 0;
+    if (in) {
+      r = perm[p];
+      const uint4 rq = req[r];
+      lin = req_lin(rq);
+      L = req_lout(rq);
+      thr = rq.y;
+      kind = rq.z & 3u;
+    }
+    const uint32_t pf = in ? (uint32_t)(m.p0 + m.p1 * (uint64_t)lin) : 0u;
+    stage[lane] = make_uint4(L, (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2), pf, 0u);
+    wave_sync_lds();
+    const int bl = in ? b1 - b0 + 1 : 0;
+    int jmax = bl;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) jmax = max(jmax, __shfl_xor(jmax, o));
+    uint32_t acc2 = 0, P = 0;
+    for (int j = 0; j < jmax; ++j) {
+      if (j < bl) {
+        const uint4 sj = stage[b0 + j];
+        P += sj.z;
+        const uint32_t mu = min(sj.x, L);
+        acc2 = mad24_v(mu, mad24_v(d2, mu, sj.y), acc2);
+      }
+    }
+    wave_sync_lds();
+    const uint32_t F = in ? P + __umul24(L, d0) + (acc2 >> 1) : 0u;
+    // lanes past the window hold F = 0 and send nothing; what they receive is unused
+    const uint32_t D = seg_max32(F, b0, b1, lane);
+    const uint32_t contrib = (in && lane == b1) ? D : 0u;
+    const uint32_t incl = scan_add32(contrib);
+    const uint32_t S = S0 + incl - contrib;
+    bool met = false;
+    if (in) {
+      const uint32_t e2e = S + F, ttft = S + P;
+      tlo += e2e & 0xFFFFu;
+      thi += e2e >> 16;
+      met = kind == 0 ? ttft <= thr : (kind == 2 ? e2e <= thr : (uint64_t)(F - P) <= (uint64_t)thr * L);
+      if (DETAIL) {
+        detail[2 * r] = (int64_t)ttft;
+        detail[2 * r + 1] = (int64_t)e2e;
+      }
+    }
+    nmet += ballot_count(met);
+    S0 += readlane(incl, kWave - 1);
+    s += w;
+  }
+  Seg<6>::template all2<OpAdd, OpAdd>(tlo, thi, lane);
+  return Score{nmet, (uint64_t)tlo + ((uint64_t)thi << 16)};
+}
+
 template <bool DETAIL>
 __device__ __forceinline__ Score replay_batches(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm,
                                                 const uint8_t *flags, uint4 *stage, int64_t *detail) {
+  if ((m.flags & (kFlagStaticNarrow | kFlagTime32)) == (kFlagStaticNarrow | kFlagTime32))
+    return replay_batches_windows32<DETAIL>(m, req, perm, flags, stage, detail);
   if (m.flags & kFlagWindows) return replay_batches_windows<DETAIL>(m, req, perm, flags, stage, detail);
   return replay_batches_one<DETAIL>(m, req, perm, flags, stage, detail);
 }

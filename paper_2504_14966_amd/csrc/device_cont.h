@@ -152,6 +152,43 @@ __device__ __forceinline__ uint32_t dpp_old(uint32_t old, uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWMASK, 0xF, false);
 }
 
+// v in the lanes of mask, 0 elsewhere, as one v_cndmask (a select the compiler cannot turn
+// into a branch around the instruction that produced v)
+__device__ __forceinline__ uint32_t keep_lanes(uint32_t v, uint64_t mask) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(v), "s"(mask));
+  return r;
+}
+
+__device__ __forceinline__ uint32_t add_sat(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
+
+// Inclusive scan over the 64 lanes with additions that saturate at 2^32 - 1: every value is
+// nonnegative, so each lane gets min(its true prefix sum, 2^32 - 1) whatever the order.
+__device__ __forceinline__ uint32_t scan_add_sat32(uint32_t v) {
+  v = add_sat(v, dpp_old<kDppRowShr1, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr2, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr4, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowShr8, 0xF>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowBcast15, 0xA>(0u, v));
+  v = add_sat(v, dpp_old<kDppRowBcast31, 0xC>(0u, v));
+  return v;
+}
+
+// Maximum of v over the lane's batch [b0, b1], exact at the batch's last lane b1: a max-scan
+// confined to batches. Every DPP step runs on the whole wave (a lane left out would read as 0
+// to its neighbour): in the row shifts the sending lane zeroes its value unless its batch
+// reaches the receiver; in the row broadcasts (one sender, many receivers) the receiver keeps
+// the value only when its batch starts at or below the sending lane (15 or 47, then 31).
+__device__ __forceinline__ uint32_t seg_max32(uint32_t v, int b0, int b1, int lane) {
+  v = max(v, dpp_old<kDppRowShr1, 0xF>(0u, b1 >= lane + 1 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr2, 0xF>(0u, b1 >= lane + 2 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr4, 0xF>(0u, b1 >= lane + 4 ? v : 0u));
+  v = max(v, dpp_old<kDppRowShr8, 0xF>(0u, b1 >= lane + 8 ? v : 0u));
+  v = max(v, keep_lanes(dpp_old<kDppRowBcast15, 0xA>(0u, v), __ballot(b0 <= (lane | 15) - 16)));
+  v = max(v, keep_lanes(dpp_old<kDppRowBcast31, 0xC>(0u, v), __ballot(b0 <= 31)));
+  return v;
+}
+
 // inclusive scans over the 64 lanes
 __device__ __forceinline__ uint32_t scan_add32(uint32_t v) {
   v += dpp_old<kDppRowShr1, 0xF>(0u, v);

@@ -708,8 +708,9 @@ int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, c
   if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57),
-                                    static_narrow(h, model, n));
+  sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57),
+                              static_narrow(h, model, n));
+  if (sized_narrow(h, model, n)) dm.flags |= sa::kFlagTime32;  // every layout's timeline in 32 bits
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 64 * 16 + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);

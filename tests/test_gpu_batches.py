@@ -234,3 +234,19 @@ def test_eval_batches_wide_model(sl, orc, n, B):
     perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
     starts = random_layouts(rng, k, n, B)
     assert np.array_equal(_eval(sl, q, m, perms, starts), oracle_rows_batches(q, m, perms, starts))
+
+
+@pytest.mark.parametrize("n,B", [(64, 16), (200, 5), (130, 17)])
+def test_eval_batches_wide_timeline(sl, orc, n, B):
+    # narrow pair costs but the timeline above 2^32: the windowed replay in 64 bits (below
+    # 2^32 the 32-bit windows take over)
+    rng = np.random.default_rng(3 * n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    m = Model(B, SEARCH, p0=5_000_000, p1=100, d0=16_000_000 // max(1, B // 16), d1=1000, d2=3)
+    li, lo = q.in_len.astype(object), q.out_len.astype(object)
+    assert sum(m.p0 + m.p1 * li) + (m.d0 + m.d1) * sum(lo) + m.d2 * sum(lo * li + lo * (lo + 1) // 2) > 2**32
+    k = 32
+    perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
+    starts = random_layouts(rng, k, n, B)
+    starts[0] = orc.max_starts(n, B)
+    assert np.array_equal(_eval(sl, q, m, perms, starts), orc.eval_rows_batches(q, m, perms, starts))
