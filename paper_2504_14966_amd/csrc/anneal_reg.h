@@ -11,11 +11,13 @@
 //     mu (e_j + d2 mu)) / 2, mu = min(L_j, L), the batch's members reached by rotating the
 //     row (row_ror, or the two rotations that stay inside an 8-lane half, or quad
 //     permutations); the rotations read the same source registers, so they are independent;
-//   - the batch prefill P and duration D by segment all-reduces, the batch starts by one
-//     exclusive 64-bit add-scan of D placed at each batch's last lane;
+//   - the batch prefill P and duration D by segment all-reduces, the batch starts by an
+//     exclusive add-scan of D (32-bit, starting at the batch size, when the host bounds the
+//     whole timeline below 2^32; else 64-bit from each batch's last lane);
 //   - TTFT = S + P, e2e = S + F and the SLO tests per lane; the met count by ballot, the
-//     latency sum by one 64-bit wave reduction.
-// The 32-bit products and sums are exact under the fixed-size delta kernel's width checks.
+//     latency sum by two 32-bit reductions of 16-bit halves (or one 64-bit reduction).
+// A move inside one batch changes no member's times and needs no replay. The 32-bit
+// products and sums are exact under the fixed-size delta kernel's width checks.
 #pragma once
 #include "anneal_sized.h"
 #include "anneal_wave.h"
@@ -253,12 +255,14 @@ __global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q
 // Same register layout of the order; the layout is a 64-bit scalar mask of start flags
 // (bit p set iff a batch begins at position p). The squeeze / delay / swap rules are the
 // ones of plan_move taken on the mask (batch begin = highest flag at or below a position,
-// batch end = next flag above it, or n). The whole queue is one window of at most 64
-// positions: each lane gathers its batch's members with ds_bpermute, eight offsets in flight
-// at a time (pair terms), the batch prefill is the difference of one add-scan at the batch's
-// ends, the batch durations are one 64-bit max-scan of (first position of the batch << 32 |
-// finish offset), the starts one 32-bit add-scan. Every time fits 32 bits (the host's check
-// for the search's delta kernel).
+// batch end = next flag above it, or n; each lane's bounds are kept until a squeeze or delay
+// changes the mask). The whole queue is one window of at most 64 positions: each lane
+// gathers its batch's members with ds_bpermute, 8 or 16 offsets in flight at a time (pair
+// terms), its TTFT is the prefill add-scan read at the batch's last lane plus the decode
+// durations of the earlier batches, and the durations are a 32-bit max-scan confined to
+// batches. Prefills, offsets and durations fit 32 bits (the fixed-size width checks); the
+// timeline's prefix sums are plain 32-bit scans when the host bounds it below 2^32, and
+// saturate otherwise.
 
 __host__ __device__ __forceinline__ bool reg_sized_fits(int n) { return n >= 1 && n <= 64; }
 
@@ -523,10 +527,11 @@ __global__ void __launch_bounds__(256) anneal_reg_sized_kernel(DevModel m, Queue
 //
 // A member's prefill and decode times depend only on its own lengths and its batch's size,
 // so the replay needs no gathers: each lane takes its batch size from the flag mask and
-// its two closed forms in 64 bits; the batch durations are one 64-bit max-scan of (first
-// position of the batch << 58 | time), the starts one 64-bit add-scan (every time below
-// 2^57, the host's check). Fixed-size batches take swap / insert proposals with the layout
-// fixed; the batch-size search takes squeeze / delay / swap as above.
+// its two closed forms, in 32 bits when every member's time fits (else 64-bit closed forms,
+// a 64-bit max-scan of (first position of the batch << 58 | time) and a 64-bit add-scan,
+// every time below 2^57: the host's checks). Fixed-size batches take swap / insert
+// proposals with the layout fixed; the batch-size search takes squeeze / delay / swap as
+// above.
 
 struct RegFit {
   uint32_t A;   // output length | request id << 16
