@@ -154,9 +154,78 @@ __device__ Score replay_fit_windows(const DevFit &f, const uint4 *__restrict__ r
   return Score{nmet, wave_sum_u64(tl)};
 }
 
+// The same windows when every member's time fits 32 bits (totals only): the closed forms in
+// 32-bit arithmetic (exact, the wrap-around only inside ring expressions whose value fits),
+// durations by the 32-bit max-scan confined to batches, starts by saturating 32-bit scans
+// (a start that saturates meets no threshold, every threshold being below 2^32 - 1), and
+// the total latency exactly as the sum of the member times plus each batch's duration times
+// the number of requests after it.
+__device__ Score replay_fit_windows32(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm,
+                                      const uint8_t *flags) {
+  const int lane = lane_id();
+  const int n = f.n, B = f.B;
+  const uint32_t ap = (uint32_t)f.ap, bp = (uint32_t)f.bp, cp = (uint32_t)f.cp, dp = (uint32_t)f.dp;
+  const uint32_t ad = (uint32_t)f.ad, bd = (uint32_t)f.bd, cd = (uint32_t)f.cd, dd = (uint32_t)f.dd;
+  uint32_t S0 = 0;    // start of the window, saturated
+  uint64_t tsum = 0;  // per lane: member times and duration-weighted counts
+  int64_t nmet = 0;
+  for (int s = 0; s < n;) {
+    const int p = s + lane;
+    bool st = p == n;
+    if (p < n) {
+      if (flags) st = lane == 0 || flags[p] != 0;
+      else st = (uint64_t)lane == (((uint64_t)lane * f.bmagic) >> 32) * (uint64_t)B;
+    }
+    bool st64 = s + kWave == n;
+    if (s + kWave < n) st64 = flags ? flags[s + kWave] != 0 : (kWave % B) == 0;
+    uint64_t lastm = (__ballot(st) >> 1) | (st64 ? uint64_t(1) << 63 : 0ull);
+    if (lastm == 0ull) lastm = uint64_t(1) << 63;
+    const int w = 64 - __clzll(lastm);
+    const bool in = lane < w;
+    const uint64_t below = lastm & ((uint64_t(1) << lane) - 1);
+    const int b0 = below ? 64 - __clzll(below) : 0;
+    const int b1 = lane + __builtin_ctzll(in ? (lastm >> lane) : 1ull);
+    uint32_t tp = 0, td = 0, E = 0, L = 0;
+    uint4 rq = make_uint4(0u, 0u, 0u, 0u);
+    if (in) {
+      rq = req[perm[p]];
+      const uint32_t b = (uint32_t)(b1 - b0 + 1), l = rq.x & 0xFFFFu;
+      L = rq.x >> 16;
+      tp = ap * b * l + bp * b + cp * l + dp;
+      td = L * (bd * b + dd) + (ad * b + cd) * (L * l + ((L * (L + 1u)) >> 1));
+      E = tp + td;
+    }
+    // lanes past the window hold E = 0 and send nothing; what they receive is unused
+    const uint32_t D = seg_max32(E, b0, b1, lane);
+    const bool last = in && lane == b1;
+    const uint32_t contrib = last ? D : 0u;
+    // durations of the window's earlier batches: the inclusive scan moved up one lane
+    const uint32_t excl =
+        scan_add_sat32((uint32_t)__builtin_amdgcn_update_dpp(0, (int)contrib, kDppWaveShr1, 0xF, 0xF, false));
+    const uint32_t S = add_sat(S0, excl);
+    bool met = false;
+    if (in) {
+      const uint32_t ttft = add_sat(S, tp), e2e = add_sat(S, E);
+      const uint32_t kind = rq.z;
+      met = kind == 0   ? ttft <= rq.y
+            : kind == 1 ? (uint64_t)td <= (uint64_t)rq.y * L
+            : kind == 2 ? e2e <= rq.y
+                        : (ttft <= rq.y && (uint64_t)td <= (uint64_t)rq.w * L);
+    }
+    nmet += ballot_count(met);
+    tsum += (uint64_t)E + (uint64_t)contrib * (uint32_t)(last ? n - 1 - p : 0);
+    S0 = add_sat(S0, add_sat(readlane(excl, kWave - 1), readlane(contrib, kWave - 1)));
+    s += w;
+  }
+  return Score{nmet, wave_sum_u64(tsum)};
+}
+
 template <bool DETAIL>
 __device__ __forceinline__ Score replay_fit(const DevFit &f, const uint4 *__restrict__ req, const uint16_t *perm,
                                             const uint8_t *flags, int64_t *detail) {
+  if constexpr (!DETAIL) {
+    if (f.m32) return replay_fit_windows32(f, req, perm, flags);
+  }
   if (f.win) return replay_fit_windows<DETAIL>(f, req, perm, flags, detail);
   return replay_fit_batches<DETAIL>(f, req, perm, flags, detail);
 }

@@ -145,6 +145,28 @@ def test_anneal_fit_shapes(sl, orc, n, B, policy):
     _check_winner(res, False)
 
 
+@pytest.mark.parametrize("n,B,policy,scale", [(150, 16, 0, 1), (200, 16, 2, 1), (150, 16, 0, 64), (130, 33, 2, 64)])
+def test_anneal_fit_windows_widths(sl, orc, n, B, policy, scale):
+    # more than 64 requests (windows of whole batches): member times below 2^32 take the
+    # 32-bit windows, above it the 64-bit ones
+    from paper_2504_14966_amd.workloads import TABLE2_10NS
+    rng = np.random.default_rng(n + B + scale)
+    q = random_queue(rng, n, max_in=2000, max_out=300, thr_hi=2_000_000_000)
+    q.kind[::4] = 3
+    thr2 = (rng.integers(1_500_000, 1_800_000, n) * scale).astype(np.uint32)
+    coef = {k: v * scale for k, v in TABLE2_10NS.items()}
+    fd, fo = sl.FitModel(B, policy, **coef), orc.FitModel(B, policy, **coef)
+    chains, iters = 6, 150
+    res = _anneal(sl, q, fd, chains, iters, 1.0, 0.99, 3, thr2, None)
+    info = orc.start_fit(q, fo, None, thr2)
+    for c in range(chains):
+        w = orc.anneal_chain_fit(q, fo, c, iters, 1.0, 0.99, 3, thr2=thr2, start_info=info)
+        assert res["rec"][c].tolist() == w["rec"].tolist(), c
+        assert res["cur"][c].tolist() == w["cur"].tolist() and res["best"][c].tolist() == w["best"].tolist(), c
+        assert res["cs"][c].tolist() == w["cur_starts"].tolist() and res["bs"][c].tolist() == w["best_starts"].tolist(), c
+    _check_winner(res, False)
+
+
 @pytest.mark.parametrize("policy", [0, 2])
 def test_fit_huge_times_batch_replay(sl, orc, policy):
     # member times of 2^56 and more: the windowed replay's keys would not hold them, so the
