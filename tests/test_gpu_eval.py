@@ -95,8 +95,8 @@ def _timeline_end(q, m):
 
 @pytest.mark.parametrize("n,B,wide", [(1, 1, False), (7, 3, False), (33, 8, False), (64, 64, False),
                                       (100, 33, False), (257, 64, False), (300, 1, False), (1024, 64, False),
-                                      (1024, 48, False), (64, 16, True), (130, 17, True), (64, 1, True),
-                                      (200, 5, True)])
+                                      (1024, 48, False), (200, 20, False), (90, 32, False), (50, 2, False),
+                                      (64, 16, True), (130, 17, True), (64, 1, True), (200, 5, True)])
 def test_static_rows_without_detail(sl, orc, n, B, wide):
     # totals only: a timeline within 32 bits takes the 32-bit start scan and latency sum,
     # a wider one the 64-bit path
