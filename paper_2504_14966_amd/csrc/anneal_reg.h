@@ -250,6 +250,236 @@ __global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q
                                     ws);
 }
 
+// ---- 65 to 192 requests: H = 2 or 3 positions per lane ----
+//
+// Position p sits in lane p mod 64 of part p / 64 (H registers per field). Batches of at
+// most 16 never straddle the parts, so each part replays as above; a part's batch starts
+// add the earlier parts' totals. A swap reads and writes the two positions in their parts;
+// an insert shifts each part by one DPP wave shift and carries the element that crosses a
+// part boundary with one v_readlane and one v_writelane.
+
+__host__ __device__ __forceinline__ int reg_parts(int n, int B) {
+  if (n < 1 || n > 192 || B < 1 || B > 16 || (B & (B - 1)) != 0) return 0;
+  return (n + 63) / 64;
+}
+
+template <int H>
+struct RegStateH {
+  RegState h[H];
+};
+
+// lane l of x[part] for a wave-uniform part index (scalar branches around each v_readlane,
+// so that no dynamically indexed register array is formed)
+template <int H>
+__device__ __forceinline__ uint32_t read_part(const uint32_t (&x)[H], int part, int l) {
+  if (H > 2 && part == 2) return readlane(x[H > 2 ? 2 : 0], l);
+  if (part == 1) return readlane(x[1], l);
+  return readlane(x[0], l);
+}
+
+template <int LG, bool T32, int H>
+__device__ __forceinline__ Score reg_replay_h(const RegStateH<H> &s, int n, uint32_t d0, uint32_t d2, int lane) {
+  constexpr int B = 1 << LG;
+  uint32_t F[H], P[H], D[H], kind[H];
+  bool valid[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    valid[h] = lane + 64 * h < n;
+    const uint32_t L = s.h[h].A & 0xFFFFu, e = s.h[h].E & 0x3FFFFFFFu;
+    kind[h] = s.h[h].E >> 30;
+    const uint32_t acc = mad24_v(L, mad24_v(d2, L, e), pair_sum_others<LG>(L, e, d2, lane));
+    P[h] = Seg<LG>::template all<OpAdd>(s.h[h].PF, lane);
+    F[h] = valid[h] ? P[h] + __umul24(L, d0) + (acc >> 1) : 0u;
+    D[h] = Seg<LG>::template all<OpMax>(F[h], lane);
+  }
+  int64_t nmet = 0;
+  if constexpr (T32) {
+    uint32_t lo = 0, hi = 0, carry = 0;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      uint32_t v = D[h];
+      if constexpr (LG <= 0) v += dpp_old<kDppRowShr1, 0xF>(0u, v);
+      if constexpr (LG <= 1) v += dpp_old<kDppRowShr2, 0xF>(0u, v);
+      if constexpr (LG <= 2) v += dpp_old<kDppRowShr4, 0xF>(0u, v);
+      if constexpr (LG <= 3) v += dpp_old<kDppRowShr8, 0xF>(0u, v);
+      v += dpp_old<kDppRowBcast15, 0xA>(0u, v);
+      v += dpp_old<kDppRowBcast31, 0xC>(0u, v);
+      const uint32_t S = carry + v - D[h];
+      const uint32_t ttft = S + P[h], e2e = S + F[h];
+      const uint32_t x = kind[h] == 0 ? ttft : (kind[h] == 2 ? e2e : F[h] - P[h]);
+      nmet += __popcll(__ballot(valid[h] && x <= s.h[h].T));
+      lo += valid[h] ? (e2e & 0xFFFFu) : 0u;
+      hi += valid[h] ? (e2e >> 16) : 0u;
+      carry += readlane(v, kWave - 1);
+    }
+    // each lane's halves below 2^18, their sums below 2^24
+    wave_all2<OpAdd, OpAdd>(lo, hi);
+    return Score{nmet, (uint64_t)lo + ((uint64_t)hi << 16)};
+  } else {
+    uint64_t carry = 0, tsum = 0;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)D[h] : 0ull;
+      const uint64_t incl = scan_add64(contrib);
+      const uint64_t S = carry + incl - contrib;
+      const uint64_t ttft = S + P[h], e2e = S + F[h];
+      const bool met = valid[h] && (kind[h] == 0   ? ttft <= (uint64_t)s.h[h].T
+                                    : kind[h] == 2 ? e2e <= (uint64_t)s.h[h].T
+                                                   : F[h] - P[h] <= s.h[h].T);
+      nmet += __popcll(__ballot(met));
+      tsum += valid[h] ? e2e : 0ull;
+      carry += rl64(incl, kWave - 1);
+    }
+    return Score{nmet, wave_sum64_dpp(tsum)};
+  }
+}
+
+template <int LG, int OBJ, bool T32, int H>
+__device__ void anneal_reg_h_body(const DevModel &m, const QueuePtrs &q, int chains, int chain, uint32_t rng_chain,
+                                  int iters, double T0, double alpha, uint32_t key0, uint32_t key1, uint64_t swap_thr,
+                                  const SearchParams &srch, unsigned char *ws) {
+  const int n = m.n;
+  const int lane = lane_id();
+  const uint32_t d0 = (uint32_t)m.d0, d2 = (uint32_t)m.d2;
+  const WsHeader *hd = reinterpret_cast<const WsHeader *>(ws);
+  const int64_t t_ref = hd->t_ref;
+  const int64_t allmet = hd->allmet;
+  const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
+  const size_t stride = ws_perm_stride(n);
+  uint16_t *gbest = reinterpret_cast<uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)chain * stride;
+  uint16_t *gcur = reinterpret_cast<uint16_t *>(ws + ws_off_cur(n, chains)) + (size_t)chain * stride;
+  RegStateH<H> cur;
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    cur.h[h] = RegState{0u, 0u, 0u, 0u};
+    const int p = lane + 64 * h;
+    if (p < n) {
+      const uint32_t r = start[p];
+      const uint32_t lin = q.in_len[r], L = q.out_len[r], kind = q.kind[r], thr = q.thr[r];
+      const uint32_t e = (uint32_t)(2 * (m.d1 + m.d2 * lin) + m.d2);
+      const uint64_t thr_l = (uint64_t)thr * L;
+      cur.h[h].A = L | (r << 16);
+      cur.h[h].E = e | (kind << 30);
+      cur.h[h].PF = (uint32_t)(m.p0 + m.p1 * lin);
+      cur.h[h].T = kind == 1 ? (uint32_t)min(thr_l, (uint64_t)0xFFFFFFFFu) : thr;
+      gbest[p] = (uint16_t)r;
+    }
+  }
+  const Score s0 = reg_replay_h<LG, T32, H>(cur, n, d0, d2, lane);
+  int64_t cn = s0.n;
+  uint64_t ct = s0.t;
+  int64_t bn = cn;
+  uint64_t bt = ct;
+  int64_t biter = -1, accepts = 0;
+  uint64_t digest = kFnvOffset;
+  Cooling cool{T0, alpha, srch.level_len, srch.level_len};
+  ProposalStream ps;
+  const int iters_run = (srch.early_exit && allmet) ? 0 : iters;
+  for (int k = 0; k < iters_run; ++k) {
+    if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
+    const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
+    const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
+    const int pi = i >> 6, li = i & 63, pj = j >> 6, lj = j & 63;
+    RegStateH<H> cand;
+    // one field across the parts: x in, y out
+    auto field = [&](auto get, auto put) {
+      uint32_t x[H], y[H];
+#pragma unroll
+      for (int h = 0; h < H; ++h) x[h] = get(cur.h[h]);
+      const uint32_t xi = read_part<H>(x, pi, li);
+      if (((pk >> 20) & 1u) == 0u) {
+        // swap positions i and j
+        const uint32_t xj = read_part<H>(x, pj, lj);
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+          y[h] = x[h];
+          if (h == pi) y[h] = wlane_m0(xj, li, y[h]);
+          if (h == pj) y[h] = wlane_m0(xi, lj, y[h]);
+        }
+      } else {
+        // insert: the request at i moves to j; positions [i, j) take p + 1, or (j, i] take
+        // p - 1
+        const bool right = i < j;
+        const int lo = right ? i : j + 1;
+        const uint32_t span = (uint32_t)(right ? j - i : i - j);
+#pragma unroll
+        for (int h = 0; h < H; ++h) {
+          uint32_t sh;
+          if (right) {
+            sh = dppv<0x130>(x[h]);
+            if (h + 1 < H) sh = wlane_m0(readlane(x[h + 1 < H ? h + 1 : h], 0), kWave - 1, sh);
+          } else {
+            sh = dppv<0x138>(x[h]);
+            if (h > 0) sh = wlane_m0(readlane(x[h > 0 ? h - 1 : 0], kWave - 1), 0, sh);
+          }
+          y[h] = (uint32_t)(lane + 64 * h - lo) < span ? sh : x[h];
+          if (h == pj) y[h] = wlane_m0(xi, lj, y[h]);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < H; ++h) put(cand.h[h], y[h]);
+    };
+    field([](const RegState &r) { return r.A; }, [](RegState &r, uint32_t v) { r.A = v; });
+    field([](const RegState &r) { return r.E; }, [](RegState &r, uint32_t v) { r.E = v; });
+    field([](const RegState &r) { return r.PF; }, [](RegState &r, uint32_t v) { r.PF = v; });
+    field([](const RegState &r) { return r.T; }, [](RegState &r, uint32_t v) { r.T = v; });
+    // a move inside one batch keeps every batch's members: no replay
+    const Score sc = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay_h<LG, T32, H>(cand, n, d0, d2, lane);
+    if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
+      cur = cand;
+      cn = sc.n;
+      ct = sc.t;
+      ++accepts;
+      digest = (digest ^ (uint64_t)k) * kFnvPrime;
+      digest = (digest ^ (uint64_t)cn) * kFnvPrime;
+      digest = (digest ^ ct) * kFnvPrime;
+      if (obj_better<OBJ>(cn, ct, bn, bt)) {
+        bn = cn;
+        bt = ct;
+        biter = k;
+#pragma unroll
+        for (int h = 0; h < H; ++h)
+          if (lane + 64 * h < n) gbest[lane + 64 * h] = (uint16_t)(cur.h[h].A >> 16);
+      }
+    }
+    cool.step();
+  }
+#pragma unroll
+  for (int h = 0; h < H; ++h)
+    if (lane + 64 * h < n) gcur[lane + 64 * h] = (uint16_t)(cur.h[h].A >> 16);
+  if (lane == 0) write_record(ws, n, chain, cn, ct, bn, bt, biter, accepts, digest, allmet);
+}
+
+// The chain body for any request count the register kernels take (at most 192): one, two
+// or three positions per lane.
+template <int LG, int OBJ>
+__device__ __forceinline__ void anneal_reg_any(const DevModel &m, const QueuePtrs &q, int chains, int chain,
+                                               uint32_t rng_chain, int iters, double T0, double alpha, uint32_t key0,
+                                               uint32_t key1, uint64_t swap_thr, const SearchParams &srch,
+                                               unsigned char *ws) {
+  const bool t32 = (m.flags & kFlagTime32) != 0;
+  if (m.n <= 64) {
+    if (t32) anneal_reg_body<LG, OBJ, true>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+    else anneal_reg_body<LG, OBJ, false>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+  } else if (m.n <= 128) {
+    if (t32) anneal_reg_h_body<LG, OBJ, true, 2>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+    else anneal_reg_h_body<LG, OBJ, false, 2>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+  } else {
+    if (t32) anneal_reg_h_body<LG, OBJ, true, 3>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+    else anneal_reg_h_body<LG, OBJ, false, 3>(m, q, chains, chain, rng_chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+  }
+}
+
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(256) anneal_reg_h_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
+                                                            double alpha, uint32_t key0, uint32_t key1,
+                                                            uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  anneal_reg_any<LG, OBJ>(m, q, chains, chain, (uint32_t)chain, iters, T0, alpha, key0, key1, swap_thr, srch, ws);
+}
+
 // ---- the joint order / batch-size search on small queues, state in registers ----
 //
 // Same register layout of the order; the layout is a 64-bit scalar mask of start flags

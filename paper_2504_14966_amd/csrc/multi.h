@@ -309,6 +309,27 @@ __global__ void __launch_bounds__(256) multi_reg_kernel(DevModel m, int n, int i
                                     swap_thr, srch, slot);
 }
 
+// The same for instances of up to 192 requests (one, two or three positions per lane, by
+// each instance's own request count).
+template <int LG, int OBJ>
+__global__ void __launch_bounds__(256) multi_reg_h_kernel(DevModel m, int n, int instances, int chains, int groups,
+                                                           int iters, double T0, double alpha, uint32_t key0,
+                                                           uint32_t key1, uint64_t swap_thr, SearchParams srch,
+                                                           unsigned char *mws) {
+  const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
+  const int nk = slot_n(mws, k);
+  if (nk == 0) return;
+  const int waves = blockDim.x >> 6;
+  const int chain = uniform(g * waves + (int)(threadIdx.x >> 6));
+  if (chain >= chains) return;
+  unsigned char *slot = mws + mws_off_slot(n, instances, chains, k);
+  const SlotQueue sq = slot_queue(slot, n, chains);
+  DevModel mk = m;
+  mk.n = nk;
+  anneal_reg_any<LG, OBJ>(mk, QueuePtrs{sq.in_len, sq.out_len, sq.kind, sq.thr}, chains, chain,
+                          (uint32_t)(k * chains + chain), iters, T0, alpha, key0, key1, swap_thr, srch, slot);
+}
+
 // One workgroup per instance: its winner over chains.
 __global__ void __launch_bounds__(1024) multi_reduce_kernel(int n, int instances, int chains, unsigned char *mws) {
   const int k = blockIdx.x;

@@ -400,6 +400,27 @@ int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevM
     HIP_TRY(hipGetLastError());
     done = true;
   }
+  if (!done && model->policy == SCHED_STATIC && sa::reg_parts(n, model->max_batch) > 1 &&
+      static_narrow(h, model, n)) {
+    // 65 to 192 requests: two or three positions per lane, still no LDS
+    const int cus = std::max(1, cu_count());
+    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
+    const int grid = (chains + waves - 1) / waves;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    const sa::QueuePtrs qp = dev_queue(queue);
+    const uint64_t st = model->swap_threshold;
+    sa::DevModel dr = dm;
+    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
+    switch (model->max_batch) {
+      case 1: sa::anneal_reg_h_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 2: sa::anneal_reg_h_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 4: sa::anneal_reg_h_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      case 8: sa::anneal_reg_h_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+      default: sa::anneal_reg_h_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
+    }
+    HIP_TRY(hipGetLastError());
+    done = true;
+  }
   if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
     // chains per workgroup: enough to spread the chains over every CU, at most 16 and
     // at most what the LDS holds
@@ -804,9 +825,12 @@ int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, c
   sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(dm, n, instances, chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
   bool done = nk_max == 0;
-  if (!done && model->policy == SCHED_STATIC && sa::reg_kernel_fits(nk_max, model->max_batch) &&
+  if (!done && model->policy == SCHED_STATIC &&
+      sa::reg_parts(nk_max, model->max_batch) > 0 &&
       static_narrow(h, model, n)) {
-    // every instance small: the register kernel per instance, no LDS
+    // every instance small: the register kernel per instance, no LDS (two or three positions
+    // per lane when an instance holds more than 64 requests)
+    const bool two = nk_max > 64;
     const int total = instances * chains, cus = std::max(1, cu_count());
     const int waves = total >= 4 * cus && chains >= 4 ? 4 : (total >= 2 * cus && chains >= 2 ? 2 : 1);
     const int groups = (chains + waves - 1) / waves, grid = instances * groups;
@@ -816,7 +840,13 @@ int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, c
     sa::DevModel dr = dm;
     if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
 #define SA_MULTI_REG(LG)                                                                                         \
-  if (srch.objective)                                                                                          \
+  if (two && srch.objective)                                                                                   \
+    sa::multi_reg_h_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,    \
+                                                                  alpha, k0, k1, st, srch, w);                 \
+  else if (two)                                                                                                \
+    sa::multi_reg_h_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,    \
+                                                                  alpha, k0, k1, st, srch, w);                 \
+  else if (srch.objective)                                                                                     \
     sa::multi_reg_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,     \
                                                                  alpha, k0, k1, st, srch, w);                  \
   else                                                                                                         \

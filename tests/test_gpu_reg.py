@@ -87,6 +87,33 @@ def test_reg_kernel_wide_timeline(sl, orc, B, search):
     _run_check(sl, orc, q, m, 6, 300, 2.0, 0.99, 21, search)
 
 
+@pytest.mark.parametrize("n,B", [(65, 1), (100, 2), (128, 4), (129, 8), (150, 16), (192, 16), (177, 1), (70, 16)])
+@pytest.mark.parametrize("thr", [0, 1 << 32, 1 << 31])
+def test_reg_parts_shapes_and_moves(sl, orc, n, B, thr):
+    # 65 to 192 requests: two or three positions per lane; swaps and inserts across parts
+    rng = np.random.default_rng(n * 17 + B * 3 + (thr >> 30))
+    q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=60_000 * n)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2, swap_threshold=thr)
+    _run_check(sl, orc, q, m, 6, 300, 0.8, 0.995, 17)
+
+
+@pytest.mark.parametrize("n,B,search", [(120, 8, (1, 20, 0)), (190, 16, (1, 7, 1)), (99, 4, (0, 5, 1))])
+def test_reg_parts_objectives(sl, orc, n, B, search):
+    rng = np.random.default_rng(300 + n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=6_000_000)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    _run_check(sl, orc, q, m, 6, 400, 3.0, 0.97, 5, search)
+
+
+@pytest.mark.parametrize("n,B", [(128, 16), (160, 4)])
+def test_reg_parts_wide_timeline(sl, orc, n, B):
+    rng = np.random.default_rng(910 + n + B)
+    q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    m = Model(B, 0, p0=5_000_000, p1=100, d0=16_000_000, d1=1000, d2=3)
+    assert _static_narrow(q, m) and _timeline_end(q, m) > 2**32
+    _run_check(sl, orc, q, m, 6, 250, 2.0, 0.99, 29)
+
+
 @pytest.mark.parametrize("B,search", [(8, (1, 20, 0)), (16, (1, 7, 1)), (4, (0, 5, 0)), (2, (1, 3, 1))])
 def test_reg_kernel_objectives(sl, orc, B, search):
     rng = np.random.default_rng(200 + B)
