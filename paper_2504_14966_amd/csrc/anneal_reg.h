@@ -277,39 +277,45 @@ __device__ __forceinline__ uint32_t read_part(const uint32_t (&x)[H], int part, 
   return readlane(x[0], l);
 }
 
+// A part's own values: each member's finish offset F within its batch, and its batch's
+// prefill P and duration D (the same on every lane of a batch).
+struct PartVals {
+  uint32_t F, P, D;
+};
+
+template <int LG>
+__device__ __forceinline__ PartVals part_local(const RegState &st, bool valid, uint32_t d0, uint32_t d2, int lane) {
+  const uint32_t L = st.A & 0xFFFFu, e = st.E & 0x3FFFFFFFu;
+  const uint32_t acc = mad24_v(L, mad24_v(d2, L, e), pair_sum_others<LG>(L, e, d2, lane));
+  const uint32_t P = Seg<LG>::template all<OpAdd>(st.PF, lane);
+  const uint32_t F = valid ? P + __umul24(L, d0) + (acc >> 1) : 0u;
+  return PartVals{F, P, Seg<LG>::template all<OpMax>(F, lane)};
+}
+
+// Starts across the parts, SLO tests and sums from the parts' values.
 template <int LG, bool T32, int H>
-__device__ __forceinline__ Score reg_replay_h(const RegStateH<H> &s, int n, uint32_t d0, uint32_t d2, int lane) {
+__device__ __forceinline__ Score part_combine(const RegStateH<H> &s, const PartVals (&pv)[H], int n, int lane) {
   constexpr int B = 1 << LG;
-  uint32_t F[H], P[H], D[H], kind[H];
-  bool valid[H];
-#pragma unroll
-  for (int h = 0; h < H; ++h) {
-    valid[h] = lane + 64 * h < n;
-    const uint32_t L = s.h[h].A & 0xFFFFu, e = s.h[h].E & 0x3FFFFFFFu;
-    kind[h] = s.h[h].E >> 30;
-    const uint32_t acc = mad24_v(L, mad24_v(d2, L, e), pair_sum_others<LG>(L, e, d2, lane));
-    P[h] = Seg<LG>::template all<OpAdd>(s.h[h].PF, lane);
-    F[h] = valid[h] ? P[h] + __umul24(L, d0) + (acc >> 1) : 0u;
-    D[h] = Seg<LG>::template all<OpMax>(F[h], lane);
-  }
   int64_t nmet = 0;
   if constexpr (T32) {
     uint32_t lo = 0, hi = 0, carry = 0;
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-      uint32_t v = D[h];
+      const bool valid = lane + 64 * h < n;
+      const uint32_t kind = s.h[h].E >> 30, D = pv[h].D, F = pv[h].F, P = pv[h].P;
+      uint32_t v = D;
       if constexpr (LG <= 0) v += dpp_old<kDppRowShr1, 0xF>(0u, v);
       if constexpr (LG <= 1) v += dpp_old<kDppRowShr2, 0xF>(0u, v);
       if constexpr (LG <= 2) v += dpp_old<kDppRowShr4, 0xF>(0u, v);
       if constexpr (LG <= 3) v += dpp_old<kDppRowShr8, 0xF>(0u, v);
       v += dpp_old<kDppRowBcast15, 0xA>(0u, v);
       v += dpp_old<kDppRowBcast31, 0xC>(0u, v);
-      const uint32_t S = carry + v - D[h];
-      const uint32_t ttft = S + P[h], e2e = S + F[h];
-      const uint32_t x = kind[h] == 0 ? ttft : (kind[h] == 2 ? e2e : F[h] - P[h]);
-      nmet += __popcll(__ballot(valid[h] && x <= s.h[h].T));
-      lo += valid[h] ? (e2e & 0xFFFFu) : 0u;
-      hi += valid[h] ? (e2e >> 16) : 0u;
+      const uint32_t S = carry + v - D;
+      const uint32_t ttft = S + P, e2e = S + F;
+      const uint32_t x = kind == 0 ? ttft : (kind == 2 ? e2e : F - P);
+      nmet += __popcll(__ballot(valid && x <= s.h[h].T));
+      lo += valid ? (e2e & 0xFFFFu) : 0u;
+      hi += valid ? (e2e >> 16) : 0u;
       carry += readlane(v, kWave - 1);
     }
     // each lane's halves below 2^18, their sums below 2^24
@@ -319,15 +325,17 @@ __device__ __forceinline__ Score reg_replay_h(const RegStateH<H> &s, int n, uint
     uint64_t carry = 0, tsum = 0;
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-      const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)D[h] : 0ull;
+      const bool valid = lane + 64 * h < n;
+      const uint32_t kind = s.h[h].E >> 30, F = pv[h].F, P = pv[h].P;
+      const uint64_t contrib = (lane & (B - 1)) == B - 1 ? (uint64_t)pv[h].D : 0ull;
       const uint64_t incl = scan_add64(contrib);
       const uint64_t S = carry + incl - contrib;
-      const uint64_t ttft = S + P[h], e2e = S + F[h];
-      const bool met = valid[h] && (kind[h] == 0   ? ttft <= (uint64_t)s.h[h].T
-                                    : kind[h] == 2 ? e2e <= (uint64_t)s.h[h].T
-                                                   : F[h] - P[h] <= s.h[h].T);
+      const uint64_t ttft = S + P, e2e = S + F;
+      const bool met = valid && (kind == 0   ? ttft <= (uint64_t)s.h[h].T
+                                 : kind == 2 ? e2e <= (uint64_t)s.h[h].T
+                                             : F - P <= s.h[h].T);
       nmet += __popcll(__ballot(met));
-      tsum += valid[h] ? e2e : 0ull;
+      tsum += valid ? e2e : 0ull;
       carry += rl64(incl, kWave - 1);
     }
     return Score{nmet, wave_sum64_dpp(tsum)};
@@ -365,7 +373,12 @@ __device__ void anneal_reg_h_body(const DevModel &m, const QueuePtrs &q, int cha
       gbest[p] = (uint16_t)r;
     }
   }
-  const Score s0 = reg_replay_h<LG, T32, H>(cur, n, d0, d2, lane);
+  // each part's values are kept with the state; a proposal recomputes only the parts that
+  // hold a changed position (the finish offsets move with their requests in the others)
+  PartVals cpv[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) cpv[h] = part_local<LG>(cur.h[h], lane + 64 * h < n, d0, d2, lane);
+  const Score s0 = part_combine<LG, T32, H>(cur, cpv, n, lane);
   int64_t cn = s0.n;
   uint64_t ct = s0.t;
   int64_t bn = cn;
@@ -380,15 +393,13 @@ __device__ void anneal_reg_h_body(const DevModel &m, const QueuePtrs &q, int cha
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     const int pi = i >> 6, li = i & 63, pj = j >> 6, lj = j & 63;
+    const bool swap = ((pk >> 20) & 1u) == 0u;
     RegStateH<H> cand;
-    // one field across the parts: x in, y out
-    auto field = [&](auto get, auto put) {
-      uint32_t x[H], y[H];
-#pragma unroll
-      for (int h = 0; h < H; ++h) x[h] = get(cur.h[h]);
+    PartVals npv[H];
+    // one per-position field across the parts (x in, y out)
+    auto move = [&](const uint32_t (&x)[H], uint32_t (&y)[H]) {
       const uint32_t xi = read_part<H>(x, pi, li);
-      if (((pk >> 20) & 1u) == 0u) {
-        // swap positions i and j
+      if (swap) {
         const uint32_t xj = read_part<H>(x, pj, lj);
 #pragma unroll
         for (int h = 0; h < H; ++h) {
@@ -416,17 +427,41 @@ __device__ void anneal_reg_h_body(const DevModel &m, const QueuePtrs &q, int cha
           if (h == pj) y[h] = wlane_m0(xi, lj, y[h]);
         }
       }
-#pragma unroll
-      for (int h = 0; h < H; ++h) put(cand.h[h], y[h]);
     };
-    field([](const RegState &r) { return r.A; }, [](RegState &r, uint32_t v) { r.A = v; });
-    field([](const RegState &r) { return r.E; }, [](RegState &r, uint32_t v) { r.E = v; });
-    field([](const RegState &r) { return r.PF; }, [](RegState &r, uint32_t v) { r.PF = v; });
-    field([](const RegState &r) { return r.T; }, [](RegState &r, uint32_t v) { r.T = v; });
-    // a move inside one batch keeps every batch's members: no replay
-    const Score sc = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay_h<LG, T32, H>(cand, n, d0, d2, lane);
+    {
+      uint32_t x[H], y[H];
+#define SA_MOVE_FIELD(GET, PUT)                      \
+  _Pragma("unroll") for (int h = 0; h < H; ++h) x[h] = GET; \
+  move(x, y);                                        \
+  _Pragma("unroll") for (int h = 0; h < H; ++h) PUT = y[h];
+      SA_MOVE_FIELD(cur.h[h].A, cand.h[h].A)
+      SA_MOVE_FIELD(cur.h[h].E, cand.h[h].E)
+      SA_MOVE_FIELD(cur.h[h].PF, cand.h[h].PF)
+      SA_MOVE_FIELD(cur.h[h].T, cand.h[h].T)
+      SA_MOVE_FIELD(cpv[h].F, npv[h].F)
+#undef SA_MOVE_FIELD
+    }
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      npv[h].P = cpv[h].P;
+      npv[h].D = cpv[h].D;
+    }
+    Score sc{cn, ct};
+    // a move inside one batch keeps every batch's members and every member's offset: no
+    // replay (the offsets moved with their requests)
+    if ((i >> LG) != (j >> LG)) {
+      const int plo = min(pi, pj), phi = max(pi, pj);
+#pragma unroll
+      for (int h = 0; h < H; ++h) {
+        const bool touched = swap ? (h == pi || h == pj) : (h >= plo && h <= phi);
+        if (touched) npv[h] = part_local<LG>(cand.h[h], lane + 64 * h < n, d0, d2, lane);
+      }
+      sc = part_combine<LG, T32, H>(cand, npv, n, lane);
+    }
     if (obj_accept<OBJ>(cn, ct, sc.n - cn, (int64_t)(sc.t - ct), t_ref, cool.T, w3)) {
       cur = cand;
+#pragma unroll
+      for (int h = 0; h < H; ++h) cpv[h] = npv[h];
       cn = sc.n;
       ct = sc.t;
       ++accepts;
