@@ -217,3 +217,22 @@ def _reg_fit_check(sl, orc, n, B, policy, search, scale):
     if not (search and search[0]):
         k = max(range(chains), key=lambda c: (rec[c, 2], -rec[c, 3], -c))
         assert key.cpu().numpy().tolist() == [rec[k, 2], rec[k, 3], k]
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_reg_random_sweep(sl, orc, seed):
+    # seeded random shapes across the register kernels' whole range: 1 to 192 requests, every
+    # power-of-two batch size up to 16, narrow or wide timelines, any move mix, both objectives
+    rng = np.random.default_rng(4000 + seed)
+    n = int(rng.integers(1, 193))
+    B = int(rng.choice([1, 2, 4, 8, 16]))
+    thr = int(rng.choice([0, 1 << 31, 1 << 32, int(rng.integers(0, 1 << 32))]))
+    if rng.random() < 0.3:
+        q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+        m = Model(B, 0, p0=5_000_000, p1=100, d0=16_000_000, d1=1000, d2=3, swap_threshold=thr)
+    else:
+        q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=60_000 * n)
+        m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2, swap_threshold=thr)
+    assert _static_narrow(q, m)
+    search = None if rng.random() < 0.5 else (1, int(rng.integers(1, 30)), int(rng.integers(0, 2)))
+    _run_check(sl, orc, q, m, 4, 200, float(rng.choice([0.5, 2.0, 50.0])), 0.98, seed, search)
