@@ -236,3 +236,56 @@ def test_reg_random_sweep(sl, orc, seed):
     assert _static_narrow(q, m)
     search = None if rng.random() < 0.5 else (1, int(rng.integers(1, 30)), int(rng.integers(0, 2)))
     _run_check(sl, orc, q, m, 4, 200, float(rng.choice([0.5, 2.0, 50.0])), 0.98, seed, search)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_reg_search_random_sweep(sl, orc, seed):
+    # the register search kernel over random shapes: 1 to 64 requests, maximum batch 1 to 64,
+    # narrow or wide timelines, both objectives
+    rng = np.random.default_rng(5000 + seed)
+    n = int(rng.integers(1, 65))
+    B = int(rng.integers(1, 65))
+    if rng.random() < 0.3:
+        q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+        m = Model(B, 2, p0=5_000_000, p1=100, d0=16_000_000 // max(1, min(n, B) // 16 + 1), d1=1000, d2=3)
+    else:
+        q = random_queue(rng, n, max_in=3000, max_out=150, thr_hi=60_000 * n)
+        m = Model(B, 2, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    assert _static_narrow(q, m)
+    search = None if rng.random() < 0.5 else (1, int(rng.integers(1, 30)), int(rng.integers(0, 2)))
+    _search_check(sl, orc, q, m, 4, 250, float(rng.choice([0.5, 2.0, 50.0])), 0.98, seed, search)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_fit_random_sweep(sl, orc, seed):
+    # the fitted model over random shapes: 1 to 200 requests (register or window kernels),
+    # both policies, member times below or above 2^32
+    rng = np.random.default_rng(6000 + seed)
+    n = int(rng.integers(1, 201))
+    B = int(rng.integers(1, 33))
+    policy = int(rng.choice([0, 2]))
+    scale = int(rng.choice([1, 1, 64]))
+    _reg_fit_sweep_case(sl, orc, rng, n, B, policy, scale, seed)
+
+
+def _reg_fit_sweep_case(sl, orc, rng, n, B, policy, scale, seed):
+    import torch
+    from paper_2504_14966_amd.workloads import TABLE2_10NS
+    q = random_queue(rng, n, max_in=2000, max_out=300, thr_hi=2_000_000_000)
+    q.kind[::5] = 3
+    thr2 = (rng.integers(1_500_000, 1_800_000, n) * scale).astype(np.uint32)
+    coef = {k: v * scale for k, v in TABLE2_10NS.items()}
+    fd, fo = sl.FitModel(B, policy, **coef), orc.FitModel(B, policy, **coef)
+    dq = sl.DeviceQueue.from_queue(q)
+    chains, iters = 4, 120
+    ws = sl.sched_anneal_fit(dq, fd, chains, iters, 1.0, 0.98, seed, tpot_thr=sl.thr_to_device(thr2))
+    rec, cur, best = sl.sched_chains(ws, n, chains, perms=True)
+    cs, bs, _ = sl.sched_starts(ws, n, chains)
+    torch.cuda.synchronize()
+    rec, cur, best, cs, bs = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best), cs.cpu().numpy(), bs.cpu().numpy()
+    info = orc.start_fit(q, fo, None, thr2)
+    for c in range(chains):
+        w = orc.anneal_chain_fit(q, fo, c, iters, 1.0, 0.98, seed, thr2=thr2, start_info=info)
+        assert rec[c].tolist() == w["rec"].tolist(), c
+        assert cur[c].tolist() == w["cur"].tolist() and best[c].tolist() == w["best"].tolist(), c
+        assert cs[c].tolist() == w["cur_starts"].tolist() and bs[c].tolist() == w["best_starts"].tolist(), c
