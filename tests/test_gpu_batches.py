@@ -250,3 +250,40 @@ def test_eval_batches_wide_timeline(sl, orc, n, B):
     starts = random_layouts(rng, k, n, B)
     starts[0] = orc.max_starts(n, B)
     assert np.array_equal(_eval(sl, q, m, perms, starts), orc.eval_rows_batches(q, m, perms, starts))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_eval_random_sweep(sl, orc, seed):
+    # both evaluation calls over random shapes and the three width regimes: narrow timeline,
+    # narrow pair costs with a timeline above 2^32, and 64-bit pair costs
+    rng = np.random.default_rng(7000 + seed)
+    regime = int(rng.integers(0, 3))
+    n = int(rng.integers(1, 1025 if regime < 2 else 201))
+    B = int(rng.integers(1, 65))
+    if regime == 0:
+        q = random_queue(rng, n, max_in=3000, max_out=200)
+        kw = dict(p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    elif regime == 1:
+        q = random_queue(rng, n, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+        kw = dict(p0=5_000_000, p1=100, d0=16_000_000 // max(1, min(n, B) // 16 + 1), d1=1000, d2=3)
+    else:
+        q = random_queue(rng, n, max_in=3000, max_out=200, thr_hi=4_000_000_000)
+        kw = dict(p0=2000, p1=40, d0=8000, d1=300, d2=9000)
+    # the library's int64 bound (every prefill, then per decode step a full batch of the
+    # longest contexts; the sum over requests and the objective's scale below 2^62)
+    b = min(n, B)
+    step = kw["d0"] + kw["d1"] * b + kw["d2"] * b * (int(q.in_len.max()) + int(q.out_len.max()))
+    clock = sum(kw["p0"] + kw["p1"] * int(x) for x in q.in_len) + int(q.out_len.astype(np.int64).sum()) * step
+    assert clock * n * (n + 2) < 2**62
+    k = 8 if n > 256 else 16
+    perms = np.stack([rng.permutation(n) for _ in range(k)]).astype(np.uint16)
+    # fixed batches through sched_eval
+    m0 = Model(B, 0, **kw)
+    dq = sl.DeviceQueue.from_queue(q)
+    out = sl.sched_eval(dq, m0, sl.perms_to_device(perms)).cpu().numpy()
+    for r in range(k):
+        assert out[r].tolist() == list(orc.replay(q, m0, perms[r])[:2]), (r, n, B, regime)
+    # explicit layouts through sched_eval_batches
+    m2 = Model(B, SEARCH, **kw)
+    starts = random_layouts(rng, k, n, B)
+    assert np.array_equal(_eval(sl, q, m2, perms, starts), orc.eval_rows_batches(q, m2, perms, starts))
