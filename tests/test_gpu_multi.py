@@ -188,3 +188,19 @@ def test_multi_workload_sampled(sl, orc):
     inst = _assign(sl, W.queue, cap)
     assert np.array_equal(inst, orc.assign(W.queue, I, cap))
     _check_instances(sl, orc, W.queue, W.model, inst, I, W.chains, 400, W.T0, W.alpha, W.seed, None, (0, 511))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_anneal_multi_random_sweep(sl, orc, seed):
+    # random instance counts and capacities: instances of one to three positions per lane
+    # (up to 192 requests), or the delta kernels above, in one launch; both objectives
+    rng = np.random.default_rng(8000 + seed)
+    I = int(rng.integers(1, 7))
+    n = int(rng.integers(I, 500))
+    B = int(rng.choice([1, 2, 4, 8, 16, 16, 16, 24]))
+    q = random_queue(rng, n, max_in=1500, max_out=60, thr_hi=900_000)
+    m = Model(B, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+    caps = [int(x) for x in rng.integers(2000, 60000, I)]
+    inst = orc.assign(q, I, caps)
+    search = None if rng.random() < 0.5 else (1, int(rng.integers(1, 20)), int(rng.integers(0, 2)))
+    _check_instances(sl, orc, q, m, inst, I, 6, 150, 0.8, 0.99, seed, search, range(0, 6, 2))
