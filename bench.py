@@ -171,6 +171,7 @@ def time_anneal(sl, W, steps, warmup, torch):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kern_ms = [a.elapsed_time(b) for a, b in ev]
+    time_anneal.last_ws = ws
     return wall, kern_ms, key.cpu().tolist()
 
 
@@ -199,29 +200,65 @@ def _oracle_job(args):
     W = workload(wl)
     info = oracle.start(W.queue, W.model)
     t = time.perf_counter()
+    recs = {}
     for c in chains:
-        oracle.anneal_chain(W.queue, W.model, c, iters, W.T0, W.alpha, W.seed, start_info=info)
-    return time.perf_counter() - t
+        r = oracle.anneal_chain(W.queue, W.model, c, iters, W.T0, W.alpha, W.seed, start_info=info)
+        recs[c] = (r["rec"], r["cur"], r["best"])
+    return time.perf_counter() - t, recs
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# One GPU's share of the host: at most this many worker processes, whatever the affinity
+# mask shows (the host's cores are shared among the GPUs of the node).
+MAX_CPU_WORKERS = 16
 
 
 def cpu_baseline(wl: int, chains_per_core: int, iters: int):
+    """The oracle on a bounded sample of the workload (chains_per_core whole chains per worker
+    process); returns the baseline record and the oracle's per-chain results."""
     import multiprocessing as mp
     import oracle
     oracle.build(force=False)
     try:
-        cores = len(os.sched_getaffinity(0))
+        affinity = len(os.sched_getaffinity(0))
     except AttributeError:
-        cores = os.cpu_count() or 1
-    cores = max(1, min(cores, 16))
+        affinity = os.cpu_count() or 1
+    cores = max(1, min(affinity, MAX_CPU_WORKERS))
     jobs = [(wl, list(range(k * chains_per_core, (k + 1) * chains_per_core)), iters) for k in range(cores)]
     t = time.perf_counter()
     with mp.get_context("spawn").Pool(cores) as pool:
-        per = pool.map(_oracle_job, jobs)
+        res = pool.map(_oracle_job, jobs)
     wall = time.perf_counter() - t
+    per = [r[0] for r in res]
+    recs = {c: v for r in res for c, v in r[1].items()}
     total = cores * chains_per_core * iters
-    return dict(value=total / wall, unit="chain-iters/s", cores=cores, kind="oracle",
+    return dict(value=total / wall, unit="chain-iters/s", cores=cores, kind="oracle", affinity_cores=affinity,
+                cpu_model=cpu_model(), one_core=total / sum(per),
                 sample=f"workload {wl}: chains 0..{cores * chains_per_core - 1}, {iters} iterations each, "
-                       f"{cores} worker processes, {wall:.1f} s wall ({total / sum(per):.0f} chain-iters/s per core)")
+                       f"{cores} worker processes (of {affinity} cores in the affinity mask, at most "
+                       f"{MAX_CPU_WORKERS}: one GPU's share of the host), {wall:.1f} s wall "
+                       f"({total / sum(per):.0f} chain-iters/s per core)"), recs
+
+
+def compare_chains(sl, ws, n, chains, recs) -> dict:
+    """The GPU's per-chain records and orders of the timed run against the oracle's."""
+    import torch
+    rec, cur, best = sl.sched_chains(ws, n, chains, perms=True)
+    torch.cuda.synchronize()
+    rec, cur, best = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best)
+    bad = [c for c, (r, cu, be) in recs.items()
+           if not (np.array_equal(rec[c], r) and np.array_equal(cur[c], cu) and np.array_equal(best[c], be))]
+    return dict(chains_checked=len(recs), bit_exact=not bad, mismatched_chains=bad[:8])
 
 
 # Oracle samples per workload (chains x iterations, or evaluation rows), as planned for the
@@ -314,6 +351,7 @@ def main():
     W = workload(args.workload)
     log(f"[bench] workload {W.name}: {W.chains} chains x {W.iters} iters, warmup {args.warmup}, steps {args.steps}")
     wall, kern_ms, key = time_anneal(sl, W, args.steps, args.warmup, torch)
+    main_ws = time_anneal.last_ws
     ms_per_step = wall * 1000.0 / args.steps
     chain_iters = W.chains * W.iters
     value = chain_iters * args.steps / wall
@@ -495,14 +533,16 @@ def main():
     cpu = None
     if args.cpu_all:
         try:
-            ncores = max(1, min(len(os.sched_getaffinity(0)), 16))
+            ncores = max(1, min(len(os.sched_getaffinity(0)), MAX_CPU_WORKERS))
         except AttributeError:
-            ncores = max(1, min(os.cpu_count() or 1, 16))
+            ncores = max(1, min(os.cpu_count() or 1, MAX_CPU_WORKERS))
         extras["oracle_all_workloads"] = cpu_all(ncores)
     if not args.no_cpu:
         log("[bench] CPU oracle baseline ...")
-        cpu = cpu_baseline(args.workload, args.cpu_chains_per_core, W.iters)
-        log(f"[bench] oracle {cpu['value']:.4g} chain-iters/s on {cpu['cores']} cores")
+        cpu, recs = cpu_baseline(args.workload, args.cpu_chains_per_core, W.iters)
+        log(f"[bench] oracle {cpu['value']:.4g} chain-iters/s on {cpu['cores']} cores ({cpu['cpu_model']})")
+        cpu["parity"] = compare_chains(sl, main_ws, W.queue.n, W.chains, recs)
+        log(f"[bench] oracle chains against the timed run's GPU records: {cpu['parity']}")
 
     line = {
         "metric": "SA chain-iterations/s",

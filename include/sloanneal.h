@@ -296,6 +296,21 @@ int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint
 int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t *perms,
                     hipStream_t stream);
 
+/* The acceptance step of Algorithm 1 (Priority Mapping Algorithm section) as the annealing
+ * kernels evaluate it, on caller-given inputs: a test and observability readout, so that
+ * the single-precision screen in front of the double-precision rule can be compared with a
+ * reference decision by decision. All arrays DEVICE, k elements:
+ *   rule 0 : a = delta, b = t_ref (>= 1); keep iff delta >= 0 or
+ *            w3 * 2^-32 < exp(delta / (t_ref * T)) (the rule of sched_anneal);
+ *   rule 1 : a = num, b = t_ref, c = t, d = t' (t, t' >= 1); keep iff num >= 0 or
+ *            w3 * 2^-32 < exp((num * t_ref) / ((t * t') * T)) (SCHED_OBJ_RATIO);
+ *   c, d   : used by rule 1 only (nullable for rule 0); T > 0;
+ *   out    : bit 0 = kept; bit 1 = decided by the single-precision screen (else the
+ *            double-precision rule decided, or the candidate was not worse).
+ * SCHED_EINVAL for another rule, k < 0 or a null array that the rule reads. */
+int sched_accept_check(int32_t rule, int64_t k, const int64_t *a, const int64_t *b, const uint64_t *c,
+                       const uint64_t *d, const double *T, const uint32_t *w3, uint8_t *out, hipStream_t stream);
+
 /* Static message for a SCHED_* code; for SCHED_EHIP the last HIP error seen by this thread. */
 const char *sched_strerror(int code);
 

@@ -98,6 +98,8 @@ def lib():
         L.orc_better.restype = C.c_int
         L.orc_accept_ratio.argtypes = [i64, i64, i64, i64, dbl, u32]
         L.orc_accept_ratio.restype = C.c_int
+        L.orc_accept_many.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_accept_many.restype = None
         L.orc_levels.argtypes = [dbl, dbl, dbl]
         L.orc_levels.restype = i32
         L.orc_start_ex.argtypes = [vp, vp, vp, vp, vp, vp, vp]
@@ -248,6 +250,22 @@ def better_key(k1, k2, search: Search | None = None) -> bool:
 
 def accept_ratio(num: int, t_ref: int, t: int, t2: int, T: float, w3: int) -> bool:
     return bool(lib().orc_accept_ratio(int(num), int(t_ref), int(t), int(t2), float(T), int(w3)))
+
+
+def accept_many(rule: int, a, b, T, w3, c=None, d=None) -> np.ndarray:
+    """Acceptance decisions over arrays: rule 0 is accept(a, b, T, w3) (delta, t_ref), rule 1
+    accept_ratio(a, b, c, d, T, w3) (num, t_ref, t, t'); uint8 0 / 1 per element."""
+    a = np.ascontiguousarray(a, dtype=np.int64)
+    k = a.shape[0]
+    b = np.ascontiguousarray(b, dtype=np.int64)
+    c = np.ascontiguousarray(np.zeros(k) if c is None else c, dtype=np.int64)
+    d = np.ascontiguousarray(np.zeros(k) if d is None else d, dtype=np.int64)
+    T = np.ascontiguousarray(T, dtype=np.float64)
+    w3 = np.ascontiguousarray(w3, dtype=np.uint32)
+    assert b.shape == c.shape == d.shape == T.shape == w3.shape == (k,)
+    out = np.zeros(k, np.uint8)
+    lib().orc_accept_many(int(rule), int(k), _p(a), _p(b), _p(c), _p(d), _p(T), _p(w3), _p(out))
+    return out
 
 
 def levels(T0: float, T_thres: float, tau: float) -> int:

@@ -119,6 +119,11 @@ int orc_better(const orc_search *s, int64_t n1, int64_t t1, int64_t n2, int64_t 
  * or u < exp(x), x = ((double)num * t_ref) / (((double)t * t') * T), u = w3 * 2^-32. */
 int orc_accept_ratio(int64_t num, int64_t t_ref, int64_t t, int64_t t2, double T, uint32_t w3);
 
+/* orc_accept (rule 0: a = delta, b = t_ref) or orc_accept_ratio (rule 1: a = num, b = t_ref,
+ * c = t, d = t') for each of k elements; out[r] = 1 if accepted else 0. */
+void orc_accept_many(int32_t rule, int64_t k, const int64_t *a, const int64_t *b, const int64_t *c,
+                     const int64_t *d, const double *T, const uint32_t *w3, uint8_t *out);
+
 /* Temperature levels of Algorithm 1: T = T0, then T *= tau after each level, until T <
  * T_thres (the first level always runs). Pinned: T0 500, T_thres 20, tau 0.95 -> 63. */
 int32_t orc_levels(double T0, double T_thres, double tau);

@@ -93,6 +93,16 @@ int orc_accept_ratio(int64_t num, int64_t t_ref, int64_t t, int64_t t2, double T
   return u < orc_det_exp(x);
 }
 
+/* The two acceptance rules over arrays (rule 0: orc_accept(a, b, T, w3); rule 1:
+ * orc_accept_ratio(a, b, c, d, T, w3)), one decision per element. */
+void orc_accept_many(int32_t rule, int64_t k, const int64_t *a, const int64_t *b, const int64_t *c,
+                     const int64_t *d, const double *T, const uint32_t *w3, uint8_t *out) {
+  for (int64_t r = 0; r < k; r++) {
+    out[r] = (uint8_t)(rule == 1 ? orc_accept_ratio(a[r], b[r], c[r], d[r], T[r], w3[r])
+                                 : orc_accept(a[r], b[r], T[r], w3[r]));
+  }
+}
+
 int32_t orc_levels(double T0, double T_thres, double tau) {
   int32_t levels = 0;
   double T = T0;

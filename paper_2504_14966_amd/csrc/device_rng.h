@@ -83,20 +83,26 @@ __device__ __forceinline__ double fast_exp_neg(double x) {
 // and denominators outside [1e-30, 1e30] take the double-precision rule itself. The
 // screen needs xl > lu + 2^-10 >= -32 to accept, far above the -708 cutoff of
 // fast_exp_neg, so its acceptances never fall where E = 0.
-__device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
-  if (delta >= 0) return true;
+// Returns the decision in bit 0 and, in bit 1, whether the single-precision screen took it
+// (0: not worse, or the double-precision rule decided).
+__device__ __forceinline__ int metropolis_rule(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
+  if (delta >= 0) return 1;
   const double den = (double)t_ref * T;
   if (w3 != 0u && den > 1e-30 && den < 1e30) {
     const float xl = (float)delta * __builtin_amdgcn_rcpf((float)den) * 1.44269504f;
     const float lu = __builtin_amdgcn_logf((float)w3) - 32.0f;
     const float g = xl - lu;
     const float tau = fabsf(xl) * 1.52587890625e-5f + 9.765625e-4f;
-    if (g > tau) return true;
-    if (g < -tau) return false;
+    if (g > tau) return 3;
+    if (g < -tau) return 2;
   }
   const double x = (double)delta / den;
   const double u = (double)w3 * (1.0 / 4294967296.0);
-  return u < fast_exp_neg(x);
+  return u < fast_exp_neg(x) ? 1 : 0;
+}
+
+__device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double T, uint32_t w3) {
+  return (metropolis_rule(delta, t_ref, T, w3) & 1) != 0;
 }
 
 // Metropolis rule for the ratio objective G = n / t, with energy G * t_ref: a candidate
@@ -104,10 +110,11 @@ __device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double 
 // int64: the host bounds n * t below 2^63). Keep it iff num >= 0, or u < e^x with
 // x = (num * t_ref) / ((t * t') * T) formed by three double operations in that order. The
 // single-precision screen is the one above with the same error budget: (float) of the
-// numerator and of the denominator, a 1-ulp reciprocal and two products.
-__device__ __forceinline__ bool metropolis_ratio(int64_t num, int64_t t_ref, uint64_t t, uint64_t t2, double T,
-                                                 uint32_t w3) {
-  if (num >= 0) return true;
+// numerator and of the denominator, a 1-ulp reciprocal and two products. Bits as for
+// metropolis_rule.
+__device__ __forceinline__ int metropolis_ratio_rule(int64_t num, int64_t t_ref, uint64_t t, uint64_t t2, double T,
+                                                     uint32_t w3) {
+  if (num >= 0) return 1;
   const double a = (double)num * (double)t_ref;
   const double den = ((double)t * (double)t2) * T;
   if (w3 != 0u && den > 1e-30 && den < 1e30 && a > -1e30) {
@@ -115,12 +122,17 @@ __device__ __forceinline__ bool metropolis_ratio(int64_t num, int64_t t_ref, uin
     const float lu = __builtin_amdgcn_logf((float)w3) - 32.0f;
     const float g = xl - lu;
     const float tau = fabsf(xl) * 1.52587890625e-5f + 9.765625e-4f;
-    if (g > tau) return true;
-    if (g < -tau) return false;
+    if (g > tau) return 3;
+    if (g < -tau) return 2;
   }
   const double x = a / den;
   const double u = (double)w3 * (1.0 / 4294967296.0);
-  return u < fast_exp_neg(x);
+  return u < fast_exp_neg(x) ? 1 : 0;
+}
+
+__device__ __forceinline__ bool metropolis_ratio(int64_t num, int64_t t_ref, uint64_t t, uint64_t t2, double T,
+                                                 uint32_t w3) {
+  return (metropolis_ratio_rule(num, t_ref, t, t2, T, w3) & 1) != 0;
 }
 
 // Objective OBJ (0: attainment, then total latency; 1: ratio n / t): strict improvement.

@@ -515,4 +515,21 @@ __global__ void __launch_bounds__(256) shuffle_kernel(uint32_t key0, uint32_t ke
   }
 }
 
+// The acceptance rule of the annealing kernels on given inputs, one element per thread:
+// rule 0 is metropolis(a, b, T, w3), rule 1 metropolis_ratio(a, b, c, d, T, w3); out holds
+// the decision in bit 0 and whether the single-precision screen took it in bit 1.
+__global__ void __launch_bounds__(256) accept_check_kernel(int rule, int64_t k, const int64_t *__restrict__ a,
+                                                           const int64_t *__restrict__ b,
+                                                           const uint64_t *__restrict__ c,
+                                                           const uint64_t *__restrict__ d,
+                                                           const double *__restrict__ T,
+                                                           const uint32_t *__restrict__ w3, uint8_t *__restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; r < k; r += stride) {
+    const int v = rule == 1 ? metropolis_ratio_rule(a[r], b[r], c[r], d[r], T[r], w3[r])
+                            : metropolis_rule(a[r], b[r], T[r], w3[r]);
+    out[r] = (uint8_t)v;
+  }
+}
+
 }  // namespace sa

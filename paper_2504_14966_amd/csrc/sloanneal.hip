@@ -989,6 +989,17 @@ int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, c
   return SCHED_OK;
 }
 
+int sched_accept_check(int32_t rule, int64_t k, const int64_t *a, const int64_t *b, const uint64_t *c,
+                       const uint64_t *d, const double *T, const uint32_t *w3, uint8_t *out, hipStream_t stream) {
+  if ((rule != 0 && rule != 1) || k < 0) return SCHED_EINVAL;
+  if (k == 0) return SCHED_OK;
+  if (!a || !b || !T || !w3 || !out || (rule == 1 && (!c || !d))) return SCHED_EINVAL;
+  const int grid = (int)std::min<int64_t>((k + 255) / 256, 4096);
+  sa::accept_check_kernel<<<grid, 256, 0, stream>>>(rule, k, a, b, c, d, T, w3, out);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
 int32_t sched_levels(double T0, double T_thres, double tau) {
   if (!(T0 > 0.0) || !std::isfinite(T0) || !(T_thres > 0.0) || !std::isfinite(T_thres) || !(tau > 0.0) ||
       !(tau < 1.0))

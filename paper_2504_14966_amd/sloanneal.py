@@ -20,7 +20,7 @@ SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, 
 EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
            "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_assign",
            "sched_ws_bytes_multi", "sched_anneal_multi", "sched_multi_instance_ws", "sched_multi_best",
-           "sched_eval_fit", "sched_anneal_fit", "sched_strerror")
+           "sched_eval_fit", "sched_anneal_fit", "sched_accept_check", "sched_strerror")
 KIND_TTFT_TPOT = 3
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 OBJ_LEX, OBJ_RATIO = 0, 1
@@ -101,6 +101,8 @@ def load_library(path: str = LIB_PATH):
     L.sched_start_info.restype = C.c_int
     L.sched_gen_perms.argtypes = [u64, i32, i64, i64, vp, vp]
     L.sched_gen_perms.restype = C.c_int
+    L.sched_accept_check.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sched_accept_check.restype = C.c_int
     L.sched_strerror.argtypes = [C.c_int]
     L.sched_strerror.restype = C.c_char_p
     _lib = L
@@ -392,3 +394,14 @@ def sched_anneal_fit(dq: DeviceQueue, fit: FitModel, chains: int, iters: int, T0
                               int(chains), int(iters), float(T0), float(alpha), int(seed) & (2**64 - 1), _ptr(ws),
                               int(ws.numel()), _stream(stream)))
     return ws
+
+
+def sched_accept_check(rule: int, a: torch.Tensor, b: torch.Tensor, T: torch.Tensor, w3: torch.Tensor,
+                       c: torch.Tensor | None = None, d: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """The kernels' acceptance rule on given inputs (int64 a, b, c, d; float64 T; w3 as the
+    int32 bits of uint32): uint8 per element, bit 0 kept, bit 1 decided by the screen."""
+    k = int(a.numel())
+    out = torch.empty(k, dtype=torch.uint8, device=a.device)
+    _check(load_library().sched_accept_check(int(rule), k, _ptr(a), _ptr(b), _ptr(c), _ptr(d), _ptr(T), _ptr(w3),
+                                             _ptr(out), _stream(stream)))
+    return out

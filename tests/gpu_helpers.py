@@ -74,3 +74,19 @@ def oracle_rows_batches(q, m, perms: np.ndarray, starts: np.ndarray) -> np.ndarr
     with mp.get_context("spawn").Pool(len(parts)) as pool:
         out = pool.map(_rows_batches_job, [(q, m, p, s) for p, s in parts])
     return np.concatenate(out)
+
+
+def _fy_rows_job(args):
+    import hashlib
+    import oracle
+    q, m, seed, lo, hi = args
+    perms = oracle.fy_perms(seed, q.n, hi - lo, row0=lo)
+    return lo, hi, hashlib.sha256(np.ascontiguousarray(perms).tobytes()).hexdigest(), oracle.eval_rows(q, m, perms)
+
+
+def oracle_fy_rows(q, m, seed: int, rows: int, block: int = 1 << 15):
+    """Rows 0..rows-1 of the Fisher-Yates family, generated and scored by the oracle in worker
+    processes: a list of (lo, hi, sha256 of the orders' bytes, (n, t) per row)."""
+    jobs = [(q, m, seed, lo, min(rows, lo + block)) for lo in range(0, rows, block)]
+    with mp.get_context("spawn").Pool(min(workers(), len(jobs))) as pool:
+        return pool.map(_fy_rows_job, jobs)

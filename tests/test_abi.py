@@ -79,6 +79,10 @@ def test_host_side_rejections_without_gpu(lib):
     assert lib.sched_gen_perms(0, 0, 0, 1, 8, None) == sl.SCHED_EINVAL
     assert lib.sched_gen_perms(0, 8, -1, 1, 8, None) == sl.SCHED_EINVAL
     assert lib.sched_gen_perms(0, 8, 0, 0, None, None) == sl.SCHED_OK
+    assert lib.sched_accept_check(2, 1, 8, 8, None, None, 8, 8, 8, None) == sl.SCHED_EINVAL
+    assert lib.sched_accept_check(0, -1, 8, 8, None, None, 8, 8, 8, None) == sl.SCHED_EINVAL
+    assert lib.sched_accept_check(1, 1, 8, 8, None, None, 8, 8, 8, None) == sl.SCHED_EINVAL
+    assert lib.sched_accept_check(0, 0, None, None, None, None, None, None, None, None) == sl.SCHED_OK
 
 
 def test_product_path_has_no_oracle_dependency():

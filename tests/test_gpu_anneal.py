@@ -59,9 +59,11 @@ def _check(orc, res, q, m, sample, iters, T0, alpha, seed):
         assert orc.replay(q, m, res["best"][c]) == (r[c, 2], r[c, 3])
 
 
-def _sample(chains, extra=8, seed=0):
+def _sample(chains, extra=8, seed=0, first=8):
     rng = np.random.default_rng(seed)
-    s = set(range(min(chains, 8))) | {chains - 1} | set(rng.integers(0, chains, extra).tolist())
+    s = set(range(min(chains, first))) | {chains - 1}
+    rest = np.setdiff1d(np.arange(chains), sorted(s))
+    s |= set(rng.choice(rest, size=min(extra, rest.size), replace=False).tolist())
     return sorted(s)
 
 
@@ -73,22 +75,29 @@ def test_workload_1(sl, orc):
     assert res["key"][:2].tolist() == [bn, bt]
 
 
-def test_workload_2_full(sl, orc):
+def test_workload_2_every_chain(sl, orc):
+    """All 1024 chains of the 64-request workload, replayed one by one by the oracle."""
     W = workload(2)
     res = _run(sl, W.queue, W.model, W.chains, W.iters, W.T0, W.alpha, W.seed)
-    _check(orc, res, W.queue, W.model, _sample(W.chains), W.iters, W.T0, W.alpha, W.seed)
+    _check(orc, res, W.queue, W.model, list(range(W.chains)), W.iters, W.T0, W.alpha, W.seed)
 
 
 def test_workload_3_full(sl, orc):
+    """Chains 0..63, the last chain and 64 seeded-random ones of the continuous workload."""
     W = workload(3)
     res = _run(sl, W.queue, W.model, W.chains, W.iters, W.T0, W.alpha, W.seed)
-    _check(orc, res, W.queue, W.model, _sample(W.chains, extra=5), W.iters, W.T0, W.alpha, W.seed)
+    sample = _sample(W.chains, extra=64, seed=3, first=64)
+    assert len(sample) == 129
+    _check(orc, res, W.queue, W.model, sample, W.iters, W.T0, W.alpha, W.seed)
 
 
 def test_workload_4_full(sl, orc):
+    """Chains 0..63, the last chain and 64 seeded-random ones of the burst workload."""
     W = workload(4)
     res = _run(sl, W.queue, W.model, W.chains, W.iters, W.T0, W.alpha, W.seed)
-    _check(orc, res, W.queue, W.model, _sample(W.chains, extra=6), W.iters, W.T0, W.alpha, W.seed)
+    sample = _sample(W.chains, extra=64, seed=4, first=64)
+    assert len(sample) == 129
+    _check(orc, res, W.queue, W.model, sample, W.iters, W.T0, W.alpha, W.seed)
 
 
 @pytest.mark.parametrize("n,B,policy,thr", [(1, 1, 0, 1 << 31), (2, 3, 1, 1 << 31), (9, 3, 0, 0), (9, 3, 1, 1 << 32),
