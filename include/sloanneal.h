@@ -260,6 +260,25 @@ void *sched_multi_instance_ws(void *ws, int32_t n, int32_t instances, int32_t ch
 int sched_multi_best(const void *ws, int32_t instances, uint16_t *orders, int64_t *keys, int32_t *counts,
                      hipStream_t stream);
 
+/* ---- no device allocation ----
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): sched_anneal followed by sched_best, with
+ * the annealing workspace in a fixed scratch array that the library holds on every GPU it
+ * runs on (SCHED_NOALLOC_MAX_BYTES per GPU, kept until the process ends) instead of a
+ * caller's workspace. The call allocates nothing. Every call on one GPU shares that GPU's
+ * scratch and leaves its contents there (nothing in it has to start at zero: each call
+ * writes what it later reads), so calls that overlap on one GPU race: serialise them, e.g.
+ * on one stream. The stream must belong to the current device.
+ *   perm_out : n uint16 (DEVICE), the best order over chains; key_out : 3 int64 (DEVICE) =
+ *              (n_met, t_sum, chain), as sched_best returns them.
+ * Arguments otherwise and errors as sched_anneal; SCHED_ENOSPC when sched_ws_bytes(n,
+ * chains) exceeds SCHED_NOALLOC_MAX_BYTES (it holds up to 5404 chains of 1024 requests,
+ * 20971 of 256 and 30840 of 128 or fewer). */
+#define SCHED_NOALLOC_MAX_BYTES (32u << 20)
+int sched_anneal_noalloc(const sched_queue_t *queue, const sched_model_t *model, int32_t chains, int32_t iters,
+                         double T0, double alpha, uint64_t seed, uint16_t *perm_out, int64_t *key_out,
+                         hipStream_t stream);
+
 /* Best order over all chains of the last sched_anneal on ws.
  *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain). */
 int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream);

@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -565,6 +566,33 @@ int launch_multi_static(const sched_model_t *model, const sa::DevModel &dm, int 
   return SCHED_OK;
 }
 
+// Fixed device scratch of sched_anneal_noalloc: the annealing workspace for callers that
+// cannot allocate. Each GPU the library runs on holds its own copy until the process ends.
+// Host code never passes the array's name to a kernel (on the host it is only a stand-in for
+// the symbol); it uses the device address obtained once per device below.
+static __device__ __align__(256) unsigned char scratch[SCHED_NOALLOC_MAX_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Address of the current device's copy of `scratch`, looked up on the first call on that
+// device with the device current.
+int scratch_address(void **out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return SCHED_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return SCHED_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SCHED_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -682,6 +710,21 @@ int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, cons
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
+}
+
+int sched_anneal_noalloc(const sched_queue_t *queue, const sched_model_t *model, int32_t chains, int32_t iters,
+                         double T0, double alpha, uint64_t seed, uint16_t *perm_out, int64_t *key_out,
+                         hipStream_t stream) {
+  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N || chains < 1) return SCHED_EINVAL;
+  if (!perm_out || !key_out) return SCHED_EINVAL;
+  if (sched_ws_bytes(queue->n, chains) > (size_t)SCHED_NOALLOC_MAX_BYTES) return SCHED_ENOSPC;
+  void *ws = nullptr;
+  int rc = scratch_address(&ws);
+  if (rc) return rc;
+  rc = sched_anneal_ex(queue, model, nullptr, chains, iters, T0, alpha, seed, ws, (size_t)SCHED_NOALLOC_MAX_BYTES,
+                       stream);
+  if (rc) return rc;
+  return sched_best(ws, perm_out, key_out, stream);
 }
 
 int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream) {
@@ -1017,7 +1060,9 @@ const char *sched_strerror(int code) {
   switch (code) {
     case SCHED_OK: return "ok";
     case SCHED_EINVAL: return "invalid argument, size, model parameter or queue entry";
-    case SCHED_ENOSPC: return "workspace smaller than sched_ws_bytes(n, chains)";
+    case SCHED_ENOSPC:
+      return "workspace smaller than sched_ws_bytes(n, chains) (for sched_anneal_noalloc: that size exceeds "
+             "SCHED_NOALLOC_MAX_BYTES)";
     case SCHED_ERANGE: return "queue and model could overflow the int64 clock or objective";
     case SCHED_EHIP: return g_hip_msg.empty() ? "HIP runtime error" : g_hip_msg.c_str();
     default: return "unknown error code";

@@ -20,7 +20,7 @@ SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, 
 EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
            "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_assign",
            "sched_ws_bytes_multi", "sched_anneal_multi", "sched_multi_instance_ws", "sched_multi_best",
-           "sched_eval_fit", "sched_anneal_fit", "sched_accept_check", "sched_strerror")
+           "sched_eval_fit", "sched_anneal_fit", "sched_accept_check", "sched_anneal_noalloc", "sched_strerror")
 KIND_TTFT_TPOT = 3
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 OBJ_LEX, OBJ_RATIO = 0, 1
@@ -101,6 +101,8 @@ def load_library(path: str = LIB_PATH):
     L.sched_start_info.restype = C.c_int
     L.sched_gen_perms.argtypes = [u64, i32, i64, i64, vp, vp]
     L.sched_gen_perms.restype = C.c_int
+    L.sched_anneal_noalloc.argtypes = [vp, vp, i32, i32, dbl, dbl, u64, vp, vp, vp]
+    L.sched_anneal_noalloc.restype = C.c_int
     L.sched_accept_check.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sched_accept_check.restype = C.c_int
     L.sched_strerror.argtypes = [C.c_int]
@@ -234,6 +236,20 @@ def sched_anneal(dq: DeviceQueue, model, chains: int, iters: int, T0: float, alp
         _check(L.sched_anneal_ex(C.byref(q), C.byref(m), C.byref(search), int(chains), int(iters), float(T0),
                                  float(alpha), int(seed) & (2**64 - 1), _ptr(ws), int(ws.numel()), _stream(stream)))
     return ws
+
+
+def sched_anneal_noalloc(dq: DeviceQueue, model, chains: int, iters: int, T0: float, alpha: float, seed: int,
+                         perm_out: torch.Tensor | None = None, key_out: torch.Tensor | None = None, stream=None):
+    """sched_anneal + sched_best in the library's fixed device scratch (the C call allocates
+    nothing; outputs are allocated here unless given): (best order n int16 bits, key 3 int64)."""
+    dev = dq.in_len.device
+    perm = perm_out if perm_out is not None else torch.empty(dq.n, dtype=torch.int16, device=dev)
+    key = key_out if key_out is not None else torch.empty(3, dtype=torch.int64, device=dev)
+    q, m = dq.c(), _model(model)
+    _check(load_library().sched_anneal_noalloc(C.byref(q), C.byref(m), int(chains), int(iters), float(T0),
+                                               float(alpha), int(seed) & (2**64 - 1), _ptr(perm), _ptr(key),
+                                               _stream(stream)))
+    return perm, key
 
 
 def sched_levels(T0: float, T_thres: float, tau: float) -> int:
