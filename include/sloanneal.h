@@ -6,10 +6,16 @@
  * Conventions for every entry point:
  *   - array arguments are DEVICE pointers unless stated otherwise; the caller owns them
  *     (e.g. torch tensors) and the library never frees or retains them;
- *   - work is enqueued on the caller's stream and runs asynchronously. sched_eval and
- *     sched_anneal first copy the n-entry request queue to the host and synchronise the
- *     stream once, to validate it and to choose integer widths; nothing else blocks;
- *   - every call returns SCHED_OK (0) or a negative SCHED_E* code and then enqueues nothing;
+ *   - work is enqueued on the caller's stream and runs asynchronously; no call blocks,
+ *     synchronises or reads device memory on the host, so calls may be enqueued behind
+ *     other work on the stream;
+ *   - every call checks its host arguments (sizes, pointers, model, settings) and returns
+ *     SCHED_OK (0) or a negative SCHED_E* code, enqueueing nothing on an error. The
+ *     contents of the device arrays (queue entries, instance indices, capacities) and the
+ *     int64 range they imply are checked on the device by the call's first kernel, which
+ *     also picks the integer widths and so the kernel that runs. A failure there makes the
+ *     call's outputs read as its documentation says (rows (-2, code), best key (-2, code,
+ *     -1), ...) with code SCHED_EINVAL or SCHED_ERANGE, and sched_status reports it;
  *   - the library keeps no global state: all annealing state lives in the caller's
  *     workspace, so calls on distinct workspaces and streams are independent;
  *   - latencies are int64 microseconds; results are bit-identical run to run.
@@ -86,8 +92,11 @@ typedef struct {
  *            (-1, -1)
  *   detail : nullable; k x n x 2 int64 (ttft, e2e) indexed by request id; rows that are
  *            not permutations are left untouched
- * Returns SCHED_EINVAL for k < 0, a null pointer, a bad queue or model, SCHED_ERANGE if
- * the clock could overflow. k == 0 is a no-op. */
+ * Returns SCHED_EINVAL for k < 0, a null pointer, a bad queue descriptor or model.
+ * Checked on the device: a queue entry out of range (l_out = 0, kind above SCHED_E2E,
+ * threshold above SCHED_THR_MAX) makes every row read (-2, SCHED_EINVAL), a queue and model
+ * that could overflow the int64 clock every row (-2, SCHED_ERANGE); detail is then left
+ * untouched. k == 0 is a no-op (the queue is not read). */
 int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
                int64_t k, int64_t *out, int64_t *detail, hipStream_t stream);
 
@@ -102,7 +111,7 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
  *            layout is not valid
  *   detail : nullable; k x n x 2 int64 (ttft, e2e) by request id; invalid rows untouched
  * model->policy must be SCHED_STATIC or SCHED_STATIC_SEARCH (SCHED_EINVAL otherwise);
- * other errors as for sched_eval. */
+ * other errors, and the device checks of the queue, as for sched_eval. */
 int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
                        const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail, hipStream_t stream);
 
@@ -132,7 +141,11 @@ size_t sched_ws_bytes(int32_t n, int32_t chains);
  * allowed changes nothing and counts as neither accepted nor rejected (no digest step).
  * Layouts are read back with sched_starts.
  * Returns SCHED_EINVAL for chains < 1, iters < 0, T0 <= 0, alpha <= 0 or non-finite,
- * a bad queue or model; SCHED_ENOSPC for a short workspace; SCHED_ERANGE on overflow risk. */
+ * a bad queue descriptor or model; SCHED_ENOSPC for a short workspace. Checked on the
+ * device: a queue entry out of range (SCHED_EINVAL) or overflow risk of the int64 clock
+ * (SCHED_ERANGE) ends the call after its first kernel; sched_status then reads the code,
+ * sched_best's key (-2, code, -1), sched_chains' records (-2, code, -1, ...) and
+ * sched_start_info's info (-2, code, -1, -1), and the orders in ws are not written. */
 int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t chains,
                  int32_t iters, double T0, double alpha, uint64_t seed, void *ws, size_t ws_bytes,
                  hipStream_t stream);
@@ -158,8 +171,8 @@ typedef struct {
 /* sched_anneal with search settings (search == NULL: {SCHED_OBJ_LEX, 1, 0, 0}, which is
  * sched_anneal). The paper's schedule (T0 500, T_thres 20, tau 0.95, iter 100) is
  * T0 = 500, alpha = 0.95, level_len = 100, iters = 100 * sched_levels(500, 20, 0.95).
- * Errors as sched_anneal, and SCHED_EINVAL for bad settings; SCHED_ERANGE when the ratio's
- * int64 cross products could overflow. */
+ * Errors as sched_anneal, and SCHED_EINVAL for bad settings; on the device SCHED_ERANGE
+ * also when the ratio's int64 cross products could overflow. */
 int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
                     int32_t chains, int32_t iters, double T0, double alpha, uint64_t seed, void *ws,
                     size_t ws_bytes, hipStream_t stream);
@@ -195,11 +208,12 @@ enum { SCHED_TTFT_TPOT = 3 };
 
 /* sched_eval / sched_eval_batches under the fitted model.
  *   tpot_thr : nullable DEVICE n x uint32, the TPOT thresholds of SCHED_TTFT_TPOT requests
- *              (SCHED_EINVAL for a queue with that kind when it is null)
+ *              (a queue with that kind fails the device check, SCHED_EINVAL, when it is null)
  *   starts   : nullable DEVICE k x n uint8 batch layouts (as for sched_eval_batches); null =
  *              maximum-size batches
- * Other arguments, outputs and errors as for sched_eval_batches; SCHED_ERANGE when the
- * latencies could overflow int64. */
+ * Other arguments, outputs and errors as for sched_eval_batches (the device check of the
+ * kinds accepts SCHED_TTFT_TPOT when tpot_thr is given; SCHED_ERANGE when the latencies
+ * could overflow int64). */
 int sched_eval_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
                    const uint16_t *perms, const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail,
                    hipStream_t stream);
@@ -224,8 +238,9 @@ int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, c
  *   capacity : DEVICE, instances x int64 tokens per instance (token_num(m) = m * mu / sigma,
  *              computed by the caller), each 1 .. 2^48
  *   inst_out : DEVICE, n x int32, the instance of every request
- * SCHED_EINVAL for instances outside 1 .. SCHED_MAX_INSTANCES, null pointers, a bad queue
- * or a capacity out of range. */
+ * SCHED_EINVAL for instances outside 1 .. SCHED_MAX_INSTANCES, null pointers or a bad queue
+ * descriptor. Checked on the device: a queue entry or a capacity out of range makes every
+ * entry of inst_out read SCHED_EINVAL. */
 int sched_assign(const sched_queue_t *queue, int32_t instances, const int64_t *capacity, int32_t *inst_out,
                  hipStream_t stream);
 
@@ -242,7 +257,10 @@ size_t sched_ws_bytes_multi(int32_t n, int32_t instances, int32_t chains);
  *   ws      : DEVICE, at least sched_ws_bytes_multi(n, instances, chains) bytes, 256-aligned
  * Instance k's chains are read with sched_best / sched_chains / sched_start_info on
  * sched_multi_instance_ws(ws, ...k); their orders index the instance's own queue. An
- * instance with no request runs nothing. Errors as sched_anneal_ex. */
+ * instance with no request runs nothing. Errors as sched_anneal_ex; the device checks also
+ * reject an inst_of entry outside 0 .. instances - 1 (SCHED_EINVAL), and after a failed
+ * check sched_status(ws) reads the code, sched_multi_best's keys (-2, code, -1) with counts
+ * 0 and orders untouched, and each instance workspace reads as a failed sched_anneal's. */
 int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
                        const int32_t *inst_of, int32_t instances, int32_t chains, int32_t iters, double T0,
                        double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream);
@@ -256,7 +274,9 @@ void *sched_multi_instance_ws(void *ws, int32_t n, int32_t instances, int32_t ch
  *            instance 1's, ...
  *   keys   : DEVICE nullable, instances x 3 int64 (n_met, t_sum, chain); (-1, -1, -1) for an
  *            instance without requests
- *   counts : DEVICE nullable, instances x int32 requests per instance */
+ *   counts : DEVICE nullable, instances x int32 requests per instance
+ * (Scheduling Solution section: the per-instance results of Algorithm 2's priority
+ * mapping.) */
 int sched_multi_best(const void *ws, int32_t instances, uint16_t *orders, int64_t *keys, int32_t *counts,
                      hipStream_t stream);
 
@@ -279,8 +299,12 @@ int sched_anneal_noalloc(const sched_queue_t *queue, const sched_model_t *model,
                          double T0, double alpha, uint64_t seed, uint16_t *perm_out, int64_t *key_out,
                          hipStream_t stream);
 
-/* Best order over all chains of the last sched_anneal on ws.
- *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain). */
+/* Best order over all chains of the last sched_anneal on ws: the priority order Algorithm 1
+ * returns (Priority Mapping Algorithm section), taken as the best of every chain's
+ * best-so-far order (attainment first, then lower total latency; lowest chain id on ties).
+ *   perm_out : n uint16 (DEVICE); key_out : 3 int64 (DEVICE) = (n_met, t_sum, chain); after
+ *   a call whose device checks failed the key reads (-2, code, -1) and perm_out is left
+ *   untouched. */
 int sched_best(const void *ws, uint16_t *perm_out, int64_t *key_out, hipStream_t stream);
 
 /* Per-chain readout of the last sched_anneal on ws (observability and parity checks).
@@ -329,6 +353,14 @@ int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t 
  * SCHED_EINVAL for another rule, k < 0 or a null array that the rule reads. */
 int sched_accept_check(int32_t rule, int64_t k, const int64_t *a, const int64_t *b, const uint64_t *c,
                        const uint64_t *d, const double *T, const uint32_t *w3, uint8_t *out, hipStream_t stream);
+
+/* The device checks' verdict of the last annealing call on ws (a sched_anneal* workspace, a
+ * sched_anneal_multi workspace or an instance workspace inside one): an observability
+ * readout for the asynchronous calls.
+ *   out : 3 int64 (DEVICE) = (status: SCHED_OK, SCHED_EINVAL or SCHED_ERANGE; the integer
+ *         widths that hold for the queue, a bit set; the index of the kernel that ran among
+ *         the call's candidates, -1 when the checks failed). */
+int sched_status(const void *ws, int64_t *out, hipStream_t stream);
 
 /* Static message for a SCHED_* code; for SCHED_EHIP the last HIP error seen by this thread. */
 const char *sched_strerror(int code);

@@ -239,6 +239,7 @@ template <int LG, int OBJ>
 __global__ void __launch_bounds__(256) anneal_reg_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
                                                           double alpha, uint32_t key0, uint32_t key1,
                                                           uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
@@ -509,6 +510,7 @@ template <int LG, int OBJ>
 __global__ void __launch_bounds__(256) anneal_reg_h_kernel(DevModel m, QueuePtrs q, int chains, int iters, double T0,
                                                             double alpha, uint32_t key0, uint32_t key1,
                                                             uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
@@ -779,6 +781,7 @@ template <int OBJ>
 __global__ void __launch_bounds__(256) anneal_reg_sized_kernel(DevModel m, QueuePtrs q, int chains, int iters,
                                                                 double T0, double alpha, uint32_t key0, uint32_t key1,
                                                                 SearchParams srch, unsigned char *ws) {
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;
@@ -978,6 +981,7 @@ __global__ void __launch_bounds__(256) anneal_reg_fit_kernel(DevFit f, QueuePtrs
                                                               int iters, double T0, double alpha, uint32_t key0,
                                                               uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                               unsigned char *ws) {
+  if (!fit_gate_open(ws, f)) return;
   const int waves = blockDim.x >> 6;
   const int chain = uniform((int)blockIdx.x * waves + (int)(threadIdx.x >> 6));
   if (chain >= chains) return;

@@ -321,6 +321,7 @@ __global__ void __launch_bounds__(256) eval_sized_kernel(DevModel m, QueuePtrs q
                                                           const uint8_t *__restrict__ starts, int64_t rows,
                                                           int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!eval_gate(q, m, rows, out)) return;
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
@@ -469,6 +470,7 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
                                                                     uint32_t key1, SearchParams srch,
                                                                     unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n, B = m.B;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
@@ -750,6 +752,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
                                                              int iters, double T0, double alpha, uint32_t key0,
                                                              uint32_t key1, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n, B = m.B;
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);

@@ -37,6 +37,7 @@
 #pragma once
 #include "device_common.h"
 #include "device_cont.h"
+#include "device_plan.h"
 #include "device_replay.h"
 #include "device_rng.h"
 
@@ -646,6 +647,7 @@ __global__ void __launch_bounds__(1024) anneal_static_kernel(DevModel m, StaticP
                                                               uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                               unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n;
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
@@ -675,6 +677,7 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
                                                            const uint16_t *__restrict__ perms, int64_t rows,
                                                            int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!eval_gate(q, m, rows, out)) return;
   constexpr int Bp = 1 << LG, G = kWave >> LG;
   const int n = m.n, B = m.B;
   const int M = (n + B - 1) / B, R = (M + G - 1) / G;

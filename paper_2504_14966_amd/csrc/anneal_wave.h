@@ -462,6 +462,7 @@ __global__ void __launch_bounds__(1024) anneal_wave_kernel(DevModel m, StaticPar
                                                             uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                             unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n;
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);

@@ -8,13 +8,28 @@ namespace sa {
 
 constexpr int kWave = 64;
 
+// The kernels one call may run, in order of preference: the first candidate whose needed
+// flags the device-side checks of the queue set is the one that runs (the last needs none);
+// every other launch returns at once. `allow` are the check flags this launch may use.
+struct Gate {
+  uint32_t need[4];
+  int32_t count;  // candidates (1 .. 4)
+  int32_t self;   // this launch's candidate index
+  uint32_t allow;
+  uint32_t pad;
+};
+
 // Integer latency model plus sizes, passed by value to every kernel.
 struct DevModel {
   int32_t n;       // requests
   int32_t B;       // max batch
   int32_t policy;  // 0 static, 1 continuous, 2 static with searched batch sizes
-  int32_t flags;   // bit 0: continuous-admission event arithmetic fits 32 bits
+  int32_t flags;   // kFlag* widths below (the host's, plus the device checks' allowed by the gate)
   uint64_t p0, p1, d0, d1, d2;
+  int64_t t_ref;     // the caller's Metropolis scale (0: total latency of the input order)
+  int32_t max_kind;  // largest SLO kind accepted
+  int32_t ratio;     // 1: the ratio objective (its cross products must fit int64)
+  Gate gate;
 };
 
 // One request packed into 16 bytes for a single ds_read_b128 gather:
@@ -41,7 +56,10 @@ struct WsHeader {
   int64_t best_chain, best_n, best_t;
   int64_t max_batch;
   int64_t objective, level_len, early_exit;
-  int64_t reserved[16];
+  // written by the device-side checks of the queue before anything else of a call runs:
+  // 0 or a negative SCHED_E* code, the width flags, the candidate kernel that runs (-1: none)
+  int64_t plan_status, plan_flags, plan_selected;
+  int64_t reserved[13];
 };
 static_assert(sizeof(WsHeader) <= 256, "header fits its slot");
 // Search settings of Algorithm 1: objective 0 = attainment, then total latency; 1 = the
@@ -57,6 +75,10 @@ constexpr int kFlagNarrowTime = 4;     // list scheduling: every time on the tim
 constexpr int kFlagWindows = 8;        // explicit batches: every time below 2^57 (windowed replay)
 constexpr int kFlagStaticNarrow = 16;  // static batches of any layout: 24-bit pair costs, 32-bit offsets
 constexpr int kFlagTime32 = 32;        // static batches of any layout: every time on the timeline fits 32 bits
+constexpr int kFlagFitWindows = 64;    // fitted model: the timeline (and every member's time) below 2^57
+constexpr int kFlagFitMember32 = 128;  // fitted model: every member's time, in any batch, below 2^32 - 1
+constexpr int kFlagInst64 = 256;       // several instances: each holds at most 64 requests
+constexpr int kFlagInst192 = 512;      // several instances: each holds at most 192 requests
 constexpr uint64_t kWsMagic = 0x534c4f414e4e3031ull;  // "SLOANN01"
 
 __host__ __device__ __forceinline__ size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }

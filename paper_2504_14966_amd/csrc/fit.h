@@ -26,7 +26,44 @@ struct DevFit {
   uint32_t win;  // 1: every member's time is below 2^57 (the windowed replay's keys fit)
   uint32_t m32;  // 1: every member's time, in any batch, is below 2^32 - 1
   uint64_t bmagic;     // floor(2^32 / B) + 1: lane / B = (lane * bmagic) >> 32 for lanes below 64
+  // for the device checks of the queue, which set win and m32 where the gate allows them
+  int64_t t_ref;     // the caller's Metropolis scale (0: total latency of the input order)
+  int32_t max_kind;  // largest SLO kind accepted (3 with the second threshold array)
+  int32_t ratio;     // 1: the ratio objective
+  Gate gate;
 };
+
+// The device checks under the fitted model, formed by the whole workgroup.
+__device__ __forceinline__ Plan fit_plan_in_block(const QueuePtrs &q, const DevFit &f) {
+  const FitCoef c{f.ap, f.bp, f.cp, f.dp, f.ad, f.bd, f.cd, f.dd};
+  const QueueStats s = block_queue_stats(q, f.n, f.B, f.max_kind, &c);
+  Plan p = plan_decide(s, f.n, f.B, f.ratio, f.t_ref, 0, 0, 0, 0, 0, &c, f.gate);
+  if (p.status == 0) p.selected = plan_select(f.gate, p.flags);
+  return p;
+}
+__device__ __forceinline__ void fit_take_flags(DevFit &f, uint32_t flags) {
+  const uint32_t a = flags & f.gate.allow;
+  f.win = (a & kFlagFitWindows) ? 1u : 0u;
+  f.m32 = (a & kFlagFitMember32) ? 1u : 0u;
+}
+// As gate_open, for the fitted-model kernels.
+__device__ __forceinline__ bool fit_gate_open(const unsigned char *ws, DevFit &f) {
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  if (h->plan_selected != (int64_t)f.gate.self) return false;
+  fit_take_flags(f, (uint32_t)h->plan_flags);
+  return true;
+}
+// As eval_gate, for the fitted-model evaluation.
+__device__ __forceinline__ bool eval_fit_gate(const QueuePtrs &q, DevFit &f, int64_t rows, int64_t *out) {
+  const Plan p = fit_plan_in_block(q, f);
+  if (p.status != 0) {
+    if (f.gate.self == f.gate.count - 1) error_rows(rows, p.status, out);
+    return false;
+  }
+  if (p.selected != f.gate.self) return false;
+  fit_take_flags(f, p.flags);
+  return true;
+}
 
 // Request record: x = l_in | l_out << 16, y = threshold, z = kind, w = second threshold.
 __device__ __forceinline__ void load_fit_requests(const QueuePtrs &q, const uint32_t *thr2, int n, uint4 *req) {
@@ -237,6 +274,7 @@ __global__ void __launch_bounds__(256) eval_fit_kernel(DevFit f, QueuePtrs q, co
                                                         const uint8_t *__restrict__ starts, int64_t rows,
                                                         int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!eval_fit_gate(q, f, rows, out)) return;
   const int n = f.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
@@ -286,8 +324,9 @@ __global__ void __launch_bounds__(256) eval_fit_kernel(DevFit f, QueuePtrs q, co
   }
 }
 
-// Algorithm 1 initialisation under the fitted model, one workgroup of 1024 threads: every
-// request's latency alone (b = 1), a stable bitonic sort by (latency, id), the scores of the
+// Algorithm 1 initialisation under the fitted model, one workgroup of 1024 threads, after
+// the device checks of the queue (verdict to the header; a failed check ends the call):
+// every request's latency alone (b = 1), a stable bitonic sort by (latency, id), the scores of the
 // sorted and the input orders with maximum-size batches, t_ref.
 __global__ void __launch_bounds__(1024) start_fit_kernel(DevFit f, QueuePtrs q, const uint32_t *thr2, int chains,
                                                           int iters, int64_t t_ref_user, SearchParams srch,
@@ -296,6 +335,13 @@ __global__ void __launch_bounds__(1024) start_fit_kernel(DevFit f, QueuePtrs q, 
   __shared__ uint64_t key_solo[1024];
   __shared__ uint16_t key_id[1024];
   __shared__ uint16_t ident[1024];
+  const Plan plan = fit_plan_in_block(q, f);
+  if (plan.status != 0) {
+    if (threadIdx.x == 0) write_failed_header(ws, plan, f.n, chains, iters, f.policy, f.B);
+    return;
+  }
+  if (threadIdx.x == 0) write_plan(ws, plan);
+  fit_take_flags(f, plan.flags);
   const int n = f.n;
   const int tid = threadIdx.x;
   load_fit_requests(q, thr2, n, req);
@@ -372,6 +418,7 @@ __global__ void __launch_bounds__(256) anneal_fit_kernel(DevFit f, QueuePtrs q, 
                                                           uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                           unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!fit_gate_open(ws, f)) return;
   const int n = f.n, B = f.B;
   const bool search = f.policy == 2;
   uint4 *req = reinterpret_cast<uint4 *>(lds);

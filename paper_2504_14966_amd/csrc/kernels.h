@@ -11,6 +11,7 @@
 //   small copy kernels for the readouts and the Fisher-Yates family.
 #pragma once
 #include "device_common.h"
+#include "device_plan.h"
 #include "device_replay.h"
 #include "device_rng.h"
 #include "device_cont.h"
@@ -45,10 +46,14 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
                                                        int64_t rows, int64_t *__restrict__ out,
                                                        int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!eval_gate(q, m, rows, out)) return;
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const bool ls = m.policy == 1 && (m.flags & kFlagListSched);
-  const size_t per_wave = lds_align((size_t)n * 2) + 64 * 16 + 32 * 4 + (ls ? lds_align(cont_ls_scratch_bytes(n)) : 0);
+  // continuous admission always leaves room for the list-scheduling scratch (the host sizes
+  // the LDS by the policy; whether the list scheduling runs is the device check's)
+  const size_t per_wave =
+      lds_align((size_t)n * 2) + 64 * 16 + 32 * 4 + (m.policy == 1 ? lds_align(cont_ls_scratch_bytes(n)) : 0);
   const int wave = uniform((int)(threadIdx.x >> 6));
   unsigned char *wbase = lds + lds_align((size_t)n * 16) + (size_t)wave * per_wave;
   uint16_t *perm = reinterpret_cast<uint16_t *>(wbase);
@@ -178,8 +183,17 @@ __device__ void start_body(const DevModel &m, const QueuePtrs &q, int chains, in
   }
 }
 
+// The first kernel of a single-queue annealing call: the device checks of the queue (their
+// verdict goes to the header; a failed check ends the call here), then the start order.
 __global__ void __launch_bounds__(1024) start_kernel(DevModel m, QueuePtrs q, int chains, int iters,
                                                       int64_t t_ref_user, SearchParams srch, unsigned char *ws) {
+  const Plan p = plan_in_block(q, m);
+  if (p.status != 0) {
+    if (threadIdx.x == 0) write_failed_header(ws, p, m.n, chains, iters, m.policy, m.B);
+    return;
+  }
+  if (threadIdx.x == 0) write_plan(ws, p);
+  m.flags |= (int32_t)(p.flags & m.gate.allow);
   start_body(m, q, chains, iters, t_ref_user, srch, ws);
 }
 
@@ -266,6 +280,7 @@ __global__ void __launch_bounds__(kBlock) anneal_kernel(DevModel m, QueuePtrs q,
                                                          double alpha, uint32_t key0, uint32_t key1,
                                                          uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t per_wave = lds_align((size_t)n * 2) * 2 + 64 * 16;
@@ -288,6 +303,7 @@ __global__ void __launch_bounds__(1024) anneal_cont_kernel(DevModel m, QueuePtrs
                                                             double alpha, uint32_t key0, uint32_t key1,
                                                             uint64_t swap_thr, SearchParams srch, unsigned char *ws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(ws, m.gate, m.flags)) return;
   const int n = m.n;
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
@@ -449,10 +465,23 @@ __device__ void reduce_body(unsigned char *ws) {
   }
 }
 
-__global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) { reduce_body(ws); }
+__global__ void __launch_bounds__(1024) reduce_kernel(unsigned char *ws) {
+  if (!plan_ok(ws)) return;
+  reduce_body(ws);
+}
 
+// After a call whose queue failed the device checks the key reads (-2, code, -1) and the
+// order is left as it is.
 __global__ void __launch_bounds__(256) best_copy_kernel(const unsigned char *ws, uint16_t *perm_out, int64_t *key_out) {
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  if (h->plan_status != 0) {
+    if (threadIdx.x == 0) {
+      key_out[0] = -2;
+      key_out[1] = h->plan_status;
+      key_out[2] = -1;
+    }
+    return;
+  }
   const int n = h->n, chains = h->chains;
   const int64_t c = h->best_chain;
   const uint16_t *src = reinterpret_cast<const uint16_t *>(ws + ws_off_best(n, chains)) + (size_t)c * ws_perm_stride(n);
@@ -464,10 +493,21 @@ __global__ void __launch_bounds__(256) best_copy_kernel(const unsigned char *ws,
   }
 }
 
+// After a call whose queue failed the device checks every record reads (-2, code, -1, ...)
+// and the orders are left as they are.
 __global__ void __launch_bounds__(256) chains_copy_kernel(const unsigned char *ws, int64_t *per_chain, uint16_t *cur_out,
                                                            uint16_t *best_out) {
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
   const int n = h->n, chains = h->chains;
+  if (h->plan_status != 0) {
+    const int64_t status = h->plan_status;
+    for (int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; u < (int64_t)chains * 8;
+         u += (int64_t)gridDim.x * blockDim.x) {
+      const int w = (int)(u & 7);
+      per_chain[u] = w == 0 ? -2 : (w == 1 ? status : -1);
+    }
+    return;
+  }
   const size_t stride = ws_perm_stride(n);
   const int64_t *rec = reinterpret_cast<const int64_t *>(ws + ws_off_records(n));
   const uint16_t *cur = reinterpret_cast<const uint16_t *>(ws + ws_off_cur(n, chains));
@@ -483,9 +523,20 @@ __global__ void __launch_bounds__(256) chains_copy_kernel(const unsigned char *w
   }
 }
 
+// After a call whose queue failed the device checks info reads (-2, code, -1, -1) and the
+// order is left as it is.
 __global__ void __launch_bounds__(256) start_copy_kernel(const unsigned char *ws, uint16_t *start_out, int64_t *info) {
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
   const int n = h->n;
+  if (h->plan_status != 0) {
+    if (threadIdx.x == 0) {
+      info[0] = -2;
+      info[1] = h->plan_status;
+      info[2] = -1;
+      info[3] = -1;
+    }
+    return;
+  }
   const uint16_t *src = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
   for (int p = threadIdx.x; p < n; p += blockDim.x) start_out[p] = src[p];
   if (threadIdx.x == 0) {
@@ -494,6 +545,15 @@ __global__ void __launch_bounds__(256) start_copy_kernel(const unsigned char *ws
     info[2] = h->start_t;
     info[3] = h->allmet;
   }
+}
+
+// The device checks' verdict of the last call on a workspace (single-queue or several
+// instances: the fields sit at the same offsets): status, width flags, selected kernel.
+__global__ void status_copy_kernel(const unsigned char *ws, int64_t *out) {
+  const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
+  out[0] = h->plan_status;
+  out[1] = h->plan_flags;
+  out[2] = h->plan_selected;
 }
 
 // One thread per row: Durstenfeld's in-place Fisher-Yates, drawing from Philox.

@@ -34,9 +34,16 @@ struct MultiHeader {
   uint64_t magic;
   int32_t n, instances, chains, pad;
   int64_t slot_bytes;
-  int64_t reserved[28];
+  int64_t reserved0[10];
+  // the device checks' verdict, at the offsets a single-queue header keeps it
+  int64_t plan_status, plan_flags, plan_selected;
+  int64_t reserved[15];
 };
 static_assert(sizeof(MultiHeader) <= 256, "header fits its slot");
+static_assert(offsetof(MultiHeader, plan_status) == offsetof(WsHeader, plan_status) &&
+                  offsetof(MultiHeader, plan_flags) == offsetof(WsHeader, plan_flags) &&
+                  offsetof(MultiHeader, plan_selected) == offsetof(WsHeader, plan_selected),
+              "the verdict sits where the single-queue readers look");
 
 __host__ __device__ __forceinline__ size_t mws_queue_bytes(int n) {
   const size_t a = round_up((size_t)n * 2, 256), b = round_up((size_t)n, 256), c = round_up((size_t)n * 4, 256);
@@ -80,9 +87,9 @@ constexpr int64_t kAssignNarrowCap = int64_t(1) << 25;
 // and lane i of the new list is the median of list[i], list[i + 1] and that key (one DPP
 // shift and one v_med3_u32). A reset restores the initial sorted list. Request sizes are
 // loaded 64 at a time and the instances written 64 at a time.
-__global__ void __launch_bounds__(64) assign_sorted_kernel(QueuePtrs q, int n, int instances,
-                                                            const int64_t *__restrict__ capacity,
-                                                            int32_t *__restrict__ inst_out) {
+__device__ __forceinline__ void assign_sorted_body(const QueuePtrs &q, int n, int instances,
+                                                   const int64_t *__restrict__ capacity,
+                                                   int32_t *__restrict__ inst_out) {
   __shared__ uint32_t srt[64];
   const int lane = lane_id();
   const bool live = lane < instances;
@@ -120,8 +127,8 @@ __global__ void __launch_bounds__(64) assign_sorted_kernel(QueuePtrs q, int n, i
 }
 
 // One wave: instance of every request, 64-bit remaining tokens (any capacity).
-__global__ void __launch_bounds__(64) assign_kernel(QueuePtrs q, int n, int instances,
-                                                     const int64_t *__restrict__ capacity, int32_t *__restrict__ inst_out) {
+__device__ __forceinline__ void assign_wide_body(const QueuePtrs &q, int n, int instances,
+                                                 const int64_t *__restrict__ capacity, int32_t *__restrict__ inst_out) {
   const int lane = lane_id();
   const bool live = lane < instances;
   const int64_t cap = live ? capacity[lane] : INT64_MIN;
@@ -155,10 +162,87 @@ __global__ void __launch_bounds__(64) assign_kernel(QueuePtrs q, int n, int inst
   }
 }
 
+// One wave: the checks of the assignment (every queue entry as for the other calls, every
+// capacity within 1 .. 2^48; on failure every entry of inst_out reads SCHED_EINVAL), then
+// the sorted-key body when every capacity is below kAssignNarrowCap, else the 64-bit one.
+__global__ void __launch_bounds__(64) assign_kernel(QueuePtrs q, int n, int instances,
+                                                     const int64_t *__restrict__ capacity, int32_t *__restrict__ inst_out) {
+  const int lane = lane_id();
+  bool bad = false, wide = false;
+  for (int r = lane; r < n; r += kWave)
+    bad |= q.out_len[r] < 1u || q.kind[r] > 2u || q.thr[r] > kThrMax;
+  if (lane < instances) {
+    const int64_t c = capacity[lane];
+    bad |= c < 1 || c > (int64_t(1) << 48);
+    wide = c >= kAssignNarrowCap;
+  }
+  if (__ballot(bad) != 0ull) {
+    for (int r = lane; r < n; r += kWave) inst_out[r] = kPlanEInval;
+    return;
+  }
+  if (__ballot(wide) == 0ull)
+    assign_sorted_body(q, n, instances, capacity, inst_out);
+  else
+    assign_wide_body(q, n, instances, capacity, inst_out);
+}
+
+// One workgroup of 1024 threads: the device checks of a several-instance call -- every queue
+// entry, every instance index within 0 .. instances - 1, the int64 range and widths of the
+// whole queue (each instance's queue is part of it, so its bounds hold there too) and each
+// instance's request count (at most 64 or 192 requests: the register kernels) -- and the
+// multi-instance header; every slot's header gets the verdict too, so that the single-queue
+// readouts on a slot see it.
+__global__ void __launch_bounds__(1024) multi_plan_kernel(DevModel m, QueuePtrs q, const int32_t *__restrict__ inst_of,
+                                                           int instances, int chains, int iters, int64_t slot_bytes,
+                                                           unsigned char *mws) {
+  __shared__ int cnt[64];
+  __shared__ uint32_t bad_inst;
+  const int n = m.n;
+  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
+  if (threadIdx.x == 0) bad_inst = 0u;
+  __syncthreads();
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    const int32_t k = inst_of[r];
+    if (k < 0 || k >= instances)
+      atomicOr(&bad_inst, 1u);
+    else
+      atomicAdd(&cnt[k], 1);
+  }
+  QueueStats s = block_queue_stats(q, n, m.B, m.max_kind, nullptr);  // its barrier orders the counts
+  s.bad |= bad_inst;
+  int nk_max = 0;
+  for (int k = 0; k < instances; ++k) nk_max = max(nk_max, cnt[k]);
+  Plan p = plan_decide(s, n, m.B, m.ratio, m.t_ref, m.p0, m.p1, m.d0, m.d1, m.d2, nullptr, m.gate);
+  if (p.status == 0) {
+    if (nk_max <= 64) p.flags |= kFlagInst64;
+    if (nk_max <= 192) p.flags |= kFlagInst192;
+    p.selected = plan_select(m.gate, p.flags);
+  }
+  if (threadIdx.x == 0) {
+    MultiHeader *mh = reinterpret_cast<MultiHeader *>(mws);
+    mh->magic = kMultiMagic;
+    mh->n = n;
+    mh->instances = instances;
+    mh->chains = chains;
+    mh->slot_bytes = slot_bytes;
+    mh->plan_status = p.status;
+    mh->plan_flags = p.flags;
+    mh->plan_selected = p.selected;
+  }
+  if ((int)threadIdx.x < instances) {
+    unsigned char *slot = mws + mws_off_slot(n, instances, chains, (int)threadIdx.x);
+    if (p.status != 0)
+      write_failed_header(slot, p, 0, chains, iters, m.policy, m.B);
+    else
+      write_plan(slot, p);
+  }
+}
+
 // One workgroup of 1024 threads per instance: the instance's requests in arrival order.
 __global__ void __launch_bounds__(1024) gather_kernel(QueuePtrs q, int n, const int32_t *__restrict__ inst_of, int chains,
                                                        int instances, unsigned char *mws) {
   __shared__ int wave_cnt[16];
+  if (!plan_ok(mws)) return;
   const int k = blockIdx.x;
   const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
   const bool mine = tid < n && inst_of[tid] == k;
@@ -190,6 +274,7 @@ __device__ __forceinline__ int slot_n(const unsigned char *mws, int k) {
 // One workgroup per instance: its start order and workspace header.
 __global__ void __launch_bounds__(1024) multi_start_kernel(DevModel m, int n, int instances, int chains, int iters,
                                                             int64_t t_ref_user, SearchParams srch, unsigned char *mws) {
+  if (!gate_status(mws, m.gate, m.flags)) return;
   const int k = blockIdx.x;
   const int nk = slot_n(mws, k);
   unsigned char *slot = mws + mws_off_slot(n, instances, chains, k);
@@ -229,6 +314,7 @@ __global__ void __launch_bounds__(kBlock) multi_anneal_kernel(DevModel m, int n,
                                                                uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                                unsigned char *mws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(mws, m.gate, m.flags)) return;
   const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
   const int nk = slot_n(mws, k);
   if (nk == 0) return;
@@ -258,6 +344,7 @@ __global__ void __launch_bounds__(1024) multi_static_kernel(DevModel m, StaticPa
                                                              double alpha, uint32_t key0, uint32_t key1,
                                                              uint64_t swap_thr, SearchParams srch, unsigned char *mws) {
   extern __shared__ __align__(16) unsigned char lds[];
+  if (!gate_open(mws, m.gate, m.flags)) return;
   const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
   const int nk = slot_n(mws, k);
   if (nk == 0) return;
@@ -290,6 +377,7 @@ __global__ void __launch_bounds__(256) multi_reg_kernel(DevModel m, int n, int i
                                                          int iters, double T0, double alpha, uint32_t key0,
                                                          uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                          unsigned char *mws) {
+  if (!gate_open(mws, m.gate, m.flags)) return;
   const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
   const int nk = slot_n(mws, k);
   if (nk == 0) return;
@@ -316,6 +404,7 @@ __global__ void __launch_bounds__(256) multi_reg_h_kernel(DevModel m, int n, int
                                                            int iters, double T0, double alpha, uint32_t key0,
                                                            uint32_t key1, uint64_t swap_thr, SearchParams srch,
                                                            unsigned char *mws) {
+  if (!gate_open(mws, m.gate, m.flags)) return;
   const int k = blockIdx.x / groups, g = blockIdx.x - k * groups;
   const int nk = slot_n(mws, k);
   if (nk == 0) return;
@@ -332,6 +421,7 @@ __global__ void __launch_bounds__(256) multi_reg_h_kernel(DevModel m, int n, int
 
 // One workgroup per instance: its winner over chains.
 __global__ void __launch_bounds__(1024) multi_reduce_kernel(int n, int instances, int chains, unsigned char *mws) {
+  if (!plan_ok(mws)) return;
   const int k = blockIdx.x;
   if (slot_n(mws, k) == 0) return;
   reduce_body(mws + mws_off_slot(n, instances, chains, k));
@@ -344,6 +434,17 @@ __global__ void __launch_bounds__(256) multi_best_kernel(const unsigned char *mw
   const MultiHeader *mh = reinterpret_cast<const MultiHeader *>(mws);
   const int n = mh->n, instances = mh->instances, chains = mh->chains;
   const int k = blockIdx.x;
+  if (mh->plan_status != 0) {  // the queue failed the checks: (-2, code, -1), no requests
+    if (threadIdx.x == 0) {
+      if (keys) {
+        keys[3 * k] = -2;
+        keys[3 * k + 1] = mh->plan_status;
+        keys[3 * k + 2] = -1;
+      }
+      if (counts) counts[k] = 0;
+    }
+    return;
+  }
   int off = 0;
   for (int j = 0; j < k; ++j) off += slot_n(mws, j);
   const int nk = slot_n(mws, k);
@@ -364,15 +465,6 @@ __global__ void __launch_bounds__(256) multi_best_kernel(const unsigned char *mw
     }
     if (counts) counts[k] = nk;
   }
-}
-
-__global__ void multi_header_kernel(unsigned char *mws, int n, int instances, int chains, int64_t slot_bytes) {
-  MultiHeader *mh = reinterpret_cast<MultiHeader *>(mws);
-  mh->magic = kMultiMagic;
-  mh->n = n;
-  mh->instances = instances;
-  mh->chains = chains;
-  mh->slot_bytes = slot_bytes;
 }
 
 }  // namespace sa

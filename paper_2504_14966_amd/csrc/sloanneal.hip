@@ -1,11 +1,14 @@
-// C-ABI of the annealing library (declared in include/sloanneal.h): argument and queue
-// validation, int64 range pre-checks, workspace sizing and kernel launches on the caller's
-// stream.
+// C-ABI of the annealing library (declared in include/sloanneal.h): argument checks, workspace
+// sizing and kernel launches on the caller's stream. Nothing blocks: the queue's contents are
+// checked on the device by each call's first kernel (entries, the int64 range, the integer
+// widths that pick the kernel), and every candidate kernel of a call is enqueued behind it,
+// of which only the selected one runs.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <functional>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -34,12 +37,6 @@ int hip_fail(hipError_t e) {
     if (_e != hipSuccess) return hip_fail(_e); \
   } while (0)
 
-struct HostQueue {
-  std::vector<uint16_t> in_len, out_len;
-  std::vector<uint8_t> kind;
-  std::vector<uint32_t> thr;
-};
-
 int check_model(const sched_model_t *m, int n) {
   if (!m) return SCHED_EINVAL;
   if (m->max_batch < 1 || m->max_batch > SCHED_MAX_BATCH) return SCHED_EINVAL;
@@ -50,58 +47,29 @@ int check_model(const sched_model_t *m, int n) {
   return SCHED_OK;
 }
 
-// Reads the queue back (one stream synchronisation) and validates every entry (kinds up to
-// max_kind).
-int fetch_queue(const sched_queue_t *q, hipStream_t stream, HostQueue &h, int max_kind = 2) {
+int check_search(const sched_search_t *search, sa::SearchParams &srch) {
+  srch = sa::SearchParams{SCHED_OBJ_LEX, 1, 0, 0};
+  if (!search) return SCHED_OK;
+  if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
+      (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
+    return SCHED_EINVAL;
+  srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
+  return SCHED_OK;
+}
+int check_chain_args(int32_t chains, int32_t iters, double T0, double alpha) {
+  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
+    return SCHED_EINVAL;
+  return SCHED_OK;
+}
+
+// Host-side checks of a queue descriptor (its contents are checked on the device).
+int check_queue(const sched_queue_t *q) {
   if (!q || q->n < 1 || q->n > SCHED_MAX_N) return SCHED_EINVAL;
   if (!q->in_len || !q->out_len || !q->kind || !q->thr_us) return SCHED_EINVAL;
-  const size_t n = (size_t)q->n;
-  h.in_len.resize(n);
-  h.out_len.resize(n);
-  h.kind.resize(n);
-  h.thr.resize(n);
-  HIP_TRY(hipMemcpyAsync(h.in_len.data(), q->in_len, n * 2, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipMemcpyAsync(h.out_len.data(), q->out_len, n * 2, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipMemcpyAsync(h.kind.data(), q->kind, n, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipMemcpyAsync(h.thr.data(), q->thr_us, n * 4, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipStreamSynchronize(stream));
-  for (size_t r = 0; r < n; ++r) {
-    if (h.out_len[r] < 1 || h.kind[r] > max_kind || h.thr[r] > SCHED_THR_MAX) return SCHED_EINVAL;
-  }
   return SCHED_OK;
 }
 
-// Worst-case clock: every request's prefill plus, per request, its decode iterations at
-// the largest possible step cost. The sum over requests and the Metropolis delta
-// (|dn| <= n times t_ref) must stay below 2^62.
-// Bound on the timeline of any order and any batch layout: every prefill, plus per decode
-// step (at most the sum of output lengths) the cost of a full batch of the longest contexts.
-long double timeline_bound(const HostQueue &h, const sched_model_t *m, int n) {
-  long double max_lin = 0, max_lout = 0, sum_lout = 0, pre = 0;
-  for (int r = 0; r < n; ++r) {
-    max_lin = std::max<long double>(max_lin, h.in_len[r]);
-    max_lout = std::max<long double>(max_lout, h.out_len[r]);
-    sum_lout += h.out_len[r];
-    pre += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
-  }
-  const long double b = std::min(n, m->max_batch);
-  const long double step = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * b * (max_lin + max_lout);
-  return pre + sum_lout * step;
-}
-
-int range_check(const HostQueue &h, const sched_model_t *m, int n) {
-  const long double lim = std::ldexp(1.0L, 62);
-  const long double clock = timeline_bound(h, m, n);
-  const long double tsum = clock * n;
-  const long double tref = m->t_ref_us > 0 ? (long double)m->t_ref_us : tsum;
-  if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
-  return SCHED_OK;
-}
-
-// The fitted model: every coefficient >= 0, batches of 1 .. 64. A member's time is largest
-// at the largest batch, and a batch lasts at most the sum of its members' times, so the
-// timeline ends before the sum over requests of their time in a batch of min(n, B); the sum
-// of latencies, the Metropolis delta and (for the ratio) the cross products stay below 2^62.
+// The fitted model: every coefficient >= 0, batches of 1 .. 64.
 int check_fit(const sched_fit_model_t *f) {
   if (!f || f->max_batch < 1 || f->max_batch > SCHED_MAX_BATCH) return SCHED_EINVAL;
   if (f->policy != SCHED_STATIC && f->policy != SCHED_STATIC_SEARCH) return SCHED_EINVAL;
@@ -111,123 +79,85 @@ int check_fit(const sched_fit_model_t *f) {
   return SCHED_OK;
 }
 
-// Sum over requests of their time in a batch of min(n, B): a member's time grows with its
-// batch size, and a batch lasts at most the sum of its members' times, so this bounds the
-// timeline and every member's time.
-long double fit_timeline_bound(const HostQueue &h, const sched_fit_model_t *f, int n) {
-  const long double b = std::min(n, f->max_batch);
-  long double end = 0;
-  for (int r = 0; r < n; ++r) {
-    const long double l = h.in_len[r], L = h.out_len[r];
-    end += (long double)f->ap * b * l + (long double)f->bp * b + (long double)f->cp * l + (long double)f->dp +
-           L * ((long double)f->bd * b + (long double)f->dd) +
-           ((long double)f->ad * b + (long double)f->cd) * (L * l + L * (L + 1) / 2);
+// Width flags each kernel may take from the device checks (the device adds the ones that
+// hold for the queue): single-queue annealing, evaluation and several instances.
+constexpr uint32_t kAnnealFlags = sa::kFlagNarrowPrefill | sa::kFlagListSched | sa::kFlagNarrowTime | sa::kFlagWindows;
+constexpr uint32_t kEvalFlags = sa::kFlagNarrowPrefill | sa::kFlagListSched | sa::kFlagNarrowTime;
+constexpr uint32_t kMultiFlags = kEvalFlags;
+constexpr uint32_t kSN = sa::kFlagStaticNarrow, kT32 = sa::kFlagTime32;
+
+// The kernels one call may run, in order of preference, each with the width flags it needs
+// and the ones it may use. All of them are enqueued; on the device each reads the verdict of
+// the checks and only the first whose needs hold runs (the last needs none, so exactly one
+// runs when the queue passes the checks, none when it fails them).
+template <class M>
+struct Candidates {
+  sa::Gate gate{};
+  uint32_t allow[4] = {0u, 0u, 0u, 0u};
+  std::function<hipError_t(const M &)> launch[4];
+  void add(uint32_t need, uint32_t allow_flags, std::function<hipError_t(const M &)> fn) {
+    if (gate.count >= 4) return;  // at most three per call by construction
+    gate.need[gate.count] = need;
+    allow[gate.count] = allow_flags;
+    launch[gate.count] = std::move(fn);
+    ++gate.count;
   }
-  return end;
-}
-
-int fit_range_check(const HostQueue &h, const sched_fit_model_t *f, int n, bool ratio) {
-  const long double end = fit_timeline_bound(h, f, n);
-  const long double tsum = end * n, lim = std::ldexp(1.0L, 62);
-  const long double tref = f->t_ref > 0 ? (long double)f->t_ref : tsum;
-  if (!(tsum < lim) || !(tref * (n + 1) + tsum < lim)) return SCHED_ERANGE;
-  if (ratio && !(tsum * (n + 1) < lim)) return SCHED_ERANGE;
-  return SCHED_OK;
-}
-
-// The largest time of one request in any batch (times grow with the batch size).
-long double fit_member_bound(const HostQueue &h, const sched_fit_model_t *f, int n) {
-  const long double b = std::min(n, f->max_batch);
-  long double mx = 0;
-  for (int r = 0; r < n; ++r) {
-    const long double l = h.in_len[r], L = h.out_len[r];
-    mx = std::max(mx, (long double)f->ap * b * l + (long double)f->bp * b + (long double)f->cp * l +
-                          (long double)f->dp + L * ((long double)f->bd * b + (long double)f->dd) +
-                          ((long double)f->ad * b + (long double)f->cd) * (L * l + L * (L + 1) / 2));
+  // The model of the kernel that runs the checks: every candidate's needs, its own flags.
+  M checker(M m, uint32_t allow_flags) const {
+    m.gate = gate;
+    m.gate.self = -1;
+    m.gate.allow = allow_flags;
+    return m;
   }
-  return mx;
-}
-
-// win: the windowed replay's keys hold every member's time (below 2^57 with margin);
-// m32: every member's time fits 32 bits
-sa::DevFit dev_fit(const sched_fit_model_t *f, int n, bool win, bool m32 = false) {
-  return sa::DevFit{n, f->max_batch, f->policy, 0, (uint64_t)f->ap, (uint64_t)f->bp, (uint64_t)f->cp,
-                    (uint64_t)f->dp, (uint64_t)f->ad, (uint64_t)f->bd, (uint64_t)f->cd, (uint64_t)f->dd,
-                    win ? 1u : 0u, m32 ? 1u : 0u, (1ull << 32) / (uint64_t)f->max_batch + 1};
-}
-
-// The ratio objective compares n1 t2 with n2 t1 and forms n' t - n t' in int64: the
-// worst-case total latency times (n + 1) stays below 2^62.
-int ratio_range_check(const HostQueue &h, const sched_model_t *m, int n) {
-  long double max_lin = 0, max_lout = 0, sum_lout = 0, pre = 0;
-  for (int r = 0; r < n; ++r) {
-    max_lin = std::max<long double>(max_lin, h.in_len[r]);
-    max_lout = std::max<long double>(max_lout, h.out_len[r]);
-    sum_lout += h.out_len[r];
-    pre += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
+  int run(const M &m) const {
+    if (gate.count < 1 || gate.need[gate.count - 1] != 0u) return SCHED_EINVAL;
+    for (int c = 0; c < gate.count; ++c) {
+      M mc = checker(m, allow[c]);
+      mc.gate.self = c;
+      const hipError_t e = launch[c](mc);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+    return SCHED_OK;
   }
-  const long double b = std::min(n, m->max_batch);
-  const long double step = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * b * (max_lin + max_lout);
-  const long double tsum = (pre + sum_lout * step) * n;
-  return tsum * (n + 1) < std::ldexp(1.0L, 62) ? SCHED_OK : SCHED_ERANGE;
-}
+};
 
-// The continuous event loop's 32-bit arithmetic: group prefill sums, the context sum C of
-// the running requests, d0 + d1 b + d2 C and d2 b all stay below 2^32.
-bool prefill_narrow(const HostQueue &h, const sched_model_t *m, int n) {
-  long double lmax = 0, Lmax = 0;
-  for (int r = 0; r < n; ++r) {
-    lmax = std::max<long double>(lmax, h.in_len[r]);
-    Lmax = std::max<long double>(Lmax, h.out_len[r]);
-  }
-  const long double b = std::min(n, m->max_batch), two32 = 4294967296.0L;
-  const long double pf = (long double)m->p0 + (long double)m->p1 * lmax;
-  const long double cmax = b * (lmax + Lmax);
-  const long double x = (long double)m->d0 + (long double)m->d1 * b + (long double)m->d2 * cmax;
-  return pf * b < two32 && cmax < two32 && x < two32 && (long double)m->d2 * b < two32;
-}
-
-// List scheduling packs (finish step << 10 | position) into 32 bits and keeps prefix
-// sums of prefill costs in 32 bits: the total of all output lengths stays below 2^22 and
-// the total prefill below 2^32.
-bool list_sched_ok(const HostQueue &h, const sched_model_t *m, int n) {
-  long double lsum = 0, pfsum = 0;
-  for (int r = 0; r < n; ++r) {
-    lsum += h.out_len[r];
-    pfsum += (long double)m->p0 + (long double)m->p1 * h.in_len[r];
-  }
-  return n <= 1024 && lsum < 4194304.0L && pfsum < 4294967296.0L;
-}
-
-// Continuous admission: every time on the timeline is at most the sum of the prefills plus
-// the decode steps' costs, sum over steps of d0 + d1 b + d2 C. There are at most sum(l_out)
-// steps, the b terms add up to sum(l_out) and the C terms to sum(l_out l_in + l_out (l_out
-// + 1) / 2), whatever the order.
-bool timeline_narrow(const HostQueue &h, const sched_model_t *m, int n) {
-  long double pf = 0, L = 0, ctx = 0;
-  for (int r = 0; r < n; ++r) {
-    const long double lo = h.out_len[r], li = h.in_len[r];
-    pf += (long double)m->p0 + (long double)m->p1 * li;
-    L += lo;
-    ctx += lo * li + lo * (lo + 1) / 2;
-  }
-  return pf + ((long double)m->d0 + (long double)m->d1) * L + (long double)m->d2 * ctx < 4294967296.0L;
-}
-
-sa::DevModel dev_model(const sched_model_t *m, int n, bool narrow_prefill, bool list_sched = false,
-                       bool narrow_time = false, bool windows = false, bool static_narrow_w = false) {
-  sa::DevModel d;
+// max_kind: the largest SLO kind the call accepts; ratio: the ratio objective.
+sa::DevModel dev_model(const sched_model_t *m, int n, int max_kind = 2, int ratio = 0) {
+  sa::DevModel d{};
   d.n = n;
   d.B = m->max_batch;
   d.policy = m->policy;
-  d.flags = (narrow_prefill ? sa::kFlagNarrowPrefill : 0) | (narrow_prefill && list_sched ? sa::kFlagListSched : 0) |
-            (narrow_prefill && list_sched && narrow_time ? sa::kFlagNarrowTime : 0) | (windows ? sa::kFlagWindows : 0) |
-            (static_narrow_w ? sa::kFlagStaticNarrow : 0);
+  d.flags = 0;
   d.p0 = (uint64_t)m->p0;
   d.p1 = (uint64_t)m->p1;
   d.d0 = (uint64_t)m->d0;
   d.d1 = (uint64_t)m->d1;
   d.d2 = (uint64_t)m->d2;
+  d.t_ref = m->t_ref_us;
+  d.max_kind = max_kind;
+  d.ratio = ratio;
+  return d;
+}
+
+sa::DevFit dev_fit(const sched_fit_model_t *f, int n, int max_kind, int ratio) {
+  sa::DevFit d{};
+  d.n = n;
+  d.B = f->max_batch;
+  d.policy = f->policy;
+  d.ap = (uint64_t)f->ap;
+  d.bp = (uint64_t)f->bp;
+  d.cp = (uint64_t)f->cp;
+  d.dp = (uint64_t)f->dp;
+  d.ad = (uint64_t)f->ad;
+  d.bd = (uint64_t)f->bd;
+  d.cd = (uint64_t)f->cd;
+  d.dd = (uint64_t)f->dd;
+  d.win = 0u;
+  d.m32 = 0u;
+  d.bmagic = (1ull << 32) / (uint64_t)f->max_batch + 1;
+  d.t_ref = f->t_ref;
+  d.max_kind = max_kind;
+  d.ratio = ratio;
   return d;
 }
 
@@ -241,27 +171,6 @@ size_t eval_lds_bytes(int n, bool ls, int waves) {
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * waves;
 }
 
-// The delta kernel keeps finish offsets, prefills, slacks and doubled pair costs in 32
-// bits and forms each doubled pair cost mu * (e + d2 * mu), e = 2 (d1 + d2 l_in) + d2, with
-// 24-bit multiplies. Every finish offset is at most B * max prefill + L_max * d0 + B *
-// (d1 * L_max + d2 * (l_max * L_max + L_max (L_max + 1) / 2)).
-bool static_narrow(const HostQueue &h, const sched_model_t *m, int n) {
-  long double lmax = 0, Lmax = 0;
-  for (int r = 0; r < n; ++r) {
-    lmax = std::max<long double>(lmax, h.in_len[r]);
-    Lmax = std::max<long double>(Lmax, h.out_len[r]);
-  }
-  const long double b = std::min(n, m->max_batch);
-  const long double pf = (long double)m->p0 + (long double)m->p1 * lmax;
-  const long double fmax = b * pf + Lmax * m->d0 +
-                           b * ((long double)m->d1 * Lmax + (long double)m->d2 * (lmax * Lmax + Lmax * (Lmax + 1) / 2));
-  const long double emax = 2.0L * ((long double)m->d1 + (long double)m->d2 * lmax) + m->d2;
-  const long double inner = emax + (long double)m->d2 * Lmax;
-  const long double two24 = 16777216.0L, two32 = 4294967296.0L;
-  return fmax < two32 - 1 && inner < two24 && (long double)m->d2 < two24 && b * Lmax * inner < two32 &&
-         (long double)m->d0 < two24;
-}
-
 size_t static_wave_lds(int n, int B) { return sa::static_chain_bytes(n, B); }
 size_t wave_chain_lds(int n, int B) { return sa::wave_chain_bytes(n, B); }
 
@@ -273,92 +182,10 @@ int device_attr(hipDeviceAttribute_t attr, int fallback) {
 int max_lds_per_block() { return device_attr(hipDeviceAttributeMaxSharedMemoryPerBlock, 65536); }
 int cu_count() { return device_attr(hipDeviceAttributeMultiprocessorCount, 256); }
 
-template <int LG, int OBJ>
-hipError_t launch_static(int waves, size_t lds, const sa::DevModel &dm, const sa::StaticParams &sp,
-                         const sa::QueuePtrs &q, int chains, int iters, double T0, double alpha, uint64_t seed,
-                         uint64_t swap_thr, const sa::SearchParams &srch, unsigned char *w, hipStream_t stream) {
-  if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_static_kernel<LG, OBJ>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  const int grid = (chains + waves - 1) / waves;
-  sa::anneal_static_kernel<LG, OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, q, chains, iters, T0, alpha,
-                                                                       (uint32_t)seed, (uint32_t)(seed >> 32), swap_thr,
-                                                                       srch, w);
-  return hipGetLastError();
-}
-
-// The batch-size search's delta kernel keeps finish offsets, prefills and pair costs as the
-// fixed-size delta kernel does (static_narrow) and every time on the timeline in 32 bits:
-// whatever the layout, the timeline ends within the sum of all prefills plus, per decode
-// iteration, d0 + d1 b + d2 C; there are at most sum(l_out) iterations, the b terms add up
-// to sum(l_out) and the C terms to sum(l_out l_in + l_out (l_out + 1) / 2).
-bool sized_narrow(const HostQueue &h, const sched_model_t *m, int n) {
-  long double pf = 0, L = 0, ctx = 0;
-  for (int r = 0; r < n; ++r) {
-    const long double lo = h.out_len[r], li = h.in_len[r];
-    pf += (long double)m->p0 + (long double)m->p1 * li;
-    L += lo;
-    ctx += lo * li + lo * (lo + 1) / 2;
-  }
-  const long double end = pf + ((long double)m->d0 + (long double)m->d1) * L + (long double)m->d2 * ctx;
-  return static_narrow(h, m, n) && end < 4294967295.0L - 1.0L;
-}
-
 size_t sized_chain_lds(int n) {
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15), sb = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
   return pb + fb + 2 * ub + sb;
-}
-
-// Joint order / batch-size search: the delta kernel when the widths allow (as many chains
-// per workgroup as spread the chains over every CU, at most 16 and at most what the LDS
-// holds), else the full-replay kernel, four chains per workgroup.
-template <int OBJ>
-int launch_sized(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
-                 int chains, int iters, double T0, double alpha, uint64_t seed, const sa::SearchParams &srch,
-                 unsigned char *w, hipStream_t stream) {
-  const int n = dm.n;
-  if (sa::reg_sized_fits(n) && static_narrow(h, model, n)) {
-    // small queue: the order, every request field and the layout in registers, no LDS
-    const int cus = std::max(1, cu_count());
-    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
-    const int grid = (chains + waves - 1) / waves;
-    sa::DevModel dr = dm;  // the whole timeline in 32 bits: plain prefix sums
-    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
-    sa::anneal_reg_sized_kernel<OBJ><<<grid, waves * 64, 0, stream>>>(dr, dev_queue(queue), chains, iters, T0, alpha,
-                                                                      (uint32_t)seed, (uint32_t)(seed >> 32), srch, w);
-    HIP_TRY(hipGetLastError());
-    return SCHED_OK;
-  }
-  if (sized_narrow(h, model, n)) {
-    const size_t soa = (size_t)(n + 1) * 16, per = sized_chain_lds(n);
-    const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
-    int waves = 1;
-    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
-    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-    if (soa + per * waves <= (size_t)lim) {
-      const size_t lds = soa + per * waves;
-      if (lds > 65536)
-        HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel<OBJ>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
-      const int grid = (chains + waves - 1) / waves;
-      sa::anneal_sized_kernel<OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, dev_queue(queue), chains, iters, T0,
-                                                                      alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
-                                                                      srch, w);
-      HIP_TRY(hipGetLastError());
-      return SCHED_OK;
-    }
-  }
-  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
-  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb + 64 * 16);
-  const int grid = (chains + 3) / 4;
-  sa::anneal_sized_generic_kernel<OBJ><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), chains, iters, T0, alpha,
-                                                                   (uint32_t)seed, (uint32_t)(seed >> 32), srch, w);
-  HIP_TRY(hipGetLastError());
-  return SCHED_OK;
 }
 
 size_t anneal_lds_bytes(int n) {
@@ -366,204 +193,294 @@ size_t anneal_lds_bytes(int n) {
   return ((size_t)n * 16 + 15) / 16 * 16 + per_wave * sa::kWavesPerBlock;
 }
 
-// Every chain of one sched_anneal: the kernel for the policy and the widths the queue and
-// model allow (see the checks above), objective OBJ.
+// Chains per workgroup of the register kernels: four, or fewer so that the chains spread
+// over every CU.
+int reg_waves(int chains) {
+  const int cus = std::max(1, cu_count());
+  return chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
+}
+
+// Everything one sched_anneal launch needs besides the model and the gate.
+struct ChainArgs {
+  sa::QueuePtrs q;
+  int chains, iters;
+  double T0, alpha;
+  uint32_t k0, k1;
+  uint64_t swap_thr;
+  sa::SearchParams srch;
+  unsigned char *w;
+  hipStream_t stream;
+};
+
+// The joint order / batch-size search: on small queues the register kernel (order, request
+// fields and layout in registers, no LDS) when the 32-bit pair-cost widths hold; else the
+// delta kernel when the widths and the whole timeline fit 32 bits (as many chains per
+// workgroup as spread the chains over every CU, at most 16 and at most what the LDS holds);
+// the full-replay kernel, four chains per workgroup, in any case.
 template <int OBJ>
-int launch_chains(const HostQueue &h, const sched_model_t *model, const sa::DevModel &dm, const sched_queue_t *queue,
-                  int chains, int iters, double T0, double alpha, uint64_t seed, const sa::SearchParams &srch,
-                  unsigned char *w, hipStream_t stream) {
-  const int n = dm.n;
-  int rc = SCHED_OK;
-  bool done = false;
-  if (model->policy == SCHED_STATIC_SEARCH) {
-    if ((rc = launch_sized<OBJ>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream))) return rc;
-    done = true;
-  }
-  if (!done && model->policy == SCHED_STATIC && sa::reg_kernel_fits(n, model->max_batch) &&
-      static_narrow(h, model, n)) {
-    // small queue: the order and every request field in registers, no LDS; four chains per
-    // workgroup, or fewer so that the chains spread over every CU
-    const int cus = std::max(1, cu_count());
-    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
-    const int grid = (chains + waves - 1) / waves;
-    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    const sa::QueuePtrs qp = dev_queue(queue);
-    const uint64_t st = model->swap_threshold;
-    sa::DevModel dr = dm;  // every time in 32 bits: the 32-bit start scan and latency sum
-    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
-    switch (model->max_batch) {
-      case 1: sa::anneal_reg_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 2: sa::anneal_reg_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 4: sa::anneal_reg_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 8: sa::anneal_reg_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      default: sa::anneal_reg_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-    }
-    HIP_TRY(hipGetLastError());
-    done = true;
-  }
-  if (!done && model->policy == SCHED_STATIC && sa::reg_parts(n, model->max_batch) > 1 &&
-      static_narrow(h, model, n)) {
-    // 65 to 192 requests: two or three positions per lane, still no LDS
-    const int cus = std::max(1, cu_count());
-    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
-    const int grid = (chains + waves - 1) / waves;
-    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    const sa::QueuePtrs qp = dev_queue(queue);
-    const uint64_t st = model->swap_threshold;
-    sa::DevModel dr = dm;
-    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
-    switch (model->max_batch) {
-      case 1: sa::anneal_reg_h_kernel<0, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 2: sa::anneal_reg_h_kernel<1, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 4: sa::anneal_reg_h_kernel<2, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      case 8: sa::anneal_reg_h_kernel<3, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-      default: sa::anneal_reg_h_kernel<4, OBJ><<<grid, waves * 64, 0, stream>>>(dr, qp, chains, iters, T0, alpha, k0, k1, st, srch, w); break;
-    }
-    HIP_TRY(hipGetLastError());
-    done = true;
-  }
-  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
-    // chains per workgroup: enough to spread the chains over every CU, at most 16 and
-    // at most what the LDS holds
-    int lg = 0;
-    while ((1 << lg) < model->max_batch) ++lg;
-    // a batch of more than 32 requests fills a wave: the lane-per-batch kernel
-    const bool wave_kernel = lg == 6;
-    const size_t soa = (size_t)(n + 1) * 16;
-    const size_t per = wave_kernel ? wave_chain_lds(n, model->max_batch) : static_wave_lds(n, model->max_batch);
-    const int lim = max_lds_per_block();
-    const int cus = std::max(1, cu_count());
+void add_sized(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, const ChainArgs &a) {
+  if (sa::reg_sized_fits(n)) {
+    const int waves = reg_waves(a.chains), grid = (a.chains + waves - 1) / waves;
+    c.add(kSN, kAnnealFlags | kT32, [=](const sa::DevModel &d) {
+      sa::anneal_reg_sized_kernel<OBJ><<<grid, waves * 64, 0, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha,
+                                                                         a.k0, a.k1, a.srch, a.w);
+      return hipGetLastError();
+    });
+  } else {
+    const size_t soa = (size_t)(n + 1) * 16, per = sized_chain_lds(n);
+    const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
     int waves = 1;
-    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
+    while (waves < 16 && (int64_t)waves * cus < a.chains) waves <<= 1;
     while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-    if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= chains)) {
-      sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2,
-                          (1ull << 32) / (uint64_t)model->max_batch + 1};
+    if (soa + per * waves <= (size_t)lim) {
       const size_t lds = soa + per * waves;
-      const sa::QueuePtrs qp = dev_queue(queue);
-      const uint64_t st = model->swap_threshold;
-      hipError_t e = hipSuccess;
-      switch (lg) {
-        case 0: e = launch_static<0, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        case 1: e = launch_static<1, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        case 2: e = launch_static<2, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        case 3: e = launch_static<3, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        case 4: e = launch_static<4, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        case 5: e = launch_static<5, OBJ>(waves, lds, dm, sp, qp, chains, iters, T0, alpha, seed, st, srch, w, stream); break;
-        default: {
-          if (lds > 65536) {
-            e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_wave_kernel<OBJ>),
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-            if (e != hipSuccess) break;
-          }
-          const int grid = (chains + waves - 1) / waves;
-          sa::anneal_wave_kernel<OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, qp, chains, iters, T0, alpha,
-                                                                         (uint32_t)seed, (uint32_t)(seed >> 32), st,
-                                                                         srch, w);
-          e = hipGetLastError();
-          break;
+      const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
+      const int grid = (a.chains + waves - 1) / waves;
+      c.add(kSN | kT32, kAnnealFlags, [=](const sa::DevModel &d) {
+        if (lds > 65536) {
+          const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel<OBJ>),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+          if (e != hipSuccess) return e;
         }
-      }
-      if (e != hipSuccess) return hip_fail(e);
-      done = true;
+        sa::anneal_sized_kernel<OBJ><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0,
+                                                                          a.alpha, a.k0, a.k1, a.srch, a.w);
+        return hipGetLastError();
+      });
     }
   }
-  if (!done && model->policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagNarrowPrefill)) {
-    const bool ls = (dm.flags & sa::kFlagListSched) != 0;
-    const size_t soa = (size_t)n * 16;
-    const bool inc = ls && std::min(model->max_batch, n) <= 32;
-    const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) + (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0) +
-                       (inc ? sa::cont_inc_bytes(n, model->max_batch) : 0);
-    const int cus = std::max(1, cu_count());
-    const int lim = max_lds_per_block();
-    int waves = 1;
-    while (waves < 16 && (int64_t)waves * cus < chains) waves <<= 1;
-    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-    const size_t lds = soa + per * waves;
-    if (lds <= (size_t)lim) {
-      const void *fn =
-          ls ? (const void *)&sa::anneal_cont_kernel<true, OBJ> : (const void *)&sa::anneal_cont_kernel<false, OBJ>;
-      if (lds > 65536) HIP_TRY(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-      const int grid = (chains + waves - 1) / waves;
-      if (ls) {
-        sa::anneal_cont_kernel<true, OBJ><<<grid, waves * 64, lds, stream>>>(
-            dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
-            srch, w);
-      } else {
-        sa::anneal_cont_kernel<false, OBJ><<<grid, waves * 64, lds, stream>>>(
-            dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
-            srch, w);
-      }
-      HIP_TRY(hipGetLastError());
-      done = true;
-    }
-  }
-  if (!done) {
-    const int grid = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
-    sa::anneal_kernel<OBJ><<<grid, sa::kBlock, anneal_lds_bytes(n), stream>>>(
-        dm, dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32), model->swap_threshold,
-        srch, w);
-    HIP_TRY(hipGetLastError());
-  }
-  return SCHED_OK;
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb + 64 * 16);
+  const int grid = (a.chains + 3) / 4;
+  c.add(0u, kAnnealFlags, [=](const sa::DevModel &d) {
+    sa::anneal_sized_generic_kernel<OBJ><<<grid, 256, lds, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0,
+                                                                       a.k1, a.srch, a.w);
+    return hipGetLastError();
+  });
 }
 
 template <int LG, int OBJ>
-hipError_t launch_multi_static_lg(int grid, int waves, size_t lds, const sa::DevModel &dm, const sa::StaticParams &sp,
-                                  int n, int instances, int chains, int groups, int iters, double T0, double alpha,
-                                  uint64_t seed, uint64_t swap_thr, const sa::SearchParams &srch, unsigned char *w,
-                                  hipStream_t stream) {
-  if (lds > 65536) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::multi_static_kernel<LG, OBJ>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-  }
-  sa::multi_static_kernel<LG, OBJ><<<grid, waves * 64, lds, stream>>>(dm, sp, n, instances, chains, groups, iters, T0,
-                                                                      alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
-                                                                      swap_thr, srch, w);
+hipError_t launch_reg(bool parts, int grid, int waves, const sa::DevModel &d, const ChainArgs &a) {
+  if (parts)
+    sa::anneal_reg_h_kernel<LG, OBJ><<<grid, waves * 64, 0, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0,
+                                                                        a.k1, a.swap_thr, a.srch, a.w);
+  else
+    sa::anneal_reg_kernel<LG, OBJ><<<grid, waves * 64, 0, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0,
+                                                                      a.k1, a.swap_thr, a.srch, a.w);
   return hipGetLastError();
 }
 
-// Every instance's chains on the static delta kernels, with as many chains per workgroup as
-// the single-queue launch would take for all of them (LDS for the largest instance); sets
-// `done` when the LDS allows it.
-template <int OBJ>
-int launch_multi_static(const sched_model_t *model, const sa::DevModel &dm, int n, int nk_max, int instances,
-                        int chains, int total, int iters, double T0, double alpha, uint64_t seed,
-                        const sa::SearchParams &srch, unsigned char *w, hipStream_t stream, bool &done) {
-  int lg = 0;
-  while ((1 << lg) < model->max_batch) ++lg;
-  const size_t soa = (size_t)(nk_max + 1) * 16;
-  const size_t per = lg == 6 ? wave_chain_lds(nk_max, model->max_batch) : static_wave_lds(nk_max, model->max_batch);
-  const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
-  int waves = 1;
-  while (waves < 16 && waves < chains && (int64_t)waves * cus < total) waves <<= 1;
-  while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
-  if (soa + per * waves > (size_t)lim || (waves < 4 && (int64_t)waves * cus < total)) return SCHED_OK;
-  const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
-  const size_t lds = soa + per * waves;
-  const int groups = (chains + waves - 1) / waves, grid = instances * groups;
-  const uint64_t st = model->swap_threshold;
-  hipError_t e = hipSuccess;
-  switch (lg) {
-#define SA_MULTI_LG(L)                                                                                            \
-  case L:                                                                                                          \
-    e = launch_multi_static_lg<L, OBJ>(grid, waves, lds, dm, sp, n, instances, chains, groups, iters, T0, alpha, \
-                                       seed, st, srch, w, stream);                                               \
-    break;
-    SA_MULTI_LG(0)
-    SA_MULTI_LG(1)
-    SA_MULTI_LG(2)
-    SA_MULTI_LG(3)
-    SA_MULTI_LG(4)
-    SA_MULTI_LG(5)
-    SA_MULTI_LG(6)
-#undef SA_MULTI_LG
-    default: return SCHED_EINVAL;
+template <int LG, int OBJ>
+hipError_t launch_static(int waves, size_t lds, const sa::DevModel &d, const sa::StaticParams &sp, const ChainArgs &a) {
+  const void *fn = LG == 6 ? reinterpret_cast<const void *>(&sa::anneal_wave_kernel<OBJ>)
+                           : reinterpret_cast<const void *>(&sa::anneal_static_kernel<LG, OBJ>);
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
   }
-  if (e != hipSuccess) return hip_fail(e);
-  done = true;
-  return SCHED_OK;
+  const int grid = (a.chains + waves - 1) / waves;
+  if constexpr (LG == 6)
+    sa::anneal_wave_kernel<OBJ><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0,
+                                                                     a.k1, a.swap_thr, a.srch, a.w);
+  else
+    sa::anneal_static_kernel<LG, OBJ><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0,
+                                                                           a.alpha, a.k0, a.k1, a.swap_thr, a.srch,
+                                                                           a.w);
+  return hipGetLastError();
+}
+
+// The kernels a single-queue sched_anneal may run, by policy, in order of preference:
+//   static: the register kernel (up to 64 requests, or 65 to 192 with two or three positions
+//     per lane; batches of 1 .. 16, a power of two) or else the LDS delta kernel (one lane per
+//     batch member, or one batch per wave for batches of more than 32), both on the 32-bit
+//     pair-cost widths, the register kernel also on a 32-bit timeline when it holds;
+//   continuous: list scheduling when its 32-bit keys fit, the event loop when the 32-bit event
+//     arithmetic does, each as the LDS allows;
+//   always last: the full-replay kernel (any widths).
+template <int OBJ>
+void add_chains(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, const ChainArgs &a) {
+  const int B = model->max_batch;
+  if (model->policy == SCHED_STATIC_SEARCH) {
+    add_sized<OBJ>(c, model, n, a);
+    return;
+  }
+  if (model->policy == SCHED_STATIC) {
+    if (sa::reg_kernel_fits(n, B) || sa::reg_parts(n, B) > 1) {
+      const bool parts = !sa::reg_kernel_fits(n, B);
+      const int waves = reg_waves(a.chains), grid = (a.chains + waves - 1) / waves;
+      c.add(kSN, kAnnealFlags | kT32, [=](const sa::DevModel &d) {
+        switch (B) {
+          case 1: return launch_reg<0, OBJ>(parts, grid, waves, d, a);
+          case 2: return launch_reg<1, OBJ>(parts, grid, waves, d, a);
+          case 4: return launch_reg<2, OBJ>(parts, grid, waves, d, a);
+          case 8: return launch_reg<3, OBJ>(parts, grid, waves, d, a);
+          default: return launch_reg<4, OBJ>(parts, grid, waves, d, a);
+        }
+      });
+    } else {
+      // chains per workgroup: enough to spread the chains over every CU, at most 16 and at
+      // most what the LDS holds
+      int lg = 0;
+      while ((1 << lg) < B) ++lg;
+      const size_t soa = (size_t)(n + 1) * 16;
+      const size_t per = lg == 6 ? wave_chain_lds(n, B) : static_wave_lds(n, B);
+      const int lim = max_lds_per_block(), cus = std::max(1, cu_count());
+      int waves = 1;
+      while (waves < 16 && (int64_t)waves * cus < a.chains) waves <<= 1;
+      while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+      if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= a.chains)) {
+        const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)B + 1};
+        const size_t lds = soa + per * waves;
+        c.add(kSN, kAnnealFlags, [=](const sa::DevModel &d) {
+          switch (lg) {
+            case 0: return launch_static<0, OBJ>(waves, lds, d, sp, a);
+            case 1: return launch_static<1, OBJ>(waves, lds, d, sp, a);
+            case 2: return launch_static<2, OBJ>(waves, lds, d, sp, a);
+            case 3: return launch_static<3, OBJ>(waves, lds, d, sp, a);
+            case 4: return launch_static<4, OBJ>(waves, lds, d, sp, a);
+            case 5: return launch_static<5, OBJ>(waves, lds, d, sp, a);
+            default: return launch_static<6, OBJ>(waves, lds, d, sp, a);
+          }
+        });
+      }
+    }
+  }
+  if (model->policy == SCHED_CONTINUOUS) {
+    for (int ls = 1; ls >= 0; --ls) {
+      const size_t soa = (size_t)n * 16;
+      const bool inc = ls && std::min(B, n) <= 32;
+      const size_t per = (((size_t)n * 2 + 15) & ~size_t(15)) +
+                         (ls ? ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) : 0) +
+                         (inc ? sa::cont_inc_bytes(n, B) : 0);
+      const int cus = std::max(1, cu_count()), lim = max_lds_per_block();
+      int waves = 1;
+      while (waves < 16 && (int64_t)waves * cus < a.chains) waves <<= 1;
+      while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+      const size_t lds = soa + per * waves;
+      if (lds > (size_t)lim) continue;
+      const int grid = (a.chains + waves - 1) / waves;
+      const uint32_t need = sa::kFlagNarrowPrefill | (ls ? sa::kFlagListSched : 0u);
+      c.add(need, kAnnealFlags, [=](const sa::DevModel &d) {
+        const void *fn = ls ? (const void *)&sa::anneal_cont_kernel<true, OBJ>
+                            : (const void *)&sa::anneal_cont_kernel<false, OBJ>;
+        if (lds > 65536) {
+          const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+          if (e != hipSuccess) return e;
+        }
+        if (ls)
+          sa::anneal_cont_kernel<true, OBJ><<<grid, waves * 64, lds, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha,
+                                                                                 a.k0, a.k1, a.swap_thr, a.srch, a.w);
+        else
+          sa::anneal_cont_kernel<false, OBJ><<<grid, waves * 64, lds, a.stream>>>(
+              d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0, a.k1, a.swap_thr, a.srch, a.w);
+        return hipGetLastError();
+      });
+    }
+  }
+  const int grid = (a.chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+  const size_t lds = anneal_lds_bytes(n);
+  c.add(0u, kAnnealFlags, [=](const sa::DevModel &d) {
+    sa::anneal_kernel<OBJ><<<grid, sa::kBlock, lds, a.stream>>>(d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0, a.k1,
+                                                                a.swap_thr, a.srch, a.w);
+    return hipGetLastError();
+  });
+}
+
+// Everything one sched_anneal_multi launch needs besides the model and the gate.
+struct MultiArgs {
+  int n, instances, chains, iters;
+  double T0, alpha;
+  uint32_t k0, k1;
+  uint64_t swap_thr;
+  sa::SearchParams srch;
+  unsigned char *w;
+  hipStream_t stream;
+};
+
+template <int LG, int OBJ>
+hipError_t launch_multi_reg(bool parts, int grid, int waves, int groups, const sa::DevModel &d, const MultiArgs &a) {
+  if (parts)
+    sa::multi_reg_h_kernel<LG, OBJ><<<grid, waves * 64, 0, a.stream>>>(d, a.n, a.instances, a.chains, groups, a.iters,
+                                                                       a.T0, a.alpha, a.k0, a.k1, a.swap_thr, a.srch,
+                                                                       a.w);
+  else
+    sa::multi_reg_kernel<LG, OBJ><<<grid, waves * 64, 0, a.stream>>>(d, a.n, a.instances, a.chains, groups, a.iters,
+                                                                     a.T0, a.alpha, a.k0, a.k1, a.swap_thr, a.srch,
+                                                                     a.w);
+  return hipGetLastError();
+}
+
+template <int LG, int OBJ>
+hipError_t launch_multi_static(int grid, int waves, int groups, size_t lds, const sa::DevModel &d,
+                               const sa::StaticParams &sp, const MultiArgs &a) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::multi_static_kernel<LG, OBJ>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  sa::multi_static_kernel<LG, OBJ><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.n, a.instances, a.chains, groups,
+                                                                        a.iters, a.T0, a.alpha, a.k0, a.k1, a.swap_thr,
+                                                                        a.srch, a.w);
+  return hipGetLastError();
+}
+
+// The kernels a sched_anneal_multi may run, in order of preference (static admission):
+// the register kernel when every instance holds at most 64 requests, its two- and
+// three-position form when every instance holds at most 192 (batches of 1 .. 16, a power of
+// two, on the 32-bit pair-cost widths); the LDS delta kernels, laid out for the whole queue
+// (an instance never holds more); always last the full-replay kernel (LDS for the whole
+// queue too).
+template <int OBJ>
+void add_multi(Candidates<sa::DevModel> &c, const sched_model_t *model, const MultiArgs &a) {
+  const int B = model->max_batch, n = a.n, total = a.instances * a.chains;
+  const int cus = std::max(1, cu_count());
+  if (model->policy == SCHED_STATIC && sa::reg_parts(1, B) > 0) {
+    const int waves = total >= 4 * cus && a.chains >= 4 ? 4 : (total >= 2 * cus && a.chains >= 2 ? 2 : 1);
+    const int groups = (a.chains + waves - 1) / waves, grid = a.instances * groups;
+    for (int parts = 0; parts <= 1; ++parts) {
+      c.add(kSN | (parts ? sa::kFlagInst192 : sa::kFlagInst64), kMultiFlags | kT32, [=](const sa::DevModel &d) {
+        switch (B) {
+          case 1: return launch_multi_reg<0, OBJ>(parts, grid, waves, groups, d, a);
+          case 2: return launch_multi_reg<1, OBJ>(parts, grid, waves, groups, d, a);
+          case 4: return launch_multi_reg<2, OBJ>(parts, grid, waves, groups, d, a);
+          case 8: return launch_multi_reg<3, OBJ>(parts, grid, waves, groups, d, a);
+          default: return launch_multi_reg<4, OBJ>(parts, grid, waves, groups, d, a);
+        }
+      });
+    }
+  }
+  if (model->policy == SCHED_STATIC) {
+    int lg = 0;
+    while ((1 << lg) < B) ++lg;
+    const size_t soa = (size_t)(n + 1) * 16;
+    const size_t per = lg == 6 ? wave_chain_lds(n, B) : static_wave_lds(n, B);
+    const int lim = max_lds_per_block();
+    int waves = 1;
+    while (waves < 16 && waves < a.chains && (int64_t)waves * cus < total) waves <<= 1;
+    while (waves > 1 && soa + per * waves > (size_t)lim) waves >>= 1;
+    if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= total)) {
+      const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)B + 1};
+      const size_t lds = soa + per * waves;
+      const int groups = (a.chains + waves - 1) / waves, grid = a.instances * groups;
+      c.add(kSN, kMultiFlags, [=](const sa::DevModel &d) {
+        switch (lg) {
+          case 0: return launch_multi_static<0, OBJ>(grid, waves, groups, lds, d, sp, a);
+          case 1: return launch_multi_static<1, OBJ>(grid, waves, groups, lds, d, sp, a);
+          case 2: return launch_multi_static<2, OBJ>(grid, waves, groups, lds, d, sp, a);
+          case 3: return launch_multi_static<3, OBJ>(grid, waves, groups, lds, d, sp, a);
+          case 4: return launch_multi_static<4, OBJ>(grid, waves, groups, lds, d, sp, a);
+          case 5: return launch_multi_static<5, OBJ>(grid, waves, groups, lds, d, sp, a);
+          default: return launch_multi_static<6, OBJ>(grid, waves, groups, lds, d, sp, a);
+        }
+      });
+    }
+  }
+  const int groups = (a.chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
+  const size_t lds = anneal_lds_bytes(n);
+  c.add(0u, kMultiFlags, [=](const sa::DevModel &d) {
+    sa::multi_anneal_kernel<OBJ><<<a.instances * groups, sa::kBlock, lds, a.stream>>>(
+        d, a.n, a.instances, a.chains, groups, a.iters, a.T0, a.alpha, a.k0, a.k1, a.swap_thr, a.srch, a.w);
+    return hipGetLastError();
+  });
 }
 
 // Fixed device scratch of sched_anneal_noalloc: the annealing workspace for callers that
@@ -600,69 +517,70 @@ extern "C" {
 int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms, int64_t k, int64_t *out,
                int64_t *detail, hipStream_t stream) {
   if (k < 0) return SCHED_EINVAL;
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  int rc = check_model(model, queue->n);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if ((rc = check_model(model, queue->n))) return rc;
   if (k > 0 && (!perms || !out)) return SCHED_EINVAL;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h))) return rc;
-  if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
-                                    timeline_narrow(h, model, n));
-  if (model->policy != SCHED_CONTINUOUS && static_narrow(h, model, n)) {
+  const sa::DevModel dm = dev_model(model, n);
+  const sa::QueuePtrs qp = dev_queue(queue);
+  Candidates<sa::DevModel> c;
+  if (model->policy != SCHED_CONTINUOUS) {
+    // static batches on the 32-bit pair-cost widths: one order per wave with the delta
+    // kernels' arithmetic, on a 32-bit timeline when it holds
     int lg = 0;
     while ((1 << lg) < model->max_batch) ++lg;
     const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
     const size_t lds = (size_t)(n + 1) * 16 + ((((size_t)n * 2 + 15) & ~size_t(15)) + 64 * 8 + 32 * 4) * 4;
-    const int64_t want4 = (k + 3) / 4;
-    const int g4 = (int)std::min<int64_t>(want4, 256 * 32);
-    const bool t32 = sized_narrow(h, model, n);  // the whole timeline in 32 bits
-    hipError_t e = hipSuccess;
-#define SA_EVAL_CASE(L)                                                                                            \
-  case L:                                                                                                        \
-    if (detail)                                                                                                  \
-      sa::eval_static_kernel<L, true><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, detail);  \
-    else if (t32)                                                                                                \
-      sa::eval_static_kernel<L, false, true><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out,     \
-                                                                       nullptr);                                 \
-    else                                                                                                         \
-      sa::eval_static_kernel<L, false><<<g4, 256, lds, stream>>>(dm, sp, dev_queue(queue), perms, k, out, nullptr); \
+    const int g4 = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
+    auto launch = [=](const sa::DevModel &d, bool t32) {
+#define SA_EVAL_CASE(L)                                                                                        \
+  case L:                                                                                                      \
+    if (detail)                                                                                                \
+      sa::eval_static_kernel<L, true><<<g4, 256, lds, stream>>>(d, sp, qp, perms, k, out, detail);             \
+    else if (t32)                                                                                              \
+      sa::eval_static_kernel<L, false, true><<<g4, 256, lds, stream>>>(d, sp, qp, perms, k, out, nullptr);     \
+    else                                                                                                       \
+      sa::eval_static_kernel<L, false><<<g4, 256, lds, stream>>>(d, sp, qp, perms, k, out, nullptr);           \
     break;
-    switch (lg) {
-      SA_EVAL_CASE(0)
-      SA_EVAL_CASE(1)
-      SA_EVAL_CASE(2)
-      SA_EVAL_CASE(3)
-      SA_EVAL_CASE(4)
-      SA_EVAL_CASE(5)
-      default:
-        SA_EVAL_CASE(6)
-    }
+      switch (lg) {
+        SA_EVAL_CASE(0)
+        SA_EVAL_CASE(1)
+        SA_EVAL_CASE(2)
+        SA_EVAL_CASE(3)
+        SA_EVAL_CASE(4)
+        SA_EVAL_CASE(5)
+        default:
+          SA_EVAL_CASE(6)
+      }
 #undef SA_EVAL_CASE
-    e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e);
-    return SCHED_OK;
+      return hipGetLastError();
+    };
+    if (!detail) c.add(kSN | kT32, kEvalFlags, [=](const sa::DevModel &d) { return launch(d, true); });
+    c.add(kSN, kEvalFlags, [=](const sa::DevModel &d) { return launch(d, false); });
   }
-  // one order per wave, up to four waves per workgroup as the LDS allows
-  const bool ls = dm.policy == SCHED_CONTINUOUS && (dm.flags & sa::kFlagListSched);
+  // any widths: one order per wave, up to four waves per workgroup as the LDS allows (with
+  // room for list scheduling under continuous admission)
+  const bool ls = model->policy == SCHED_CONTINUOUS;
+  const size_t lim = (size_t)max_lds_per_block() - sa::kCheckLdsBytes;  // the checks' own LDS on top
   int waves = sa::kWavesPerBlock;
-  while (waves > 1 && eval_lds_bytes(n, ls, waves) > (size_t)max_lds_per_block()) waves >>= 1;
+  while (waves > 1 && eval_lds_bytes(n, ls, waves) > lim) waves >>= 1;
   const size_t lds = eval_lds_bytes(n, ls, waves);
   const int grid = (int)std::min<int64_t>((k + waves - 1) / waves, 256 * 32);
-  if (lds > 65536) {
-    HIP_TRY(hipFuncSetAttribute(reinterpret_cast<const void *>(detail ? (const void *)&sa::eval_kernel<true>
-                                                                      : (const void *)&sa::eval_kernel<false>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds));
-  }
-  if (detail) {
-    sa::eval_kernel<true><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), perms, k, out, detail);
-  } else {
-    sa::eval_kernel<false><<<grid, waves * 64, lds, stream>>>(dm, dev_queue(queue), perms, k, out, nullptr);
-  }
-  HIP_TRY(hipGetLastError());
-  return SCHED_OK;
+  c.add(0u, kEvalFlags, [=](const sa::DevModel &d) {
+    const void *fn = detail ? (const void *)&sa::eval_kernel<true> : (const void *)&sa::eval_kernel<false>;
+    if (lds > 65536) {
+      const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    if (detail)
+      sa::eval_kernel<true><<<grid, waves * 64, lds, stream>>>(d, qp, perms, k, out, detail);
+    else
+      sa::eval_kernel<false><<<grid, waves * 64, lds, stream>>>(d, qp, perms, k, out, nullptr);
+    return hipGetLastError();
+  });
+  return c.run(dm);
 }
 
 size_t sched_ws_bytes(int32_t n, int32_t chains) {
@@ -678,35 +596,29 @@ int sched_anneal(const sched_queue_t *queue, const sched_model_t *model, int32_t
 int sched_anneal_ex(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
                     int32_t chains, int32_t iters, double T0, double alpha, uint64_t seed, void *ws, size_t ws_bytes,
                     hipStream_t stream) {
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
-    return SCHED_EINVAL;
-  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
-  if (search) {
-    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
-        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
-      return SCHED_EINVAL;
-    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
-  }
-  int rc = check_model(model, queue->n);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if ((rc = check_chain_args(chains, iters, T0, alpha))) return rc;
+  sa::SearchParams srch;
+  if ((rc = check_search(search, srch))) return rc;
+  if ((rc = check_model(model, queue->n))) return rc;
   // the ratio needs a positive total latency: every request takes at least p0 + d0 + d1
   if (srch.objective == SCHED_OBJ_RATIO && model->p0 + model->d0 + model->d1 < 1) return SCHED_EINVAL;
   if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
   if (ws_bytes < sched_ws_bytes(queue->n, chains)) return SCHED_ENOSPC;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h))) return rc;
-  if ((rc = range_check(h, model, queue->n))) return rc;
-  if (srch.objective == SCHED_OBJ_RATIO && (rc = ratio_range_check(h, model, queue->n))) return rc;
   const int n = queue->n;
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
-                                    timeline_narrow(h, model, n), timeline_bound(h, model, n) < std::ldexp(1.0L, 57));
+  const sa::DevModel dm = dev_model(model, n, 2, srch.objective == SCHED_OBJ_RATIO);
   unsigned char *w = static_cast<unsigned char *>(ws);
-  sa::start_kernel<<<1, 1024, 0, stream>>>(dm, dev_queue(queue), chains, iters, model->t_ref_us, srch, w);
+  const ChainArgs a{dev_queue(queue), chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
+                    model->swap_threshold, srch, w, stream};
+  Candidates<sa::DevModel> c;
+  if (srch.objective)
+    add_chains<1>(c, model, n, a);
+  else
+    add_chains<0>(c, model, n, a);
+  sa::start_kernel<<<1, 1024, 0, stream>>>(c.checker(dm, kAnnealFlags), a.q, chains, iters, model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
-  rc = srch.objective ? launch_chains<1>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream)
-                      : launch_chains<0>(h, model, dm, queue, chains, iters, T0, alpha, seed, srch, w, stream);
-  if (rc) return rc;
+  if ((rc = c.run(dm))) return rc;
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
@@ -762,28 +674,28 @@ int sched_gen_perms(uint64_t seed, int32_t n, int64_t row0, int64_t k, uint16_t 
 int sched_eval_batches(const sched_queue_t *queue, const sched_model_t *model, const uint16_t *perms,
                        const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail, hipStream_t stream) {
   if (k < 0) return SCHED_EINVAL;
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  int rc = check_model(model, queue->n);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if ((rc = check_model(model, queue->n))) return rc;
   if (model->policy == SCHED_CONTINUOUS) return SCHED_EINVAL;
   if (k > 0 && (!perms || !starts || !out)) return SCHED_EINVAL;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h))) return rc;
-  if ((rc = range_check(h, model, queue->n))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
-  sa::DevModel dm = dev_model(model, n, false, false, false, timeline_bound(h, model, n) < std::ldexp(1.0L, 57),
-                              static_narrow(h, model, n));
-  if (sized_narrow(h, model, n)) dm.flags |= sa::kFlagTime32;  // every layout's timeline in 32 bits
+  const sa::QueuePtrs qp = dev_queue(queue);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 64 * 16 + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
-  if (detail)
-    sa::eval_sized_kernel<true><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), perms, starts, k, out, detail);
-  else
-    sa::eval_sized_kernel<false><<<grid, 256, lds, stream>>>(dm, dev_queue(queue), perms, starts, k, out, nullptr);
-  HIP_TRY(hipGetLastError());
-  return SCHED_OK;
+  Candidates<sa::DevModel> c;
+  // one kernel: the windowed replay, the 32-bit pair costs and the 32-bit timeline are taken
+  // where they hold
+  c.add(0u, sa::kFlagWindows | kSN | kT32, [=](const sa::DevModel &d) {
+    if (detail)
+      sa::eval_sized_kernel<true><<<grid, 256, lds, stream>>>(d, qp, perms, starts, k, out, detail);
+    else
+      sa::eval_sized_kernel<false><<<grid, 256, lds, stream>>>(d, qp, perms, starts, k, out, nullptr);
+    return hipGetLastError();
+  });
+  return c.run(dev_model(model, n));
 }
 
 int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint8_t *winner_starts,
@@ -795,25 +707,19 @@ int sched_starts(const void *ws, uint8_t *cur_starts, uint8_t *best_starts, uint
   return SCHED_OK;
 }
 
+int sched_status(const void *ws, int64_t *out, hipStream_t stream) {
+  if (!ws || !out) return SCHED_EINVAL;
+  sa::status_copy_kernel<<<1, 1, 0, stream>>>(static_cast<const unsigned char *>(ws), out);
+  HIP_TRY(hipGetLastError());
+  return SCHED_OK;
+}
+
 int sched_assign(const sched_queue_t *queue, int32_t instances, const int64_t *capacity, int32_t *inst_out,
                  hipStream_t stream) {
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !capacity || !inst_out) return SCHED_EINVAL;
-  HostQueue h;
-  int rc = fetch_queue(queue, stream, h);
+  int rc = check_queue(queue);
   if (rc) return rc;
-  std::vector<int64_t> cap((size_t)instances);
-  HIP_TRY(hipMemcpyAsync(cap.data(), capacity, (size_t)instances * 8, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipStreamSynchronize(stream));
-  bool narrow = true;
-  for (int64_t c : cap) {
-    if (c < 1 || c > (int64_t(1) << 48)) return SCHED_EINVAL;
-    narrow = narrow && c < sa::kAssignNarrowCap;
-  }
-  if (narrow)
-    sa::assign_sorted_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
-  else
-    sa::assign_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
+  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !capacity || !inst_out) return SCHED_EINVAL;
+  sa::assign_kernel<<<1, 64, 0, stream>>>(dev_queue(queue), queue->n, instances, capacity, inst_out);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
 }
@@ -826,109 +732,37 @@ size_t sched_ws_bytes_multi(int32_t n, int32_t instances, int32_t chains) {
 int sched_anneal_multi(const sched_queue_t *queue, const sched_model_t *model, const sched_search_t *search,
                        const int32_t *inst_of, int32_t instances, int32_t chains, int32_t iters, double T0,
                        double alpha, uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !inst_of) return SCHED_EINVAL;
-  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
-    return SCHED_EINVAL;
-  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
-  if (search) {
-    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
-        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
-      return SCHED_EINVAL;
-    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
-  }
-  int rc = check_model(model, queue->n);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if (instances < 1 || instances > SCHED_MAX_INSTANCES || !inst_of) return SCHED_EINVAL;
+  if ((rc = check_chain_args(chains, iters, T0, alpha))) return rc;
+  sa::SearchParams srch;
+  if ((rc = check_search(search, srch))) return rc;
+  if ((rc = check_model(model, queue->n))) return rc;
   if (model->policy == SCHED_STATIC_SEARCH) return SCHED_EINVAL;
   if (srch.objective == SCHED_OBJ_RATIO && model->p0 + model->d0 + model->d1 < 1) return SCHED_EINVAL;
   const int n = queue->n;
   if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
   if (ws_bytes < sched_ws_bytes_multi(n, instances, chains)) return SCHED_ENOSPC;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h))) return rc;
-  std::vector<int32_t> inst((size_t)n);
-  HIP_TRY(hipMemcpyAsync(inst.data(), inst_of, (size_t)n * 4, hipMemcpyDeviceToHost, stream));
-  HIP_TRY(hipStreamSynchronize(stream));
-  std::vector<int> cnt((size_t)instances, 0);
-  for (int32_t v : inst) {
-    if (v < 0 || v >= instances) return SCHED_EINVAL;
-    ++cnt[(size_t)v];
-  }
-  // every instance's queue is part of the whole one, so the whole queue's bounds hold for it
-  if ((rc = range_check(h, model, n))) return rc;
-  if (srch.objective == SCHED_OBJ_RATIO && (rc = ratio_range_check(h, model, n))) return rc;
-  const int nk_max = *std::max_element(cnt.begin(), cnt.end());
-  const sa::DevModel dm = dev_model(model, n, prefill_narrow(h, model, n), list_sched_ok(h, model, n),
-                                    timeline_narrow(h, model, n));
+  const sa::DevModel dm = dev_model(model, n, 2, srch.objective == SCHED_OBJ_RATIO);
   unsigned char *w = static_cast<unsigned char *>(ws);
-  sa::multi_header_kernel<<<1, 1, 0, stream>>>(w, n, instances, chains, (int64_t)sa::mws_slot_bytes(n, chains));
+  const MultiArgs a{n, instances, chains, iters, T0, alpha, (uint32_t)seed, (uint32_t)(seed >> 32),
+                    model->swap_threshold, srch, w, stream};
+  Candidates<sa::DevModel> c;
+  if (srch.objective)
+    add_multi<1>(c, model, a);
+  else
+    add_multi<0>(c, model, a);
+  const sa::QueuePtrs qp = dev_queue(queue);
+  sa::multi_plan_kernel<<<1, 1024, 0, stream>>>(c.checker(dm, 0u), qp, inst_of, instances, chains, iters,
+                                                (int64_t)sa::mws_slot_bytes(n, chains), w);
   HIP_TRY(hipGetLastError());
-  sa::gather_kernel<<<instances, 1024, 0, stream>>>(dev_queue(queue), n, inst_of, chains, instances, w);
+  sa::gather_kernel<<<instances, 1024, 0, stream>>>(qp, n, inst_of, chains, instances, w);
   HIP_TRY(hipGetLastError());
-  sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(dm, n, instances, chains, iters, model->t_ref_us, srch, w);
+  sa::multi_start_kernel<<<instances, 1024, 0, stream>>>(c.checker(dm, kMultiFlags), n, instances, chains, iters,
+                                                         model->t_ref_us, srch, w);
   HIP_TRY(hipGetLastError());
-  bool done = nk_max == 0;
-  if (!done && model->policy == SCHED_STATIC &&
-      sa::reg_parts(nk_max, model->max_batch) > 0 &&
-      static_narrow(h, model, n)) {
-    // every instance small: the register kernel per instance, no LDS (two or three positions
-    // per lane when an instance holds more than 64 requests)
-    const bool two = nk_max > 64;
-    const int total = instances * chains, cus = std::max(1, cu_count());
-    const int waves = total >= 4 * cus && chains >= 4 ? 4 : (total >= 2 * cus && chains >= 2 ? 2 : 1);
-    const int groups = (chains + waves - 1) / waves, grid = instances * groups;
-    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    const uint64_t st = model->swap_threshold;
-    // every instance's timeline is within the whole queue's bound
-    sa::DevModel dr = dm;
-    if (sized_narrow(h, model, n)) dr.flags |= sa::kFlagTime32;
-#define SA_MULTI_REG(LG)                                                                                         \
-  if (two && srch.objective)                                                                                   \
-    sa::multi_reg_h_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,    \
-                                                                  alpha, k0, k1, st, srch, w);                 \
-  else if (two)                                                                                                \
-    sa::multi_reg_h_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,    \
-                                                                  alpha, k0, k1, st, srch, w);                 \
-  else if (srch.objective)                                                                                     \
-    sa::multi_reg_kernel<LG, 1><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,     \
-                                                                 alpha, k0, k1, st, srch, w);                  \
-  else                                                                                                         \
-    sa::multi_reg_kernel<LG, 0><<<grid, waves * 64, 0, stream>>>(dr, n, instances, chains, groups, iters, T0,     \
-                                                                 alpha, k0, k1, st, srch, w);
-    switch (model->max_batch) {
-      case 1: SA_MULTI_REG(0) break;
-      case 2: SA_MULTI_REG(1) break;
-      case 4: SA_MULTI_REG(2) break;
-      case 8: SA_MULTI_REG(3) break;
-      default: SA_MULTI_REG(4) break;
-    }
-#undef SA_MULTI_REG
-    HIP_TRY(hipGetLastError());
-    done = true;
-  }
-  if (!done && model->policy == SCHED_STATIC && static_narrow(h, model, n)) {
-    // every instance's queue is part of the whole one, so the delta kernel's widths hold
-    const int total = instances * chains;
-    if (srch.objective)
-      rc = launch_multi_static<1>(model, dm, n, nk_max, instances, chains, total, iters, T0, alpha, seed, srch, w,
-                                  stream, done);
-    else
-      rc = launch_multi_static<0>(model, dm, n, nk_max, instances, chains, total, iters, T0, alpha, seed, srch, w,
-                                  stream, done);
-    if (rc) return rc;
-  }
-  if (!done) {
-    const int groups = (chains + sa::kWavesPerBlock - 1) / sa::kWavesPerBlock;
-    const size_t lds = anneal_lds_bytes(nk_max);
-    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-    if (srch.objective)
-      sa::multi_anneal_kernel<1><<<instances * groups, sa::kBlock, lds, stream>>>(
-          dm, n, instances, chains, groups, iters, T0, alpha, k0, k1, model->swap_threshold, srch, w);
-    else
-      sa::multi_anneal_kernel<0><<<instances * groups, sa::kBlock, lds, stream>>>(
-          dm, n, instances, chains, groups, iters, T0, alpha, k0, k1, model->swap_threshold, srch, w);
-    HIP_TRY(hipGetLastError());
-  }
+  if ((rc = c.run(dm))) return rc;
   sa::multi_reduce_kernel<<<instances, 1024, 0, stream>>>(n, instances, chains, w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;
@@ -953,80 +787,77 @@ int sched_eval_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, con
                    const uint16_t *perms, const uint8_t *starts, int64_t k, int64_t *out, int64_t *detail,
                    hipStream_t stream) {
   if (k < 0) return SCHED_EINVAL;
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  int rc = check_fit(fit);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if ((rc = check_fit(fit))) return rc;
   if (k > 0 && (!perms || !out)) return SCHED_EINVAL;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
-  if ((rc = fit_range_check(h, fit, queue->n, false))) return rc;
   if (k == 0) return SCHED_OK;
   const int n = queue->n;
+  const sa::QueuePtrs qp = dev_queue(queue);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
   const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (pb + fb + 32 * 4);
   const int grid = (int)std::min<int64_t>((k + 3) / 4, 256 * 32);
-  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57));
-  if (detail)
-    sa::eval_fit_kernel<true><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, perms, starts, k, out, detail);
-  else
-    sa::eval_fit_kernel<false><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, perms, starts, k, out,
-                                                           nullptr);
-  HIP_TRY(hipGetLastError());
-  return SCHED_OK;
+  Candidates<sa::DevFit> c;
+  c.add(0u, sa::kFlagFitWindows, [=](const sa::DevFit &d) {
+    if (detail)
+      sa::eval_fit_kernel<true><<<grid, 256, lds, stream>>>(d, qp, tpot_thr, perms, starts, k, out, detail);
+    else
+      sa::eval_fit_kernel<false><<<grid, 256, lds, stream>>>(d, qp, tpot_thr, perms, starts, k, out, nullptr);
+    return hipGetLastError();
+  });
+  return c.run(dev_fit(fit, n, tpot_thr ? 3 : 2, 0));
 }
 
 int sched_anneal_fit(const sched_queue_t *queue, const sched_fit_model_t *fit, const uint32_t *tpot_thr,
                      const sched_search_t *search, int32_t chains, int32_t iters, double T0, double alpha,
                      uint64_t seed, void *ws, size_t ws_bytes, hipStream_t stream) {
-  if (!queue || queue->n < 1 || queue->n > SCHED_MAX_N) return SCHED_EINVAL;
-  if (chains < 1 || iters < 0 || !(T0 > 0.0) || !std::isfinite(T0) || !(alpha > 0.0) || !std::isfinite(alpha))
-    return SCHED_EINVAL;
-  sa::SearchParams srch{SCHED_OBJ_LEX, 1, 0, 0};
-  if (search) {
-    if ((search->objective != SCHED_OBJ_LEX && search->objective != SCHED_OBJ_RATIO) || search->level_len < 1 ||
-        (search->early_exit != 0 && search->early_exit != 1) || search->reserved != 0)
-      return SCHED_EINVAL;
-    srch = sa::SearchParams{search->objective, search->level_len, search->early_exit, 0};
-  }
-  int rc = check_fit(fit);
+  int rc = check_queue(queue);
   if (rc) return rc;
+  if ((rc = check_chain_args(chains, iters, T0, alpha))) return rc;
+  sa::SearchParams srch;
+  if ((rc = check_search(search, srch))) return rc;
+  if ((rc = check_fit(fit))) return rc;
   if (srch.objective == SCHED_OBJ_RATIO && fit->dp + fit->dd < 1) return SCHED_EINVAL;  // positive latencies
   if (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)) return SCHED_EINVAL;
   if (ws_bytes < sched_ws_bytes(queue->n, chains)) return SCHED_ENOSPC;
-  HostQueue h;
-  if ((rc = fetch_queue(queue, stream, h, tpot_thr ? 3 : 2))) return rc;
-  if ((rc = fit_range_check(h, fit, queue->n, srch.objective == SCHED_OBJ_RATIO))) return rc;
   const int n = queue->n;
-  const sa::DevFit df = dev_fit(fit, n, fit_timeline_bound(h, fit, n) < std::ldexp(1.0L, 57),
-                                fit_member_bound(h, fit, n) < 4294967295.0L);
+  const sa::DevFit df = dev_fit(fit, n, tpot_thr ? 3 : 2, srch.objective == SCHED_OBJ_RATIO);
   unsigned char *w = static_cast<unsigned char *>(ws);
-  sa::start_fit_kernel<<<1, 1024, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, fit->t_ref, srch, w);
-  HIP_TRY(hipGetLastError());
+  const sa::QueuePtrs qp = dev_queue(queue);
   const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
-  if (n <= 64 && df.win) {
-    // small queue: order, request fields and layout in registers, no LDS
-    const int cus = std::max(1, cu_count());
-    const int waves = chains >= 4 * cus ? 4 : (chains >= 2 * cus ? 2 : 1);
-    const int rgrid = (chains + waves - 1) / waves;
-    if (srch.objective)
-      sa::anneal_reg_fit_kernel<1><<<rgrid, waves * 64, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0,
-                                                                     alpha, k0, k1, fit->swap_threshold, srch, w);
-    else
-      sa::anneal_reg_fit_kernel<0><<<rgrid, waves * 64, 0, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0,
-                                                                     alpha, k0, k1, fit->swap_threshold, srch, w);
-    HIP_TRY(hipGetLastError());
-  } else {
-    const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
-    const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb);
-    const int grid = (chains + 3) / 4;
-    if (srch.objective)
-      sa::anneal_fit_kernel<1><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0,
-                                                           k1, fit->swap_threshold, srch, w);
-    else
-      sa::anneal_fit_kernel<0><<<grid, 256, lds, stream>>>(df, dev_queue(queue), tpot_thr, chains, iters, T0, alpha, k0,
-                                                           k1, fit->swap_threshold, srch, w);
-    HIP_TRY(hipGetLastError());
+  const uint64_t st = fit->swap_threshold;
+  constexpr uint32_t kFitFlags = sa::kFlagFitWindows | sa::kFlagFitMember32;
+  Candidates<sa::DevFit> c;
+  if (n <= 64) {
+    // small queue: order, request fields and layout in registers, no LDS (the windowed
+    // replay's keys must fit)
+    const int waves = reg_waves(chains), grid = (chains + waves - 1) / waves;
+    c.add(sa::kFlagFitWindows, kFitFlags, [=](const sa::DevFit &d) {
+      if (srch.objective)
+        sa::anneal_reg_fit_kernel<1><<<grid, waves * 64, 0, stream>>>(d, qp, tpot_thr, chains, iters, T0, alpha, k0,
+                                                                      k1, st, srch, w);
+      else
+        sa::anneal_reg_fit_kernel<0><<<grid, waves * 64, 0, stream>>>(d, qp, tpot_thr, chains, iters, T0, alpha, k0,
+                                                                      k1, st, srch, w);
+      return hipGetLastError();
+    });
   }
+  const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
+  const size_t lds = (((size_t)n * 16 + 15) & ~size_t(15)) + 4 * (2 * pb + 2 * fb);
+  const int grid = (chains + 3) / 4;
+  c.add(0u, kFitFlags, [=](const sa::DevFit &d) {
+    if (srch.objective)
+      sa::anneal_fit_kernel<1><<<grid, 256, lds, stream>>>(d, qp, tpot_thr, chains, iters, T0, alpha, k0, k1, st, srch,
+                                                           w);
+    else
+      sa::anneal_fit_kernel<0><<<grid, 256, lds, stream>>>(d, qp, tpot_thr, chains, iters, T0, alpha, k0, k1, st, srch,
+                                                           w);
+    return hipGetLastError();
+  });
+  sa::start_fit_kernel<<<1, 1024, 0, stream>>>(c.checker(df, kFitFlags), qp, tpot_thr, chains, iters, fit->t_ref, srch,
+                                               w);
+  HIP_TRY(hipGetLastError());
+  if ((rc = c.run(df))) return rc;
   sa::reduce_kernel<<<1, 1024, 0, stream>>>(w);
   HIP_TRY(hipGetLastError());
   return SCHED_OK;

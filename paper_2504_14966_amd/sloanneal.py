@@ -20,7 +20,12 @@ SCHED_OK, SCHED_EINVAL, SCHED_ENOSPC, SCHED_ERANGE, SCHED_EHIP = 0, -1, -2, -3, 
 EXPORTS = ("sched_eval", "sched_eval_batches", "sched_ws_bytes", "sched_anneal", "sched_anneal_ex", "sched_levels",
            "sched_best", "sched_chains", "sched_start_info", "sched_starts", "sched_gen_perms", "sched_assign",
            "sched_ws_bytes_multi", "sched_anneal_multi", "sched_multi_instance_ws", "sched_multi_best",
-           "sched_eval_fit", "sched_anneal_fit", "sched_accept_check", "sched_anneal_noalloc", "sched_strerror")
+           "sched_eval_fit", "sched_anneal_fit", "sched_accept_check", "sched_anneal_noalloc", "sched_status",
+           "sched_strerror")
+# width flags of the device checks (sched_status word 1)
+FLAG_NARROW_PREFILL, FLAG_LIST_SCHED, FLAG_NARROW_TIME, FLAG_WINDOWS = 1, 2, 4, 8
+FLAG_STATIC_NARROW, FLAG_TIME32, FLAG_FIT_WINDOWS, FLAG_FIT_MEMBER32 = 16, 32, 64, 128
+FLAG_INST64, FLAG_INST192 = 256, 512
 KIND_TTFT_TPOT = 3
 POLICY_STATIC, POLICY_CONTINUOUS, POLICY_STATIC_SEARCH = 0, 1, 2
 OBJ_LEX, OBJ_RATIO = 0, 1
@@ -105,6 +110,8 @@ def load_library(path: str = LIB_PATH):
     L.sched_anneal_noalloc.restype = C.c_int
     L.sched_accept_check.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sched_accept_check.restype = C.c_int
+    L.sched_status.argtypes = [vp, vp, vp]
+    L.sched_status.restype = C.c_int
     L.sched_strerror.argtypes = [C.c_int]
     L.sched_strerror.restype = C.c_char_p
     _lib = L
@@ -267,6 +274,15 @@ def sched_best(ws: torch.Tensor, n: int, stream=None):
     return perm, key
 
 
+def sched_status(ws: torch.Tensor, stream=None) -> torch.Tensor:
+    """The device checks' verdict of the last annealing call on ws (a single-queue, several-
+    instance or instance workspace): 3 int64 on the device (status, width flags, selected
+    kernel among the call's candidates or -1)."""
+    out = torch.empty(3, dtype=torch.int64, device=ws.device)
+    _check(load_library().sched_status(_ptr(ws), _ptr(out), _stream(stream)))
+    return out
+
+
 def sched_chains(ws: torch.Tensor, n: int, chains: int, perms: bool = False, stream=None):
     rec = torch.empty((chains, 8), dtype=torch.int64, device=ws.device)
     cur = best = None
@@ -347,6 +363,10 @@ def sched_anneal_multi(dq: DeviceQueue, model, inst_of: torch.Tensor, instances:
                                 _ptr(inst_of), int(instances), int(chains), int(iters), float(T0), float(alpha),
                                 int(seed) & (2**64 - 1), _ptr(mws.buf), int(mws.buf.numel()), _stream(stream)))
     return mws
+
+
+def sched_multi_status(mws: MultiWorkspace, stream=None) -> torch.Tensor:
+    return sched_status(mws.buf, stream)
 
 
 def sched_multi_best(mws: MultiWorkspace, stream=None):

@@ -1,0 +1,311 @@
+"""The boundary's asynchrony and its device-side checks of the queue.
+
+* No entry point blocks: sched_eval, sched_eval_batches, sched_anneal_ex, sched_anneal_fit,
+  sched_assign and sched_anneal_multi all return while a long annealing run enqueued before
+  them on the same stream is still running, and their results equal those of the same calls
+  on an idle stream.
+* A queue whose contents fail the checks (an entry out of range, an instance index or a
+  capacity out of range, overflow risk of the int64 clock) makes the outputs read as the
+  header documents, and sched_status reports the code; a later good call on the same
+  workspace reads normally again.
+* The width flags the device derives from the queue (which pick the kernel) equal an exact
+  big-integer evaluation of the same bounds, on random queues and models spread across the
+  bounds' edges, and the kernel each call selects is the expected candidate.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.dirname(__file__))
+from paper_2504_14966_amd.workloads import Model, Queue, random_queue, workload  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sl():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2504_14966_amd.sloanneal as m
+    m.load_library()
+    return m
+
+
+def _copy(q):
+    return Queue(q.in_len.copy(), q.out_len.copy(), q.kind.copy(), q.thr_us.copy())
+
+
+# ---- exact evaluation of the device checks' bounds (Python integers, no rounding) ----
+
+def expected_plan(q, m, ratio=False, max_kind=2):
+    """(status, flags) of the device checks for an integer latency model."""
+    n, B = int(q.n), int(m.max_batch)
+    lin = [int(v) for v in q.in_len]
+    lout = [int(v) for v in q.out_len]
+    if any(L < 1 for L in lout) or any(int(k) > max_kind for k in q.kind) or any(int(t) > 0xFFFFFFFE for t in q.thr_us):
+        return -1, 0
+    p0, p1, d0, d1, d2 = (int(m.p0), int(m.p1), int(m.d0), int(m.d1), int(m.d2))
+    b = min(n, B)
+    lmax, Lmax, slin, sL = max(lin), max(lout), sum(lin), sum(lout)
+    sctx = sum(L * l + L * (L + 1) // 2 for l, L in zip(lin, lout))
+    pre = n * p0 + p1 * slin
+    end = pre + sL * (d0 + d1 * b + d2 * b * (lmax + Lmax))
+    flags = 0
+    pf1 = p0 + p1 * lmax
+    cmax = b * (lmax + Lmax)
+    narrow = pf1 * b < 2**32 and cmax < 2**32 and d0 + d1 * b + d2 * cmax < 2**32 and d2 * b < 2**32
+    tl = pre + (d0 + d1) * sL + d2 * sctx
+    if narrow:
+        flags |= 1
+        if sL < 2**22 and pre < 2**32:
+            flags |= 2
+            if tl < 2**32:
+                flags |= 4
+    if end < 2**57:
+        flags |= 8
+    fmax = b * pf1 + Lmax * d0 + b * (d1 * Lmax + d2 * (lmax * Lmax + Lmax * (Lmax + 1) // 2))
+    inner = 2 * (d1 + d2 * lmax) + d2 + d2 * Lmax
+    if fmax < 2**32 - 1 and inner < 2**24 and d2 < 2**24 and b * Lmax * inner < 2**32 and d0 < 2**24:
+        flags |= 16
+        if tl < 2**32 - 2:
+            flags |= 32
+    tsum = end * n
+    tref = int(m.t_ref_us) if int(m.t_ref_us) > 0 else tsum
+    if not tsum < 2**62 or not tref * (n + 1) + tsum < 2**62 or (ratio and not tsum * (n + 1) < 2**62):
+        return -3, 0
+    return 0, flags
+
+
+def expected_fit_plan(q, f, ratio=False, max_kind=2):
+    n, B = int(q.n), int(f.max_batch)
+    if any(int(L) < 1 for L in q.out_len) or any(int(k) > max_kind for k in q.kind) or \
+            any(int(t) > 0xFFFFFFFE for t in q.thr_us):
+        return -1, 0
+    b = min(n, B)
+
+    def member(l, L):
+        return (f.ap * b * l + f.bp * b + f.cp * l + f.dp + L * (f.bd * b + f.dd) +
+                (f.ad * b + f.cd) * (L * l + L * (L + 1) // 2))
+    times = [member(int(l), int(L)) for l, L in zip(q.in_len, q.out_len)]
+    end = sum(times)
+    flags = (64 if end < 2**57 else 0) | (128 if max(times) < 2**32 - 1 else 0)
+    tsum = end * n
+    tref = int(f.t_ref) if int(f.t_ref) > 0 else tsum
+    if not tsum < 2**62 or not tref * (n + 1) + tsum < 2**62 or (ratio and not tsum * (n + 1) < 2**62):
+        return -3, 0
+    return 0, flags
+
+
+def _status(sl, ws):
+    return [int(v) for v in sl.sched_status(ws).cpu().tolist()]
+
+
+# ---- no call blocks ----
+
+def test_calls_return_while_earlier_work_runs(sl):
+    import torch
+    long_w = workload(4)  # 1024 requests; 4096 chains x 20000 proposals take about 0.1 s
+    dq_long = sl.DeviceQueue.from_queue(long_w.queue)
+    ws_long = sl.alloc_ws(long_w.queue.n, 4096)
+    W2, W5 = workload(2), workload(5)
+    dq2, dq5 = sl.DeviceQueue.from_queue(W2.queue), sl.DeviceQueue.from_queue(W5.queue)
+    perms = sl.sched_gen_perms(5, W5.queue.n, 4096)
+    starts = torch.zeros((4096, W5.queue.n), dtype=torch.uint8, device="cuda")
+    starts[:, ::W5.model.max_batch] = 1
+    fit = sl.FitModel(16, 0, **sl.TABLE2_10NS)
+    cap = torch.tensor([3000, 5000, 4000], dtype=torch.int64, device="cuda")
+    inst = torch.tensor(np.arange(W2.queue.n) % 3, dtype=torch.int32, device="cuda")
+    bufs = dict(ws2=sl.alloc_ws(64, 256), wsf=sl.alloc_ws(64, 64), mws=sl.MultiWorkspace(64, 3, 64),
+                ev=torch.empty((4096, 2), dtype=torch.int64, device="cuda"),
+                eb=torch.empty((4096, 2), dtype=torch.int64, device="cuda"))
+
+    def enqueue_all():
+        sl.sched_eval(dq5, W5.model, perms, out=bufs["ev"])
+        sl.sched_eval_batches(dq5, W5.model, perms, starts, out=bufs["eb"])
+        sl.sched_anneal(dq2, W2.model, 256, 500, W2.T0, W2.alpha, 3, ws=bufs["ws2"])
+        sl.sched_anneal_fit(dq2, fit, 64, 200, 1.0, 0.99, 4, ws=bufs["wsf"])
+        out = sl.sched_assign(dq2, cap)
+        sl.sched_anneal_multi(dq2, W2.model, inst, 3, 64, 200, W2.T0, W2.alpha, 5, mws=bufs["mws"])
+        return out
+
+    # warm-up on an idle stream: the reference results (and every first-call set-up done)
+    for v in bufs.values():
+        (v.buf if hasattr(v, "buf") else v).zero_()
+    ref_assign = enqueue_all().cpu()
+    torch.cuda.synchronize()
+    ref = {k: (v.buf if hasattr(v, "buf") else v).clone() for k, v in bufs.items()}
+    for v in bufs.values():
+        (v.buf if hasattr(v, "buf") else v).zero_()
+    torch.cuda.synchronize()
+    sl.sched_anneal(dq_long, long_w.model, 4096, 20000, long_w.T0, long_w.alpha, 1, ws=ws_long)
+    running = torch.cuda.Event()
+    running.record()
+    got_assign = enqueue_all()
+    still_running = not running.query()
+    torch.cuda.synchronize()
+    assert still_running, "a call waited for the work enqueued before it"
+    assert torch.equal(got_assign.cpu(), ref_assign)
+    for k, v in bufs.items():
+        assert torch.equal((v.buf if hasattr(v, "buf") else v), ref[k]), k
+
+
+# ---- failures reported through the outputs ----
+
+def test_anneal_reports_failed_checks_and_recovers(sl):
+    import ctypes as C
+    import torch
+    L = sl.load_library()
+    W = workload(2)
+    ws = sl.alloc_ws(64, 16)
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    sl.sched_anneal(dq, W.model, 16, 100, W.T0, W.alpha, 1, ws=ws)
+    good_perm, good_key = sl.sched_best(ws, 64)
+    good_perm, good_key = good_perm.cpu().clone(), good_key.cpu().tolist()
+    assert _status(sl, ws)[0] == 0 and good_key[0] >= 0
+    for field, val, code in (("out_len", 0, -1), ("kind", 7, -1), ("thr_us", 0xFFFFFFFF, -1)):
+        q = _copy(W.queue)
+        getattr(q, field)[17] = val
+        sl.sched_anneal(sl.DeviceQueue.from_queue(q), W.model, 16, 100, W.T0, W.alpha, 1, ws=ws)
+        st = _status(sl, ws)
+        assert st[0] == code and st[2] == -1, (field, st)
+        perm = torch.full((64,), 7, dtype=torch.int16, device="cuda")
+        key = torch.empty(3, dtype=torch.int64, device="cuda")
+        assert L.sched_best(C.c_void_p(ws.data_ptr()), C.c_void_p(perm.data_ptr()), C.c_void_p(key.data_ptr()),
+                            None) == 0
+        assert key.cpu().tolist() == [-2, code, -1]
+        assert bool((perm == 7).all())  # the output order is left untouched
+        rec = sl.sched_chains(ws, 64, 16).cpu().numpy()
+        assert (rec[:, 0] == -2).all() and (rec[:, 1] == code).all() and (rec[:, 2:] == -1).all()
+        _, info = sl.sched_start_info(ws, 64)
+        assert info.cpu().tolist() == [-2, code, -1, -1]
+    big = Model(16, 0, p0=2000, p1=40, d0=2**50, d1=300, d2=2)
+    sl.sched_anneal(dq, big, 16, 100, W.T0, W.alpha, 1, ws=ws)
+    assert _status(sl, ws)[0] == sl.SCHED_ERANGE
+    assert sl.sched_best(ws, 64)[1].cpu().tolist() == [-2, sl.SCHED_ERANGE, -1]
+    # a good call on the same workspace reads normally again
+    sl.sched_anneal(dq, W.model, 16, 100, W.T0, W.alpha, 1, ws=ws)
+    perm, key = sl.sched_best(ws, 64)
+    assert _status(sl, ws)[0] == 0
+    assert key.cpu().tolist() == good_key and torch.equal(perm.cpu(), good_perm)
+
+
+def test_ratio_bound_checked_on_device(sl):
+    # find a model whose plain bound holds and whose ratio bound fails, by the exact
+    # evaluation, then check the device agrees for both objectives
+    W = workload(2)
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    ws = sl.alloc_ws(64, 4)
+    d0 = 1
+    while True:
+        m = Model(16, 0, p0=2000, p1=40, d0=d0, d1=300, d2=2, t_ref_us=1)
+        if expected_plan(W.queue, m, ratio=True)[0] == -3:
+            break
+        d0 *= 2
+    assert expected_plan(W.queue, m)[0] == 0
+    sl.sched_anneal(dq, m, 4, 10, 1.0, 0.9, 1, ws=ws)
+    assert _status(sl, ws)[0] == 0
+    sl.sched_anneal(dq, m, 4, 10, 1.0, 0.9, 1, ws=ws, search=sl.Search(sl.OBJ_RATIO))
+    assert _status(sl, ws)[0] == sl.SCHED_ERANGE
+
+
+def test_fit_multi_and_assign_report_failed_checks(sl):
+    import torch
+    W = workload(2)
+    fit = sl.FitModel(16, 0, **sl.TABLE2_10NS)
+    q = _copy(W.queue)
+    q.kind[3] = 3  # the chat kind without the second threshold array
+    ws = sl.alloc_ws(64, 8)
+    sl.sched_anneal_fit(sl.DeviceQueue.from_queue(q), fit, 8, 10, 1.0, 0.9, 1, ws=ws)
+    assert _status(sl, ws)[0] == sl.SCHED_EINVAL
+    assert sl.sched_best(ws, 64)[1].cpu().tolist() == [-2, sl.SCHED_EINVAL, -1]
+    thr2 = sl.thr_to_device(np.full(64, 1000, np.uint32))
+    sl.sched_anneal_fit(sl.DeviceQueue.from_queue(q), fit, 8, 10, 1.0, 0.9, 1, ws=ws, tpot_thr=thr2)
+    assert _status(sl, ws)[0] == 0
+    # several instances: an instance index out of range
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    for bad_value in (3, -1):
+        inst = torch.tensor(np.arange(64) % 3, dtype=torch.int32, device="cuda")
+        inst[40] = bad_value
+        mws = sl.sched_anneal_multi(dq, W.model, inst, 3, 16, 10, 1.0, 0.9, 1)
+        assert _status(sl, mws.buf)[0] == sl.SCHED_EINVAL
+        orders, keys, counts = sl.sched_multi_best(mws)
+        assert keys.cpu().tolist() == [[-2, sl.SCHED_EINVAL, -1]] * 3 and counts.cpu().tolist() == [0, 0, 0]
+        for k in range(3):
+            assert sl.sched_best(mws.instance(k), 64)[1].cpu().tolist() == [-2, sl.SCHED_EINVAL, -1]
+    # assignment: a capacity out of range, or a bad queue entry
+    dq = sl.DeviceQueue.from_queue(W.queue)
+    for cap in ([1000, 0], [1000, 2**48 + 1], [-5, 1000]):
+        out = sl.sched_assign(dq, torch.tensor(cap, dtype=torch.int64, device="cuda"))
+        assert out.cpu().tolist() == [sl.SCHED_EINVAL] * 64
+    q = _copy(W.queue)
+    q.out_len[0] = 0
+    out = sl.sched_assign(sl.DeviceQueue.from_queue(q), torch.tensor([10**6], dtype=torch.int64, device="cuda"))
+    assert out.cpu().tolist() == [sl.SCHED_EINVAL] * 64
+
+
+# ---- the widths the device derives, against exact integers ----
+
+def _random_model(rng, B, policy):
+    def lu(lo_bits, hi_bits):
+        return int(2 ** rng.uniform(lo_bits, hi_bits)) if rng.random() < 0.9 else 0
+    return Model(B, policy, p0=lu(0, 34), p1=lu(0, 20), d0=lu(0, 30), d1=lu(0, 22), d2=lu(0, 26),
+                 t_ref_us=int(rng.choice([0, 1, 10**6, 2**40])))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_device_flags_match_exact_bounds(sl, seed):
+    rng = np.random.default_rng(1000 + seed)
+    ws = sl.alloc_ws(1024, 1)
+    checked = {0: 0, -3: 0}
+    for case in range(70):
+        n = int(rng.choice([1, 2, 7, 64, 65, 192, 256, 1024]))
+        B = int(rng.choice([1, 3, 16, 32, 64]))
+        policy = int(rng.choice([0, 1, 2]))
+        q = random_queue(rng, n)
+        if rng.random() < 0.5:  # long contexts: the 32-bit and 2^22 bounds come into play
+            q = Queue(rng.integers(0, 65536, n).astype(np.uint16), rng.integers(1, 65536, n).astype(np.uint16),
+                      q.kind, q.thr_us)
+        m = _random_model(rng, B, policy)
+        ratio = bool(rng.random() < 0.3) and m.p0 + m.d0 + m.d1 >= 1
+        want = expected_plan(q, m, ratio=ratio)
+        sl.sched_anneal(sl.DeviceQueue.from_queue(q), m, 1, 0, 1.0, 0.9, 0, ws=ws,
+                        search=sl.Search(sl.OBJ_RATIO if ratio else sl.OBJ_LEX))
+        st = _status(sl, ws)
+        assert (st[0], st[1]) == want, (case, n, B, policy, m, ratio, st, want)
+        checked[want[0]] = checked.get(want[0], 0) + 1
+    assert checked[0] >= 10 and checked[-3] >= 5, checked
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_device_fit_flags_match_exact_bounds(sl, seed):
+    rng = np.random.default_rng(2000 + seed)
+    ws = sl.alloc_ws(1024, 1)
+    for case in range(40):
+        n = int(rng.choice([1, 5, 64, 200, 1024]))
+        B = int(rng.choice([1, 8, 16, 64]))
+        q = random_queue(rng, n)
+        coef = {k: int(2 ** rng.uniform(0, 24)) for k in ("ap", "bp", "cp", "dp", "ad", "bd", "cd", "dd")}
+        f = sl.FitModel(B, int(rng.choice([0, 2])), **coef, t_ref=int(rng.choice([0, 1000])))
+        want = expected_fit_plan(q, f)
+        sl.sched_anneal_fit(sl.DeviceQueue.from_queue(q), f, 1, 0, 1.0, 0.9, 0, ws=ws)
+        st = _status(sl, ws)
+        assert (st[0], st[1]) == want, (case, n, B, coef, st, want)
+
+
+def test_selected_kernels(sl):
+    # (workload, expected candidate): the register kernel, the continuous list-scheduling
+    # kernel and the batch-per-wave delta kernel are each the first candidate of their call
+    ws = sl.alloc_ws(1024, 64)
+    for cfg in (2, 3, 4):
+        W = workload(cfg)
+        sl.sched_anneal(sl.DeviceQueue.from_queue(W.queue), W.model, 64, 0, W.T0, W.alpha, 0, ws=ws)
+        st = _status(sl, ws)
+        assert st[0] == 0 and st[2] == 0, (cfg, st)
+    # pair costs beyond 24 bits: the static delta kernels are out, the full replay runs
+    W = workload(2)
+    wide = Model(16, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2**25, t_ref_us=10**6)
+    sl.sched_anneal(sl.DeviceQueue.from_queue(W.queue), wide, 64, 0, 1.0, 0.9, 0, ws=ws)
+    st = _status(sl, ws)
+    assert st[0] == 0 and not st[1] & 16 and st[2] == 1, st

@@ -142,17 +142,32 @@ def test_empty_batch_of_rows(sl):
 
 
 def test_bad_queue_entries_rejected(sl):
+    # the queue's contents are checked on the device: every row reads (-2, code), detail
+    # is left untouched; both admission policies, with and without detail
+    import torch
     W = workload(1)
-    for field, val in (("out_len", 0), ("kind", 3)):
-        q = Queue(W.queue.in_len.copy(), W.queue.out_len.copy(), W.queue.kind.copy(), W.queue.thr_us.copy())
-        getattr(q, field)[2] = val
-        with pytest.raises(sl.SchedError) as e:
-            _eval(sl, q, W.model, np.arange(8, dtype=np.uint16)[None])
-        assert e.value.code == sl.SCHED_EINVAL
-    m = Model(4, 0, p0=2000, p1=40, d0=2**55, d1=300, d2=2)
-    with pytest.raises(sl.SchedError) as e:
-        _eval(sl, W.queue, m, np.arange(8, dtype=np.uint16)[None])
-    assert e.value.code == sl.SCHED_ERANGE
+    perms = np.stack([np.arange(8, dtype=np.uint16), np.arange(8, dtype=np.uint16)[::-1]])
+    for policy in (0, 1):
+        m = Model(4, policy, p0=2000, p1=40, d0=8000, d1=300, d2=2)
+        for field, val in (("out_len", 0), ("kind", 3), ("thr_us", 0xFFFFFFFF)):
+            q = Queue(W.queue.in_len.copy(), W.queue.out_len.copy(), W.queue.kind.copy(), W.queue.thr_us.copy())
+            getattr(q, field)[2] = val
+            assert _eval(sl, q, m, perms).tolist() == [[-2, sl.SCHED_EINVAL]] * 2
+            dq = sl.DeviceQueue.from_queue(q)
+            det = torch.full((2, 8, 2), 7, dtype=torch.int64, device="cuda")
+            out, _ = sl.sched_eval(dq, m, sl.perms_to_device(perms), detail=det)
+            assert out.cpu().tolist() == [[-2, sl.SCHED_EINVAL]] * 2
+            assert bool((det == 7).all())
+        big = Model(4, policy, p0=2000, p1=40, d0=2**55, d1=300, d2=2)
+        assert _eval(sl, W.queue, big, perms).tolist() == [[-2, sl.SCHED_ERANGE]] * 2
+    # the layout evaluation checks the same way
+    q = Queue(W.queue.in_len.copy(), W.queue.out_len.copy(), W.queue.kind.copy(), W.queue.thr_us.copy())
+    q.out_len[5] = 0
+    st = np.zeros((2, 8), np.uint8)
+    st[:, ::4] = 1
+    out = sl.sched_eval_batches(sl.DeviceQueue.from_queue(q), W.model, sl.perms_to_device(perms),
+                                sl.starts_to_device(st))
+    assert out.cpu().tolist() == [[-2, sl.SCHED_EINVAL]] * 2
 
 
 def test_fisher_yates_family(sl, orc):

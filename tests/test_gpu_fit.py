@@ -74,9 +74,10 @@ def test_eval_fit_worked_and_rejections(sl, orc):
         assert out[r].tolist() == [c["n"], c["t"]]
         assert det[r, :, 0].tolist() == c["ttft"] and det[r, :, 1].tolist() == c["e2e"]
     # the chat kind needs the second threshold array
+    # (checked on the device: every row reads (-2, SCHED_EINVAL))
     q3 = Queue(q.in_len, q.out_len, np.array([3, 2, 1], np.uint8), q.thr_us)
-    with pytest.raises(sl.SchedError):
-        sl.sched_eval_fit(sl.DeviceQueue.from_queue(q3), fd, sl.perms_to_device(perms))
+    bad = sl.sched_eval_fit(sl.DeviceQueue.from_queue(q3), fd, sl.perms_to_device(perms)).cpu().tolist()
+    assert bad == [[-2, sl.SCHED_EINVAL]] * len(perms)
     L = sl.load_library()
     bad = sl.FitModel(2, 1, **g["model_10ns"])   # continuous admission is not a fitted-model policy
     qq = dq.c()
