@@ -321,7 +321,8 @@ __global__ void __launch_bounds__(256) eval_sized_kernel(DevModel m, QueuePtrs q
                                                           const uint8_t *__restrict__ starts, int64_t rows,
                                                           int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
-  if (!eval_gate(q, m, rows, out)) return;
+  const EvalRows span = eval_gate(q, m, rows, out);
+  if (span.end <= span.begin) return;
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
@@ -339,7 +340,8 @@ __global__ void __launch_bounds__(256) eval_sized_kernel(DevModel m, QueuePtrs q
   __syncthreads();
   const int lane = lane_id();
   const int waves = blockDim.x >> 6;
-  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+  for (int64_t row = span.begin + (int64_t)blockIdx.x * waves + wave; row < span.end;
+       row += (int64_t)gridDim.x * waves) {
     const uint16_t *src = perms + row * n;
     const uint8_t *fsrc = starts + row * n;
     if (lane < 32) bitmap[lane] = 0u;

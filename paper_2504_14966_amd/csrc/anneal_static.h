@@ -677,7 +677,8 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
                                                            const uint16_t *__restrict__ perms, int64_t rows,
                                                            int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
-  if (!eval_gate(q, m, rows, out)) return;
+  const EvalRows span = eval_gate(q, m, rows, out);
+  if (span.end <= span.begin) return;
   constexpr int Bp = 1 << LG, G = kWave >> LG;
   const int n = m.n, B = m.B;
   const int M = (n + B - 1) / B, R = (M + G - 1) / G;
@@ -707,7 +708,8 @@ __global__ void __launch_bounds__(256) eval_static_kernel(DevModel m, StaticPara
   const int lane = lane_id();
   const int seg = lane >> LG, mm = lane & (Bp - 1);
   const uint32_t d2m = sp.d2 & 0xFFFFFFu;
-  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+  for (int64_t row = span.begin + (int64_t)blockIdx.x * waves + wave; row < span.end;
+       row += (int64_t)gridDim.x * waves) {
     const uint16_t *src = perms + row * n;
     if (lane < 32) bitmap[lane] = 0u;
     wave_sync_lds();

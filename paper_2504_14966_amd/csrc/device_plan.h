@@ -134,10 +134,14 @@ __host__ __device__ inline Plan plan_decide(const QueueStats &s, int n_, int B, 
   return p;
 }
 
+// The first candidate whose needs hold (the loop is unrolled so that the candidate list is
+// only ever indexed by constants and the model it travels in stays in registers).
 __host__ __device__ inline int32_t plan_select(const Gate &g, uint32_t flags) {
-  for (int c = 0; c < g.count; ++c)
-    if ((g.need[c] & flags) == g.need[c]) return c;
-  return -1;
+  int32_t sel = -1;
+#pragma unroll
+  for (int c = 3; c >= 0; --c)
+    if (c < g.count && (g.need[c] & flags) == g.need[c]) sel = c;
+  return sel;
 }
 
 // Static LDS the checks take in a workgroup (on top of a kernel's dynamic LDS).
@@ -241,18 +245,53 @@ __device__ __forceinline__ void error_rows(int64_t rows, int32_t status, int64_t
   }
 }
 
-// Evaluation launches (no workspace): every workgroup forms the plan from the queue; true
-// when this launch is the selected candidate, with the allowed flags added to m.flags. When
-// the queue fails the checks the last candidate writes the error rows.
-__device__ __forceinline__ bool eval_gate(const QueuePtrs &q, DevModel &m, int64_t rows, int64_t *out) {
-  const Plan p = plan_in_block(q, m);
-  if (p.status != 0) {
-    if (m.gate.self == m.gate.count - 1) error_rows(rows, p.status, out);
-    return false;
+// Evaluation calls have no workspace. The first candidate launched forms the verdict in
+// every workgroup: on a failed check it writes the error rows; when another candidate is
+// selected, its workgroup 0 leaves the verdict in row 0 of the output as a marker
+// (kEvalMarker - selected, flags) and no row is replayed. A later candidate reads the marker
+// and, when it is the one selected, replays rows 1 .. rows - 1; the fix-up launch after
+// every candidate (self == kEvalFixup) finds the marker still there and replays row 0. Row
+// 0 is written by no candidate that reads it, so no workgroup can see it overwritten.
+constexpr int64_t kEvalMarker = -16;
+constexpr int32_t kEvalFixup = -2;
+
+struct EvalRows {
+  int64_t begin, end;  // rows this launch replays (none when end <= begin)
+};
+
+// The launch's rows, with the allowed flags of the verdict added to `flags`. plan: forms the
+// verdict (called by the first candidate only).
+template <class PlanFn>
+__device__ __forceinline__ EvalRows eval_rows_of(PlanFn plan, const Gate &g, int64_t rows, int64_t *out,
+                                                 uint32_t &flags) {
+  if (g.self != 0) {
+    const int64_t mark = out[0];
+    const bool mine = g.self == kEvalFixup ? mark <= kEvalMarker : mark == kEvalMarker - g.self;
+    if (!mine) return EvalRows{0, 0};
+    flags |= (uint32_t)out[1] & g.allow;
+    return g.self == kEvalFixup ? EvalRows{0, 1} : EvalRows{1, rows};
   }
-  if (p.selected != m.gate.self) return false;
-  m.flags |= (int32_t)(p.flags & m.gate.allow);
-  return true;
+  const Plan p = plan();
+  if (p.status != 0) {
+    error_rows(rows, p.status, out);
+    return EvalRows{0, 0};
+  }
+  if (p.selected != 0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      out[0] = kEvalMarker - p.selected;
+      out[1] = (int64_t)p.flags;
+    }
+    return EvalRows{0, 0};
+  }
+  flags |= p.flags & g.allow;
+  return EvalRows{0, rows};
+}
+
+__device__ __forceinline__ EvalRows eval_gate(const QueuePtrs &q, DevModel &m, int64_t rows, int64_t *out) {
+  uint32_t f = 0u;
+  const EvalRows r = eval_rows_of([&]() { return plan_in_block(q, m); }, m.gate, rows, out, f);
+  m.flags |= (int32_t)f;
+  return r;
 }
 
 // The verdict into a workspace header (thread 0 of the checking workgroup).

@@ -54,15 +54,11 @@ __device__ __forceinline__ bool fit_gate_open(const unsigned char *ws, DevFit &f
   return true;
 }
 // As eval_gate, for the fitted-model evaluation.
-__device__ __forceinline__ bool eval_fit_gate(const QueuePtrs &q, DevFit &f, int64_t rows, int64_t *out) {
-  const Plan p = fit_plan_in_block(q, f);
-  if (p.status != 0) {
-    if (f.gate.self == f.gate.count - 1) error_rows(rows, p.status, out);
-    return false;
-  }
-  if (p.selected != f.gate.self) return false;
-  fit_take_flags(f, p.flags);
-  return true;
+__device__ __forceinline__ EvalRows eval_fit_gate(const QueuePtrs &q, DevFit &f, int64_t rows, int64_t *out) {
+  uint32_t flags = 0u;
+  const EvalRows r = eval_rows_of([&]() { return fit_plan_in_block(q, f); }, f.gate, rows, out, flags);
+  fit_take_flags(f, flags);
+  return r;
 }
 
 // Request record: x = l_in | l_out << 16, y = threshold, z = kind, w = second threshold.
@@ -274,7 +270,8 @@ __global__ void __launch_bounds__(256) eval_fit_kernel(DevFit f, QueuePtrs q, co
                                                         const uint8_t *__restrict__ starts, int64_t rows,
                                                         int64_t *__restrict__ out, int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
-  if (!eval_fit_gate(q, f, rows, out)) return;
+  const EvalRows span = eval_fit_gate(q, f, rows, out);
+  if (span.end <= span.begin) return;
   const int n = f.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
@@ -288,7 +285,8 @@ __global__ void __launch_bounds__(256) eval_fit_kernel(DevFit f, QueuePtrs q, co
   __syncthreads();
   const int lane = lane_id();
   const int waves = blockDim.x >> 6;
-  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+  for (int64_t row = span.begin + (int64_t)blockIdx.x * waves + wave; row < span.end;
+       row += (int64_t)gridDim.x * waves) {
     const uint16_t *src = perms + row * n;
     if (lane < 32) bitmap[lane] = 0u;
     wave_sync_lds();

@@ -46,7 +46,8 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
                                                        int64_t rows, int64_t *__restrict__ out,
                                                        int64_t *__restrict__ detail) {
   extern __shared__ __align__(16) unsigned char lds[];
-  if (!eval_gate(q, m, rows, out)) return;
+  const EvalRows span = eval_gate(q, m, rows, out);
+  if (span.end <= span.begin) return;
   const int n = m.n;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const bool ls = m.policy == 1 && (m.flags & kFlagListSched);
@@ -64,7 +65,8 @@ __global__ void __launch_bounds__(kBlock) eval_kernel(DevModel m, QueuePtrs q, c
   __syncthreads();
   const int lane = lane_id();
   const int waves = blockDim.x >> 6;
-  for (int64_t row = (int64_t)blockIdx.x * waves + wave; row < rows; row += (int64_t)gridDim.x * waves) {
+  for (int64_t row = span.begin + (int64_t)blockIdx.x * waves + wave; row < span.end;
+       row += (int64_t)gridDim.x * waves) {
     const uint16_t *src = perms + row * n;
     if (lane < 32) bitmap[lane] = 0u;
     wave_sync_lds();

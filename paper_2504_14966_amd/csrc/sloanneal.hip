@@ -568,19 +568,26 @@ int sched_eval(const sched_queue_t *queue, const sched_model_t *model, const uin
   while (waves > 1 && eval_lds_bytes(n, ls, waves) > lim) waves >>= 1;
   const size_t lds = eval_lds_bytes(n, ls, waves);
   const int grid = (int)std::min<int64_t>((k + waves - 1) / waves, 256 * 32);
-  c.add(0u, kEvalFlags, [=](const sa::DevModel &d) {
+  auto generic = [=](const sa::DevModel &d, int g) {
     const void *fn = detail ? (const void *)&sa::eval_kernel<true> : (const void *)&sa::eval_kernel<false>;
     if (lds > 65536) {
       const hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
     }
     if (detail)
-      sa::eval_kernel<true><<<grid, waves * 64, lds, stream>>>(d, qp, perms, k, out, detail);
+      sa::eval_kernel<true><<<g, waves * 64, lds, stream>>>(d, qp, perms, k, out, detail);
     else
-      sa::eval_kernel<false><<<grid, waves * 64, lds, stream>>>(d, qp, perms, k, out, nullptr);
+      sa::eval_kernel<false><<<g, waves * 64, lds, stream>>>(d, qp, perms, k, out, nullptr);
     return hipGetLastError();
-  });
-  return c.run(dm);
+  };
+  c.add(0u, kEvalFlags, [=](const sa::DevModel &d) { return generic(d, grid); });
+  if ((rc = c.run(dm)) || c.gate.count < 2) return rc;
+  // row 0 when a candidate other than the first replayed the rest (its verdict marker sits
+  // there until now)
+  sa::DevModel fix = c.checker(dm, kEvalFlags);
+  fix.gate.self = sa::kEvalFixup;
+  const hipError_t e = generic(fix, 1);
+  return e == hipSuccess ? SCHED_OK : hip_fail(e);
 }
 
 size_t sched_ws_bytes(int32_t n, int32_t chains) {

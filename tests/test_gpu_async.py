@@ -309,3 +309,41 @@ def test_selected_kernels(sl):
     sl.sched_anneal(sl.DeviceQueue.from_queue(W.queue), wide, 64, 0, 1.0, 0.9, 0, ws=ws)
     st = _status(sl, ws)
     assert st[0] == 0 and not st[1] & 16 and st[2] == 1, st
+
+
+@pytest.mark.parametrize("detail", [False, True])
+@pytest.mark.parametrize("rows", [1, 2, 5, 300])
+@pytest.mark.parametrize("which", ["pairs", "generic"])
+def test_eval_when_a_later_candidate_runs(sl, orc, detail, rows, which):
+    # the first candidate is not the one selected: its verdict waits in row 0 until the
+    # fix-up launch replays that row (here a row that is not a permutation, then a valid one)
+    import torch
+    rng = np.random.default_rng(rows + (7 if detail else 0))
+    q = random_queue(rng, 40, max_in=3000, max_out=250, thr_hi=4_000_000_000)
+    if which == "pairs":  # 24-bit pair costs hold, the timeline is wider than 32 bits
+        m = Model(8, 0, p0=5_000_000, p1=100, d0=8_000_000, d1=1000, d2=3)
+        want_flags = 16
+    else:  # pair costs beyond 24 bits: only the full replay
+        m = Model(8, 0, p0=2000, p1=40, d0=8000, d1=300, d2=2**25, t_ref_us=10**6)
+        want_flags = 0
+    ws = sl.alloc_ws(40, 1)
+    sl.sched_anneal(sl.DeviceQueue.from_queue(q), m, 1, 0, 1.0, 0.9, 0, ws=ws)
+    st = _status(sl, ws)
+    assert st[0] == 0 and st[1] & 48 == want_flags, st
+    perms = np.stack([rng.permutation(40) for _ in range(rows)]).astype(np.uint16)
+    for bad_first in (True, False):
+        p = perms.copy()
+        if bad_first:
+            p[0, 3] = p[0, 4]
+        dq = sl.DeviceQueue.from_queue(q)
+        det = torch.full((rows, 40, 2), 5, dtype=torch.int64, device="cuda") if detail else False
+        res = sl.sched_eval(dq, m, sl.perms_to_device(p), detail=det)
+        out = (res[0] if detail else res).cpu().numpy()
+        for r in range(rows):
+            want = orc.replay(q, m, p[r], detail=detail)
+            assert out[r].tolist() == list(want[:2]), (r, bad_first)
+            if detail and want[0] >= 0:
+                dd = det.cpu().numpy()
+                assert np.array_equal(dd[r, :, 0], want[2]) and np.array_equal(dd[r, :, 1], want[3]), r
+        if detail and bad_first:
+            assert bool((det[0] == 5).all())
