@@ -381,13 +381,23 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
         const int p = n0 + done + lane;
         LP = ((posr[p].x >> 16) << 10) | (uint32_t)p;
       }
-      uint32_t top = __builtin_amdgcn_readfirstlane(list);
-      for (int t = 0; t < S; ++t) {
-        const uint32_t nk = (top & ~1023u) + rl(LP, t);
+      // Step t pops lane t and admits the key (f_t << 10) + LP[t], formed in lane t by the
+      // vector unit and read out once: the step's dependence chain is the median, two
+      // vector operations and one lane read. Unrolled by hand (the lane operations are
+      // convergent, which keeps the compiler from unrolling a loop of run-time length).
+      auto step = [&](int t) {
+        const uint32_t nk = rl((list & ~1023u) + LP, t);
         const uint32_t below = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)list, kDppWaveShr1, 0xF, 0xF, true);
         list = med3_u32(below, list, nk);
-        top = rl(list, t + 1);
+      };
+      int t = 0;
+      for (; t + 4 <= S; t += 4) {
+        step(t);
+        step(t + 1);
+        step(t + 2);
+        step(t + 3);
       }
+      for (; t < S; ++t) step(t);
       if (lane < S) ev[done + lane] = list;
       const uint32_t moved = (uint32_t)__builtin_amdgcn_ds_bpermute((lane + S) << 2, (int)list);
       list = lane < n0 ? moved : kInf;
