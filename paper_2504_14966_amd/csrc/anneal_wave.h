@@ -122,16 +122,19 @@ struct WaveChain {
   __device__ __forceinline__ uint32_t slo(bool valid, uint32_t kind, uint32_t thr, uint32_t P, uint32_t Fv, uint64_t S,
                                           uint32_t &a_in, uint32_t &b_in) const {
     // thresholds are at most 2^32 - 2, so a start of 2^32 or more compares like 2^32 - 1
+    // (plain logical operations, no short-circuit: the vector code needs no branches)
     const uint32_t S32 = (S >> 32) ? 0xFFFFFFFFu : (uint32_t)S;
     const bool tpot = kind == 1u;
     const bool tpot_ok = Fv - P <= thr;
     const uint32_t off = kind == 0u ? P : Fv;
     const uint32_t sl = thr - off;
-    const bool always = tpot && tpot_ok;
-    const bool never = tpot ? !tpot_ok : off > thr;
-    const bool met = valid && (always || (!never && S32 <= sl));
-    a_in = (met && !always) ? sl : 0xFFFFFFFFu;
-    b_in = (valid && !met && !never) ? sl + 1u : 0u;
+    // flex: a TTFT or end-to-end member whose offset alone does not exceed the threshold,
+    // met iff S <= sl; a TPOT member is met iff tpot_ok, whatever S
+    const bool flex = valid & !tpot & !(off > thr);
+    const bool in = S32 <= sl;
+    const bool met = (flex & in) | (valid & tpot & tpot_ok);
+    a_in = (flex & in) ? sl : 0xFFFFFFFFu;
+    b_in = (flex & !in) ? sl + 1u : 0u;
     return (uint32_t)__popcll(__ballot(met));
   }
 
@@ -218,9 +221,9 @@ struct WaveChain {
     const uint32_t o = t0.x, e = t0.y, Lo = t0.z, eo = t0.w;
     const uint32_t Le = t1.x, ee = t1.y, dP = t1.z, corr = t1.w;
     const uint32_t FeBase = t2.x, kinde = t2.y, thre = t2.z, Pc = t2.w;
-    // lanes past the batch read the zero spare record and F[n] = 0
-    uint32_t r = N;
-    if (valid) r = perm[k * B + lane];
+    // lanes past the batch read the zero spare record and F[n] = 0 (their position is
+    // clamped into the order and the read discarded, so that the row has no branch)
+    const uint32_t r = valid ? (uint32_t)perm[min(k * B + lane, N - 1)] : (uint32_t)N;
     const uint4 rq = req[r];
     const uint32_t Fm = F[r];
     const uint32_t Lm = rq.x >> 16, em = rq.z >> 2;
@@ -259,8 +262,7 @@ struct WaveChain {
   __device__ void recount_row(int k, int64_t shift, int64_t &dn) {
     const int q0 = k * B;
     const bool valid = lane < batch_size(k);
-    uint32_t r = N;
-    if (valid) r = perm[q0 + lane];
+    const uint32_t r = valid ? (uint32_t)perm[min(q0 + lane, N - 1)] : (uint32_t)N;
     const uint4 rq = req[r];
     const uint32_t Fm = F[r];
     const uint64_t S = start_of(cur, k) + (uint64_t)shift;

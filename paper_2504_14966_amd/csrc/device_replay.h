@@ -62,26 +62,29 @@ __device__ __forceinline__ void apply_move_lds(T *perm, int type, int i, int j, 
     // per round suffices (LDS accesses of a wave execute in order)
     const T x = perm[i];
     // four named values rather than an array: an array of 16-byte records is not kept in
-    // registers by the compiler, which then stages it in scratch memory
+    // registers by the compiler, which then stages it in scratch memory. A lane past the
+    // range writes to position j instead of skipping its store (no branch): j is written
+    // last, with the moved entry, and no read of j follows a write to it (reads of a round
+    // come first, and only the last round reaches j).
     if (i < j) {
       for (int c0 = i; c0 < j; c0 += 4 * kWave) {
         const int p = c0 + lane;
         const T v0 = perm[min(p + 1, j)], v1 = perm[min(p + kWave + 1, j)];
         const T v2 = perm[min(p + 2 * kWave + 1, j)], v3 = perm[min(p + 3 * kWave + 1, j)];
-        if (p < j) perm[p] = v0;
-        if (p + kWave < j) perm[p + kWave] = v1;
-        if (p + 2 * kWave < j) perm[p + 2 * kWave] = v2;
-        if (p + 3 * kWave < j) perm[p + 3 * kWave] = v3;
+        perm[min(p, j)] = v0;
+        perm[min(p + kWave, j)] = v1;
+        perm[min(p + 2 * kWave, j)] = v2;
+        perm[min(p + 3 * kWave, j)] = v3;
       }
     } else {
       for (int c0 = i; c0 > j; c0 -= 4 * kWave) {
         const int p = c0 - lane;
         const T v0 = perm[max(p - 1, j)], v1 = perm[max(p - kWave - 1, j)];
         const T v2 = perm[max(p - 2 * kWave - 1, j)], v3 = perm[max(p - 3 * kWave - 1, j)];
-        if (p > j) perm[p] = v0;
-        if (p - kWave > j) perm[p - kWave] = v1;
-        if (p - 2 * kWave > j) perm[p - 2 * kWave] = v2;
-        if (p - 3 * kWave > j) perm[p - 3 * kWave] = v3;
+        perm[max(p, j)] = v0;
+        perm[max(p - kWave, j)] = v1;
+        perm[max(p - 2 * kWave, j)] = v2;
+        perm[max(p - 3 * kWave, j)] = v3;
       }
     }
     if (lane == 0) perm[j] = x;
