@@ -451,18 +451,19 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     const uint32_t dC = v ? b * s - outq + la : 0u;  // two's complement: a signed change
     const uint32_t dCi = scan_add32(dC);
     const uint32_t Ck = Ccarry + dCi - dC;
-    TT seg = 0;
-    if (v) seg = (TT)s * (TT)(d0 + d1 * b + d2 * Ck) + (TT)(d2 * b) * (TT)((s * (s + 1u)) >> 1);
+    // (lanes past the events, none when 64 divides n, have s = 0 and so seg = 0; they read
+    // clamped positions and store to entry 0 of each array, which no read uses, so that the
+    // passes have no branches)
+    const TT seg = (TT)s * (TT)(d0 + d1 * b + d2 * Ck) + (TT)(d2 * b) * (TT)((s * (s + 1u)) >> 1);
     const TT SEG = segcarry + scan_add(seg);
     const uint32_t PRE = precarry + scan_add32(pfa);
     const uint32_t rs = max(rscarry, scan_max32((v && (k == 1 || s != 0)) ? (uint32_t)k : 0u));
-    const uint32_t fnext = k < N ? (ev[k] >> 10) : kInf;
-    if (v) {
-      preA[k] = PRE;
-      rsA[k] = rs;
-      segA[k] = SEG;
-      if (k == N || fnext != f) runpre[rs] = PRE;
-    }
+    const uint32_t fnext = k < N ? (ev[min(k, N - 1)] >> 10) : kInf;
+    const int kw = v ? k : 0;
+    preA[kw] = PRE;
+    rsA[kw] = rs;
+    segA[kw] = SEG;
+    runpre[(v && (k == N || fnext != f)) ? rs : 0u] = PRE;
     fcarry = rl(f, kWave - 1);
     Ccarry += rl(dCi, kWave - 1);
     segcarry = rl_any(SEG, kWave - 1);
@@ -477,28 +478,22 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
   for (int c0 = 0; c0 < N; c0 += kWave) {
     const int k = c0 + lane + 1;
     const bool v = k <= N;
-    uint32_t q = 0, rsk = 1;
-    TT SEG = 0;
-    if (v) {
-      q = ev[k - 1] & 1023u;
-      rsk = rsA[k];
-      SEG = segA[k];
-    }
-    const TT e2e = PR0 + SEG + (TT)(rsk > 1 ? preA[rsk - 1] : 0u);
-    if (v && k <= nadm) tta[k] = PR0 + SEG + (TT)runpre[rsk];
+    const int kc = min(k, N);
+    const uint32_t q = v ? (ev[kc - 1] & 1023u) : 0u, rsk = v ? rsA[kc] : 1u;
+    const TT SEG = v ? segA[kc] : (TT)0;
+    const TT e2e = PR0 + SEG + (TT)(rsk > 1 ? preA[max(rsk, 2u) - 1] : 0u);
+    tta[(v && k <= nadm) ? k : 0] = PR0 + SEG + (TT)runpre[rsk];
     wave_sync_lds();
-    bool met = false;
-    if (v) {
-      const uint4 rq = posr[q];
-      const TT ttft = (int)q < n0 ? PR0 : tta[q - n0 + 1];
-      const uint32_t kind = rq.z & 3u, thr = rq.y, L = rq.x >> 16;
-      met = kind == 0 ? ttft <= (TT)thr : (kind == 2 ? e2e <= (TT)thr : (uint64_t)(e2e - ttft) <= (uint64_t)thr * L);
-      tsum += (uint64_t)e2e;
-      if (DETAIL) {
-        const int r = perm[rm.src((int)q)];
-        detail[2 * r] = (int64_t)ttft;
-        detail[2 * r + 1] = (int64_t)e2e;
-      }
+    const uint4 rq = posr[q];
+    const TT ttft = (int)q < n0 ? PR0 : tta[max((int)q - n0 + 1, 0)];
+    const uint32_t kind = rq.z & 3u, thr = rq.y, L = rq.x >> 16;
+    const bool met = v & (kind == 0 ? ttft <= (TT)thr
+                                    : (kind == 2 ? e2e <= (TT)thr : (uint64_t)(e2e - ttft) <= (uint64_t)thr * L));
+    tsum += v ? (uint64_t)e2e : 0ull;
+    if (DETAIL && v) {
+      const int r = perm[rm.src((int)q)];
+      detail[2 * r] = (int64_t)ttft;
+      detail[2 * r + 1] = (int64_t)e2e;
     }
     nmet += __popcll(__ballot(met));
   }
