@@ -11,7 +11,11 @@ SRC = os.path.join(HERE, "csrc", "sloanneal.hip")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off",
          "-fno-fast-math", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-Wall", "-Wno-unused-function"]
+         "-Wall", "-Wno-unused-function",
+         # small register arrays indexed by constants stay separate registers (split by the
+         # scalar replacement pass); the target's alloca-to-vector promotion would instead
+         # hold them as one vector value, copied whole wherever an element changes
+         "-mllvm", "-disable-promote-alloca-to-vector"]
 
 
 def build(extra: list[str] | None = None, out: str = LIB) -> str:

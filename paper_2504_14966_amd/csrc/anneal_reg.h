@@ -35,12 +35,6 @@ __device__ __forceinline__ uint32_t dppv(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
 }
 
-// v_writelane of a wave-uniform value into lane k (lane select in m0)
-__device__ __forceinline__ uint32_t wlane_m0(uint32_t v, int k, uint32_t old) {
-  asm volatile("v_writelane_b32 %0, %1, m0" : "=v"(old) : "s"(v), "{m0}"(k), "0"(old));
-  return old;
-}
-
 // sum over the other members j of the lane's batch of mu (e_j + d2 mu), mu = min(L_j, L)
 template <int LG>
 __device__ __forceinline__ uint32_t pair_sum_others(uint32_t L, uint32_t e, uint32_t d2, int lane) {

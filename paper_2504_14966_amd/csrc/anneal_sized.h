@@ -20,6 +20,7 @@
 // widths), the evaluation kernel over K (order, layout) rows and the full-replay annealing
 // kernel. The delta kernel for queues whose timelines fit 32 bits is further below.
 #pragma once
+#include <utility>
 #include "device_common.h"
 #include "device_replay.h"
 #include "device_rng.h"
@@ -563,15 +564,16 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
 
 // ---- delta kernel: timelines that fit 32 bits ----
 //
-// Per chain (one wave), in LDS:
+// Per chain (one wave). In LDS:
 //   perm, flags   the current order and layout;
-//   F[r]          request r's finish offset within its batch, prefill included (u32);
-//   S[p]          start time of the batch holding position p (u32); S[n] = end of the
-//                 timeline;
-//   lim[p]        the member at p meets its SLO iff S[p] < lim[p] (u32): thr - P + 1 for
-//                 TTFT (P = batch prefill), thr - F + 1 for end-to-end, all or nothing for
+//   F[r]          request r's finish offset within its batch, prefill included (u32).
+// In registers, position p in row p / 64, lane p % 64 (NR rows):
+//   S             start time of the batch holding p (u32);
+//   lim           the member at p meets its SLO iff S < lim (u32): thr - P + 1 for TTFT
+//                 (P = batch prefill), thr - F + 1 for end-to-end, all or nothing for
 //                 TPOT (F - P against thr * l_out, which does not depend on the start);
-//                 0 when it can never be met.
+//                 0 when it can never be met, and past the last position;
+// and the end of the timeline as one wave-uniform value.
 // A move changes the members of at most two batches (A before C). Each is scored in one
 // pass with its new members in lanes: a member that stays gets
 //   F' = F + [pf(g) + w(g, m) / 2] - [pf(o) + w(o, m) / 2]
@@ -579,12 +581,14 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
 //   F'(g) = P' + L_g d0 + sum over the new members j of w(j, g) / 2,
 // with w(j, m) = mu (e_j + d2 mu), mu = min(L_j, L_m), e_j = 2 (d1 + d2 l_j) + d2, twice
 // what j adds to m's decode iterations. Three DPP reductions give P', the newcomer's sum
-// and the new duration. Every request of the two batches is counted once, in its new
-// batch, against its old start, offset and limit (read at its old position), so the
-// changes of n and t over them are lane sums. Later batches keep their members and only
+// and the new duration. The two batches keep their members between them, so the change
+// of t over them is a lane sum of new minus old latencies (old start: that of the old
+// batch holding the member's old position). Later batches keep their members and only
 // shift: by D'(A) - D(A) between A and C (swap), by the change of the end of the two
-// batches after C; their met counts are recounted position by position (S + shift <
-// lim). Nothing is written until the proposal is accepted.
+// batches after C. One pass over the register rows from A on counts the change of the met
+// flags by position: the positions of A and C lose their old flags (their new ones come
+// from the batch passes), the shifted ones compare S + shift with lim. Nothing is written
+// until the proposal is accepted.
 //
 // Widths (host check): every finish offset, batch prefill, doubled pair-cost sum over a
 // batch and 24-bit multiply operand as in the fixed-size delta kernel, and every time on
@@ -594,10 +598,63 @@ struct SizedState {
   const uint4 *req;
   uint16_t *perm;
   uint8_t *flags;
-  uint32_t *F, *S, *lim;
+  uint32_t *F;
   int n, B, lane;
   uint32_t d0, d2;
 };
+
+// f(integral_constant<int, u>) for u = 0 .. N-1: the row loops index their arrays with
+// constants from the start (a loop variable, even one unrolled later, turns an array into
+// one vector value that the compiler copies whole wherever an element changes)
+template <class F, int... I>
+__device__ __forceinline__ void static_for_seq(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_seq(f, std::make_integer_sequence<int, N>{});
+}
+
+// Rows of a wave's positions (S, lim) are plain register arrays indexed by constants only:
+// the row of a single position is picked by a wave-uniform branch tree, so that every row
+// keeps a register of its own.
+template <int LO, int HI, int NR>
+__device__ __forceinline__ uint32_t row_lane(const uint32_t (&v)[NR], int u, int l) {
+  if constexpr (HI - LO == 1) {
+    return readlane(v[LO], l);
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (u < MID) return row_lane<LO, MID>(v, u, l);
+    return row_lane<MID, HI>(v, u, l);
+  }
+}
+template <int LO, int HI, int NR>
+__device__ __forceinline__ void set_row_lane(uint32_t (&v)[NR], int u, int l, uint32_t x) {
+  if constexpr (HI - LO == 1) {
+    v[LO] = wlane_m0(x, l, v[LO]);
+  } else {
+    constexpr int MID = (LO + HI) / 2;
+    if (u < MID)
+      set_row_lane<LO, MID>(v, u, l, x);
+    else
+      set_row_lane<MID, HI>(v, u, l, x);
+  }
+}
+template <int NR>
+__device__ __forceinline__ uint32_t start_at(const uint32_t (&S)[NR], uint32_t end, int x, int n) {
+  const int xc = min(x, n - 1);
+  const uint32_t v = row_lane<0, NR>(S, xc >> 6, xc & 63);
+  return x >= n ? end : v;  // position n: the end of the timeline
+}
+template <int NR>
+__device__ __forceinline__ void swap_lims(uint32_t (&lim)[NR], int x, int y) {
+  const uint32_t a = row_lane<0, NR>(lim, x >> 6, x & 63), b = row_lane<0, NR>(lim, y >> 6, y & 63);
+  set_row_lane<0, NR>(lim, x >> 6, x & 63, b);
+  set_row_lane<0, NR>(lim, y >> 6, y & 63, a);
+}
+
+// Number of register rows for n positions (the kernel is instantiated for these).
+__host__ __device__ constexpr int sized_rows_for(int n) { return n <= 128 ? 2 : (n <= 256 ? 4 : (n <= 512 ? 8 : 16)); }
 
 // limit of a member: met iff batch start < limit
 __device__ __forceinline__ uint32_t member_limit(uint32_t kind, uint32_t thr, uint32_t P, uint32_t F) {
@@ -613,109 +670,101 @@ struct BatchNew {
   uint32_t D;
 };
 
+// Scores the changed batch [xs, xe) (xe > xs) with new start SX: adds to dt the change of
+// its members' latencies (old start S0 for old positions before ob, S1 from ob on) and to
+// the lane counter met whether the lane's member meets its SLO in the new batch. Lanes
+// past the batch read its last member's records and are masked out.
 __device__ __forceinline__ BatchNew batch_pass(const SizedState &c, int xs, int xe, const Remap &rm, int g, int o,
-                                               uint32_t SX, int64_t &dt, int &dn) {
+                                               uint32_t SX, int ob, uint32_t S0, uint32_t S1, int64_t &dt, int &met) {
   const int lane = c.lane;
   const int p = xs + lane;
   const bool act = p < xe;
+  const int q = rm.src(min(p, xe - 1));
+  const int r = c.perm[q];
+  const Req rq = load_req(c.req, r);
+  // absent g or o read the spare all-zero record: its prefill and pair costs vanish
   const Req rg = load_req(c.req, g >= 0 ? g : c.n), ro = load_req(c.req, o >= 0 ? o : c.n);
-  uint32_t pf = 0, tsum = 0, Fst = 0, kind = 0, thr = 0, Fold = 0, Sold = 0, limold = 0;
-  int r = 0;
-  if (act) {
-    const int q = rm.src(p);
-    r = c.perm[q];
-    const Req rq = load_req(c.req, r);
-    kind = rq.kind;
-    thr = rq.thr;
-    pf = rq.pf;
-    Fold = c.F[r];
-    Sold = c.S[q];
-    limold = c.lim[q];
-    if (g >= 0) tsum = w2(rq.L, rq.e, rg.L, c.d2);
-    if (r != g) {
-      uint32_t f = Fold;
-      if (g >= 0) f += rg.pf + (w2(rg.L, rg.e, rq.L, c.d2) >> 1);
-      if (o >= 0) f -= ro.pf + (w2(ro.L, ro.e, rq.L, c.d2) >> 1);
-      Fst = f;
-    }
-  }
-  uint32_t P = pf, T = tsum, Mx = Fst;
+  const uint32_t Fold = c.F[r];
+  const uint32_t f = Fold + rg.pf + (w2(rg.L, rg.e, rq.L, c.d2) >> 1) - ro.pf - (w2(ro.L, ro.e, rq.L, c.d2) >> 1);
+  const bool newcomer = r == g;
+  uint32_t P = act ? rq.pf : 0u, T = act ? w2(rq.L, rq.e, rg.L, c.d2) : 0u, Mx = (act && !newcomer) ? f : 0u;
   Seg<6>::template all3<OpAdd, OpAdd, OpMax>(P, T, Mx, lane);
   const uint32_t Fg = g >= 0 ? P + __umul24(rg.L, c.d0) + (T >> 1) : 0u;
-  const uint32_t Fn = (act && r == g) ? Fg : Fst;
-  const uint32_t limn = member_limit(kind, thr, P, Fn);
-  const bool met_new = act && SX < limn, met_old = act && Sold < limold;
-  dn += __popcll(__ballot(met_new)) - __popcll(__ballot(met_old));
-  if (act) dt += (int64_t)(SX + Fn) - (int64_t)(Sold + Fold);
+  const uint32_t Fn = newcomer ? Fg : f;
+  const uint32_t limn = member_limit(rq.kind, rq.thr, P, Fn);
+  met += (act && SX < limn) ? 1 : 0;
+  const uint32_t Sold = q < ob ? S0 : S1;
+  dt += act ? (int64_t)(SX + Fn) - (int64_t)(Sold + Fold) : 0;
   return BatchNew{Fn, limn, r, max(Mx, Fg)};
 }
 
-// met-count change of positions [a, b) when their batch starts move by delta (mod 2^32).
-// Long ranges take four chunks of 64 positions per round with every load issued before the
-// compares; short ones a chunk at a time.
-__device__ __forceinline__ int recount_shift(const SizedState &c, int a, int b, uint32_t delta) {
-  int dn = 0;
-  int c0 = a;
-  if (b - a > 2 * kWave) {
-    for (; c0 + 4 * kWave <= b; c0 += 4 * kWave) {
-      uint32_t sv[4], lv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        sv[u] = c.S[c0 + u * kWave + c.lane];
-        lv[u] = c.lim[c0 + u * kWave + c.lane];
-      }
-      uint32_t cnt_now = 0, cnt_was = 0;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        cnt_was += (uint32_t)__popcll(__ballot(sv[u] < lv[u]));
-        cnt_now += (uint32_t)__popcll(__ballot(sv[u] + delta < lv[u]));
-      }
-      dn += (int)cnt_now - (int)cnt_was;
+// Change of the met flags by position from b0 on: [b0, b1) and [b2, b3) lose their old
+// flags, [b1, b2) moves by sM, [b3, n) by sE (b0 <= b1 <= b2 <= b3). Rows wholly before b0
+// are skipped, rows wholly inside one shifted range take one compare per position.
+template <int NR>
+__device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32_t (&lim)[NR], int lane, int b0, int b1,
+                                           int b2, int b3, uint32_t sM, uint32_t sE) {
+  int cnt = 0;
+  static_for<NR>([=, &S, &lim, &cnt](auto uc) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    const int base = u * kWave;
+    if (base + kWave <= b0) return;
+    const uint32_t s = S[u], l = lim[u];
+    bool now;
+    if (base >= b3) {
+      now = s + sE < l;
+    } else if (base >= b1 && base + kWave <= b2) {
+      now = s + sM < l;
+    } else {
+      const int p = base + lane;
+      const bool chg = (unsigned)(p - b0) < (unsigned)(b1 - b0) || (unsigned)(p - b2) < (unsigned)(b3 - b2);
+      const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
+      now = !chg && s + d < l;
     }
-  }
-  for (; c0 < b; c0 += kWave) {
-    const int p = c0 + c.lane;
-    bool was = false, now = false;
-    if (p < b) {
-      const uint32_t sv = c.S[p], lv = c.lim[p];
-      was = sv < lv;
-      now = sv + delta < lv;
-    }
-    dn += __popcll(__ballot(now)) - __popcll(__ballot(was));
-  }
-  return dn;
+    cnt += (int)now - (int)(s < l);
+  });
+  return cnt;
 }
 
-// S[p] += delta for p in [a, b_incl]; long ranges four chunks per round, loads before stores
-__device__ __forceinline__ void apply_shift(const SizedState &c, int a, int b_incl, uint32_t delta) {
-  int c0 = a;
-  if (b_incl - a >= 2 * kWave) {
-    for (; c0 + 4 * kWave <= b_incl + 1; c0 += 4 * kWave) {
-      uint32_t sv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) sv[u] = c.S[c0 + u * kWave + c.lane];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) c.S[c0 + u * kWave + c.lane] = sv[u] + delta;
+// The accepted move on the rows: A = [b0, b1) starts at SA with limits limA (by lane
+// position), C = [b2, b3) at SC with limC, [b1, b2) shifts by sM, [b3, n] by sE.
+template <int NR>
+__device__ __forceinline__ void row_apply(uint32_t (&S)[NR], uint32_t (&lim)[NR], uint32_t &end, int lane, int b0, int b1,
+                                          int b2, int b3, uint32_t sM, uint32_t sE, uint32_t SA, uint32_t SC,
+                                          uint32_t limA, uint32_t limC) {
+  static_for<NR>([=, &S, &lim](auto uc) __attribute__((always_inline)) {
+    constexpr int u = decltype(uc)::value;
+    const int base = u * kWave;
+    if (base + kWave <= b0) return;
+    if (base >= b3) {
+      S[u] += sE;
+      return;
     }
-  }
-  for (; c0 <= b_incl; c0 += kWave) {
-    const int p = c0 + c.lane;
-    if (p <= b_incl) c.S[p] += delta;
-  }
-}
-
-__device__ __forceinline__ void write_batch(const SizedState &c, int xs, int xe, const BatchNew &bn, uint32_t SX) {
-  const int p = xs + c.lane;
-  if (p < xe) {
-    c.F[bn.r] = bn.Fn;
-    c.S[p] = SX;
-    c.lim[p] = bn.limn;
-  }
+    if (base >= b1 && base + kWave <= b2) {
+      S[u] += sM;
+      return;
+    }
+    const int p = base + lane;
+    const bool inA = (unsigned)(p - b0) < (unsigned)(b1 - b0), inC = (unsigned)(p - b2) < (unsigned)(b3 - b2);
+    const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
+    S[u] = inA ? SA : (inC ? SC : S[u] + d);
+    lim[u] = inA ? limA : (inC ? limC : lim[u]);
+  });
+  end += sE;
 }
 
 // F, S, lim of an order with maximum-size batches; returns its (n, t).
-__device__ Score sized_init(const SizedState &c) {
+template <int NR>
+__device__ __forceinline__ Score sized_init(const SizedState &c, uint32_t (&S)[NR], uint32_t (&lim)[NR], uint32_t &end) {
   const int lane = c.lane;
+  // an opaque zero: stores of a constant would be merged into one block fill, after which
+  // the compiler keeps the rows as one vector value
+  uint32_t zero = 0u;
+  asm volatile("" : "+v"(zero));
+  static_for<NR>([&S, &lim, zero](auto uc) __attribute__((always_inline)) {
+    S[decltype(uc)::value] = zero;
+    lim[decltype(uc)::value] = zero;
+  });
   uint32_t Sc = 0;
   int64_t nmet = 0;
   uint64_t tl = 0;
@@ -736,20 +785,27 @@ __device__ Score sized_init(const SizedState &c) {
     const uint32_t limv = member_limit(rq.kind, rq.thr, P, F);
     if (act) {
       c.F[r] = F;
-      c.S[s + lane] = Sc;
-      c.lim[s + lane] = limv;
       tl += (uint64_t)(Sc + F);
     }
     nmet += __popcll(__ballot(act && Sc < limv));
+    // lane l holds position s + l: rotate into the rows' lanes
+    const uint32_t lr = (uint32_t)__shfl((int)limv, (lane - s) & 63);
+    static_for<NR>([=, &S, &lim](auto uc) __attribute__((always_inline)) {
+      constexpr int u = decltype(uc)::value;
+      const bool mine = (unsigned)(u * kWave + lane - s) < (unsigned)b;
+      S[u] = mine ? Sc : S[u];
+      lim[u] = mine ? lr : lim[u];
+    });
     Sc += D;
   }
-  if (lane == 0) c.S[c.n] = Sc;
+  end = Sc;
   wave_sync_lds();
   return Score{nmet, wave_sum_u64(tl)};
 }
 
-// One wave per chain, blockDim / 64 chains per workgroup.
-template <int OBJ>
+// One wave per chain, blockDim / 64 chains per workgroup, positions in NR register rows
+// (n <= 64 NR).
+template <int OBJ, int NR>
 __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticParams sp, QueuePtrs q, int chains,
                                                              int iters, double T0, double alpha, uint32_t key0,
                                                              uint32_t key1, SearchParams srch, unsigned char *ws) {
@@ -759,8 +815,8 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
   const int waves = blockDim.x >> 6;
   uint4 *req = reinterpret_cast<uint4 *>(lds);
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
-  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15), sb = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
-  const size_t per_wave = pb + fb + 2 * ub + sb;
+  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15);
+  const size_t per_wave = pb + fb + ub;
   const int wave = uniform((int)(threadIdx.x >> 6));
   unsigned char *wb = lds + (size_t)(n + 1) * 16 + (size_t)wave * per_wave;
   for (int r = threadIdx.x; r <= n; r += blockDim.x) {
@@ -784,9 +840,8 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
                reinterpret_cast<uint16_t *>(wb),
                wb + pb,
                reinterpret_cast<uint32_t *>(wb + pb + fb),
-               reinterpret_cast<uint32_t *>(wb + pb + fb + ub),
-               reinterpret_cast<uint32_t *>(wb + pb + fb + ub + sb),
                n, B, lane, sp.d0, sp.d2};
+  uint32_t S[NR], lim[NR], end;  // register rows (position p: row p / 64, lane p % 64)
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
   const int64_t t_ref = h->t_ref, allmet = h->allmet;
   const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
@@ -804,7 +859,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     gbest_f[p] = fl;
   }
   wave_sync_lds();
-  const Score s0 = sized_init(c);
+  const Score s0 = sized_init(c, S, lim, end);
   int64_t cn = s0.n, bn = s0.n, biter = -1, accepts = 0;
   uint64_t ct = s0.t, bt = s0.t, digest = kFnvOffset;
   Cooling cool{T0, alpha, srch.level_len, srch.level_len};
@@ -815,12 +870,13 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
     const int op = (int)(pk >> 20), i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     // plan: new ranges of the changed batches A = [as, ae) and C = [cs, ce), who joins and
-    // leaves each, the shifted ranges and the flag writes
+    // leaves each, the range between them (swap) and the flag writes; old positions
+    // before ob belonged to a batch starting at SA, the others to one starting at S1
     bool made = false, inside = false;
-    int as = 0, ae = 0, cs = 0, ce = 0, gA = -1, oA = -1, gC = -1, oC = -1, mid0 = 0, mid1 = 0, uend = n;
+    int as = 0, ae = 0, cs = 0, ce = 0, gA = -1, oA = -1, gC = -1, oC = -1, ob = n;
     int set0 = -1, clr0 = -1;
     Remap rm{0, 0, 0};
-    uint32_t SA = 0, SCold = 0, DAold = 0;
+    uint32_t SA = 0, S1 = 0, DAold = 0;
     if (op == 2) {
       if (n >= 2) {
         made = true;
@@ -834,10 +890,10 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           const int plo = uniform(c.perm[lo]), phi = uniform(c.perm[hi]);
           as = sa, ae = ea, cs = sc, ce = ec;
           gA = phi, oA = plo, gC = plo, oC = phi;
-          mid0 = ea, mid1 = sc, uend = ec;
-          SA = c.S[sa];
-          SCold = c.S[sc];
-          DAold = c.S[ea] - SA;
+          ob = sc;
+          SA = start_at(S, end, sa, n);
+          S1 = start_at(S, end, sc, n);
+          DAold = start_at(S, end, ea, n) - SA;
         }
       }
     } else {
@@ -851,10 +907,11 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
             rm = Remap{2, i, s};
             as = sp2, ae = s + 1, gA = x;
             cs = s + 1, ce = e, oC = x;
-            uend = e;
             clr0 = s;
             set0 = s + 1 < e ? s + 1 : -1;
-            SA = c.S[sp2];
+            ob = s;
+            SA = start_at(S, end, sp2, n);
+            S1 = start_at(S, end, s, n);
           }
         }
       } else if (e == n) {
@@ -863,9 +920,8 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           rm = Remap{2, i, n - 1};
           as = s, ae = n - 1, oA = x;
           cs = n - 1, ce = n, gC = x;
-          uend = n;
           set0 = n - 1;
-          SA = c.S[s];
+          SA = start_at(S, end, s, n);
         }
       } else {
         const int en = batch_end(c.flags, n, e, lane);
@@ -874,10 +930,11 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           rm = Remap{2, i, e - 1};
           as = s, ae = e - 1, oA = x;
           cs = e - 1, ce = en, gC = x;
-          uend = en;
           set0 = e - 1;
           clr0 = e;
-          SA = c.S[s];
+          ob = e;
+          SA = start_at(S, end, s, n);
+          S1 = start_at(S, end, e, n);
         }
       }
     }
@@ -891,45 +948,43 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     BatchNew nA{0, 0, 0, 0}, nC{0, 0, 0, 0};
     uint32_t SC = 0, shift_mid = 0, shift_end = 0;
     if (!inside) {
-      if (as < ae) nA = batch_pass(c, as, ae, rm, gA, oA, SA, dtl, dn);
+      int met = 0;
+      if (as < ae) nA = batch_pass(c, as, ae, rm, gA, oA, SA, ob, SA, S1, dtl, met);
       const uint32_t DA = as < ae ? nA.D : 0u;
-      SC = op == 2 ? SCold + DA - DAold : SA + DA;
-      if (cs < ce) nC = batch_pass(c, cs, ce, rm, gC, oC, SC, dtl, dn);
+      SC = op == 2 ? S1 + DA - DAold : SA + DA;
+      if (cs < ce) nC = batch_pass(c, cs, ce, rm, gC, oC, SC, ob, SA, S1, dtl, met);
       const uint32_t DC = cs < ce ? nC.D : 0u;
-      const uint32_t old_end = c.S[uend];
+      const uint32_t old_end = start_at(S, end, ce, n);
       shift_end = SC + DC - old_end;
-      const int64_t d_end = (int64_t)(SC + DC) - (int64_t)old_end;
-      dn += recount_shift(c, uend, n, shift_end);
-      dT = d_end * (int64_t)(n - uend);
-      if (op == 2 && mid0 < mid1) {
-        shift_mid = DA - DAold;
-        dn += recount_shift(c, mid0, mid1, shift_mid);
-        dT += ((int64_t)DA - (int64_t)DAold) * (int64_t)(mid1 - mid0);
-      }
+      shift_mid = DA - DAold;  // used between A and C of a swap only
+      met += row_recount(S, lim, lane, as, ae, cs, ce, shift_mid, shift_end);
+      dn = (int)Seg<6>::template all<OpAdd>((uint32_t)met, lane);
+      dT = ((int64_t)(SC + DC) - (int64_t)old_end) * (int64_t)(n - ce);
+      if (op == 2) dT += ((int64_t)DA - (int64_t)DAold) * (int64_t)(cs - ae);
       dT += wave_sum_i64(dtl);
     }
     const int64_t nn = cn + dn;
     const uint64_t nt = ct + (uint64_t)dT;
     if (obj_accept<OBJ>(cn, ct, dn, dT, t_ref, cool.T, w3)) {
       if (inside) {
-        if (lane == 0) {
-          const uint32_t a = c.lim[rm.i];
-          c.lim[rm.i] = c.lim[rm.j];
-          c.lim[rm.j] = a;
-        }
+        swap_lims(lim, rm.i, rm.j);
         apply_move_lds(c.perm, 1, rm.i, rm.j, lane);
       } else {
-        // shifts first: they read S of positions the batch writes below do not touch
-        if (op == 2 && mid0 < mid1) apply_shift(c, mid0, mid1 - 1, shift_mid);
-        apply_shift(c, uend, n, shift_end);
-        wave_sync_lds();
         apply_move_lds(c.perm, rm.kind, rm.i, rm.j, lane);
         if (lane == 0) {
           if (clr0 >= 0) c.flags[clr0] = 0;
           if (set0 >= 0) c.flags[set0] = 1;
         }
-        if (as < ae) write_batch(c, as, ae, nA, SA);
-        if (cs < ce) write_batch(c, cs, ce, nC, SC);
+        if (as + lane < ae) c.F[nA.r] = nA.Fn;
+        if (cs + lane < ce) c.F[nC.r] = nC.Fn;
+        // lane l of a batch pass holds position start + l: rotate into the rows' lanes
+        const uint32_t limA = (uint32_t)__shfl((int)nA.limn, (lane - as) & 63);
+        const uint32_t limC = (uint32_t)__shfl((int)nC.limn, (lane - cs) & 63);
+        // fresh copies of the bounds and shifts: the compiler would otherwise keep the sums
+        // of the recount pass live across the decision to reuse them here
+        int b0 = as, b1 = ae, b2 = cs, b3 = ce, ln = lane;
+        asm volatile("" : "+s"(b0), "+s"(b1), "+s"(b2), "+s"(b3), "+v"(shift_mid), "+v"(shift_end), "+v"(ln));
+        row_apply(S, lim, end, ln, b0, b1, b2, b3, shift_mid, shift_end, SA, SC, limA, limC);
         wave_sync_lds();
       }
       cn = nn;

@@ -115,6 +115,11 @@ __device__ __forceinline__ uint32_t dpp(uint32_t v) {
 constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
 
 __device__ __forceinline__ uint32_t readlane(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+// v_writelane of a wave-uniform value into lane k (lane select in m0)
+__device__ __forceinline__ uint32_t wlane_m0(uint32_t v, int k, uint32_t old) {
+  asm volatile("v_writelane_b32 %0, %1, m0" : "=v"(old) : "s"(v), "{m0}"(k), "0"(old));
+  return old;
+}
 
 struct OpAdd {
   static constexpr uint32_t identity = 0u;

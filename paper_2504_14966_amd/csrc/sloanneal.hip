@@ -184,8 +184,8 @@ int cu_count() { return device_attr(hipDeviceAttributeMultiprocessorCount, 256);
 
 size_t sized_chain_lds(int n) {
   const size_t pb = ((size_t)n * 2 + 15) & ~size_t(15), fb = ((size_t)n + 15) & ~size_t(15);
-  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15), sb = ((size_t)(n + 1) * 4 + 15) & ~size_t(15);
-  return pb + fb + 2 * ub + sb;
+  const size_t ub = ((size_t)n * 4 + 15) & ~size_t(15);
+  return pb + fb + ub;
 }
 
 size_t anneal_lds_bytes(int n) {
@@ -212,6 +212,21 @@ struct ChainArgs {
   hipStream_t stream;
 };
 
+static_assert(sa::sized_rows_for(SCHED_MAX_N) * 64 >= SCHED_MAX_N, "register rows must cover every position");
+
+template <int OBJ, int NR>
+hipError_t launch_sized(int grid, int waves, size_t lds, const sa::DevModel &d, const sa::StaticParams &sp,
+                        const ChainArgs &a) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel<OBJ, NR>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  sa::anneal_sized_kernel<OBJ, NR><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0, a.alpha,
+                                                                        a.k0, a.k1, a.srch, a.w);
+  return hipGetLastError();
+}
+
 // The joint order / batch-size search: on small queues the register kernel (order, request
 // fields and layout in registers, no LDS) when the 32-bit pair-cost widths hold; else the
 // delta kernel when the widths and the whole timeline fit 32 bits (as many chains per
@@ -236,15 +251,14 @@ void add_sized(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, c
       const size_t lds = soa + per * waves;
       const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)model->max_batch + 1};
       const int grid = (a.chains + waves - 1) / waves;
+      const int rows = sa::sized_rows_for(n);
       c.add(kSN | kT32, kAnnealFlags, [=](const sa::DevModel &d) {
-        if (lds > 65536) {
-          const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_sized_kernel<OBJ>),
-                                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-          if (e != hipSuccess) return e;
+        switch (rows) {
+          case 2: return launch_sized<OBJ, 2>(grid, waves, lds, d, sp, a);
+          case 4: return launch_sized<OBJ, 4>(grid, waves, lds, d, sp, a);
+          case 8: return launch_sized<OBJ, 8>(grid, waves, lds, d, sp, a);
+          default: return launch_sized<OBJ, 16>(grid, waves, lds, d, sp, a);
         }
-        sa::anneal_sized_kernel<OBJ><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0,
-                                                                          a.alpha, a.k0, a.k1, a.srch, a.w);
-        return hipGetLastError();
       });
     }
   }

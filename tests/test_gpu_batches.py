@@ -145,7 +145,8 @@ def test_anneal_search_worked_queue(sl, orc):
 
 @pytest.mark.parametrize("n,B,chains,iters,seed", [(1, 3, 5, 40, 0), (2, 1, 8, 100, 1), (9, 4, 70, 700, 2),
                                                    (40, 7, 33, 900, 3), (100, 33, 20, 600, 4),
-                                                   (64, 64, 10, 500, 5)])
+                                                   (64, 64, 10, 500, 5), (200, 17, 12, 500, 6),
+                                                   (450, 40, 8, 400, 7), (1000, 64, 4, 300, 8)])
 def test_anneal_search_random_queues(sl, orc, n, B, chains, iters, seed):
     rng = np.random.default_rng(seed)
     q = random_queue(rng, n, max_in=1500, max_out=40, thr_hi=400_000 * max(1, n // B))
