@@ -572,20 +572,21 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
 //   lim           the member at p meets its SLO iff S < lim (u32): thr - P + 1 for TTFT
 //                 (P = batch prefill), thr - F + 1 for end-to-end, all or nothing for
 //                 TPOT (F - P against thr * l_out, which does not depend on the start);
-//                 0 when it can never be met, and past the last position;
-// and the end of the timeline as one wave-uniform value.
+//                 0 when it can never be met, and past the last position.
 // A move changes the members of at most two batches (A before C). Each is scored in one
 // pass with its new members in lanes: a member that stays gets
 //   F' = F + [pf(g) + w(g, m) / 2] - [pf(o) + w(o, m) / 2]
 // for the request g that joins and o that leaves (either may be absent), and the newcomer
 //   F'(g) = P' + L_g d0 + sum over the new members j of w(j, g) / 2,
 // with w(j, m) = mu (e_j + d2 mu), mu = min(L_j, L_m), e_j = 2 (d1 + d2 l_j) + d2, twice
-// what j adds to m's decode iterations. Three DPP reductions give P', the newcomer's sum
-// and the new duration. The two batches keep their members between them, so the change
-// of t over them is a lane sum of new minus old latencies (old start: that of the old
-// batch holding the member's old position). Later batches keep their members and only
-// shift: by D'(A) - D(A) between A and C (swap), by the change of the end of the two
-// batches after C. One pass over the register rows from A on counts the change of the met
+// what j adds to m's decode iterations. Four DPP reductions give P', the newcomer's sum,
+// the new duration and the old one (the largest old offset of the members before the
+// move), so that the start times of A and C before and after the move follow from one
+// start read from the rows (swap: two). The two batches keep their members between them,
+// so the change of t over them is a lane sum of new minus old latencies (old start: that
+// of the old batch holding the member's old position). Later batches keep their members
+// and only shift: by D'(A) - D(A) between A and C (swap), by the change of the end of the
+// two batches after C. One pass over the register rows from A on counts the change of the met
 // flags by position: the positions of A and C lose their old flags (their new ones come
 // from the batch passes), the shifted ones compare S + shift with lim. Nothing is written
 // until the proposal is accepted.
@@ -640,11 +641,10 @@ __device__ __forceinline__ void set_row_lane(uint32_t (&v)[NR], int u, int l, ui
       set_row_lane<MID, HI>(v, u, l, x);
   }
 }
+// start of the batch holding position x (x < n)
 template <int NR>
-__device__ __forceinline__ uint32_t start_at(const uint32_t (&S)[NR], uint32_t end, int x, int n) {
-  const int xc = min(x, n - 1);
-  const uint32_t v = row_lane<0, NR>(S, xc >> 6, xc & 63);
-  return x >= n ? end : v;  // position n: the end of the timeline
+__device__ __forceinline__ uint32_t start_at(const uint32_t (&S)[NR], int x) {
+  return row_lane<0, NR>(S, x >> 6, x & 63);
 }
 template <int NR>
 __device__ __forceinline__ void swap_lims(uint32_t (&lim)[NR], int x, int y) {
@@ -663,65 +663,119 @@ __device__ __forceinline__ uint32_t member_limit(uint32_t kind, uint32_t thr, ui
   return thr >= off ? thr - off + 1u : 0u;
 }
 
-// New values of one changed batch's members (lanes 0 .. xe - xs - 1).
+// One changed batch [xs, xe) with its new members in lanes 0 .. xe - xs - 1 (lanes past
+// the batch read its last member's records, or the first position's, and are masked out):
+// what needs no start time -- each member's new finish offset and limit, its old offset
+// and old position, the new duration and the old one (the members that stay and o, who
+// leaves).
 struct BatchNew {
-  uint32_t Fn, limn;
-  int r;
-  uint32_t D;
+  uint32_t Fn, limn, Fold;
+  int r, q;
+  bool act;
+  uint32_t D, Dold;
 };
 
-// Scores the changed batch [xs, xe) (xe > xs) with new start SX: adds to dt the change of
-// its members' latencies (old start S0 for old positions before ob, S1 from ob on) and to
-// the lane counter met whether the lane's member meets its SLO in the new batch. Lanes
-// past the batch read its last member's records and are masked out.
-__device__ __forceinline__ BatchNew batch_pass(const SizedState &c, int xs, int xe, const Remap &rm, int g, int o,
-                                               uint32_t SX, int ob, uint32_t S0, uint32_t S1, int64_t &dt, int &met) {
-  const int lane = c.lane;
-  const int p = xs + lane;
+// Loads of one changed batch [xs, xe) (may be empty); the reductions follow in batch_scan2.
+struct BatchLoad {
+  Req rq, rg;
+  uint32_t Fold, Fo, f, P, T, Mx, Mo;
+  int r, q;
+  bool act;
+};
+__device__ __forceinline__ BatchLoad batch_load(const SizedState &c, int xs, int xe, const Remap &rm, int g, int o) {
+  const int p = xs + c.lane;
   const bool act = p < xe;
-  const int q = rm.src(min(p, xe - 1));
+  const int q = rm.src(max(min(p, xe - 1), 0));
   const int r = c.perm[q];
   const Req rq = load_req(c.req, r);
   // absent g or o read the spare all-zero record: its prefill and pair costs vanish
   const Req rg = load_req(c.req, g >= 0 ? g : c.n), ro = load_req(c.req, o >= 0 ? o : c.n);
-  const uint32_t Fold = c.F[r];
+  const uint32_t Fold = c.F[r], Fo = o >= 0 ? c.F[max(o, 0)] : 0u;
   const uint32_t f = Fold + rg.pf + (w2(rg.L, rg.e, rq.L, c.d2) >> 1) - ro.pf - (w2(ro.L, ro.e, rq.L, c.d2) >> 1);
-  const bool newcomer = r == g;
-  uint32_t P = act ? rq.pf : 0u, T = act ? w2(rq.L, rq.e, rg.L, c.d2) : 0u, Mx = (act && !newcomer) ? f : 0u;
-  Seg<6>::template all3<OpAdd, OpAdd, OpMax>(P, T, Mx, lane);
-  const uint32_t Fg = g >= 0 ? P + __umul24(rg.L, c.d0) + (T >> 1) : 0u;
-  const uint32_t Fn = newcomer ? Fg : f;
-  const uint32_t limn = member_limit(rq.kind, rq.thr, P, Fn);
-  met += (act && SX < limn) ? 1 : 0;
-  const uint32_t Sold = q < ob ? S0 : S1;
-  dt += act ? (int64_t)(SX + Fn) - (int64_t)(Sold + Fold) : 0;
-  return BatchNew{Fn, limn, r, max(Mx, Fg)};
+  const bool stay = act && r != g;
+  return BatchLoad{rq, rg, Fold, Fo, f, act ? rq.pf : 0u, act ? w2(rq.L, rq.e, rg.L, c.d2) : 0u, stay ? f : 0u,
+                   stay ? Fold : 0u, r, q, act};
+}
+__device__ __forceinline__ BatchNew batch_finish(const SizedState &c, const BatchLoad &l, int g) {
+  const uint32_t Fg = g >= 0 ? l.P + __umul24(l.rg.L, c.d0) + (l.T >> 1) : 0u;
+  const uint32_t Fn = l.r == g ? Fg : l.f;
+  const uint32_t limn = member_limit(l.rq.kind, l.rq.thr, l.P, Fn);
+  return BatchNew{Fn, limn, l.Fold, l.r, l.q, l.act, max(l.Mx, Fg), max(l.Mo, l.Fo)};
+}
+// Both changed batches at once (A and C; either may be empty, its lanes all masked out:
+// duration 0, old duration that of the one who left it, if any), the eight reductions
+// interleaved.
+__device__ __forceinline__ void batch_scan2(const SizedState &c, int as, int ae, int gA, int oA, int cs, int ce, int gC,
+                                            int oC, const Remap &rm, BatchNew &nA, BatchNew &nC) {
+  BatchLoad a = batch_load(c, as, ae, rm, gA, oA), b = batch_load(c, cs, ce, rm, gC, oC);
+#pragma unroll
+  for (int st = 0; st < Seg<6>::kSteps; ++st) {
+    a.P = Seg<6>::template step<OpAdd>(a.P, st);
+    b.P = Seg<6>::template step<OpAdd>(b.P, st);
+    a.T = Seg<6>::template step<OpAdd>(a.T, st);
+    b.T = Seg<6>::template step<OpAdd>(b.T, st);
+    a.Mx = Seg<6>::template step<OpMax>(a.Mx, st);
+    b.Mx = Seg<6>::template step<OpMax>(b.Mx, st);
+    a.Mo = Seg<6>::template step<OpMax>(a.Mo, st);
+    b.Mo = Seg<6>::template step<OpMax>(b.Mo, st);
+  }
+  a.P = readlane(a.P, kWave - 1), a.T = readlane(a.T, kWave - 1), a.Mx = readlane(a.Mx, kWave - 1);
+  a.Mo = readlane(a.Mo, kWave - 1);
+  b.P = readlane(b.P, kWave - 1), b.T = readlane(b.T, kWave - 1), b.Mx = readlane(b.Mx, kWave - 1);
+  b.Mo = readlane(b.Mo, kWave - 1);
+  nA = batch_finish(c, a, gA);
+  nC = batch_finish(c, b, gC);
+}
+
+// The rest, with the batch's new start SX: adds to dt the change of its members'
+// latencies (old start S0 for old positions before ob, S1 from ob on) and to the lane
+// counter met whether the lane's member meets its SLO in the new batch.
+__device__ __forceinline__ void batch_tally(const BatchNew &b, uint32_t SX, int ob, uint32_t S0, uint32_t S1,
+                                            int64_t &dt, int &met) {
+  met += (b.act && SX < b.limn) ? 1 : 0;
+  const uint32_t Sold = b.q < ob ? S0 : S1;
+  dt += b.act ? (int64_t)(SX + b.Fn) - (int64_t)(Sold + b.Fold) : 0;
+}
+
+// Rows by their place against the changed ranges: before r0 wholly before b0 (untouched),
+// from rE on wholly at or after b3 (shifted by sE), in [rM0, rM1) wholly inside [b1, b2)
+// (shifted by sM); the others hold positions of A or C or a range bound.
+struct RowSpan {
+  int r0, rE, rM0, rM1;
+};
+__device__ __forceinline__ RowSpan row_span(int b0, int b1, int b2, int b3) {
+  return RowSpan{b0 >> 6, (b3 + kWave - 1) >> 6, (b1 + kWave - 1) >> 6, b2 >> 6};
 }
 
 // Change of the met flags by position from b0 on: [b0, b1) and [b2, b3) lose their old
-// flags, [b1, b2) moves by sM, [b3, n) by sE (b0 <= b1 <= b2 <= b3). Rows wholly before b0
-// are skipped, rows wholly inside one shifted range take one compare per position.
+// flags, [b1, b2) moves by sM, [b3, n) by sE (b0 <= b1 <= b2 <= b3). The lane index comes
+// in as a fresh copy each call, so that no per-row position is kept live across calls.
 template <int NR>
 __device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32_t (&lim)[NR], int lane, int b0, int b1,
                                            int b2, int b3, uint32_t sM, uint32_t sE) {
+  const RowSpan rs = row_span(b0, b1, b2, b3);
   int cnt = 0;
   static_for<NR>([=, &S, &lim, &cnt](auto uc) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
-    const int base = u * kWave;
-    if (base + kWave <= b0) return;
+    if (u < rs.r0) return;
     const uint32_t s = S[u], l = lim[u];
-    bool now;
-    if (base >= b3) {
-      now = s + sE < l;
-    } else if (base >= b1 && base + kWave <= b2) {
-      now = s + sM < l;
+    // each branch forms its own contribution behind an opaque copy: merged, the branches
+    // would leave a lane-mask merge through the exec mask after them
+    int v;
+    if (u >= rs.rE) {
+      v = (int)(s + sE < l) - (int)(s < l);
+      asm volatile("" : "+v"(v));
+    } else if (u >= rs.rM0 && u < rs.rM1) {
+      v = (int)(s + sM < l) - (int)(s < l);
+      asm volatile("" : "+v"(v));
     } else {
-      const int p = base + lane;
+      const int p = lane + u * kWave;
       const bool chg = (unsigned)(p - b0) < (unsigned)(b1 - b0) || (unsigned)(p - b2) < (unsigned)(b3 - b2);
       const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
-      now = !chg && s + d < l;
+      v = (int)(!chg && s + d < l) - (int)(s < l);
+      asm volatile("" : "+v"(v));
     }
-    cnt += (int)now - (int)(s < l);
+    cnt += v;
   });
   return cnt;
 }
@@ -729,33 +783,30 @@ __device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32
 // The accepted move on the rows: A = [b0, b1) starts at SA with limits limA (by lane
 // position), C = [b2, b3) at SC with limC, [b1, b2) shifts by sM, [b3, n] by sE.
 template <int NR>
-__device__ __forceinline__ void row_apply(uint32_t (&S)[NR], uint32_t (&lim)[NR], uint32_t &end, int lane, int b0, int b1,
-                                          int b2, int b3, uint32_t sM, uint32_t sE, uint32_t SA, uint32_t SC,
-                                          uint32_t limA, uint32_t limC) {
+__device__ __forceinline__ void row_apply(uint32_t (&S)[NR], uint32_t (&lim)[NR], int lane, int b0, int b1, int b2,
+                                          int b3, uint32_t sM, uint32_t sE, uint32_t SA, uint32_t SC, uint32_t limA,
+                                          uint32_t limC) {
+  const RowSpan rs = row_span(b0, b1, b2, b3);
   static_for<NR>([=, &S, &lim](auto uc) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
-    const int base = u * kWave;
-    if (base + kWave <= b0) return;
-    if (base >= b3) {
+    if (u < rs.r0) return;
+    if (u >= rs.rE) {
       S[u] += sE;
-      return;
-    }
-    if (base >= b1 && base + kWave <= b2) {
+    } else if (u >= rs.rM0 && u < rs.rM1) {
       S[u] += sM;
-      return;
+    } else {
+      const int p = lane + u * kWave;
+      const bool inA = (unsigned)(p - b0) < (unsigned)(b1 - b0), inC = (unsigned)(p - b2) < (unsigned)(b3 - b2);
+      const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
+      S[u] = inA ? SA : (inC ? SC : S[u] + d);
+      lim[u] = inA ? limA : (inC ? limC : lim[u]);
     }
-    const int p = base + lane;
-    const bool inA = (unsigned)(p - b0) < (unsigned)(b1 - b0), inC = (unsigned)(p - b2) < (unsigned)(b3 - b2);
-    const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
-    S[u] = inA ? SA : (inC ? SC : S[u] + d);
-    lim[u] = inA ? limA : (inC ? limC : lim[u]);
   });
-  end += sE;
 }
 
 // F, S, lim of an order with maximum-size batches; returns its (n, t).
 template <int NR>
-__device__ __forceinline__ Score sized_init(const SizedState &c, uint32_t (&S)[NR], uint32_t (&lim)[NR], uint32_t &end) {
+__device__ __forceinline__ Score sized_init(const SizedState &c, uint32_t (&S)[NR], uint32_t (&lim)[NR]) {
   const int lane = c.lane;
   // an opaque zero: stores of a constant would be merged into one block fill, after which
   // the compiler keeps the rows as one vector value
@@ -798,7 +849,6 @@ __device__ __forceinline__ Score sized_init(const SizedState &c, uint32_t (&S)[N
     });
     Sc += D;
   }
-  end = Sc;
   wave_sync_lds();
   return Score{nmet, wave_sum_u64(tl)};
 }
@@ -841,7 +891,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
                wb + pb,
                reinterpret_cast<uint32_t *>(wb + pb + fb),
                n, B, lane, sp.d0, sp.d2};
-  uint32_t S[NR], lim[NR], end;  // register rows (position p: row p / 64, lane p % 64)
+  uint32_t S[NR], lim[NR];  // register rows (position p: row p / 64, lane p % 64)
   const WsHeader *h = reinterpret_cast<const WsHeader *>(ws);
   const int64_t t_ref = h->t_ref, allmet = h->allmet;
   const uint16_t *start = reinterpret_cast<const uint16_t *>(ws + ws_off_start());
@@ -859,7 +909,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     gbest_f[p] = fl;
   }
   wave_sync_lds();
-  const Score s0 = sized_init(c, S, lim, end);
+  const Score s0 = sized_init(c, S, lim);
   int64_t cn = s0.n, bn = s0.n, biter = -1, accepts = 0;
   uint64_t ct = s0.t, bt = s0.t, digest = kFnvOffset;
   Cooling cool{T0, alpha, srch.level_len, srch.level_len};
@@ -870,13 +920,15 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
     const int op = (int)(pk >> 20), i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
     // plan: new ranges of the changed batches A = [as, ae) and C = [cs, ce), who joins and
-    // leaves each, the range between them (swap) and the flag writes; old positions
-    // before ob belonged to a batch starting at SA, the others to one starting at S1
-    bool made = false, inside = false;
-    int as = 0, ae = 0, cs = 0, ce = 0, gA = -1, oA = -1, gC = -1, oC = -1, ob = n;
+    // leaves each, the range between them (swap) and the flag writes. Old positions
+    // before ob belonged to a batch starting at SA, the others to one starting at S1. The
+    // start times come from the register rows at the positions xa (swap: also xc), in the
+    // old batch of A (in_first) or the second old batch, and the old durations of the
+    // batches from the scans.
+    bool made = false, inside = false, in_first = true;
+    int as = 0, ae = 0, cs = 0, ce = 0, gA = -1, oA = -1, gC = -1, oC = -1, ob = n, xa = 0, xc = 0, x = 0;
     int set0 = -1, clr0 = -1;
     Remap rm{0, 0, 0};
-    uint32_t SA = 0, S1 = 0, DAold = 0;
     if (op == 2) {
       if (n >= 2) {
         made = true;
@@ -891,14 +943,13 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           as = sa, ae = ea, cs = sc, ce = ec;
           gA = phi, oA = plo, gC = plo, oC = phi;
           ob = sc;
-          SA = start_at(S, end, sa, n);
-          S1 = start_at(S, end, sc, n);
-          DAold = start_at(S, end, ea, n) - SA;
+          xa = lo, xc = hi;
         }
       }
     } else {
       const int s = batch_begin(c.flags, i, lane), e = batch_end(c.flags, n, i, lane);
-      const int x = uniform(c.perm[i]);
+      x = uniform(c.perm[i]);
+      xa = i;
       if (op == 0) {
         if (s > 0) {
           const int sp2 = batch_begin(c.flags, s - 1, lane);
@@ -910,8 +961,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
             clr0 = s;
             set0 = s + 1 < e ? s + 1 : -1;
             ob = s;
-            SA = start_at(S, end, sp2, n);
-            S1 = start_at(S, end, s, n);
+            in_first = false;
           }
         }
       } else if (e == n) {
@@ -921,7 +971,6 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           as = s, ae = n - 1, oA = x;
           cs = n - 1, ce = n, gC = x;
           set0 = n - 1;
-          SA = start_at(S, end, s, n);
         }
       } else {
         const int en = batch_end(c.flags, n, e, lane);
@@ -933,8 +982,6 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           set0 = e - 1;
           clr0 = e;
           ob = e;
-          SA = start_at(S, end, s, n);
-          S1 = start_at(S, end, e, n);
         }
       }
     }
@@ -942,26 +989,45 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
       cool.step();
       continue;
     }
-    int64_t dtl = 0;
-    int dn = 0;
     int64_t dT = 0;
-    BatchNew nA{0, 0, 0, 0}, nC{0, 0, 0, 0};
-    uint32_t SC = 0, shift_mid = 0, shift_end = 0;
+    int dn = 0;
+    BatchNew nA{}, nC{};
+    uint32_t SA = 0, SC = 0, shift_mid = 0, shift_end = 0;
     if (!inside) {
+      const uint32_t Sa = start_at(S, xa), Sc = op == 2 ? start_at(S, xc) : 0u;
+      batch_scan2(c, as, ae, gA, oA, cs, ce, gC, oC, rm, nA, nC);
+      const uint32_t DA = nA.D, DAold = nA.Dold, DC = nC.D, DCold = nC.Dold;
+      // old starts: SA of the old batch of A, S1 of the second old batch
+      uint32_t S1;
+      if (op == 2) {
+        SA = Sa;
+        S1 = Sc;
+        SC = S1 + DA - DAold;
+      } else {
+        SA = in_first ? Sa : Sa - DAold;
+        S1 = in_first ? Sa + DAold : Sa;
+        SC = SA + DA;
+      }
+      int64_t dtl = 0;
       int met = 0;
-      if (as < ae) nA = batch_pass(c, as, ae, rm, gA, oA, SA, ob, SA, S1, dtl, met);
-      const uint32_t DA = as < ae ? nA.D : 0u;
-      SC = op == 2 ? S1 + DA - DAold : SA + DA;
-      if (cs < ce) nC = batch_pass(c, cs, ce, rm, gC, oC, SC, ob, SA, S1, dtl, met);
-      const uint32_t DC = cs < ce ? nC.D : 0u;
-      const uint32_t old_end = start_at(S, end, ce, n);
+      batch_tally(nA, SA, ob, SA, S1, dtl, met);
+      batch_tally(nC, SC, ob, SA, S1, dtl, met);
+      // end of the two batches before the move (an insert that opens a new last batch:
+      // S1 is the end of the only old batch and C had no old members)
+      const uint32_t old_end = S1 + DCold;
       shift_end = SC + DC - old_end;
       shift_mid = DA - DAold;  // used between A and C of a swap only
-      met += row_recount(S, lim, lane, as, ae, cs, ce, shift_mid, shift_end);
-      dn = (int)Seg<6>::template all<OpAdd>((uint32_t)met, lane);
+      int lnr = lane;
+      asm volatile("" : "+v"(lnr));
+      met += row_recount(S, lim, lnr, as, ae, cs, ce, shift_mid, shift_end);
+      // one reduction for the met count and the latency change, the latter as two exact
+      // parts (each lane's change lies within +-2^33: 2^24 * sum(hi) + sum(lo))
+      uint32_t mu = (uint32_t)met, lo = (uint32_t)dtl & 0xFFFFFFu, hi = (uint32_t)(int32_t)(dtl >> 24);
+      Seg<6>::template all3<OpAdd, OpAdd, OpAdd>(mu, lo, hi, lane);
+      dn = (int)mu;
       dT = ((int64_t)(SC + DC) - (int64_t)old_end) * (int64_t)(n - ce);
       if (op == 2) dT += ((int64_t)DA - (int64_t)DAold) * (int64_t)(cs - ae);
-      dT += wave_sum_i64(dtl);
+      dT += (int64_t)(int32_t)hi * (int64_t)(1 << 24) + (int64_t)lo;
     }
     const int64_t nn = cn + dn;
     const uint64_t nt = ct + (uint64_t)dT;
@@ -984,7 +1050,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
         // of the recount pass live across the decision to reuse them here
         int b0 = as, b1 = ae, b2 = cs, b3 = ce, ln = lane;
         asm volatile("" : "+s"(b0), "+s"(b1), "+s"(b2), "+s"(b3), "+v"(shift_mid), "+v"(shift_end), "+v"(ln));
-        row_apply(S, lim, end, ln, b0, b1, b2, b3, shift_mid, shift_end, SA, SC, limA, limC);
+        row_apply(S, lim, ln, b0, b1, b2, b3, shift_mid, shift_end, SA, SC, limA, limC);
         wave_sync_lds();
       }
       cn = nn;

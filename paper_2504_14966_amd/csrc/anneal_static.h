@@ -200,6 +200,20 @@ struct Seg {
     b = finish(b, lane);
     c = finish(c, lane);
   }
+  template <class O1, class O2, class O3, class O4>
+  __device__ static __forceinline__ void all4(uint32_t &a, uint32_t &b, uint32_t &c, uint32_t &d, int lane) {
+#pragma unroll
+    for (int s = 0; s < kSteps; ++s) {
+      a = step<O1>(a, s);
+      b = step<O2>(b, s);
+      c = step<O3>(c, s);
+      d = step<O4>(d, s);
+    }
+    a = finish(a, lane);
+    b = finish(b, lane);
+    c = finish(c, lane);
+    d = finish(d, lane);
+  }
   // exact sum of 32-bit values as two 16-bit-half sums (each below 2^22)
   __device__ static __forceinline__ uint64_t sum_wide(uint32_t v, int lane) {
     const uint32_t lo = all<OpAdd>(v & 0xFFFFu, lane), hi = all<OpAdd>(v >> 16, lane);
