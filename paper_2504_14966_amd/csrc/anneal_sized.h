@@ -657,10 +657,12 @@ __device__ __forceinline__ void swap_lims(uint32_t (&lim)[NR], int x, int y) {
 __host__ __device__ constexpr int sized_rows_for(int n) { return n <= 128 ? 2 : (n <= 256 ? 4 : (n <= 512 ? 8 : 16)); }
 
 // limit of a member: met iff batch start < limit
+// (both forms on every lane and a select: lanes of one wave hold requests of every kind)
 __device__ __forceinline__ uint32_t member_limit(uint32_t kind, uint32_t thr, uint32_t P, uint32_t F) {
-  if (kind == 1) return F - P <= thr ? 0xFFFFFFFFu : 0u;
   const uint32_t off = kind == 0 ? P : F;
-  return thr >= off ? thr - off + 1u : 0u;
+  const uint32_t by_start = thr >= off ? thr - off + 1u : 0u;
+  const uint32_t tpot = F - P <= thr ? 0xFFFFFFFFu : 0u;
+  return kind == 1 ? tpot : by_start;
 }
 
 // One changed batch [xs, xe) with its new members in lanes 0 .. xe - xs - 1 (lanes past
@@ -672,13 +674,13 @@ struct BatchNew {
   uint32_t Fn, limn, Fold;
   int r, q;
   bool act;
-  uint32_t D, Dold;
+  uint32_t D, Dold, Pold;  // Pold: the old batch's prefill (the members before the move)
 };
 
 // Loads of one changed batch [xs, xe) (may be empty); the reductions follow in batch_scan2.
 struct BatchLoad {
   Req rq, rg;
-  uint32_t Fold, Fo, f, P, T, Mx, Mo;
+  uint32_t Fold, Fo, f, P, T, Mx, Mo, pfo;
   int r, q;
   bool act;
 };
@@ -694,13 +696,13 @@ __device__ __forceinline__ BatchLoad batch_load(const SizedState &c, int xs, int
   const uint32_t f = Fold + rg.pf + (w2(rg.L, rg.e, rq.L, c.d2) >> 1) - ro.pf - (w2(ro.L, ro.e, rq.L, c.d2) >> 1);
   const bool stay = act && r != g;
   return BatchLoad{rq, rg, Fold, Fo, f, act ? rq.pf : 0u, act ? w2(rq.L, rq.e, rg.L, c.d2) : 0u, stay ? f : 0u,
-                   stay ? Fold : 0u, r, q, act};
+                   stay ? Fold : 0u, ro.pf, r, q, act};
 }
 __device__ __forceinline__ BatchNew batch_finish(const SizedState &c, const BatchLoad &l, int g) {
   const uint32_t Fg = g >= 0 ? l.P + __umul24(l.rg.L, c.d0) + (l.T >> 1) : 0u;
   const uint32_t Fn = l.r == g ? Fg : l.f;
   const uint32_t limn = member_limit(l.rq.kind, l.rq.thr, l.P, Fn);
-  return BatchNew{Fn, limn, l.Fold, l.r, l.q, l.act, max(l.Mx, Fg), max(l.Mo, l.Fo)};
+  return BatchNew{Fn, limn, l.Fold, l.r, l.q, l.act, max(l.Mx, Fg), max(l.Mo, l.Fo), l.P - l.rg.pf + l.pfo};
 }
 // Both changed batches at once (A and C; either may be empty, its lanes all masked out:
 // duration 0, old duration that of the one who left it, if any), the eight reductions
@@ -747,12 +749,18 @@ __device__ __forceinline__ RowSpan row_span(int b0, int b1, int b2, int b3) {
   return RowSpan{b0 >> 6, (b3 + kWave - 1) >> 6, (b1 + kWave - 1) >> 6, b2 >> 6};
 }
 
-// Change of the met flags by position from b0 on: [b0, b1) and [b2, b3) lose their old
-// flags, [b1, b2) moves by sM, [b3, n) by sE (b0 <= b1 <= b2 <= b3). The lane index comes
-// in as a fresh copy each call, so that no per-row position is kept live across calls.
+// The move on the rows, before it is decided (most proposals that make a move are
+// accepted; a rejected one is undone by row_undo): A = [b0, b1) takes start SA and limits
+// limA (by lane position), C = [b2, b3) start SC and limits limC, [b1, b2) shifts by sM,
+// [b3, n] by sE (b0 <= b1 <= b2 <= b3). Returns the lane's change of the met flags from b0
+// on: the positions of A and C lose their old flags (their new ones are counted by the
+// batch tallies), the shifted ones compare the new start with the limit. The lane index
+// comes in as a fresh copy each call, so that no per-row position is kept live across
+// calls.
 template <int NR>
-__device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32_t (&lim)[NR], int lane, int b0, int b1,
-                                           int b2, int b3, uint32_t sM, uint32_t sE) {
+__device__ __forceinline__ int row_update(uint32_t (&S)[NR], uint32_t (&lim)[NR], int lane, int b0, int b1, int b2,
+                                          int b3, uint32_t sM, uint32_t sE, uint32_t SA, uint32_t SC, uint32_t limA,
+                                          uint32_t limC) {
   const RowSpan rs = row_span(b0, b1, b2, b3);
   int cnt = 0;
   static_for<NR>([=, &S, &lim, &cnt](auto uc) __attribute__((always_inline)) {
@@ -763,16 +771,27 @@ __device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32
     // would leave a lane-mask merge through the exec mask after them
     int v;
     if (u >= rs.rE) {
-      v = (int)(s + sE < l) - (int)(s < l);
+      const uint32_t x = s + sE;
+      v = (int)(x < l) - (int)(s < l);
+      S[u] = x;
       asm volatile("" : "+v"(v));
     } else if (u >= rs.rM0 && u < rs.rM1) {
-      v = (int)(s + sM < l) - (int)(s < l);
+      const uint32_t x = s + sM;
+      v = (int)(x < l) - (int)(s < l);
+      S[u] = x;
       asm volatile("" : "+v"(v));
     } else {
       const int p = lane + u * kWave;
-      const bool chg = (unsigned)(p - b0) < (unsigned)(b1 - b0) || (unsigned)(p - b2) < (unsigned)(b3 - b2);
+      const bool inA = (unsigned)(p - b0) < (unsigned)(b1 - b0), inC = (unsigned)(p - b2) < (unsigned)(b3 - b2);
       const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
-      v = (int)(!chg && s + d < l) - (int)(s < l);
+      const uint32_t x = s + d;
+      v = (int)(!(inA || inC) && x < l) - (int)(s < l);
+      uint32_t sn = inC ? SC : x;
+      sn = inA ? SA : sn;
+      uint32_t ln = inC ? limC : l;
+      ln = inA ? limA : ln;
+      S[u] = sn;
+      lim[u] = ln;
       asm volatile("" : "+v"(v));
     }
     cnt += v;
@@ -780,26 +799,32 @@ __device__ __forceinline__ int row_recount(const uint32_t (&S)[NR], const uint32
   return cnt;
 }
 
-// The accepted move on the rows: A = [b0, b1) starts at SA with limits limA (by lane
-// position), C = [b2, b3) at SC with limC, [b1, b2) shifts by sM, [b3, n] by sE.
+// Undoes row_update for a rejected move: shifted positions move back, the positions of A
+// and C take their old start (SA before ob, S1 from ob on) and their old limit, formed
+// again from the order and offsets (both still the old ones) and the old batch prefills
+// (PA before ob, PC from ob on).
 template <int NR>
-__device__ __forceinline__ void row_apply(uint32_t (&S)[NR], uint32_t (&lim)[NR], int lane, int b0, int b1, int b2,
-                                          int b3, uint32_t sM, uint32_t sE, uint32_t SA, uint32_t SC, uint32_t limA,
-                                          uint32_t limC) {
+__device__ __forceinline__ void row_undo(const SizedState &c, uint32_t (&S)[NR], uint32_t (&lim)[NR], int lane, int b0,
+                                         int b1, int b2, int b3, uint32_t sM, uint32_t sE, int ob, uint32_t SA,
+                                         uint32_t S1, uint32_t PA, uint32_t PC) {
   const RowSpan rs = row_span(b0, b1, b2, b3);
   static_for<NR>([=, &S, &lim](auto uc) __attribute__((always_inline)) {
     constexpr int u = decltype(uc)::value;
     if (u < rs.r0) return;
     if (u >= rs.rE) {
-      S[u] += sE;
+      S[u] -= sE;
     } else if (u >= rs.rM0 && u < rs.rM1) {
-      S[u] += sM;
+      S[u] -= sM;
     } else {
       const int p = lane + u * kWave;
-      const bool inA = (unsigned)(p - b0) < (unsigned)(b1 - b0), inC = (unsigned)(p - b2) < (unsigned)(b3 - b2);
+      const bool chg = (unsigned)(p - b0) < (unsigned)(b1 - b0) || (unsigned)(p - b2) < (unsigned)(b3 - b2);
       const uint32_t d = p >= b3 ? sE : (p >= b1 ? sM : 0u);
-      S[u] = inA ? SA : (inC ? SC : S[u] + d);
-      lim[u] = inA ? limA : (inC ? limC : lim[u]);
+      const bool first = p < ob;
+      const int r = c.perm[min(p, c.n - 1)];
+      const Req rq = load_req(c.req, r);
+      const uint32_t lo = member_limit(rq.kind, rq.thr, first ? PA : PC, c.F[r]);
+      S[u] = chg ? (first ? SA : S1) : S[u] - d;
+      lim[u] = chg ? lo : lim[u];
     }
   });
 }
@@ -992,7 +1017,7 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
     int64_t dT = 0;
     int dn = 0;
     BatchNew nA{}, nC{};
-    uint32_t SA = 0, SC = 0, shift_mid = 0, shift_end = 0;
+    uint32_t SA = 0, SC = 0, S1k = 0, shift_mid = 0, shift_end = 0;
     if (!inside) {
       const uint32_t Sa = start_at(S, xa), Sc = op == 2 ? start_at(S, xc) : 0u;
       batch_scan2(c, as, ae, gA, oA, cs, ce, gC, oC, rm, nA, nC);
@@ -1017,9 +1042,14 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
       const uint32_t old_end = S1 + DCold;
       shift_end = SC + DC - old_end;
       shift_mid = DA - DAold;  // used between A and C of a swap only
+      // the new limits of A and C, lane l of a batch scan holding position start + l,
+      // rotated into the rows' lanes
+      const uint32_t limA = (uint32_t)__shfl((int)nA.limn, (lane - as) & 63);
+      const uint32_t limC = (uint32_t)__shfl((int)nC.limn, (lane - cs) & 63);
       int lnr = lane;
       asm volatile("" : "+v"(lnr));
-      met += row_recount(S, lim, lnr, as, ae, cs, ce, shift_mid, shift_end);
+      met += row_update(S, lim, lnr, as, ae, cs, ce, shift_mid, shift_end, SA, SC, limA, limC);
+      S1k = S1;
       // one reduction for the met count and the latency change, the latter as two exact
       // parts (each lane's change lies within +-2^33: 2^24 * sum(hi) + sum(lo))
       uint32_t mu = (uint32_t)met, lo = (uint32_t)dtl & 0xFFFFFFu, hi = (uint32_t)(int32_t)(dtl >> 24);
@@ -1043,14 +1073,6 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
         }
         if (as + lane < ae) c.F[nA.r] = nA.Fn;
         if (cs + lane < ce) c.F[nC.r] = nC.Fn;
-        // lane l of a batch pass holds position start + l: rotate into the rows' lanes
-        const uint32_t limA = (uint32_t)__shfl((int)nA.limn, (lane - as) & 63);
-        const uint32_t limC = (uint32_t)__shfl((int)nC.limn, (lane - cs) & 63);
-        // fresh copies of the bounds and shifts: the compiler would otherwise keep the sums
-        // of the recount pass live across the decision to reuse them here
-        int b0 = as, b1 = ae, b2 = cs, b3 = ce, ln = lane;
-        asm volatile("" : "+s"(b0), "+s"(b1), "+s"(b2), "+s"(b3), "+v"(shift_mid), "+v"(shift_end), "+v"(ln));
-        row_apply(S, lim, ln, b0, b1, b2, b3, shift_mid, shift_end, SA, SC, limA, limC);
         wave_sync_lds();
       }
       cn = nn;
@@ -1068,6 +1090,10 @@ __global__ void __launch_bounds__(1024) anneal_sized_kernel(DevModel m, StaticPa
           gbest_f[p] = c.flags[p];
         }
       }
+    } else if (!inside) {
+      int lnu = lane;
+      asm volatile("" : "+v"(lnu));
+      row_undo(c, S, lim, lnu, as, ae, cs, ce, shift_mid, shift_end, ob, SA, S1k, nA.Pold, nC.Pold);
     }
     cool.step();
   }
