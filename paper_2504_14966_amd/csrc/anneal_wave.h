@@ -325,15 +325,16 @@ struct WaveChain {
       const bool valid = lane < batch_size(k);
       const uint4 t0 = tab[3 * k], t1 = tab[3 * k + 1];
       const uint32_t o = t0.x, Lo = t0.z, eo = t0.w, Le = t1.x, ee = t1.y, dP = t1.z;
-      uint32_t r = N;
-      if (valid) r = perm[q0 + lane];
+      // as in changed_row: lanes past the batch read a clamped position, and they and the
+      // leaving member write the spare slot F[n + 1] (no branch)
+      const uint32_t r = valid ? (uint32_t)perm[min(q0 + lane, N - 1)] : (uint32_t)N;
       const uint32_t Lm = req[r].x >> 16;
       const uint32_t Fm = F[r];
       const uint32_t mue = min(Lm, Le), muo = min(Lm, Lo);
       const uint32_t wem = vmul24(mue, vmad24(d2, mue, ee));
       const uint32_t wom = vmul24(muo, vmad24(d2, muo, eo));
       const int32_t dwh = (int32_t)(wem - wom) >> 1;
-      if (valid && r != o) F[r] = Fm - dP - (uint32_t)dwh;
+      F[(valid && r != o) ? r : N + 1] = Fm - dP - (uint32_t)dwh;
     }
     // every leaving member's slot held a newcomer's candidate value
     if (lane < M && mv.changes(lane)) F[ovec] = fo;

@@ -208,6 +208,29 @@ __device__ __forceinline__ uint32_t scan_max32(uint32_t v) {
   v = max(v, dpp_old<kDppRowBcast31, 0xC>(0u, v));
   return v;
 }
+// one step of four interleaved inclusive add-scans
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ void scan_step4(uint32_t &a, uint32_t &b, uint32_t &c, uint32_t &d) {
+  a += dpp_old<CTRL, ROWMASK>(0u, a);
+  b += dpp_old<CTRL, ROWMASK>(0u, b);
+  c += dpp_old<CTRL, ROWMASK>(0u, c);
+  d += dpp_old<CTRL, ROWMASK>(0u, d);
+}
+// Sum of 64-bit values over the 64 lanes (mod 2^64), exactly, as four 16-bit limb sums
+// (each below 2^22) scanned together by DPP: no round trip through the LDS unit.
+__device__ __forceinline__ uint64_t wave_sum_u64_dpp(uint64_t v) {
+  uint32_t a0 = (uint32_t)v & 0xFFFFu, a1 = (uint32_t)v >> 16, a2 = (uint32_t)(v >> 32) & 0xFFFFu;
+  uint32_t a3 = (uint32_t)(v >> 48);
+  scan_step4<kDppRowShr1, 0xF>(a0, a1, a2, a3);
+  scan_step4<kDppRowShr2, 0xF>(a0, a1, a2, a3);
+  scan_step4<kDppRowShr4, 0xF>(a0, a1, a2, a3);
+  scan_step4<kDppRowShr8, 0xF>(a0, a1, a2, a3);
+  scan_step4<kDppRowBcast15, 0xA>(a0, a1, a2, a3);
+  scan_step4<kDppRowBcast31, 0xC>(a0, a1, a2, a3);
+  return (uint64_t)rl(a0, kWave - 1) + ((uint64_t)rl(a1, kWave - 1) << 16) + ((uint64_t)rl(a2, kWave - 1) << 32) +
+         ((uint64_t)rl(a3, kWave - 1) << 48);
+}
+
 template <int CTRL, int ROWMASK>
 __device__ __forceinline__ uint64_t add_dpp64(uint64_t v) {
   const uint32_t lo = dpp_old<CTRL, ROWMASK>(0u, (uint32_t)v), hi = dpp_old<CTRL, ROWMASK>(0u, (uint32_t)(v >> 32));
@@ -498,7 +521,7 @@ __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req
     nmet += __popcll(__ballot(met));
   }
   wave_sync_lds();
-  return Score{nmet, wave_sum_u64(tsum)};
+  return Score{nmet, wave_sum_u64_dpp(tsum)};
 }
 
 }  // namespace sa
