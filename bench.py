@@ -123,15 +123,15 @@ def expected_work(W) -> dict:
 STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 172.0 KiB x 2.0 + WRITE_SIZE 16,681.5 KiB x 1.0, burst workload, one launch
-    "41cc03d9c88fd4a5d4d9b6f74212e0893bb1947a62d043015a746fcb172a93c5": 17434068,
+    # FETCH_SIZE 175.9 KiB x 2.0 + WRITE_SIZE 16,682.2 KiB x 1.0, burst workload, one launch
+    "772ad588e211c0f20ecaa1b9ef3c495e391b88b66c062e0dbe7d54f045fc55e3": 17442849,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "41cc03d9c88fd4a5d4d9b6f74212e0893bb1947a62d043015a746fcb172a93c5": 0.677,
+    "772ad588e211c0f20ecaa1b9ef3c495e391b88b66c062e0dbe7d54f045fc55e3": 0.716,
 }
 
 
