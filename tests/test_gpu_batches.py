@@ -146,7 +146,8 @@ def test_anneal_search_worked_queue(sl, orc):
 @pytest.mark.parametrize("n,B,chains,iters,seed", [(1, 3, 5, 40, 0), (2, 1, 8, 100, 1), (9, 4, 70, 700, 2),
                                                    (40, 7, 33, 900, 3), (100, 33, 20, 600, 4),
                                                    (64, 64, 10, 500, 5), (200, 17, 12, 500, 6),
-                                                   (450, 40, 8, 400, 7), (1000, 64, 4, 300, 8)])
+                                                   (450, 40, 8, 400, 7), (1000, 64, 4, 300, 8),
+                                                   (77, 3, 6, 600, 9), (130, 2, 6, 600, 10), (260, 5, 4, 500, 11)])
 def test_anneal_search_random_queues(sl, orc, n, B, chains, iters, seed):
     rng = np.random.default_rng(seed)
     q = random_queue(rng, n, max_in=1500, max_out=40, thr_hi=400_000 * max(1, n // B))
@@ -186,7 +187,8 @@ def _pq(rng, n, in_lo, in_hi, out_lo, out_hi, thr_hi):
 SEARCH_PATHS = {
     # delta kernel: batch size 1 (squeeze and delay never allowed)
     "delta_b1": (lambda r: _pq(r, 300, 16, 2048, 1, 6, 4_000_000_000), Model(1, SEARCH, 2000, 40, 8000, 300, 2), 6, 300),
-    # delta kernel: one batch of everything at the start; delays open new last batches
+    # one batch of everything at the start (50 requests: the register search kernel); delays
+    # open new last batches
     "delta_one_batch": (lambda r: _pq(r, 50, 16, 2048, 1, 300, 3_000_000), Model(64, SEARCH, 2000, 40, 8000, 300, 2), 8, 600),
     # delta kernel: equal output lengths (ties in every batch)
     "delta_ties": (lambda r: _pq(r, 90, 16, 64, 7, 7, 2_000_000), Model(12, SEARCH, 2000, 40, 8000, 300, 2), 8, 800),
