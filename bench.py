@@ -124,14 +124,14 @@ STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", 
                          "sloanneal.hip")
 TRAFFIC_BY_SOURCE = {
     # FETCH_SIZE 175.9 KiB x 2.0 + WRITE_SIZE 16,682.2 KiB x 1.0, burst workload, one launch
-    "772ad588e211c0f20ecaa1b9ef3c495e391b88b66c062e0dbe7d54f045fc55e3": 17442849,
+    "901976da04f2a0f4a61e575bae0df1ddb3b6fb033d39a44edfeb2a243b38cfb4": 17442849,
 }
 
 
 # VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
 # the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
 VALU_BUSY_BY_SOURCE = {
-    "772ad588e211c0f20ecaa1b9ef3c495e391b88b66c062e0dbe7d54f045fc55e3": 0.716,
+    "901976da04f2a0f4a61e575bae0df1ddb3b6fb033d39a44edfeb2a243b38cfb4": 0.716,
 }
 
 

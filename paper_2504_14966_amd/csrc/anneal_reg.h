@@ -12,8 +12,8 @@
 //     row (row_ror, or the two rotations that stay inside an 8-lane half, or quad
 //     permutations); the rotations read the same source registers, so they are independent;
 //   - the batch prefill P and duration D by segment all-reduces, the batch starts by an
-//     exclusive add-scan of D (32-bit, starting at the batch size, when the host bounds the
-//     whole timeline below 2^32; else 64-bit from each batch's last lane);
+//     exclusive add-scan of D (32-bit, starting at the batch size, when the device check
+//     bounds the whole timeline below 2^32; else 64-bit from each batch's last lane);
 //   - TTFT = S + P, e2e = S + F and the SLO tests per lane; the met count by ballot, the
 //     latency sum by two 32-bit reductions of 16-bit halves (or one 64-bit reduction).
 // A move inside one batch changes no member's times and needs no replay. The 32-bit
@@ -522,7 +522,7 @@ __global__ void __launch_bounds__(256) anneal_reg_h_kernel(DevModel m, QueuePtrs
 // terms), its TTFT is the prefill add-scan read at the batch's last lane plus the decode
 // durations of the earlier batches, and the durations are a 32-bit max-scan confined to
 // batches. Prefills, offsets and durations fit 32 bits (the fixed-size width checks); the
-// timeline's prefix sums are plain 32-bit scans when the host bounds it below 2^32, and
+// timeline's prefix sums are plain 32-bit scans when the device check bounds it below 2^32, and
 // saturate otherwise.
 
 __host__ __device__ __forceinline__ bool reg_sized_fits(int n) { return n >= 1 && n <= 64; }

@@ -586,14 +586,16 @@ __global__ void __launch_bounds__(256) anneal_sized_generic_kernel(DevModel m, Q
 // so the change of t over them is a lane sum of new minus old latencies (old start: that
 // of the old batch holding the member's old position). Later batches keep their members
 // and only shift: by D'(A) - D(A) between A and C (swap), by the change of the end of the
-// two batches after C. One pass over the register rows from A on counts the change of the met
-// flags by position: the positions of A and C lose their old flags (their new ones come
-// from the batch passes), the shifted ones compare S + shift with lim. Nothing is written
-// until the proposal is accepted.
+// two batches after C. One pass over the register rows from A on writes the move's starts
+// and limits and counts the change of the met flags by position: the positions of A and C
+// lose their old flags (their new ones come from the batch passes), the shifted ones
+// compare S + shift with lim. Most moves are accepted, so the rows are written before the
+// decision and restored when the move is rejected; the order, layout and F change only
+// on acceptance.
 //
-// Widths (host check): every finish offset, batch prefill, doubled pair-cost sum over a
-// batch and 24-bit multiply operand as in the fixed-size delta kernel, and every time on
-// the timeline of any layout below 2^32 - 1.
+// Widths (checked on the device before any chain runs): every finish offset, batch
+// prefill, doubled pair-cost sum over a batch and 24-bit multiply operand as in the
+// fixed-size delta kernel, and every time on the timeline of any layout below 2^32 - 1.
 
 struct SizedState {
   const uint4 *req;
@@ -605,8 +607,8 @@ struct SizedState {
 };
 
 // f(integral_constant<int, u>) for u = 0 .. N-1: the row loops index their arrays with
-// constants from the start (a loop variable, even one unrolled later, turns an array into
-// one vector value that the compiler copies whole wherever an element changes)
+// compile-time constants, so that each row becomes a register of its own (an array that
+// the compiler keeps as one vector value is copied whole wherever an element changes)
 template <class F, int... I>
 __device__ __forceinline__ void static_for_seq(F &&f, std::integer_sequence<int, I...>) {
   (f(std::integral_constant<int, I>{}), ...);

@@ -32,7 +32,7 @@
 // batch records go to a second array that is copied on accept.
 //
 // Lane layout: a batch occupies Bp = 2^LG lanes (B <= Bp), G = 64 / Bp batches per row.
-// Widths: F, P, D, w and slacks are u32 (the host checks every finish offset and 2w stay
+// Widths: F, P, D, w and slacks are u32 (the device check keeps every finish offset and 2w
 // below 2^32 and the multiply-add operands below 2^24); starts, sums, objective are u64.
 #pragma once
 #include "device_common.h"

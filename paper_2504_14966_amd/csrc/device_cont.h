@@ -320,7 +320,7 @@ __device__ __forceinline__ uint64_t scan_add(uint64_t v) { return scan_add64(v);
 __device__ __forceinline__ uint32_t rl_any(uint32_t v, int l) { return rl(v, l); }
 __device__ __forceinline__ uint64_t rl_any(uint64_t v, int l) { return rl64(v, l); }
 
-// NARROW: every time on the timeline fits 32 bits (the host bounds the total by
+// NARROW: every time on the timeline fits 32 bits (the device check bounds the total by
 // sum(prefill) + (d0 + d1) sum(l_out) + d2 sum(l_out l_in + l_out (l_out + 1) / 2)).
 template <bool DETAIL, bool NARROW, bool INC = false>
 __device__ Score replay_cont_ls(const DevModel &m, const uint4 *__restrict__ req, const uint16_t *perm, Remap rm,

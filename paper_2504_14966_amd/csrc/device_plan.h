@@ -4,7 +4,7 @@
 // copying the queue to the host, so that nothing blocks.
 //
 // Every bound is an exact integer (saturating at 2^64 - 1, products formed in 128 bits),
-// compared against the same limits a host-side check would use:
+// compared against the limits each kernel is written for:
 //   range: the timeline of any order ends before every prefill plus, per decode step (at
 //     most the sum of output lengths), the cost of a full batch of the longest contexts;
 //     n times that, and t_ref (n + 1) plus it, stay below 2^62 (and for the ratio

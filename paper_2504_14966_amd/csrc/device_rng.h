@@ -107,7 +107,7 @@ __device__ __forceinline__ bool metropolis(int64_t delta, int64_t t_ref, double 
 
 // Metropolis rule for the ratio objective G = n / t, with energy G * t_ref: a candidate
 // (n', t') from (n, t) changes the energy by num * t_ref / (t t'), num = n' t - n t' (exact
-// int64: the host bounds n * t below 2^63). Keep it iff num >= 0, or u < e^x with
+// int64: the device check bounds n * t below 2^63). Keep it iff num >= 0, or u < e^x with
 // x = (num * t_ref) / ((t * t') * T) formed by three double operations in that order. The
 // single-precision screen is the one above with the same error budget: (float) of the
 // numerator and of the denominator, a 1-ulp reciprocal and two products. Bits as for
