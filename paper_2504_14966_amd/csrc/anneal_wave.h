@@ -73,6 +73,52 @@ __device__ __forceinline__ void wave_all3(uint32_t &a, uint32_t &b, uint32_t &c)
   c = readlane(c, 63);
 }
 
+// Lane-parallel setup of the changed batches of a move, lane k = batch k with prefill Pk:
+// for each changed batch the leaving request o and the joining request e, their fields, the
+// prefill change, w(e, e) - w(o, e) and the newcomer's finish offset up to half its pair-cost
+// sum over the current members, written as three 16-byte entries of `tab`; fo and ovec take
+// o's old finish offset and id.
+__device__ __forceinline__ void wave_prologue(const uint4 *req, const uint16_t *perm, const uint32_t *F, uint4 *tab,
+                                              uint32_t d0, uint32_t d2, int M, int B, int lane, uint32_t Pk,
+                                              const Move &mv, uint32_t &fo, uint32_t &ovec) {
+  const int k = lane;
+  const bool chg = k < M && mv.changes(k);
+  int opos, epos;
+  if (mv.type == 1) {
+    const int lo = min(mv.i, mv.j), hi = max(mv.i, mv.j);
+    opos = k == mv.a ? lo : hi;
+    epos = k == mv.a ? hi : lo;
+  } else if (mv.i < mv.j) {  // insert moving right: each batch passes its first member left
+    opos = k == mv.a ? mv.i : k * B;
+    epos = k == mv.c ? mv.i : (k + 1) * B;
+  } else {  // insert moving left: each batch passes its last member right
+    opos = k == mv.c ? mv.i : (k + 1) * B - 1;
+    epos = k == mv.a ? mv.i : k * B - 1;
+  }
+  if (!chg) {
+    opos = 0;
+    epos = 0;
+  }
+  const uint32_t o = perm[opos], e = perm[epos];
+  const uint4 ro = req[o], re = req[e];
+  fo = F[o];
+  ovec = o;
+  const uint32_t Lo = ro.x >> 16, eo = ro.z >> 2, Le = re.x >> 16, ee = re.z >> 2;
+  const uint32_t dP = re.w - ro.w;
+  const uint32_t Pc = Pk + dP;
+  const uint32_t corr = w2(Le, ee, Le, d2) - w2(Lo, eo, Le, d2);  // w(e, e) - w(o, e)
+  // the newcomer's offset up to half its pair-cost sum over the current members: every
+  // pair cost mu (e_j + d2 mu) = 2 mu (d1 + d2 l_j) + d2 mu (mu + 1) is even, so that sum
+  // and corr halve exactly one by one (corr as a signed value, |corr| < 2^31)
+  const uint32_t FeBase = Pc + __umul24(Le, d0) + (uint32_t)((int32_t)corr >> 1);
+  if (chg) {
+    tab[3 * k] = make_uint4(o, e, Lo, eo);
+    tab[3 * k + 1] = make_uint4(Le, ee, dP, corr);
+    tab[3 * k + 2] = make_uint4(FeBase, re.z & 3u, re.y, Pc);
+  }
+  wave_sync_lds();
+}
+
 // batch records, lane k = batch k
 struct LaneRecs {
   uint32_t Slo, Shi, P, D, cnt, A, Bv;
@@ -176,41 +222,7 @@ struct WaveChain {
   }
 
   // Lane-parallel setup of the changed batches of a move (lane k = batch k).
-  __device__ void prologue(const Move &mv) {
-    const int k = lane;
-    const bool chg = k < M && mv.changes(k);
-    int opos, epos;
-    if (mv.type == 1) {
-      const int lo = min(mv.i, mv.j), hi = max(mv.i, mv.j);
-      opos = k == mv.a ? lo : hi;
-      epos = k == mv.a ? hi : lo;
-    } else if (mv.i < mv.j) {  // insert moving right: each batch passes its first member left
-      opos = k == mv.a ? mv.i : k * B;
-      epos = k == mv.c ? mv.i : (k + 1) * B;
-    } else {  // insert moving left: each batch passes its last member right
-      opos = k == mv.c ? mv.i : (k + 1) * B - 1;
-      epos = k == mv.a ? mv.i : k * B - 1;
-    }
-    if (!chg) {
-      opos = 0;
-      epos = 0;
-    }
-    const uint32_t o = perm[opos], e = perm[epos];
-    const uint4 ro = req[o], re = req[e];
-    fo = F[o];
-    ovec = o;
-    const uint32_t Lo = ro.x >> 16, eo = ro.z >> 2, Le = re.x >> 16, ee = re.z >> 2;
-    const uint32_t dP = re.w - ro.w;
-    const uint32_t Pc = cur.P + dP;
-    const uint32_t corr = w2(Le, ee, Le, d2) - w2(Lo, eo, Le, d2);  // w(e, e) - w(o, e)
-    const uint32_t FeBase = Pc + __umul24(Le, d0);
-    if (chg) {
-      tab[3 * k] = make_uint4(o, e, Lo, eo);
-      tab[3 * k + 1] = make_uint4(Le, ee, dP, corr);
-      tab[3 * k + 2] = make_uint4(FeBase, re.z & 3u, re.y, Pc);
-    }
-    wave_sync_lds();
-  }
+  __device__ void prologue(const Move &mv) { wave_prologue(req, perm, F, tab, d0, d2, M, B, lane, cur.P, mv, fo, ovec); }
 
   // Candidate of changed batch k starting `shift` later: finish offsets (written to F),
   // record, met-count and latency changes. Returns the duration change.
@@ -219,7 +231,7 @@ struct WaveChain {
     const bool valid = lane < bs;
     const uint4 t0 = tab[3 * k], t1 = tab[3 * k + 1], t2 = tab[3 * k + 2];
     const uint32_t o = t0.x, e = t0.y, Lo = t0.z, eo = t0.w;
-    const uint32_t Le = t1.x, ee = t1.y, dP = t1.z, corr = t1.w;
+    const uint32_t Le = t1.x, ee = t1.y, dP = t1.z;
     const uint32_t FeBase = t2.x, kinde = t2.y, thre = t2.z, Pc = t2.w;
     // lanes past the batch read the zero spare record and F[n] = 0 (their position is
     // clamped into the order and the read discarded, so that the row has no branch)
@@ -235,7 +247,7 @@ struct WaveChain {
     const bool is_out = r == o;
     uint32_t tsum = te, dsum = (valid && !is_out) ? (uint32_t)dwh : 0u;
     wave_all2<OpAdd, OpAdd>(tsum, dsum);
-    const uint32_t Fe = FeBase + ((tsum + corr) >> 1);
+    const uint32_t Fe = FeBase + (tsum >> 1);
     const uint32_t Fc = is_out ? Fe : Fm + dP + (uint32_t)dwh;
     F[valid ? (is_out ? e : r) : N + 1] = Fc;
     const uint32_t Fn = valid ? Fc : 0u;

@@ -18,6 +18,7 @@
 #include "anneal_static.h"
 #include "anneal_wave.h"
 #include "anneal_sized.h"
+#include "anneal_wave_rows.h"
 #include "multi.h"
 #include "anneal_reg.h"
 #include "fit.h"
@@ -213,6 +214,8 @@ struct ChainArgs {
 };
 
 static_assert(sa::sized_rows_for(SCHED_MAX_N) * 64 >= SCHED_MAX_N, "register rows must cover every position");
+static_assert(sa::limit_rows_for((SCHED_MAX_N + 32) / 33) * 33 >= SCHED_MAX_N,
+              "limit rows must cover every batch when batches hold 33 or more");
 
 template <int OBJ, int NR>
 hipError_t launch_sized(int grid, int waves, size_t lds, const sa::DevModel &d, const sa::StaticParams &sp,
@@ -283,6 +286,19 @@ hipError_t launch_reg(bool parts, int grid, int waves, const sa::DevModel &d, co
   return hipGetLastError();
 }
 
+template <int OBJ, int MR>
+hipError_t launch_rows(int waves, size_t lds, const sa::DevModel &d, const sa::StaticParams &sp, const ChainArgs &a) {
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&sa::anneal_rows_kernel<OBJ, MR>),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int grid = (a.chains + waves - 1) / waves;
+  sa::anneal_rows_kernel<OBJ, MR><<<grid, waves * 64, lds, a.stream>>>(d, sp, a.q, a.chains, a.iters, a.T0, a.alpha,
+                                                                       a.k0, a.k1, a.swap_thr, a.srch, a.w);
+  return hipGetLastError();
+}
+
 template <int LG, int OBJ>
 hipError_t launch_static(int waves, size_t lds, const sa::DevModel &d, const sa::StaticParams &sp, const ChainArgs &a) {
   const void *fn = LG == 6 ? reinterpret_cast<const void *>(&sa::anneal_wave_kernel<OBJ>)
@@ -306,7 +322,9 @@ hipError_t launch_static(int waves, size_t lds, const sa::DevModel &d, const sa:
 //   static: the register kernel (up to 64 requests, or 65 to 192 with two or three positions
 //     per lane; batches of 1 .. 16, a power of two) or else the LDS delta kernel (one lane per
 //     batch member, or one batch per wave for batches of more than 32), both on the 32-bit
-//     pair-cost widths, the register kernel also on a 32-bit timeline when it holds;
+//     pair-cost widths, the register kernel also on a 32-bit timeline when it holds, and
+//     one batch per wave with the members' SLO limits in registers ahead of the plain one
+//     when the timeline fits 32 bits;
 //   continuous: list scheduling when its 32-bit keys fit, the event loop when the 32-bit event
 //     arithmetic does, each as the LDS allows;
 //   always last: the full-replay kernel (any widths).
@@ -344,6 +362,23 @@ void add_chains(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, 
       if (soa + per * waves <= (size_t)lim && (waves >= 4 || (int64_t)waves * cus >= a.chains)) {
         const sa::StaticParams sp{(uint32_t)model->d0, (uint32_t)model->d2, (1ull << 32) / (uint64_t)B + 1};
         const size_t lds = soa + per * waves;
+        if (lg == 6) {
+          // the limit-row kernel when the whole timeline fits 32 bits (its chains take a
+          // little more LDS: the order carries 64 spare entries)
+          const size_t rper = sa::rows_chain_bytes(n, B);
+          int rwaves = waves;
+          while (rwaves > 1 && soa + rper * rwaves > (size_t)lim) rwaves >>= 1;
+          const size_t rlds = soa + rper * rwaves;
+          const int rows = sa::limit_rows_for((n + B - 1) / B);
+          if (rlds <= (size_t)lim && (rwaves >= 4 || (int64_t)rwaves * cus >= a.chains))
+            c.add(kSN | kT32, kAnnealFlags, [=](const sa::DevModel &d) {
+              switch (rows) {
+                case 8: return launch_rows<OBJ, 8>(rwaves, rlds, d, sp, a);
+                case 16: return launch_rows<OBJ, 16>(rwaves, rlds, d, sp, a);
+                default: return launch_rows<OBJ, 32>(rwaves, rlds, d, sp, a);
+              }
+            });
+        }
         c.add(kSN, kAnnealFlags, [=](const sa::DevModel &d) {
           switch (lg) {
             case 0: return launch_static<0, OBJ>(waves, lds, d, sp, a);

@@ -1,7 +1,8 @@
 """GPU parity of every kernel path the host dispatch can choose, against the oracle.
 
 The library picks a kernel from the queue and model: the static delta kernels (32-bit
-finish offsets; batch records in LDS for B <= 32, in lane-per-batch registers for B > 32),
+finish offsets; batch records in LDS for B <= 32, in lane-per-batch registers for B > 32,
+with every member's SLO limit in registers too when the whole timeline fits 32 bits),
 the continuous list-scheduling replay (total output below 2^22 tokens), the continuous
 event loop (32-bit event arithmetic), or the general full-replay kernels (64-bit
 everything). Each case below is built so that its
@@ -41,6 +42,9 @@ CASES = {
     "static_b1_n1024": (lambda r: _queue(r, 1024, 16, 2048, 1, 6, 4_000_000_000), Model(1, 0, 2000, 40, 8000, 300, 2), 8, 150),
     # static, one batch per wave (B > 32) with a ragged last batch: lane-per-batch kernel
     "static_wave_ragged": (lambda r: _queue(r, 150, 16, 2048, 1, 300, 4_000_000_000), Model(40, 0, 2000, 40, 8000, 300, 2), 8, 400),
+    # static, one batch per wave with a timeline beyond 2^32 (every finish offset still
+    # within 32 bits): the lane-per-batch kernel without the registers of member limits
+    "static_wave_wide_time": (lambda r: _queue(r, 300, 16, 2048, 1000, 3000, 4_000_000_000), Model(40, 0, 2000, 40, 8000, 300, 2), 4, 120),
     # static, B > 32 and B > n: a single batch, every move keeps the objective
     "static_wave_one_batch": (lambda r: _queue(r, 50, 16, 2048, 1, 300, 4_000_000_000), Model(64, 0, 2000, 40, 8000, 300, 2), 4, 100),
     # static, d2 so large that pair costs exceed 24 bits: general full-replay kernel
@@ -59,6 +63,12 @@ CASES = {
     # continuous, list scheduling with a timeline longer than 2^32 us (64-bit segment sums)
     "cont_ls_wide_time": (lambda r: _queue(r, 40, 16, 2048, 20000, 60000, 4_000_000_000), Model(8, 1, 2000, 40, 8000, 300, 2), 4, 60),
 }
+
+
+# the candidate that must run, for cases where the order of candidates is the point: under
+# static admission with B > 32, the kernel with the member limits in registers comes first
+# and needs a 32-bit timeline; the plain lane-per-batch kernel follows it
+SELECTED = {"static_wave_ragged": 0, "static_wave_wide_time": 1}
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
@@ -86,7 +96,11 @@ def test_anneal_path(sl, orc, name):
     dq = sl.DeviceQueue.from_queue(q)
     ws = sl.sched_anneal(dq, m, chains, iters, 0.7, 0.99, 11)
     rec, cur, best = sl.sched_chains(ws, q.n, chains, perms=True)
+    status = sl.sched_status(ws).cpu().tolist()
     torch.cuda.synchronize()
+    assert status[0] == 0, (name, status)
+    if name in SELECTED:
+        assert status[2] == SELECTED[name], (name, status)
     rec, cur, best = rec.cpu().numpy(), sl.as_u16(cur), sl.as_u16(best)
     info = orc.start(q, m)
     want = oracle_chains(q, m, list(range(chains)), iters, 0.7, 0.99, 11, info)
