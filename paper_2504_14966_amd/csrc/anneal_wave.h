@@ -73,14 +73,27 @@ __device__ __forceinline__ void wave_all3(uint32_t &a, uint32_t &b, uint32_t &c)
   c = readlane(c, 63);
 }
 
+// Request records whose third word holds e above the kind (e << 2 | kind, KTOP false) or e
+// below flag bits for the kind (e | 2^30 for end-to-end | 2^31 for TPOT, KTOP true): e, and
+// the kind code a newcomer's entry carries (the kind, or the whole word).
+template <bool KTOP>
+__device__ __forceinline__ uint32_t rec_e(uint32_t z) {
+  return KTOP ? (z & 0x3FFFFFFFu) : (z >> 2);
+}
+template <bool KTOP>
+__device__ __forceinline__ uint32_t rec_kind_code(uint32_t z) {
+  return KTOP ? z : (z & 3u);
+}
+
 // Lane-parallel setup of the changed batches of a move, lane k = batch k with prefill Pk:
 // for each changed batch the leaving request o and the joining request e, their fields, the
 // prefill change, w(e, e) - w(o, e) and the newcomer's finish offset up to half its pair-cost
 // sum over the current members, written as three 16-byte entries of `tab`; fo and ovec take
-// o's old finish offset and id.
+// o's old finish offset and id, Pn the batch's prefill after the move.
+template <bool KTOP = false>
 __device__ __forceinline__ void wave_prologue(const uint4 *req, const uint16_t *perm, const uint32_t *F, uint4 *tab,
                                               uint32_t d0, uint32_t d2, int M, int B, int lane, uint32_t Pk,
-                                              const Move &mv, uint32_t &fo, uint32_t &ovec) {
+                                              const Move &mv, uint32_t &fo, uint32_t &ovec, uint32_t &Pn) {
   const int k = lane;
   const bool chg = k < M && mv.changes(k);
   int opos, epos;
@@ -103,9 +116,10 @@ __device__ __forceinline__ void wave_prologue(const uint4 *req, const uint16_t *
   const uint4 ro = req[o], re = req[e];
   fo = F[o];
   ovec = o;
-  const uint32_t Lo = ro.x >> 16, eo = ro.z >> 2, Le = re.x >> 16, ee = re.z >> 2;
+  const uint32_t Lo = ro.x >> 16, eo = rec_e<KTOP>(ro.z), Le = re.x >> 16, ee = rec_e<KTOP>(re.z);
   const uint32_t dP = re.w - ro.w;
   const uint32_t Pc = Pk + dP;
+  Pn = chg ? Pc : Pk;
   const uint32_t corr = w2(Le, ee, Le, d2) - w2(Lo, eo, Le, d2);  // w(e, e) - w(o, e)
   // the newcomer's offset up to half its pair-cost sum over the current members: every
   // pair cost mu (e_j + d2 mu) = 2 mu (d1 + d2 l_j) + d2 mu (mu + 1) is even, so that sum
@@ -114,7 +128,7 @@ __device__ __forceinline__ void wave_prologue(const uint4 *req, const uint16_t *
   if (chg) {
     tab[3 * k] = make_uint4(o, e, Lo, eo);
     tab[3 * k + 1] = make_uint4(Le, ee, dP, corr);
-    tab[3 * k + 2] = make_uint4(FeBase, re.z & 3u, re.y, Pc);
+    tab[3 * k + 2] = make_uint4(FeBase, rec_kind_code<KTOP>(re.z), re.y, Pc);
   }
   wave_sync_lds();
 }
@@ -222,7 +236,10 @@ struct WaveChain {
   }
 
   // Lane-parallel setup of the changed batches of a move (lane k = batch k).
-  __device__ void prologue(const Move &mv) { wave_prologue(req, perm, F, tab, d0, d2, M, B, lane, cur.P, mv, fo, ovec); }
+  __device__ void prologue(const Move &mv) {
+    uint32_t Pn;
+    wave_prologue(req, perm, F, tab, d0, d2, M, B, lane, cur.P, mv, fo, ovec, Pn);
+  }
 
   // Candidate of changed batch k starting `shift` later: finish offsets (written to F),
   // record, met-count and latency changes. Returns the duration change.

@@ -47,14 +47,15 @@ __device__ __forceinline__ int64_t rows_met(const LimRows<MR> &lim, uint32_t S) 
   return (int64_t)cnt;
 }
 
-// The limit of a member from its record's kind and thr1 = threshold + 1: met iff the batch
-// starts before it. TTFT: thr1 - P, end-to-end: thr1 - F (0 when not positive: never met),
-// TPOT: 2^32 - 1 when F - P < thr1, else 0. The zero spare record gives 0.
-__device__ __forceinline__ uint32_t limit_of(uint32_t kind, uint32_t thr1, uint32_t P, uint32_t F) {
-  const uint32_t off = kind == 0u ? P : F;
+// The limit of a member from its record's third word z (e | 2^30 for end-to-end | 2^31 for
+// TPOT, TTFT with neither) and thr1 = threshold + 1: met iff the batch starts before it.
+// TTFT: thr1 - P, end-to-end: thr1 - F (0 when not positive: never met), TPOT: 2^32 - 1 when
+// F - P < thr1, else 0. The zero spare record gives 0.
+__device__ __forceinline__ uint32_t limit_of(uint32_t z, uint32_t thr1, uint32_t P, uint32_t F) {
+  const uint32_t off = z < (1u << 30) ? P : F;
   const uint32_t by_start = __builtin_elementwise_sub_sat(thr1, off);
   const uint32_t tpot = F - P < thr1 ? 0xFFFFFFFFu : 0u;
-  return kind == 1u ? tpot : by_start;
+  return (int32_t)z < 0 ? tpot : by_start;
 }
 
 // batch records, lane k = batch k: start, prefill, duration
@@ -105,18 +106,19 @@ __device__ __forceinline__ Score rows_init(RowChain &c, LimRows<MR> &lim) {
     const int bs = c.batch_size(k);
     const bool valid = lane < bs;
     const int r = valid ? (int)c.perm[q0 + lane] : c.N;
-    const Req rq = load_req(c.req, r);
+    const uint4 rq = c.req[r];
+    const uint32_t L = rq.x >> 16;
     uint32_t P = 0, acc = 0;
     for (int jj = 0; jj < bs; ++jj) {
-      const Req o = load_req(c.req, c.perm[q0 + jj]);
-      P += o.pf;
-      acc += w2(o.L, o.e, rq.L, c.d2);
+      const uint4 o = c.req[c.perm[q0 + jj]];
+      P += o.w;
+      acc += w2(o.x >> 16, rec_e<true>(o.z), L, c.d2);
     }
-    const uint32_t Fv = valid ? P + __umul24(rq.L, c.d0) + (acc >> 1) : 0u;
+    const uint32_t Fv = valid ? P + __umul24(L, c.d0) + (acc >> 1) : 0u;
     if (valid) c.F[r] = Fv;
     const uint64_t SF = Seg<6>::sum_wide(Fv, lane);
     const uint32_t D = Seg<6>::template all<OpMax>(Fv, lane);
-    lim[k] = valid ? limit_of(rq.kind, rq.thr, P, Fv) : 0u;
+    lim[k] = valid ? limit_of(rq.z, rq.y, P, Fv) : 0u;
     c.cur.S = lane == k ? carry : c.cur.S;
     c.cur.P = lane == k ? P : c.cur.P;
     c.cur.D = lane == k ? D : c.cur.D;
@@ -151,7 +153,7 @@ __device__ __forceinline__ int64_t rows_changed(RowChain &c, LimRows<MR> &lim, i
   const uint32_t r = valid ? rr : (uint32_t)N;
   const uint4 rq = c.req[r];
   const uint32_t Fm = c.F[r];
-  const uint32_t Lm = rq.x >> 16, em = rq.z >> 2;
+  const uint32_t Lm = rq.x >> 16, em = rec_e<true>(rq.z);
   const uint32_t mue = min(Lm, Le), muo = min(Lm, Lo);
   const uint32_t te = vmul24(mue, vmad24(c.vd2, mue, em));   // w(m, e)
   const uint32_t wem = vmul24(mue, vmad24(c.vd2, mue, ee));  // w(e, m)
@@ -167,12 +169,11 @@ __device__ __forceinline__ int64_t rows_changed(RowChain &c, LimRows<MR> &lim, i
   const uint32_t Fc = is_out ? Fe : Fs;
   c.F[is_out ? e : r] = Fc;
   // lanes past the batch hold the spare record: limit 0
-  const uint32_t kind = is_out ? kinde : (rq.z & 3u), thr1 = is_out ? thre : rq.y;
-  lim[k] = limit_of(kind, thr1, Pc, Fc);
+  const uint32_t z = is_out ? kinde : rq.z, thr1 = is_out ? thre : rq.y;
+  lim[k] = limit_of(z, thr1, Pc, Fc);
   const uint32_t S = readlane(c.cur.S, k) + (uint32_t)shift;
   const uint32_t D0 = readlane(c.cur.D, k), Fo = readlane(c.fo, k);
   c.cand.S = wlane_m0(S, k, c.cand.S);
-  c.cand.P = lane != k ? c.cand.P : Pc;
   c.cand.D = wlane_m0(Dn, k, c.cand.D);
   const int64_t dSF =
       (int64_t)(bs - 1) * (int64_t)(int32_t)rfl(dP) + (int64_t)(int32_t)dsum + ((int64_t)Fe - (int64_t)Fo);
@@ -192,7 +193,7 @@ __device__ __forceinline__ void rows_shift(RowChain &c, int k0, int k1, int64_t 
 template <int MR>
 __device__ __forceinline__ int64_t rows_propose(RowChain &c, LimRows<MR> &lim, const Move &mv, int64_t &dt) {
   c.cand = c.cur;
-  wave_prologue(c.req, c.perm, c.F, c.tab, c.d0, c.d2, c.M, c.B, c.lane, c.cur.P, mv, c.fo, c.ovec);
+  wave_prologue<true>(c.req, c.perm, c.F, c.tab, c.d0, c.d2, c.M, c.B, c.lane, c.cur.P, mv, c.fo, c.ovec, c.cand.P);
   dt = 0;
   int64_t carry = rows_changed(c, lim, mv.a, 0, dt);
   const int64_t shift_mid = carry;  // start change of the batches between a and c (swap)
@@ -229,7 +230,7 @@ __device__ __forceinline__ void rows_undo(RowChain &c, LimRows<MR> &lim, const M
     const bool is_out = r == o;
     const uint32_t Fold = is_out ? readlane(c.fo, k) : Fm - dP - (uint32_t)dwh;
     c.F[r] = Fold;
-    lim[k] = limit_of(rq.z & 3u, rq.y, readlane(c.cur.P, k), Fold);
+    lim[k] = limit_of(rq.z, rq.y, readlane(c.cur.P, k), Fold);
   }
   wave_sync_lds();
 }
@@ -358,8 +359,15 @@ __global__ void __launch_bounds__(1024) anneal_rows_kernel(DevModel m, StaticPar
   load_static_records(q, m, req);
   __syncthreads();
   // thresholds as thr1 = threshold + 1 (a TPOT product above 2^32 - 2 is first lowered to
-  // 2^32 - 2, which decides alike: F - P stays below 2^32 - 1); the spare record keeps 0
-  for (int r = threadIdx.x; r < n; r += blockDim.x) req[r].y = min(req[r].y, 0xFFFFFFFEu) + 1u;
+  // 2^32 - 2, which decides alike: F - P stays below 2^32 - 1), and the kind as flag bits
+  // above e (e | 2^30 for end-to-end | 2^31 for TPOT; e < 2^24 by the width checks); the
+  // spare record keeps 0
+  for (int r = threadIdx.x; r < n; r += blockDim.x) {
+    const uint4 v = req[r];
+    const uint32_t kind = v.z & 3u;
+    req[r].y = min(v.y, 0xFFFFFFFEu) + 1u;
+    req[r].z = (v.z >> 2) | (kind == 2u ? 1u << 30 : 0u) | (kind == 1u ? 1u << 31 : 0u);
+  }
   __syncthreads();
   const int chain = uniform((int)blockIdx.x * waves + wave);
   if (chain >= chains) return;
