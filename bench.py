@@ -116,22 +116,29 @@ def expected_work(W) -> dict:
                 delta_algorithm_ops=OPS_CHANGED_MEMBER * members + OPS_SHIFTED_BATCH * shifted)
 
 
-# HBM bytes per launch of the dominant kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
-# passes (KiB, scaled by the factor a 256 MiB device copy gives each counter: 2.0 for
-# FETCH_SIZE, 1.0 for WRITE_SIZE), keyed by the SHA-256 of the sources that kernel is
-# compiled and launched from; any other source gives null.
-STATIC_KERNEL_SOURCES = ("anneal_wave.h", "anneal_static.h", "device_common.h", "device_replay.h", "device_rng.h",
-                         "sloanneal.hip")
-TRAFFIC_BY_SOURCE = {
-    # FETCH_SIZE 175.9 KiB x 2.0 + WRITE_SIZE 16,682.2 KiB x 1.0, burst workload, one launch
-    "901976da04f2a0f4a61e575bae0df1ddb3b6fb033d39a44edfeb2a243b38cfb4": 17442849,
-}
-
-
-# VALU busy share of the dominant kernel from the same counter runs (4 x SQ_INSTS_VALU over
-# the active cycles of all 1024 SIMDs, GRBM_GUI_ACTIVE / 8 per XCD), same keying.
-VALU_BUSY_BY_SOURCE = {
-    "901976da04f2a0f4a61e575bae0df1ddb3b6fb033d39a44edfeb2a243b38cfb4": 0.716,
+# Figures of the dominant kernel from its rocprofv3 runs, keyed by the SHA-256 of the sources
+# it is compiled and launched from (every header it includes and the file that launches it);
+# any other source gives null. From the counter runs over one launch of the burst workload:
+#   traffic: HBM bytes per launch, FETCH_SIZE and WRITE_SIZE (KiB) scaled by the factors a
+#     256 MiB device copy gives each counter in the same runs (2.0 and 1.0);
+#   valu_busy: 4 x SQ_INSTS_VALU over the active cycles of all 1024 SIMDs (GRBM_GUI_ACTIVE / 8
+#     per XCD), the share of cycles the vector units issue;
+#   lds_bank_conflict_cycles_per_lds_instr: SQ_LDS_BANK_CONFLICT / SQ_INSTS_LDS, and
+#   lds_instr_per_chain_iter: SQ_INSTS_LDS per proposal.
+# From the launch itself: vgprs (the code object's count for the kernel), LDS bytes per
+# workgroup (the request records, (n + 1) x 16, and 16 chains of 7,056 bytes each) and the
+# waves per SIMD that are resident (4096 chains, 16 per CU in one workgroup; the LDS allows
+# one such workgroup per CU, the registers five waves per SIMD).
+HEADLINE_KERNEL_SOURCES = ("anneal_wave_rows.h", "anneal_wave.h", "anneal_sized.h", "anneal_static.h", "kernels.h",
+                           "device_cont.h", "device_plan.h", "device_replay.h", "device_rng.h", "device_common.h",
+                           "sloanneal.hip")
+PROFILE_BY_SOURCE = {
+    # anneal_rows_kernel<0, 16> on the burst workload: FETCH_SIZE 161.4 KiB x 2.0 + WRITE_SIZE
+    # 16,677.6 KiB x 1.0; 441.7 VALU and 54.9 LDS instructions, 116.3 bank-conflict cycles
+    # per proposal
+    "e265f3e4d95da1bc857c0d7c2984ebc158f254d86b0a8044c800ac9c08a141da": {
+        "traffic": 17408407, "valu_busy": 0.666, "lds_bank_conflict_cycles_per_lds_instr": 2.12,
+        "lds_instr_per_chain_iter": 54.9, "vgprs": 89, "lds_bytes_per_workgroup": 129296, "waves_per_simd": 4},
 }
 
 
@@ -139,18 +146,15 @@ def kernel_source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2504_14966_amd", "csrc")
-    for f in STATIC_KERNEL_SOURCES:
+    for f in HEADLINE_KERNEL_SOURCES:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
-def measured_traffic():
-    return TRAFFIC_BY_SOURCE.get(kernel_source_hash())
-
-
-def measured_valu_busy():
-    return VALU_BUSY_BY_SOURCE.get(kernel_source_hash())
+def measured_profile():
+    """The profile figures of the headline kernel, or None when its sources changed since."""
+    return PROFILE_BY_SOURCE.get(kernel_source_hash())
 
 
 def time_anneal(sl, W, steps, warmup, torch):
@@ -544,6 +548,7 @@ def main():
         cpu["parity"] = compare_chains(sl, main_ws, W.queue.n, W.chains, recs)
         log(f"[bench] oracle chains against the timed run's GPU records: {cpu['parity']}")
 
+    prof = measured_profile()
     line = {
         "metric": "SA chain-iterations/s",
         "value": value,
@@ -561,11 +566,11 @@ def main():
                    "policy": "static" if W.model.policy == 0 else "continuous", "chains": W.chains,
                    "iters": W.iters, "T0": W.T0, "alpha": W.alpha, "parallelism": "chains"},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12, "unit": "TOP/s",
-                     "frac": achieved / PEAK_LANE_OPS, "traffic": measured_traffic(),
-                     "rocprof_valu_busy": measured_valu_busy(),
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": (prof or {}).get("traffic"),
+                     "rocprof": prof,
                      "delta_algorithm_frac": (work.get("delta_algorithm_ops", 0.0) * chain_iters / (k_ms * 1e-3))
                                              / PEAK_LANE_OPS,
-                     "kernel": "anneal_wave_kernel", "kernel_ms": k_ms,
+                     "kernel": "anneal_rows_kernel", "kernel_ms": k_ms,
                      "algo_lane_ops_per_chain_iter": work["ops"], "work_per_chain_iter": work},
         "cpu_baseline": cpu,
         "extras": extras,
