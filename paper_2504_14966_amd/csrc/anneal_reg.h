@@ -77,6 +77,27 @@ __device__ __forceinline__ uint32_t pair_sum_others(uint32_t L, uint32_t e, uint
   return acc;
 }
 
+// A move on positions held one per lane, as the byte address of each lane's source lane:
+// a swap exchanges lanes i and `to`; an insert moves lane i to lane `to` and shifts the lanes
+// between by one toward i. Every field of the candidate is then one lane permute
+// (ds_bpermute) with this address, instead of v_readlane / v_writelane pairs whose scalar
+// hand-offs serialise.
+__device__ __forceinline__ int move_src_addr(bool swap, int i, int to, int lane) {
+  int src;
+  if (swap) {
+    src = lane == i ? to : (lane == to ? i : lane);
+  } else {
+    const bool right = i < to;
+    const int lo = right ? i : to + 1;
+    const uint32_t span = (uint32_t)(right ? to - i : i - to);
+    src = lane == to ? i : ((uint32_t)(lane - lo) < span ? lane + (right ? 1 : -1) : lane);
+  }
+  return src << 2;
+}
+__device__ __forceinline__ uint32_t from_lane(int addr, uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute(addr, (int)x);
+}
+
 // 64-bit all-reduce (sum) over the wave, result in every lane
 __device__ __forceinline__ uint64_t wave_sum64_dpp(uint64_t v) {
   const uint64_t incl = scan_add64(v);
@@ -170,29 +191,10 @@ __device__ void anneal_reg_body(const DevModel &m, const QueuePtrs &q, int chain
     if ((k & (kWave - 1)) == 0) ps.refill(k, lane, n, rng_chain, key0, key1, swap_thr, 0);
     const uint32_t pk = ps.packed(k), w3 = ps.word3(k);
     const int i = (int)(pk & 1023u), j = (int)((pk >> 10) & 1023u);
-    RegState cand;
-    if (((pk >> 20) & 1u) == 0u) {
-      // swap positions i and j
-      auto sw = [&](uint32_t x) {
-        const uint32_t xi = readlane(x, i), xj = readlane(x, j);
-        return wlane_m0(xi, j, wlane_m0(xj, i, x));
-      };
-      cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
-    } else {
-      // insert: the request at i moves to j, the ones between shift by one toward i (lanes
-      // [i, j) take x[lane + 1], or lanes (j, i] take x[lane - 1])
-      const bool right = i < j;
-      const int lo = right ? i : j + 1;
-      const uint32_t span = (uint32_t)(right ? j - i : i - j);
-      const bool in_rng = (uint32_t)(lane - lo) < span;
-      auto ins = [&](uint32_t x, uint32_t sh) { return wlane_m0(readlane(x, i), j, in_rng ? sh : x); };
-      if (right)
-        cand = RegState{ins(cur.A, dppv<0x130>(cur.A)), ins(cur.E, dppv<0x130>(cur.E)),
-                        ins(cur.PF, dppv<0x130>(cur.PF)), ins(cur.T, dppv<0x130>(cur.T))};
-      else
-        cand = RegState{ins(cur.A, dppv<0x138>(cur.A)), ins(cur.E, dppv<0x138>(cur.E)),
-                        ins(cur.PF, dppv<0x138>(cur.PF)), ins(cur.T, dppv<0x138>(cur.T))};
-    }
+    // swap positions i and j, or insert the request at i at j (the ones between shift by
+    // one toward i)
+    const int addr = move_src_addr(((pk >> 20) & 1u) == 0u, i, j, lane);
+    const RegState cand{from_lane(addr, cur.A), from_lane(addr, cur.E), from_lane(addr, cur.PF), from_lane(addr, cur.T)};
     // a move inside one batch keeps every batch's members: the score is unchanged (and the
     // move is kept under either objective), so the replay is skipped
     const Score s = (i >> LG) == (j >> LG) ? Score{cn, ct} : reg_replay<LG, T32>(cand, n, d0, d2, lane);
@@ -709,30 +711,14 @@ __device__ void anneal_reg_sized_body(const DevModel &m, const QueuePtrs &q, int
     const uint32_t pk = ds.packed(k), w3 = ds.word3(k);
     const RegMove mv = reg_plan(fm, n, B, (int)(pk >> 20), (int)(pk & 1023u), (int)((pk >> 10) & 1023u));
     if (mv.made) {
-      RegState cand;
       uint64_t fc = fm;
       int nb0 = cb0, nb1 = cb1;
-      if (mv.op == 2) {
-        const int i = mv.i, j = mv.j;
-        auto sw = [&](uint32_t x) {
-          const uint32_t xi = readlane(x, i), xj = readlane(x, j);
-          return wlane_m0(xi, j, wlane_m0(xj, i, x));
-        };
-        cand = RegState{sw(cur.A), sw(cur.E), sw(cur.PF), sw(cur.T)};
-      } else {
-        // lanes [i, to) take x[lane + 1], or lanes (to, i] take x[lane - 1]
-        const int i = mv.i, to = mv.to;
-        const bool right = i < to;
-        const int lo = right ? i : to + 1;
-        const uint32_t span = (uint32_t)(right ? to - i : i - to);
-        const bool in_rng = (uint32_t)(lane - lo) < span;
-        auto ins = [&](uint32_t x, uint32_t sh) { return wlane_m0(readlane(x, i), to, in_rng ? sh : x); };
-        if (right)
-          cand = RegState{ins(cur.A, dppv<0x130>(cur.A)), ins(cur.E, dppv<0x130>(cur.E)),
-                          ins(cur.PF, dppv<0x130>(cur.PF)), ins(cur.T, dppv<0x130>(cur.T))};
-        else
-          cand = RegState{ins(cur.A, dppv<0x138>(cur.A)), ins(cur.E, dppv<0x138>(cur.E)),
-                          ins(cur.PF, dppv<0x138>(cur.PF)), ins(cur.T, dppv<0x138>(cur.T))};
+      // a swap of i and j, or an insert from i to `to` (lanes [i, to) take x[lane + 1], or
+      // lanes (to, i] take x[lane - 1])
+      const int addr = move_src_addr(mv.op == 2, mv.i, mv.op == 2 ? mv.j : mv.to, lane);
+      const RegState cand{from_lane(addr, cur.A), from_lane(addr, cur.E), from_lane(addr, cur.PF),
+                          from_lane(addr, cur.T)};
+      if (mv.op != 2) {
         if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
         if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
         bounds(fc, nb0, nb1);
@@ -915,25 +901,10 @@ __device__ void anneal_reg_fit_body(const DevFit &f, const QueuePtrs &q, const u
       mv = RegMove{true, ((pk >> 20) & 1u) ? 3 : 2, i, j, j, -1, -1};
     }
     if (mv.made) {
-      RegFit cand;
       uint64_t fc = fm;
-      if (mv.op == 2) {
-        const int i = mv.i, j = mv.j;
-        auto sw = [&](uint32_t x) {
-          const uint32_t xi = readlane(x, i), xj = readlane(x, j);
-          return wlane_m0(xi, j, wlane_m0(xj, i, x));
-        };
-        cand = RegFit{sw(cur.A), sw(cur.LK), sw(cur.T), sw(cur.T2)};
-      } else {
-        const int i = mv.i, to = mv.to;
-        const bool right = i < to;
-        const bool in_rng = right ? (lane >= i && lane < to) : (lane > to && lane <= i);
-        auto ins = [&](uint32_t x) {
-          const uint32_t xi = readlane(x, i);
-          const uint32_t sh = right ? dppv<0x130>(x) : dppv<0x138>(x);
-          return wlane_m0(xi, to, in_rng ? sh : x);
-        };
-        cand = RegFit{ins(cur.A), ins(cur.LK), ins(cur.T), ins(cur.T2)};
+      const int addr = move_src_addr(mv.op == 2, mv.i, mv.op == 2 ? mv.j : mv.to, lane);
+      const RegFit cand{from_lane(addr, cur.A), from_lane(addr, cur.LK), from_lane(addr, cur.T), from_lane(addr, cur.T2)};
+      if (mv.op != 2) {
         if (mv.clr0 >= 0) fc &= ~(uint64_t(1) << mv.clr0);
         if (mv.set0 >= 0) fc |= uint64_t(1) << mv.set0;
       }
