@@ -133,11 +133,11 @@ HEADLINE_KERNEL_SOURCES = ("anneal_wave_rows.h", "anneal_wave.h", "anneal_sized.
                            "device_cont.h", "device_plan.h", "device_replay.h", "device_rng.h", "device_common.h",
                            "sloanneal.hip")
 PROFILE_BY_SOURCE = {
-    # anneal_rows_kernel<0, 16> on the burst workload: FETCH_SIZE 161.4 KiB x 2.0 + WRITE_SIZE
-    # 16,677.6 KiB x 1.0; 441.7 VALU and 54.9 LDS instructions, 116.3 bank-conflict cycles
-    # per proposal
+    # anneal_rows_kernel<0, 16> on the burst workload: 17,420,949 B of HBM traffic (FETCH_SIZE
+    # x 2.0 + WRITE_SIZE x 1.0); 441.7 VALU and 54.9 LDS instructions, 116.3 bank-conflict
+    # cycles per proposal
     "e265f3e4d95da1bc857c0d7c2984ebc158f254d86b0a8044c800ac9c08a141da": {
-        "traffic": 17408407, "valu_busy": 0.666, "lds_bank_conflict_cycles_per_lds_instr": 2.12,
+        "traffic": 17420949, "valu_busy": 0.668, "lds_bank_conflict_cycles_per_lds_instr": 2.12,
         "lds_instr_per_chain_iter": 54.9, "vgprs": 89, "lds_bytes_per_workgroup": 129296, "waves_per_simd": 4},
 }
 
