@@ -110,6 +110,12 @@ PATHS = {
     "cont_wide": (lambda r: _pq(r, 24, 16, 2048, 4, 40, 4_000_000_000), Model(6, 1, 2000, 40, 8000, 300, 1 << 25), 8, 300),
     "cont_ls_b48": (lambda r: _pq(r, 100, 16, 2048, 4, 200, 3_000_000), Model(48, 1, 2000, 40, 8000, 300, 2), 8, 300),
     "search_wide": (lambda r: _pq(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 2, 2000, 40, 8000, 300, 1 << 22), 8, 300),
+    # one batch per wave with the member limits in registers: 4 batches of 40 (8 register
+    # rows, a ragged last batch) and 31 batches of 33 (32 rows)
+    "static_rows_mr8": (lambda r: _pq(r, 150, 16, 2048, 1, 300, 4_000_000_000), Model(40, 0, 2000, 40, 8000, 300, 2), 4,
+                        200),
+    "static_rows_mr32": (lambda r: _pq(r, 1000, 16, 2048, 1, 60, 4_000_000_000), Model(33, 0, 2000, 40, 8000, 300, 2), 4,
+                         100),
 }
 
 
