@@ -7,11 +7,12 @@
 // holds, lane by lane, the limits of batch k's members: a member meets its SLO iff its
 // batch starts before its limit (thr + 1 - P for TTFT with P the batch prefill, thr + 1 - F
 // for end-to-end with F its finish offset, all or nothing for TPOT, whose time per output
-// token does not depend on the start; the staged records hold thr + 1). A changed batch rewrites its row; each proposal then
-// counts the met members of every row at its candidate start with one compare and one
-// population count per row. No batch needs bounds on the starts that keep its flags, and
-// no shifted batch is recounted member by member. A row is a set: only its count is read,
-// and a changed batch rewrites all of it, so which lane holds which member does not matter.
+// token does not depend on the start; the staged records hold thr + 1 and the kind as flag
+// bits above e). A changed batch rewrites its row; each proposal then counts the met
+// members of every row at its candidate start with one compare and one population count
+// per row. No batch needs bounds on the starts that keep its flags, and no shifted batch
+// is recounted member by member. A row is a set: only its count is read, and a changed
+// batch rewrites all of it, so which lane holds which member does not matter.
 //
 // Per changed batch one three-way reduction gives the newcomer's pair-cost sum, the change
 // of the staying members' finish offsets (for the latency delta) and their largest new
