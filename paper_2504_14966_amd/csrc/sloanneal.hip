@@ -19,6 +19,7 @@
 #include "anneal_wave.h"
 #include "anneal_sized.h"
 #include "anneal_wave_rows.h"
+#include "anneal_cont_spec.h"
 #include "multi.h"
 #include "anneal_reg.h"
 #include "fit.h"
@@ -394,6 +395,34 @@ void add_chains(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, 
     }
   }
   if (model->policy == SCHED_CONTINUOUS) {
+    // Two proposals scored per round by two waves of one workgroup per chain (sliding-window
+    // list scheduling, 32-bit times), when at least as many chains fit on a CU at once as
+    // under the single-proposal list-scheduling kernel.
+    if (std::min(B, n) <= 32) {
+      const int cus = std::max(1, cu_count()), lim = max_lds_per_block();
+      int w1 = 1;
+      while (w1 < 16 && (int64_t)w1 * cus < a.chains) w1 <<= 1;
+      const size_t per1 = (((size_t)n * 2 + 15) & ~size_t(15)) + ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) +
+                          sa::cont_inc_bytes(n, B);
+      while (w1 > 1 && (size_t)n * 16 + per1 * w1 > (size_t)lim) w1 >>= 1;
+      const size_t lds1 = (size_t)n * 16 + per1 * w1;
+      const int64_t res1 = lds1 <= (size_t)lim ? (int64_t)w1 * std::max<int64_t>(1, lim / (int64_t)lds1) : 0;
+      const size_t lds = sa::spec_chain_bytes(n, B);
+      const void *fn = (const void *)&sa::anneal_cont_spec_kernel<OBJ>;
+      int nb = 0;
+      if (lds > (size_t)lim ||
+          (lds > 65536 && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) ||
+          hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, 128, lds) != hipSuccess)
+        nb = 0;
+      if (nb > 0 && std::min<int64_t>(a.chains, (int64_t)nb * cus) >= std::min<int64_t>(a.chains, res1 * cus)) {
+        c.add(sa::kFlagNarrowPrefill | sa::kFlagListSched | sa::kFlagNarrowTime, kAnnealFlags,
+              [=](const sa::DevModel &d) {
+                sa::anneal_cont_spec_kernel<OBJ><<<a.chains, 128, lds, a.stream>>>(
+                    d, a.q, a.chains, a.iters, a.T0, a.alpha, a.k0, a.k1, a.swap_thr, a.srch, a.w);
+                return hipGetLastError();
+              });
+      }
+    }
     for (int ls = 1; ls >= 0; --ls) {
       const size_t soa = (size_t)n * 16;
       const bool inc = ls && std::min(B, n) <= 32;

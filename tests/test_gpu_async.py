@@ -295,8 +295,9 @@ def test_device_fit_flags_match_exact_bounds(sl, seed):
 
 
 def test_selected_kernels(sl):
-    # (workload, expected candidate): the register kernel, the continuous list-scheduling
-    # kernel and the batch-per-wave delta kernel are each the first candidate of their call
+    # (workload, expected candidate): the register kernel, the continuous kernel scoring two
+    # proposals per round and the batch-per-wave kernel with member limits in registers are
+    # each the first candidate of their call
     ws = sl.alloc_ws(1024, 64)
     for cfg in (2, 3, 4):
         W = workload(cfg)

@@ -62,13 +62,22 @@ CASES = {
     "cont_ls_b64": (lambda r: _queue(r, 150, 16, 2048, 4, 200, 3_000_000), Model(64, 1, 2000, 40, 8000, 300, 2), 8, 200),
     # continuous, list scheduling with a timeline longer than 2^32 us (64-bit segment sums)
     "cont_ls_wide_time": (lambda r: _queue(r, 40, 16, 2048, 20000, 60000, 4_000_000_000), Model(8, 1, 2000, 40, 8000, 300, 2), 4, 60),
+    # continuous, two proposals per round: one running request (63 admissions per window
+    # chunk, a ragged second chunk), a single admission after the initial group, a single
+    # request (every move is the identity); odd proposal counts end on a lone proposal
+    "cont_spec_b1": (lambda r: _queue(r, 70, 16, 2048, 1, 200, 3_000_000), Model(1, 1, 2000, 40, 8000, 300, 2), 4, 301),
+    "cont_spec_b32_n33": (lambda r: _queue(r, 33, 16, 2048, 1, 200, 3_000_000), Model(32, 1, 2000, 40, 8000, 300, 2), 4, 257),
+    "cont_spec_one": (lambda r: _queue(r, 1, 16, 2048, 1, 200, 3_000_000), Model(4, 1, 2000, 40, 8000, 300, 2), 2, 65),
 }
 
 
 # the candidate that must run, for cases where the order of candidates is the point: under
 # static admission with B > 32, the kernel with the member limits in registers comes first
-# and needs a 32-bit timeline; the plain lane-per-batch kernel follows it
-SELECTED = {"static_wave_ragged": 0, "static_wave_wide_time": 1}
+# and needs a 32-bit timeline; the plain lane-per-batch kernel follows it. Under continuous
+# admission with at most 32 running requests the kernel scoring two proposals per round
+# comes first and needs 32-bit times; the single-proposal list-scheduling kernel follows it
+SELECTED = {"static_wave_ragged": 0, "static_wave_wide_time": 1, "cont_ls_ties": 0, "cont_ls_b_gt_n": 0,
+            "cont_spec_b1": 0, "cont_spec_b32_n33": 0, "cont_spec_one": 0, "cont_ls_wide_time": 1}
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
