@@ -109,6 +109,8 @@ PATHS = {
                         4, 40),
     "cont_wide": (lambda r: _pq(r, 24, 16, 2048, 4, 40, 4_000_000_000), Model(6, 1, 2000, 40, 8000, 300, 1 << 25), 8, 300),
     "cont_ls_b48": (lambda r: _pq(r, 100, 16, 2048, 4, 200, 3_000_000), Model(48, 1, 2000, 40, 8000, 300, 2), 8, 300),
+    # continuous with at most 32 running: two proposals per round, an odd proposal count
+    "cont_spec_b16": (lambda r: _pq(r, 80, 16, 2048, 4, 200, 3_000_000), Model(16, 1, 2000, 40, 8000, 300, 2), 8, 301),
     "search_wide": (lambda r: _pq(r, 48, 16, 2048, 8, 300, 4_000_000_000), Model(8, 2, 2000, 40, 8000, 300, 1 << 22), 8, 300),
     # one batch per wave with the member limits in registers: 4 batches of 40 (8 register
     # rows, a ragged last batch) and 31 batches of 33 (32 rows)
@@ -127,7 +129,7 @@ def test_paths_ratio(sl, orc, name):
     _check(orc, res, q, m, range(chains), iters, 0.7, 0.99, 9, (RATIO, 3, 0))
 
 
-@pytest.mark.parametrize("policy", [0, 2])
+@pytest.mark.parametrize("policy", [0, 1, 2])
 def test_paper_schedule(sl, orc, policy):
     """T0 500, T_thres 20, tau 0.95, iter 100 (63 levels, 6300 proposals), objective G, early
     exit, on the 8-request queue (max batch 4)."""
