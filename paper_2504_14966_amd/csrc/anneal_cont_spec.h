@@ -30,23 +30,24 @@
 
 namespace sa {
 
-// Candidate position p reads current position src(p), without branches: a swap exchanges
-// i and j, an insert (remove at i, re-insert at j) shifts the positions between them by
-// one towards i and puts i at j, the identity maps p to p.
+// Candidate position p reads current position src(p), without branches: position j reads
+// i, and the positions in [rlo, rlo + rspan) read p + dir. An insert (remove at i,
+// re-insert at j) shifts the positions between i and j by one towards i; a swap is the
+// one-position range {i} reading j; the identity has no j and an empty range.
 struct SrcMap {
-  int j, ito, isw, rlo, dir;
+  int j, ito, rlo, dir;
   uint32_t rspan;
   __device__ __forceinline__ int src(int p) const {
     const int shifted = (uint32_t)(p - rlo) < rspan ? p + dir : p;
-    return p == j ? ito : (p == isw ? j : shifted);
+    return p == j ? ito : shifted;
   }
 };
 
 __device__ __forceinline__ SrcMap src_map(int kind, int i, int j) {
-  if (kind == 0 || i == j) return SrcMap{-1, 0, -1, 0, 0, 0u};
-  if (kind == 1) return SrcMap{j, i, i, 0, 0, 0u};
-  if (i < j) return SrcMap{j, i, -1, i, 1, (uint32_t)(j - i)};
-  return SrcMap{j, i, -1, j + 1, -1, (uint32_t)(i - j)};
+  if (kind == 0 || i == j) return SrcMap{-1, 0, 0, 0, 0u};
+  if (kind == 1) return SrcMap{j, i, i, j - i, 1u};
+  if (i < j) return SrcMap{j, i, i, 1, (uint32_t)(j - i)};
+  return SrcMap{j, i, j + 1, -1, (uint32_t)(i - j)};
 }
 
 // one wave's five arrays of n + 1 entries
