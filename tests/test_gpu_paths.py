@@ -68,6 +68,9 @@ CASES = {
     "cont_spec_b1": (lambda r: _queue(r, 70, 16, 2048, 1, 200, 3_000_000), Model(1, 1, 2000, 40, 8000, 300, 2), 4, 301),
     "cont_spec_b32_n33": (lambda r: _queue(r, 33, 16, 2048, 1, 200, 3_000_000), Model(32, 1, 2000, 40, 8000, 300, 2), 4, 257),
     "cont_spec_one": (lambda r: _queue(r, 1, 16, 2048, 1, 200, 3_000_000), Model(4, 1, 2000, 40, 8000, 300, 2), 2, 65),
+    # more chains than the GPU holds at once: later workgroups start as earlier ones end
+    "cont_spec_many_chains": (lambda r: _queue(r, 40, 16, 2048, 1, 200, 3_000_000), Model(8, 1, 2000, 40, 8000, 300, 2),
+                              2500, 60),
 }
 
 
@@ -77,7 +80,8 @@ CASES = {
 # admission with at most 32 running requests the kernel scoring two proposals per round
 # comes first and needs 32-bit times; the single-proposal list-scheduling kernel follows it
 SELECTED = {"static_wave_ragged": 0, "static_wave_wide_time": 1, "cont_ls_ties": 0, "cont_ls_b_gt_n": 0,
-            "cont_spec_b1": 0, "cont_spec_b32_n33": 0, "cont_spec_one": 0, "cont_ls_wide_time": 1}
+            "cont_spec_b1": 0, "cont_spec_b32_n33": 0, "cont_spec_one": 0, "cont_spec_many_chains": 0,
+            "cont_ls_wide_time": 1}
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
