@@ -9,18 +9,19 @@
 // proposals whenever the first is rejected.
 //
 // One workgroup of two waves per chain: wave w scores proposal k + w. The replay is the
-// list-scheduling one with the running requests in a sliding window (at most 32 of them)
-// and 32-bit times; it is bound by the issue of its own serial steps, so the second wave
-// of a chain works in issue slots the SIMD would otherwise leave empty. The waves meet
-// once per round at the workgroup barrier, after which both take the same decisions from
-// the two scores, and once more when a move is accepted (the first wave applies it to the
-// shared records before either replays again).
+// list-scheduling one with 32-bit times (the running requests in a sliding window when at
+// most 32 run, else one pop per step from lane 0), restarted at the chunk of admissions
+// holding the candidate's first change; it is bound by the issue of its own serial steps,
+// so the second wave of a chain works in issue slots the SIMD would otherwise leave empty.
+// The waves meet once per round at the workgroup barrier, after which both take the same
+// decisions from the two scores, and once more when a move is accepted (the first wave
+// applies it to the shared records before either replays again).
 //
 // Candidate records are read from the current order's records through a branch-free
 // position map, so one copy of them serves both waves. LDS per chain: those records
 // (16 B per position, request id above the kind bits), per wave five 32-bit arrays of
 // n + 1 entries (prefill prefix sums, run starts, run-end prefills, segment-cost prefix
-// sums, TTFTs), three sets of admission pops plus window chunk-start keys (the current
+// sums, TTFTs), three sets of admission pops plus chunk-start keys (the current
 // order's and one per wave), and the two waves' scores in two slots used in alternate
 // rounds. The request table is not staged in LDS: each chain reads its start order's
 // records once from global memory.
@@ -52,10 +53,15 @@ __device__ __forceinline__ SrcMap src_map(int kind, int i, int j) {
 
 // one wave's five arrays of n + 1 entries
 __host__ __device__ __forceinline__ size_t spec_cand_bytes(int n) { return ((size_t)20 * (n + 1) + 15) / 16 * 16; }
-// chunk-start keys: 32 per window chunk
+// Admissions per chunk and running keys kept per chunk start: with at most 32 running, the
+// sliding window's 64 - n0 admissions and 32 keys; with more, 64 admissions and 64 keys.
+__host__ __device__ __forceinline__ int spec_chunk_len(int n0) { return n0 <= 32 ? 64 - n0 : 64; }
+__host__ __device__ __forceinline__ int spec_snap_len(int n0) { return n0 <= 32 ? 32 : 64; }
+// chunk-start keys of one order
 __host__ __device__ __forceinline__ size_t spec_chunk_bytes(int n, int B) {
   const int n0 = n < B ? n : B, nadm = n - n0;
-  return nadm > 0 ? (size_t)((nadm + (64 - n0) - 1) / (64 - n0)) * 32 * 4 : 0;
+  const int S = spec_chunk_len(n0);
+  return nadm > 0 ? (size_t)((nadm + S - 1) / S) * spec_snap_len(n0) * 4 : 0;
 }
 __host__ __device__ __forceinline__ size_t spec_pop_bytes(int n) { return ((size_t)4 * n + 15) / 16 * 16; }
 // scores exchanged per round: 2 slots x 2 waves x 32 B
@@ -126,15 +132,41 @@ __device__ __forceinline__ Score spec_replay(const DevModel &m, const uint4 *__r
     wave_sync_lds();
   }
 
-  // list scheduling in a sliding window: before step t of a chunk, lanes [0, t) hold the
-  // keys popped so far and lanes [t, t + n0) the running keys, sorted, kInf above; popping
-  // lane t and inserting key nk leaves lane i = median(list[i - 1], list[i], nk)
-  const int Sfull = kWave - n0;
+  // admissions before the chunk holding the first changed one are the current order's
+  const int Sfull = spec_chunk_len(n0), SN = spec_snap_len(n0);
   const int cr = lo >= n0 ? (lo - n0) / Sfull : 0;
   int done = min(cr * Sfull, nadm);
   for (int x = lane; x < done; x += kWave) ev[x] = cc.ev_cur[x];
-  for (int x = lane; x < cr * 32; x += kWave) snap[x] = cc.snap_cur[x];
-  if (done > 0) list = lane < n0 ? cc.snap_cur[cr * 32 + lane] : kInf;
+  for (int x = lane; x < cr * SN; x += kWave) snap[x] = cc.snap_cur[x];
+  if (done > 0) list = lane < n0 ? cc.snap_cur[cr * SN + lane] : kInf;
+  if (n0 > 32) {
+    // More than 32 running: the sorted keys fill lanes [0, n0), kInf above; a step pops
+    // lane 0 and leaves lane i = max(list[i], min(list[i + 1], nk)); the pops enter lane 0
+    // of a second register that moves up one lane per step.
+    while (done < nadm) {
+      const int cnt = min(kWave, nadm - done);
+      snap[(done / kWave) * kWave + lane] = list;
+      uint32_t LP = 0;
+      if (lane < cnt) {
+        const int p = n0 + done + lane;
+        LP = ((posr[sm.src(p)].x >> 16) << 10) | (uint32_t)p;
+      }
+      uint32_t evq = 0;
+      uint32_t top = __builtin_amdgcn_readfirstlane(list);
+      for (int t = 0; t < cnt; ++t) {
+        const uint32_t nk = (top & ~1023u) + rl(LP, t);
+        evq = dpp_old<kDppWaveShr1, 0xF>(list, evq);
+        const uint32_t sh = dpp_old<kDppWaveShl1, 0xF>(kInf, list);
+        list = max(list, min(sh, nk));
+        top = __builtin_amdgcn_readfirstlane(list);
+      }
+      if (lane < cnt) ev[done + cnt - 1 - lane] = evq;
+      done += cnt;
+    }
+  }
+  // At most 32 running: a sliding window. Before step t of a chunk, lanes [0, t) hold the
+  // keys popped so far and lanes [t, t + n0) the running keys, sorted, kInf above; popping
+  // lane t and inserting key nk leaves lane i = median(list[i - 1], list[i], nk).
   while (done < nadm) {
     const int S = min(Sfull, nadm - done);
     if (lane < n0) snap[(done / Sfull) * 32 + lane] = list;

@@ -395,15 +395,15 @@ void add_chains(Candidates<sa::DevModel> &c, const sched_model_t *model, int n, 
     }
   }
   if (model->policy == SCHED_CONTINUOUS) {
-    // Two proposals scored per round by two waves of one workgroup per chain (sliding-window
-    // list scheduling, 32-bit times), when at least as many chains fit on a CU at once as
-    // under the single-proposal list-scheduling kernel.
-    if (std::min(B, n) <= 32) {
+    // Two proposals scored per round by two waves of one workgroup per chain (list
+    // scheduling, 32-bit times), when at least as many chains fit on a CU at once as under
+    // the single-proposal list-scheduling kernel.
+    {
       const int cus = std::max(1, cu_count()), lim = max_lds_per_block();
       int w1 = 1;
       while (w1 < 16 && (int64_t)w1 * cus < a.chains) w1 <<= 1;
       const size_t per1 = (((size_t)n * 2 + 15) & ~size_t(15)) + ((sa::cont_ls_scratch_bytes(n) + 15) & ~size_t(15)) +
-                          sa::cont_inc_bytes(n, B);
+                          (std::min(B, n) <= 32 ? sa::cont_inc_bytes(n, B) : 0);
       while (w1 > 1 && (size_t)n * 16 + per1 * w1 > (size_t)lim) w1 >>= 1;
       const size_t lds1 = (size_t)n * 16 + per1 * w1;
       const int64_t res1 = lds1 <= (size_t)lim ? (int64_t)w1 * std::max<int64_t>(1, lim / (int64_t)lds1) : 0;

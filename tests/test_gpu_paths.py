@@ -68,6 +68,10 @@ CASES = {
     "cont_spec_b1": (lambda r: _queue(r, 70, 16, 2048, 1, 200, 3_000_000), Model(1, 1, 2000, 40, 8000, 300, 2), 4, 301),
     "cont_spec_b32_n33": (lambda r: _queue(r, 33, 16, 2048, 1, 200, 3_000_000), Model(32, 1, 2000, 40, 8000, 300, 2), 4, 257),
     "cont_spec_one": (lambda r: _queue(r, 1, 16, 2048, 1, 200, 3_000_000), Model(4, 1, 2000, 40, 8000, 300, 2), 2, 65),
+    # 48 running with a timeline beyond 2^32: the two-proposal kernel is listed (first) and
+    # refused on the device, the single-proposal list-scheduling kernel runs
+    "cont_ls_b48_wide_time": (lambda r: _queue(r, 60, 16, 2048, 20000, 60000, 4_000_000_000),
+                              Model(48, 1, 2000, 40, 8000, 300, 2), 4, 60),
     # more chains than the GPU holds at once: later workgroups start as earlier ones end
     "cont_spec_many_chains": (lambda r: _queue(r, 40, 16, 2048, 1, 200, 3_000_000), Model(8, 1, 2000, 40, 8000, 300, 2),
                               2500, 60),
@@ -77,11 +81,11 @@ CASES = {
 # the candidate that must run, for cases where the order of candidates is the point: under
 # static admission with B > 32, the kernel with the member limits in registers comes first
 # and needs a 32-bit timeline; the plain lane-per-batch kernel follows it. Under continuous
-# admission with at most 32 running requests the kernel scoring two proposals per round
-# comes first and needs 32-bit times; the single-proposal list-scheduling kernel follows it
+# admission the kernel scoring two proposals per round comes first and needs 32-bit times;
+# the single-proposal list-scheduling kernel follows it
 SELECTED = {"static_wave_ragged": 0, "static_wave_wide_time": 1, "cont_ls_ties": 0, "cont_ls_b_gt_n": 0,
             "cont_spec_b1": 0, "cont_spec_b32_n33": 0, "cont_spec_one": 0, "cont_spec_many_chains": 0,
-            "cont_ls_wide_time": 1}
+            "cont_ls_wide_time": 1, "cont_ls_b48": 0, "cont_ls_b64": 0, "cont_ls_b48_wide_time": 1}
 
 
 @pytest.mark.parametrize("name", sorted(CASES))
