@@ -54,9 +54,9 @@ __device__ __forceinline__ SrcMap src_map(int kind, int i, int j) {
 // one wave's five arrays of n + 1 entries
 __host__ __device__ __forceinline__ size_t spec_cand_bytes(int n) { return ((size_t)20 * (n + 1) + 15) / 16 * 16; }
 // Admissions per chunk and running keys kept per chunk start: with at most 32 running, the
-// sliding window's 64 - n0 admissions and 32 keys; with more, 64 admissions and 64 keys.
+// sliding window's 64 - n0 admissions and 32 keys; with more, 64 admissions and n0 keys.
 __host__ __device__ __forceinline__ int spec_chunk_len(int n0) { return n0 <= 32 ? 64 - n0 : 64; }
-__host__ __device__ __forceinline__ int spec_snap_len(int n0) { return n0 <= 32 ? 32 : 64; }
+__host__ __device__ __forceinline__ int spec_snap_len(int n0) { return n0 <= 32 ? 32 : n0; }
 // chunk-start keys of one order
 __host__ __device__ __forceinline__ size_t spec_chunk_bytes(int n, int B) {
   const int n0 = n < B ? n : B, nadm = n - n0;
@@ -145,7 +145,7 @@ __device__ __forceinline__ Score spec_replay(const DevModel &m, const uint4 *__r
     // of a second register that moves up one lane per step.
     while (done < nadm) {
       const int cnt = min(kWave, nadm - done);
-      snap[(done / kWave) * kWave + lane] = list;
+      if (lane < n0) snap[(done / kWave) * SN + lane] = list;
       uint32_t LP = 0;
       if (lane < cnt) {
         const int p = n0 + done + lane;
