@@ -136,7 +136,7 @@ PROFILE_BY_SOURCE = {
     # anneal_rows_kernel<0, 16> on the burst workload: 17,420,949 B of HBM traffic (FETCH_SIZE
     # x 2.0 + WRITE_SIZE x 1.0); 441.7 VALU and 54.9 LDS instructions, 116.3 bank-conflict
     # cycles per proposal
-    "51c69b5424cada8cda2bc67a597efe2d3285e234253395ecf6f3f0e4509ab2e9": {
+    "1f154805f7b7b131cace531dcce6adf36ad3addcbe0c516645046ec6066bef04": {
         "traffic": 17420949, "valu_busy": 0.668, "lds_bank_conflict_cycles_per_lds_instr": 2.12,
         "lds_instr_per_chain_iter": 54.9, "vgprs": 89, "lds_bytes_per_workgroup": 129296, "waves_per_simd": 4},
 }
